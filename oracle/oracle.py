@@ -1,0 +1,154 @@
+"""NumPy-facing wrapper around the plain C oracle (``oracle/oracle.c``).
+
+TEST INFRASTRUCTURE ONLY: the test suite, the smoke check and the CPU-baseline
+leg of the benchmark are the only callers.  The HIP library never imports,
+loads or calls anything here, and this module never imports the HIP library.
+
+Each function takes and returns NumPy arrays; the arithmetic lives in the C
+file, whose definitions cite the paper (Methodology; Tables 1 and 2).
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "oracle.c")
+_LIB = os.path.join(_HERE, "liboracle.so")
+
+_lib = None
+
+
+def build(force: bool = True) -> str:
+    """Compile liboracle.so with gcc and OpenMP (no HIP)."""
+    if force or not os.path.exists(_LIB):
+        tmp = _LIB + ".tmp"
+        subprocess.check_call(
+            ["gcc", "-O2", "-fopenmp", "-fPIC", "-shared", "-std=c11",
+             "-Wall", "-Wextra", "-o", tmp, _SRC])
+        os.replace(tmp, _LIB)
+    return _LIB
+
+
+def _load():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
+            build(force=True)
+        lib = ctypes.CDLL(_LIB)
+        p = ctypes.c_void_p
+        i64 = ctypes.c_int64
+        for name in ("oracle_gemm_i16i32", "oracle_gemm_i32_s24"):
+            getattr(lib, name).argtypes = [p, p, p, i64, i64, i64, i64]
+        for name in ("oracle_conv2d_direct", "oracle_conv2d_im2col"):
+            getattr(lib, name).argtypes = [p, p, p] + [i64] * 9
+        for name in ("oracle_attn_i32", "oracle_attn_i32_assoc", "oracle_attn_f64",
+                     "oracle_attn_f64_assoc", "oracle_attn_f32"):
+            getattr(lib, name).argtypes = [p, p, p, p, i64, i64]
+        _lib = lib
+    return _lib
+
+
+def _ptr(a: np.ndarray):
+    return ctypes.c_void_p(a.ctypes.data)
+
+
+def _c(a, dtype):
+    a = np.asarray(a)
+    if a.dtype != dtype:
+        raise TypeError(f"expected {np.dtype(dtype)}, got {a.dtype}")
+    return np.ascontiguousarray(a)
+
+
+def gemm_i16i32(A, B):
+    """C = A @ B (mod 2^32), A [batch][M][K] or [M][K] int16, B [..][K][N] int16."""
+    A = _c(A, np.int16)
+    B = _c(B, np.int16)
+    squeeze = A.ndim == 2
+    if squeeze:
+        A, B = A[None], B[None]
+    batch, M, K = A.shape
+    assert B.shape[0] == batch and B.shape[1] == K
+    N = B.shape[2]
+    C = np.empty((batch, M, N), np.int32)
+    _load().oracle_gemm_i16i32(_ptr(A), _ptr(B), _ptr(C), M, N, K, batch)
+    return C[0] if squeeze else C
+
+
+def gemm_i32_s24(A, B):
+    """C = sext24(A) @ sext24(B) (mod 2^32); shapes as gemm_i16i32, int32."""
+    A = _c(A, np.int32)
+    B = _c(B, np.int32)
+    squeeze = A.ndim == 2
+    if squeeze:
+        A, B = A[None], B[None]
+    batch, M, K = A.shape
+    assert B.shape[0] == batch and B.shape[1] == K
+    N = B.shape[2]
+    C = np.empty((batch, M, N), np.int32)
+    _load().oracle_gemm_i32_s24(_ptr(A), _ptr(B), _ptr(C), M, N, K, batch)
+    return C[0] if squeeze else C
+
+
+def conv_out_shape(N, Ci, H, W, Co, KH, KW, stride, pad):
+    Ho = (H + 2 * pad - KH) // stride + 1
+    Wo = (W + 2 * pad - KW) // stride + 1
+    return (N, Co, Ho, Wo)
+
+
+def _conv(fn, x, w, stride, pad):
+    x = _c(x, np.int16)
+    w = _c(w, np.int16)
+    N, Ci, H, W = x.shape
+    Co, Ci2, KH, KW = w.shape
+    assert Ci == Ci2
+    y = np.empty(conv_out_shape(N, Ci, H, W, Co, KH, KW, stride, pad), np.int32)
+    fn(_ptr(x), _ptr(w), _ptr(y), N, Ci, H, W, Co, KH, KW, stride, pad)
+    return y
+
+
+def conv2d_direct(x, w, stride=1, pad=0):
+    """Direct 7-loop cross-correlation, zero padding, NCHW/OIHW -> NCHW int32."""
+    return _conv(_load().oracle_conv2d_direct, x, w, stride, pad)
+
+
+def conv2d_im2col(x, w, stride=1, pad=0):
+    """The same convolution via explicit im2col and the GEMM oracle."""
+    return _conv(_load().oracle_conv2d_im2col, x, w, stride, pad)
+
+
+def _attn(fn, Q, K, V, dtype, out_dtype):
+    Q, K, V = (_c(t, dtype) for t in (Q, K, V))
+    L, d = Q.shape
+    assert K.shape == (L, d) and V.shape == (L, d)
+    O = np.empty((L, d), out_dtype)
+    fn(_ptr(Q), _ptr(K), _ptr(V), _ptr(O), L, d)
+    return O
+
+
+def attn_i32(Q, K, V):
+    """O = (Q K^T) V (mod 2^32), [L][d] int32."""
+    return _attn(_load().oracle_attn_i32, Q, K, V, np.int32, np.int32)
+
+
+def attn_i32_assoc(Q, K, V):
+    """O = Q (K^T V) (mod 2^32): an invariant, equal bit for bit to attn_i32."""
+    return _attn(_load().oracle_attn_i32_assoc, Q, K, V, np.int32, np.int32)
+
+
+def attn_f64(Q, K, V):
+    """float64 reference R = (Q K^T) V from float32 inputs."""
+    return _attn(_load().oracle_attn_f64, Q, K, V, np.float32, np.float64)
+
+
+def attn_f64_assoc(Q, K, V):
+    """float64 Q (K^T V) from float32 inputs (cross-check of attn_f64)."""
+    return _attn(_load().oracle_attn_f64_assoc, Q, K, V, np.float32, np.float64)
+
+
+def attn_f32(Q, K, V):
+    """plain float32, sequential summation order."""
+    return _attn(_load().oracle_attn_f32, Q, K, V, np.float32, np.float32)

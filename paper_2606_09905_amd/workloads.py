@@ -1,0 +1,93 @@
+"""Seeded synthetic inputs for the integer GEMM substrate.
+
+This module only draws random numbers; it holds none of the method's
+arithmetic, so both the HIP path and the CPU oracle can take their inputs from
+it.  The paper gives no shapes for its operator table and uses no dataset, so
+the workloads below are synthetic by definition: a small INT16 GEMM (values in
+[-1024, 1023]), smul24 INT32 GEMMs over the full signed 24-bit range, an INT16
+3x3 convolution, the FP32 and INT32 attention cores, and the large INT16 GEMMs
+(values in [-256, 255]).  Integers are uniform over a closed range; FP32 inputs
+are N(0, 1) / sqrt(d).
+"""
+from __future__ import annotations
+
+from dataclasses import dataclass, field
+
+import numpy as np
+
+
+def ints(rng: np.random.Generator, shape, lo: int, hi: int, dtype) -> np.ndarray:
+    """Uniform integers in the closed range [lo, hi]."""
+    return rng.integers(lo, hi, size=shape, dtype=dtype, endpoint=True)
+
+
+def normal_f32(rng: np.random.Generator, shape, scale: float) -> np.ndarray:
+    """float32 samples of N(0, 1) * scale (drawn in float64, then rounded)."""
+    return (rng.standard_normal(shape) * scale).astype(np.float32)
+
+
+@dataclass(frozen=True)
+class Workload:
+    name: str
+    op: str            # "gemm_i16i32" | "gemm_i32_s24" | "conv2d" | "attn_f32" | "attn_i32"
+    seed: int
+    dims: dict = field(default_factory=dict)
+    lo: int = 0
+    hi: int = 0
+    bound: int = 0     # operand-range contract: max |x|
+
+    @property
+    def ops(self) -> float:
+        """Algorithmic operations (2 per multiply-add) of one evaluation."""
+        d = self.dims
+        if self.op in ("gemm_i16i32", "gemm_i32_s24"):
+            return 2.0 * d["M"] * d["N"] * d["K"] * d["batch"]
+        if self.op == "conv2d":
+            ho = (d["H"] + 2 * d["pad"] - d["KH"]) // d["stride"] + 1
+            wo = (d["W"] + 2 * d["pad"] - d["KW"]) // d["stride"] + 1
+            return 2.0 * d["N"] * d["Co"] * ho * wo * d["Ci"] * d["KH"] * d["KW"]
+        if self.op in ("attn_f32", "attn_i32"):
+            return 4.0 * d["L"] * d["L"] * d["d"]
+        raise ValueError(self.op)
+
+    def generate(self):
+        """Inputs as NumPy arrays, drawn in a fixed order from default_rng(seed)."""
+        rng = np.random.default_rng(self.seed)
+        d = self.dims
+        if self.op == "gemm_i16i32":
+            a_shape = (d["batch"], d["M"], d["K"])
+            b_shape = (d["batch"], d["K"], d["N"])
+            A = ints(rng, a_shape, self.lo, self.hi, np.int16)
+            B = ints(rng, b_shape, self.lo, self.hi, np.int16)
+            return A, B
+        if self.op == "gemm_i32_s24":
+            A = ints(rng, (d["batch"], d["M"], d["K"]), self.lo, self.hi, np.int32)
+            B = ints(rng, (d["batch"], d["K"], d["N"]), self.lo, self.hi, np.int32)
+            return A, B
+        if self.op == "conv2d":
+            x = ints(rng, (d["N"], d["Ci"], d["H"], d["W"]), self.lo, self.hi, np.int16)
+            w = ints(rng, (d["Co"], d["Ci"], d["KH"], d["KW"]), self.lo, self.hi, np.int16)
+            return x, w
+        if self.op == "attn_f32":
+            s = 1.0 / np.sqrt(d["d"])
+            return tuple(normal_f32(rng, (d["L"], d["d"]), s) for _ in range(3))
+        if self.op == "attn_i32":
+            return tuple(ints(rng, (d["L"], d["d"]), self.lo, self.hi, np.int32) for _ in range(3))
+        raise ValueError(self.op)
+
+
+def _gemm(name, op, seed, M, N, K, batch, lo, hi):
+    return Workload(name, op, seed, dict(M=M, N=N, K=K, batch=batch), lo, hi, max(-lo, hi))
+
+
+WORKLOADS = {w.name: w for w in [
+    _gemm("gemm_i16_256", "gemm_i16i32", 1, 256, 256, 256, 1, -1024, 1023),
+    _gemm("gemm_s24_1024", "gemm_i32_s24", 2, 1024, 1024, 1024, 1, -(1 << 23), (1 << 23) - 1),
+    _gemm("gemm_s24_16x512", "gemm_i32_s24", 3, 512, 512, 512, 16, -(1 << 23), (1 << 23) - 1),
+    Workload("conv_8x64x56x56_128_3x3", "conv2d", 4,
+             dict(N=8, Ci=64, H=56, W=56, Co=128, KH=3, KW=3, stride=1, pad=1), -256, 255, 256),
+    Workload("attn_f32_4096x64", "attn_f32", 5, dict(L=4096, d=64)),
+    Workload("attn_i32_4096x64", "attn_i32", 6, dict(L=4096, d=64), -64, 63, 64),
+    _gemm("gemm_i16_8192", "gemm_i16i32", 7, 8192, 8192, 8192, 1, -256, 255),
+    _gemm("gemm_i16_64x2048", "gemm_i16i32", 8, 2048, 2048, 2048, 64, -256, 255),
+]}

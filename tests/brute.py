@@ -1,0 +1,67 @@
+"""Definitional brute force in Python integers (and exact rationals).
+
+Independent of the C oracle: used by the CPU tests to pin the oracle on tiny
+inputs.  Every function is the textbook definition with arbitrary-precision
+Python arithmetic, reduced to two's-complement 32 bits at the very end.
+"""
+from __future__ import annotations
+
+from fractions import Fraction
+
+
+def wrap32(v: int) -> int:
+    v &= 0xFFFFFFFF
+    return v - (1 << 32) if v >= (1 << 31) else v
+
+
+def sext24(x: int) -> int:
+    u = x & 0xFFFFFF
+    return u - (1 << 24) if u >= (1 << 23) else u
+
+
+def gemm(A, B, f=lambda v: v):
+    """A: list of rows (M x K), B: (K x N); f maps each operand first."""
+    M, K = len(A), len(A[0]) if A else 0
+    N = len(B[0]) if B else 0
+    return [[wrap32(sum(f(int(A[i][k])) * f(int(B[k][j])) for k in range(K)))
+             for j in range(N)] for i in range(M)]
+
+
+def conv2d(x, w, stride, pad):
+    """x [N][Ci][H][W], w [Co][Ci][KH][KW] nested lists -> y [N][Co][Ho][Wo]."""
+    N, Ci, H, W = len(x), len(x[0]), len(x[0][0]), len(x[0][0][0])
+    Co, KH, KW = len(w), len(w[0][0]), len(w[0][0][0])
+    Ho = (H + 2 * pad - KH) // stride + 1
+    Wo = (W + 2 * pad - KW) // stride + 1
+    y = [[[[0] * Wo for _ in range(Ho)] for _ in range(Co)] for _ in range(N)]
+    for n in range(N):
+        for co in range(Co):
+            for oh in range(Ho):
+                for ow in range(Wo):
+                    s = 0
+                    for ci in range(Ci):
+                        for kh in range(KH):
+                            for kw in range(KW):
+                                ih, iw = oh * stride - pad + kh, ow * stride - pad + kw
+                                if 0 <= ih < H and 0 <= iw < W:
+                                    s += int(x[n][ci][ih][iw]) * int(w[co][ci][kh][kw])
+                    y[n][co][oh][ow] = wrap32(s)
+    return y
+
+
+def attn_int(Q, K, V):
+    """(Q K^T) V in exact integers, reduced mod 2^32."""
+    L, d = len(Q), len(Q[0])
+    S = [[sum(int(Q[i][t]) * int(K[j][t]) for t in range(d)) for j in range(L)] for i in range(L)]
+    return [[wrap32(sum(S[i][j] * int(V[j][t]) for j in range(L))) for t in range(d)]
+            for i in range(L)]
+
+
+def attn_exact(Q, K, V):
+    """(Q K^T) V as exact rationals of the float inputs."""
+    L, d = len(Q), len(Q[0])
+    q = [[Fraction(float(v)) for v in r] for r in Q]
+    k = [[Fraction(float(v)) for v in r] for r in K]
+    v = [[Fraction(float(x)) for x in r] for r in V]
+    S = [[sum(q[i][t] * k[j][t] for t in range(d)) for j in range(L)] for i in range(L)]
+    return [[sum(S[i][j] * v[j][t] for j in range(L)) for t in range(d)] for i in range(L)]
