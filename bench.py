@@ -1,0 +1,192 @@
+"""Benchmark of the tiled integer GEMM substrate on one MI355X.
+
+One step = one evaluation of the packed INT16-input / INT32-accumulation GEMM
+at M = N = K = 8192 (operands uniform in [-256, 255], seed 7) through a
+persistent executor, with inputs resident in HBM.  Prints ONE JSON line.
+
+The timing follows the paper's split (one-time setup / cached steady state /
+execute-only): setup = executor creation; cached = host wall time of
+back-to-back runs / steps; execute-only = HIP events around each launch on
+the executor's stream.  `--all` also measures every other workload and writes
+them to --all-out (not to stdout).
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HEADLINE = "gemm_i16_8192"
+METRIC = "GOPS (2·M·N·K/s) packed INT16/INT32 GEMM; conv & attention-core GOPS"
+
+# MI355X datasheet peaks (dense)
+PEAK = {"f16": 2500.0, "i8": 5000.0, "f32": 157.3, "hbm": 8000.0}  # TFLOP/s, TOP/s, GB/s
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default=HEADLINE)
+    ap.add_argument("--all", action="store_true", help="also measure every workload")
+    ap.add_argument("--all-out", default=os.path.join(ROOT, "gpurun_out", "bench_all.json"))
+    ap.add_argument("--no-cpu", action="store_true", help="skip the oracle CPU baseline")
+    ap.add_argument("--cpu-rows", type=int, default=2048,
+                    help="rows of A in the oracle's CPU sample of the headline GEMM")
+    return ap.parse_args()
+
+
+def make_executor(w, qx):
+    d = w.dims
+    if w.op == "gemm_i16i32":
+        return qx.Executor.gemm_i16i32(d["M"], d["N"], d["K"], d["batch"], w.bound, w.bound)
+    if w.op == "gemm_i32_s24":
+        return qx.Executor.gemm_i32_s24(d["M"], d["N"], d["K"], d["batch"])
+    if w.op == "conv2d":
+        return qx.Executor.conv2d(d["N"], d["Ci"], d["H"], d["W"], d["Co"], d["KH"], d["KW"],
+                                  d["stride"], d["pad"], w.bound, w.bound)
+    if w.op == "attn_f32":
+        return qx.Executor.attn("f32", d["L"], d["d"])
+    if w.op == "attn_i32":
+        return qx.Executor.attn("i32", d["L"], d["d"], w.bound)
+    raise ValueError(w.op)
+
+
+def measure(w, steps, warmup, torch, qx):
+    """Setup, cached steady state and execute-only time of one workload."""
+    inputs = [torch.from_numpy(np.ascontiguousarray(a)).cuda() for a in w.generate()]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    ex = make_executor(w, qx)
+    setup_ms = (time.perf_counter() - t0) * 1e3
+    plan = ex.plan()
+    out = torch.empty(ex.out_shape, dtype=ex.out_dtype, device="cuda")
+    ptrs = [t.data_ptr() for t in inputs]
+    stream = torch.cuda.current_stream()
+    for _ in range(warmup):
+        ex.run_ptrs(ptrs, out.data_ptr(), stream)
+    torch.cuda.synchronize()
+    # cached steady state: back-to-back runs, one final sync
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        ex.run_ptrs(ptrs, out.data_ptr(), stream)
+    torch.cuda.synchronize()
+    cached_s = (time.perf_counter() - t0) / steps
+    # execute-only: events around each run on the same stream
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+           for _ in range(steps)]
+    for a, b in evs:
+        a.record(stream)
+        ex.run_ptrs(ptrs, out.data_ptr(), stream)
+        b.record(stream)
+    torch.cuda.synchronize()
+    exec_ms = [a.elapsed_time(b) for a, b in evs]
+    ex.close()
+    return {
+        "setup_ms": setup_ms,
+        "cached_ms": cached_s * 1e3,
+        "exec_ms_mean": float(np.mean(exec_ms)),
+        "exec_ms_median": float(np.median(exec_ms)),
+        "plan": plan,
+        "ops": w.ops,
+    }
+
+
+def cpu_baseline(w, rows):
+    """The oracle on a bounded sample of the headline GEMM: `rows` rows of A
+    against the full B, on the host cores (OpenMP)."""
+    from oracle import oracle as orc
+    A, B = w.generate()
+    A = np.ascontiguousarray(A[0, :rows])
+    orc.gemm_i16i32(A[:2], B[0])          # build/load outside the timed region
+    t0 = time.perf_counter()
+    orc.gemm_i16i32(A, B[0])
+    dt = time.perf_counter() - t0
+    d = w.dims
+    ops = 2.0 * rows * d["N"] * d["K"]
+    cores = int(os.environ.get("OMP_NUM_THREADS", 0)) or len(os.sched_getaffinity(0))
+    return {
+        "value": ops / dt / 1e9, "unit": "GOPS", "cores": cores, "kind": "oracle",
+        "sample": f"{rows} of {d['M']} rows of A x full B ({ops:.3e} ops, {dt:.1f} s)",
+    }
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1",
+                          "n_gpus": args.gpus}), flush=True)
+        sys.exit(2)
+    import torch
+    from paper_2606_09905_amd import qx
+    from paper_2606_09905_amd.workloads import WORKLOADS
+    if not torch.cuda.is_available():
+        print(json.dumps({"error": "no GPU visible"}), flush=True)
+        sys.exit(1)
+    qx.lib()
+    w = WORKLOADS[args.workload]
+    r = measure(w, args.steps, args.warmup, torch, qx)
+    ms = r["cached_ms"]
+    gops = w.ops / (ms / 1e3) / 1e9
+    exec_s = r["exec_ms_mean"] / 1e3
+    achieved_tflops = w.ops / exec_s / 1e12
+    route = r["plan"]["route_name"]
+    unit_peak = {"f16_exact": "f16", "i8_direct": "i8", "i8_karatsuba": "i8", "i8_offset4": "i8",
+                 "s24_i8limb": "i8", "attn_f32_mfma": "f32", "attn_i32_mfma": "i8"}.get(route, "f16")
+    peak = PEAK[unit_peak]
+    line = {
+        "metric": METRIC,
+        "value": round(gops, 1),
+        "unit": "GOPS",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "i16",
+        "data": "synthetic",
+        "config": {"workload": w.name, **w.dims, "operand_range": [w.lo, w.hi], "seed": w.seed,
+                   "route": route, "chunk": r["plan"]["chunk"]},
+        "roofline": {
+            "bound": "mfma",
+            "achieved": round(achieved_tflops, 1),
+            "peak": peak,
+            "unit": "TFLOP/s" if unit_peak in ("f16", "f32") else "TOP/s",
+            "frac": round(achieved_tflops / peak, 4),
+            "traffic": None,
+            "kernel": "k_gemm_f16x" if route == "f16_exact" else route,
+            "frac_of_int8_peak": round(achieved_tflops / PEAK["i8"], 4),
+        },
+        "timing": {"setup_ms": round(r["setup_ms"], 2), "cached_ms": round(ms, 4),
+                   "exec_ms": round(r["exec_ms_mean"], 4)},
+    }
+    if not args.no_cpu:
+        line["cpu_baseline"] = cpu_baseline(w, args.cpu_rows)
+    if args.all:
+        res = {}
+        for name, wl in WORKLOADS.items():
+            m = measure(wl, max(args.steps, 10), args.warmup, torch, qx)
+            m["gops_cached"] = wl.ops / (m["cached_ms"] / 1e3) / 1e9
+            m["gops_exec"] = wl.ops / (m["exec_ms_mean"] / 1e3) / 1e9
+            res[name] = m
+            print(f"[bench] {name}: {m['gops_cached']:.1f} GOPS cached, "
+                  f"{m['gops_exec']:.1f} GOPS exec-only, route {m['plan']['route_name']}",
+                  file=sys.stderr, flush=True)
+        os.makedirs(os.path.dirname(args.all_out), exist_ok=True)
+        with open(args.all_out, "w") as f:
+            json.dump(res, f, indent=1)
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

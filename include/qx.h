@@ -1,0 +1,193 @@
+/*
+ * qx.h -- C ABI of the MI355X (gfx950) tiled integer matrix-multiplication
+ * substrate: packed INT16-input / INT32-accumulation GEMM, INT32 GEMM under
+ * the smul24 operand contract, GEMM-backed Conv2D through im2col lowering,
+ * the single-head attention core O = (Q K^T) V, and a persistent executor.
+ *
+ * The operations are the ones the paper's Methodology names (tiled
+ * matrix-multiplication substrate reused by every operator, GEMM-backed
+ * convolution through lowering, attention core O = (Q K^T) V, persistent
+ * executors that assemble and allocate once, smul24 operand-range contracts
+ * that decide tiling, packing and accumulation at run time), measured in its
+ * Table 1 (INT32 and packed INT16 / INT32-accumulation GEMM) and Table 2
+ * (Conv2D and attention-core rows).
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ *  - Tensors are caller-owned DEVICE pointers (HIP device memory of the
+ *    current device), dense and row-major, never freed or kept by the
+ *    library.  Pointers to operands with zero elements may be NULL.
+ *  - `stream` is a hipStream_t passed as void* (NULL = the default stream).
+ *    Work is enqueued on it; a return of QX_OK means "enqueued", nothing is
+ *    synchronised.
+ *  - Integer results are exact modulo 2^32 (two's complement), the reading
+ *    of "INT32 accumulation" used throughout.  When the declared contract
+ *    guarantees |result| < 2^31 no wrap ever happens.
+ *  - Arguments are validated on the host before any HIP call; a failure
+ *    returns a status and leaves a message in qx_last_error().  HIP errors
+ *    map to QX_ERR_DEVICE (QX_ERR_OUT_OF_MEMORY for allocation failures).
+ *  - Operand-range contracts (`bound_*` = largest |x| the caller promises)
+ *    pick the exact route.  Operands outside a declared bound give an
+ *    unspecified but memory-safe result.  0 means "no promise": the full
+ *    range of the type.
+ *  - One-shot calls keep an internal plan + workspace cache keyed by shape,
+ *    contract, route, device and stream; calls that share a key must not
+ *    overlap in time.  Executor handles are not thread-safe; different
+ *    handles may run concurrently on different streams.
+ *  - Only gfx950 devices are supported (QX_ERR_UNSUPPORTED otherwise).
+ */
+#ifndef QX_H
+#define QX_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    QX_OK = 0,
+    QX_ERR_INVALID_ARG = 1,   /* null pointer, negative size, size overflow, bad enum */
+    QX_ERR_UNSUPPORTED = 2,   /* valid request this build cannot run (device, route, shape) */
+    QX_ERR_RANGE = 3,         /* declared bound outside what the operation accepts */
+    QX_ERR_OUT_OF_MEMORY = 4, /* workspace allocation failed */
+    QX_ERR_DEVICE = 5         /* a HIP call failed; details in qx_last_error() */
+} qx_status;
+
+typedef enum { QX_DT_F32 = 0, QX_DT_I32 = 1 } qx_attn_dtype;
+
+/* Exact routes of the integer contraction (chosen from the contract).
+ *  I8_DIRECT    operands in [-127, 127]: one int8 MFMA product per multiply-add.
+ *  F16_EXACT    |a|, |b| <= 2048 and chunk*|a|max*|b|max <= 2^24: fp16 MFMA with
+ *               fp32 partial sums over `chunk` K-steps (every partial is an exactly
+ *               representable integer), flushed into int32.
+ *  I8_KARATSUBA operands in [-8127, 8127]: balanced base-128 limbs h, l and h+l,
+ *               three int8 MFMA products.
+ *  I8_OFFSET4   any int16: offset base-256 limbs, four int8 MFMA products plus a
+ *               rank-1 correction from row and column sums.
+ *  VALU_DOT2    any int16: v_dot2_i32_i16 on the vector ALU (comparison path).
+ *  S24_VALU     smul24: v_mad_i32_i24-class vector multiply (contract-native).
+ *  S24_I8LIMB   smul24: three offset int8 limbs, eight int8 MFMA products with
+ *               i+j <= 3, plus a rank-1 correction. */
+typedef enum {
+    QX_ROUTE_AUTO = 0,
+    QX_ROUTE_I8_DIRECT = 1,
+    QX_ROUTE_F16_EXACT = 2,
+    QX_ROUTE_I8_KARATSUBA = 3,
+    QX_ROUTE_I8_OFFSET4 = 4,
+    QX_ROUTE_VALU_DOT2 = 5,
+    QX_ROUTE_S24_VALU = 6,
+    QX_ROUTE_S24_I8LIMB = 7,
+    QX_ROUTE_ATTN_F32_MFMA = 8,  /* attention: fp32 MFMA, S tile kept on chip */
+    QX_ROUTE_ATTN_I32_MFMA = 9,  /* attention: int8 MFMA for QK^T, S split into int8 limbs */
+    QX_ROUTE_ATTN_I32_VALU = 10  /* attention: vector-ALU int32, any operand range */
+} qx_route;
+
+/* What the planner decided for one operation (for tests and reporting). */
+typedef struct {
+    int32_t route;            /* qx_route that will run */
+    int32_t chunk;            /* F16_EXACT: K elements per fp32 partial sum; else 0 */
+    int32_t products;         /* matrix products issued per multiply-add (1, 3, 4, 8 ...) */
+    int32_t tile_m, tile_n, tile_k;  /* workgroup tile of the main kernel */
+    int32_t kernels;          /* kernel launches per run */
+    int32_t exact_no_wrap;    /* 1: contract proves |result| < 2^31; 0: defined mod 2^32 */
+    int64_t workspace_bytes;  /* device workspace owned by the plan */
+} qx_plan_info;
+
+typedef struct qx_exec_s* qx_exec;   /* opaque persistent executor */
+
+/* ---- one-shot operations ------------------------------------------------ */
+
+/* Packed INT16-input / INT32-accumulation GEMM (Methodology; Table 1, right).
+ *   C[b] = A[b] . B[b]   for b < batch
+ * A [batch][M][K] int16, B [batch][K][N] int16, C [batch][M][N] int32.
+ * bound_a / bound_b: max |x| promised for A / B, in [0, 32768] (0 = 32768).
+ * M, N, K, batch >= 0; K == 0 writes zeros; M, N or batch == 0 is a no-op. */
+qx_status qgemm_i16i32(const int16_t* A, const int16_t* B, int32_t* C,
+                       int64_t M, int64_t N, int64_t K, int64_t batch,
+                       int32_t bound_a, int32_t bound_b, void* stream);
+
+/* INT32 GEMM under the smul24 contract (Methodology; Table 1, left).
+ *   C[b,i,j] = sum_k sext24(A[b,i,k]) * sext24(B[b,k,j])   (mod 2^32)
+ * Each int32 operand is read as its low 24 bits, sign-extended (bits 24..31
+ * are ignored, always -- this is the contract, not an error).  Shapes and
+ * size rules as qgemm_i16i32. */
+qx_status qgemm_i32_s24(const int32_t* A, const int32_t* B, int32_t* C,
+                        int64_t M, int64_t N, int64_t K, int64_t batch, void* stream);
+
+/* GEMM-backed Conv2D through im2col lowering (Methodology; Table 2,
+ * INT16-IN/INT32-ACC row).  Cross-correlation with zero padding, no bias,
+ * dilation or groups:
+ *   y[n,co,oh,ow] = sum_{ci,kh,kw} x[n,ci,oh*s-p+kh,ow*s-p+kw] * w[co,ci,kh,kw]
+ * x NCHW int16 [N][C_in][H][W], w OIHW int16 [C_out][C_in][KH][KW],
+ * y NCHW int32 [N][C_out][Ho][Wo], Ho = (H+2p-KH)/s + 1, Wo likewise.
+ * stride >= 1, pad >= 0, KH, KW >= 1, Ho, Wo >= 1; bounds as qgemm_i16i32. */
+qx_status conv2d_gemm(const int16_t* x, const int16_t* w, int32_t* y,
+                      int64_t N, int64_t C_in, int64_t H, int64_t W, int64_t C_out,
+                      int64_t KH, int64_t KW, int64_t stride, int64_t pad,
+                      int32_t bound_x, int32_t bound_w, void* stream);
+
+/* Single-head attention core (Methodology: O = (Q K^T) V; Table 2, attention
+ * rows): no scale, softmax or mask.  Q, K, V, O are [L][d] row-major.
+ *  QX_DT_F32: float32 in and out.  The association (Q K^T) V is evaluated
+ *             (never Q (K^T V)); the sum order is fixed, so repeated runs are
+ *             bit-identical.
+ *  QX_DT_I32: int32 in and out, exact mod 2^32.  bound = max |q|, |k|, |v|
+ *             (0 = full int32); bound <= 127 runs on int8 MFMA, larger on VALU.
+ * L >= 0, d in [0, 256] (the MFMA routes need d % 32 == 0 and d <= 128). */
+qx_status attn_core(qx_attn_dtype dt, const void* Q, const void* K, const void* V, void* O,
+                    int64_t L, int64_t d, int32_t bound, void* stream);
+
+/* ---- persistent executor (Methodology: assemble and allocate once, cache
+ *      launch metadata, re-dispatch) ---------------------------------------- */
+
+/* Plan tiles, choose the route (route = QX_ROUTE_AUTO, or force one; an
+ * infeasible forced route returns QX_ERR_RANGE), allocate the workspace and
+ * build the cached launch records, on the current device.  *out receives the
+ * handle.  Nothing is enqueued. */
+qx_status qx_exec_create_gemm_i16i32(qx_exec* out, int64_t M, int64_t N, int64_t K,
+                                     int64_t batch, int32_t bound_a, int32_t bound_b,
+                                     int32_t route);
+qx_status qx_exec_create_gemm_i32_s24(qx_exec* out, int64_t M, int64_t N, int64_t K,
+                                      int64_t batch, int32_t route);
+qx_status qx_exec_create_conv2d(qx_exec* out, int64_t N, int64_t C_in, int64_t H, int64_t W,
+                                int64_t C_out, int64_t KH, int64_t KW, int64_t stride,
+                                int64_t pad, int32_t bound_x, int32_t bound_w, int32_t route);
+qx_status qx_exec_create_attn(qx_exec* out, qx_attn_dtype dt, int64_t L, int64_t d,
+                              int32_t bound, int32_t route);
+
+/* Enqueue one evaluation: inputs = {A, B} (GEMMs), {x, w} (conv) or
+ * {Q, K, V} (attention), device pointers with the shapes given at create.
+ * Allocates nothing.  Calls on one handle must not overlap in time. */
+qx_status qx_exec_run(qx_exec h, const void* const* inputs, void* output, void* stream);
+
+/* The plan a handle carries. */
+qx_status qx_exec_plan(qx_exec h, qx_plan_info* out);
+
+/* Free the workspace and the handle (waits for the device to finish any
+ * work that may use the workspace).  NULL is accepted. */
+qx_status qx_exec_destroy(qx_exec h);
+
+/* ---- planner queries (pure host logic, no device needed) ---------------- */
+qx_status qx_plan_gemm_i16i32(qx_plan_info* out, int64_t M, int64_t N, int64_t K,
+                              int64_t batch, int32_t bound_a, int32_t bound_b, int32_t route);
+qx_status qx_plan_gemm_i32_s24(qx_plan_info* out, int64_t M, int64_t N, int64_t K,
+                               int64_t batch, int32_t route);
+qx_status qx_plan_conv2d(qx_plan_info* out, int64_t N, int64_t C_in, int64_t H, int64_t W,
+                         int64_t C_out, int64_t KH, int64_t KW, int64_t stride, int64_t pad,
+                         int32_t bound_x, int32_t bound_w, int32_t route);
+qx_status qx_plan_attn(qx_plan_info* out, qx_attn_dtype dt, int64_t L, int64_t d,
+                       int32_t bound, int32_t route);
+
+/* Message of the last failing call on this thread ("" if none).  Valid
+ * until the next qx call on the same thread. */
+const char* qx_last_error(void);
+
+/* Release the one-shot plan cache (frees its workspaces). */
+void qx_release_cache(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* QX_H */

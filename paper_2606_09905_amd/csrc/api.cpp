@@ -1,0 +1,817 @@
+// api.cpp -- planner, persistent executor and the C ABI of libqx.
+//
+// Planner: turns an operation, its shape and its operand-range contract into
+// a route, tiles, launch records and a workspace size (Methodology: operand
+// range contracts propagate to the operators and decide tiling, packing and
+// accumulation at run time).  Pure host logic; exported through the
+// qx_plan_* queries so it can be checked without a device.
+//
+// Executor: a handle that planned once, allocated its workspace once and
+// keeps the launch records; a run patches the caller's pointers into the
+// cached parameter blocks and enqueues the launches (Methodology: persistent
+// executors that assemble kernels and allocate device buffers once and cache
+// dispatch metadata).
+#include <hip/hip_runtime.h>
+
+#include <cstdarg>
+#include <cstdio>
+#include <map>
+#include <mutex>
+#include <string>
+#include <tuple>
+#include <vector>
+
+#include "../../include/qx.h"
+#include "qx_internal.h"
+
+using namespace qx;
+
+namespace {
+
+thread_local std::string g_err;
+
+qx_status fail(qx_status s, const char* fmt, ...) {
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof buf, fmt, ap);
+    va_end(ap);
+    g_err = buf;
+    return s;
+}
+
+qx_status hip_fail(hipError_t e, const char* what) {
+    return fail(e == hipErrorOutOfMemory ? QX_ERR_OUT_OF_MEMORY : QX_ERR_DEVICE, "%s: %s (%d)", what,
+                hipGetErrorString(e), (int)e);
+}
+
+constexpr int64_t kMaxDim = (int64_t)1 << 30;
+constexpr int64_t kMaxBatch = 65535;
+constexpr uint32_t kMagic = 0x71786578u;  // "qxex"
+
+enum OpKind : int32_t { OP_GEMM_I16 = 1, OP_GEMM_S24 = 2, OP_CONV = 3, OP_ATTN_F32 = 4, OP_ATTN_I32 = 5 };
+
+// A fully planned operation: route facts plus launch records with unbound
+// pointers.  Built on the host with no device call.
+struct Plan {
+    OpKind op{};
+    qx_plan_info info{};
+    std::vector<LaunchRec> launches;
+    int n_inputs = 0;
+    uint64_t in_align = 16;  // required alignment of every input pointer
+};
+
+bool mul_ok(int64_t a, int64_t b, int64_t lim, int64_t* out) {
+    if (a < 0 || b < 0) return false;
+    if (a != 0 && b > lim / a) return false;
+    *out = a * b;
+    return true;
+}
+
+uint64_t round_up(uint64_t v, uint64_t a) { return (v + a - 1) / a * a; }
+
+// ---------------------------------------------------------------------------
+// Exactness rules of the integer routes.
+// ---------------------------------------------------------------------------
+// Largest multiple of 16 with chunk * ba * bb <= 2^24: every partial sum of
+// that many products is an integer of magnitude <= 2^24, exactly
+// representable in fp32.  0 if infeasible (operands beyond fp16's exact
+// integer range, or fewer than 16 products per partial).
+int64_t f16_chunk(int64_t ba, int64_t bb) {
+    if (ba > 2048 || bb > 2048) return 0;
+    const int64_t prod = std::max<int64_t>(ba * bb, 1);
+    int64_t c = ((int64_t)1 << 24) / prod;
+    c = c / 16 * 16;
+    return c >= 16 ? c : 0;
+}
+
+bool route_applies_i16(int32_t r) {
+    return r == R_I8_DIRECT || r == R_F16_EXACT || r == R_I8_KARATSUBA || r == R_I8_OFFSET4 ||
+           r == R_VALU_DOT2;
+}
+
+// Route feasibility for an int16 contraction with bounds ba, bb (max |x|).
+bool feasible_i16(int32_t r, int64_t ba, int64_t bb) {
+    switch (r) {
+    case R_I8_DIRECT: return ba <= 127 && bb <= 127;
+    case R_F16_EXACT: return f16_chunk(ba, bb) > 0;
+    case R_I8_KARATSUBA: return ba <= 8127 && bb <= 8127;
+    case R_I8_OFFSET4:
+    case R_VALU_DOT2: return true;
+    default: return false;
+    }
+}
+
+int32_t auto_i16(int64_t ba, int64_t bb) {
+    if (feasible_i16(R_I8_DIRECT, ba, bb)) return R_I8_DIRECT;
+    if (feasible_i16(R_F16_EXACT, ba, bb)) return R_F16_EXACT;
+    if (feasible_i16(R_I8_KARATSUBA, ba, bb)) return R_I8_KARATSUBA;
+    return R_I8_OFFSET4;
+}
+
+int32_t products_of(int32_t r) {
+    switch (r) {
+    case R_I8_KARATSUBA: return 3;
+    case R_I8_OFFSET4: return 4;
+    case R_S24_I8LIMB: return 8;
+    case R_ATTN_I32_MFMA: return 3;
+    default: return 1;
+    }
+}
+
+qx_status check_bound16(int32_t b, const char* name, int64_t* out) {
+    if (b < 0 || b > 32768) return fail(QX_ERR_INVALID_ARG, "%s = %d: must be in [0, 32768]", name, b);
+    *out = b == 0 ? 32768 : b;
+    return QX_OK;
+}
+
+// ---------------------------------------------------------------------------
+// Integer GEMM planning shared by the GEMM and convolution operators.
+// ---------------------------------------------------------------------------
+struct GemmSpec {
+    int64_t M, N, K, batch;
+    int64_t ba, bb;      // bounds (i16 routes); unused for s24
+    bool s24;
+    int32_t route;       // requested
+    // operand bindings
+    Bind a_bind, b_bind;
+    uint64_t b_ws_off;   // when b_bind == BIND_WS
+    int64_t lda, ldb, ldc, sA, sB, sC;
+    int32_t out_mode, hw;
+};
+
+// Appends the launches of one integer GEMM; ws_used is the workspace end.
+qx_status plan_int_gemm(const GemmSpec& s, Plan* pl, uint64_t* ws_used) {
+    int32_t route = s.route;
+    if (!s.s24) {
+        if (route == R_AUTO) route = auto_i16(s.ba, s.bb);
+        if (!route_applies_i16(route))
+            return fail(QX_ERR_INVALID_ARG, "route %d does not apply to an int16 contraction", route);
+        if (!feasible_i16(route, s.ba, s.bb))
+            return fail(QX_ERR_RANGE, "route %d cannot be exact for bounds %lld x %lld", route,
+                        (long long)s.ba, (long long)s.bb);
+    } else {
+        if (route == R_AUTO) route = R_S24_I8LIMB;
+        if (route != R_S24_I8LIMB && route != R_S24_VALU)
+            return fail(QX_ERR_INVALID_ARG, "route %d does not apply to the smul24 GEMM", route);
+    }
+    qx_plan_info& info = pl->info;
+    info.route = route;
+    info.products = products_of(route);
+    info.chunk = 0;
+    if (s.s24) {
+        info.exact_no_wrap = 0;
+    } else {
+        const double maxabs = (double)s.K * (double)s.ba * (double)s.bb;
+        info.exact_no_wrap = maxabs < 2147483648.0 ? 1 : 0;
+    }
+
+    if (route == R_VALU_DOT2 || route == R_S24_VALU) {
+        if ((s.M + 63) / 64 > 65535) return fail(QX_ERR_UNSUPPORTED, "M too large for the VALU route");
+        ValuGemmParams v{};
+        v.sA = s.sA; v.sB = s.sB; v.sC = s.sC;
+        v.M = (int32_t)s.M; v.N = (int32_t)s.N; v.K = (int32_t)s.K;
+        v.lda = (int32_t)s.lda; v.ldb = (int32_t)s.ldb; v.ldc = (int32_t)s.ldc;
+        v.b_trans = 0; v.out_mode = s.out_mode; v.hw = s.hw;
+        LaunchRec rec;
+        build_valu_gemm(route == R_VALU_DOT2 ? VK_I16_DOT2 : VK_S24, v, (int)s.batch, &rec);
+        rec.bind(offsetof(ValuGemmParams, A), s.a_bind);
+        rec.bind(offsetof(ValuGemmParams, B), s.b_bind, s.b_ws_off);
+        rec.bind(offsetof(ValuGemmParams, C), BIND_OUT);
+        pl->launches.push_back(rec);
+        info.tile_m = 64; info.tile_n = 64; info.tile_k = 16;
+        return QX_OK;
+    }
+
+    GemmParams g{};
+    g.sA = s.sA; g.sB = s.sB; g.sC = s.sC;
+    g.M = (int32_t)s.M; g.N = (int32_t)s.N; g.K = (int32_t)s.K;
+    g.lda = (int32_t)s.lda; g.ldb = (int32_t)s.ldb; g.ldc = (int32_t)s.ldc;
+    g.out_mode = s.out_mode; g.hw = s.hw; g.b_mode = B_KN;
+    const bool offset = route == R_I8_OFFSET4 || route == R_S24_I8LIMB;
+    uint64_t rs_off = 0, cs_off = 0;
+    if (offset) {
+        g.corr_c = route == R_I8_OFFSET4 ? 128 : 32896;
+        rs_off = round_up(*ws_used, 256);
+        cs_off = round_up(rs_off + 4 * (uint64_t)s.batch * (uint64_t)s.M, 256);
+        *ws_used = cs_off + 4 * (uint64_t)s.batch * (uint64_t)s.N;
+        SumsParams sp{};
+        sp.sA = s.sA; sp.sB = s.sB;
+        sp.M = (int32_t)s.M; sp.N = (int32_t)s.N; sp.K = (int32_t)s.K;
+        sp.lda = (int32_t)s.lda; sp.ldb = (int32_t)s.ldb;
+        sp.s24 = s.s24 ? 1 : 0; sp.batch = (int32_t)s.batch;
+        LaunchRec rec;
+        build_sums(sp, &rec);
+        rec.bind(offsetof(SumsParams, A), s.a_bind);
+        rec.bind(offsetof(SumsParams, B), s.b_bind, s.b_ws_off);
+        rec.bind(offsetof(SumsParams, rowsum), BIND_WS, rs_off);
+        rec.bind(offsetof(SumsParams, colsum), BIND_WS, cs_off);
+        pl->launches.push_back(rec);
+    }
+    if (route == R_F16_EXACT) {
+        const int64_t chunk = f16_chunk(s.ba, s.bb);
+        g.chunk_tiles = chunk >= 64 ? (int32_t)(chunk / 64) : 0;
+        info.chunk = chunk >= 64 ? (int32_t)(chunk / 64 * 64) : 16;
+    }
+    LaunchRec rec;
+    int tm = 0, tn = 0, tk = 0;
+    if (!build_gemm_mfma(route, g, (int)s.batch, &rec, &tm, &tn, &tk))
+        return fail(QX_ERR_UNSUPPORTED, "no kernel for route %d", route);
+    rec.bind(offsetof(GemmParams, A), s.a_bind);
+    rec.bind(offsetof(GemmParams, B), s.b_bind, s.b_ws_off);
+    rec.bind(offsetof(GemmParams, C), BIND_OUT);
+    if (offset) {
+        rec.bind(offsetof(GemmParams, rowsum), BIND_WS, rs_off);
+        rec.bind(offsetof(GemmParams, colsum), BIND_WS, cs_off);
+    }
+    pl->launches.push_back(rec);
+    info.tile_m = tm; info.tile_n = tn; info.tile_k = tk;
+    return QX_OK;
+}
+
+void add_fill_out(Plan* pl, int64_t n32) {
+    FillParams f{};
+    f.n32 = n32;
+    f.value = 0;
+    LaunchRec rec;
+    build_fill(f, &rec);
+    rec.bind(offsetof(FillParams, ptr), BIND_OUT);
+    pl->launches.push_back(rec);
+}
+
+qx_status check_dims(std::initializer_list<std::pair<const char*, int64_t>> dims) {
+    for (auto& d : dims) {
+        if (d.second < 0) return fail(QX_ERR_INVALID_ARG, "%s = %lld must be >= 0", d.first, (long long)d.second);
+        if (d.second > kMaxDim)
+            return fail(QX_ERR_UNSUPPORTED, "%s = %lld exceeds 2^30", d.first, (long long)d.second);
+    }
+    return QX_OK;
+}
+
+qx_status plan_gemm(Plan* pl, bool s24, int64_t M, int64_t N, int64_t K, int64_t batch, int32_t bound_a,
+                    int32_t bound_b, int32_t route) {
+    qx_status st = check_dims({{"M", M}, {"N", N}, {"K", K}, {"batch", batch}});
+    if (st) return st;
+    if (batch > kMaxBatch) return fail(QX_ERR_UNSUPPORTED, "batch = %lld exceeds 65535", (long long)batch);
+    int64_t ba = 0, bb = 0;
+    if (!s24) {
+        if ((st = check_bound16(bound_a, "bound_a", &ba))) return st;
+        if ((st = check_bound16(bound_b, "bound_b", &bb))) return st;
+    }
+    int64_t t;
+    if (!mul_ok(M, K, (int64_t)1 << 40, &t) || !mul_ok(K, N, (int64_t)1 << 40, &t) ||
+        !mul_ok(M, N, (int64_t)1 << 40, &t))
+        return fail(QX_ERR_UNSUPPORTED, "matrix larger than 2^40 elements");
+    int64_t total;
+    if (!mul_ok(M * N, batch, (int64_t)1 << 42, &total) || !mul_ok(M * K, batch, (int64_t)1 << 42, &total) ||
+        !mul_ok(K * N, batch, (int64_t)1 << 42, &total))
+        return fail(QX_ERR_UNSUPPORTED, "batched operands larger than 2^42 elements");
+    pl->op = s24 ? OP_GEMM_S24 : OP_GEMM_I16;
+    pl->n_inputs = 2;
+    pl->in_align = 16;
+    if (route < 0 || route > R_ATTN_I32_VALU) return fail(QX_ERR_INVALID_ARG, "unknown route %d", route);
+    // Route choice happens even for empty problems so that plan queries and
+    // forced-route errors do not depend on the sizes.
+    GemmSpec s{};
+    s.M = M; s.N = N; s.K = K; s.batch = batch; s.ba = ba; s.bb = bb; s.s24 = s24; s.route = route;
+    s.a_bind = BIND_IN0; s.b_bind = BIND_IN1; s.b_ws_off = 0;
+    s.lda = K; s.ldb = N; s.ldc = N; s.sA = M * K; s.sB = K * N; s.sC = M * N;
+    s.out_mode = OUT_ROWMAJOR; s.hw = 1;
+    uint64_t ws = 0;
+    Plan scratch;
+    scratch.info = pl->info;
+    if ((st = plan_int_gemm(s, &scratch, &ws))) return st;
+    pl->info = scratch.info;
+    if (M == 0 || N == 0 || batch == 0) {
+        pl->launches.clear();
+        pl->info.kernels = 0;
+        pl->info.workspace_bytes = 0;
+        return QX_OK;
+    }
+    if (K == 0) {
+        add_fill_out(pl, M * N * batch);
+        pl->info.kernels = 1;
+        pl->info.workspace_bytes = 0;
+        return QX_OK;
+    }
+    pl->launches = scratch.launches;
+    pl->info.kernels = (int32_t)pl->launches.size();
+    pl->info.workspace_bytes = (int64_t)ws;
+    return QX_OK;
+}
+
+qx_status plan_conv(Plan* pl, int64_t N, int64_t Ci, int64_t H, int64_t W, int64_t Co, int64_t KH, int64_t KW,
+                    int64_t stride, int64_t pad, int32_t bound_x, int32_t bound_w, int32_t route) {
+    qx_status st = check_dims({{"N", N}, {"C_in", Ci}, {"H", H}, {"W", W}, {"C_out", Co}, {"KH", KH},
+                               {"KW", KW}, {"stride", stride}, {"pad", pad}});
+    if (st) return st;
+    if (stride < 1) return fail(QX_ERR_INVALID_ARG, "stride = %lld must be >= 1", (long long)stride);
+    if (KH < 1 || KW < 1) return fail(QX_ERR_INVALID_ARG, "kernel size must be >= 1");
+    const int64_t Ho = (H + 2 * pad - KH) >= 0 ? (H + 2 * pad - KH) / stride + 1 : 0;
+    const int64_t Wo = (W + 2 * pad - KW) >= 0 ? (W + 2 * pad - KW) / stride + 1 : 0;
+    if (Ho < 1 || Wo < 1)
+        return fail(QX_ERR_INVALID_ARG, "kernel %lldx%lld larger than the padded %lldx%lld input", (long long)KH,
+                    (long long)KW, (long long)(H + 2 * pad), (long long)(W + 2 * pad));
+    int64_t ba, bb;
+    if ((st = check_bound16(bound_w, "bound_w", &ba))) return st;
+    if ((st = check_bound16(bound_x, "bound_x", &bb))) return st;
+    int64_t Kd, P, t;
+    if (!mul_ok(Ci, KH * KW, kMaxDim, &Kd) || !mul_ok(N, Ho * Wo, kMaxDim, &P) ||
+        !mul_ok(Kd, P, (int64_t)1 << 40, &t) || !mul_ok(Co, P, (int64_t)1 << 40, &t))
+        return fail(QX_ERR_UNSUPPORTED, "convolution too large");
+    if (Kd > 65535) return fail(QX_ERR_UNSUPPORTED, "C_in*KH*KW = %lld exceeds 65535", (long long)Kd);
+    if (route < 0 || route > R_ATTN_I32_VALU) return fail(QX_ERR_INVALID_ARG, "unknown route %d", route);
+    pl->op = OP_CONV;
+    pl->n_inputs = 2;
+    pl->in_align = 16;
+    // GEMM view: A = w [Co][Kd], B = col [Kd][P] in the workspace, C = y (NCHW scatter).
+    GemmSpec s{};
+    s.M = Co; s.N = P; s.K = Kd; s.batch = 1; s.ba = ba; s.bb = bb; s.s24 = false; s.route = route;
+    s.a_bind = BIND_IN1; s.b_bind = BIND_WS; s.b_ws_off = 0;
+    s.lda = Kd; s.ldb = P; s.ldc = P; s.sA = 0; s.sB = 0; s.sC = 0;
+    s.out_mode = OUT_CONV; s.hw = (int32_t)(Ho * Wo);
+    uint64_t ws = round_up(2 * (uint64_t)Kd * (uint64_t)P, 256);
+    Plan g;
+    g.info = pl->info;
+    if ((st = plan_int_gemm(s, &g, &ws))) return st;
+    pl->info = g.info;
+    if (N == 0 || Co == 0) {
+        pl->launches.clear();
+        pl->info.kernels = 0;
+        pl->info.workspace_bytes = 0;
+        return QX_OK;
+    }
+    if (Ci == 0) {
+        add_fill_out(pl, N * Co * Ho * Wo);
+        pl->info.kernels = 1;
+        pl->info.workspace_bytes = 0;
+        return QX_OK;
+    }
+    Im2colParams ip{};
+    ip.P = P;
+    ip.Kd = (int32_t)Kd;
+    ip.g = ConvGeom{(int32_t)Ci, (int32_t)H, (int32_t)W, (int32_t)KH, (int32_t)KW, (int32_t)stride, (int32_t)pad,
+                    (int32_t)Ho, (int32_t)Wo};
+    LaunchRec rec;
+    build_im2col(ip, &rec);
+    rec.bind(offsetof(Im2colParams, x), BIND_IN0);
+    rec.bind(offsetof(Im2colParams, col), BIND_WS, 0);
+    pl->launches.push_back(rec);
+    for (auto& r : g.launches) pl->launches.push_back(r);
+    pl->info.kernels = (int32_t)pl->launches.size();
+    pl->info.workspace_bytes = (int64_t)ws;
+    return QX_OK;
+}
+
+qx_status plan_attn(Plan* pl, qx_attn_dtype dt, int64_t L, int64_t d, int32_t bound, int32_t route) {
+    qx_status st = check_dims({{"L", L}, {"d", d}});
+    if (st) return st;
+    if (dt != QX_DT_F32 && dt != QX_DT_I32) return fail(QX_ERR_INVALID_ARG, "unknown attention dtype %d", (int)dt);
+    if (d > 256) return fail(QX_ERR_UNSUPPORTED, "d = %lld exceeds 256", (long long)d);
+    if (L > (1 << 20)) return fail(QX_ERR_UNSUPPORTED, "L = %lld exceeds 2^20", (long long)L);
+    if (bound < 0) return fail(QX_ERR_INVALID_ARG, "bound = %d must be >= 0", bound);
+    pl->op = dt == QX_DT_F32 ? OP_ATTN_F32 : OP_ATTN_I32;
+    pl->n_inputs = 3;
+    pl->in_align = 16;
+    qx_plan_info& info = pl->info;
+    const bool mfma_shape = d >= 32 && d <= 128 && d % 32 == 0;
+    int32_t r = route;
+    if (dt == QX_DT_F32) {
+        if (r == R_AUTO) r = mfma_shape ? R_ATTN_F32_MFMA : R_ATTN_F32_VALU;
+        if (r != R_ATTN_F32_MFMA && r != R_ATTN_F32_VALU)
+            return fail(QX_ERR_INVALID_ARG, "route %d does not apply to FP32 attention", route);
+        if (r == R_ATTN_F32_MFMA && !mfma_shape)
+            return fail(QX_ERR_UNSUPPORTED, "fp32 MFMA attention needs d in {32, 64, 96, 128}");
+        info.exact_no_wrap = 0;
+    } else {
+        const int64_t b = bound == 0 ? ((int64_t)1 << 31) : bound;
+        const bool in8 = b <= 127 && (double)d * (double)b * (double)b < 8388608.0;
+        if (r == R_AUTO) r = (mfma_shape && in8) ? R_ATTN_I32_MFMA : R_ATTN_I32_VALU;
+        if (r != R_ATTN_I32_MFMA && r != R_ATTN_I32_VALU)
+            return fail(QX_ERR_INVALID_ARG, "route %d does not apply to INT32 attention", route);
+        if (r == R_ATTN_I32_MFMA && !in8)
+            return fail(QX_ERR_RANGE, "int8 attention needs bound <= 127 and d*bound^2 < 2^23");
+        if (r == R_ATTN_I32_MFMA && !mfma_shape)
+            return fail(QX_ERR_UNSUPPORTED, "int8 MFMA attention needs d in {32, 64, 96, 128}");
+        info.exact_no_wrap = ((double)L * (double)d * (double)b * (double)b * (double)b < 2147483648.0) ? 1 : 0;
+    }
+    info.route = r;
+    info.products = r == R_ATTN_I32_MFMA ? 3 : 1;
+    info.chunk = 0;
+    if (L == 0 || d == 0) {
+        info.kernels = 0;
+        info.workspace_bytes = 0;
+        return QX_OK;
+    }
+    uint64_t ws = 0;
+    if (r == R_ATTN_F32_VALU || r == R_ATTN_I32_VALU) {
+        // S = Q K^T into the workspace, then O = S V, both on the vector ALU.
+        const int kind = r == R_ATTN_F32_VALU ? VK_F32 : VK_I32;
+        int64_t ss;
+        if (!mul_ok(L, L, (int64_t)1 << 34, &ss) || (L + 63) / 64 > 65535)
+            return fail(QX_ERR_UNSUPPORTED, "L too large for the VALU route");
+        ws = 4 * (uint64_t)ss;
+        ValuGemmParams v{};
+        v.M = (int32_t)L; v.N = (int32_t)L; v.K = (int32_t)d;
+        v.lda = (int32_t)d; v.ldb = (int32_t)d; v.ldc = (int32_t)L; v.b_trans = 1; v.out_mode = OUT_ROWMAJOR;
+        LaunchRec r1;
+        build_valu_gemm(kind, v, 1, &r1);
+        r1.bind(offsetof(ValuGemmParams, A), BIND_IN0);
+        r1.bind(offsetof(ValuGemmParams, B), BIND_IN1);
+        r1.bind(offsetof(ValuGemmParams, C), BIND_WS, 0);
+        ValuGemmParams v2{};
+        v2.M = (int32_t)L; v2.N = (int32_t)d; v2.K = (int32_t)L;
+        v2.lda = (int32_t)L; v2.ldb = (int32_t)d; v2.ldc = (int32_t)d; v2.b_trans = 0; v2.out_mode = OUT_ROWMAJOR;
+        LaunchRec r2;
+        build_valu_gemm(kind, v2, 1, &r2);
+        r2.bind(offsetof(ValuGemmParams, A), BIND_WS, 0);
+        r2.bind(offsetof(ValuGemmParams, B), BIND_IN2);
+        r2.bind(offsetof(ValuGemmParams, C), BIND_OUT);
+        pl->launches.push_back(r1);
+        pl->launches.push_back(r2);
+        info.tile_m = 64; info.tile_n = 64; info.tile_k = 16;
+    } else {
+        // Key splits: enough workgroups to cover the chip (>= 512), split
+        // boundaries on 32-key blocks.
+        const int64_t qgroups = (L + 127) / 128;
+        const int64_t kblocks = (L + 31) / 32;
+        int64_t splits = std::min<int64_t>(std::max<int64_t>((512 + qgroups - 1) / qgroups, 1), kblocks);
+        const int64_t kps = ((kblocks + splits - 1) / splits) * 32;
+        splits = (L + kps - 1) / kps;
+        AttnParams a{};
+        a.L = (int32_t)L; a.d = (int32_t)d; a.splits = (int32_t)splits; a.keys_per_split = (int32_t)kps;
+        a.limbs = 3;
+        LaunchRec rec;
+        if (r == R_ATTN_F32_MFMA) {
+            build_attn_f32(a, &rec);
+            rec.bind(offsetof(AttnParams, Q), BIND_IN0);
+            rec.bind(offsetof(AttnParams, K), BIND_IN1);
+            rec.bind(offsetof(AttnParams, V), BIND_IN2);
+            rec.bind(offsetof(AttnParams, O), BIND_OUT);
+            if (splits > 1) {
+                ws = 4 * (uint64_t)splits * (uint64_t)L * (uint64_t)d;
+                rec.bind(offsetof(AttnParams, part), BIND_WS, 0);
+                pl->launches.push_back(rec);
+                ReduceParams rp{};
+                rp.n = L * d;
+                rp.splits = (int32_t)splits;
+                LaunchRec rr;
+                build_reduce(rp, &rr);
+                rr.bind(offsetof(ReduceParams, part), BIND_WS, 0);
+                rr.bind(offsetof(ReduceParams, out), BIND_OUT);
+                pl->launches.push_back(rr);
+            } else {
+                pl->launches.push_back(rec);
+            }
+        } else {
+            // column sums of V (the offset limbs' correction), then the
+            // output cleared for split accumulation, then the kernel.
+            ws = 4 * (uint64_t)d;
+            SumsParams sp{};
+            sp.M = 0; sp.N = (int32_t)d; sp.K = (int32_t)L; sp.lda = 0; sp.ldb = (int32_t)d;
+            sp.s24 = 1; sp.batch = 1;
+            LaunchRec rs;
+            build_sums(sp, &rs);
+            rs.bind(offsetof(SumsParams, B), BIND_IN2);
+            rs.bind(offsetof(SumsParams, colsum), BIND_WS, 0);
+            pl->launches.push_back(rs);
+            if (splits > 1) add_fill_out(pl, L * d);
+            build_attn_i32(a, &rec);
+            rec.bind(offsetof(AttnParams, Q), BIND_IN0);
+            rec.bind(offsetof(AttnParams, K), BIND_IN1);
+            rec.bind(offsetof(AttnParams, V), BIND_IN2);
+            rec.bind(offsetof(AttnParams, O), BIND_OUT);
+            rec.bind(offsetof(AttnParams, vcs), BIND_WS, 0);
+            pl->launches.push_back(rec);
+        }
+        info.tile_m = 128; info.tile_n = (int32_t)d; info.tile_k = (int32_t)kps;
+    }
+    info.kernels = (int32_t)pl->launches.size();
+    info.workspace_bytes = (int64_t)ws;
+    return QX_OK;
+}
+
+}  // namespace
+
+// ---------------------------------------------------------------------------
+// Executor
+// ---------------------------------------------------------------------------
+struct qx_exec_s {
+    uint32_t magic;
+    int device;
+    Plan plan;
+    void* ws;
+    uint64_t ws_bytes;
+};
+
+namespace {
+
+qx_status check_device(int* dev) {
+    hipError_t e = hipGetDevice(dev);
+    if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+    hipDeviceProp_t prop;
+    e = hipGetDeviceProperties(&prop, *dev);
+    if (e != hipSuccess) return hip_fail(e, "hipGetDeviceProperties");
+    if (strncmp(prop.gcnArchName, "gfx950", 6) != 0)
+        return fail(QX_ERR_UNSUPPORTED, "device %d is %s; this library is built for gfx950 only", *dev,
+                    prop.gcnArchName);
+    return QX_OK;
+}
+
+qx_status make_exec(Plan&& pl, qx_exec* out) {
+    if (!out) return fail(QX_ERR_INVALID_ARG, "out is NULL");
+    *out = nullptr;
+    int dev = 0;
+    qx_status st = check_device(&dev);
+    if (st) return st;
+    qx_exec h = new qx_exec_s();
+    h->magic = kMagic;
+    h->device = dev;
+    h->ws = nullptr;
+    h->ws_bytes = (uint64_t)pl.info.workspace_bytes;
+    h->plan = std::move(pl);
+    if (h->ws_bytes) {
+        hipError_t e = hipMalloc(&h->ws, h->ws_bytes);
+        if (e != hipSuccess) {
+            h->ws = nullptr;
+            h->magic = 0;
+            delete h;
+            (void)hipGetLastError();
+            return hip_fail(e, "workspace hipMalloc");
+        }
+    }
+    *out = h;
+    return QX_OK;
+}
+
+qx_status run_exec(qx_exec h, const void* const* inputs, void* output, void* stream) {
+    if (!h || h->magic != kMagic) return fail(QX_ERR_INVALID_ARG, "invalid executor handle");
+    const Plan& pl = h->plan;
+    if (pl.launches.empty()) return QX_OK;
+    if (!inputs) return fail(QX_ERR_INVALID_ARG, "inputs is NULL");
+    for (int i = 0; i < pl.n_inputs; ++i) {
+        if (!inputs[i]) return fail(QX_ERR_INVALID_ARG, "input %d is NULL", i);
+        if ((uintptr_t)inputs[i] % pl.in_align)
+            return fail(QX_ERR_INVALID_ARG, "input %d is not %llu-byte aligned", i, (unsigned long long)pl.in_align);
+    }
+    if (!output) return fail(QX_ERR_INVALID_ARG, "output is NULL");
+    int dev = -1;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+    if (dev != h->device)
+        return fail(QX_ERR_INVALID_ARG, "handle was created on device %d, current device is %d", h->device, dev);
+    hipStream_t s = (hipStream_t)stream;
+    for (const LaunchRec& r0 : pl.launches) {
+        LaunchRec r = r0;
+        for (int i = 0; i < r.nslots; ++i) {
+            const Slot& sl = r.slots[i];
+            const void* ptr = nullptr;
+            switch (sl.bind) {
+            case BIND_IN0: ptr = inputs[0]; break;
+            case BIND_IN1: ptr = inputs[1]; break;
+            case BIND_IN2: ptr = inputs[2]; break;
+            case BIND_OUT: ptr = output; break;
+            case BIND_WS: ptr = (const char*)h->ws + sl.ws_off; break;
+            }
+            memcpy(r.blob + sl.off, &ptr, sizeof(void*));
+        }
+        void* args[1] = {r.blob};
+        e = hipLaunchKernel(r.fn, r.grid, r.block, args, r.shmem, s);
+        if (e != hipSuccess) return hip_fail(e, r.name);
+    }
+    return QX_OK;
+}
+
+// One-shot calls: a cache of executors keyed by the full request.
+typedef std::tuple<int, int, int64_t, int64_t, int64_t, int64_t, int64_t, int64_t, int64_t, int64_t, int64_t,
+                   int64_t, int64_t, int64_t, uintptr_t>
+    Key;
+std::mutex g_cache_mu;
+std::map<Key, qx_exec>* g_cache = new std::map<Key, qx_exec>();
+
+template <class MakePlan>
+qx_status oneshot(const Key& key0, MakePlan make_plan, const void* const* inputs, void* output, void* stream) {
+    int dev = -1;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+    Key key = key0;
+    std::get<1>(key) = dev;
+    qx_exec h = nullptr;
+    {
+        std::lock_guard<std::mutex> lk(g_cache_mu);
+        auto it = g_cache->find(key);
+        if (it != g_cache->end()) h = it->second;
+    }
+    if (!h) {
+        Plan pl;
+        qx_status st = make_plan(&pl);
+        if (st) return st;
+        if ((st = make_exec(std::move(pl), &h))) return st;
+        std::lock_guard<std::mutex> lk(g_cache_mu);
+        auto ins = g_cache->emplace(key, h);
+        if (!ins.second) {  // another thread won the race
+            qx_exec_destroy(h);
+            h = ins.first->second;
+        }
+    }
+    return run_exec(h, inputs, output, stream);
+}
+
+}  // namespace
+
+// ---------------------------------------------------------------------------
+// C ABI
+// ---------------------------------------------------------------------------
+extern "C" {
+
+const char* qx_last_error(void) { return g_err.c_str(); }
+
+qx_status qx_plan_gemm_i16i32(qx_plan_info* out, int64_t M, int64_t N, int64_t K, int64_t batch, int32_t bound_a,
+                              int32_t bound_b, int32_t route) {
+    g_err.clear();
+    if (!out) return fail(QX_ERR_INVALID_ARG, "out is NULL");
+    Plan pl;
+    qx_status st = plan_gemm(&pl, false, M, N, K, batch, bound_a, bound_b, route);
+    if (!st) *out = pl.info;
+    return st;
+}
+
+qx_status qx_plan_gemm_i32_s24(qx_plan_info* out, int64_t M, int64_t N, int64_t K, int64_t batch, int32_t route) {
+    g_err.clear();
+    if (!out) return fail(QX_ERR_INVALID_ARG, "out is NULL");
+    Plan pl;
+    qx_status st = plan_gemm(&pl, true, M, N, K, batch, 0, 0, route);
+    if (!st) *out = pl.info;
+    return st;
+}
+
+qx_status qx_plan_conv2d(qx_plan_info* out, int64_t N, int64_t C_in, int64_t H, int64_t W, int64_t C_out,
+                         int64_t KH, int64_t KW, int64_t stride, int64_t pad, int32_t bound_x, int32_t bound_w,
+                         int32_t route) {
+    g_err.clear();
+    if (!out) return fail(QX_ERR_INVALID_ARG, "out is NULL");
+    Plan pl;
+    qx_status st = plan_conv(&pl, N, C_in, H, W, C_out, KH, KW, stride, pad, bound_x, bound_w, route);
+    if (!st) *out = pl.info;
+    return st;
+}
+
+qx_status qx_plan_attn(qx_plan_info* out, qx_attn_dtype dt, int64_t L, int64_t d, int32_t bound, int32_t route) {
+    g_err.clear();
+    if (!out) return fail(QX_ERR_INVALID_ARG, "out is NULL");
+    Plan pl;
+    qx_status st = plan_attn(&pl, dt, L, d, bound, route);
+    if (!st) *out = pl.info;
+    return st;
+}
+
+qx_status qx_exec_create_gemm_i16i32(qx_exec* out, int64_t M, int64_t N, int64_t K, int64_t batch, int32_t bound_a,
+                                     int32_t bound_b, int32_t route) {
+    g_err.clear();
+    if (!out) return fail(QX_ERR_INVALID_ARG, "out is NULL");
+    *out = nullptr;
+    Plan pl;
+    qx_status st = plan_gemm(&pl, false, M, N, K, batch, bound_a, bound_b, route);
+    if (st) return st;
+    return make_exec(std::move(pl), out);
+}
+
+qx_status qx_exec_create_gemm_i32_s24(qx_exec* out, int64_t M, int64_t N, int64_t K, int64_t batch, int32_t route) {
+    g_err.clear();
+    if (!out) return fail(QX_ERR_INVALID_ARG, "out is NULL");
+    *out = nullptr;
+    Plan pl;
+    qx_status st = plan_gemm(&pl, true, M, N, K, batch, 0, 0, route);
+    if (st) return st;
+    return make_exec(std::move(pl), out);
+}
+
+qx_status qx_exec_create_conv2d(qx_exec* out, int64_t N, int64_t C_in, int64_t H, int64_t W, int64_t C_out,
+                                int64_t KH, int64_t KW, int64_t stride, int64_t pad, int32_t bound_x, int32_t bound_w,
+                                int32_t route) {
+    g_err.clear();
+    if (!out) return fail(QX_ERR_INVALID_ARG, "out is NULL");
+    *out = nullptr;
+    Plan pl;
+    qx_status st = plan_conv(&pl, N, C_in, H, W, C_out, KH, KW, stride, pad, bound_x, bound_w, route);
+    if (st) return st;
+    return make_exec(std::move(pl), out);
+}
+
+qx_status qx_exec_create_attn(qx_exec* out, qx_attn_dtype dt, int64_t L, int64_t d, int32_t bound, int32_t route) {
+    g_err.clear();
+    if (!out) return fail(QX_ERR_INVALID_ARG, "out is NULL");
+    *out = nullptr;
+    Plan pl;
+    qx_status st = plan_attn(&pl, dt, L, d, bound, route);
+    if (st) return st;
+    return make_exec(std::move(pl), out);
+}
+
+qx_status qx_exec_run(qx_exec h, const void* const* inputs, void* output, void* stream) {
+    g_err.clear();
+    return run_exec(h, inputs, output, stream);
+}
+
+qx_status qx_exec_plan(qx_exec h, qx_plan_info* out) {
+    g_err.clear();
+    if (!h || h->magic != kMagic) return fail(QX_ERR_INVALID_ARG, "invalid executor handle");
+    if (!out) return fail(QX_ERR_INVALID_ARG, "out is NULL");
+    *out = h->plan.info;
+    return QX_OK;
+}
+
+qx_status qx_exec_destroy(qx_exec h) {
+    g_err.clear();
+    if (!h) return QX_OK;
+    if (h->magic != kMagic) return fail(QX_ERR_INVALID_ARG, "invalid executor handle");
+    h->magic = 0;
+    qx_status st = QX_OK;
+    if (h->ws) {
+        int cur = -1;
+        (void)hipGetDevice(&cur);
+        if (cur != h->device) (void)hipSetDevice(h->device);
+        hipError_t e = hipDeviceSynchronize();
+        if (e == hipSuccess) e = hipFree(h->ws);
+        if (e != hipSuccess) st = hip_fail(e, "workspace free");
+        if (cur != h->device && cur >= 0) (void)hipSetDevice(cur);
+    }
+    delete h;
+    return st;
+}
+
+void qx_release_cache(void) {
+    std::map<Key, qx_exec> old;
+    {
+        std::lock_guard<std::mutex> lk(g_cache_mu);
+        old.swap(*g_cache);
+    }
+    for (auto& kv : old) qx_exec_destroy(kv.second);
+}
+
+static bool empty_ok(const void* p, int64_t n) { return p != nullptr || n == 0; }
+
+qx_status qgemm_i16i32(const int16_t* A, const int16_t* B, int32_t* C, int64_t M, int64_t N, int64_t K,
+                       int64_t batch, int32_t bound_a, int32_t bound_b, void* stream) {
+    g_err.clear();
+    Plan probe;
+    qx_status st = plan_gemm(&probe, false, M, N, K, batch, bound_a, bound_b, R_AUTO);
+    if (st) return st;
+    if (!empty_ok(A, M * K * batch) || !empty_ok(B, K * N * batch) || !empty_ok(C, M * N * batch))
+        return fail(QX_ERR_INVALID_ARG, "NULL pointer for a non-empty operand");
+    if (probe.launches.empty()) return QX_OK;
+    const void* in[2] = {A, B};
+    Key key{OP_GEMM_I16, 0, M, N, K, batch, bound_a, bound_b, 0, 0, 0, 0, 0, 0, (uintptr_t)stream};
+    return oneshot(key, [&](Plan* pl) { return plan_gemm(pl, false, M, N, K, batch, bound_a, bound_b, R_AUTO); },
+                   in, C, stream);
+}
+
+qx_status qgemm_i32_s24(const int32_t* A, const int32_t* B, int32_t* C, int64_t M, int64_t N, int64_t K,
+                        int64_t batch, void* stream) {
+    g_err.clear();
+    Plan probe;
+    qx_status st = plan_gemm(&probe, true, M, N, K, batch, 0, 0, R_AUTO);
+    if (st) return st;
+    if (!empty_ok(A, M * K * batch) || !empty_ok(B, K * N * batch) || !empty_ok(C, M * N * batch))
+        return fail(QX_ERR_INVALID_ARG, "NULL pointer for a non-empty operand");
+    if (probe.launches.empty()) return QX_OK;
+    const void* in[2] = {A, B};
+    Key key{OP_GEMM_S24, 0, M, N, K, batch, 0, 0, 0, 0, 0, 0, 0, 0, (uintptr_t)stream};
+    return oneshot(key, [&](Plan* pl) { return plan_gemm(pl, true, M, N, K, batch, 0, 0, R_AUTO); }, in, C,
+                   stream);
+}
+
+qx_status conv2d_gemm(const int16_t* x, const int16_t* w, int32_t* y, int64_t N, int64_t C_in, int64_t H, int64_t W,
+                      int64_t C_out, int64_t KH, int64_t KW, int64_t stride, int64_t pad, int32_t bound_x,
+                      int32_t bound_w, void* stream) {
+    g_err.clear();
+    Plan probe;
+    qx_status st = plan_conv(&probe, N, C_in, H, W, C_out, KH, KW, stride, pad, bound_x, bound_w, R_AUTO);
+    if (st) return st;
+    if (probe.launches.empty()) return QX_OK;
+    if (!empty_ok(x, N * C_in * H * W) || !empty_ok(w, C_out * C_in * KH * KW) || !y)
+        return fail(QX_ERR_INVALID_ARG, "NULL pointer for a non-empty operand");
+    const void* in[2] = {x, w};
+    Key key{OP_CONV, 0, N, C_in, H, W, C_out, KH, KW, stride, pad, bound_x, bound_w, 0, (uintptr_t)stream};
+    return oneshot(key,
+                   [&](Plan* pl) {
+                       return plan_conv(pl, N, C_in, H, W, C_out, KH, KW, stride, pad, bound_x, bound_w, R_AUTO);
+                   },
+                   in, y, stream);
+}
+
+qx_status attn_core(qx_attn_dtype dt, const void* Q, const void* K, const void* V, void* O, int64_t L, int64_t d,
+                    int32_t bound, void* stream) {
+    g_err.clear();
+    Plan probe;
+    qx_status st = plan_attn(&probe, dt, L, d, bound, R_AUTO);
+    if (st) return st;
+    if (probe.launches.empty()) return QX_OK;
+    if (!Q || !K || !V || !O) return fail(QX_ERR_INVALID_ARG, "NULL pointer for a non-empty operand");
+    const void* in[3] = {Q, K, V};
+    Key key{dt == QX_DT_F32 ? OP_ATTN_F32 : OP_ATTN_I32, 0, L, d, bound, 0, 0, 0, 0, 0, 0, 0, 0, 0,
+            (uintptr_t)stream};
+    return oneshot(key, [&](Plan* pl) { return plan_attn(pl, dt, L, d, bound, R_AUTO); }, in, O, stream);
+}
+
+}  // extern "C"

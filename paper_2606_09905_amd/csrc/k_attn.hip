@@ -1,0 +1,304 @@
+// k_attn.hip -- the single-head attention core O = (Q K^T) V on matrix cores
+// (Methodology: attention operator of the form O = (Q K^T) V; Table 2,
+// attention rows).  No scale, softmax or mask.
+//
+// Both kernels keep S on chip.  A wave owns 32 queries; per block of 32 keys
+// it forms S^T = K_blk Q^T with one MFMA chain, whose 32x32 accumulator
+// (lane = query, 16 registers = 16 keys) is exactly the A operand layout of
+// the second product O += S V once the V operand is gathered with the same
+// key permutation (the order of a contraction's terms is free).  Keys are
+// split across workgroups; partial results are combined in a fixed order.
+//
+//  * FP32: v_mfma_f32_32x32x2f32 for both products; per-split partials are
+//    reduced in split order, so repeated runs are bit-identical.
+//  * INT32 (|q|,|k|,|v| <= 127 and d*max^2 < 2^23): S^T on
+//    v_mfma_i32_32x32x32_i8; every S is read as three offset int8 limbs,
+//    S = s0 + 2^8 s1 + 2^16 s2 + 32896, where the limbs are the bytes of
+//    S xor 0x8080; O gets three int8 products mod 2^32 plus 32896 * colsum(V).
+//    Integer partials from different splits are added with atomics (exact
+//    and order-independent mod 2^32).
+#include "qx_internal.h"
+
+namespace qx {
+
+typedef float f16x __attribute__((ext_vector_type(16)));
+typedef float f4 __attribute__((ext_vector_type(4)));
+typedef int i16x __attribute__((ext_vector_type(16)));
+typedef int i4 __attribute__((ext_vector_type(4)));
+
+constexpr int AT = 256;      // 4 waves
+constexpr int AQW = 32;      // queries per wave
+constexpr int AQ = 4 * AQW;  // queries per workgroup
+constexpr int AKB = 32;      // keys per block
+
+// ---------------------------------------------------------------------------
+// FP32
+// ---------------------------------------------------------------------------
+template <int D>
+__global__ __launch_bounds__(AT) void k_attn_f32(const AttnParams p) {
+    constexpr int DP = D + 4;            // padded LDS row (floats)
+    constexpr int HALF = D / 2;          // K-slot h of a 32x32x2 MFMA covers d-half h
+    constexpr int NTO = D / 32;          // output column tiles
+    constexpr int LD4 = AKB * D / 4 / AT;  // float4 loads per thread per operand
+    __shared__ float Ks[AKB][DP];
+    __shared__ float Vs[AKB][DP];
+
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, h = lane >> 5, l32 = lane & 31;
+    const int q0 = blockIdx.x * AQ + wave * AQW;
+    const int split = blockIdx.y;
+    const int key_lo = split * p.keys_per_split;
+    const int key_hi = min(p.L, key_lo + p.keys_per_split);
+    const float* Q = (const float*)p.Q;
+    const float* Kp = (const float*)p.K;
+    const float* Vp = (const float*)p.V;
+
+    float qf[HALF];
+    {
+        const int q = q0 + l32;
+#pragma unroll
+        for (int t = 0; t < HALF; t += 4) {
+            f4 v = (q < p.L) ? *(const f4*)(Q + (int64_t)q * D + HALF * h + t) : f4{};
+            qf[t] = v[0]; qf[t + 1] = v[1]; qf[t + 2] = v[2]; qf[t + 3] = v[3];
+        }
+    }
+    f16x o[NTO];
+#pragma unroll
+    for (int n = 0; n < NTO; ++n) o[n] = f16x{};
+
+    f4 rk[LD4], rv[LD4];
+    auto load = [&](int kb) {
+#pragma unroll
+        for (int i = 0; i < LD4; ++i) {
+            const int v = tid + AT * i, row = v / (D / 4), c4 = v % (D / 4);
+            const int key = kb + row;
+            const bool in = key < key_hi;
+            rk[i] = in ? *(const f4*)(Kp + (int64_t)key * D + c4 * 4) : f4{};
+            rv[i] = in ? *(const f4*)(Vp + (int64_t)key * D + c4 * 4) : f4{};
+        }
+    };
+    auto stash = [&]() {
+#pragma unroll
+        for (int i = 0; i < LD4; ++i) {
+            const int v = tid + AT * i, row = v / (D / 4), c4 = v % (D / 4);
+            *(f4*)&Ks[row][c4 * 4] = rk[i];
+            *(f4*)&Vs[row][c4 * 4] = rv[i];
+        }
+    };
+
+    if (key_lo < key_hi) load(key_lo);
+    for (int kb = key_lo; kb < key_hi; kb += AKB) {
+        __syncthreads();              // previous block fully consumed
+        stash();
+        __syncthreads();
+        if (kb + AKB < key_hi) load(kb + AKB);
+        // S^T[key][query] = sum_t K[key][t] Q[query][t]
+        f16x s = f16x{};
+#pragma unroll
+        for (int t = 0; t < HALF; t += 4) {
+            const f4 kv = *(const f4*)&Ks[l32][HALF * h + t];
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+                s = __builtin_amdgcn_mfma_f32_32x32x2f32(kv[e], qf[t + e], s, 0, 0, 0);
+        }
+        // O[query][c] += sum_key S[query][key] V[key][c]; register r of lane
+        // half h holds key 8*(r/4) + 4*h + r%4.
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+            const int key = 8 * (r >> 2) + 4 * h + (r & 3);
+#pragma unroll
+            for (int n = 0; n < NTO; ++n)
+                o[n] = __builtin_amdgcn_mfma_f32_32x32x2f32(s[r], Vs[key][n * 32 + l32], o[n], 0, 0, 0);
+        }
+    }
+
+    float* dst = p.splits > 1 ? (float*)p.part + (int64_t)split * p.L * D : (float*)p.O;
+#pragma unroll
+    for (int n = 0; n < NTO; ++n)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+            const int q = q0 + 8 * (r >> 2) + 4 * h + (r & 3);
+            if (q < p.L) dst[(int64_t)q * D + n * 32 + l32] = o[n][r];
+        }
+}
+
+__global__ __launch_bounds__(AT) void k_reduce_splits(const ReduceParams p) {
+    const int64_t i = (int64_t)blockIdx.x * AT + threadIdx.x;
+    if (i >= p.n) return;
+    float s = p.part[i];
+    for (int k = 1; k < p.splits; ++k) s += p.part[(int64_t)k * p.n + i];
+    p.out[i] = s;
+}
+
+// ---------------------------------------------------------------------------
+// INT32 through int8 matrix cores
+// ---------------------------------------------------------------------------
+// Byte j of four words, packed into one word (a, b, c, d -> bytes 0..3).
+__device__ __forceinline__ uint32_t gather_byte(uint32_t a, uint32_t b, uint32_t c, uint32_t d, int j) {
+    const uint32_t sel = (uint32_t)j | ((uint32_t)(4 + j) << 8) | (0x0C0Cu << 16);
+    const uint32_t lo = __builtin_amdgcn_perm(b, a, sel);   // (a_j, b_j, 0, 0)
+    const uint32_t hi = __builtin_amdgcn_perm(d, c, sel);   // (c_j, d_j, 0, 0)
+    return __builtin_amdgcn_perm(hi, lo, 0x05040100u);      // (a_j, b_j, c_j, d_j)
+}
+
+template <int D>
+__global__ __launch_bounds__(AT) void k_attn_i32(const AttnParams p) {
+    constexpr int NTO = D / 32;
+    constexpr int KCH = D / 16;                 // 16-byte chunks per key row (int8)
+    constexpr int KW = AKB * D / 4 / AT;        // packed K words per thread
+    __shared__ i4 Ks8[AKB][KCH];                // int8 K rows
+    __shared__ uint32_t Vt8[D][AKB / 4 + 1];    // int8 V^T: [column][keys], padded
+
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, h = lane >> 5, l32 = lane & 31;
+    const int q0 = blockIdx.x * AQ + wave * AQW;
+    const int split = blockIdx.y;
+    const int key_lo = split * p.keys_per_split;
+    const int key_hi = min(p.L, key_lo + p.keys_per_split);
+    const int32_t* Q = (const int32_t*)p.Q;
+    const int32_t* Kp = (const int32_t*)p.K;
+    const int32_t* Vp = (const int32_t*)p.V;
+
+    auto pack4 = [](i4 v) -> uint32_t {
+        return ((uint32_t)v[0] & 0xFFu) | (((uint32_t)v[1] & 0xFFu) << 8) |
+               (((uint32_t)v[2] & 0xFFu) << 16) | ((uint32_t)v[3] << 24);
+    };
+    // Q fragment: lane (query, half h), MFMA t: Q[query][32t + 16h + e], e < 16.
+    i4 qf[NTO];
+    {
+        const int q = q0 + l32;
+#pragma unroll
+        for (int t = 0; t < NTO; ++t) {
+#pragma unroll
+            for (int w = 0; w < 4; ++w) {
+                const i4 v = (q < p.L) ? *(const i4*)(Q + (int64_t)q * D + 32 * t + 16 * h + 4 * w) : i4{};
+                qf[t][w] = (int)pack4(v);
+            }
+        }
+    }
+    i16x o[3][NTO];
+#pragma unroll
+    for (int j = 0; j < 3; ++j)
+#pragma unroll
+        for (int n = 0; n < NTO; ++n) o[j][n] = i16x{};
+
+    uint32_t rk[KW], rv[KW];
+    auto load = [&](int kb) {
+#pragma unroll
+        for (int i = 0; i < KW; ++i) {
+            const int v = tid + AT * i;
+            // K: word v covers key v/(D/4), columns 4*(v%(D/4)) .. +3
+            const int krow = v / (D / 4), kc = v % (D / 4);
+            const int key = kb + krow;
+            rk[i] = key < key_hi ? pack4(*(const i4*)(Kp + (int64_t)key * D + kc * 4)) : 0u;
+            // V^T: word v covers column v % D, keys 4*(v / D) .. +3
+            const int col = v % D, kq = v / D;
+            uint32_t w = 0;
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                const int key2 = kb + kq * 4 + e;
+                const uint32_t x = key2 < key_hi ? (uint32_t)Vp[(int64_t)key2 * D + col] : 0u;
+                w |= (x & 0xFFu) << (8 * e);
+            }
+            rv[i] = w;
+        }
+    };
+    auto stash = [&]() {
+#pragma unroll
+        for (int i = 0; i < KW; ++i) {
+            const int v = tid + AT * i;
+            const int krow = v / (D / 4), kc = v % (D / 4);
+            ((uint32_t*)&Ks8[krow][0])[kc] = rk[i];
+            Vt8[v % D][v / D] = rv[i];
+        }
+    };
+
+    if (key_lo < key_hi) load(key_lo);
+    for (int kb = key_lo; kb < key_hi; kb += AKB) {
+        __syncthreads();
+        stash();
+        __syncthreads();
+        if (kb + AKB < key_hi) load(kb + AKB);
+        i16x s = i16x{};
+#pragma unroll
+        for (int t = 0; t < NTO; ++t)
+            s = __builtin_amdgcn_mfma_i32_32x32x32_i8(Ks8[l32][2 * t + h], qf[t], s, 0, 0, 0);
+        // Offset limbs: bytes 0..2 of S ^ 0x8080.  K-slot (h, e) of the
+        // second product is key 8*(e/4) + 4*h + e%4, as the S^T layout gives.
+        uint32_t x[16];
+#pragma unroll
+        for (int r = 0; r < 16; ++r) x[r] = (uint32_t)s[r] ^ 0x8080u;
+        i4 limb[3];
+#pragma unroll
+        for (int j = 0; j < 3; ++j)
+#pragma unroll
+            for (int w = 0; w < 4; ++w)
+                limb[j][w] = (int)gather_byte(x[4 * w], x[4 * w + 1], x[4 * w + 2], x[4 * w + 3], j);
+#pragma unroll
+        for (int n = 0; n < NTO; ++n) {
+            i4 vb;
+#pragma unroll
+            for (int w = 0; w < 4; ++w) vb[w] = (int)Vt8[n * 32 + l32][2 * w + h];
+#pragma unroll
+            for (int j = 0; j < 3; ++j)
+                o[j][n] = __builtin_amdgcn_mfma_i32_32x32x32_i8(limb[j], vb, o[j][n], 0, 0, 0);
+        }
+    }
+
+    int32_t* O = (int32_t*)p.O;
+#pragma unroll
+    for (int n = 0; n < NTO; ++n) {
+        const int c = n * 32 + l32;
+        const uint32_t corr = split == 0 ? 32896u * (uint32_t)p.vcs[c] : 0u;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+            const int q = q0 + 8 * (r >> 2) + 4 * h + (r & 3);
+            if (q >= p.L) continue;
+            const uint32_t v = (uint32_t)o[0][n][r] + ((uint32_t)o[1][n][r] << 8) +
+                               ((uint32_t)o[2][n][r] << 16) + corr;
+            if (p.splits > 1) atomicAdd(O + (int64_t)q * D + c, (int)v);
+            else O[(int64_t)q * D + c] = (int32_t)v;
+        }
+    }
+}
+
+// ---------------------------------------------------------------------------
+// Builders
+// ---------------------------------------------------------------------------
+bool build_attn_f32(const AttnParams& p, LaunchRec* rec) {
+    switch (p.d) {
+    case 32: rec->fn = (const void*)k_attn_f32<32>; break;
+    case 64: rec->fn = (const void*)k_attn_f32<64>; break;
+    case 96: rec->fn = (const void*)k_attn_f32<96>; break;
+    case 128: rec->fn = (const void*)k_attn_f32<128>; break;
+    default: return false;
+    }
+    rec->name = "attn_f32";
+    rec->grid = dim3((unsigned)((p.L + AQ - 1) / AQ), (unsigned)p.splits, 1);
+    rec->block = dim3(AT, 1, 1);
+    rec->set_params(p);
+    return true;
+}
+
+bool build_attn_i32(const AttnParams& p, LaunchRec* rec) {
+    switch (p.d) {
+    case 32: rec->fn = (const void*)k_attn_i32<32>; break;
+    case 64: rec->fn = (const void*)k_attn_i32<64>; break;
+    case 96: rec->fn = (const void*)k_attn_i32<96>; break;
+    case 128: rec->fn = (const void*)k_attn_i32<128>; break;
+    default: return false;
+    }
+    rec->name = "attn_i32";
+    rec->grid = dim3((unsigned)((p.L + AQ - 1) / AQ), (unsigned)p.splits, 1);
+    rec->block = dim3(AT, 1, 1);
+    rec->set_params(p);
+    return true;
+}
+
+void build_reduce(const ReduceParams& p, LaunchRec* rec) {
+    rec->fn = (const void*)k_reduce_splits;
+    rec->grid = dim3((unsigned)((p.n + AT - 1) / AT), 1, 1);
+    rec->block = dim3(AT, 1, 1);
+    rec->name = "reduce_splits";
+    rec->set_params(p);
+}
+
+}  // namespace qx

@@ -1,0 +1,599 @@
+// k_gemm.hip -- the tiled integer GEMM substrate on gfx950 matrix cores.
+//
+// Two exact routes share one tile skeleton (global -> registers -> encode ->
+// LDS, double-buffered; LDS -> registers -> MFMA; int32 epilogue):
+//
+//  * F16_EXACT: int16 operands with |a|,|b| <= 2048 are exact in fp16 and
+//    their products exact in fp32.  v_mfma_f32_32x32x16_f16 accumulates in
+//    fp32 for `chunk` K elements with chunk*max|a|*max|b| <= 2^24, so every
+//    partial sum is an integer fp32 represents exactly whatever the internal
+//    summation order; the partials are then converted and added into int32
+//    (mod 2^32) accumulators.
+//  * I8 limbs: operands are split into int8 limb planes while being staged,
+//    each limb product runs on v_mfma_i32_32x32x32_i8 (int32 accumulation),
+//    and the epilogue recombines the planes mod 2^32 (direct, Karatsuba
+//    base 128, offset base 256 with a rank-1 correction, and the smul24
+//    three-limb split with eight products).
+//
+// These realise the packed INT16-input / INT32-accumulation GEMM and the
+// smul24 INT32 GEMM of the paper (Methodology; Table 1), with the operand
+// range contract deciding the route (Methodology: contracts determine
+// feasible tiling, packing and accumulation).
+#include <algorithm>
+
+#include "qx_internal.h"
+
+namespace qx {
+
+typedef _Float16 h8 __attribute__((ext_vector_type(8)));
+typedef _Float16 h4 __attribute__((ext_vector_type(4)));
+typedef float f16x __attribute__((ext_vector_type(16)));
+typedef int i16x __attribute__((ext_vector_type(16)));
+typedef unsigned u16x __attribute__((ext_vector_type(16)));
+typedef int i4 __attribute__((ext_vector_type(4)));
+typedef short s8 __attribute__((ext_vector_type(8)));
+typedef short s4 __attribute__((ext_vector_type(4)));
+
+constexpr int NT = 256;  // threads per workgroup (4 waves)
+
+// Workgroup -> output tile.  Tiles are walked in groups of 8 tile-rows so
+// that consecutive workgroups share B panels.
+__device__ __forceinline__ void tile_coords(int tiles_m, int tiles_n, int& tm, int& tn) {
+    const int pid = blockIdx.x;
+    constexpr int G = 8;
+    const int per_group = G * tiles_n;
+    const int gid = pid / per_group;
+    const int first_m = gid * G;
+    const int gsz = min(tiles_m - first_m, G);
+    const int in = pid - gid * per_group;
+    tm = first_m + in % gsz;
+    tn = in / gsz;
+}
+
+// Store one int32 result with the epilogue's layout.
+__device__ __forceinline__ void store_c(const GemmParams& p, int32_t* C, int gm, int gn, uint32_t v) {
+    if (gm >= p.M || gn >= p.N) return;
+    if (p.out_mode == OUT_ROWMAJOR) {
+        C[(int64_t)gm * p.ldc + gn] = (int32_t)v;
+    } else {
+        const int img = gn / p.hw, pix = gn - img * p.hw;
+        C[((int64_t)img * p.M + gm) * p.hw + pix] = (int32_t)v;
+    }
+}
+
+// ===========================================================================
+// F16_EXACT
+// ===========================================================================
+// LDS rows hold BK fp16 as 16-byte chunks; chunk index is XOR-swizzled with
+// the row so that the eight consecutive rows read by one ds_read_b128 pass
+// land in distinct banks.
+__device__ __forceinline__ int swz_a(int row, int c) { return c ^ (row & 7); }
+__device__ __forceinline__ int swz_b(int col, int c) { return c ^ ((col ^ (col >> 3)) & 7); }
+
+template <int BM, int BN, int BK, int WM, int WN, bool ALIGNED, bool FLUSH_STEP>
+__global__ __launch_bounds__(NT) void k_gemm_f16x(const GemmParams p) {
+    static_assert(BK == 64, "chunk swizzle assumes 8 chunks per row");
+    constexpr int KCH = BK / 8;
+    constexpr int TM = WM / 32, TN = WN / 32;
+    constexpr int WAVES_N = BN / WN;
+    static_assert((BM / WM) * (BN / WN) == 4, "four waves");
+    constexpr int A_VECS = BM * KCH / NT;         // 16-byte A vectors per thread
+    constexpr int B_NBLK = BN / 8;                // B staged as 4(k) x 8(n) blocks
+    static_assert((BK / 4) * B_NBLK == NT, "one B block per thread");
+
+    __shared__ h8 As[2][BM][KCH];
+    __shared__ h8 Bs[2][BN][KCH];
+
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int wm = wave / WAVES_N, wn = wave % WAVES_N;
+    const int tiles_m = (p.M + BM - 1) / BM;
+    int tm, tn;
+    tile_coords(tiles_m, p.tiles_n, tm, tn);
+    const int m0 = tm * BM, n0 = tn * BN;
+    const int b = blockIdx.z;
+    const int16_t* A = (const int16_t*)p.A + b * p.sA;
+    const int16_t* B = (const int16_t*)p.B + b * p.sB;
+    int32_t* C = (int32_t*)p.C + b * p.sC;
+
+    s8 ra[A_VECS];
+    s8 rb[4];
+    const int bkb = tid / B_NBLK, bnb = tid % B_NBLK;
+
+    auto load = [&](int k0) {
+#pragma unroll
+        for (int i = 0; i < A_VECS; ++i) {
+            const int v = tid + NT * i, row = v / KCH, c = v % KCH;
+            const int gm = m0 + row, gk = k0 + c * 8;
+            if (ALIGNED) {
+                ra[i] = (gm < p.M && gk < p.K) ? *(const s8*)(A + (int64_t)gm * p.lda + gk) : s8{};
+            } else {
+#pragma unroll
+                for (int e = 0; e < 8; ++e)
+                    ra[i][e] = (gm < p.M && gk + e < p.K) ? A[(int64_t)gm * p.lda + gk + e] : (short)0;
+            }
+        }
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            const int gk = k0 + bkb * 4 + r, gn = n0 + bnb * 8;
+            if (ALIGNED) {
+                rb[r] = (gk < p.K && gn < p.N) ? *(const s8*)(B + (int64_t)gk * p.ldb + gn) : s8{};
+            } else {
+#pragma unroll
+                for (int e = 0; e < 8; ++e)
+                    rb[r][e] = (gk < p.K && gn + e < p.N) ? B[(int64_t)gk * p.ldb + gn + e] : (short)0;
+            }
+        }
+    };
+    auto stash = [&](int buf) {
+#pragma unroll
+        for (int i = 0; i < A_VECS; ++i) {
+            const int v = tid + NT * i, row = v / KCH, c = v % KCH;
+            h8 h;
+#pragma unroll
+            for (int e = 0; e < 8; ++e) h[e] = (_Float16)ra[i][e];
+            As[buf][row][swz_a(row, c)] = h;
+        }
+#pragma unroll
+        for (int c = 0; c < 8; ++c) {
+            const int col = bnb * 8 + c;
+            h4 h;
+#pragma unroll
+            for (int r = 0; r < 4; ++r) h[r] = (_Float16)rb[r][c];
+            h4* dst = (h4*)&Bs[buf][col][swz_b(col, bkb >> 1)];
+            dst[bkb & 1] = h;
+        }
+    };
+
+    f16x acc[TM][TN];
+    u16x iacc[TM][TN];
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j) {
+            acc[i][j] = f16x{};
+            iacc[i][j] = u16x{};
+        }
+    auto flush = [&]() {
+#pragma unroll
+        for (int i = 0; i < TM; ++i)
+#pragma unroll
+            for (int j = 0; j < TN; ++j) {
+#pragma unroll
+                for (int r = 0; r < 16; ++r) iacc[i][j][r] += (uint32_t)(int32_t)acc[i][j][r];
+                acc[i][j] = f16x{};
+            }
+    };
+
+    const int ktiles = (p.K + BK - 1) / BK;
+    load(0);
+    stash(0);
+    __syncthreads();
+    int since_flush = 0;
+    for (int t = 0; t < ktiles; ++t) {
+        const int buf = t & 1;
+        if (t + 1 < ktiles) load((t + 1) * BK);
+#pragma unroll
+        for (int ks = 0; ks < BK / 16; ++ks) {
+            h8 a[TM], bv[TN];
+            const int c = ks * 2 + (lane >> 5);
+#pragma unroll
+            for (int i = 0; i < TM; ++i) {
+                const int row = wm * WM + i * 32 + (lane & 31);
+                a[i] = As[buf][row][swz_a(row, c)];
+            }
+#pragma unroll
+            for (int j = 0; j < TN; ++j) {
+                const int col = wn * WN + j * 32 + (lane & 31);
+                bv[j] = Bs[buf][col][swz_b(col, c)];
+            }
+#pragma unroll
+            for (int i = 0; i < TM; ++i)
+#pragma unroll
+                for (int j = 0; j < TN; ++j)
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_f16(a[i], bv[j], acc[i][j], 0, 0, 0);
+            if (FLUSH_STEP) flush();
+        }
+        if (!FLUSH_STEP && ++since_flush == p.chunk_tiles) {
+            flush();
+            since_flush = 0;
+        }
+        if (t + 1 < ktiles) stash(buf ^ 1);
+        __syncthreads();
+    }
+    if (!FLUSH_STEP) flush();
+
+    // 32x32 accumulator layout: lane holds column (lane & 31) and rows
+    // 8*(r/4) + 4*(lane/32) + r%4.
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+                const int gm = m0 + wm * WM + i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+                const int gn = n0 + wn * WN + j * 32 + (lane & 31);
+                store_c(p, C, gm, gn, iacc[i][j][r]);
+            }
+}
+
+// ===========================================================================
+// int8 limb routes
+// ===========================================================================
+// A scheme splits each operand into PLANES int8 limbs, issues PRODUCTS limb
+// products into GROUPS accumulators, and recombines them mod 2^32.
+struct SchemeDirect {   // |x| <= 127
+    static constexpr int PLANES = 1, GROUPS = 1, PRODUCTS = 1;
+    static constexpr int pa[1] = {0}, pb[1] = {0}, pg[1] = {0};
+    template <class T> __device__ static void split(T x, uint32_t* l) { l[0] = (uint32_t)x & 0xFFu; }
+    __device__ static uint32_t combine(const uint32_t* g) { return g[0]; }
+};
+struct SchemeKaratsuba {  // x in [-8256, 8127]: balanced base 128, h, l, h+l
+    static constexpr int PLANES = 3, GROUPS = 3, PRODUCTS = 3;
+    static constexpr int pa[3] = {0, 1, 2}, pb[3] = {0, 1, 2}, pg[3] = {0, 1, 2};
+    template <class T> __device__ static void split(T xv, uint32_t* l) {
+        const int x = (int)xv;
+        const int lo = ((x + 64) & 127) - 64;
+        const int hi = (x - lo) >> 7;
+        l[0] = (uint32_t)hi & 0xFFu;
+        l[1] = (uint32_t)lo & 0xFFu;
+        l[2] = (uint32_t)(hi + lo) & 0xFFu;
+    }
+    // a*b = 2^14 hh + 2^7 (mm - hh - ll) + ll
+    __device__ static uint32_t combine(const uint32_t* g) {
+        return (g[0] << 14) + ((g[2] - g[0] - g[1]) << 7) + g[1];
+    }
+};
+struct SchemeOffset4 {  // any int16: x = 256*s1 + s0 + 128, s1 = x>>8, s0 = (x & 255) - 128
+    static constexpr int PLANES = 2, GROUPS = 3, PRODUCTS = 4;
+    static constexpr int pa[4] = {0, 0, 1, 1}, pb[4] = {0, 1, 0, 1}, pg[4] = {0, 1, 1, 2};
+    template <class T> __device__ static void split(T xv, uint32_t* l) {
+        const uint32_t x = (uint32_t)(int)xv;
+        l[0] = (x >> 8) & 0xFFu;          // s1 (arithmetic high byte of an int16)
+        l[1] = (x & 0xFFu) ^ 0x80u;       // s0 = low byte - 128
+    }
+    __device__ static uint32_t combine(const uint32_t* g) { return (g[0] << 16) + (g[1] << 8) + g[2]; }
+};
+struct SchemeS24 {  // smul24: u = sext24(x) + 2^23, s_i = byte_i(u) - 128, x = sum 2^(8i) s_i + 32896
+    static constexpr int PLANES = 3, GROUPS = 4, PRODUCTS = 8;
+    static constexpr int pa[8] = {0, 0, 1, 0, 1, 2, 1, 2};
+    static constexpr int pb[8] = {0, 1, 0, 2, 1, 0, 2, 1};
+    static constexpr int pg[8] = {0, 1, 1, 2, 2, 2, 3, 3};
+    template <class T> __device__ static void split(T xv, uint32_t* l) {
+        const uint32_t u = ((uint32_t)(int)xv & 0xFFFFFFu) ^ 0x808080u ^ 0x800000u;
+        l[0] = u & 0xFFu;
+        l[1] = (u >> 8) & 0xFFu;
+        l[2] = (u >> 16) & 0xFFu;
+    }
+    __device__ static uint32_t combine(const uint32_t* g) {
+        return g[0] + (g[1] << 8) + (g[2] << 16) + (g[3] << 24);
+    }
+};
+
+// Aligned vector load of N elements (whole 16-byte transactions).
+template <class T, int N>
+struct alignas(N * sizeof(T) >= 16 ? 16 : N * sizeof(T)) VecN {
+    T v[N];
+};
+template <class T, int N>
+__device__ __forceinline__ void load_vec(const T* src, T (&dst)[N]) {
+    const VecN<T, N> x = *(const VecN<T, N>*)src;
+#pragma unroll
+    for (int e = 0; e < N; ++e) dst[e] = x.v[e];
+}
+
+// 64-byte LDS rows (BK = 64 int8) as four 16-byte chunks; the swizzle keeps
+// the eight rows of one ds_read_b128 pass in distinct banks.
+__device__ __forceinline__ int swz8(int row, int c) { return c ^ ((row >> 1) & 3); }
+
+template <class S, class T, int BM, int BN, int WM, int WN, bool ALIGNED>
+__global__ __launch_bounds__(NT) void k_gemm_i8limb(const GemmParams p) {
+    constexpr int BK = 64, KCH = 4;
+    constexpr int P = S::PLANES, G = S::GROUPS;
+    constexpr int TM = WM / 32, TN = WN / 32;
+    constexpr int WAVES_N = BN / WN;
+    static_assert((BM / WM) * (BN / WN) == 4, "four waves");
+    constexpr int A_VECS = BM * BK / 8 / NT;      // 8-element A vectors per thread
+    constexpr int BWN = BN / 16;                  // B staged as 4(k) x BWN(n) blocks
+    static_assert((BK / 4) * (BN / BWN) == NT, "one B block per thread");
+
+    __shared__ i4 As[2][P][BM][KCH];
+    __shared__ i4 Bs[2][P][BN][KCH];
+
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int wm = wave / WAVES_N, wn = wave % WAVES_N;
+    const int tiles_m = (p.M + BM - 1) / BM;
+    int tm, tn;
+    tile_coords(tiles_m, p.tiles_n, tm, tn);
+    const int m0 = tm * BM, n0 = tn * BN;
+    const int b = blockIdx.z;
+    const T* A = (const T*)p.A + b * p.sA;
+    const T* B = (const T*)p.B + b * p.sB;
+    int32_t* C = (int32_t*)p.C + b * p.sC;
+
+    T ra[A_VECS][8];
+    T rb[4][BWN];
+    const int bkb = tid / (BN / BWN), bnb = tid % (BN / BWN);
+
+    auto load = [&](int k0) {
+#pragma unroll
+        for (int i = 0; i < A_VECS; ++i) {
+            const int v = tid + NT * i, row = v / 8, e8 = v % 8;
+            const int gm = m0 + row, gk = k0 + e8 * 8;
+            const T* src = A + (int64_t)gm * p.lda + gk;
+            if (ALIGNED && gm < p.M && gk < p.K) {
+                load_vec<T, 8>(src, ra[i]);
+            } else {
+#pragma unroll
+                for (int e = 0; e < 8; ++e) ra[i][e] = (gm < p.M && gk + e < p.K) ? src[e] : (T)0;
+            }
+        }
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            const int gk = k0 + bkb * 4 + r, gn = n0 + bnb * BWN;
+            const T* src = B + (int64_t)gk * p.ldb + gn;
+            if (ALIGNED && gk < p.K && gn < p.N) {
+                load_vec<T, BWN>(src, rb[r]);
+            } else {
+#pragma unroll
+                for (int e = 0; e < BWN; ++e) rb[r][e] = (gk < p.K && gn + e < p.N) ? src[e] : (T)0;
+            }
+        }
+    };
+    auto stash = [&](int buf) {
+#pragma unroll
+        for (int i = 0; i < A_VECS; ++i) {
+            const int v = tid + NT * i, row = v / 8, e8 = v % 8;
+            uint32_t w[P][2] = {};
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+                uint32_t l[P];
+                S::split(ra[i][e], l);
+#pragma unroll
+                for (int q = 0; q < P; ++q) w[q][e >> 2] |= l[q] << (8 * (e & 3));
+            }
+#pragma unroll
+            for (int q = 0; q < P; ++q) {
+                uint32_t* dst = (uint32_t*)&As[buf][q][row][swz8(row, e8 >> 1)];
+                dst[(e8 & 1) * 2 + 0] = w[q][0];
+                dst[(e8 & 1) * 2 + 1] = w[q][1];
+            }
+        }
+#pragma unroll
+        for (int c = 0; c < BWN; ++c) {
+            const int col = bnb * BWN + c;
+            uint32_t w[P] = {};
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                uint32_t l[P];
+                S::split(rb[r][c], l);
+#pragma unroll
+                for (int q = 0; q < P; ++q) w[q] |= l[q] << (8 * r);
+            }
+#pragma unroll
+            for (int q = 0; q < P; ++q) {
+                uint32_t* dst = (uint32_t*)&Bs[buf][q][col][swz8(col, bkb >> 2)];
+                dst[bkb & 3] = w[q];
+            }
+        }
+    };
+
+    i16x acc[G][TM][TN];
+#pragma unroll
+    for (int g = 0; g < G; ++g)
+#pragma unroll
+        for (int i = 0; i < TM; ++i)
+#pragma unroll
+            for (int j = 0; j < TN; ++j) acc[g][i][j] = i16x{};
+
+    const int ktiles = (p.K + BK - 1) / BK;
+    load(0);
+    stash(0);
+    __syncthreads();
+    for (int t = 0; t < ktiles; ++t) {
+        const int buf = t & 1;
+        if (t + 1 < ktiles) load((t + 1) * BK);
+#pragma unroll
+        for (int ks = 0; ks < BK / 32; ++ks) {
+            const int c = ks * 2 + (lane >> 5);
+            i4 a[P][TM], bv[P][TN];
+#pragma unroll
+            for (int q = 0; q < P; ++q) {
+#pragma unroll
+                for (int i = 0; i < TM; ++i) {
+                    const int row = wm * WM + i * 32 + (lane & 31);
+                    a[q][i] = As[buf][q][row][swz8(row, c)];
+                }
+#pragma unroll
+                for (int j = 0; j < TN; ++j) {
+                    const int col = wn * WN + j * 32 + (lane & 31);
+                    bv[q][j] = Bs[buf][q][col][swz8(col, c)];
+                }
+            }
+#pragma unroll
+            for (int pr = 0; pr < S::PRODUCTS; ++pr)
+#pragma unroll
+                for (int i = 0; i < TM; ++i)
+#pragma unroll
+                    for (int j = 0; j < TN; ++j)
+                        acc[S::pg[pr]][i][j] = __builtin_amdgcn_mfma_i32_32x32x32_i8(
+                            a[S::pa[pr]][i], bv[S::pb[pr]][j], acc[S::pg[pr]][i][j], 0, 0, 0);
+        }
+        if (t + 1 < ktiles) stash(buf ^ 1);
+        __syncthreads();
+    }
+
+    const uint32_t cc = (uint32_t)p.corr_c;
+    const uint32_t kcc = (uint32_t)p.K * cc * cc;
+    const int32_t* rs = p.rowsum ? p.rowsum + (int64_t)b * p.M : nullptr;
+    const int32_t* cs = p.colsum ? p.colsum + (int64_t)b * p.N : nullptr;
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+                const int gm = m0 + wm * WM + i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+                const int gn = n0 + wn * WN + j * 32 + (lane & 31);
+                if (gm >= p.M || gn >= p.N) continue;
+                uint32_t g[G];
+#pragma unroll
+                for (int q = 0; q < G; ++q) g[q] = (uint32_t)acc[q][i][j][r];
+                uint32_t v = S::combine(g);
+                if (cc) v += cc * ((uint32_t)rs[gm] + (uint32_t)cs[gn]) - kcc;
+                store_c(p, C, gm, gn, v);
+            }
+}
+
+// ===========================================================================
+// Row / column sums for the rank-1 correction of offset limb routes.
+// ===========================================================================
+__global__ __launch_bounds__(NT) void k_sums(const SumsParams p) {
+    // blockIdx.y == 0: row sums of A (one wave per row); == 1: column sums of B.
+    const int b = blockIdx.z;
+    if (blockIdx.y == 0) {
+        const int row = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
+        if (row >= p.M) return;
+        uint32_t s = 0;
+        if (p.s24) {
+            const int32_t* a = (const int32_t*)p.A + b * p.sA + (int64_t)row * p.lda;
+            for (int k = lane; k < p.K; k += 64) s += (uint32_t)((int32_t)((uint32_t)a[k] << 8) >> 8);
+        } else {
+            const int16_t* a = (const int16_t*)p.A + b * p.sA + (int64_t)row * p.lda;
+            for (int k = lane; k < p.K; k += 64) s += (uint32_t)(int32_t)a[k];
+        }
+        for (int off = 32; off > 0; off >>= 1) s += __shfl_xor(s, off, 64);
+        if (lane == 0) p.rowsum[(int64_t)b * p.M + row] = (int32_t)s;
+    } else {
+        const int col = blockIdx.x * NT + threadIdx.x;
+        if (col >= p.N) return;
+        uint32_t s = 0;
+        if (p.s24) {
+            const int32_t* bb = (const int32_t*)p.B + b * p.sB + col;
+            for (int k = 0; k < p.K; ++k) s += (uint32_t)((int32_t)((uint32_t)bb[(int64_t)k * p.ldb] << 8) >> 8);
+        } else {
+            const int16_t* bb = (const int16_t*)p.B + b * p.sB + col;
+            for (int k = 0; k < p.K; ++k) s += (uint32_t)(int32_t)bb[(int64_t)k * p.ldb];
+        }
+        p.colsum[(int64_t)b * p.N + col] = (int32_t)s;
+    }
+}
+
+// ===========================================================================
+// Explicit im2col (Methodology: convolution through lowering).
+// ===========================================================================
+__global__ __launch_bounds__(NT) void k_im2col(const Im2colParams p) {
+    const int64_t pix = (int64_t)blockIdx.x * NT + threadIdx.x;
+    const int k = blockIdx.y;
+    if (pix >= p.P) return;
+    const ConvGeom& g = p.g;
+    const int kw = k % g.KW, kh = (k / g.KW) % g.KH, ci = k / (g.KW * g.KH);
+    const int hw = g.Ho * g.Wo;
+    const int n = (int)(pix / hw), rem = (int)(pix - (int64_t)n * hw);
+    const int oh = rem / g.Wo, ow = rem - oh * g.Wo;
+    const int ih = oh * g.stride - g.pad + kh, iw = ow * g.stride - g.pad + kw;
+    int16_t v = 0;
+    if (ih >= 0 && ih < g.H && iw >= 0 && iw < g.W)
+        v = p.x[(((int64_t)n * g.Ci + ci) * g.H + ih) * g.W + iw];
+    p.col[(int64_t)k * p.P + pix] = v;
+}
+
+__global__ __launch_bounds__(NT) void k_fill(const FillParams p) {
+    const int64_t i = (int64_t)blockIdx.x * NT + threadIdx.x;
+    if (i < p.n32) ((int32_t*)p.ptr)[i] = p.value;
+}
+
+// ===========================================================================
+// Builders
+// ===========================================================================
+template <class K>
+static void fill_gemm_rec(LaunchRec* rec, K* fn, const GemmParams& p0, int BM, int BN, int batch,
+                          const char* name) {
+    GemmParams p = p0;
+    const int tiles_m = (p.M + BM - 1) / BM;
+    p.tiles_n = (p.N + BN - 1) / BN;
+    rec->fn = (const void*)fn;
+    rec->grid = dim3((unsigned)(tiles_m * p.tiles_n), 1, (unsigned)batch);
+    rec->block = dim3(NT, 1, 1);
+    rec->shmem = 0;
+    rec->name = name;
+    rec->set_params(p);
+}
+
+// Vector loads need 16-byte aligned rows and batch strides, and whole
+// vectors inside K (A vectors of 8) and N (B vectors of bvec); pointers are
+// bound per run and the executor checks their alignment there.
+static bool aligned_for(const GemmParams& p, int elem, int bvec) {
+    const int v = 16 / elem;
+    return p.lda % v == 0 && p.ldb % v == 0 && p.sA % v == 0 && p.sB % v == 0 &&
+           p.K % 8 == 0 && p.N % bvec == 0 && p.b_mode == B_KN;
+}
+
+bool build_gemm_mfma(int32_t route, const GemmParams& p, int batch, LaunchRec* rec,
+                     int* tile_m, int* tile_n, int* tile_k) {
+    *tile_k = 64;
+    switch (route) {
+    case R_F16_EXACT: {
+        *tile_m = 128;
+        *tile_n = 128;
+        const bool al = aligned_for(p, 2, 8);
+        const bool step = p.chunk_tiles == 0;  // chunk of 16: flush after every MFMA step
+        if (al && !step) fill_gemm_rec(rec, k_gemm_f16x<128, 128, 64, 64, 64, true, false>, p, 128, 128, batch, "gemm_f16x");
+        else if (al) fill_gemm_rec(rec, k_gemm_f16x<128, 128, 64, 64, 64, true, true>, p, 128, 128, batch, "gemm_f16x_step");
+        else if (!step) fill_gemm_rec(rec, k_gemm_f16x<128, 128, 64, 64, 64, false, false>, p, 128, 128, batch, "gemm_f16x_u");
+        else fill_gemm_rec(rec, k_gemm_f16x<128, 128, 64, 64, 64, false, true>, p, 128, 128, batch, "gemm_f16x_step_u");
+        return true;
+    }
+    case R_I8_DIRECT:
+    case R_I8_KARATSUBA:
+    case R_I8_OFFSET4: {
+        *tile_m = 128;
+        *tile_n = 128;
+        const bool al = aligned_for(p, 2, 8);
+#define QX_I8(S, NAME)                                                                                       \
+    if (al) fill_gemm_rec(rec, k_gemm_i8limb<S, int16_t, 128, 128, 64, 64, true>, p, 128, 128, batch, NAME);  \
+    else fill_gemm_rec(rec, k_gemm_i8limb<S, int16_t, 128, 128, 64, 64, false>, p, 128, 128, batch, NAME "_u");
+        if (route == R_I8_DIRECT) { QX_I8(SchemeDirect, "gemm_i8_direct") }
+        else if (route == R_I8_KARATSUBA) { QX_I8(SchemeKaratsuba, "gemm_i8_karatsuba") }
+        else { QX_I8(SchemeOffset4, "gemm_i8_offset4") }
+#undef QX_I8
+        return true;
+    }
+    case R_S24_I8LIMB: {
+        *tile_m = 128;
+        *tile_n = 64;
+        const bool al = aligned_for(p, 4, 4);
+        if (al) fill_gemm_rec(rec, k_gemm_i8limb<SchemeS24, int32_t, 128, 64, 64, 32, true>, p, 128, 64, batch, "gemm_s24_i8limb");
+        else fill_gemm_rec(rec, k_gemm_i8limb<SchemeS24, int32_t, 128, 64, 64, 32, false>, p, 128, 64, batch, "gemm_s24_i8limb_u");
+        return true;
+    }
+    default:
+        return false;
+    }
+}
+
+void build_sums(const SumsParams& p, LaunchRec* rec) {
+    const int gx = std::max((p.M + 3) / 4, (p.N + NT - 1) / NT);
+    rec->fn = (const void*)k_sums;
+    rec->grid = dim3((unsigned)std::max(gx, 1), 2, (unsigned)p.batch);
+    rec->block = dim3(NT, 1, 1);
+    rec->name = "rowcol_sums";
+    rec->set_params(p);
+}
+
+void build_im2col(const Im2colParams& p, LaunchRec* rec) {
+    rec->fn = (const void*)k_im2col;
+    rec->grid = dim3((unsigned)((p.P + NT - 1) / NT), (unsigned)p.Kd, 1);
+    rec->block = dim3(NT, 1, 1);
+    rec->name = "im2col";
+    rec->set_params(p);
+}
+
+void build_fill(const FillParams& p, LaunchRec* rec) {
+    rec->fn = (const void*)k_fill;
+    rec->grid = dim3((unsigned)(p.n32 > 0 ? (p.n32 + NT - 1) / NT : 1), 1, 1);
+    rec->block = dim3(NT, 1, 1);
+    rec->name = "fill";
+    rec->set_params(p);
+}
+
+}  // namespace qx

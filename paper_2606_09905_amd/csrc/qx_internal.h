@@ -1,0 +1,179 @@
+// qx_internal.h -- definitions shared by the HIP kernels and the host side of
+// the library (planner, executor, C ABI).  Not installed; the public
+// interface is include/qx.h.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+#include <string.h>
+
+namespace qx {
+
+// ---------------------------------------------------------------------------
+// Kernel parameter blocks.  Every kernel takes exactly one of these by value,
+// so a launch is fully described by (function, grid, block, parameter bytes)
+// and the executor can cache it and patch the pointer fields per run.
+// ---------------------------------------------------------------------------
+
+// Epilogue store modes of the GEMM kernels.
+enum OutMode : int32_t {
+    OUT_ROWMAJOR = 0,  // C[m][n] at C + m*ldc + n
+    OUT_CONV = 1,      // C[m][n] -> y[(n / hw) * M * hw + m * hw + n % hw]  (NCHW scatter)
+};
+
+// B operand layouts.
+enum BMode : int32_t {
+    B_KN = 0,          // B[k][n] at B + k*ldb + n   (row-major K x N)
+    B_IM2COL = 1,      // B[k][n] gathered from an NCHW image (implicit lowering)
+};
+
+struct ConvGeom {      // geometry for B_IM2COL / OUT_CONV
+    int32_t Ci, H, W, KH, KW, stride, pad, Ho, Wo;
+};
+
+// Integer GEMM  C[b] = A[b] . B[b]  for every route.
+struct GemmParams {
+    const void* A;          // [M][lda] int16 or int32 (route dependent)
+    const void* B;          // see BMode
+    void* C;                // int32 output, see OutMode
+    const int32_t* rowsum;  // limb routes with an offset: per (batch,row) sums of A
+    const int32_t* colsum;  // per (batch,col) sums of B
+    int64_t sA, sB, sC;     // batch strides (elements)
+    int32_t M, N, K;
+    int32_t lda, ldb, ldc;
+    int32_t chunk_tiles;    // F16_EXACT: flush fp32 partials every chunk_tiles K-tiles
+    int32_t corr_c;         // offset constant c of the limb split (0: none)
+    int32_t out_mode;       // OutMode
+    int32_t b_mode;         // BMode
+    int32_t hw;             // OUT_CONV: Ho*Wo
+    int32_t tiles_n;        // number of N tiles (grid swizzle)
+    ConvGeom g;
+};
+
+// Per-row / per-column sums used by the rank-1 correction of offset limb routes.
+struct SumsParams {
+    const void* A;
+    const void* B;
+    int32_t* rowsum;        // [batch][M]
+    int32_t* colsum;        // [batch][N]
+    int64_t sA, sB;
+    int32_t M, N, K, lda, ldb;
+    int32_t s24;            // 1: operands are int32 read through sext24; 0: int16
+    int32_t batch;
+};
+
+// Explicit im2col: col[k][p] (int16), k = (ci*KH + kh)*KW + kw, p = (n*Ho + oh)*Wo + ow.
+struct Im2colParams {
+    const int16_t* x;
+    int16_t* col;
+    int64_t P;              // N*Ho*Wo
+    int32_t Kd;             // Ci*KH*KW
+    ConvGeom g;
+};
+
+// Attention core O = (Q K^T) V.
+struct AttnParams {
+    const void* Q;
+    const void* K;
+    const void* V;
+    void* O;
+    void* part;             // F32: split partials [splits][L][d] float
+    const int32_t* vcs;     // I32: column sums of V over all keys
+    int32_t L, d;
+    int32_t splits;         // key splits
+    int32_t keys_per_split;
+    int32_t limbs;          // I32: int8 limbs of S
+};
+
+struct ReduceParams {
+    const float* part;      // [splits][n]
+    float* out;             // [n]
+    int64_t n;
+    int32_t splits;
+};
+
+struct FillParams {
+    void* ptr;
+    int64_t n32;            // number of 32-bit words
+    int32_t value;
+};
+
+// Generic vector-ALU GEMM (fallbacks and attention on VALU).
+enum ValuKind : int32_t {
+    VK_I16_DOT2 = 0,        // int16 in, v_dot2_i32_i16, wrapping int32
+    VK_S24 = 1,             // int32 in, sext24 products (v_mad_i32_i24 class), wrapping
+    VK_I32 = 2,             // int32 in, low 32 bits of products, wrapping
+    VK_F32 = 3,             // float in and out, fixed summation order
+};
+
+struct ValuGemmParams {
+    const void* A;          // [M][lda]
+    const void* B;          // b_trans ? [N][ldb] : [K][ldb]
+    void* C;                // [M][ldc]
+    int64_t sA, sB, sC;
+    int32_t M, N, K, lda, ldb, ldc;
+    int32_t b_trans;
+    int32_t out_mode;
+    int32_t hw;
+};
+
+// ---------------------------------------------------------------------------
+// Cached launch records.
+// ---------------------------------------------------------------------------
+enum Bind : uint8_t { BIND_IN0 = 0, BIND_IN1 = 1, BIND_IN2 = 2, BIND_OUT = 3, BIND_WS = 4 };
+
+struct Slot {
+    uint16_t off;           // byte offset of a pointer field in the parameter blob
+    uint8_t bind;           // what it points at
+    uint64_t ws_off;        // BIND_WS: byte offset into the workspace
+};
+
+struct LaunchRec {
+    const void* fn = nullptr;
+    dim3 grid{1, 1, 1};
+    dim3 block{1, 1, 1};
+    uint32_t shmem = 0;
+    alignas(16) unsigned char blob[256];
+    uint32_t blob_size = 0;
+    Slot slots[8];
+    int nslots = 0;
+    const char* name = "";
+
+    template <class P>
+    void set_params(const P& p) {
+        static_assert(sizeof(P) <= sizeof(blob), "parameter block too large");
+        memcpy(blob, &p, sizeof(P));
+        blob_size = sizeof(P);
+    }
+    void bind(size_t off, Bind b, uint64_t ws_off = 0) {
+        slots[nslots].off = (uint16_t)off;
+        slots[nslots].bind = b;
+        slots[nslots].ws_off = ws_off;
+        ++nslots;
+    }
+};
+
+// ---------------------------------------------------------------------------
+// Kernel-family builders (defined in the .hip files).  Each fills a launch
+// record for a fully planned problem; pointers are bound through slots.
+// ---------------------------------------------------------------------------
+enum Route : int32_t {
+    R_AUTO = 0, R_I8_DIRECT = 1, R_F16_EXACT = 2, R_I8_KARATSUBA = 3, R_I8_OFFSET4 = 4,
+    R_VALU_DOT2 = 5, R_S24_VALU = 6, R_S24_I8LIMB = 7,
+    R_ATTN_F32_MFMA = 8, R_ATTN_I32_MFMA = 9, R_ATTN_I32_VALU = 10,
+    R_ATTN_F32_VALU = 11,   // internal fallback for shapes the fp32 MFMA kernel does not take
+};
+
+// Integer GEMM main kernel for an MFMA route; returns false if unsupported.
+bool build_gemm_mfma(int32_t route, const GemmParams& p, int batch, LaunchRec* rec,
+                     int* tile_m, int* tile_n, int* tile_k);
+void build_sums(const SumsParams& p, LaunchRec* rec);
+void build_im2col(const Im2colParams& p, LaunchRec* rec);
+void build_valu_gemm(int32_t kind, const ValuGemmParams& p, int batch, LaunchRec* rec);
+bool build_attn_f32(const AttnParams& p, LaunchRec* rec);
+bool build_attn_i32(const AttnParams& p, LaunchRec* rec);
+void build_reduce(const ReduceParams& p, LaunchRec* rec);
+void build_fill(const FillParams& p, LaunchRec* rec);
+
+}  // namespace qx

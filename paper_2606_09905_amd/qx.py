@@ -1,0 +1,337 @@
+"""Thin Python binding of libqx (the C ABI in include/qx.h).
+
+Argument marshalling only: every step of every operation runs in the HIP
+kernels of libqx.so.  torch supplies device memory and the current stream.
+If the library is missing, every call raises; there is no fallback.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import re
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libqx.so")
+HEADER_PATH = os.path.join(os.path.dirname(_HERE), "include", "qx.h")
+
+# qx_status
+OK, ERR_INVALID_ARG, ERR_UNSUPPORTED, ERR_RANGE, ERR_OUT_OF_MEMORY, ERR_DEVICE = range(6)
+STATUS_NAMES = ["OK", "INVALID_ARG", "UNSUPPORTED", "RANGE", "OUT_OF_MEMORY", "DEVICE"]
+
+# qx_attn_dtype
+DT_F32, DT_I32 = 0, 1
+
+# qx_route
+ROUTE = {
+    "auto": 0, "i8_direct": 1, "f16_exact": 2, "i8_karatsuba": 3, "i8_offset4": 4,
+    "valu_dot2": 5, "s24_valu": 6, "s24_i8limb": 7,
+    "attn_f32_mfma": 8, "attn_i32_mfma": 9, "attn_i32_valu": 10, "attn_f32_valu": 11,
+}
+ROUTE_NAME = {v: k for k, v in ROUTE.items()}
+
+
+class QxError(RuntimeError):
+    def __init__(self, status: int, message: str):
+        self.status = status
+        name = STATUS_NAMES[status] if 0 <= status < len(STATUS_NAMES) else str(status)
+        super().__init__(f"qx {name}: {message}")
+
+
+class PlanInfo(ctypes.Structure):
+    _fields_ = [
+        ("route", ctypes.c_int32), ("chunk", ctypes.c_int32), ("products", ctypes.c_int32),
+        ("tile_m", ctypes.c_int32), ("tile_n", ctypes.c_int32), ("tile_k", ctypes.c_int32),
+        ("kernels", ctypes.c_int32), ("exact_no_wrap", ctypes.c_int32),
+        ("workspace_bytes", ctypes.c_int64),
+    ]
+
+    def as_dict(self) -> dict:
+        d = {f: getattr(self, f) for f, _ in self._fields_}
+        d["route_name"] = ROUTE_NAME.get(self.route, str(self.route))
+        return d
+
+
+_lib = None
+_i64, _i32, _p = ctypes.c_int64, ctypes.c_int32, ctypes.c_void_p
+
+
+def lib() -> ctypes.CDLL:
+    """Load libqx.so (built in-tree); raises if it has not been built."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is missing: build it with "
+                               "`python -m paper_2606_09905_amd.build`")
+        L = ctypes.CDLL(LIB_PATH)
+        sig = {
+            "qgemm_i16i32": [_p, _p, _p, _i64, _i64, _i64, _i64, _i32, _i32, _p],
+            "qgemm_i32_s24": [_p, _p, _p, _i64, _i64, _i64, _i64, _p],
+            "conv2d_gemm": [_p, _p, _p] + [_i64] * 9 + [_i32, _i32, _p],
+            "attn_core": [_i32, _p, _p, _p, _p, _i64, _i64, _i32, _p],
+            "qx_exec_create_gemm_i16i32": [_p, _i64, _i64, _i64, _i64, _i32, _i32, _i32],
+            "qx_exec_create_gemm_i32_s24": [_p, _i64, _i64, _i64, _i64, _i32],
+            "qx_exec_create_conv2d": [_p] + [_i64] * 9 + [_i32, _i32, _i32],
+            "qx_exec_create_attn": [_p, _i32, _i64, _i64, _i32, _i32],
+            "qx_exec_run": [_p, _p, _p, _p],
+            "qx_exec_plan": [_p, _p],
+            "qx_exec_destroy": [_p],
+            "qx_plan_gemm_i16i32": [_p, _i64, _i64, _i64, _i64, _i32, _i32, _i32],
+            "qx_plan_gemm_i32_s24": [_p, _i64, _i64, _i64, _i64, _i32],
+            "qx_plan_conv2d": [_p] + [_i64] * 9 + [_i32, _i32, _i32],
+            "qx_plan_attn": [_p, _i32, _i64, _i64, _i32, _i32],
+        }
+        for name, args in sig.items():
+            fn = getattr(L, name)
+            fn.argtypes = args
+            fn.restype = ctypes.c_int
+        L.qx_last_error.argtypes = []
+        L.qx_last_error.restype = ctypes.c_char_p
+        L.qx_release_cache.argtypes = []
+        L.qx_release_cache.restype = None
+        _lib = L
+    return _lib
+
+
+def header_functions() -> list[str]:
+    """Names of every function include/qx.h declares."""
+    with open(HEADER_PATH) as f:
+        text = f.read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b([A-Za-z_]\w*)\s*\(", text)) -
+                  {"if", "defined", "sizeof"})
+
+
+def check(status: int) -> None:
+    if status != OK:
+        msg = lib().qx_last_error()
+        raise QxError(status, msg.decode() if msg else "")
+
+
+# ---------------------------------------------------------------------------
+# torch marshalling
+# ---------------------------------------------------------------------------
+def _torch():
+    import torch
+    return torch
+
+
+def _stream(stream):
+    torch = _torch()
+    if stream is None:
+        return ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+    if hasattr(stream, "cuda_stream"):
+        return ctypes.c_void_p(stream.cuda_stream)
+    return ctypes.c_void_p(int(stream))
+
+
+def _dev_tensor(t, dtype, name):
+    torch = _torch()
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a torch.Tensor")
+    if t.dtype != dtype:
+        raise TypeError(f"{name} must be {dtype}, got {t.dtype}")
+    if t.device.type != "cuda":
+        raise ValueError(f"{name} must be on a GPU device")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    return ctypes.c_void_p(t.data_ptr())
+
+
+def _gemm_shapes(A, B):
+    if A.dim() == 2 and B.dim() == 2:
+        (M, K), (K2, N) = A.shape, B.shape
+        batch, out_shape = 1, (M, N)
+    elif A.dim() == 3 and B.dim() == 3:
+        (batch, M, K), (b2, K2, N) = A.shape, B.shape
+        if b2 != batch:
+            raise ValueError("batch mismatch")
+        out_shape = (batch, M, N)
+    else:
+        raise ValueError("A and B must both be 2-D or both 3-D")
+    if K2 != K:
+        raise ValueError(f"inner dimensions differ: {K} vs {K2}")
+    return batch, M, N, K, out_shape
+
+
+def qgemm_i16i32(A, B, bound_a: int = 0, bound_b: int = 0, out=None, stream=None):
+    """C = A @ B, int16 in, int32 out (exact mod 2^32); [M,K]@[K,N] or batched."""
+    torch = _torch()
+    batch, M, N, K, shape = _gemm_shapes(A, B)
+    if out is None:
+        out = torch.empty(shape, dtype=torch.int32, device=A.device)
+    check(lib().qgemm_i16i32(_dev_tensor(A, torch.int16, "A"), _dev_tensor(B, torch.int16, "B"),
+                             _dev_tensor(out, torch.int32, "C"), M, N, K, batch,
+                             int(bound_a), int(bound_b), _stream(stream)))
+    return out
+
+
+def qgemm_i32_s24(A, B, out=None, stream=None):
+    """C = sext24(A) @ sext24(B) mod 2^32, int32 in and out."""
+    torch = _torch()
+    batch, M, N, K, shape = _gemm_shapes(A, B)
+    if out is None:
+        out = torch.empty(shape, dtype=torch.int32, device=A.device)
+    check(lib().qgemm_i32_s24(_dev_tensor(A, torch.int32, "A"), _dev_tensor(B, torch.int32, "B"),
+                              _dev_tensor(out, torch.int32, "C"), M, N, K, batch, _stream(stream)))
+    return out
+
+
+def conv_out_hw(H, W, KH, KW, stride, pad):
+    return (H + 2 * pad - KH) // stride + 1, (W + 2 * pad - KW) // stride + 1
+
+
+def conv2d_gemm(x, w, stride: int = 1, pad: int = 0, bound_x: int = 0, bound_w: int = 0,
+                out=None, stream=None):
+    """NCHW int16 x, OIHW int16 w -> NCHW int32 y (cross-correlation, zero padding)."""
+    torch = _torch()
+    N, Ci, H, W = x.shape
+    Co, Ci2, KH, KW = w.shape
+    if Ci2 != Ci:
+        raise ValueError("channel mismatch")
+    Ho, Wo = conv_out_hw(H, W, KH, KW, stride, pad)
+    if out is None:
+        out = torch.empty((N, Co, max(Ho, 0), max(Wo, 0)), dtype=torch.int32, device=x.device)
+    check(lib().conv2d_gemm(_dev_tensor(x, torch.int16, "x"), _dev_tensor(w, torch.int16, "w"),
+                            _dev_tensor(out, torch.int32, "y"), N, Ci, H, W, Co, KH, KW,
+                            stride, pad, int(bound_x), int(bound_w), _stream(stream)))
+    return out
+
+
+def attn_core(Q, K, V, bound: int = 0, out=None, stream=None):
+    """O = (Q K^T) V for [L, d] float32 or int32 tensors."""
+    torch = _torch()
+    if Q.dtype == torch.float32:
+        dt = DT_F32
+    elif Q.dtype == torch.int32:
+        dt = DT_I32
+    else:
+        raise TypeError("Q must be float32 or int32")
+    L, d = Q.shape
+    if out is None:
+        out = torch.empty((L, d), dtype=Q.dtype, device=Q.device)
+    check(lib().attn_core(dt, _dev_tensor(Q, Q.dtype, "Q"), _dev_tensor(K, Q.dtype, "K"),
+                          _dev_tensor(V, Q.dtype, "V"), _dev_tensor(out, Q.dtype, "O"), L, d,
+                          int(bound), _stream(stream)))
+    return out
+
+
+# ---------------------------------------------------------------------------
+# planner queries (host only)
+# ---------------------------------------------------------------------------
+def _route(route) -> int:
+    return ROUTE[route] if isinstance(route, str) else int(route)
+
+
+def plan_gemm_i16i32(M, N, K, batch=1, bound_a=0, bound_b=0, route="auto") -> dict:
+    info = PlanInfo()
+    check(lib().qx_plan_gemm_i16i32(ctypes.byref(info), M, N, K, batch, bound_a, bound_b, _route(route)))
+    return info.as_dict()
+
+
+def plan_gemm_i32_s24(M, N, K, batch=1, route="auto") -> dict:
+    info = PlanInfo()
+    check(lib().qx_plan_gemm_i32_s24(ctypes.byref(info), M, N, K, batch, _route(route)))
+    return info.as_dict()
+
+
+def plan_conv2d(N, Ci, H, W, Co, KH, KW, stride=1, pad=0, bound_x=0, bound_w=0, route="auto") -> dict:
+    info = PlanInfo()
+    check(lib().qx_plan_conv2d(ctypes.byref(info), N, Ci, H, W, Co, KH, KW, stride, pad,
+                               bound_x, bound_w, _route(route)))
+    return info.as_dict()
+
+
+def plan_attn(dtype: str, L, d, bound=0, route="auto") -> dict:
+    info = PlanInfo()
+    check(lib().qx_plan_attn(ctypes.byref(info), DT_F32 if dtype == "f32" else DT_I32, L, d,
+                             bound, _route(route)))
+    return info.as_dict()
+
+
+# ---------------------------------------------------------------------------
+# persistent executor
+# ---------------------------------------------------------------------------
+class Executor:
+    """Owns a qx_exec handle: planned and allocated once, re-dispatched by run()."""
+
+    def __init__(self, handle: ctypes.c_void_p, out_shape, out_dtype, n_inputs: int):
+        self._h = handle
+        self.out_shape = tuple(out_shape)
+        self.out_dtype = out_dtype
+        self.n_inputs = n_inputs
+
+    @classmethod
+    def gemm_i16i32(cls, M, N, K, batch=1, bound_a=0, bound_b=0, route="auto"):
+        torch = _torch()
+        h = ctypes.c_void_p()
+        check(lib().qx_exec_create_gemm_i16i32(ctypes.byref(h), M, N, K, batch, bound_a, bound_b,
+                                               _route(route)))
+        return cls(h, (batch, M, N), torch.int32, 2)
+
+    @classmethod
+    def gemm_i32_s24(cls, M, N, K, batch=1, route="auto"):
+        torch = _torch()
+        h = ctypes.c_void_p()
+        check(lib().qx_exec_create_gemm_i32_s24(ctypes.byref(h), M, N, K, batch, _route(route)))
+        return cls(h, (batch, M, N), torch.int32, 2)
+
+    @classmethod
+    def conv2d(cls, N, Ci, H, W, Co, KH, KW, stride=1, pad=0, bound_x=0, bound_w=0, route="auto"):
+        torch = _torch()
+        h = ctypes.c_void_p()
+        check(lib().qx_exec_create_conv2d(ctypes.byref(h), N, Ci, H, W, Co, KH, KW, stride, pad,
+                                          bound_x, bound_w, _route(route)))
+        Ho, Wo = conv_out_hw(H, W, KH, KW, stride, pad)
+        return cls(h, (N, Co, Ho, Wo), torch.int32, 2)
+
+    @classmethod
+    def attn(cls, dtype: str, L, d, bound=0, route="auto"):
+        torch = _torch()
+        h = ctypes.c_void_p()
+        check(lib().qx_exec_create_attn(ctypes.byref(h), DT_F32 if dtype == "f32" else DT_I32, L, d,
+                                        bound, _route(route)))
+        return cls(h, (L, d), torch.float32 if dtype == "f32" else torch.int32, 3)
+
+    def plan(self) -> dict:
+        info = PlanInfo()
+        check(lib().qx_exec_plan(self._h, ctypes.byref(info)))
+        return info.as_dict()
+
+    def run_ptrs(self, in_ptrs, out_ptr: int, stream=None) -> None:
+        """Enqueue with raw device pointers (ints)."""
+        arr = (ctypes.c_void_p * len(in_ptrs))(*[ctypes.c_void_p(p) for p in in_ptrs])
+        check(lib().qx_exec_run(self._h, arr, ctypes.c_void_p(out_ptr), _stream(stream)))
+
+    def run(self, inputs, out=None, stream=None):
+        torch = _torch()
+        if len(inputs) != self.n_inputs:
+            raise ValueError(f"expected {self.n_inputs} inputs")
+        if out is None:
+            out = torch.empty(self.out_shape, dtype=self.out_dtype, device=inputs[0].device)
+        ptrs = []
+        for i, t in enumerate(inputs):
+            if t.device.type != "cuda" or not t.is_contiguous():
+                raise ValueError(f"input {i} must be a contiguous GPU tensor")
+            ptrs.append(t.data_ptr())
+        if not out.is_contiguous() or out.dtype != self.out_dtype:
+            raise ValueError("bad output tensor")
+        self.run_ptrs(ptrs, out.data_ptr(), stream)
+        return out
+
+    def close(self) -> None:
+        if self._h:
+            check(lib().qx_exec_destroy(self._h))
+            self._h = None
+
+    def __enter__(self):
+        return self
+
+    def __exit__(self, *exc):
+        self.close()
+
+    def __del__(self):
+        try:
+            if self._h:
+                lib().qx_exec_destroy(self._h)
+        except Exception:
+            pass

@@ -1,0 +1,180 @@
+"""Host-only checks of libqx: it loads, exports every declared symbol, and
+its planner picks exact routes from the operand-range contract.  No device
+call is made here (validation and planning run before any HIP call)."""
+import ctypes
+
+import pytest
+
+from paper_2606_09905_amd import qx
+from paper_2606_09905_amd.workloads import WORKLOADS
+
+
+def test_library_exports_every_header_symbol():
+    L = qx.lib()
+    names = qx.header_functions()
+    assert len(names) >= 17
+    for n in names:
+        assert hasattr(L, n), n
+
+
+def test_auto_routes_for_the_workloads():
+    w = WORKLOADS
+    d = w["gemm_i16_256"].dims
+    p = qx.plan_gemm_i16i32(d["M"], d["N"], d["K"], 1, 1024, 1024)
+    assert p["route_name"] == "f16_exact" and p["chunk"] == 16 and p["exact_no_wrap"] == 1
+    for name in ("gemm_i16_8192", "gemm_i16_64x2048"):
+        d = w[name].dims
+        p = qx.plan_gemm_i16i32(d["M"], d["N"], d["K"], d["batch"], 256, 256)
+        assert p["route_name"] == "f16_exact" and p["chunk"] == 256 and p["exact_no_wrap"] == 1
+        assert p["workspace_bytes"] == 0 and p["kernels"] == 1
+    p = qx.plan_gemm_i32_s24(1024, 1024, 1024, 1)
+    assert p["route_name"] == "s24_i8limb" and p["products"] == 8 and p["exact_no_wrap"] == 0
+    assert p["workspace_bytes"] >= 4 * 2048
+    d = w["conv_8x64x56x56_128_3x3"].dims
+    p = qx.plan_conv2d(d["N"], d["Ci"], d["H"], d["W"], d["Co"], d["KH"], d["KW"], 1, 1, 256, 256)
+    assert p["route_name"] == "f16_exact" and p["kernels"] == 2
+    assert p["workspace_bytes"] >= 2 * 576 * 8 * 56 * 56
+    assert qx.plan_attn("f32", 4096, 64)["route_name"] == "attn_f32_mfma"
+    p = qx.plan_attn("i32", 4096, 64, 64)
+    assert p["route_name"] == "attn_i32_mfma" and p["products"] == 3
+
+
+@pytest.mark.parametrize("b,route", [
+    (1, "i8_direct"), (127, "i8_direct"), (128, "f16_exact"), (256, "f16_exact"),
+    (1024, "f16_exact"), (2048, "i8_karatsuba"), (8127, "i8_karatsuba"),
+    (8128, "i8_offset4"), (0, "i8_offset4"), (32768, "i8_offset4"),
+])
+def test_route_boundaries(b, route):
+    assert qx.plan_gemm_i16i32(64, 64, 64, 1, b, b)["route_name"] == route
+
+
+@pytest.mark.parametrize("ba,bb,chunk", [
+    (128, 128, 1024), (256, 256, 256), (255, 255, 256), (300, 300, 176), (512, 512, 64),
+    (724, 724, 32), (1024, 1024, 16), (2048, 512, 16), (1, 2048, 8192),
+])
+def test_f16_chunk_rule(ba, bb, chunk):
+    # chunk: largest multiple of 16 with chunk * ba * bb <= 2^24; the kernel
+    # flushes every 64 K (one tile) or every 16 K (one MFMA step) within it.
+    p = qx.plan_gemm_i16i32(64, 64, 64, 1, ba, bb, "f16_exact")
+    largest = (2 ** 24 // (ba * bb)) // 16 * 16
+    assert largest >= 16
+    expect = largest // 64 * 64 if largest >= 64 else 16
+    assert p["chunk"] == expect == (chunk // 64 * 64 if chunk >= 64 else 16)
+    assert p["chunk"] * ba * bb <= 2 ** 24
+
+
+def test_f16_infeasible_and_forced_routes():
+    with pytest.raises(qx.QxError) as e:
+        qx.plan_gemm_i16i32(64, 64, 64, 1, 2049, 16, "f16_exact")
+    assert e.value.status == qx.ERR_RANGE
+    with pytest.raises(qx.QxError) as e:
+        qx.plan_gemm_i16i32(64, 64, 64, 1, 1448, 1448, "f16_exact")  # chunk < 16
+    assert e.value.status == qx.ERR_RANGE
+    with pytest.raises(qx.QxError) as e:
+        qx.plan_gemm_i16i32(64, 64, 64, 1, 128, 5, "i8_direct")
+    assert e.value.status == qx.ERR_RANGE
+    with pytest.raises(qx.QxError) as e:
+        qx.plan_gemm_i16i32(64, 64, 64, 1, 8128, 5, "i8_karatsuba")
+    assert e.value.status == qx.ERR_RANGE
+    with pytest.raises(qx.QxError) as e:
+        qx.plan_gemm_i16i32(64, 64, 64, 1, 0, 0, "s24_valu")
+    assert e.value.status == qx.ERR_INVALID_ARG
+    with pytest.raises(qx.QxError) as e:
+        qx.plan_gemm_i32_s24(64, 64, 64, 1, "f16_exact")
+    assert e.value.status == qx.ERR_INVALID_ARG
+    for r in ("i8_offset4", "valu_dot2"):
+        assert qx.plan_gemm_i16i32(5, 5, 5, 1, 0, 0, r)["route_name"] == r
+    assert qx.plan_gemm_i32_s24(5, 5, 5, 1, "s24_valu")["route_name"] == "s24_valu"
+
+
+@pytest.mark.parametrize("args", [
+    (-1, 4, 4, 1), (4, -1, 4, 1), (4, 4, -1, 1), (4, 4, 4, -1),
+])
+def test_negative_dims_rejected(args):
+    with pytest.raises(qx.QxError) as e:
+        qx.plan_gemm_i16i32(*args)
+    assert e.value.status == qx.ERR_INVALID_ARG
+    assert "must be >= 0" in str(e.value)
+
+
+def test_size_limits_and_bad_bounds():
+    with pytest.raises(qx.QxError) as e:
+        qx.plan_gemm_i16i32(1 << 31, 4, 4)
+    assert e.value.status == qx.ERR_UNSUPPORTED
+    with pytest.raises(qx.QxError) as e:
+        qx.plan_gemm_i16i32(1 << 21, 1 << 21, 4)
+    assert e.value.status == qx.ERR_UNSUPPORTED
+    with pytest.raises(qx.QxError) as e:
+        qx.plan_gemm_i16i32(4, 4, 4, 70000)
+    assert e.value.status == qx.ERR_UNSUPPORTED
+    for bad in (-1, 32769):
+        with pytest.raises(qx.QxError) as e:
+            qx.plan_gemm_i16i32(4, 4, 4, 1, bad, 1)
+        assert e.value.status == qx.ERR_INVALID_ARG
+    with pytest.raises(qx.QxError) as e:
+        qx.plan_gemm_i16i32(4, 4, 4, 1, 1, 1, 99)
+    assert e.value.status == qx.ERR_INVALID_ARG
+
+
+def test_empty_and_degenerate_plans():
+    p = qx.plan_gemm_i16i32(0, 5, 5)
+    assert p["kernels"] == 0 and p["workspace_bytes"] == 0
+    p = qx.plan_gemm_i16i32(5, 5, 0)
+    assert p["kernels"] == 1  # K == 0: the output is filled with zeros
+    p = qx.plan_gemm_i32_s24(3, 0, 9, 2)
+    assert p["kernels"] == 0
+    assert qx.plan_attn("f32", 0, 64)["kernels"] == 0
+    assert qx.plan_conv2d(0, 3, 5, 5, 2, 3, 3, 1, 1)["kernels"] == 0
+    assert qx.plan_conv2d(1, 0, 5, 5, 2, 3, 3, 1, 1)["kernels"] == 1
+
+
+def test_conv_validation():
+    with pytest.raises(qx.QxError) as e:
+        qx.plan_conv2d(1, 1, 2, 2, 1, 5, 5, 1, 0)   # kernel larger than the input
+    assert e.value.status == qx.ERR_INVALID_ARG
+    with pytest.raises(qx.QxError) as e:
+        qx.plan_conv2d(1, 1, 8, 8, 1, 3, 3, 0, 1)   # stride 0
+    assert e.value.status == qx.ERR_INVALID_ARG
+    with pytest.raises(qx.QxError) as e:
+        qx.plan_conv2d(1, 1, 8, 8, 1, 0, 3, 1, 1)   # empty kernel
+    assert e.value.status == qx.ERR_INVALID_ARG
+    p = qx.plan_conv2d(2, 3, 7, 9, 4, 3, 2, 2, 1, 0, 0)
+    assert p["route_name"] == "i8_offset4"
+
+
+def test_attention_plans():
+    assert qx.plan_attn("f32", 100, 48)["route_name"] == "attn_f32_valu"
+    assert qx.plan_attn("i32", 100, 64, 0)["route_name"] == "attn_i32_valu"
+    assert qx.plan_attn("i32", 100, 64, 127)["route_name"] == "attn_i32_mfma"
+    assert qx.plan_attn("i32", 100, 128, 127)["route_name"] == "attn_i32_mfma"
+    with pytest.raises(qx.QxError) as e:
+        qx.plan_attn("i32", 100, 64, 128, "attn_i32_mfma")
+    assert e.value.status == qx.ERR_RANGE
+    with pytest.raises(qx.QxError) as e:
+        qx.plan_attn("f32", 100, 48, 0, "attn_f32_mfma")
+    assert e.value.status == qx.ERR_UNSUPPORTED
+    with pytest.raises(qx.QxError) as e:
+        qx.plan_attn("f32", 100, 300)
+    assert e.value.status == qx.ERR_UNSUPPORTED
+    # key splits: every split boundary on a 32-key block, enough workgroups
+    p = qx.plan_attn("f32", 4096, 64)
+    assert p["tile_k"] % 32 == 0 and (4096 // 128) * (4096 // p["tile_k"]) >= 512
+
+
+def test_null_pointer_validation_before_device():
+    # Validation returns before any HIP call, so this runs without a GPU.
+    L = qx.lib()
+    st = L.qgemm_i16i32(None, None, None, 4, 4, 4, 1, 0, 0, None)
+    assert st == qx.ERR_INVALID_ARG
+    assert b"NULL" in L.qx_last_error()
+    st = L.qgemm_i16i32(None, None, None, -4, 4, 4, 1, 0, 0, None)
+    assert st == qx.ERR_INVALID_ARG
+    # empty problems are a no-op and need no pointers
+    assert L.qgemm_i16i32(None, None, None, 0, 0, 4, 1, 0, 0, None) == qx.OK
+    assert L.qgemm_i16i32(None, None, None, 0, 4, 4, 1, 0, 0, None) == qx.ERR_INVALID_ARG  # B non-empty
+    assert L.attn_core(0, None, None, None, None, 0, 64, 0, None) == qx.OK
+    assert L.attn_core(7, None, None, None, None, 4, 64, 0, None) == qx.ERR_INVALID_ARG
+    assert L.qx_exec_run(None, None, None, None) == qx.ERR_INVALID_ARG
+    assert L.qx_exec_destroy(None) == qx.OK
+    info = qx.PlanInfo()
+    assert L.qx_exec_plan(None, ctypes.byref(info)) == qx.ERR_INVALID_ARG

@@ -1,0 +1,339 @@
+"""GPU parity: the HIP path (through the C ABI) against the CPU oracle.
+
+Integer results must match bit for bit; FP32 attention must satisfy
+max|O - R| / max|R| <= 1e-4 against the float64 reference R.  Small shapes
+span several tiles and ragged tails on every route; the full-size workloads
+are checked on oracle-computed sampled rows and with Freivalds' check
+C r == A (B r), exact in int64, which covers every output element.
+"""
+import sys
+import zlib
+
+import numpy as np
+import pytest
+
+from oracle import oracle as orc
+from paper_2606_09905_amd import qx
+from paper_2606_09905_amd.workloads import WORKLOADS
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+
+
+def _say(msg):
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+def dev(a: np.ndarray):
+    return torch.from_numpy(np.ascontiguousarray(a)).cuda()
+
+
+def host(t) -> np.ndarray:
+    torch.cuda.synchronize()
+    return t.cpu().numpy()
+
+
+def run_exec(ex, inputs):
+    out = ex.run([dev(a) for a in inputs])
+    return host(out)
+
+
+def rand_int(rng, shape, b, dtype):
+    return rng.integers(-b, b, size=shape, dtype=np.int64, endpoint=True).astype(dtype)
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    qx.lib()
+    yield
+    qx.lib().qx_release_cache()
+
+
+# ---------------------------------------------------------------------------
+# INT16 GEMM, every route
+# ---------------------------------------------------------------------------
+GEMM_SHAPES = [  # M, N, K, batch
+    (1, 1, 1, 1), (3, 5, 7, 1), (15, 17, 16, 2), (33, 65, 127, 1), (128, 128, 64, 1),
+    (129, 257, 200, 3), (256, 256, 256, 1), (200, 136, 64, 2), (64, 72, 520, 1),
+]
+I16_ROUTES = [  # route, bound
+    ("i8_direct", 127), ("f16_exact", 256), ("f16_exact", 1024), ("f16_exact", 2048),
+    ("i8_karatsuba", 8127), ("i8_offset4", 32768), ("valu_dot2", 32768),
+]
+
+
+@pytest.mark.parametrize("route,bound", I16_ROUTES)
+@pytest.mark.parametrize("shape", GEMM_SHAPES)
+def test_gemm_i16_routes(route, bound, shape):
+    M, N, K, batch = shape
+    b_eff = bound if route != "f16_exact" or bound != 2048 else 2048
+    bb = 16 if (route == "f16_exact" and bound == 2048) else bound  # keep chunk >= 16
+    rng = np.random.default_rng(zlib.crc32(repr((route, bound, shape)).encode()))
+    A = rand_int(rng, (batch, M, K), min(b_eff, 32767), np.int16)
+    B = rand_int(rng, (batch, K, N), min(bb, 32767), np.int16)
+    with qx.Executor.gemm_i16i32(M, N, K, batch, bound, bb, route) as ex:
+        assert ex.plan()["route_name"] == route
+        got = run_exec(ex, (A, B))
+    ref = orc.gemm_i16i32(A, B)
+    assert np.array_equal(got, ref)
+
+
+@pytest.mark.parametrize("route,bound", I16_ROUTES)
+def test_gemm_i16_extremes(route, bound):
+    # All operands at the contract's most negative value: largest products,
+    # fp16 partial sums exactly at chunk * bound^2, wrap-around for full int16.
+    b = min(bound, 32768)
+    bb = 16 if (route == "f16_exact" and bound == 2048) else b
+    for K in (64, 1000, 4096):
+        A = np.full((1, 64, K), -b, np.int16)
+        B = np.full((1, K, 64), -bb, np.int16)
+        A[0, ::3, ::2] = min(b, 32767)          # mix in the most positive value
+        with qx.Executor.gemm_i16i32(64, 64, K, 1, bound, bb, route) as ex:
+            got = run_exec(ex, (A, B))
+        assert np.array_equal(got, orc.gemm_i16i32(A, B)), (route, K)
+
+
+def test_f16_exact_mixed_magnitudes():
+    # Products alternating between 2^16 and 1 inside one fp32 partial sum:
+    # a narrow internal adder would lose the small terms.
+    K = 8192
+    A = np.ones((1, 64, K), np.int16)
+    B = np.ones((1, K, 64), np.int16)
+    A[0, :, ::2] = -256
+    B[0, ::2, :] = -256
+    A[0, 5, 1::4] = 255
+    with qx.Executor.gemm_i16i32(64, 64, K, 1, 256, 256, "f16_exact") as ex:
+        got = run_exec(ex, (A, B))
+    assert np.array_equal(got, orc.gemm_i16i32(A, B))
+
+
+def test_gemm_i16_oneshot_and_empty():
+    rng = np.random.default_rng(3)
+    A = rand_int(rng, (96, 80), 1024, np.int16)
+    B = rand_int(rng, (80, 112), 1024, np.int16)
+    C = host(qx.qgemm_i16i32(dev(A), dev(B), 1024, 1024))
+    assert np.array_equal(C, orc.gemm_i16i32(A, B))
+    # K == 0 -> zeros; M == 0 -> empty
+    Z = qx.qgemm_i16i32(torch.empty((5, 0), dtype=torch.int16, device="cuda"),
+                        torch.empty((0, 7), dtype=torch.int16, device="cuda"))
+    assert Z.shape == (5, 7) and int(Z.abs().sum()) == 0
+    E = qx.qgemm_i16i32(torch.empty((0, 9), dtype=torch.int16, device="cuda"),
+                        torch.ones((9, 4), dtype=torch.int16, device="cuda"))
+    assert E.shape == (0, 4)
+
+
+# ---------------------------------------------------------------------------
+# smul24 GEMM
+# ---------------------------------------------------------------------------
+@pytest.mark.parametrize("route", ["s24_i8limb", "s24_valu"])
+@pytest.mark.parametrize("shape", GEMM_SHAPES)
+def test_gemm_s24_routes(route, shape):
+    M, N, K, batch = shape
+    rng = np.random.default_rng(M * 7 + N + K)
+    # full 32-bit words: bits 24..31 must be ignored
+    A = rng.integers(-(1 << 31), (1 << 31) - 1, (batch, M, K), dtype=np.int32, endpoint=True)
+    B = rng.integers(-(1 << 31), (1 << 31) - 1, (batch, K, N), dtype=np.int32, endpoint=True)
+    with qx.Executor.gemm_i32_s24(M, N, K, batch, route) as ex:
+        got = run_exec(ex, (A, B))
+    assert np.array_equal(got, orc.gemm_i32_s24(A, B))
+
+
+@pytest.mark.parametrize("route", ["s24_i8limb", "s24_valu"])
+def test_gemm_s24_extremes_and_accumulator_wrap(route):
+    # -2^23 everywhere: all limbs -128, each limb product 2^14; with K = 2^17
+    # the int32 accumulators of the matrix cores pass 2^31 and must wrap.
+    K = 1 << 17
+    A = np.full((1, 32, K), -(1 << 23), np.int32)
+    B = np.full((1, K, 32), -(1 << 23), np.int32)
+    A[0, 1, :] = (1 << 23) - 1
+    B[0, :, 2] = 0x01000005
+    with qx.Executor.gemm_i32_s24(32, 32, K, 1, route) as ex:
+        got = run_exec(ex, (A, B))
+    assert np.array_equal(got, orc.gemm_i32_s24(A, B))
+
+
+# ---------------------------------------------------------------------------
+# Conv2D
+# ---------------------------------------------------------------------------
+CONV_CASES = [  # N, Ci, H, W, Co, KH, KW, stride, pad, bound
+    (1, 1, 3, 3, 1, 3, 3, 1, 1, 256), (2, 3, 9, 7, 5, 3, 3, 1, 1, 256),
+    (1, 16, 13, 11, 40, 3, 3, 2, 1, 1024), (2, 8, 12, 12, 4, 5, 5, 1, 2, 127),
+    (3, 5, 17, 9, 7, 3, 2, 3, 0, 0), (1, 64, 20, 20, 130, 1, 1, 1, 0, 8000),
+]
+
+
+@pytest.mark.parametrize("case", CONV_CASES)
+def test_conv(case):
+    N, Ci, H, W, Co, KH, KW, s, p, b = case
+    rng = np.random.default_rng(sum(case))
+    bx = b if b else 32767
+    x = rand_int(rng, (N, Ci, H, W), bx, np.int16)
+    w = rand_int(rng, (Co, Ci, KH, KW), bx, np.int16)
+    y = host(qx.conv2d_gemm(dev(x), dev(w), s, p, b, b))
+    assert np.array_equal(y, orc.conv2d_direct(x, w, s, p))
+
+
+# ---------------------------------------------------------------------------
+# Attention core
+# ---------------------------------------------------------------------------
+def normwise(O, R):
+    return float(np.abs(O.astype(np.float64) - R).max() / max(np.abs(R).max(), 1e-300))
+
+
+@pytest.mark.parametrize("L,d", [(1, 32), (31, 64), (32, 64), (100, 64), (257, 32), (300, 128),
+                                 (1024, 64), (77, 96), (100, 48)])
+def test_attn_f32(L, d):
+    rng = np.random.default_rng(L + d)
+    Q, K, V = ((rng.standard_normal((L, d)) / np.sqrt(d)).astype(np.float32) for _ in range(3))
+    O = host(qx.attn_core(dev(Q), dev(K), dev(V)))
+    R = orc.attn_f64(Q, K, V)
+    assert normwise(O, R) <= 1e-4
+    # elementwise a-priori bound of fp32 evaluation in any order: (d + L) u |Q||K|^T|V|
+    absref = (np.abs(Q).astype(np.float64) @ np.abs(K).astype(np.float64).T) @ np.abs(V)
+    assert (np.abs(O - R) <= (d + L) * 2.0 ** -24 * absref + 1e-30).all()
+
+
+@pytest.mark.parametrize("L,d,b", [(1, 32, 64), (33, 64, 64), (128, 64, 127), (300, 32, 100),
+                                   (1024, 128, 127), (257, 96, 64), (1000, 64, 64)])
+def test_attn_i32_mfma(L, d, b):
+    rng = np.random.default_rng(L * 3 + d + b)
+    Q, K, V = (rand_int(rng, (L, d), b, np.int32) for _ in range(3))
+    O = host(qx.attn_core(dev(Q), dev(K), dev(V), bound=b))
+    assert np.array_equal(O, orc.attn_i32(Q, K, V))
+
+
+@pytest.mark.parametrize("L,d", [(1, 5), (40, 64), (129, 17)])
+def test_attn_i32_valu_full_range(L, d):
+    rng = np.random.default_rng(L + 11 * d)
+    Q, K, V = (rng.integers(-(1 << 31), (1 << 31) - 1, (L, d), dtype=np.int32, endpoint=True)
+               for _ in range(3))
+    O = host(qx.attn_core(dev(Q), dev(K), dev(V), bound=0))
+    assert np.array_equal(O, orc.attn_i32(Q, K, V))
+
+
+def test_attn_i32_extremes():
+    L, d, b = 512, 64, 127
+    Q = np.full((L, d), -b, np.int32)
+    K = np.full((L, d), -b, np.int32)
+    V = np.full((L, d), b, np.int32)
+    K[::2] = b
+    O = host(qx.attn_core(dev(Q), dev(K), dev(V), bound=b))
+    assert np.array_equal(O, orc.attn_i32(Q, K, V))
+
+
+# ---------------------------------------------------------------------------
+# Determinism and the executor
+# ---------------------------------------------------------------------------
+def test_repeatable_bit_identical():
+    rng = np.random.default_rng(0)
+    L, d = 2048, 64
+    Q, K, V = ((rng.standard_normal((L, d)) / 8).astype(np.float32) for _ in range(3))
+    tq, tk, tv = dev(Q), dev(K), dev(V)
+    first = host(qx.attn_core(tq, tk, tv))
+    for _ in range(5):
+        assert np.array_equal(host(qx.attn_core(tq, tk, tv)), first)
+    A = rand_int(rng, (512, 768), 256, np.int16)
+    B = rand_int(rng, (768, 640), 256, np.int16)
+    ta, tb = dev(A), dev(B)
+    with qx.Executor.gemm_i16i32(512, 640, 768, 1, 256, 256) as ex:
+        outs = [host(ex.run([ta, tb])) for _ in range(5)]
+    assert all(np.array_equal(o, outs[0]) for o in outs)
+    assert np.array_equal(outs[0][0], orc.gemm_i16i32(A, B))
+
+
+def test_executor_reuse_and_errors():
+    rng = np.random.default_rng(5)
+    with qx.Executor.gemm_i32_s24(100, 90, 80, 2) as ex:
+        for _ in range(3):
+            A = rng.integers(-(1 << 23), (1 << 23) - 1, (2, 100, 80), dtype=np.int32)
+            B = rng.integers(-(1 << 23), (1 << 23) - 1, (2, 80, 90), dtype=np.int32)
+            assert np.array_equal(run_exec(ex, (A, B)), orc.gemm_i32_s24(A, B))
+        t = torch.zeros(2 * 100 * 80 + 1, dtype=torch.int32, device="cuda")
+        with pytest.raises(qx.QxError) as e:          # misaligned input pointer
+            ex.run_ptrs([t.data_ptr() + 4, t.data_ptr()], t.data_ptr())
+        assert e.value.status == qx.ERR_INVALID_ARG
+
+
+# ---------------------------------------------------------------------------
+# Full-size workloads (the benchmark's launch configuration)
+# ---------------------------------------------------------------------------
+def freivalds(A, B, C, trials=3, seed=0):
+    """C[b] == A[b] B[b] exactly (int64), all elements covered w.h.p."""
+    rng = np.random.default_rng(seed)
+    for b in range(A.shape[0]):
+        for _ in range(trials):
+            r = rng.integers(0, 1 << 20, size=(C.shape[2],), dtype=np.int64)
+            lhs = C[b].astype(np.int64) @ r
+            rhs = A[b].astype(np.int64) @ (B[b].astype(np.int64) @ r)
+            if not np.array_equal(lhs, rhs):
+                return False
+    return True
+
+
+@pytest.mark.parametrize("name", ["gemm_i16_256", "gemm_s24_1024", "gemm_s24_16x512"])
+def test_workload_small_full_oracle(name):
+    w = WORKLOADS[name]
+    A, B = w.generate()
+    d = w.dims
+    _say(f"[{name}] full oracle")
+    if w.op == "gemm_i16i32":
+        ex = qx.Executor.gemm_i16i32(d["M"], d["N"], d["K"], d["batch"], w.bound, w.bound)
+        ref = orc.gemm_i16i32(A, B)
+    else:
+        ex = qx.Executor.gemm_i32_s24(d["M"], d["N"], d["K"], d["batch"])
+        ref = orc.gemm_i32_s24(A, B)
+    with ex:
+        got = run_exec(ex, (A, B))
+    assert np.array_equal(got, ref)
+
+
+def test_workload_conv_full_oracle():
+    w = WORKLOADS["conv_8x64x56x56_128_3x3"]
+    x, wt = w.generate()
+    d = w.dims
+    with qx.Executor.conv2d(d["N"], d["Ci"], d["H"], d["W"], d["Co"], d["KH"], d["KW"],
+                            d["stride"], d["pad"], w.bound, w.bound) as ex:
+        y = run_exec(ex, (x, wt))
+    assert np.array_equal(y, orc.conv2d_direct(x, wt, d["stride"], d["pad"]))
+
+
+def test_workload_attn_full_oracle():
+    wf = WORKLOADS["attn_f32_4096x64"]
+    Q, K, V = wf.generate()
+    with qx.Executor.attn("f32", 4096, 64) as ex:
+        O = run_exec(ex, (Q, K, V))
+    R = orc.attn_f64(Q, K, V)
+    err = normwise(O, R)
+    _say(f"[attn_f32_4096x64] normwise error {err:.3e}")
+    assert err <= 1e-4
+    wi = WORKLOADS["attn_i32_4096x64"]
+    Q, K, V = wi.generate()
+    with qx.Executor.attn("i32", 4096, 64, wi.bound) as ex:
+        O = run_exec(ex, (Q, K, V))
+    assert np.array_equal(O, orc.attn_i32(Q, K, V))
+
+
+@pytest.mark.parametrize("name", ["gemm_i16_8192", "gemm_i16_64x2048"])
+def test_workload_large_gemm(name):
+    w = WORKLOADS[name]
+    d = w.dims
+    _say(f"[{name}] generate")
+    A, B = w.generate()
+    with qx.Executor.gemm_i16i32(d["M"], d["N"], d["K"], d["batch"], w.bound, w.bound) as ex:
+        C = run_exec(ex, (A, B))
+    _say(f"[{name}] sampled rows against the oracle")
+    rng = np.random.default_rng(1)
+    batches = [0] if d["batch"] == 1 else [0, d["batch"] // 2, d["batch"] - 1]
+    for b in batches:
+        rows = np.sort(rng.choice(d["M"], size=16 if d["batch"] == 1 else 8, replace=False))
+        rows = np.unique(np.concatenate([rows, [0, d["M"] - 1]]))
+        ref = orc.gemm_i16i32(np.ascontiguousarray(A[b, rows]), B[b])
+        assert np.array_equal(C[b, rows], ref)
+    _say(f"[{name}] Freivalds over every batch")
+    sel = range(d["batch"]) if d["batch"] <= 64 else range(0, d["batch"], 8)
+    sel = list(sel)
+    assert freivalds(A[sel], B[sel], C[sel], trials=2)
