@@ -548,8 +548,15 @@ qx_status run_exec(qx_exec h, const void* const* inputs, void* output, void* str
     if (!h || h->magic != kMagic) return fail(QX_ERR_INVALID_ARG, "invalid executor handle");
     const Plan& pl = h->plan;
     if (pl.launches.empty()) return QX_OK;
-    if (!inputs) return fail(QX_ERR_INVALID_ARG, "inputs is NULL");
+    // Only inputs some launch reads are required (a K == 0 GEMM just clears
+    // its output and may get NULL operands).
+    unsigned used = 0;
+    for (const LaunchRec& r : pl.launches)
+        for (int i = 0; i < r.nslots; ++i)
+            if (r.slots[i].bind <= BIND_IN2) used |= 1u << r.slots[i].bind;
+    if (used && !inputs) return fail(QX_ERR_INVALID_ARG, "inputs is NULL");
     for (int i = 0; i < pl.n_inputs; ++i) {
+        if (!(used & (1u << i))) continue;
         if (!inputs[i]) return fail(QX_ERR_INVALID_ARG, "input %d is NULL", i);
         if ((uintptr_t)inputs[i] % pl.in_align)
             return fail(QX_ERR_INVALID_ARG, "input %d is not %llu-byte aligned", i, (unsigned long long)pl.in_align);

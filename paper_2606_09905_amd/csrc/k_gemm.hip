@@ -221,14 +221,16 @@ __global__ __launch_bounds__(NT) void k_gemm_f16x(const GemmParams p) {
 // ===========================================================================
 // A scheme splits each operand into PLANES int8 limbs, issues PRODUCTS limb
 // products into GROUPS accumulators, and recombines them mod 2^32.
+// PAD is the operand value whose limbs are all zero: padding a ragged K tail
+// with it adds nothing to any limb product.
 struct SchemeDirect {   // |x| <= 127
-    static constexpr int PLANES = 1, GROUPS = 1, PRODUCTS = 1;
+    static constexpr int PLANES = 1, GROUPS = 1, PRODUCTS = 1, PAD = 0;
     static constexpr int pa[1] = {0}, pb[1] = {0}, pg[1] = {0};
     template <class T> __device__ static void split(T x, uint32_t* l) { l[0] = (uint32_t)x & 0xFFu; }
     __device__ static uint32_t combine(const uint32_t* g) { return g[0]; }
 };
 struct SchemeKaratsuba {  // x in [-8256, 8127]: balanced base 128, h, l, h+l
-    static constexpr int PLANES = 3, GROUPS = 3, PRODUCTS = 3;
+    static constexpr int PLANES = 3, GROUPS = 3, PRODUCTS = 3, PAD = 0;
     static constexpr int pa[3] = {0, 1, 2}, pb[3] = {0, 1, 2}, pg[3] = {0, 1, 2};
     template <class T> __device__ static void split(T xv, uint32_t* l) {
         const int x = (int)xv;
@@ -244,7 +246,7 @@ struct SchemeKaratsuba {  // x in [-8256, 8127]: balanced base 128, h, l, h+l
     }
 };
 struct SchemeOffset4 {  // any int16: x = 256*s1 + s0 + 128, s1 = x>>8, s0 = (x & 255) - 128
-    static constexpr int PLANES = 2, GROUPS = 3, PRODUCTS = 4;
+    static constexpr int PLANES = 2, GROUPS = 3, PRODUCTS = 4, PAD = 128;
     static constexpr int pa[4] = {0, 0, 1, 1}, pb[4] = {0, 1, 0, 1}, pg[4] = {0, 1, 1, 2};
     template <class T> __device__ static void split(T xv, uint32_t* l) {
         const uint32_t x = (uint32_t)(int)xv;
@@ -254,7 +256,7 @@ struct SchemeOffset4 {  // any int16: x = 256*s1 + s0 + 128, s1 = x>>8, s0 = (x 
     __device__ static uint32_t combine(const uint32_t* g) { return (g[0] << 16) + (g[1] << 8) + g[2]; }
 };
 struct SchemeS24 {  // smul24: u = sext24(x) + 2^23, s_i = byte_i(u) - 128, x = sum 2^(8i) s_i + 32896
-    static constexpr int PLANES = 3, GROUPS = 4, PRODUCTS = 8;
+    static constexpr int PLANES = 3, GROUPS = 4, PRODUCTS = 8, PAD = 0x8080;
     static constexpr int pa[8] = {0, 0, 1, 0, 1, 2, 1, 2};
     static constexpr int pb[8] = {0, 1, 0, 2, 1, 0, 2, 1};
     static constexpr int pg[8] = {0, 1, 1, 2, 2, 2, 3, 3};
@@ -324,7 +326,7 @@ __global__ __launch_bounds__(NT) void k_gemm_i8limb(const GemmParams p) {
                 load_vec<T, 8>(src, ra[i]);
             } else {
 #pragma unroll
-                for (int e = 0; e < 8; ++e) ra[i][e] = (gm < p.M && gk + e < p.K) ? src[e] : (T)0;
+                for (int e = 0; e < 8; ++e) ra[i][e] = (gm < p.M && gk + e < p.K) ? src[e] : (T)S::PAD;
             }
         }
 #pragma unroll
@@ -335,7 +337,7 @@ __global__ __launch_bounds__(NT) void k_gemm_i8limb(const GemmParams p) {
                 load_vec<T, BWN>(src, rb[r]);
             } else {
 #pragma unroll
-                for (int e = 0; e < BWN; ++e) rb[r][e] = (gk < p.K && gn + e < p.N) ? src[e] : (T)0;
+                for (int e = 0; e < BWN; ++e) rb[r][e] = (gk < p.K && gn + e < p.N) ? src[e] : (T)S::PAD;
             }
         }
     };

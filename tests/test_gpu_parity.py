@@ -40,6 +40,17 @@ def run_exec(ex, inputs):
     return host(out)
 
 
+def same(got, ref, what=""):
+    """Bit-exact comparison that reports a short summary instead of arrays."""
+    got, ref = np.asarray(got), np.asarray(ref)
+    assert got.shape == ref.shape, f"{what} shape {got.shape} != {ref.shape}"
+    bad = np.flatnonzero(got.reshape(-1) != ref.reshape(-1))
+    if bad.size:
+        i = np.unravel_index(bad[0], got.shape)
+        raise AssertionError(f"{what} {bad.size} of {got.size} elements differ; first at {i}: "
+                             f"got {got[i]} expected {ref[i]}")
+
+
 def rand_int(rng, shape, b, dtype):
     return rng.integers(-b, b, size=shape, dtype=np.int64, endpoint=True).astype(dtype)
 
@@ -79,7 +90,7 @@ def test_gemm_i16_routes(route, bound, shape):
         assert ex.plan()["route_name"] == route
         got = run_exec(ex, (A, B))
     ref = orc.gemm_i16i32(A, B)
-    assert np.array_equal(got, ref)
+    same(got, ref)
 
 
 @pytest.mark.parametrize("route,bound", I16_ROUTES)
@@ -94,7 +105,7 @@ def test_gemm_i16_extremes(route, bound):
         A[0, ::3, ::2] = min(b, 32767)          # mix in the most positive value
         with qx.Executor.gemm_i16i32(64, 64, K, 1, bound, bb, route) as ex:
             got = run_exec(ex, (A, B))
-        assert np.array_equal(got, orc.gemm_i16i32(A, B)), (route, K)
+        same(got, orc.gemm_i16i32(A, B), str((route, K)))
 
 
 def test_f16_exact_mixed_magnitudes():
@@ -108,7 +119,7 @@ def test_f16_exact_mixed_magnitudes():
     A[0, 5, 1::4] = 255
     with qx.Executor.gemm_i16i32(64, 64, K, 1, 256, 256, "f16_exact") as ex:
         got = run_exec(ex, (A, B))
-    assert np.array_equal(got, orc.gemm_i16i32(A, B))
+    same(got, orc.gemm_i16i32(A, B))
 
 
 def test_gemm_i16_oneshot_and_empty():
@@ -116,7 +127,7 @@ def test_gemm_i16_oneshot_and_empty():
     A = rand_int(rng, (96, 80), 1024, np.int16)
     B = rand_int(rng, (80, 112), 1024, np.int16)
     C = host(qx.qgemm_i16i32(dev(A), dev(B), 1024, 1024))
-    assert np.array_equal(C, orc.gemm_i16i32(A, B))
+    same(C, orc.gemm_i16i32(A, B))
     # K == 0 -> zeros; M == 0 -> empty
     Z = qx.qgemm_i16i32(torch.empty((5, 0), dtype=torch.int16, device="cuda"),
                         torch.empty((0, 7), dtype=torch.int16, device="cuda"))
@@ -139,7 +150,7 @@ def test_gemm_s24_routes(route, shape):
     B = rng.integers(-(1 << 31), (1 << 31) - 1, (batch, K, N), dtype=np.int32, endpoint=True)
     with qx.Executor.gemm_i32_s24(M, N, K, batch, route) as ex:
         got = run_exec(ex, (A, B))
-    assert np.array_equal(got, orc.gemm_i32_s24(A, B))
+    same(got, orc.gemm_i32_s24(A, B))
 
 
 @pytest.mark.parametrize("route", ["s24_i8limb", "s24_valu"])
@@ -153,7 +164,7 @@ def test_gemm_s24_extremes_and_accumulator_wrap(route):
     B[0, :, 2] = 0x01000005
     with qx.Executor.gemm_i32_s24(32, 32, K, 1, route) as ex:
         got = run_exec(ex, (A, B))
-    assert np.array_equal(got, orc.gemm_i32_s24(A, B))
+    same(got, orc.gemm_i32_s24(A, B))
 
 
 # ---------------------------------------------------------------------------
@@ -174,7 +185,7 @@ def test_conv(case):
     x = rand_int(rng, (N, Ci, H, W), bx, np.int16)
     w = rand_int(rng, (Co, Ci, KH, KW), bx, np.int16)
     y = host(qx.conv2d_gemm(dev(x), dev(w), s, p, b, b))
-    assert np.array_equal(y, orc.conv2d_direct(x, w, s, p))
+    same(y, orc.conv2d_direct(x, w, s, p))
 
 
 # ---------------------------------------------------------------------------
@@ -203,7 +214,7 @@ def test_attn_i32_mfma(L, d, b):
     rng = np.random.default_rng(L * 3 + d + b)
     Q, K, V = (rand_int(rng, (L, d), b, np.int32) for _ in range(3))
     O = host(qx.attn_core(dev(Q), dev(K), dev(V), bound=b))
-    assert np.array_equal(O, orc.attn_i32(Q, K, V))
+    same(O, orc.attn_i32(Q, K, V))
 
 
 @pytest.mark.parametrize("L,d", [(1, 5), (40, 64), (129, 17)])
@@ -212,7 +223,7 @@ def test_attn_i32_valu_full_range(L, d):
     Q, K, V = (rng.integers(-(1 << 31), (1 << 31) - 1, (L, d), dtype=np.int32, endpoint=True)
                for _ in range(3))
     O = host(qx.attn_core(dev(Q), dev(K), dev(V), bound=0))
-    assert np.array_equal(O, orc.attn_i32(Q, K, V))
+    same(O, orc.attn_i32(Q, K, V))
 
 
 def test_attn_i32_extremes():
@@ -222,7 +233,7 @@ def test_attn_i32_extremes():
     V = np.full((L, d), b, np.int32)
     K[::2] = b
     O = host(qx.attn_core(dev(Q), dev(K), dev(V), bound=b))
-    assert np.array_equal(O, orc.attn_i32(Q, K, V))
+    same(O, orc.attn_i32(Q, K, V))
 
 
 # ---------------------------------------------------------------------------
@@ -235,14 +246,14 @@ def test_repeatable_bit_identical():
     tq, tk, tv = dev(Q), dev(K), dev(V)
     first = host(qx.attn_core(tq, tk, tv))
     for _ in range(5):
-        assert np.array_equal(host(qx.attn_core(tq, tk, tv)), first)
+        same(host(qx.attn_core(tq, tk, tv)), first)
     A = rand_int(rng, (512, 768), 256, np.int16)
     B = rand_int(rng, (768, 640), 256, np.int16)
     ta, tb = dev(A), dev(B)
     with qx.Executor.gemm_i16i32(512, 640, 768, 1, 256, 256) as ex:
         outs = [host(ex.run([ta, tb])) for _ in range(5)]
     assert all(np.array_equal(o, outs[0]) for o in outs)
-    assert np.array_equal(outs[0][0], orc.gemm_i16i32(A, B))
+    same(outs[0][0], orc.gemm_i16i32(A, B))
 
 
 def test_executor_reuse_and_errors():
@@ -251,7 +262,7 @@ def test_executor_reuse_and_errors():
         for _ in range(3):
             A = rng.integers(-(1 << 23), (1 << 23) - 1, (2, 100, 80), dtype=np.int32)
             B = rng.integers(-(1 << 23), (1 << 23) - 1, (2, 80, 90), dtype=np.int32)
-            assert np.array_equal(run_exec(ex, (A, B)), orc.gemm_i32_s24(A, B))
+            same(run_exec(ex, (A, B)), orc.gemm_i32_s24(A, B))
         t = torch.zeros(2 * 100 * 80 + 1, dtype=torch.int32, device="cuda")
         with pytest.raises(qx.QxError) as e:          # misaligned input pointer
             ex.run_ptrs([t.data_ptr() + 4, t.data_ptr()], t.data_ptr())
@@ -288,7 +299,7 @@ def test_workload_small_full_oracle(name):
         ref = orc.gemm_i32_s24(A, B)
     with ex:
         got = run_exec(ex, (A, B))
-    assert np.array_equal(got, ref)
+    same(got, ref)
 
 
 def test_workload_conv_full_oracle():
@@ -298,7 +309,7 @@ def test_workload_conv_full_oracle():
     with qx.Executor.conv2d(d["N"], d["Ci"], d["H"], d["W"], d["Co"], d["KH"], d["KW"],
                             d["stride"], d["pad"], w.bound, w.bound) as ex:
         y = run_exec(ex, (x, wt))
-    assert np.array_equal(y, orc.conv2d_direct(x, wt, d["stride"], d["pad"]))
+    same(y, orc.conv2d_direct(x, wt, d["stride"], d["pad"]))
 
 
 def test_workload_attn_full_oracle():
@@ -314,7 +325,7 @@ def test_workload_attn_full_oracle():
     Q, K, V = wi.generate()
     with qx.Executor.attn("i32", 4096, 64, wi.bound) as ex:
         O = run_exec(ex, (Q, K, V))
-    assert np.array_equal(O, orc.attn_i32(Q, K, V))
+    same(O, orc.attn_i32(Q, K, V))
 
 
 @pytest.mark.parametrize("name", ["gemm_i16_8192", "gemm_i16_64x2048"])
@@ -332,7 +343,7 @@ def test_workload_large_gemm(name):
         rows = np.sort(rng.choice(d["M"], size=16 if d["batch"] == 1 else 8, replace=False))
         rows = np.unique(np.concatenate([rows, [0, d["M"] - 1]]))
         ref = orc.gemm_i16i32(np.ascontiguousarray(A[b, rows]), B[b])
-        assert np.array_equal(C[b, rows], ref)
+        same(C[b, rows], ref)
     _say(f"[{name}] Freivalds over every batch")
     sel = range(d["batch"]) if d["batch"] <= 64 else range(0, d["batch"], 8)
     sel = list(sel)
