@@ -138,7 +138,19 @@ struct GemmSpec {
     uint64_t b_ws_off;   // when b_bind == BIND_WS
     int64_t lda, ldb, ldc, sA, sB, sC;
     int32_t out_mode, hw;
+    bool allow_nt;       // plain GEMM: large fp16-exact problems may take encode + NT GEMM
 };
+
+// The encode + direct-to-LDS route pays two HBM-bound encoding passes; it is
+// used when the contraction is large enough for them to be small change and
+// the chunk covers at least one 64-wide K tile.
+bool use_nt(int32_t route, int64_t chunk, int64_t M, int64_t N, int64_t K, int64_t batch) {
+    if (route != R_F16_EXACT || chunk < 64) return false;
+    const double macs = (double)M * (double)N * (double)K * (double)batch;
+    return macs >= (double)(1 << 24) && M >= 32 && N >= 32 && K >= 64;
+}
+
+int64_t pad_up(int64_t v, int64_t a) { return (v + a - 1) / a * a; }
 
 // Appends the launches of one integer GEMM; ws_used is the workspace end.
 qx_status plan_int_gemm(const GemmSpec& s, Plan* pl, uint64_t* ws_used) {
@@ -180,6 +192,51 @@ qx_status plan_int_gemm(const GemmSpec& s, Plan* pl, uint64_t* ws_used) {
         rec.bind(offsetof(ValuGemmParams, C), BIND_OUT);
         pl->launches.push_back(rec);
         info.tile_m = 64; info.tile_n = 64; info.tile_k = 16;
+        return QX_OK;
+    }
+
+    if (s.allow_nt && use_nt(route, f16_chunk(s.ba, s.bb), s.M, s.N, s.K, s.batch)) {
+        const int64_t chunk = f16_chunk(s.ba, s.bb);
+        int bm, bn;
+        nt_tile_shape(s.M, s.N, s.batch, &bm, &bn);
+        const int64_t Mp = pad_up(s.M, bm), Np = pad_up(s.N, bn), Kp = pad_up(s.K, 64);
+        const uint64_t a_off = round_up(*ws_used, 256);
+        const uint64_t b_off = round_up(a_off + 2 * (uint64_t)s.batch * Mp * Kp, 256);
+        *ws_used = b_off + 2 * (uint64_t)s.batch * Np * Kp;
+        EncParams ea{};
+        ea.s_src = s.sA; ea.s_dst = Mp * Kp;
+        ea.M = (int32_t)s.M; ea.N = 0; ea.K = (int32_t)s.K;
+        ea.Mp = (int32_t)Mp; ea.Np = 0; ea.Kp = (int32_t)Kp;
+        ea.ld_src = (int32_t)s.lda; ea.batch = (int32_t)s.batch;
+        LaunchRec r1;
+        build_enc_a(ea, &r1);
+        r1.bind(offsetof(EncParams, src), s.a_bind);
+        r1.bind(offsetof(EncParams, dst), BIND_WS, a_off);
+        EncParams eb{};
+        eb.s_src = s.sB; eb.s_dst = Np * Kp;
+        eb.M = 0; eb.N = (int32_t)s.N; eb.K = (int32_t)s.K;
+        eb.Mp = 0; eb.Np = (int32_t)Np; eb.Kp = (int32_t)Kp;
+        eb.ld_src = (int32_t)s.ldb; eb.batch = (int32_t)s.batch;
+        LaunchRec r2;
+        build_enc_bt(eb, &r2);
+        r2.bind(offsetof(EncParams, src), s.b_bind, s.b_ws_off);
+        r2.bind(offsetof(EncParams, dst), BIND_WS, b_off);
+        GemmParams g{};
+        g.sA = Mp * Kp; g.sB = Np * Kp; g.sC = s.sC;
+        g.M = (int32_t)s.M; g.N = (int32_t)s.N; g.K = (int32_t)Kp;
+        g.lda = (int32_t)Kp; g.ldb = (int32_t)Kp; g.ldc = (int32_t)s.ldc;
+        g.out_mode = s.out_mode; g.hw = s.hw; g.b_mode = B_KN;
+        g.chunk_tiles = (int32_t)(chunk / 64);
+        LaunchRec r3;
+        build_gemm_nt(g, (int)s.batch, &r3);
+        r3.bind(offsetof(GemmParams, A), BIND_WS, a_off);
+        r3.bind(offsetof(GemmParams, B), BIND_WS, b_off);
+        r3.bind(offsetof(GemmParams, C), BIND_OUT);
+        pl->launches.push_back(r1);
+        pl->launches.push_back(r2);
+        pl->launches.push_back(r3);
+        info.chunk = (int32_t)(chunk / 64 * 64);
+        info.tile_m = bm; info.tile_n = bn; info.tile_k = 64;
         return QX_OK;
     }
 
@@ -277,6 +334,7 @@ qx_status plan_gemm(Plan* pl, bool s24, int64_t M, int64_t N, int64_t K, int64_t
     s.a_bind = BIND_IN0; s.b_bind = BIND_IN1; s.b_ws_off = 0;
     s.lda = K; s.ldb = N; s.ldc = N; s.sA = M * K; s.sB = K * N; s.sC = M * N;
     s.out_mode = OUT_ROWMAJOR; s.hw = 1;
+    s.allow_nt = true;
     uint64_t ws = 0;
     Plan scratch;
     scratch.info = pl->info;
@@ -345,6 +403,49 @@ qx_status plan_conv(Plan* pl, int64_t N, int64_t Ci, int64_t H, int64_t W, int64
         add_fill_out(pl, N * Co * Ho * Wo);
         pl->info.kernels = 1;
         pl->info.workspace_bytes = 0;
+        return QX_OK;
+    }
+    if (use_nt(pl->info.route, f16_chunk(ba, bb), Co, P, Kd, 1)) {
+        // fp16-exact: weights encoded to fp16 [Mp][Kp], lowering written as
+        // the transposed fp16 column matrix [Pp][Kp], then the NT GEMM with
+        // an NCHW scatter epilogue.
+        const int64_t chunk = f16_chunk(ba, bb);
+        int bm, bn;
+        nt_tile_shape(Co, P, 1, &bm, &bn);
+        const int64_t Mp = pad_up(Co, bm), Pp = pad_up(P, bn), Kp = pad_up(Kd, 64);
+        const uint64_t b_off = round_up(2 * (uint64_t)Mp * Kp, 256);
+        const uint64_t wsz = b_off + 2 * (uint64_t)Pp * Kp;
+        EncParams ea{};
+        ea.s_src = 0; ea.s_dst = 0;
+        ea.M = (int32_t)Co; ea.K = (int32_t)Kd; ea.Mp = (int32_t)Mp; ea.Kp = (int32_t)Kp;
+        ea.ld_src = (int32_t)Kd; ea.batch = 1;
+        LaunchRec r1;
+        build_enc_a(ea, &r1);
+        r1.bind(offsetof(EncParams, src), BIND_IN1);
+        r1.bind(offsetof(EncParams, dst), BIND_WS, 0);
+        Im2colTParams it{};
+        it.P = (int32_t)P; it.Pp = (int32_t)Pp; it.Kd = (int32_t)Kd; it.Kp = (int32_t)Kp;
+        it.g = ConvGeom{(int32_t)Ci, (int32_t)H, (int32_t)W, (int32_t)KH, (int32_t)KW, (int32_t)stride,
+                        (int32_t)pad, (int32_t)Ho, (int32_t)Wo};
+        LaunchRec r2;
+        build_im2col_t(it, &r2);
+        r2.bind(offsetof(Im2colTParams, x), BIND_IN0);
+        r2.bind(offsetof(Im2colTParams, colT), BIND_WS, b_off);
+        GemmParams gp{};
+        gp.M = (int32_t)Co; gp.N = (int32_t)P; gp.K = (int32_t)Kp;
+        gp.lda = (int32_t)Kp; gp.ldb = (int32_t)Kp; gp.ldc = (int32_t)P;
+        gp.out_mode = OUT_CONV; gp.hw = (int32_t)(Ho * Wo); gp.b_mode = B_KN;
+        gp.chunk_tiles = (int32_t)(chunk / 64);
+        LaunchRec r3;
+        build_gemm_nt(gp, 1, &r3);
+        r3.bind(offsetof(GemmParams, A), BIND_WS, 0);
+        r3.bind(offsetof(GemmParams, B), BIND_WS, b_off);
+        r3.bind(offsetof(GemmParams, C), BIND_OUT);
+        pl->launches = {r1, r2, r3};
+        pl->info.chunk = (int32_t)(chunk / 64 * 64);
+        pl->info.tile_m = bm; pl->info.tile_n = bn; pl->info.tile_k = 64;
+        pl->info.kernels = 3;
+        pl->info.workspace_bytes = (int64_t)wsz;
         return QX_OK;
     }
     Im2colParams ip{};

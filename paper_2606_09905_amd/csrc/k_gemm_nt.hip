@@ -1,0 +1,338 @@
+// k_gemm_nt.hip -- the fp16-exact route for large contractions.
+//
+// Two stages:
+//  1. Encode (HBM-bound): int16 operands become fp16 copies in the
+//     workspace, A as [Mp][Kp] and B transposed as B^T [Np][Kp], both
+//     K-contiguous and zero-padded to whole tiles (zero adds nothing to any
+//     product).  Every int16 with |x| <= 2048 is exact in fp16.  For
+//     convolution the lowering writes the transposed fp16 column matrix
+//     directly (im2col, Methodology: convolution through lowering).
+//  2. Contract: a tiled GEMM on v_mfma_f32_32x32x16_f16.  Tiles are staged
+//     global -> LDS with global_load_lds_dwordx4 (no register staging) in a
+//     three-deep ring; each wave accumulates a 64x64 block in fp32 for
+//     `chunk` K elements, then converts and adds the partial into int32.
+//     With chunk * max|a| * max|b| <= 2^24 every partial sum is an integer
+//     fp32 holds exactly, whatever order the matrix core sums in; the int32
+//     sum is exact mod 2^32 (Table 1: INT16 input, INT32 accumulation).
+//
+// LDS layout: a stage holds rows of 64 fp16 as eight 16-byte chunks; chunk c
+// of row r sits at position c ^ ((r >> 1) & 7), so the 16 rows read by one
+// ds_read_b128 pass fall in distinct banks.  The swizzle is applied on the
+// global side (each lane fetches the chunk that belongs at its LDS slot).
+#include <algorithm>
+
+#include "qx_internal.h"
+
+namespace qx {
+
+typedef _Float16 h8 __attribute__((ext_vector_type(8)));
+typedef _Float16 h2 __attribute__((ext_vector_type(2)));
+typedef float f16x __attribute__((ext_vector_type(16)));
+typedef unsigned u16x __attribute__((ext_vector_type(16)));
+typedef short s8v __attribute__((ext_vector_type(8)));
+
+// ===========================================================================
+// Stage 1: encoders
+// ===========================================================================
+// A [batch][M][lda] int16 -> A16 [batch][Mp][Kp] fp16; one thread = 8 k.
+__global__ __launch_bounds__(256) void k_enc_a(const EncParams p) {
+    const int64_t v = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    const int kv = p.Kp / 8;
+    const int64_t per_b = (int64_t)p.Mp * kv;
+    if (v >= per_b * p.batch) return;
+    const int b = (int)(v / per_b);
+    const int64_t r = v - (int64_t)b * per_b;
+    const int m = (int)(r / kv), k0 = (int)(r - (int64_t)m * kv) * 8;
+    const int16_t* src = (const int16_t*)p.src + b * p.s_src + (int64_t)m * p.ld_src;
+    h8 out;
+#pragma unroll
+    for (int e = 0; e < 8; ++e)
+        out[e] = (m < p.M && k0 + e < p.K) ? (_Float16)src[k0 + e] : (_Float16)0.0f;
+    *(h8*)((_Float16*)p.dst + b * p.s_dst + (int64_t)m * p.Kp + k0) = out;
+}
+
+// B [batch][K][ldb] int16 -> BT16 [batch][Np][Kp] fp16 through a 64x64 LDS
+// transpose; reads are coalesced along n, writes along k.
+__global__ __launch_bounds__(256) void k_enc_bt(const EncParams p) {
+    __shared__ _Float16 t[64][64 + 2];
+    const int n0 = blockIdx.x * 64, k0 = blockIdx.y * 64, b = blockIdx.z;
+    const int16_t* src = (const int16_t*)p.src + b * p.s_src;
+    const int tid = threadIdx.x;
+    // read: 64 rows (k) x 64 columns (n), 16 elements per thread
+#pragma unroll
+    for (int q = 0; q < 16; ++q) {
+        const int idx = tid + 256 * q, kk = idx / 64, nn = idx % 64;
+        const int k = k0 + kk, n = n0 + nn;
+        t[nn][kk] = (k < p.K && n < p.N) ? (_Float16)src[(int64_t)k * p.ld_src + n] : (_Float16)0.0f;
+    }
+    __syncthreads();
+    // write: row n of BT gets 64 consecutive k; 8 per thread
+#pragma unroll
+    for (int q = 0; q < 2; ++q) {
+        const int idx = tid + 256 * q, nn = idx / 8, kc = (idx % 8) * 8;
+        h8 out;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) out[e] = t[nn][kc + e];
+        *(h8*)((_Float16*)p.dst + b * p.s_dst + (int64_t)(n0 + nn) * p.Kp + k0 + kc) = out;
+    }
+}
+
+// Convolution lowering straight into the transposed fp16 column matrix:
+// colT[p][k] = x[n, ci, oh*s-p+kh, ow*s-p+kw] (0 outside the image and in the
+// padding), p = (n*Ho + oh)*Wo + ow, k = (ci*KH + kh)*KW + kw.  One thread
+// writes 8 consecutive k of one pixel.
+__global__ __launch_bounds__(256) void k_im2col_t(const Im2colTParams p) {
+    const int64_t v = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    const int kv = p.Kp / 8;
+    if (v >= (int64_t)p.Pp * kv) return;
+    const int pix = (int)(v / kv), k0 = (int)(v - (int64_t)pix * kv) * 8;
+    const ConvGeom& g = p.g;
+    const int hw = g.Ho * g.Wo;
+    h8 out;
+    if (pix < p.P) {
+        const int n = pix / hw, rem = pix - n * hw;
+        const int oh = rem / g.Wo, ow = rem - oh * g.Wo;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+            const int k = k0 + e;
+            _Float16 val = (_Float16)0.0f;
+            if (k < p.Kd) {
+                const int kw = k % g.KW, kh = (k / g.KW) % g.KH, ci = k / (g.KW * g.KH);
+                const int ih = oh * g.stride - g.pad + kh, iw = ow * g.stride - g.pad + kw;
+                if (ih >= 0 && ih < g.H && iw >= 0 && iw < g.W)
+                    val = (_Float16)p.x[(((int64_t)n * g.Ci + ci) * g.H + ih) * g.W + iw];
+            }
+            out[e] = val;
+        }
+    } else {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) out[e] = (_Float16)0.0f;
+    }
+    *(h8*)(p.colT + (int64_t)pix * p.Kp + k0) = out;
+}
+
+// ===========================================================================
+// Stage 2: contraction
+// ===========================================================================
+__device__ __forceinline__ int chunk_swz(int r) { return (r >> 1) & 7; }
+
+template <int BM, int BN, int NW>
+__global__ __launch_bounds__(NW * 64) void k_gemm_nt(const GemmParams p) {
+    constexpr int BK = 64, KCH = 8, WM = 64, WN = 64;
+    constexpr int TM = WM / 32, TN = WN / 32;
+    constexpr int WAVES_N = BN / WN;
+    static_assert((BM / WM) * (BN / WN) == NW, "wave grid");
+    constexpr int NTH = NW * 64;
+    constexpr int AL = BM * KCH / NTH, BL = BN * KCH / NTH, LPT = AL + BL;
+    static_assert(AL * NTH == BM * KCH && BL * NTH == BN * KCH, "whole loads");
+    constexpr int STAGES = 3;
+    constexpr unsigned STAGE_A = BM * KCH * 16, STAGE_B = BN * KCH * 16;
+    __shared__ h8 As[STAGES][BM][KCH];
+    __shared__ h8 Bs[STAGES][BN][KCH];
+
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, l32 = lane & 31, hh = lane >> 5;
+    const int wm = wave / WAVES_N, wn = wave % WAVES_N;
+    // Workgroup -> tile: consecutive ids go to different XCDs, so first
+    // gather each XCD's ids into one contiguous range, then walk tiles in
+    // groups of 8 tile-rows (neighbouring workgroups share B panels).
+    const int tiles_m = (p.M + BM - 1) / BM, tiles_n = p.tiles_n;
+    int pid = blockIdx.x;
+    const int total = gridDim.x;
+    if ((total & 7) == 0) pid = (pid & 7) * (total >> 3) + (pid >> 3);
+    int tm, tn;
+    {
+        constexpr int G = 8;
+        const int per_group = G * tiles_n;
+        const int gid = pid / per_group;
+        const int first_m = gid * G;
+        const int gsz = min(tiles_m - first_m, G);
+        const int in = pid - gid * per_group;
+        tm = first_m + in % gsz;
+        tn = in / gsz;
+    }
+    const int m0 = tm * BM, n0 = tn * BN;
+    const int b = blockIdx.z;
+    const _Float16* A = (const _Float16*)p.A + b * p.sA;   // [Mp][lda], lda = Kp
+    const _Float16* B = (const _Float16*)p.B + b * p.sB;   // [Np][ldb], ldb = Kp
+    int32_t* C = (int32_t*)p.C + b * p.sC;
+
+    // Per-thread byte offsets of the chunks it fetches, relative to the panel.
+    unsigned oa[AL], ob[BL];
+#pragma unroll
+    for (int i = 0; i < AL; ++i) {
+        const int q = tid + NTH * i, row = q / KCH, pc = q % KCH;
+        oa[i] = (unsigned)((row * p.lda + (pc ^ chunk_swz(row)) * 8) * 2);
+    }
+#pragma unroll
+    for (int i = 0; i < BL; ++i) {
+        const int q = tid + NTH * i, row = q / KCH, pc = q % KCH;
+        ob[i] = (unsigned)((row * p.ldb + (pc ^ chunk_swz(row)) * 8) * 2);
+    }
+    const char* a_panel = (const char*)(A + (int64_t)m0 * p.lda);
+    const char* b_panel = (const char*)(B + (int64_t)n0 * p.ldb);
+    const unsigned wave_u = __builtin_amdgcn_readfirstlane(wave);
+    const unsigned lds_a0 = (unsigned)(uintptr_t)&As[0][0][0] + wave_u * 1024;
+    const unsigned lds_b0 = (unsigned)(uintptr_t)&Bs[0][0][0] + wave_u * 1024;
+    // One wave-wide global_load_lds_dwordx4 writes 64 lanes x 16 bytes
+    // contiguously at M0; the lane -> global chunk mapping realises the swizzle.
+    auto issue = [&](int t) {
+        const int s = t % STAGES;
+        const char* ab = a_panel + t * BK * 2;
+        const char* bb = b_panel + t * BK * 2;
+        const unsigned la = lds_a0 + s * STAGE_A, lb = lds_b0 + s * STAGE_B;
+#pragma unroll
+        for (int i = 0; i < AL; ++i)
+            asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dwordx4 %0, %1"
+                         :: "v"(oa[i]), "s"(ab), "s"(la + NTH * 16 * i) : "memory", "m0");
+#pragma unroll
+        for (int i = 0; i < BL; ++i)
+            asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dwordx4 %0, %1"
+                         :: "v"(ob[i]), "s"(bb), "s"(lb + NTH * 16 * i) : "memory", "m0");
+    };
+
+    f16x acc[TM][TN];
+    u16x iacc[TM][TN];
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j) iacc[i][j] = u16x{};
+
+    // K-slot (lane half h, element e) of the MFMA is k = 16*ks + 8*h + e for
+    // both operands.
+    auto compute = [&](int s, bool first) {
+#pragma unroll
+        for (int ks = 0; ks < BK / 16; ++ks) {
+            h8 a[TM], bv[TN];
+            const int c = ks * 2 + hh;
+#pragma unroll
+            for (int i = 0; i < TM; ++i) {
+                const int row = wm * WM + i * 32 + l32;
+                a[i] = As[s][row][c ^ chunk_swz(row)];
+            }
+#pragma unroll
+            for (int j = 0; j < TN; ++j) {
+                const int col = wn * WN + j * 32 + l32;
+                bv[j] = Bs[s][col][c ^ chunk_swz(col)];
+            }
+#pragma unroll
+            for (int i = 0; i < TM; ++i)
+#pragma unroll
+                for (int j = 0; j < TN; ++j)
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_f16(a[i], bv[j],
+                                    (first && ks == 0) ? f16x{} : acc[i][j], 0, 0, 0);
+        }
+    };
+
+    const int ktiles = p.K / BK;   // K is padded to whole tiles
+    const int CT = p.chunk_tiles;
+#pragma unroll
+    for (int s = 0; s < STAGES - 1; ++s)
+        if (s < ktiles) issue(s);
+    int t = 0;
+    while (t < ktiles) {
+        const int cend = min(t + CT, ktiles);
+        for (int tc = t; tc < cend; ++tc) {
+            // Tile tc must have landed; the next one may still be in flight.
+            if (tc + 1 < ktiles) __builtin_amdgcn_s_waitcnt((LPT & 15) | ((LPT >> 4) << 14) | 0x0F70);
+            else __builtin_amdgcn_s_waitcnt(0x0F70);
+            __syncthreads();
+            if (tc + STAGES - 1 < ktiles) issue(tc + STAGES - 1);
+            compute(tc % STAGES, tc == t);
+        }
+        t = cend;
+#pragma unroll
+        for (int i = 0; i < TM; ++i)
+#pragma unroll
+            for (int j = 0; j < TN; ++j)
+#pragma unroll
+                for (int r = 0; r < 16; ++r) iacc[i][j][r] += (uint32_t)(int32_t)acc[i][j][r];
+    }
+
+    // 32x32 accumulator layout: lane holds column (lane & 31), rows
+    // 8*(r/4) + 4*(lane/32) + r%4.
+#pragma unroll
+    for (int j = 0; j < TN; ++j) {
+        const int gn = n0 + wn * WN + j * 32 + l32;
+        if (gn >= p.N) continue;
+        int64_t col_off;
+        int64_t row_stride;
+        if (p.out_mode == OUT_ROWMAJOR) {
+            col_off = gn;
+            row_stride = p.ldc;
+        } else {
+            const int img = gn / p.hw, pix = gn - img * p.hw;
+            col_off = (int64_t)img * p.M * p.hw + pix;
+            row_stride = p.hw;
+        }
+#pragma unroll
+        for (int i = 0; i < TM; ++i)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+                const int gm = m0 + wm * WM + i * 32 + 8 * (r >> 2) + 4 * hh + (r & 3);
+                if (gm < p.M) C[(int64_t)gm * row_stride + col_off] = (int32_t)iacc[i][j][r];
+            }
+    }
+}
+
+// ===========================================================================
+// Builders
+// ===========================================================================
+void nt_tile_shape(int64_t M, int64_t N, int64_t batch, int* bm, int* bn) {
+    // 128x256 (8 waves) when there are enough tiles to fill the chip,
+    // otherwise 128x128 (4 waves).
+    const int64_t big = ((M + 127) / 128) * ((N + 255) / 256) * batch;
+    if (big >= 512) {
+        *bm = 128;
+        *bn = 256;
+    } else {
+        *bm = 128;
+        *bn = 128;
+    }
+}
+
+void build_gemm_nt(const GemmParams& p0, int batch, LaunchRec* rec) {
+    int bm, bn;
+    nt_tile_shape(p0.M, p0.N, batch, &bm, &bn);
+    GemmParams p = p0;
+    const int tiles_m = (p.M + bm - 1) / bm;
+    p.tiles_n = (p.N + bn - 1) / bn;
+    rec->grid = dim3((unsigned)(tiles_m * p.tiles_n), 1, (unsigned)batch);
+    if (bn == 256) {
+        rec->fn = (const void*)k_gemm_nt<128, 256, 8>;
+        rec->block = dim3(512, 1, 1);
+        rec->name = "gemm_nt_128x256";
+    } else {
+        rec->fn = (const void*)k_gemm_nt<128, 128, 4>;
+        rec->block = dim3(256, 1, 1);
+        rec->name = "gemm_nt_128x128";
+    }
+    rec->set_params(p);
+}
+
+void build_enc_a(const EncParams& p, LaunchRec* rec) {
+    const int64_t n = (int64_t)p.batch * p.Mp * (p.Kp / 8);
+    rec->fn = (const void*)k_enc_a;
+    rec->grid = dim3((unsigned)((n + 255) / 256), 1, 1);
+    rec->block = dim3(256, 1, 1);
+    rec->name = "enc_a_f16";
+    rec->set_params(p);
+}
+
+void build_enc_bt(const EncParams& p, LaunchRec* rec) {
+    rec->fn = (const void*)k_enc_bt;
+    rec->grid = dim3((unsigned)(p.Np / 64), (unsigned)(p.Kp / 64), (unsigned)p.batch);
+    rec->block = dim3(256, 1, 1);
+    rec->name = "enc_bt_f16";
+    rec->set_params(p);
+}
+
+void build_im2col_t(const Im2colTParams& p, LaunchRec* rec) {
+    const int64_t n = (int64_t)p.Pp * (p.Kp / 8);
+    rec->fn = (const void*)k_im2col_t;
+    rec->grid = dim3((unsigned)((n + 255) / 256), 1, 1);
+    rec->block = dim3(256, 1, 1);
+    rec->name = "im2col_t_f16";
+    rec->set_params(p);
+}
+
+}  // namespace qx

@@ -72,6 +72,26 @@ struct Im2colParams {
     ConvGeom g;
 };
 
+// int16 -> fp16 operand encoders of the large-problem fp16-exact route.
+struct EncParams {
+    const void* src;        // int16 [batch][rows][ld_src]
+    void* dst;              // fp16 [batch][Mp|Np][Kp], zero padded
+    int64_t s_src, s_dst;   // batch strides (elements)
+    int32_t M, N, K;        // logical extents (A: M x K, B: K x N)
+    int32_t Mp, Np, Kp;     // padded extents
+    int32_t ld_src;
+    int32_t batch;
+};
+
+// Convolution lowering into the transposed fp16 column matrix colT [Pp][Kp].
+struct Im2colTParams {
+    const int16_t* x;
+    _Float16* colT;
+    int32_t P, Pp;          // N*Ho*Wo and its padded extent
+    int32_t Kd, Kp;         // Ci*KH*KW and its padded extent
+    ConvGeom g;
+};
+
 // Attention core O = (Q K^T) V.
 struct AttnParams {
     const void* Q;
@@ -175,5 +195,11 @@ bool build_attn_f32(const AttnParams& p, LaunchRec* rec);
 bool build_attn_i32(const AttnParams& p, LaunchRec* rec);
 void build_reduce(const ReduceParams& p, LaunchRec* rec);
 void build_fill(const FillParams& p, LaunchRec* rec);
+// fp16-exact route for large problems: encoders + direct-to-LDS NT GEMM.
+void nt_tile_shape(int64_t M, int64_t N, int64_t batch, int* bm, int* bn);
+void build_gemm_nt(const GemmParams& p, int batch, LaunchRec* rec);
+void build_enc_a(const EncParams& p, LaunchRec* rec);
+void build_enc_bt(const EncParams& p, LaunchRec* rec);
+void build_im2col_t(const Im2colTParams& p, LaunchRec* rec);
 
 }  // namespace qx

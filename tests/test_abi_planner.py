@@ -26,13 +26,16 @@ def test_auto_routes_for_the_workloads():
         d = w[name].dims
         p = qx.plan_gemm_i16i32(d["M"], d["N"], d["K"], d["batch"], 256, 256)
         assert p["route_name"] == "f16_exact" and p["chunk"] == 256 and p["exact_no_wrap"] == 1
-        assert p["workspace_bytes"] == 0 and p["kernels"] == 1
+        # encode A, encode B^T, contract: the fp16 copies live in the workspace
+        assert p["kernels"] == 3
+        assert p["workspace_bytes"] == 2 * 2 * d["M"] * d["K"] * d["batch"]
     p = qx.plan_gemm_i32_s24(1024, 1024, 1024, 1)
     assert p["route_name"] == "s24_i8limb" and p["products"] == 8 and p["exact_no_wrap"] == 0
     assert p["workspace_bytes"] >= 4 * 2048
     d = w["conv_8x64x56x56_128_3x3"].dims
     p = qx.plan_conv2d(d["N"], d["Ci"], d["H"], d["W"], d["Co"], d["KH"], d["KW"], 1, 1, 256, 256)
-    assert p["route_name"] == "f16_exact" and p["kernels"] == 2
+    # encode weights, lower to the transposed fp16 column matrix, contract
+    assert p["route_name"] == "f16_exact" and p["kernels"] == 3
     assert p["workspace_bytes"] >= 2 * 576 * 8 * 56 * 56
     assert qx.plan_attn("f32", 4096, 64)["route_name"] == "attn_f32_mfma"
     p = qx.plan_attn("i32", 4096, 64, 64)

@@ -108,6 +108,26 @@ def test_gemm_i16_extremes(route, bound):
         same(got, orc.gemm_i16i32(A, B), str((route, K)))
 
 
+@pytest.mark.parametrize("shape,bound", [
+    ((300, 520, 200, 2), 256), ((1000, 300, 136, 1), 128), ((257, 129, 1000, 1), 300),
+    ((64, 1024, 4096, 1), 256), ((513, 2000, 520, 3), 512), ((128, 25088, 576, 1), 256),
+])
+def test_gemm_i16_encode_nt_path(shape, bound):
+    # Large enough for the encode + direct-to-LDS route; ragged in M, N, K;
+    # chunks of 256, 1024, 128 (bound 300) and 64 (bound 512) K elements.
+    M, N, K, batch = shape
+    rng = np.random.default_rng(zlib.crc32(repr((shape, bound)).encode()))
+    A = rand_int(rng, (batch, M, K), bound, np.int16)
+    B = rand_int(rng, (batch, K, N), bound, np.int16)
+    A[0, 0, :] = -bound
+    B[0, :, 0] = -bound
+    with qx.Executor.gemm_i16i32(M, N, K, batch, bound, bound) as ex:
+        plan = ex.plan()
+        assert plan["route_name"] == "f16_exact" and plan["kernels"] == 3, plan
+        got = run_exec(ex, (A, B))
+    same(got, orc.gemm_i16i32(A, B))
+
+
 def test_f16_exact_mixed_magnitudes():
     # Products alternating between 2^16 and 1 inside one fp32 partial sum:
     # a narrow internal adder would lose the small terms.
