@@ -164,6 +164,15 @@ qx_status qx_exec_run(qx_exec h, const void* const* inputs, void* output, void* 
 /* The plan a handle carries. */
 qx_status qx_exec_plan(qx_exec h, qx_plan_info* out);
 
+/* Execute-only timing (Methodology: separating setup, cached steady state
+ * and execute-only kernel time): enqueue `reps` runs on `stream` with a HIP
+ * event pair around every launch, wait for them, and write the mean duration
+ * in milliseconds of launch i of the plan to kernel_ms[i] for i < min(kernels,
+ * max_kernels); names[i] (if names is not NULL) receives a static kernel name.
+ * Synchronises `stream`.  Not for use under graph capture. */
+qx_status qx_exec_profile(qx_exec h, const void* const* inputs, void* output, void* stream,
+                          int32_t reps, float* kernel_ms, const char** names, int32_t max_kernels);
+
 /* Free the workspace and the handle (waits for the device to finish any
  * work that may use the workspace).  NULL is accepted. */
 qx_status qx_exec_destroy(qx_exec h);

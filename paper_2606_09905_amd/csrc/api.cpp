@@ -13,6 +13,7 @@
 // dispatch metadata).
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <cstdarg>
 #include <cstdio>
 #include <map>
@@ -645,7 +646,8 @@ qx_status make_exec(Plan&& pl, qx_exec* out) {
     return QX_OK;
 }
 
-qx_status run_exec(qx_exec h, const void* const* inputs, void* output, void* stream) {
+qx_status run_exec(qx_exec h, const void* const* inputs, void* output, void* stream,
+                   std::vector<hipEvent_t>* evs = nullptr) {
     if (!h || h->magic != kMagic) return fail(QX_ERR_INVALID_ARG, "invalid executor handle");
     const Plan& pl = h->plan;
     if (pl.launches.empty()) return QX_OK;
@@ -684,10 +686,55 @@ qx_status run_exec(qx_exec h, const void* const* inputs, void* output, void* str
             memcpy(r.blob + sl.off, &ptr, sizeof(void*));
         }
         void* args[1] = {r.blob};
+        const size_t li = (size_t)(&r0 - pl.launches.data());
+        if (evs && (e = hipEventRecord((*evs)[2 * li], s)) != hipSuccess) return hip_fail(e, "hipEventRecord");
         e = hipLaunchKernel(r.fn, r.grid, r.block, args, r.shmem, s);
         if (e != hipSuccess) return hip_fail(e, r.name);
+        if (evs && (e = hipEventRecord((*evs)[2 * li + 1], s)) != hipSuccess) return hip_fail(e, "hipEventRecord");
     }
     return QX_OK;
+}
+
+qx_status profile_exec(qx_exec h, const void* const* inputs, void* output, void* stream, int32_t reps,
+                       float* kernel_ms, const char** names, int32_t max_kernels) {
+    if (!h || h->magic != kMagic) return fail(QX_ERR_INVALID_ARG, "invalid executor handle");
+    if (reps < 1 || max_kernels < 0 || (max_kernels > 0 && !kernel_ms))
+        return fail(QX_ERR_INVALID_ARG, "reps must be >= 1 and kernel_ms non-NULL");
+    const size_t nl = h->plan.launches.size();
+    const int nout = (int)std::min<size_t>(nl, (size_t)max_kernels);
+    for (int i = 0; i < nout; ++i) {
+        kernel_ms[i] = 0.0f;
+        if (names) names[i] = h->plan.launches[i].name;
+    }
+    if (nl == 0) return QX_OK;
+    std::vector<hipEvent_t> evs(2 * nl * (size_t)reps, nullptr);
+    qx_status st = QX_OK;
+    hipError_t e = hipSuccess;
+    for (auto& ev : evs)
+        if ((e = hipEventCreate(&ev)) != hipSuccess) break;
+    if (e != hipSuccess) {
+        st = hip_fail(e, "hipEventCreate");
+    } else {
+        for (int r = 0; r < reps && st == QX_OK; ++r) {
+            std::vector<hipEvent_t> sub(evs.begin() + 2 * nl * r, evs.begin() + 2 * nl * (r + 1));
+            st = run_exec(h, inputs, output, stream, &sub);
+        }
+        if (st == QX_OK && (e = hipStreamSynchronize((hipStream_t)stream)) != hipSuccess)
+            st = hip_fail(e, "hipStreamSynchronize");
+        for (int r = 0; r < reps && st == QX_OK; ++r)
+            for (int i = 0; i < nout; ++i) {
+                float ms = 0.0f;
+                if ((e = hipEventElapsedTime(&ms, evs[2 * nl * r + 2 * i], evs[2 * nl * r + 2 * i + 1])) !=
+                    hipSuccess) {
+                    st = hip_fail(e, "hipEventElapsedTime");
+                    break;
+                }
+                kernel_ms[i] += ms / (float)reps;
+            }
+    }
+    for (auto& ev : evs)
+        if (ev) (void)hipEventDestroy(ev);
+    return st;
 }
 
 // One-shot calls: a cache of executors keyed by the full request.
@@ -819,6 +866,12 @@ qx_status qx_exec_create_attn(qx_exec* out, qx_attn_dtype dt, int64_t L, int64_t
 qx_status qx_exec_run(qx_exec h, const void* const* inputs, void* output, void* stream) {
     g_err.clear();
     return run_exec(h, inputs, output, stream);
+}
+
+qx_status qx_exec_profile(qx_exec h, const void* const* inputs, void* output, void* stream, int32_t reps,
+                          float* kernel_ms, const char** names, int32_t max_kernels) {
+    g_err.clear();
+    return profile_exec(h, inputs, output, stream, reps, kernel_ms, names, max_kernels);
 }
 
 qx_status qx_exec_plan(qx_exec h, qx_plan_info* out) {

@@ -74,6 +74,7 @@ def lib() -> ctypes.CDLL:
             "qx_exec_create_attn": [_p, _i32, _i64, _i64, _i32, _i32],
             "qx_exec_run": [_p, _p, _p, _p],
             "qx_exec_plan": [_p, _p],
+            "qx_exec_profile": [_p, _p, _p, _p, _i32, _p, _p, _i32],
             "qx_exec_destroy": [_p],
             "qx_plan_gemm_i16i32": [_p, _i64, _i64, _i64, _i64, _i32, _i32, _i32],
             "qx_plan_gemm_i32_s24": [_p, _i64, _i64, _i64, _i64, _i32],
@@ -317,6 +318,16 @@ class Executor:
             raise ValueError("bad output tensor")
         self.run_ptrs(ptrs, out.data_ptr(), stream)
         return out
+
+    def profile(self, inputs, out, reps: int = 10, stream=None) -> list:
+        """Mean execute-only duration (ms) of every launch: [(kernel, ms), ...]."""
+        nk = self.plan()["kernels"]
+        ms = (ctypes.c_float * max(nk, 1))()
+        names = (ctypes.c_char_p * max(nk, 1))()
+        arr = (ctypes.c_void_p * len(inputs))(*[ctypes.c_void_p(t.data_ptr()) for t in inputs])
+        check(lib().qx_exec_profile(self._h, arr, ctypes.c_void_p(out.data_ptr()), _stream(stream),
+                                    int(reps), ms, names, nk))
+        return [(names[i].decode(), float(ms[i])) for i in range(nk)]
 
     def close(self) -> None:
         if self._h:

@@ -276,6 +276,19 @@ def test_repeatable_bit_identical():
     same(outs[0][0], orc.gemm_i16i32(A, B))
 
 
+def test_executor_profile_times_every_launch():
+    rng = np.random.default_rng(8)
+    A = rand_int(rng, (1, 512, 1024), 256, np.int16)
+    B = rand_int(rng, (1, 1024, 768), 256, np.int16)
+    ta, tb = dev(A), dev(B)
+    out = torch.empty((1, 512, 768), dtype=torch.int32, device="cuda")
+    with qx.Executor.gemm_i16i32(512, 768, 1024, 1, 256, 256) as ex:
+        prof = ex.profile([ta, tb], out, reps=3)
+    assert [n for n, _ in prof] == ["enc_a_f16", "enc_bt_f16", "gemm_nt_128x128"]
+    assert all(ms > 0 for _, ms in prof)
+    same(host(out), orc.gemm_i16i32(A, B))
+
+
 def test_executor_reuse_and_errors():
     rng = np.random.default_rng(5)
     with qx.Executor.gemm_i32_s24(100, 90, 80, 2) as ex:
