@@ -209,6 +209,7 @@ qx_status plan_int_gemm(const GemmSpec& s, Plan* pl, uint64_t* ws_used) {
         ea.M = (int32_t)s.M; ea.N = 0; ea.K = (int32_t)s.K;
         ea.Mp = (int32_t)Mp; ea.Np = 0; ea.Kp = (int32_t)Kp;
         ea.ld_src = (int32_t)s.lda; ea.batch = (int32_t)s.batch;
+        ea.vec = (s.lda % 8 == 0 && s.sA % 8 == 0) ? 1 : 0;
         LaunchRec r1;
         build_enc_a(ea, &r1);
         r1.bind(offsetof(EncParams, src), s.a_bind);
@@ -218,6 +219,7 @@ qx_status plan_int_gemm(const GemmSpec& s, Plan* pl, uint64_t* ws_used) {
         eb.M = 0; eb.N = (int32_t)s.N; eb.K = (int32_t)s.K;
         eb.Mp = 0; eb.Np = (int32_t)Np; eb.Kp = (int32_t)Kp;
         eb.ld_src = (int32_t)s.ldb; eb.batch = (int32_t)s.batch;
+        eb.vec = (s.ldb % 8 == 0 && s.sB % 8 == 0) ? 1 : 0;
         LaunchRec r2;
         build_enc_bt(eb, &r2);
         r2.bind(offsetof(EncParams, src), s.b_bind, s.b_ws_off);
@@ -258,13 +260,22 @@ qx_status plan_int_gemm(const GemmSpec& s, Plan* pl, uint64_t* ws_used) {
         sp.M = (int32_t)s.M; sp.N = (int32_t)s.N; sp.K = (int32_t)s.K;
         sp.lda = (int32_t)s.lda; sp.ldb = (int32_t)s.ldb;
         sp.s24 = s.s24 ? 1 : 0; sp.batch = (int32_t)s.batch;
-        LaunchRec rec;
-        build_sums(sp, &rec);
-        rec.bind(offsetof(SumsParams, A), s.a_bind);
-        rec.bind(offsetof(SumsParams, B), s.b_bind, s.b_ws_off);
-        rec.bind(offsetof(SumsParams, rowsum), BIND_WS, rs_off);
-        rec.bind(offsetof(SumsParams, colsum), BIND_WS, cs_off);
-        pl->launches.push_back(rec);
+        FillParams f{};
+        f.n32 = s.batch * s.N;
+        LaunchRec rf;
+        build_fill(f, &rf);
+        rf.bind(offsetof(FillParams, ptr), BIND_WS, cs_off);
+        LaunchRec rr;
+        build_rowsum(sp, &rr);
+        rr.bind(offsetof(SumsParams, A), s.a_bind);
+        rr.bind(offsetof(SumsParams, rowsum), BIND_WS, rs_off);
+        LaunchRec rc;
+        build_colsum(sp, &rc);
+        rc.bind(offsetof(SumsParams, B), s.b_bind, s.b_ws_off);
+        rc.bind(offsetof(SumsParams, colsum), BIND_WS, cs_off);
+        pl->launches.push_back(rf);
+        pl->launches.push_back(rr);
+        pl->launches.push_back(rc);
     }
     if (route == R_F16_EXACT) {
         const int64_t chunk = f16_chunk(s.ba, s.bb);
@@ -420,6 +431,7 @@ qx_status plan_conv(Plan* pl, int64_t N, int64_t Ci, int64_t H, int64_t W, int64
         ea.s_src = 0; ea.s_dst = 0;
         ea.M = (int32_t)Co; ea.K = (int32_t)Kd; ea.Mp = (int32_t)Mp; ea.Kp = (int32_t)Kp;
         ea.ld_src = (int32_t)Kd; ea.batch = 1;
+        ea.vec = Kd % 8 == 0 ? 1 : 0;
         LaunchRec r1;
         build_enc_a(ea, &r1);
         r1.bind(offsetof(EncParams, src), BIND_IN1);
@@ -572,10 +584,16 @@ qx_status plan_attn(Plan* pl, qx_attn_dtype dt, int64_t L, int64_t d, int32_t bo
             SumsParams sp{};
             sp.M = 0; sp.N = (int32_t)d; sp.K = (int32_t)L; sp.lda = 0; sp.ldb = (int32_t)d;
             sp.s24 = 1; sp.batch = 1;
+            FillParams f{};
+            f.n32 = d;
+            LaunchRec rf;
+            build_fill(f, &rf);
+            rf.bind(offsetof(FillParams, ptr), BIND_WS, 0);
             LaunchRec rs;
-            build_sums(sp, &rs);
+            build_colsum(sp, &rs);
             rs.bind(offsetof(SumsParams, B), BIND_IN2);
             rs.bind(offsetof(SumsParams, colsum), BIND_WS, 0);
+            pl->launches.push_back(rf);
             pl->launches.push_back(rs);
             if (splits > 1) add_fill_out(pl, L * d);
             build_attn_i32(a, &rec);

@@ -449,34 +449,50 @@ __global__ __launch_bounds__(NT) void k_gemm_i8limb(const GemmParams p) {
 // ===========================================================================
 // Row / column sums for the rank-1 correction of offset limb routes.
 // ===========================================================================
-__global__ __launch_bounds__(NT) void k_sums(const SumsParams p) {
-    // blockIdx.y == 0: row sums of A (one wave per row); == 1: column sums of B.
+// Row sums of A: one wave per row, lanes stride along the contiguous K.
+__global__ __launch_bounds__(NT) void k_rowsum(const SumsParams p) {
     const int b = blockIdx.z;
-    if (blockIdx.y == 0) {
-        const int row = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
-        if (row >= p.M) return;
-        uint32_t s = 0;
-        if (p.s24) {
-            const int32_t* a = (const int32_t*)p.A + b * p.sA + (int64_t)row * p.lda;
-            for (int k = lane; k < p.K; k += 64) s += (uint32_t)((int32_t)((uint32_t)a[k] << 8) >> 8);
-        } else {
-            const int16_t* a = (const int16_t*)p.A + b * p.sA + (int64_t)row * p.lda;
-            for (int k = lane; k < p.K; k += 64) s += (uint32_t)(int32_t)a[k];
-        }
-        for (int off = 32; off > 0; off >>= 1) s += __shfl_xor(s, off, 64);
-        if (lane == 0) p.rowsum[(int64_t)b * p.M + row] = (int32_t)s;
+    const int row = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
+    if (row >= p.M) return;
+    uint32_t s = 0;
+    if (p.s24) {
+        const int32_t* a = (const int32_t*)p.A + b * p.sA + (int64_t)row * p.lda;
+        for (int k = lane; k < p.K; k += 64) s += (uint32_t)((int32_t)((uint32_t)a[k] << 8) >> 8);
     } else {
-        const int col = blockIdx.x * NT + threadIdx.x;
-        if (col >= p.N) return;
-        uint32_t s = 0;
+        const int16_t* a = (const int16_t*)p.A + b * p.sA + (int64_t)row * p.lda;
+        for (int k = lane; k < p.K; k += 64) s += (uint32_t)(int32_t)a[k];
+    }
+    for (int off = 32; off > 0; off >>= 1) s += __shfl_xor(s, off, 64);
+    if (lane == 0) p.rowsum[(int64_t)b * p.M + row] = (int32_t)s;
+}
+
+// Column sums of B [K][ldb]: a block covers 64 columns x 256 rows (4 row
+// groups of 64 threads, coalesced along the row), reduces in LDS and adds
+// its slice into the zero-filled column sums with integer atomics (exact and
+// order-independent mod 2^32).
+__global__ __launch_bounds__(NT) void k_colsum(const SumsParams p) {
+    __shared__ uint32_t part[4][64];
+    const int b = blockIdx.z;
+    const int c = threadIdx.x & 63, g = threadIdx.x >> 6;
+    const int col = blockIdx.x * 64 + c;
+    const int k0 = blockIdx.y * 256;
+    const int k1 = min(k0 + 256, p.K);
+    uint32_t s = 0;
+    if (col < p.N) {
         if (p.s24) {
             const int32_t* bb = (const int32_t*)p.B + b * p.sB + col;
-            for (int k = 0; k < p.K; ++k) s += (uint32_t)((int32_t)((uint32_t)bb[(int64_t)k * p.ldb] << 8) >> 8);
+            for (int k = k0 + g; k < k1; k += 4)
+                s += (uint32_t)((int32_t)((uint32_t)bb[(int64_t)k * p.ldb] << 8) >> 8);
         } else {
             const int16_t* bb = (const int16_t*)p.B + b * p.sB + col;
-            for (int k = 0; k < p.K; ++k) s += (uint32_t)(int32_t)bb[(int64_t)k * p.ldb];
+            for (int k = k0 + g; k < k1; k += 4) s += (uint32_t)(int32_t)bb[(int64_t)k * p.ldb];
         }
-        p.colsum[(int64_t)b * p.N + col] = (int32_t)s;
+    }
+    part[g][c] = s;
+    __syncthreads();
+    if (g == 0 && col < p.N) {
+        const uint32_t t = part[0][c] + part[1][c] + part[2][c] + part[3][c];
+        atomicAdd((unsigned*)&p.colsum[(int64_t)b * p.N + col], t);
     }
 }
 
@@ -573,12 +589,20 @@ bool build_gemm_mfma(int32_t route, const GemmParams& p, int batch, LaunchRec* r
     }
 }
 
-void build_sums(const SumsParams& p, LaunchRec* rec) {
-    const int gx = std::max((p.M + 3) / 4, (p.N + NT - 1) / NT);
-    rec->fn = (const void*)k_sums;
-    rec->grid = dim3((unsigned)std::max(gx, 1), 2, (unsigned)p.batch);
+void build_rowsum(const SumsParams& p, LaunchRec* rec) {
+    rec->fn = (const void*)k_rowsum;
+    rec->grid = dim3((unsigned)std::max((p.M + 3) / 4, 1), 1, (unsigned)p.batch);
     rec->block = dim3(NT, 1, 1);
-    rec->name = "rowcol_sums";
+    rec->name = "rowsum";
+    rec->set_params(p);
+}
+
+void build_colsum(const SumsParams& p, LaunchRec* rec) {
+    rec->fn = (const void*)k_colsum;
+    rec->grid = dim3((unsigned)std::max((p.N + 63) / 64, 1), (unsigned)std::max((p.K + 255) / 256, 1),
+                     (unsigned)p.batch);
+    rec->block = dim3(NT, 1, 1);
+    rec->name = "colsum";
     rec->set_params(p);
 }
 

@@ -34,46 +34,67 @@ typedef short s8v __attribute__((ext_vector_type(8)));
 // ===========================================================================
 // Stage 1: encoders
 // ===========================================================================
-// A [batch][M][lda] int16 -> A16 [batch][Mp][Kp] fp16; one thread = 8 k.
-__global__ __launch_bounds__(256) void k_enc_a(const EncParams p) {
-    const int64_t v = (int64_t)blockIdx.x * 256 + threadIdx.x;
-    const int kv = p.Kp / 8;
-    const int64_t per_b = (int64_t)p.Mp * kv;
-    if (v >= per_b * p.batch) return;
-    const int b = (int)(v / per_b);
-    const int64_t r = v - (int64_t)b * per_b;
-    const int m = (int)(r / kv), k0 = (int)(r - (int64_t)m * kv) * 8;
-    const int16_t* src = (const int16_t*)p.src + b * p.s_src + (int64_t)m * p.ld_src;
-    h8 out;
+// 8 int16 -> 8 fp16 (exact for |x| <= 2048).
+__device__ __forceinline__ h8 to_h8(s8v v) {
+    h8 o;
 #pragma unroll
-    for (int e = 0; e < 8; ++e)
-        out[e] = (m < p.M && k0 + e < p.K) ? (_Float16)src[k0 + e] : (_Float16)0.0f;
-    *(h8*)((_Float16*)p.dst + b * p.s_dst + (int64_t)m * p.Kp + k0) = out;
+    for (int e = 0; e < 8; ++e) o[e] = (_Float16)v[e];
+    return o;
 }
 
-// B [batch][K][ldb] int16 -> BT16 [batch][Np][Kp] fp16 through a 64x64 LDS
-// transpose; reads are coalesced along n, writes along k.
+// A [batch][M][lda] int16 -> A16 [batch][Mp][Kp] fp16; one thread = 8 k,
+// four vectors per thread.
+__global__ __launch_bounds__(256) void k_enc_a(const EncParams p) {
+    const int kv = p.Kp / 8;
+    const int64_t per_b = (int64_t)p.Mp * kv;
+    const int64_t total = per_b * p.batch;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+        const int64_t v = ((int64_t)blockIdx.x * 4 + q) * 256 + threadIdx.x;
+        if (v >= total) return;
+        const int b = (int)(v / per_b);
+        const int64_t r = v - (int64_t)b * per_b;
+        const int m = (int)(r / kv), k0 = (int)(r - (int64_t)m * kv) * 8;
+        const int16_t* src = (const int16_t*)p.src + b * p.s_src + (int64_t)m * p.ld_src + k0;
+        h8 out;
+        if (p.vec && m < p.M && k0 + 8 <= p.K) {
+            out = to_h8(*(const s8v*)src);
+        } else {
+#pragma unroll
+            for (int e = 0; e < 8; ++e)
+                out[e] = (m < p.M && k0 + e < p.K) ? (_Float16)src[e] : (_Float16)0.0f;
+        }
+        *(h8*)((_Float16*)p.dst + b * p.s_dst + (int64_t)m * p.Kp + k0) = out;
+    }
+}
+
+// B [batch][K][ldb] int16 -> BT16 [batch][Np][Kp] fp16 through a 64(k) x
+// 128(n) LDS transpose; 16-byte reads along n and 16-byte writes along k.
 __global__ __launch_bounds__(256) void k_enc_bt(const EncParams p) {
-    __shared__ _Float16 t[64][64 + 2];
-    const int n0 = blockIdx.x * 64, k0 = blockIdx.y * 64, b = blockIdx.z;
+    __shared__ __attribute__((aligned(16))) _Float16 t[128][64 + 8];
+    const int n0 = blockIdx.x * 128, k0 = blockIdx.y * 64, b = blockIdx.z;
     const int16_t* src = (const int16_t*)p.src + b * p.s_src;
     const int tid = threadIdx.x;
-    // read: 64 rows (k) x 64 columns (n), 16 elements per thread
 #pragma unroll
-    for (int q = 0; q < 16; ++q) {
-        const int idx = tid + 256 * q, kk = idx / 64, nn = idx % 64;
-        const int k = k0 + kk, n = n0 + nn;
-        t[nn][kk] = (k < p.K && n < p.N) ? (_Float16)src[(int64_t)k * p.ld_src + n] : (_Float16)0.0f;
+    for (int q = 0; q < 4; ++q) {
+        const int idx = tid + 256 * q, kk = idx / 16, nv = (idx % 16) * 8;
+        const int k = k0 + kk, n = n0 + nv;
+        const int16_t* s = src + (int64_t)k * p.ld_src + n;
+        h8 h;
+        if (p.vec && k < p.K && n + 8 <= p.N) {
+            h = to_h8(*(const s8v*)s);
+        } else {
+#pragma unroll
+            for (int e = 0; e < 8; ++e) h[e] = (k < p.K && n + e < p.N) ? (_Float16)s[e] : (_Float16)0.0f;
+        }
+#pragma unroll
+        for (int e = 0; e < 8; ++e) t[nv + e][kk] = h[e];
     }
     __syncthreads();
-    // write: row n of BT gets 64 consecutive k; 8 per thread
 #pragma unroll
-    for (int q = 0; q < 2; ++q) {
+    for (int q = 0; q < 4; ++q) {
         const int idx = tid + 256 * q, nn = idx / 8, kc = (idx % 8) * 8;
-        h8 out;
-#pragma unroll
-        for (int e = 0; e < 8; ++e) out[e] = t[nn][kc + e];
-        *(h8*)((_Float16*)p.dst + b * p.s_dst + (int64_t)(n0 + nn) * p.Kp + k0 + kc) = out;
+        *(h8*)((_Float16*)p.dst + b * p.s_dst + (int64_t)(n0 + nn) * p.Kp + k0 + kc) = *(const h8*)&t[nn][kc];
     }
 }
 
@@ -312,7 +333,7 @@ void build_gemm_nt(const GemmParams& p0, int batch, LaunchRec* rec) {
 void build_enc_a(const EncParams& p, LaunchRec* rec) {
     const int64_t n = (int64_t)p.batch * p.Mp * (p.Kp / 8);
     rec->fn = (const void*)k_enc_a;
-    rec->grid = dim3((unsigned)((n + 255) / 256), 1, 1);
+    rec->grid = dim3((unsigned)((n + 1023) / 1024), 1, 1);
     rec->block = dim3(256, 1, 1);
     rec->name = "enc_a_f16";
     rec->set_params(p);
@@ -320,7 +341,7 @@ void build_enc_a(const EncParams& p, LaunchRec* rec) {
 
 void build_enc_bt(const EncParams& p, LaunchRec* rec) {
     rec->fn = (const void*)k_enc_bt;
-    rec->grid = dim3((unsigned)(p.Np / 64), (unsigned)(p.Kp / 64), (unsigned)p.batch);
+    rec->grid = dim3((unsigned)(p.Np / 128), (unsigned)(p.Kp / 64), (unsigned)p.batch);
     rec->block = dim3(256, 1, 1);
     rec->name = "enc_bt_f16";
     rec->set_params(p);

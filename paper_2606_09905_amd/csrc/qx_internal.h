@@ -81,6 +81,7 @@ struct EncParams {
     int32_t Mp, Np, Kp;     // padded extents
     int32_t ld_src;
     int32_t batch;
+    int32_t vec;            // rows and batch strides allow 16-byte source loads
 };
 
 // Convolution lowering into the transposed fp16 column matrix colT [Pp][Kp].
@@ -188,7 +189,8 @@ enum Route : int32_t {
 // Integer GEMM main kernel for an MFMA route; returns false if unsupported.
 bool build_gemm_mfma(int32_t route, const GemmParams& p, int batch, LaunchRec* rec,
                      int* tile_m, int* tile_n, int* tile_k);
-void build_sums(const SumsParams& p, LaunchRec* rec);
+void build_rowsum(const SumsParams& p, LaunchRec* rec);
+void build_colsum(const SumsParams& p, LaunchRec* rec);   // adds into a zeroed colsum
 void build_im2col(const Im2colParams& p, LaunchRec* rec);
 void build_valu_gemm(int32_t kind, const ValuGemmParams& p, int batch, LaunchRec* rec);
 bool build_attn_f32(const AttnParams& p, LaunchRec* rec);
