@@ -252,30 +252,23 @@ qx_status plan_int_gemm(const GemmSpec& s, Plan* pl, uint64_t* ws_used) {
     uint64_t rs_off = 0, cs_off = 0;
     if (offset) {
         g.corr_c = route == R_I8_OFFSET4 ? 128 : 32896;
+        const int slices = sums_slices((int)s.K);
+        g.cs_slices = slices;
         rs_off = round_up(*ws_used, 256);
         cs_off = round_up(rs_off + 4 * (uint64_t)s.batch * (uint64_t)s.M, 256);
-        *ws_used = cs_off + 4 * (uint64_t)s.batch * (uint64_t)s.N;
+        *ws_used = cs_off + 4 * (uint64_t)s.batch * (uint64_t)slices * (uint64_t)s.N;
         SumsParams sp{};
         sp.sA = s.sA; sp.sB = s.sB;
         sp.M = (int32_t)s.M; sp.N = (int32_t)s.N; sp.K = (int32_t)s.K;
         sp.lda = (int32_t)s.lda; sp.ldb = (int32_t)s.ldb;
         sp.s24 = s.s24 ? 1 : 0; sp.batch = (int32_t)s.batch;
-        FillParams f{};
-        f.n32 = s.batch * s.N;
-        LaunchRec rf;
-        build_fill(f, &rf);
-        rf.bind(offsetof(FillParams, ptr), BIND_WS, cs_off);
         LaunchRec rr;
-        build_rowsum(sp, &rr);
+        build_sums(sp, &rr);
         rr.bind(offsetof(SumsParams, A), s.a_bind);
+        rr.bind(offsetof(SumsParams, B), s.b_bind, s.b_ws_off);
         rr.bind(offsetof(SumsParams, rowsum), BIND_WS, rs_off);
-        LaunchRec rc;
-        build_colsum(sp, &rc);
-        rc.bind(offsetof(SumsParams, B), s.b_bind, s.b_ws_off);
-        rc.bind(offsetof(SumsParams, colsum), BIND_WS, cs_off);
-        pl->launches.push_back(rf);
+        rr.bind(offsetof(SumsParams, colsum), BIND_WS, cs_off);
         pl->launches.push_back(rr);
-        pl->launches.push_back(rc);
     }
     if (route == R_F16_EXACT) {
         const int64_t chunk = f16_chunk(s.ba, s.bb);
@@ -578,30 +571,14 @@ qx_status plan_attn(Plan* pl, qx_attn_dtype dt, int64_t L, int64_t d, int32_t bo
                 pl->launches.push_back(rec);
             }
         } else {
-            // column sums of V (the offset limbs' correction), then the
-            // output cleared for split accumulation, then the kernel.
-            ws = 4 * (uint64_t)d;
-            SumsParams sp{};
-            sp.M = 0; sp.N = (int32_t)d; sp.K = (int32_t)L; sp.lda = 0; sp.ldb = (int32_t)d;
-            sp.s24 = 1; sp.batch = 1;
-            FillParams f{};
-            f.n32 = d;
-            LaunchRec rf;
-            build_fill(f, &rf);
-            rf.bind(offsetof(FillParams, ptr), BIND_WS, 0);
-            LaunchRec rs;
-            build_colsum(sp, &rs);
-            rs.bind(offsetof(SumsParams, B), BIND_IN2);
-            rs.bind(offsetof(SumsParams, colsum), BIND_WS, 0);
-            pl->launches.push_back(rf);
-            pl->launches.push_back(rs);
+            // the output cleared for split accumulation, then the kernel
+            // (which also forms the V column sums of the offset correction)
             if (splits > 1) add_fill_out(pl, L * d);
             build_attn_i32(a, &rec);
             rec.bind(offsetof(AttnParams, Q), BIND_IN0);
             rec.bind(offsetof(AttnParams, K), BIND_IN1);
             rec.bind(offsetof(AttnParams, V), BIND_IN2);
             rec.bind(offsetof(AttnParams, O), BIND_OUT);
-            rec.bind(offsetof(AttnParams, vcs), BIND_WS, 0);
             pl->launches.push_back(rec);
         }
         info.tile_m = 128; info.tile_n = (int32_t)d; info.tile_k = (int32_t)kps;
@@ -658,6 +635,16 @@ qx_status make_exec(Plan&& pl, qx_exec* out) {
             delete h;
             (void)hipGetLastError();
             return hip_fail(e, "workspace hipMalloc");
+        }
+        // Zero once: padding that no run writes (tile tails of the encoded
+        // operands) must hold finite zeros.
+        e = hipMemset(h->ws, 0, h->ws_bytes);
+        if (e == hipSuccess) e = hipDeviceSynchronize();
+        if (e != hipSuccess) {
+            (void)hipFree(h->ws);
+            h->magic = 0;
+            delete h;
+            return hip_fail(e, "workspace clear");
         }
     }
     *out = h;

@@ -180,6 +180,14 @@ __global__ __launch_bounds__(AT) void k_attn_i32(const AttnParams p) {
 #pragma unroll
         for (int n = 0; n < NTO; ++n) o[j][n] = i16x{};
 
+    // Column sums of V over this split's keys, for the offset correction.
+    __shared__ uint32_t vsum[D];
+    if (tid < D) vsum[tid] = 0u;
+    __syncthreads();
+    uint32_t vpart[KW];
+#pragma unroll
+    for (int i = 0; i < KW; ++i) vpart[i] = 0u;
+
     uint32_t rk[KW], rv[KW];
     auto load = [&](int kb) {
 #pragma unroll
@@ -197,6 +205,7 @@ __global__ __launch_bounds__(AT) void k_attn_i32(const AttnParams p) {
                 const int key2 = kb + kq * 4 + e;
                 const uint32_t x = key2 < key_hi ? (uint32_t)Vp[(int64_t)key2 * D + col] : 0u;
                 w |= (x & 0xFFu) << (8 * e);
+                vpart[i] += x;
             }
             rv[i] = w;
         }
@@ -243,11 +252,16 @@ __global__ __launch_bounds__(AT) void k_attn_i32(const AttnParams p) {
         }
     }
 
+#pragma unroll
+    for (int i = 0; i < KW; ++i) atomicAdd(&vsum[(tid + AT * i) % D], vpart[i]);
+    __syncthreads();
+
     int32_t* O = (int32_t*)p.O;
 #pragma unroll
     for (int n = 0; n < NTO; ++n) {
         const int c = n * 32 + l32;
-        const uint32_t corr = split == 0 ? 32896u * (uint32_t)p.vcs[c] : 0u;
+        // every split adds 32896 * sum over its own keys of V[key][c]
+        const uint32_t corr = 32896u * vsum[c];
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
             const int q = q0 + 8 * (r >> 2) + 4 * h + (r & 3);

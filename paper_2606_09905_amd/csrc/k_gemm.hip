@@ -427,31 +427,73 @@ __global__ __launch_bounds__(NT) void k_gemm_i8limb(const GemmParams p) {
     const uint32_t cc = (uint32_t)p.corr_c;
     const uint32_t kcc = (uint32_t)p.K * cc * cc;
     const int32_t* rs = p.rowsum ? p.rowsum + (int64_t)b * p.M : nullptr;
-    const int32_t* cs = p.colsum ? p.colsum + (int64_t)b * p.N : nullptr;
+    // column sums arrive as cs_slices partial rows [slice][N]
+    const int32_t* cs = p.colsum ? p.colsum + (int64_t)b * p.cs_slices * p.N : nullptr;
 #pragma unroll
-    for (int i = 0; i < TM; ++i)
+    for (int j = 0; j < TN; ++j) {
+        const int gn = n0 + wn * WN + j * 32 + (lane & 31);
+        if (gn >= p.N) continue;
+        uint32_t csum = 0;
+        if (cc)
+            for (int s = 0; s < p.cs_slices; ++s) csum += (uint32_t)cs[(int64_t)s * p.N + gn];
 #pragma unroll
-        for (int j = 0; j < TN; ++j)
+        for (int i = 0; i < TM; ++i)
 #pragma unroll
             for (int r = 0; r < 16; ++r) {
                 const int gm = m0 + wm * WM + i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
-                const int gn = n0 + wn * WN + j * 32 + (lane & 31);
-                if (gm >= p.M || gn >= p.N) continue;
+                if (gm >= p.M) continue;
                 uint32_t g[G];
 #pragma unroll
                 for (int q = 0; q < G; ++q) g[q] = (uint32_t)acc[q][i][j][r];
                 uint32_t v = S::combine(g);
-                if (cc) v += cc * ((uint32_t)rs[gm] + (uint32_t)cs[gn]) - kcc;
+                if (cc) v += cc * ((uint32_t)rs[gm] + csum) - kcc;
                 store_c(p, C, gm, gn, v);
             }
+    }
 }
 
 // ===========================================================================
 // Row / column sums for the rank-1 correction of offset limb routes.
 // ===========================================================================
-// Row sums of A: one wave per row, lanes stride along the contiguous K.
-__global__ __launch_bounds__(NT) void k_rowsum(const SumsParams p) {
+// Row sums of A (blockIdx.y == 0: one wave per row, lanes stride along the
+// contiguous K) and per-slice column sums of B (blockIdx.y == 1: a block
+// covers 64 columns x SUM_SLICE rows, 4 row groups of 64 threads coalesced
+// along the row, reduced in LDS).  Column partials go to colsum[b][slice][N];
+// consumers add the slices, so no atomics and no clearing are needed.
+constexpr int SUM_SLICE = 64;
+
+__global__ __launch_bounds__(NT) void k_sums(const SumsParams p) {
+    __shared__ uint32_t part[4][64];
     const int b = blockIdx.z;
+    if (blockIdx.y == 1) {
+        if (p.N <= 0) return;
+        const int ncb = (p.N + 63) / 64;
+        const int cb = blockIdx.x % ncb, slice = blockIdx.x / ncb;
+        const int k0 = slice * SUM_SLICE;
+        if (k0 >= p.K) return;                      // whole block: uniform exit
+        const int c = threadIdx.x & 63, g = threadIdx.x >> 6;
+        const int col = cb * 64 + c;
+        const int k1 = min(k0 + SUM_SLICE, p.K);
+        uint32_t s = 0;
+        if (col < p.N) {
+            if (p.s24) {
+                const int32_t* bb = (const int32_t*)p.B + b * p.sB + col;
+                for (int k = k0 + g; k < k1; k += 4)
+                    s += (uint32_t)((int32_t)((uint32_t)bb[(int64_t)k * p.ldb] << 8) >> 8);
+            } else {
+                const int16_t* bb = (const int16_t*)p.B + b * p.sB + col;
+                for (int k = k0 + g; k < k1; k += 4) s += (uint32_t)(int32_t)bb[(int64_t)k * p.ldb];
+            }
+        }
+        part[g][c] = s;
+        __syncthreads();
+        if (g == 0 && col < p.N) {
+            const int slices = (p.K + SUM_SLICE - 1) / SUM_SLICE;
+            p.colsum[((int64_t)b * slices + slice) * p.N + col] =
+                (int32_t)(part[0][c] + part[1][c] + part[2][c] + part[3][c]);
+        }
+        return;
+    }
     const int row = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
     if (row >= p.M) return;
     uint32_t s = 0;
@@ -464,36 +506,6 @@ __global__ __launch_bounds__(NT) void k_rowsum(const SumsParams p) {
     }
     for (int off = 32; off > 0; off >>= 1) s += __shfl_xor(s, off, 64);
     if (lane == 0) p.rowsum[(int64_t)b * p.M + row] = (int32_t)s;
-}
-
-// Column sums of B [K][ldb]: a block covers 64 columns x 256 rows (4 row
-// groups of 64 threads, coalesced along the row), reduces in LDS and adds
-// its slice into the zero-filled column sums with integer atomics (exact and
-// order-independent mod 2^32).
-__global__ __launch_bounds__(NT) void k_colsum(const SumsParams p) {
-    __shared__ uint32_t part[4][64];
-    const int b = blockIdx.z;
-    const int c = threadIdx.x & 63, g = threadIdx.x >> 6;
-    const int col = blockIdx.x * 64 + c;
-    const int k0 = blockIdx.y * 256;
-    const int k1 = min(k0 + 256, p.K);
-    uint32_t s = 0;
-    if (col < p.N) {
-        if (p.s24) {
-            const int32_t* bb = (const int32_t*)p.B + b * p.sB + col;
-            for (int k = k0 + g; k < k1; k += 4)
-                s += (uint32_t)((int32_t)((uint32_t)bb[(int64_t)k * p.ldb] << 8) >> 8);
-        } else {
-            const int16_t* bb = (const int16_t*)p.B + b * p.sB + col;
-            for (int k = k0 + g; k < k1; k += 4) s += (uint32_t)(int32_t)bb[(int64_t)k * p.ldb];
-        }
-    }
-    part[g][c] = s;
-    __syncthreads();
-    if (g == 0 && col < p.N) {
-        const uint32_t t = part[0][c] + part[1][c] + part[2][c] + part[3][c];
-        atomicAdd((unsigned*)&p.colsum[(int64_t)b * p.N + col], t);
-    }
 }
 
 // ===========================================================================
@@ -589,20 +601,15 @@ bool build_gemm_mfma(int32_t route, const GemmParams& p, int batch, LaunchRec* r
     }
 }
 
-void build_rowsum(const SumsParams& p, LaunchRec* rec) {
-    rec->fn = (const void*)k_rowsum;
-    rec->grid = dim3((unsigned)std::max((p.M + 3) / 4, 1), 1, (unsigned)p.batch);
-    rec->block = dim3(NT, 1, 1);
-    rec->name = "rowsum";
-    rec->set_params(p);
-}
+int sums_slices(int K) { return std::max((K + SUM_SLICE - 1) / SUM_SLICE, 1); }
 
-void build_colsum(const SumsParams& p, LaunchRec* rec) {
-    rec->fn = (const void*)k_colsum;
-    rec->grid = dim3((unsigned)std::max((p.N + 63) / 64, 1), (unsigned)std::max((p.K + 255) / 256, 1),
-                     (unsigned)p.batch);
+void build_sums(const SumsParams& p, LaunchRec* rec) {
+    const int row_blocks = (p.M + 3) / 4;
+    const int col_blocks = ((p.N + 63) / 64) * sums_slices(p.K);
+    rec->fn = (const void*)k_sums;
+    rec->grid = dim3((unsigned)std::max(std::max(row_blocks, col_blocks), 1), 2, (unsigned)p.batch);
     rec->block = dim3(NT, 1, 1);
-    rec->name = "colsum";
+    rec->name = "rowcol_sums";
     rec->set_params(p);
 }
 

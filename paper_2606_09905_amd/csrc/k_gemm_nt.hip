@@ -132,6 +132,45 @@ __global__ __launch_bounds__(256) void k_im2col_t(const Im2colTParams p) {
     *(h8*)(p.colT + (int64_t)pix * p.Kp + k0) = out;
 }
 
+// The same lowering when C_in is a multiple of 8: a block owns one output
+// row (n, oh) and 8 input channels; it stages the KH input rows those need
+// (zero outside the image) in LDS, coalesced along W, then writes for every
+// ow the 8*KH*KW consecutive k of its channel group as 16-byte stores.
+__global__ __launch_bounds__(256) void k_im2col_t8(const Im2colTParams p) {
+    extern __shared__ _Float16 xs[];   // [8][KH][Wp], Wp = (Wo-1)*stride + KW
+    const ConvGeom& g = p.g;
+    const int oh = blockIdx.x, cg = blockIdx.y, n = blockIdx.z;
+    const int ci0 = cg * 8;
+    const int Wp = (g.Wo - 1) * g.stride + g.KW;
+    const int tid = threadIdx.x;
+    const int total = 8 * g.KH * Wp;
+    for (int idx = tid; idx < total; idx += 256) {
+        const int c = idx / (g.KH * Wp), rem = idx - c * g.KH * Wp;
+        const int kh = rem / Wp, iwp = rem - kh * Wp;
+        const int ih = oh * g.stride - g.pad + kh, iw = iwp - g.pad;
+        _Float16 v = (_Float16)0.0f;
+        if (ih >= 0 && ih < g.H && iw >= 0 && iw < g.W)
+            v = (_Float16)p.x[(((int64_t)n * g.Ci + ci0 + c) * g.H + ih) * g.W + iw];
+        xs[idx] = v;
+    }
+    __syncthreads();
+    const int kk = g.KH * g.KW;              // chunks of 8 k per pixel and group
+    const int chunks = g.Wo * kk;
+    const int64_t row0 = ((int64_t)n * g.Ho + oh) * g.Wo;
+    for (int idx = tid; idx < chunks; idx += 256) {
+        const int ow = idx / kk, q = idx - ow * kk;
+        h8 out;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+            const int kl = 8 * q + e;            // k within the group: c*KH*KW + kh*KW + kw
+            const int c = kl / kk, r = kl - c * kk;
+            const int kh = r / g.KW, kw = r - kh * g.KW;
+            out[e] = xs[(c * g.KH + kh) * Wp + ow * g.stride + kw];
+        }
+        *(h8*)(p.colT + (row0 + ow) * p.Kp + ci0 * kk + 8 * q) = out;
+    }
+}
+
 // ===========================================================================
 // Stage 2: contraction
 // ===========================================================================
@@ -302,11 +341,15 @@ void nt_tile_shape(int64_t M, int64_t N, int64_t batch, int* bm, int* bn) {
     // 128x256 (8 waves) when there are enough tiles to fill the chip,
     // otherwise 128x128 (4 waves).
     const int64_t big = ((M + 127) / 128) * ((N + 255) / 256) * batch;
+    const int64_t mid = ((M + 127) / 128) * ((N + 127) / 128) * batch;
     if (big >= 512) {
         *bm = 128;
         *bn = 256;
-    } else {
+    } else if (mid >= 256) {
         *bm = 128;
+        *bn = 128;
+    } else {
+        *bm = 64;     // two 64x64 waves per workgroup: more workgroups for small M
         *bn = 128;
     }
 }
@@ -322,6 +365,10 @@ void build_gemm_nt(const GemmParams& p0, int batch, LaunchRec* rec) {
         rec->fn = (const void*)k_gemm_nt<128, 256, 8>;
         rec->block = dim3(512, 1, 1);
         rec->name = "gemm_nt_128x256";
+    } else if (bm == 64) {
+        rec->fn = (const void*)k_gemm_nt<64, 128, 2>;
+        rec->block = dim3(128, 1, 1);
+        rec->name = "gemm_nt_64x128";
     } else {
         rec->fn = (const void*)k_gemm_nt<128, 128, 4>;
         rec->block = dim3(256, 1, 1);
@@ -348,6 +395,18 @@ void build_enc_bt(const EncParams& p, LaunchRec* rec) {
 }
 
 void build_im2col_t(const Im2colTParams& p, LaunchRec* rec) {
+    const ConvGeom& g = p.g;
+    const int Wp = (g.Wo - 1) * g.stride + g.KW;
+    const size_t lds = (size_t)8 * g.KH * Wp * 2;
+    if (g.Ci % 8 == 0 && lds <= 32768 && g.Ho <= 65535 && g.Ci / 8 <= 65535) {
+        rec->fn = (const void*)k_im2col_t8;
+        rec->grid = dim3((unsigned)g.Ho, (unsigned)(g.Ci / 8), (unsigned)(p.P / (g.Ho * g.Wo)));
+        rec->block = dim3(256, 1, 1);
+        rec->shmem = (uint32_t)lds;
+        rec->name = "im2col_t8_f16";
+        rec->set_params(p);
+        return;
+    }
     const int64_t n = (int64_t)p.Pp * (p.Kp / 8);
     rec->fn = (const void*)k_im2col_t;
     rec->grid = dim3((unsigned)((n + 255) / 256), 1, 1);

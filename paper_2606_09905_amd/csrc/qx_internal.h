@@ -48,6 +48,7 @@ struct GemmParams {
     int32_t b_mode;         // BMode
     int32_t hw;             // OUT_CONV: Ho*Wo
     int32_t tiles_n;        // number of N tiles (grid swizzle)
+    int32_t cs_slices;      // colsum holds this many partial rows per batch
     ConvGeom g;
 };
 
@@ -100,7 +101,6 @@ struct AttnParams {
     const void* V;
     void* O;
     void* part;             // F32: split partials [splits][L][d] float
-    const int32_t* vcs;     // I32: column sums of V over all keys
     int32_t L, d;
     int32_t splits;         // key splits
     int32_t keys_per_split;
@@ -189,8 +189,9 @@ enum Route : int32_t {
 // Integer GEMM main kernel for an MFMA route; returns false if unsupported.
 bool build_gemm_mfma(int32_t route, const GemmParams& p, int batch, LaunchRec* rec,
                      int* tile_m, int* tile_n, int* tile_k);
-void build_rowsum(const SumsParams& p, LaunchRec* rec);
-void build_colsum(const SumsParams& p, LaunchRec* rec);   // adds into a zeroed colsum
+// Row sums [batch][M] and per-slice column sums [batch][slices][N] in one launch.
+void build_sums(const SumsParams& p, LaunchRec* rec);
+int sums_slices(int K);
 void build_im2col(const Im2colParams& p, LaunchRec* rec);
 void build_valu_gemm(int32_t kind, const ValuGemmParams& p, int batch, LaunchRec* rec);
 bool build_attn_f32(const AttnParams& p, LaunchRec* rec);

@@ -208,6 +208,28 @@ def test_conv(case):
     same(y, orc.conv2d_direct(x, w, s, p))
 
 
+CONV_NT_CASES = [  # large enough for the encode + NT route
+    (2, 32, 30, 28, 64, 3, 3, 1, 1, 256), (4, 32, 40, 36, 128, 3, 3, 2, 1, 128),
+    (2, 16, 24, 20, 64, 5, 5, 1, 2, 256), (4, 12, 30, 30, 64, 3, 3, 1, 1, 256),
+    (8, 64, 20, 20, 96, 1, 1, 1, 0, 256),
+]
+
+
+@pytest.mark.parametrize("case", CONV_NT_CASES)
+def test_conv_encode_nt_path(case):
+    N, Ci, H, W, Co, KH, KW, s, p, b = case
+    rng = np.random.default_rng(zlib.crc32(repr(case).encode()))
+    x = rand_int(rng, (N, Ci, H, W), b, np.int16)
+    w = rand_int(rng, (Co, Ci, KH, KW), b, np.int16)
+    x[0, :, 0, 0] = -b
+    w[0, :, 0, 0] = -b
+    with qx.Executor.conv2d(N, Ci, H, W, Co, KH, KW, s, p, b, b) as ex:
+        plan = ex.plan()
+        assert plan["route_name"] == "f16_exact" and plan["kernels"] == 3, plan
+        y = run_exec(ex, (x, w))
+    same(y, orc.conv2d_direct(x, w, s, p))
+
+
 # ---------------------------------------------------------------------------
 # Attention core
 # ---------------------------------------------------------------------------
@@ -284,7 +306,8 @@ def test_executor_profile_times_every_launch():
     out = torch.empty((1, 512, 768), dtype=torch.int32, device="cuda")
     with qx.Executor.gemm_i16i32(512, 768, 1024, 1, 256, 256) as ex:
         prof = ex.profile([ta, tb], out, reps=3)
-    assert [n for n, _ in prof] == ["enc_a_f16", "enc_bt_f16", "gemm_nt_128x128"]
+    names = [n for n, _ in prof]
+    assert names[:2] == ["enc_a_f16", "enc_bt_f16"] and names[2].startswith("gemm_nt_")
     assert all(ms > 0 for _, ms in prof)
     same(host(out), orc.gemm_i16i32(A, B))
 
