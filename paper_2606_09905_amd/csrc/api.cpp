@@ -153,6 +153,28 @@ bool use_nt(int32_t route, int64_t chunk, int64_t M, int64_t N, int64_t K, int64
 
 int64_t pad_up(int64_t v, int64_t a) { return (v + a - 1) / a * a; }
 
+int32_t planes_of(int32_t r) {
+    switch (r) {
+    case R_I8_DIRECT: return 1;
+    case R_I8_OFFSET4: return 2;
+    default: return 3;
+    }
+}
+
+// The int8 limb routes take the same encode + direct-to-LDS structure for
+// large problems; the GEMM addresses every limb plane with 32-bit offsets.
+bool use_i8nt(int32_t route, int64_t M, int64_t N, int64_t K, int64_t batch) {
+    if (route != R_I8_DIRECT && route != R_I8_KARATSUBA && route != R_I8_OFFSET4 && route != R_S24_I8LIMB)
+        return false;
+    const double macs = (double)M * (double)N * (double)K * (double)batch;
+    if (!(macs >= (double)(1 << 24) && M >= 32 && N >= 32 && K >= 64)) return false;
+    int bm, bn;
+    i8nt_tile_shape(route, M, N, batch, &bm, &bn);
+    const int64_t P = planes_of(route), Kp = pad_up(K, 64);
+    const int64_t lim = (int64_t)1 << 31;
+    return P * pad_up(M, bm) * Kp < lim && P * pad_up(N, bn) * Kp < lim;
+}
+
 // Appends the launches of one integer GEMM; ws_used is the workspace end.
 qx_status plan_int_gemm(const GemmSpec& s, Plan* pl, uint64_t* ws_used) {
     int32_t route = s.route;
@@ -248,6 +270,7 @@ qx_status plan_int_gemm(const GemmSpec& s, Plan* pl, uint64_t* ws_used) {
     g.M = (int32_t)s.M; g.N = (int32_t)s.N; g.K = (int32_t)s.K;
     g.lda = (int32_t)s.lda; g.ldb = (int32_t)s.ldb; g.ldc = (int32_t)s.ldc;
     g.out_mode = s.out_mode; g.hw = s.hw; g.b_mode = B_KN;
+    const bool nt8 = s.allow_nt && use_i8nt(route, s.M, s.N, s.K, s.batch);
     const bool offset = route == R_I8_OFFSET4 || route == R_S24_I8LIMB;
     uint64_t rs_off = 0, cs_off = 0;
     if (offset) {
@@ -269,6 +292,55 @@ qx_status plan_int_gemm(const GemmSpec& s, Plan* pl, uint64_t* ws_used) {
         rr.bind(offsetof(SumsParams, rowsum), BIND_WS, rs_off);
         rr.bind(offsetof(SumsParams, colsum), BIND_WS, cs_off);
         pl->launches.push_back(rr);
+    }
+    if (nt8) {
+        // limb planes: A8 [batch][P][Mp][Kp], B8T [batch][P][Np][Kp] (int8)
+        int bm, bn;
+        i8nt_tile_shape(route, s.M, s.N, s.batch, &bm, &bn);
+        const int64_t P = planes_of(route);
+        const int64_t Mp = pad_up(s.M, bm), Np = pad_up(s.N, bn), Kp = pad_up(s.K, 64);
+        const uint64_t a_off = round_up(*ws_used, 256);
+        const uint64_t b_off = round_up(a_off + (uint64_t)s.batch * P * Mp * Kp, 256);
+        *ws_used = b_off + (uint64_t)s.batch * P * Np * Kp;
+        const int64_t v16 = s.s24 ? 4 : 8;   // elements per 16 bytes
+        EncParams ea{};
+        ea.s_src = s.sA; ea.s_dst = P * Mp * Kp;
+        ea.M = (int32_t)s.M; ea.K = (int32_t)s.K;
+        ea.Mp = (int32_t)Mp; ea.Kp = (int32_t)Kp;
+        ea.ld_src = (int32_t)s.lda; ea.batch = (int32_t)s.batch;
+        ea.vec = (s.lda % v16 == 0 && s.sA % v16 == 0) ? 1 : 0;
+        LaunchRec r1;
+        build_enc_limb_a(route, s.s24, ea, &r1);
+        r1.bind(offsetof(EncParams, src), s.a_bind);
+        r1.bind(offsetof(EncParams, dst), BIND_WS, a_off);
+        EncParams eb{};
+        eb.s_src = s.sB; eb.s_dst = P * Np * Kp;
+        eb.N = (int32_t)s.N; eb.K = (int32_t)s.K;
+        eb.Np = (int32_t)Np; eb.Kp = (int32_t)Kp;
+        eb.ld_src = (int32_t)s.ldb; eb.batch = (int32_t)s.batch;
+        eb.vec = (s.ldb % 4 == 0 && s.sB % 4 == 0) ? 1 : 0;
+        LaunchRec r2;
+        build_enc_limb_bt(route, s.s24, eb, &r2);
+        r2.bind(offsetof(EncParams, src), s.b_bind, s.b_ws_off);
+        r2.bind(offsetof(EncParams, dst), BIND_WS, b_off);
+        g.sA = P * Mp * Kp; g.sB = P * Np * Kp;
+        g.lda = (int32_t)Kp; g.ldb = (int32_t)Kp;
+        g.plane_a = Mp * Kp; g.plane_b = Np * Kp;
+        LaunchRec r3;
+        if (!build_gemm_i8nt(route, g, (int)s.batch, &r3))
+            return fail(QX_ERR_UNSUPPORTED, "no kernel for route %d", route);
+        r3.bind(offsetof(GemmParams, A), BIND_WS, a_off);
+        r3.bind(offsetof(GemmParams, B), BIND_WS, b_off);
+        r3.bind(offsetof(GemmParams, C), BIND_OUT);
+        if (offset) {
+            r3.bind(offsetof(GemmParams, rowsum), BIND_WS, rs_off);
+            r3.bind(offsetof(GemmParams, colsum), BIND_WS, cs_off);
+        }
+        pl->launches.push_back(r1);
+        pl->launches.push_back(r2);
+        pl->launches.push_back(r3);
+        info.tile_m = bm; info.tile_n = bn; info.tile_k = 64;
+        return QX_OK;
     }
     if (route == R_F16_EXACT) {
         const int64_t chunk = f16_chunk(s.ba, s.bb);

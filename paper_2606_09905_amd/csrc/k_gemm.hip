@@ -453,6 +453,244 @@ __global__ __launch_bounds__(NT) void k_gemm_i8limb(const GemmParams p) {
 }
 
 // ===========================================================================
+// int8 limb routes for large problems: encode to limb planes, then an NT
+// int8 GEMM staged global -> LDS with global_load_lds_dwordx4.
+// ===========================================================================
+// A [batch][M][lda] (T) -> A8 [batch][P][Mp][Kp] int8 limb planes; a thread
+// splits 16 consecutive k of one row.  Elements outside M x K become all-zero
+// limbs (the split of S::PAD), which add nothing to any limb product.
+template <class S, class T>
+__global__ __launch_bounds__(NT) void k_enc_limb_a(const EncParams p) {
+    constexpr int P = S::PLANES;
+    const int kv = p.Kp / 16;
+    const int64_t per_b = (int64_t)p.Mp * kv;
+    const int64_t v = (int64_t)blockIdx.x * NT + threadIdx.x;
+    if (v >= per_b * p.batch) return;
+    const int b = (int)(v / per_b);
+    const int64_t r = v - (int64_t)b * per_b;
+    const int m = (int)(r / kv), k0 = (int)(r - (int64_t)m * kv) * 16;
+    const T* src = (const T*)p.src + b * p.s_src + (int64_t)m * p.ld_src + k0;
+    T x[16];
+    bool ok[16];
+    if (p.vec && m < p.M && k0 + 16 <= p.K) {
+        load_vec<T, 16>(src, x);
+#pragma unroll
+        for (int e = 0; e < 16; ++e) ok[e] = true;
+    } else {
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+            ok[e] = m < p.M && k0 + e < p.K;
+            x[e] = ok[e] ? src[e] : (T)0;
+        }
+    }
+    uint32_t w[P][4] = {};
+#pragma unroll
+    for (int e = 0; e < 16; ++e) {
+        uint32_t l[P];
+        S::split(x[e], l);
+#pragma unroll
+        for (int q = 0; q < P; ++q) w[q][e >> 2] |= (ok[e] ? l[q] : 0u) << (8 * (e & 3));
+    }
+    int8_t* dst = (int8_t*)p.dst + b * p.s_dst + (int64_t)m * p.Kp + k0;
+#pragma unroll
+    for (int q = 0; q < P; ++q)
+        *(i4*)(dst + (int64_t)q * p.Mp * p.Kp) = i4{(int)w[q][0], (int)w[q][1], (int)w[q][2], (int)w[q][3]};
+}
+
+// B [batch][K][ldb] (T) -> B8T [batch][P][Np][Kp]: a workgroup transposes a
+// 64(k) x 64(n) block.  A thread splits a 4 x 4 sub-block, packs the four k
+// bytes of each column and plane into one dword, and stages it in LDS; the
+// rows then leave as 16-byte runs along k.
+template <class S, class T>
+__global__ __launch_bounds__(NT) void k_enc_limb_bt(const EncParams p) {
+    constexpr int P = S::PLANES, RW = 17;     // LDS row: 16 dwords of k + 1 to spread banks
+    __shared__ uint32_t t[P][64][RW];
+    const int n0 = blockIdx.x * 64, k0 = blockIdx.y * 64, b = blockIdx.z;
+    const T* src = (const T*)p.src + b * p.s_src;
+    const int tid = threadIdx.x, kg = tid >> 4, ng = tid & 15;
+    const int kb = k0 + kg * 4, nb = n0 + ng * 4;
+    uint32_t w[P][4] = {};
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+        const int k = kb + r;
+        const T* row = src + (int64_t)k * p.ld_src + nb;
+        T x[4];
+        bool ok[4];
+        if (p.vec && k < p.K && nb + 4 <= p.N) {
+            load_vec<T, 4>(row, x);
+#pragma unroll
+            for (int c = 0; c < 4; ++c) ok[c] = true;
+        } else {
+#pragma unroll
+            for (int c = 0; c < 4; ++c) {
+                ok[c] = k < p.K && nb + c < p.N;
+                x[c] = ok[c] ? row[c] : (T)0;
+            }
+        }
+#pragma unroll
+        for (int c = 0; c < 4; ++c) {
+            uint32_t l[P];
+            S::split(x[c], l);
+#pragma unroll
+            for (int q = 0; q < P; ++q) w[q][c] |= (ok[c] ? l[q] : 0u) << (8 * r);
+        }
+    }
+#pragma unroll
+    for (int q = 0; q < P; ++q)
+#pragma unroll
+        for (int c = 0; c < 4; ++c) t[q][ng * 4 + c][kg] = w[q][c];
+    __syncthreads();
+    const int nn = tid >> 2, kc = (tid & 3) * 4;
+    int8_t* dst = (int8_t*)p.dst + b * p.s_dst + (int64_t)(n0 + nn) * p.Kp + k0 + kc * 4;
+#pragma unroll
+    for (int q = 0; q < P; ++q) {
+        const uint32_t* s4 = &t[q][nn][kc];
+        *(i4*)(dst + (int64_t)q * p.Np * p.Kp) = i4{(int)s4[0], (int)s4[1], (int)s4[2], (int)s4[3]};
+    }
+}
+
+// 64-byte LDS rows (64 int8) as four 16-byte chunks; the 16 rows of one
+// ds_read_b128 lane group land in distinct banks.
+__device__ __forceinline__ int swz_i8(int row) { return (row >> 2) & 3; }
+
+template <class S, int BM, int BN>
+__global__ __launch_bounds__(NT) void k_gemm_i8nt(const GemmParams p) {
+    constexpr int BK = 64, KCH = 4, P = S::PLANES, G = S::GROUPS;
+    constexpr int WM = BM / 2, WN = BN / 2, TM = WM / 32, TN = WN / 32, STAGES = 3;
+    constexpr int AL = P * BM * KCH / NT, BL = P * BN * KCH / NT, LPT = AL + BL;
+    static_assert(AL * NT == P * BM * KCH && BL * NT == P * BN * KCH, "whole loads");
+    constexpr unsigned STAGE_A = P * BM * KCH * 16, STAGE_B = P * BN * KCH * 16;
+    __shared__ i4 As[STAGES][P][BM][KCH];
+    __shared__ i4 Bs[STAGES][P][BN][KCH];
+
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, l32 = lane & 31, hh = lane >> 5;
+    const int wm = wave >> 1, wn = wave & 1;
+    const int tiles_m = (p.M + BM - 1) / BM;
+    int pid = blockIdx.x;
+    const int total = gridDim.x;
+    if ((total & 7) == 0) pid = (pid & 7) * (total >> 3) + (pid >> 3);
+    int tm, tn;
+    {
+        constexpr int GR = 8;
+        const int per_group = GR * p.tiles_n;
+        const int gid = pid / per_group;
+        const int first_m = gid * GR;
+        const int gsz = min(tiles_m - first_m, GR);
+        const int in = pid - gid * per_group;
+        tm = first_m + in % gsz;
+        tn = in / gsz;
+    }
+    const int m0 = tm * BM, n0 = tn * BN;
+    const int b = blockIdx.z;
+    // planes: A8 [batch][P][Mp][Kp] (sA = P*Mp*Kp, lda = Kp, plane_a = Mp*Kp), B8T likewise
+    const char* a_panel = (const char*)p.A + b * p.sA + (int64_t)m0 * p.lda;
+    const char* b_panel = (const char*)p.B + b * p.sB + (int64_t)n0 * p.ldb;
+    unsigned oa[AL], ob[BL];
+#pragma unroll
+    for (int i = 0; i < AL; ++i) {
+        const int q = tid + NT * i, plane = q / (BM * KCH), rem = q % (BM * KCH);
+        const int row = rem / KCH, pc = rem % KCH;
+        oa[i] = (unsigned)((int64_t)plane * p.plane_a + row * p.lda + (pc ^ swz_i8(row)) * 16);
+    }
+#pragma unroll
+    for (int i = 0; i < BL; ++i) {
+        const int q = tid + NT * i, plane = q / (BN * KCH), rem = q % (BN * KCH);
+        const int row = rem / KCH, pc = rem % KCH;
+        ob[i] = (unsigned)((int64_t)plane * p.plane_b + row * p.ldb + (pc ^ swz_i8(row)) * 16);
+    }
+    const unsigned wave_u = __builtin_amdgcn_readfirstlane(wave);
+    const unsigned lds_a0 = (unsigned)(uintptr_t)&As[0][0][0][0] + wave_u * 1024;
+    const unsigned lds_b0 = (unsigned)(uintptr_t)&Bs[0][0][0][0] + wave_u * 1024;
+    auto issue = [&](int t) {
+        const int s = t % STAGES;
+        const char* ab = a_panel + t * BK;
+        const char* bb = b_panel + t * BK;
+        const unsigned la = lds_a0 + s * STAGE_A, lb = lds_b0 + s * STAGE_B;
+#pragma unroll
+        for (int i = 0; i < AL; ++i)
+            asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dwordx4 %0, %1"
+                         :: "v"(oa[i]), "s"(ab), "s"(la + NT * 16 * i) : "memory", "m0");
+#pragma unroll
+        for (int i = 0; i < BL; ++i)
+            asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dwordx4 %0, %1"
+                         :: "v"(ob[i]), "s"(bb), "s"(lb + NT * 16 * i) : "memory", "m0");
+    };
+
+    i16x acc[G][TM][TN];
+#pragma unroll
+    for (int g = 0; g < G; ++g)
+#pragma unroll
+        for (int i = 0; i < TM; ++i)
+#pragma unroll
+            for (int j = 0; j < TN; ++j) acc[g][i][j] = i16x{};
+
+    const int ktiles = (p.K + BK - 1) / BK;   // planes are zero-limb padded to whole tiles
+#pragma unroll
+    for (int s = 0; s < STAGES - 1; ++s)
+        if (s < ktiles) issue(s);
+    for (int t = 0; t < ktiles; ++t) {
+        if (t + 1 < ktiles) __builtin_amdgcn_s_waitcnt((LPT & 15) | ((LPT >> 4) << 14) | 0x0F70);
+        else __builtin_amdgcn_s_waitcnt(0x0F70);
+        __syncthreads();
+        if (t + STAGES - 1 < ktiles) issue(t + STAGES - 1);
+        const int s = t % STAGES;
+#pragma unroll
+        for (int ks = 0; ks < BK / 32; ++ks) {
+            const int c = ks * 2 + hh;
+            i4 a[P][TM], bv[P][TN];
+#pragma unroll
+            for (int q = 0; q < P; ++q) {
+#pragma unroll
+                for (int i = 0; i < TM; ++i) {
+                    const int row = wm * WM + i * 32 + l32;
+                    a[q][i] = As[s][q][row][c ^ swz_i8(row)];
+                }
+#pragma unroll
+                for (int j = 0; j < TN; ++j) {
+                    const int col = wn * WN + j * 32 + l32;
+                    bv[q][j] = Bs[s][q][col][c ^ swz_i8(col)];
+                }
+            }
+#pragma unroll
+            for (int pr = 0; pr < S::PRODUCTS; ++pr)
+#pragma unroll
+                for (int i = 0; i < TM; ++i)
+#pragma unroll
+                    for (int j = 0; j < TN; ++j)
+                        acc[S::pg[pr]][i][j] = __builtin_amdgcn_mfma_i32_32x32x32_i8(
+                            a[S::pa[pr]][i], bv[S::pb[pr]][j], acc[S::pg[pr]][i][j], 0, 0, 0);
+        }
+    }
+
+    int32_t* C = (int32_t*)p.C + b * p.sC;
+    const uint32_t cc = (uint32_t)p.corr_c;
+    const uint32_t kcc = (uint32_t)p.K * cc * cc;
+    const int32_t* rs = p.rowsum ? p.rowsum + (int64_t)b * p.M : nullptr;
+    const int32_t* cs = p.colsum ? p.colsum + (int64_t)b * p.cs_slices * p.N : nullptr;
+#pragma unroll
+    for (int j = 0; j < TN; ++j) {
+        const int gn = n0 + wn * WN + j * 32 + l32;
+        if (gn >= p.N) continue;
+        uint32_t csum = 0;
+        if (cc)
+            for (int sl = 0; sl < p.cs_slices; ++sl) csum += (uint32_t)cs[(int64_t)sl * p.N + gn];
+#pragma unroll
+        for (int i = 0; i < TM; ++i)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+                const int gm = m0 + wm * WM + i * 32 + 8 * (r >> 2) + 4 * hh + (r & 3);
+                if (gm >= p.M) continue;
+                uint32_t gv[G];
+#pragma unroll
+                for (int q = 0; q < G; ++q) gv[q] = (uint32_t)acc[q][i][j][r];
+                uint32_t v = S::combine(gv);
+                if (cc) v += cc * ((uint32_t)rs[gm] + csum) - kcc;
+                store_c(p, C, gm, gn, v);
+            }
+    }
+}
+
+// ===========================================================================
 // Row / column sums for the rank-1 correction of offset limb routes.
 // ===========================================================================
 // Row sums of A (blockIdx.y == 0: one wave per row, lanes stride along the
@@ -599,6 +837,58 @@ bool build_gemm_mfma(int32_t route, const GemmParams& p, int batch, LaunchRec* r
     default:
         return false;
     }
+}
+
+// int8 NT route: 128x128 workgroup tiles (four 64x64 waves) when they fill
+// the chip, else 64x64 (four 32x32 waves).
+void i8nt_tile_shape(int32_t route, int64_t M, int64_t N, int64_t batch, int* bm, int* bn) {
+    (void)route;
+    const int64_t big = ((M + 127) / 128) * ((N + 127) / 128) * batch;
+    *bm = *bn = big >= 256 ? 128 : 64;
+}
+
+template <class S>
+static void enc_limb_recs(bool s24, bool bt, const EncParams& p, LaunchRec* rec, const char* name) {
+    if (bt) {
+        rec->fn = s24 ? (const void*)k_enc_limb_bt<S, int32_t> : (const void*)k_enc_limb_bt<S, int16_t>;
+        rec->grid = dim3((unsigned)(p.Np / 64), (unsigned)(p.Kp / 64), (unsigned)p.batch);
+    } else {
+        const int64_t n = (int64_t)p.batch * p.Mp * (p.Kp / 16);
+        rec->fn = s24 ? (const void*)k_enc_limb_a<S, int32_t> : (const void*)k_enc_limb_a<S, int16_t>;
+        rec->grid = dim3((unsigned)((n + NT - 1) / NT), 1, 1);
+    }
+    rec->block = dim3(NT, 1, 1);
+    rec->shmem = 0;
+    rec->name = name;
+    rec->set_params(p);
+}
+
+static void enc_limb(int32_t route, bool s24, bool bt, const EncParams& p, LaunchRec* rec) {
+    switch (route) {
+    case R_I8_DIRECT: enc_limb_recs<SchemeDirect>(s24, bt, p, rec, bt ? "enc_limb_bt_direct" : "enc_limb_a_direct"); break;
+    case R_I8_KARATSUBA: enc_limb_recs<SchemeKaratsuba>(s24, bt, p, rec, bt ? "enc_limb_bt_karatsuba" : "enc_limb_a_karatsuba"); break;
+    case R_I8_OFFSET4: enc_limb_recs<SchemeOffset4>(s24, bt, p, rec, bt ? "enc_limb_bt_offset4" : "enc_limb_a_offset4"); break;
+    default: enc_limb_recs<SchemeS24>(s24, bt, p, rec, bt ? "enc_limb_bt_s24" : "enc_limb_a_s24"); break;
+    }
+}
+void build_enc_limb_a(int32_t route, bool s24, const EncParams& p, LaunchRec* rec) { enc_limb(route, s24, false, p, rec); }
+void build_enc_limb_bt(int32_t route, bool s24, const EncParams& p, LaunchRec* rec) { enc_limb(route, s24, true, p, rec); }
+
+bool build_gemm_i8nt(int32_t route, const GemmParams& p0, int batch, LaunchRec* rec) {
+    int bm, bn;
+    i8nt_tile_shape(route, p0.M, p0.N, batch, &bm, &bn);
+    const bool big = bm == 128;
+#define QX_NT(S, NAME)                                                                               \
+    if (big) fill_gemm_rec(rec, k_gemm_i8nt<S, 128, 128>, p0, 128, 128, batch, "gemm_i8nt_" NAME "_128x128"); \
+    else fill_gemm_rec(rec, k_gemm_i8nt<S, 64, 64>, p0, 64, 64, batch, "gemm_i8nt_" NAME "_64x64");
+    switch (route) {
+    case R_I8_DIRECT: QX_NT(SchemeDirect, "direct") return true;
+    case R_I8_KARATSUBA: QX_NT(SchemeKaratsuba, "karatsuba") return true;
+    case R_I8_OFFSET4: QX_NT(SchemeOffset4, "offset4") return true;
+    case R_S24_I8LIMB: QX_NT(SchemeS24, "s24") return true;
+    default: return false;
+    }
+#undef QX_NT
 }
 
 int sums_slices(int K) { return std::max((K + SUM_SLICE - 1) / SUM_SLICE, 1); }

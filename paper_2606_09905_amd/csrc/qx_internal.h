@@ -49,6 +49,8 @@ struct GemmParams {
     int32_t hw;             // OUT_CONV: Ho*Wo
     int32_t tiles_n;        // number of N tiles (grid swizzle)
     int32_t cs_slices;      // colsum holds this many partial rows per batch
+    int64_t plane_a;        // int8 NT route: bytes between limb planes of A and of B
+    int64_t plane_b;
     ConvGeom g;
 };
 
@@ -204,5 +206,10 @@ void build_gemm_nt(const GemmParams& p, int batch, LaunchRec* rec);
 void build_enc_a(const EncParams& p, LaunchRec* rec);
 void build_enc_bt(const EncParams& p, LaunchRec* rec);
 void build_im2col_t(const Im2colTParams& p, LaunchRec* rec);
+// int8 limb routes for large problems: limb-plane encoders + direct-to-LDS NT GEMM.
+void i8nt_tile_shape(int32_t route, int64_t M, int64_t N, int64_t batch, int* bm, int* bn);
+void build_enc_limb_a(int32_t route, bool s24, const EncParams& p, LaunchRec* rec);
+void build_enc_limb_bt(int32_t route, bool s24, const EncParams& p, LaunchRec* rec);
+bool build_gemm_i8nt(int32_t route, const GemmParams& p, int batch, LaunchRec* rec);
 
 }  // namespace qx

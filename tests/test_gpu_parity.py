@@ -128,6 +128,47 @@ def test_gemm_i16_encode_nt_path(shape, bound):
     same(got, orc.gemm_i16i32(A, B))
 
 
+I8NT_SHAPES = [  # M, N, K, batch: large enough for the limb-plane encode + NT route
+    (300, 520, 200, 2), (257, 129, 1000, 1), (64, 1024, 4096, 1), (513, 2000, 520, 3),
+    (1024, 1024, 1024, 1), (33, 700, 999, 2),
+]
+
+
+@pytest.mark.parametrize("route,bound", [("i8_direct", 127), ("i8_karatsuba", 8127),
+                                         ("i8_offset4", 32768)])
+@pytest.mark.parametrize("shape", I8NT_SHAPES)
+def test_gemm_i16_limb_encode_nt_path(route, bound, shape):
+    # Ragged M, N and K (odd K also takes the encoders' element-wise loads);
+    # offset4 adds the row/column-sum launch for its rank-1 correction.
+    M, N, K, batch = shape
+    rng = np.random.default_rng(zlib.crc32(repr((route, shape)).encode()))
+    A = rand_int(rng, (batch, M, K), min(bound, 32767), np.int16)
+    B = rand_int(rng, (batch, K, N), min(bound, 32767), np.int16)
+    A[0, 0, :] = -min(bound, 32768)
+    B[0, :, 0] = -min(bound, 32768)
+    with qx.Executor.gemm_i16i32(M, N, K, batch, bound, bound, route) as ex:
+        plan = ex.plan()
+        assert plan["route_name"] == route
+        assert plan["kernels"] == (4 if route == "i8_offset4" else 3), plan
+        got = run_exec(ex, (A, B))
+    same(got, orc.gemm_i16i32(A, B), str((route, shape)))
+
+
+@pytest.mark.parametrize("shape", I8NT_SHAPES + [(512, 512, 512, 16)])
+def test_gemm_s24_encode_nt_path(shape):
+    M, N, K, batch = shape
+    rng = np.random.default_rng(zlib.crc32(repr(("s24", shape)).encode()))
+    A = rng.integers(-(1 << 31), (1 << 31) - 1, (batch, M, K), dtype=np.int32, endpoint=True)
+    B = rng.integers(-(1 << 31), (1 << 31) - 1, (batch, K, N), dtype=np.int32, endpoint=True)
+    A[0, 0, :] = -(1 << 23)
+    B[0, :, 0] = (1 << 23) - 1
+    with qx.Executor.gemm_i32_s24(M, N, K, batch) as ex:
+        plan = ex.plan()
+        assert plan["route_name"] == "s24_i8limb" and plan["kernels"] == 4, plan
+        got = run_exec(ex, (A, B))
+    same(got, orc.gemm_i32_s24(A, B), str(shape))
+
+
 def test_f16_exact_mixed_magnitudes():
     # Products alternating between 2^16 and 1 inside one fp32 partial sum:
     # a narrow internal adder would lose the small terms.
