@@ -482,7 +482,48 @@ qx_status plan_conv(Plan* pl, int64_t N, int64_t Ci, int64_t H, int64_t W, int64
         pl->info.workspace_bytes = 0;
         return QX_OK;
     }
-    if (use_nt(pl->info.route, f16_chunk(ba, bb), Co, P, Kd, 1)) {
+    const int64_t Hp = H + 2 * pad, Wp = W + 2 * pad;
+    const bool nt = use_nt(pl->info.route, f16_chunk(ba, bb), Co, P, Kd, 1);
+    if (nt && Ci % 64 == 0 && 2 * N * Hp * Wp * Ci < ((int64_t)1 << 31)) {
+        // fp16-exact, implicit lowering: one launch writes the zero-bordered
+        // NHWC fp16 copy of x and the tap-major fp16 weights; the NT GEMM
+        // gathers its B tiles from that copy and scatters y to NCHW.
+        const int64_t chunk = f16_chunk(ba, bb);
+        int bm, bn;
+        nt_tile_shape(Co, P, 1, &bm, &bn);
+        const int64_t Mp = pad_up(Co, bm);
+        const uint64_t x_off = round_up(2 * (uint64_t)Mp * Kd, 256);
+        const uint64_t wsz = x_off + 2 * (uint64_t)(N * Hp * Wp * Ci);
+        const ConvGeom geo{(int32_t)Ci, (int32_t)H, (int32_t)W, (int32_t)KH, (int32_t)KW, (int32_t)stride,
+                           (int32_t)pad, (int32_t)Ho, (int32_t)Wo};
+        ConvPrepParams cp{};
+        cp.nimg = (int32_t)N; cp.Co = (int32_t)Co; cp.Cop = (int32_t)Mp; cp.Kd = (int32_t)Kd;
+        cp.g = geo;
+        LaunchRec r1;
+        build_conv_prep(cp, &r1);
+        r1.bind(offsetof(ConvPrepParams, x), BIND_IN0);
+        r1.bind(offsetof(ConvPrepParams, w), BIND_IN1);
+        r1.bind(offsetof(ConvPrepParams, xp), BIND_WS, x_off);
+        r1.bind(offsetof(ConvPrepParams, w16), BIND_WS, 0);
+        GemmParams gp{};
+        gp.M = (int32_t)Co; gp.N = (int32_t)P; gp.K = (int32_t)Kd;
+        gp.lda = (int32_t)Kd; gp.ldb = 0; gp.ldc = (int32_t)P;
+        gp.out_mode = OUT_CONV; gp.hw = (int32_t)(Ho * Wo); gp.b_mode = B_NHWC;
+        gp.chunk_tiles = (int32_t)(chunk / 64);
+        gp.g = geo;
+        LaunchRec r2;
+        build_gemm_nt(gp, 1, &r2);
+        r2.bind(offsetof(GemmParams, A), BIND_WS, 0);
+        r2.bind(offsetof(GemmParams, B), BIND_WS, x_off);
+        r2.bind(offsetof(GemmParams, C), BIND_OUT);
+        pl->launches = {r1, r2};
+        pl->info.chunk = (int32_t)(chunk / 64 * 64);
+        pl->info.tile_m = bm; pl->info.tile_n = bn; pl->info.tile_k = 64;
+        pl->info.kernels = 2;
+        pl->info.workspace_bytes = (int64_t)wsz;
+        return QX_OK;
+    }
+    if (nt) {
         // fp16-exact: weights encoded to fp16 [Mp][Kp], lowering written as
         // the transposed fp16 column matrix [Pp][Kp], then the NT GEMM with
         // an NCHW scatter epilogue.

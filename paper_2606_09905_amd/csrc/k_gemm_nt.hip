@@ -171,12 +171,74 @@ __global__ __launch_bounds__(256) void k_im2col_t8(const Im2colTParams p) {
     }
 }
 
+// Implicit lowering, C_in a multiple of 64.  The im2col column of pixel
+// (n, oh, ow) for K tile t is 64 consecutive channels of one kernel tap
+// (kh, kw): xp[n][oh*s + kh][ow*s + kw][ci0 .. ci0+64) of the zero-bordered
+// NHWC copy, so the contraction gathers its B tiles straight from xp.  The
+// weights take the matching order k = (kh*KW + kw)*Ci + ci; any order of the
+// K sum gives the same exact integer result.
+// blockIdx.y == 0: x NCHW int16 -> xp; a block covers 64 padded columns of
+// one padded row of one image, 64 channels per pass through LDS.
+// blockIdx.y == 1: w OIHW int16 -> w16 [Cop][Kd], one thread per 8 channels.
+__global__ __launch_bounds__(256) void k_conv_prep(const ConvPrepParams p) {
+    const ConvGeom& g = p.g;
+    const int tid = threadIdx.x;
+    if (blockIdx.y == 0) {
+        if ((int)blockIdx.x >= p.xblocks) return;
+        __shared__ short t[64][66];
+        const int Hp = g.H + 2 * g.pad, Wp = g.W + 2 * g.pad;
+        const int wch = (Wp + 63) / 64;
+        const int n = blockIdx.x / (Hp * wch), rem = blockIdx.x - n * Hp * wch;
+        const int hp = rem / wch, wp0 = (rem - hp * wch) * 64;
+        const int h = hp - g.pad;
+        const bool row_in = h >= 0 && h < g.H;
+        const int wl = tid & 63, cq = tid >> 6;
+        const int w = wp0 + wl - g.pad;
+        const bool in = row_in && w >= 0 && w < g.W;
+        _Float16* dst = p.xp + ((int64_t)n * Hp + hp) * Wp * g.Ci;
+        for (int c0 = 0; c0 < g.Ci; c0 += 64) {
+            const int16_t* src = p.x + (((int64_t)n * g.Ci + c0) * g.H + h) * g.W + w;
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+                const int c = cq + 4 * r;
+                t[c][wl] = in ? src[(int64_t)c * g.H * g.W] : (short)0;
+            }
+            __syncthreads();
+#pragma unroll
+            for (int i = 0; i < 2; ++i) {
+                const int q = tid + 256 * i, px = q >> 3, ch = q & 7;
+                if (wp0 + px < Wp) {
+                    h8 o;
+#pragma unroll
+                    for (int e = 0; e < 8; ++e) o[e] = (_Float16)t[ch * 8 + e][px];
+                    *(h8*)(dst + (int64_t)(wp0 + px) * g.Ci + c0 + ch * 8) = o;
+                }
+            }
+            __syncthreads();
+        }
+        return;
+    }
+    if ((int)blockIdx.x >= p.wblocks) return;
+    const int kc = p.Kd / 8;
+    const int64_t v = (int64_t)blockIdx.x * 256 + tid;
+    if (v >= (int64_t)p.Cop * kc) return;
+    const int co = (int)(v / kc), k0 = (int)(v - (int64_t)co * kc) * 8;
+    const int tap = k0 / g.Ci, ci0 = k0 - tap * g.Ci;
+    const int kh = tap / g.KW, kw = tap - kh * g.KW;
+    h8 o;
+#pragma unroll
+    for (int e = 0; e < 8; ++e)
+        o[e] = co < p.Co ? (_Float16)p.w[(((int64_t)co * g.Ci + ci0 + e) * g.KH + kh) * g.KW + kw]
+                         : (_Float16)0.0f;
+    *(h8*)(p.w16 + (int64_t)co * p.Kd + k0) = o;
+}
+
 // ===========================================================================
 // Stage 2: contraction
 // ===========================================================================
 __device__ __forceinline__ int chunk_swz(int r) { return (r >> 1) & 7; }
 
-template <int BM, int BN, int NW>
+template <int BM, int BN, int NW, bool IMPL>
 __global__ __launch_bounds__(NW * 64) void k_gemm_nt(const GemmParams p) {
     constexpr int BK = 64, KCH = 8, WM = 64, WN = 64;
     constexpr int TM = WM / 32, TN = WN / 32;
@@ -223,13 +285,28 @@ __global__ __launch_bounds__(NW * 64) void k_gemm_nt(const GemmParams p) {
         const int q = tid + NTH * i, row = q / KCH, pc = q % KCH;
         oa[i] = (unsigned)((row * p.lda + (pc ^ chunk_swz(row)) * 8) * 2);
     }
+    const ConvGeom& g = p.g;
+    const int Hp = g.H + 2 * g.pad, Wp = g.W + 2 * g.pad;
 #pragma unroll
     for (int i = 0; i < BL; ++i) {
         const int q = tid + NTH * i, row = q / KCH, pc = q % KCH;
-        ob[i] = (unsigned)((row * p.ldb + (pc ^ chunk_swz(row)) * 8) * 2);
+        if (IMPL) {
+            // pixel base in xp; rows past the last pixel re-read pixel 0
+            // (their results are never stored)
+            int pix = n0 + row;
+            if (pix >= p.N) pix = 0;
+            const int img = pix / p.hw, rem = pix - img * p.hw;
+            const int oh = rem / g.Wo, ow = rem - oh * g.Wo;
+            const int64_t base = (((int64_t)img * Hp + oh * g.stride) * Wp + ow * g.stride) * g.Ci;
+            ob[i] = (unsigned)((base + (pc ^ chunk_swz(row)) * 8) * 2);
+        } else {
+            ob[i] = (unsigned)((row * p.ldb + (pc ^ chunk_swz(row)) * 8) * 2);
+        }
     }
     const char* a_panel = (const char*)(A + (int64_t)m0 * p.lda);
-    const char* b_panel = (const char*)(B + (int64_t)n0 * p.ldb);
+    const char* b_panel = IMPL ? (const char*)B : (const char*)(B + (int64_t)n0 * p.ldb);
+    // IMPL: kernel tap and channel offset of the next K tile to be issued
+    int tap_h = 0, tap_w = 0, tap_c = 0;
     const unsigned wave_u = __builtin_amdgcn_readfirstlane(wave);
     const unsigned lds_a0 = (unsigned)(uintptr_t)&As[0][0][0] + wave_u * 1024;
     const unsigned lds_b0 = (unsigned)(uintptr_t)&Bs[0][0][0] + wave_u * 1024;
@@ -238,7 +315,21 @@ __global__ __launch_bounds__(NW * 64) void k_gemm_nt(const GemmParams p) {
     auto issue = [&](int t) {
         const int s = t % STAGES;
         const char* ab = a_panel + t * BK * 2;
-        const char* bb = b_panel + t * BK * 2;
+        const char* bb;
+        if (IMPL) {
+            // tiles are issued in order 0, 1, 2, ...
+            bb = b_panel + (int64_t)((tap_h * Wp + tap_w) * g.Ci + tap_c) * 2;
+            tap_c += BK;
+            if (tap_c == g.Ci) {
+                tap_c = 0;
+                if (++tap_w == g.KW) {
+                    tap_w = 0;
+                    ++tap_h;
+                }
+            }
+        } else {
+            bb = b_panel + t * BK * 2;
+        }
         const unsigned la = lds_a0 + s * STAGE_A, lb = lds_b0 + s * STAGE_B;
 #pragma unroll
         for (int i = 0; i < AL; ++i)
@@ -361,19 +452,33 @@ void build_gemm_nt(const GemmParams& p0, int batch, LaunchRec* rec) {
     const int tiles_m = (p.M + bm - 1) / bm;
     p.tiles_n = (p.N + bn - 1) / bn;
     rec->grid = dim3((unsigned)(tiles_m * p.tiles_n), 1, (unsigned)batch);
+    const bool impl = p.b_mode == B_NHWC;
     if (bn == 256) {
-        rec->fn = (const void*)k_gemm_nt<128, 256, 8>;
+        rec->fn = impl ? (const void*)k_gemm_nt<128, 256, 8, true> : (const void*)k_gemm_nt<128, 256, 8, false>;
         rec->block = dim3(512, 1, 1);
-        rec->name = "gemm_nt_128x256";
+        rec->name = impl ? "gemm_nt_conv_128x256" : "gemm_nt_128x256";
     } else if (bm == 64) {
-        rec->fn = (const void*)k_gemm_nt<64, 128, 2>;
+        rec->fn = impl ? (const void*)k_gemm_nt<64, 128, 2, true> : (const void*)k_gemm_nt<64, 128, 2, false>;
         rec->block = dim3(128, 1, 1);
-        rec->name = "gemm_nt_64x128";
+        rec->name = impl ? "gemm_nt_conv_64x128" : "gemm_nt_64x128";
     } else {
-        rec->fn = (const void*)k_gemm_nt<128, 128, 4>;
+        rec->fn = impl ? (const void*)k_gemm_nt<128, 128, 4, true> : (const void*)k_gemm_nt<128, 128, 4, false>;
         rec->block = dim3(256, 1, 1);
-        rec->name = "gemm_nt_128x128";
+        rec->name = impl ? "gemm_nt_conv_128x128" : "gemm_nt_128x128";
     }
+    rec->set_params(p);
+}
+
+void build_conv_prep(const ConvPrepParams& p0, LaunchRec* rec) {
+    ConvPrepParams p = p0;
+    const ConvGeom& g = p.g;
+    const int Hp = g.H + 2 * g.pad, Wp = g.W + 2 * g.pad;
+    p.xblocks = p.nimg * Hp * ((Wp + 63) / 64);
+    p.wblocks = (int32_t)(((int64_t)p.Cop * (p.Kd / 8) + 255) / 256);
+    rec->fn = (const void*)k_conv_prep;
+    rec->grid = dim3((unsigned)std::max(p.xblocks, p.wblocks), 2, 1);
+    rec->block = dim3(256, 1, 1);
+    rec->name = "conv_prep_nhwc_f16";
     rec->set_params(p);
 }
 

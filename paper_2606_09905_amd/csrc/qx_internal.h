@@ -26,6 +26,7 @@ enum OutMode : int32_t {
 enum BMode : int32_t {
     B_KN = 0,          // B[k][n] at B + k*ldb + n   (row-major K x N)
     B_IM2COL = 1,      // B[k][n] gathered from an NCHW image (implicit lowering)
+    B_NHWC = 2,        // B^T[n][k] gathered from a zero-bordered NHWC fp16 image
 };
 
 struct ConvGeom {      // geometry for B_IM2COL / OUT_CONV
@@ -93,6 +94,19 @@ struct Im2colTParams {
     _Float16* colT;
     int32_t P, Pp;          // N*Ho*Wo and its padded extent
     int32_t Kd, Kp;         // Ci*KH*KW and its padded extent
+    ConvGeom g;
+};
+
+// Implicit lowering of a convolution (C_in a multiple of 64): the input as a
+// zero-bordered NHWC fp16 copy xp [N][H+2pad][W+2pad][Ci] and the weights as
+// w16 [Cop][Kd] fp16 with k = (kh*KW + kw)*Ci + ci, in one launch.
+struct ConvPrepParams {
+    const int16_t* x;       // NCHW
+    const int16_t* w;       // OIHW
+    _Float16* xp;
+    _Float16* w16;
+    int32_t nimg, Co, Cop, Kd;
+    int32_t xblocks, wblocks;
     ConvGeom g;
 };
 
@@ -206,6 +220,7 @@ void build_gemm_nt(const GemmParams& p, int batch, LaunchRec* rec);
 void build_enc_a(const EncParams& p, LaunchRec* rec);
 void build_enc_bt(const EncParams& p, LaunchRec* rec);
 void build_im2col_t(const Im2colTParams& p, LaunchRec* rec);
+void build_conv_prep(const ConvPrepParams& p, LaunchRec* rec);
 // int8 limb routes for large problems: limb-plane encoders + direct-to-LDS NT GEMM.
 void i8nt_tile_shape(int32_t route, int64_t M, int64_t N, int64_t batch, int* bm, int* bn);
 void build_enc_limb_a(int32_t route, bool s24, const EncParams& p, LaunchRec* rec);

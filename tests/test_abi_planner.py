@@ -34,9 +34,14 @@ def test_auto_routes_for_the_workloads():
     assert p["workspace_bytes"] >= 4 * 2048
     d = w["conv_8x64x56x56_128_3x3"].dims
     p = qx.plan_conv2d(d["N"], d["Ci"], d["H"], d["W"], d["Co"], d["KH"], d["KW"], 1, 1, 256, 256)
-    # encode weights, lower to the transposed fp16 column matrix, contract
-    assert p["route_name"] == "f16_exact" and p["kernels"] == 3
-    assert p["workspace_bytes"] >= 2 * 576 * 8 * 56 * 56
+    # one launch writes the bordered NHWC fp16 image and the fp16 weights,
+    # then the contraction gathers its column tiles from that image
+    assert p["route_name"] == "f16_exact" and p["kernels"] == 2
+    assert p["workspace_bytes"] >= 2 * 8 * 58 * 58 * 64 + 2 * 128 * 576
+    assert p["workspace_bytes"] < 2 * 576 * 8 * 56 * 56   # no explicit column matrix
+    # C_in not a multiple of 64: explicit transposed column matrix
+    p = qx.plan_conv2d(8, 32, 56, 56, 128, 3, 3, 1, 1, 256, 256)
+    assert p["kernels"] == 3 and p["workspace_bytes"] >= 2 * 288 * 8 * 56 * 56
     assert qx.plan_attn("f32", 4096, 64)["route_name"] == "attn_f32_mfma"
     p = qx.plan_attn("i32", 4096, 64, 64)
     assert p["route_name"] == "attn_i32_mfma" and p["products"] == 3

@@ -266,9 +266,38 @@ def test_conv_encode_nt_path(case):
     w[0, :, 0, 0] = -b
     with qx.Executor.conv2d(N, Ci, H, W, Co, KH, KW, s, p, b, b) as ex:
         plan = ex.plan()
-        assert plan["route_name"] == "f16_exact" and plan["kernels"] == 3, plan
+        assert plan["route_name"] == "f16_exact", plan
+        assert plan["kernels"] == (2 if Ci % 64 == 0 else 3), plan
         y = run_exec(ex, (x, w))
     same(y, orc.conv2d_direct(x, w, s, p))
+
+
+CONV_IMPLICIT_CASES = [  # C_in a multiple of 64: implicit lowering from the NHWC copy
+    (2, 64, 30, 26, 100, 3, 3, 1, 1, 256), (3, 128, 17, 19, 64, 3, 3, 2, 1, 256),
+    (2, 64, 23, 23, 64, 7, 7, 2, 3, 128), (1, 192, 14, 14, 256, 3, 3, 1, 0, 256),
+    (4, 64, 9, 33, 48, 5, 3, 1, 2, 255), (8, 256, 32, 32, 64, 1, 1, 2, 0, 256),
+]
+
+
+@pytest.mark.parametrize("case", CONV_IMPLICIT_CASES)
+def test_conv_implicit_lowering(case):
+    # Ragged C_out and pixel counts, strides 1 and 2, pads 0..3, square and
+    # rectangular kernels; extreme values on the image border and in every tap.
+    N, Ci, H, W, Co, KH, KW, s, p, b = case
+    rng = np.random.default_rng(zlib.crc32(repr(("impl", case)).encode()))
+    x = rand_int(rng, (N, Ci, H, W), b, np.int16)
+    w = rand_int(rng, (Co, Ci, KH, KW), b, np.int16)
+    x[0, :, 0, :] = -b
+    x[-1, :, :, -1] = -b
+    w[0] = -b
+    with qx.Executor.conv2d(N, Ci, H, W, Co, KH, KW, s, p, b, b) as ex:
+        plan = ex.plan()
+        assert plan["route_name"] == "f16_exact" and plan["kernels"] == 2, plan
+        y = run_exec(ex, (x, w))
+        y2 = run_exec(ex, (x, w))
+    ref = orc.conv2d_direct(x, w, s, p)
+    same(y, ref, str(case))
+    same(y2, ref, "second run " + str(case))
 
 
 # ---------------------------------------------------------------------------
