@@ -349,28 +349,37 @@ __global__ __launch_bounds__(NW * 64) void k_gemm_nt(const GemmParams p) {
         for (int j = 0; j < TN; ++j) iacc[i][j] = u16x{};
 
     // K-slot (lane half h, element e) of the MFMA is k = 16*ks + 8*h + e for
-    // both operands.
+    // both operands.  The fragments of k-step ks+1 are read while the MFMAs of
+    // k-step ks run, and MFMA clusters raise the wave's issue priority so the
+    // other wave on the SIMD issues its LDS reads and DMA in between.
+    auto ldf = [&](int s, int ks, h8 (&a)[TM], h8 (&bv)[TN]) {
+        const int c = ks * 2 + hh;
+#pragma unroll
+        for (int i = 0; i < TM; ++i) {
+            const int row = wm * WM + i * 32 + l32;
+            a[i] = As[s][row][c ^ chunk_swz(row)];
+        }
+#pragma unroll
+        for (int j = 0; j < TN; ++j) {
+            const int col = wn * WN + j * 32 + l32;
+            bv[j] = Bs[s][col][c ^ chunk_swz(col)];
+        }
+    };
     auto compute = [&](int s, bool first) {
+        constexpr int KS = BK / 16;
+        h8 fa[KS][TM], fb[KS][TN];
+        ldf(s, 0, fa[0], fb[0]);
 #pragma unroll
-        for (int ks = 0; ks < BK / 16; ++ks) {
-            h8 a[TM], bv[TN];
-            const int c = ks * 2 + hh;
-#pragma unroll
-            for (int i = 0; i < TM; ++i) {
-                const int row = wm * WM + i * 32 + l32;
-                a[i] = As[s][row][c ^ chunk_swz(row)];
-            }
-#pragma unroll
-            for (int j = 0; j < TN; ++j) {
-                const int col = wn * WN + j * 32 + l32;
-                bv[j] = Bs[s][col][c ^ chunk_swz(col)];
-            }
+        for (int ks = 0; ks < KS; ++ks) {
+            if (ks + 1 < KS) ldf(s, ks + 1, fa[ks + 1], fb[ks + 1]);
+            __builtin_amdgcn_s_setprio(1);
 #pragma unroll
             for (int i = 0; i < TM; ++i)
 #pragma unroll
                 for (int j = 0; j < TN; ++j)
-                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_f16(a[i], bv[j],
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_f16(fa[ks][i], fb[ks][j],
                                     (first && ks == 0) ? f16x{} : acc[i][j], 0, 0, 0);
+            __builtin_amdgcn_s_setprio(0);
         }
     };
 
