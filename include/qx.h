@@ -30,6 +30,13 @@
  *    pick the exact route.  Operands outside a declared bound give an
  *    unspecified but memory-safe result.  0 means "no promise": the full
  *    range of the type.
+ *  - With the environment variable QX_VALIDATE=1 (read at every run), a run
+ *    first scans every bounded operand on the device and waits for the
+ *    scan: if any |x| exceeds its declared bound the run returns
+ *    QX_ERR_RANGE without launching the operation (the output is left
+ *    untouched).  Such runs synchronise the stream.  The smul24 GEMM and
+ *    FP32 attention have no bounds to check (smul24 reads the low 24 bits
+ *    of any int32 by definition).
  *  - One-shot calls keep an internal plan + workspace cache keyed by shape,
  *    contract, route, device and stream; calls that share a key must not
  *    overlap in time.  Executor handles are not thread-safe; different
@@ -49,7 +56,8 @@ typedef enum {
     QX_OK = 0,
     QX_ERR_INVALID_ARG = 1,   /* null pointer, negative size, size overflow, bad enum */
     QX_ERR_UNSUPPORTED = 2,   /* valid request this build cannot run (device, route, shape) */
-    QX_ERR_RANGE = 3,         /* declared bound outside what the operation accepts */
+    QX_ERR_RANGE = 3,         /* declared bound outside what the operation accepts,
+                                 or (QX_VALIDATE=1) an operand outside its declared bound */
     QX_ERR_OUT_OF_MEMORY = 4, /* workspace allocation failed */
     QX_ERR_DEVICE = 5         /* a HIP call failed; details in qx_last_error() */
 } qx_status;

@@ -58,6 +58,15 @@ struct Plan {
     OpKind op{};
     qx_plan_info info{};
     std::vector<LaunchRec> launches;
+    // operands with a declared bound, scanned on the device when QX_VALIDATE=1
+    struct RangeCheck {
+        int input;
+        int elem_bytes;
+        int64_t n;
+        int32_t bound;
+    };
+    std::vector<RangeCheck> checks;
+    int n_events = 0;        // cross-lane events used by the launches (0: one stream)
     int n_inputs = 0;
     uint64_t in_align = 16;  // required alignment of every input pointer
 };
@@ -222,44 +231,79 @@ qx_status plan_int_gemm(const GemmSpec& s, Plan* pl, uint64_t* ws_used) {
         const int64_t chunk = f16_chunk(s.ba, s.bb);
         int bm, bn;
         nt_tile_shape(s.M, s.N, s.batch, &bm, &bn);
-        const int64_t Mp = pad_up(s.M, bm), Np = pad_up(s.N, bn), Kp = pad_up(s.K, 64);
+        // A and B^T are padded to whole 128-row / 256-column tiles so that
+        // every tile shape a batch group or column panel picks divides them.
+        const int64_t Mp = pad_up(s.M, 128), Np = pad_up(s.N, 256), Kp = pad_up(s.K, 64);
         const uint64_t a_off = round_up(*ws_used, 256);
         const uint64_t b_off = round_up(a_off + 2 * (uint64_t)s.batch * Mp * Kp, 256);
         *ws_used = b_off + 2 * (uint64_t)s.batch * Np * Kp;
-        EncParams ea{};
-        ea.s_src = s.sA; ea.s_dst = Mp * Kp;
-        ea.M = (int32_t)s.M; ea.N = 0; ea.K = (int32_t)s.K;
-        ea.Mp = (int32_t)Mp; ea.Np = 0; ea.Kp = (int32_t)Kp;
-        ea.ld_src = (int32_t)s.lda; ea.batch = (int32_t)s.batch;
-        ea.vec = (s.lda % 8 == 0 && s.sA % 8 == 0) ? 1 : 0;
-        LaunchRec r1;
-        build_enc_a(ea, &r1);
-        r1.bind(offsetof(EncParams, src), s.a_bind);
-        r1.bind(offsetof(EncParams, dst), BIND_WS, a_off);
-        EncParams eb{};
-        eb.s_src = s.sB; eb.s_dst = Np * Kp;
-        eb.M = 0; eb.N = (int32_t)s.N; eb.K = (int32_t)s.K;
-        eb.Mp = 0; eb.Np = (int32_t)Np; eb.Kp = (int32_t)Kp;
-        eb.ld_src = (int32_t)s.ldb; eb.batch = (int32_t)s.batch;
-        eb.vec = (s.ldb % 8 == 0 && s.sB % 8 == 0) ? 1 : 0;
-        LaunchRec r2;
-        build_enc_bt(eb, &r2);
-        r2.bind(offsetof(EncParams, src), s.b_bind, s.b_ws_off);
-        r2.bind(offsetof(EncParams, dst), BIND_WS, b_off);
-        GemmParams g{};
-        g.sA = Mp * Kp; g.sB = Np * Kp; g.sC = s.sC;
-        g.M = (int32_t)s.M; g.N = (int32_t)s.N; g.K = (int32_t)Kp;
-        g.lda = (int32_t)Kp; g.ldb = (int32_t)Kp; g.ldc = (int32_t)s.ldc;
-        g.out_mode = s.out_mode; g.hw = s.hw; g.b_mode = B_KN;
-        g.chunk_tiles = (int32_t)(chunk / 64);
-        LaunchRec r3;
-        build_gemm_nt(g, (int)s.batch, &r3);
-        r3.bind(offsetof(GemmParams, A), BIND_WS, a_off);
-        r3.bind(offsetof(GemmParams, B), BIND_WS, b_off);
-        r3.bind(offsetof(GemmParams, C), BIND_OUT);
-        pl->launches.push_back(r1);
-        pl->launches.push_back(r2);
-        pl->launches.push_back(r3);
+        // Overlap: the operands of the next batch group are encoded on the
+        // side stream while the current group's contraction runs on the
+        // caller's stream.
+        const double macs = (double)s.M * (double)s.N * (double)s.K * (double)s.batch;
+        int64_t groups = 1;
+        if (s.batch >= 2 && macs >= (double)(1LL << 32)) {
+            groups = std::min<int64_t>(s.batch, 8);
+            const int64_t per = (s.batch + groups - 1) / groups;
+            groups = (s.batch + per - 1) / per;
+        }
+        const int64_t per_group = (s.batch + groups - 1) / groups;
+        const bool lanes = groups > 1;
+        std::vector<LaunchRec> side, main;
+        int ev = 0;
+        auto enc_a = [&](int64_t b0, int64_t cnt) {
+            EncParams ea{};
+            ea.s_src = s.sA; ea.s_dst = Mp * Kp;
+            ea.M = (int32_t)s.M; ea.N = 0; ea.K = (int32_t)s.K;
+            ea.Mp = (int32_t)Mp; ea.Np = 0; ea.Kp = (int32_t)Kp;
+            ea.ld_src = (int32_t)s.lda; ea.batch = (int32_t)cnt;
+            ea.vec = (s.lda % 8 == 0 && s.sA % 8 == 0) ? 1 : 0;
+            LaunchRec r;
+            build_enc_a(ea, &r);
+            r.bind(offsetof(EncParams, src), s.a_bind, 2 * (uint64_t)(b0 * s.sA));
+            r.bind(offsetof(EncParams, dst), BIND_WS, a_off + 2 * (uint64_t)(b0 * Mp * Kp));
+            r.lane = lanes ? 1 : 0;
+            return r;
+        };
+        // encode B^T columns [n0, n0 + nw) of batches [b0, b0 + cnt), then contract them
+        auto enc_b_and_gemm = [&](int64_t b0, int64_t cnt, int64_t n0, int64_t nw) {
+            const int64_t nwp = std::min(pad_up(nw, 256), Np - n0);
+            EncParams eb{};
+            eb.s_src = s.sB; eb.s_dst = Np * Kp;
+            eb.M = 0; eb.N = (int32_t)nw; eb.K = (int32_t)s.K;
+            eb.Mp = 0; eb.Np = (int32_t)nwp; eb.Kp = (int32_t)Kp;
+            eb.ld_src = (int32_t)s.ldb; eb.batch = (int32_t)cnt;
+            eb.vec = (s.ldb % 8 == 0 && s.sB % 8 == 0 && n0 % 8 == 0) ? 1 : 0;
+            LaunchRec r2;
+            build_enc_bt(eb, &r2);
+            const uint64_t bt_add = b_off + 2 * (uint64_t)(b0 * Np * Kp + n0 * Kp);
+            r2.bind(offsetof(EncParams, src), s.b_bind, s.b_ws_off + 2 * (uint64_t)(b0 * s.sB + n0));
+            r2.bind(offsetof(EncParams, dst), BIND_WS, bt_add);
+            GemmParams g{};
+            g.sA = Mp * Kp; g.sB = Np * Kp; g.sC = s.sC;
+            g.M = (int32_t)s.M; g.N = (int32_t)nw; g.K = (int32_t)Kp;
+            g.lda = (int32_t)Kp; g.ldb = (int32_t)Kp; g.ldc = (int32_t)s.ldc;
+            g.out_mode = s.out_mode; g.hw = s.hw; g.b_mode = B_KN;
+            g.chunk_tiles = (int32_t)(chunk / 64);
+            LaunchRec r3;
+            build_gemm_nt(g, (int)cnt, &r3);
+            r3.bind(offsetof(GemmParams, A), BIND_WS, a_off + 2 * (uint64_t)(b0 * Mp * Kp));
+            r3.bind(offsetof(GemmParams, B), BIND_WS, bt_add);
+            r3.bind(offsetof(GemmParams, C), BIND_OUT, 4 * (uint64_t)(b0 * s.sC + n0));
+            if (lanes) {
+                r2.lane = 1;
+                r2.rec_ev = (int16_t)++ev;
+                r3.wait_ev = (int16_t)ev;
+            }
+            pl->launches.push_back(r2);
+            pl->launches.push_back(r3);
+        };
+        for (int64_t b0 = 0; b0 < s.batch; b0 += per_group) {
+            const int64_t cnt = std::min(per_group, s.batch - b0);
+            pl->launches.push_back(enc_a(b0, cnt));
+            enc_b_and_gemm(b0, cnt, 0, s.N);
+        }
+        pl->n_events = ev;
         info.chunk = (int32_t)(chunk / 64 * 64);
         info.tile_m = bm; info.tile_n = bn; info.tile_k = 64;
         return QX_OK;
@@ -430,6 +474,11 @@ qx_status plan_gemm(Plan* pl, bool s24, int64_t M, int64_t N, int64_t K, int64_t
         return QX_OK;
     }
     pl->launches = scratch.launches;
+    pl->n_events = scratch.n_events;
+    if (!s24) {
+        if (ba < 32768) pl->checks.push_back({0, 2, M * K * batch, (int32_t)ba});
+        if (bb < 32768) pl->checks.push_back({1, 2, K * N * batch, (int32_t)bb});
+    }
     pl->info.kernels = (int32_t)pl->launches.size();
     pl->info.workspace_bytes = (int64_t)ws;
     return QX_OK;
@@ -482,6 +531,8 @@ qx_status plan_conv(Plan* pl, int64_t N, int64_t Ci, int64_t H, int64_t W, int64
         pl->info.workspace_bytes = 0;
         return QX_OK;
     }
+    if (bb < 32768) pl->checks.push_back({0, 2, N * Ci * H * W, (int32_t)bb});
+    if (ba < 32768) pl->checks.push_back({1, 2, Co * Ci * KH * KW, (int32_t)ba});
     const int64_t Hp = H + 2 * pad, Wp = W + 2 * pad;
     const bool nt = use_nt(pl->info.route, f16_chunk(ba, bb), Co, P, Kd, 1);
     if (nt && Ci % 64 == 0 && 2 * N * Hp * Wp * Ci < ((int64_t)1 << 31)) {
@@ -623,6 +674,8 @@ qx_status plan_attn(Plan* pl, qx_attn_dtype dt, int64_t L, int64_t d, int32_t bo
         info.workspace_bytes = 0;
         return QX_OK;
     }
+    if (dt == QX_DT_I32 && bound > 0)
+        for (int i = 0; i < 3; ++i) pl->checks.push_back({i, 4, L * d, bound});
     uint64_t ws = 0;
     if (r == R_ATTN_F32_VALU || r == R_ATTN_I32_VALU) {
         // S = Q K^T into the workspace, then O = S V, both on the vector ALU.
@@ -712,6 +765,12 @@ struct qx_exec_s {
     Plan plan;
     void* ws;
     uint64_t ws_bytes;
+    // side stream and events of plans that overlap launches (operand
+    // encoding of the next batch group or column panel with the current
+    // contraction): evs[0] = run start, evs[1..n] = plan events, last = join
+    hipStream_t side;
+    std::vector<hipEvent_t> evs;
+    uint64_t flag_off;      // QX_VALIDATE flag word in the workspace
 };
 
 namespace {
@@ -738,12 +797,34 @@ qx_status make_exec(Plan&& pl, qx_exec* out) {
     h->magic = kMagic;
     h->device = dev;
     h->ws = nullptr;
+    h->side = nullptr;
     h->ws_bytes = (uint64_t)pl.info.workspace_bytes;
     h->plan = std::move(pl);
+    // QX_VALIDATE flag word behind the plan's workspace
+    h->flag_off = round_up(h->ws_bytes, 256);
+    if (!h->plan.checks.empty()) h->ws_bytes = h->flag_off + 256;
+    if (h->plan.n_events > 0) {
+        // default-priority side stream; events without timing
+        hipError_t e = hipStreamCreateWithFlags(&h->side, hipStreamNonBlocking);
+        for (int i = 0; e == hipSuccess && i < h->plan.n_events + 2; ++i) {
+            hipEvent_t ev = nullptr;
+            e = hipEventCreateWithFlags(&ev, hipEventDisableTiming);
+            if (e == hipSuccess) h->evs.push_back(ev);
+        }
+        if (e != hipSuccess) {
+            for (hipEvent_t ev : h->evs) (void)hipEventDestroy(ev);
+            if (h->side) (void)hipStreamDestroy(h->side);
+            h->magic = 0;
+            delete h;
+            return hip_fail(e, "executor stream/event creation");
+        }
+    }
     if (h->ws_bytes) {
         hipError_t e = hipMalloc(&h->ws, h->ws_bytes);
         if (e != hipSuccess) {
             h->ws = nullptr;
+            for (hipEvent_t ev : h->evs) (void)hipEventDestroy(ev);
+            if (h->side) (void)hipStreamDestroy(h->side);
             h->magic = 0;
             delete h;
             (void)hipGetLastError();
@@ -755,12 +836,58 @@ qx_status make_exec(Plan&& pl, qx_exec* out) {
         if (e == hipSuccess) e = hipDeviceSynchronize();
         if (e != hipSuccess) {
             (void)hipFree(h->ws);
+            for (hipEvent_t ev : h->evs) (void)hipEventDestroy(ev);
+            if (h->side) (void)hipStreamDestroy(h->side);
             h->magic = 0;
             delete h;
             return hip_fail(e, "workspace clear");
         }
     }
     *out = h;
+    return QX_OK;
+}
+
+qx_status launch_direct(LaunchRec& r, hipStream_t s) {
+    void* args[1] = {r.blob};
+    hipError_t e = hipLaunchKernel(r.fn, r.grid, r.block, args, r.shmem, s);
+    return e == hipSuccess ? QX_OK : hip_fail(e, r.name);
+}
+
+// QX_VALIDATE: scan every bounded operand, wait, and refuse the run if one
+// is outside its declared bound.
+qx_status validate_ranges(qx_exec h, const void* const* inputs, hipStream_t s) {
+    const Plan& pl = h->plan;
+    uint32_t* flag = (uint32_t*)((char*)h->ws + h->flag_off);
+    FillParams f{};
+    f.ptr = flag;
+    f.n32 = 1;
+    f.value = 0;
+    LaunchRec rf;
+    build_fill(f, &rf);
+    qx_status st = launch_direct(rf, s);
+    for (size_t i = 0; st == QX_OK && i < pl.checks.size(); ++i) {
+        const Plan::RangeCheck& c = pl.checks[i];
+        if (c.n == 0) continue;
+        RangeParams rp{};
+        rp.x = inputs[c.input];
+        rp.flag = flag;
+        rp.n = c.n;
+        rp.bound = c.bound;
+        rp.elem_bytes = c.elem_bytes;
+        rp.bit = 1u << i;
+        LaunchRec rr;
+        build_range(rp, &rr);
+        st = launch_direct(rr, s);
+    }
+    if (st) return st;
+    uint32_t bad = 0;
+    hipError_t e = hipMemcpyAsync(&bad, flag, sizeof bad, hipMemcpyDeviceToHost, s);
+    if (e == hipSuccess) e = hipStreamSynchronize(s);
+    if (e != hipSuccess) return hip_fail(e, "range scan");
+    for (size_t i = 0; i < pl.checks.size(); ++i)
+        if (bad & (1u << i))
+            return fail(QX_ERR_RANGE, "input %d has an element with |x| > %d (declared bound)", pl.checks[i].input,
+                        pl.checks[i].bound);
     return QX_OK;
 }
 
@@ -789,26 +916,49 @@ qx_status run_exec(qx_exec h, const void* const* inputs, void* output, void* str
     if (dev != h->device)
         return fail(QX_ERR_INVALID_ARG, "handle was created on device %d, current device is %d", h->device, dev);
     hipStream_t s = (hipStream_t)stream;
+    const char* val = getenv("QX_VALIDATE");
+    if (val && val[0] == '1' && !pl.checks.empty()) {
+        const qx_status st = validate_ranges(h, inputs, s);
+        if (st) return st;
+    }
+    // Overlapped plans fork to the side stream after everything already on
+    // the caller's stream and join back at the end.  Per-launch timing runs
+    // every launch in plan order on the caller's stream instead.
+    const bool lanes = pl.n_events > 0 && !evs;
+    if (lanes) {
+        if ((e = hipEventRecord(h->evs[0], s)) != hipSuccess) return hip_fail(e, "hipEventRecord");
+        if ((e = hipStreamWaitEvent(h->side, h->evs[0], 0)) != hipSuccess) return hip_fail(e, "hipStreamWaitEvent");
+    }
     for (const LaunchRec& r0 : pl.launches) {
         LaunchRec r = r0;
         for (int i = 0; i < r.nslots; ++i) {
             const Slot& sl = r.slots[i];
-            const void* ptr = nullptr;
+            const char* ptr = nullptr;
             switch (sl.bind) {
-            case BIND_IN0: ptr = inputs[0]; break;
-            case BIND_IN1: ptr = inputs[1]; break;
-            case BIND_IN2: ptr = inputs[2]; break;
-            case BIND_OUT: ptr = output; break;
-            case BIND_WS: ptr = (const char*)h->ws + sl.ws_off; break;
+            case BIND_IN0: ptr = (const char*)inputs[0]; break;
+            case BIND_IN1: ptr = (const char*)inputs[1]; break;
+            case BIND_IN2: ptr = (const char*)inputs[2]; break;
+            case BIND_OUT: ptr = (const char*)output; break;
+            case BIND_WS: ptr = (const char*)h->ws; break;
             }
+            ptr += sl.add;
             memcpy(r.blob + sl.off, &ptr, sizeof(void*));
         }
         void* args[1] = {r.blob};
         const size_t li = (size_t)(&r0 - pl.launches.data());
+        hipStream_t ls = (lanes && r.lane) ? h->side : s;
+        if (lanes && r.wait_ev >= 0 && (e = hipStreamWaitEvent(ls, h->evs[r.wait_ev], 0)) != hipSuccess)
+            return hip_fail(e, "hipStreamWaitEvent");
         if (evs && (e = hipEventRecord((*evs)[2 * li], s)) != hipSuccess) return hip_fail(e, "hipEventRecord");
-        e = hipLaunchKernel(r.fn, r.grid, r.block, args, r.shmem, s);
+        e = hipLaunchKernel(r.fn, r.grid, r.block, args, r.shmem, ls);
         if (e != hipSuccess) return hip_fail(e, r.name);
         if (evs && (e = hipEventRecord((*evs)[2 * li + 1], s)) != hipSuccess) return hip_fail(e, "hipEventRecord");
+        if (lanes && r.rec_ev >= 0 && (e = hipEventRecord(h->evs[r.rec_ev], ls)) != hipSuccess)
+            return hip_fail(e, "hipEventRecord");
+    }
+    if (lanes) {
+        if ((e = hipEventRecord(h->evs.back(), h->side)) != hipSuccess) return hip_fail(e, "hipEventRecord");
+        if ((e = hipStreamWaitEvent(s, h->evs.back(), 0)) != hipSuccess) return hip_fail(e, "hipStreamWaitEvent");
     }
     return QX_OK;
 }
@@ -1006,13 +1156,16 @@ qx_status qx_exec_destroy(qx_exec h) {
     if (h->magic != kMagic) return fail(QX_ERR_INVALID_ARG, "invalid executor handle");
     h->magic = 0;
     qx_status st = QX_OK;
-    if (h->ws) {
+    if (h->ws || h->side) {
         int cur = -1;
         (void)hipGetDevice(&cur);
         if (cur != h->device) (void)hipSetDevice(h->device);
         hipError_t e = hipDeviceSynchronize();
-        if (e == hipSuccess) e = hipFree(h->ws);
-        if (e != hipSuccess) st = hip_fail(e, "workspace free");
+        if (e == hipSuccess && h->ws) e = hipFree(h->ws);
+        for (hipEvent_t ev : h->evs)
+            if (e == hipSuccess) e = hipEventDestroy(ev);
+        if (e == hipSuccess && h->side) e = hipStreamDestroy(h->side);
+        if (e != hipSuccess) st = hip_fail(e, "executor release");
         if (cur != h->device && cur >= 0) (void)hipSetDevice(cur);
     }
     delete h;

@@ -770,6 +770,18 @@ __global__ __launch_bounds__(NT) void k_fill(const FillParams p) {
     if (i < p.n32) ((int32_t*)p.ptr)[i] = p.value;
 }
 
+// Range scan: a grid-stride pass; a wave with any lane out of range sets the
+// flag once (vector atomic).
+__global__ __launch_bounds__(NT) void k_range(const RangeParams p) {
+    const int64_t stride = (int64_t)gridDim.x * NT;
+    bool bad = false;
+    for (int64_t i = (int64_t)blockIdx.x * NT + threadIdx.x; i < p.n; i += stride) {
+        const int64_t v = p.elem_bytes == 2 ? (int64_t)((const int16_t*)p.x)[i] : (int64_t)((const int32_t*)p.x)[i];
+        bad |= v > p.bound || v < -(int64_t)p.bound;
+    }
+    if (__any(bad) && (threadIdx.x & 63) == __builtin_ctzll(__ballot(bad))) atomicOr(p.flag, p.bit);
+}
+
 // ===========================================================================
 // Builders
 // ===========================================================================
@@ -908,6 +920,16 @@ void build_im2col(const Im2colParams& p, LaunchRec* rec) {
     rec->grid = dim3((unsigned)((p.P + NT - 1) / NT), (unsigned)p.Kd, 1);
     rec->block = dim3(NT, 1, 1);
     rec->name = "im2col";
+    rec->set_params(p);
+}
+
+void build_range(const RangeParams& p, LaunchRec* rec) {
+    const int64_t blocks = std::min<int64_t>((p.n + NT - 1) / NT, 2048);
+    rec->fn = (const void*)k_range;
+    rec->grid = dim3((unsigned)std::max<int64_t>(blocks, 1), 1, 1);
+    rec->block = dim3(NT, 1, 1);
+    rec->shmem = 0;
+    rec->name = "range_check";
     rec->set_params(p);
 }
 

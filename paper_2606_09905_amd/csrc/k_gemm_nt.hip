@@ -71,13 +71,15 @@ __global__ __launch_bounds__(256) void k_enc_a(const EncParams p) {
 // B [batch][K][ldb] int16 -> BT16 [batch][Np][Kp] fp16 through a 64(k) x
 // 128(n) LDS transpose; 16-byte reads along n and 16-byte writes along k.
 __global__ __launch_bounds__(256) void k_enc_bt(const EncParams p) {
-    __shared__ __attribute__((aligned(16))) _Float16 t[128][64 + 8];
-    const int n0 = blockIdx.x * 128, k0 = blockIdx.y * 64, b = blockIdx.z;
+    // 64 x 64 blocks keep the LDS footprint at 9 KB, so these workgroups can
+    // share a CU with a resident 144 KB contraction workgroup.
+    __shared__ __attribute__((aligned(16))) _Float16 t[64][64 + 8];
+    const int n0 = blockIdx.x * 64, k0 = blockIdx.y * 64, b = blockIdx.z;
     const int16_t* src = (const int16_t*)p.src + b * p.s_src;
     const int tid = threadIdx.x;
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
-        const int idx = tid + 256 * q, kk = idx / 16, nv = (idx % 16) * 8;
+    for (int q = 0; q < 2; ++q) {
+        const int idx = tid + 256 * q, kk = idx / 8, nv = (idx % 8) * 8;
         const int k = k0 + kk, n = n0 + nv;
         const int16_t* s = src + (int64_t)k * p.ld_src + n;
         h8 h;
@@ -92,7 +94,7 @@ __global__ __launch_bounds__(256) void k_enc_bt(const EncParams p) {
     }
     __syncthreads();
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
+    for (int q = 0; q < 2; ++q) {
         const int idx = tid + 256 * q, nn = idx / 8, kc = (idx % 8) * 8;
         *(h8*)((_Float16*)p.dst + b * p.s_dst + (int64_t)(n0 + nn) * p.Kp + k0 + kc) = *(const h8*)&t[nn][kc];
     }
@@ -502,7 +504,7 @@ void build_enc_a(const EncParams& p, LaunchRec* rec) {
 
 void build_enc_bt(const EncParams& p, LaunchRec* rec) {
     rec->fn = (const void*)k_enc_bt;
-    rec->grid = dim3((unsigned)(p.Np / 128), (unsigned)(p.Kp / 64), (unsigned)p.batch);
+    rec->grid = dim3((unsigned)(p.Np / 64), (unsigned)(p.Kp / 64), (unsigned)p.batch);
     rec->block = dim3(256, 1, 1);
     rec->name = "enc_bt_f16";
     rec->set_params(p);

@@ -130,6 +130,16 @@ struct ReduceParams {
     int32_t splits;
 };
 
+// Operand range scan (QX_VALIDATE): sets *flag when some |x| > bound.
+struct RangeParams {
+    const void* x;
+    uint32_t* flag;
+    int64_t n;              // elements
+    int32_t bound;
+    int32_t elem_bytes;     // 2 (int16) or 4 (int32)
+    uint32_t bit;           // value or-ed into *flag
+};
+
 struct FillParams {
     void* ptr;
     int64_t n32;            // number of 32-bit words
@@ -163,9 +173,12 @@ enum Bind : uint8_t { BIND_IN0 = 0, BIND_IN1 = 1, BIND_IN2 = 2, BIND_OUT = 3, BI
 struct Slot {
     uint16_t off;           // byte offset of a pointer field in the parameter blob
     uint8_t bind;           // what it points at
-    uint64_t ws_off;        // BIND_WS: byte offset into the workspace
+    uint64_t add;           // byte offset added to the bound pointer
 };
 
+// A launch runs on the caller's stream (lane 0) or on the executor's side
+// stream (lane 1).  Cross-lane order is explicit: a launch may wait for an
+// executor event before it starts and record one when it is enqueued.
 struct LaunchRec {
     const void* fn = nullptr;
     dim3 grid{1, 1, 1};
@@ -176,6 +189,9 @@ struct LaunchRec {
     Slot slots[8];
     int nslots = 0;
     const char* name = "";
+    uint8_t lane = 0;
+    int16_t wait_ev = -1;
+    int16_t rec_ev = -1;
 
     template <class P>
     void set_params(const P& p) {
@@ -183,10 +199,10 @@ struct LaunchRec {
         memcpy(blob, &p, sizeof(P));
         blob_size = sizeof(P);
     }
-    void bind(size_t off, Bind b, uint64_t ws_off = 0) {
+    void bind(size_t off, Bind b, uint64_t add = 0) {
         slots[nslots].off = (uint16_t)off;
         slots[nslots].bind = b;
-        slots[nslots].ws_off = ws_off;
+        slots[nslots].add = add;
         ++nslots;
     }
 };
@@ -214,6 +230,7 @@ bool build_attn_f32(const AttnParams& p, LaunchRec* rec);
 bool build_attn_i32(const AttnParams& p, LaunchRec* rec);
 void build_reduce(const ReduceParams& p, LaunchRec* rec);
 void build_fill(const FillParams& p, LaunchRec* rec);
+void build_range(const RangeParams& p, LaunchRec* rec);
 // fp16-exact route for large problems: encoders + direct-to-LDS NT GEMM.
 void nt_tile_shape(int64_t M, int64_t N, int64_t batch, int* bm, int* bn);
 void build_gemm_nt(const GemmParams& p, int batch, LaunchRec* rec);

@@ -169,6 +169,24 @@ def test_gemm_s24_encode_nt_path(shape):
     same(got, orc.gemm_i32_s24(A, B), str(shape))
 
 
+@pytest.mark.parametrize("shape", [(1000, 1100, 1400, 3), (520, 700, 1000, 13)])
+def test_gemm_overlapped_batch_groups(shape):
+    # Large enough for the side-stream overlap: batch groups of 1 and of 2
+    # (13 batches in 7 groups, the last one short).
+    M, N, K, batch = shape
+    rng = np.random.default_rng(zlib.crc32(repr(("lanes", shape)).encode()))
+    A = rand_int(rng, (batch, M, K), 256, np.int16)
+    B = rand_int(rng, (batch, K, N), 256, np.int16)
+    groups = -(-batch // -(-batch // min(batch, 8)))
+    with qx.Executor.gemm_i16i32(M, N, K, batch, 256, 256) as ex:
+        plan = ex.plan()
+        assert plan["kernels"] == 3 * groups, plan
+        C = run_exec(ex, (A, B))
+        C2 = run_exec(ex, (A, B))
+    same(C2, C, "second run")
+    same(C, orc.gemm_i16i32(A, B))
+
+
 def test_f16_exact_mixed_magnitudes():
     # Products alternating between 2^16 and 1 inside one fp32 partial sum:
     # a narrow internal adder would lose the small terms.
@@ -380,6 +398,49 @@ def test_executor_profile_times_every_launch():
     assert names[:2] == ["enc_a_f16", "enc_bt_f16"] and names[2].startswith("gemm_nt_")
     assert all(ms > 0 for _, ms in prof)
     same(host(out), orc.gemm_i16i32(A, B))
+
+
+def test_validate_scan_refuses_out_of_contract_operands(monkeypatch):
+    # QX_VALIDATE=1: every bounded operand is scanned first; one element past
+    # its declared bound gives QX_ERR_RANGE naming the operand, and the
+    # output is left untouched.
+    monkeypatch.setenv("QX_VALIDATE", "1")
+    rng = np.random.default_rng(11)
+
+    def refused(ex, inputs, which, shape):
+        out = torch.full(shape, 7, dtype=ex.out_dtype, device="cuda")
+        with pytest.raises(qx.QxError) as e:
+            ex.run([dev(a) for a in inputs], out=out)
+        assert e.value.status == qx.ERR_RANGE and f"input {which}" in str(e.value), str(e.value)
+        assert bool((out == 7).all())
+
+    A = rand_int(rng, (2, 70, 90), 256, np.int16)
+    B = rand_int(rng, (2, 90, 50), 300, np.int16)
+    with qx.Executor.gemm_i16i32(70, 50, 90, 2, 256, 300) as ex:
+        same(run_exec(ex, (A, B)), orc.gemm_i16i32(A, B))       # at the bounds: runs
+        A2 = A.copy()
+        A2[1, 69, 89] = 257
+        refused(ex, (A2, B), 0, (2, 70, 50))
+        B2 = B.copy()
+        B2[0, 0, 0] = -301
+        refused(ex, (A, B2), 1, (2, 70, 50))
+    x = rand_int(rng, (2, 8, 9, 9), 100, np.int16)
+    w = rand_int(rng, (4, 8, 3, 3), 50, np.int16)
+    with qx.Executor.conv2d(2, 8, 9, 9, 4, 3, 3, 1, 1, 100, 50) as ex:
+        same(run_exec(ex, (x, w)), orc.conv2d_direct(x, w, 1, 1))
+        x2 = x.copy()
+        x2[1, 7, 8, 8] = 101
+        refused(ex, (x2, w), 0, (2, 4, 9, 9))
+    Q, K, V = (rand_int(rng, (64, 32), 64, np.int32) for _ in range(3))
+    with qx.Executor.attn("i32", 64, 32, 64) as ex:
+        same(run_exec(ex, (Q, K, V)), orc.attn_i32(Q, K, V))
+        V2 = V.copy()
+        V2[63, 31] = -65
+        refused(ex, (Q, K, V2), 2, (64, 32))
+    # without the variable nothing is scanned: the same call is enqueued
+    monkeypatch.delenv("QX_VALIDATE")
+    with qx.Executor.gemm_i16i32(70, 50, 90, 2, 256, 300) as ex:
+        run_exec(ex, (A2, B))
 
 
 def test_executor_reuse_and_errors():
