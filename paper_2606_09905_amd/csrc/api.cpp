@@ -324,18 +324,20 @@ qx_status plan_int_gemm(const GemmSpec& s, Plan* pl, uint64_t* ws_used) {
         rs_off = round_up(*ws_used, 256);
         cs_off = round_up(rs_off + 4 * (uint64_t)s.batch * (uint64_t)s.M, 256);
         *ws_used = cs_off + 4 * (uint64_t)s.batch * (uint64_t)slices * (uint64_t)s.N;
-        SumsParams sp{};
-        sp.sA = s.sA; sp.sB = s.sB;
-        sp.M = (int32_t)s.M; sp.N = (int32_t)s.N; sp.K = (int32_t)s.K;
-        sp.lda = (int32_t)s.lda; sp.ldb = (int32_t)s.ldb;
-        sp.s24 = s.s24 ? 1 : 0; sp.batch = (int32_t)s.batch;
-        LaunchRec rr;
-        build_sums(sp, &rr);
-        rr.bind(offsetof(SumsParams, A), s.a_bind);
-        rr.bind(offsetof(SumsParams, B), s.b_bind, s.b_ws_off);
-        rr.bind(offsetof(SumsParams, rowsum), BIND_WS, rs_off);
-        rr.bind(offsetof(SumsParams, colsum), BIND_WS, cs_off);
-        pl->launches.push_back(rr);
+        if (!nt8) {  // the limb-plane encoders produce the sums themselves
+            SumsParams sp{};
+            sp.sA = s.sA; sp.sB = s.sB;
+            sp.M = (int32_t)s.M; sp.N = (int32_t)s.N; sp.K = (int32_t)s.K;
+            sp.lda = (int32_t)s.lda; sp.ldb = (int32_t)s.ldb;
+            sp.s24 = s.s24 ? 1 : 0; sp.batch = (int32_t)s.batch;
+            LaunchRec rr;
+            build_sums(sp, &rr);
+            rr.bind(offsetof(SumsParams, A), s.a_bind);
+            rr.bind(offsetof(SumsParams, B), s.b_bind, s.b_ws_off);
+            rr.bind(offsetof(SumsParams, rowsum), BIND_WS, rs_off);
+            rr.bind(offsetof(SumsParams, colsum), BIND_WS, cs_off);
+            pl->launches.push_back(rr);
+        }
     }
     if (nt8) {
         // limb planes: A8 [batch][P][Mp][Kp], B8T [batch][P][Np][Kp] (int8)
@@ -357,6 +359,7 @@ qx_status plan_int_gemm(const GemmSpec& s, Plan* pl, uint64_t* ws_used) {
         build_enc_limb_a(route, s.s24, ea, &r1);
         r1.bind(offsetof(EncParams, src), s.a_bind);
         r1.bind(offsetof(EncParams, dst), BIND_WS, a_off);
+        if (offset) r1.bind(offsetof(EncParams, sums), BIND_WS, rs_off);
         EncParams eb{};
         eb.s_src = s.sB; eb.s_dst = P * Np * Kp;
         eb.N = (int32_t)s.N; eb.K = (int32_t)s.K;
@@ -367,6 +370,7 @@ qx_status plan_int_gemm(const GemmSpec& s, Plan* pl, uint64_t* ws_used) {
         build_enc_limb_bt(route, s.s24, eb, &r2);
         r2.bind(offsetof(EncParams, src), s.b_bind, s.b_ws_off);
         r2.bind(offsetof(EncParams, dst), BIND_WS, b_off);
+        if (offset) r2.bind(offsetof(EncParams, sums), BIND_WS, cs_off);
         g.sA = P * Mp * Kp; g.sB = P * Np * Kp;
         g.lda = (int32_t)Kp; g.ldb = (int32_t)Kp;
         g.plane_a = Mp * Kp; g.plane_b = Np * Kp;

@@ -223,14 +223,18 @@ __global__ __launch_bounds__(NT) void k_gemm_f16x(const GemmParams p) {
 // products into GROUPS accumulators, and recombines them mod 2^32.
 // PAD is the operand value whose limbs are all zero: padding a ragged K tail
 // with it adds nothing to any limb product.
+// value(x) is the integer the split represents (sext24 for smul24); offset
+// schemes (PAD != 0) need its row and column sums for the rank-1 correction.
 struct SchemeDirect {   // |x| <= 127
     static constexpr int PLANES = 1, GROUPS = 1, PRODUCTS = 1, PAD = 0;
+    template <class T> __device__ static int32_t value(T x) { return (int32_t)x; }
     static constexpr int pa[1] = {0}, pb[1] = {0}, pg[1] = {0};
     template <class T> __device__ static void split(T x, uint32_t* l) { l[0] = (uint32_t)x & 0xFFu; }
     __device__ static uint32_t combine(const uint32_t* g) { return g[0]; }
 };
 struct SchemeKaratsuba {  // x in [-8256, 8127]: balanced base 128, h, l, h+l
     static constexpr int PLANES = 3, GROUPS = 3, PRODUCTS = 3, PAD = 0;
+    template <class T> __device__ static int32_t value(T x) { return (int32_t)x; }
     static constexpr int pa[3] = {0, 1, 2}, pb[3] = {0, 1, 2}, pg[3] = {0, 1, 2};
     template <class T> __device__ static void split(T xv, uint32_t* l) {
         const int x = (int)xv;
@@ -247,6 +251,7 @@ struct SchemeKaratsuba {  // x in [-8256, 8127]: balanced base 128, h, l, h+l
 };
 struct SchemeOffset4 {  // any int16: x = 256*s1 + s0 + 128, s1 = x>>8, s0 = (x & 255) - 128
     static constexpr int PLANES = 2, GROUPS = 3, PRODUCTS = 4, PAD = 128;
+    template <class T> __device__ static int32_t value(T x) { return (int32_t)x; }
     static constexpr int pa[4] = {0, 0, 1, 1}, pb[4] = {0, 1, 0, 1}, pg[4] = {0, 1, 1, 2};
     template <class T> __device__ static void split(T xv, uint32_t* l) {
         const uint32_t x = (uint32_t)(int)xv;
@@ -257,6 +262,7 @@ struct SchemeOffset4 {  // any int16: x = 256*s1 + s0 + 128, s1 = x>>8, s0 = (x 
 };
 struct SchemeS24 {  // smul24: u = sext24(x) + 2^23, s_i = byte_i(u) - 128, x = sum 2^(8i) s_i + 32896
     static constexpr int PLANES = 3, GROUPS = 4, PRODUCTS = 8, PAD = 0x8080;
+    template <class T> __device__ static int32_t value(T x) { return (int32_t)((uint32_t)(int32_t)x << 8) >> 8; }
     static constexpr int pa[8] = {0, 0, 1, 0, 1, 2, 1, 2};
     static constexpr int pb[8] = {0, 1, 0, 2, 1, 0, 2, 1};
     static constexpr int pg[8] = {0, 1, 1, 2, 2, 2, 3, 3};
@@ -456,45 +462,53 @@ __global__ __launch_bounds__(NT) void k_gemm_i8limb(const GemmParams p) {
 // int8 limb routes for large problems: encode to limb planes, then an NT
 // int8 GEMM staged global -> LDS with global_load_lds_dwordx4.
 // ===========================================================================
-// A [batch][M][lda] (T) -> A8 [batch][P][Mp][Kp] int8 limb planes; a thread
-// splits 16 consecutive k of one row.  Elements outside M x K become all-zero
-// limbs (the split of S::PAD), which add nothing to any limb product.
+// A [batch][M][lda] (T) -> A8 [batch][P][Mp][Kp] int8 limb planes.  One wave
+// per row; a lane splits 16 consecutive k per step.  Elements outside M x K
+// become all-zero limbs (the split of S::PAD), which add nothing to any limb
+// product.  Offset schemes also get the row sums of the represented values
+// (wrapping), reduced across the wave.
 template <class S, class T>
 __global__ __launch_bounds__(NT) void k_enc_limb_a(const EncParams p) {
     constexpr int P = S::PLANES;
-    const int kv = p.Kp / 16;
-    const int64_t per_b = (int64_t)p.Mp * kv;
-    const int64_t v = (int64_t)blockIdx.x * NT + threadIdx.x;
-    if (v >= per_b * p.batch) return;
-    const int b = (int)(v / per_b);
-    const int64_t r = v - (int64_t)b * per_b;
-    const int m = (int)(r / kv), k0 = (int)(r - (int64_t)m * kv) * 16;
-    const T* src = (const T*)p.src + b * p.s_src + (int64_t)m * p.ld_src + k0;
-    T x[16];
-    bool ok[16];
-    if (p.vec && m < p.M && k0 + 16 <= p.K) {
-        load_vec<T, 16>(src, x);
+    constexpr bool SUMS = S::PAD != 0;
+    const int lane = threadIdx.x & 63;
+    const int64_t rowg = (int64_t)blockIdx.x * (NT / 64) + (threadIdx.x >> 6);
+    if (rowg >= (int64_t)p.batch * p.Mp) return;                     // whole wave
+    const int b = (int)(rowg / p.Mp), m = (int)(rowg - (int64_t)b * p.Mp);
+    const T* src = (const T*)p.src + b * p.s_src + (int64_t)m * p.ld_src;
+    int8_t* dst = (int8_t*)p.dst + b * p.s_dst + (int64_t)m * p.Kp;
+    uint32_t sum = 0;
+    for (int k0 = lane * 16; k0 < p.Kp; k0 += 64 * 16) {
+        T x[16];
+        bool ok[16];
+        if (p.vec && m < p.M && k0 + 16 <= p.K) {
+            load_vec<T, 16>(src + k0, x);
 #pragma unroll
-        for (int e = 0; e < 16; ++e) ok[e] = true;
-    } else {
+            for (int e = 0; e < 16; ++e) ok[e] = true;
+        } else {
+#pragma unroll
+            for (int e = 0; e < 16; ++e) {
+                ok[e] = m < p.M && k0 + e < p.K;
+                x[e] = ok[e] ? src[k0 + e] : (T)0;
+            }
+        }
+        uint32_t w[P][4] = {};
 #pragma unroll
         for (int e = 0; e < 16; ++e) {
-            ok[e] = m < p.M && k0 + e < p.K;
-            x[e] = ok[e] ? src[e] : (T)0;
+            uint32_t l[P];
+            S::split(x[e], l);
+#pragma unroll
+            for (int q = 0; q < P; ++q) w[q][e >> 2] |= (ok[e] ? l[q] : 0u) << (8 * (e & 3));
+            if (SUMS && ok[e]) sum += (uint32_t)S::value(x[e]);
         }
+#pragma unroll
+        for (int q = 0; q < P; ++q)
+            *(i4*)(dst + (int64_t)q * p.Mp * p.Kp + k0) = i4{(int)w[q][0], (int)w[q][1], (int)w[q][2], (int)w[q][3]};
     }
-    uint32_t w[P][4] = {};
-#pragma unroll
-    for (int e = 0; e < 16; ++e) {
-        uint32_t l[P];
-        S::split(x[e], l);
-#pragma unroll
-        for (int q = 0; q < P; ++q) w[q][e >> 2] |= (ok[e] ? l[q] : 0u) << (8 * (e & 3));
+    if (SUMS) {
+        for (int off = 32; off > 0; off >>= 1) sum += __shfl_xor(sum, off, 64);
+        if (lane == 0 && m < p.M) p.sums[(int64_t)b * p.M + m] = (int32_t)sum;
     }
-    int8_t* dst = (int8_t*)p.dst + b * p.s_dst + (int64_t)m * p.Kp + k0;
-#pragma unroll
-    for (int q = 0; q < P; ++q)
-        *(i4*)(dst + (int64_t)q * p.Mp * p.Kp) = i4{(int)w[q][0], (int)w[q][1], (int)w[q][2], (int)w[q][3]};
 }
 
 // B [batch][K][ldb] (T) -> B8T [batch][P][Np][Kp]: a workgroup transposes a
@@ -504,12 +518,18 @@ __global__ __launch_bounds__(NT) void k_enc_limb_a(const EncParams p) {
 template <class S, class T>
 __global__ __launch_bounds__(NT) void k_enc_limb_bt(const EncParams p) {
     constexpr int P = S::PLANES, RW = 17;     // LDS row: 16 dwords of k + 1 to spread banks
+    constexpr bool SUMS = S::PAD != 0;
     __shared__ uint32_t t[P][64][RW];
+    __shared__ uint32_t cs[64];
     const int n0 = blockIdx.x * 64, k0 = blockIdx.y * 64, b = blockIdx.z;
     const T* src = (const T*)p.src + b * p.s_src;
     const int tid = threadIdx.x, kg = tid >> 4, ng = tid & 15;
     const int kb = k0 + kg * 4, nb = n0 + ng * 4;
-    uint32_t w[P][4] = {};
+    if (SUMS) {
+        if (tid < 64) cs[tid] = 0;
+        __syncthreads();
+    }
+    uint32_t w[P][4] = {}, csum[4] = {};
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
         const int k = kb + r;
@@ -533,13 +553,20 @@ __global__ __launch_bounds__(NT) void k_enc_limb_bt(const EncParams p) {
             S::split(x[c], l);
 #pragma unroll
             for (int q = 0; q < P; ++q) w[q][c] |= (ok[c] ? l[q] : 0u) << (8 * r);
+            if (SUMS && ok[c]) csum[c] += (uint32_t)S::value(x[c]);
         }
     }
 #pragma unroll
     for (int q = 0; q < P; ++q)
 #pragma unroll
         for (int c = 0; c < 4; ++c) t[q][ng * 4 + c][kg] = w[q][c];
+    if (SUMS)
+#pragma unroll
+        for (int c = 0; c < 4; ++c) atomicAdd(&cs[ng * 4 + c], csum[c]);
     __syncthreads();
+    // column sums of this 64-k slice: [batch][Kp/64][N]
+    if (SUMS && tid < 64 && n0 + tid < p.N)
+        p.sums[((int64_t)b * gridDim.y + blockIdx.y) * p.N + n0 + tid] = (int32_t)cs[tid];
     const int nn = tid >> 2, kc = (tid & 3) * 4;
     int8_t* dst = (int8_t*)p.dst + b * p.s_dst + (int64_t)(n0 + nn) * p.Kp + k0 + kc * 4;
 #pragma unroll
@@ -865,9 +892,9 @@ static void enc_limb_recs(bool s24, bool bt, const EncParams& p, LaunchRec* rec,
         rec->fn = s24 ? (const void*)k_enc_limb_bt<S, int32_t> : (const void*)k_enc_limb_bt<S, int16_t>;
         rec->grid = dim3((unsigned)(p.Np / 64), (unsigned)(p.Kp / 64), (unsigned)p.batch);
     } else {
-        const int64_t n = (int64_t)p.batch * p.Mp * (p.Kp / 16);
+        const int64_t rows = (int64_t)p.batch * p.Mp;    // one wave per row
         rec->fn = s24 ? (const void*)k_enc_limb_a<S, int32_t> : (const void*)k_enc_limb_a<S, int16_t>;
-        rec->grid = dim3((unsigned)((n + NT - 1) / NT), 1, 1);
+        rec->grid = dim3((unsigned)((rows + NT / 64 - 1) / (NT / 64)), 1, 1);
     }
     rec->block = dim3(NT, 1, 1);
     rec->shmem = 0;

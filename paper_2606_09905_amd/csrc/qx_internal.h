@@ -86,6 +86,9 @@ struct EncParams {
     int32_t ld_src;
     int32_t batch;
     int32_t vec;            // rows and batch strides allow 16-byte source loads
+    int32_t* sums;          // int8 limb routes with an offset: row sums [batch][M] of A
+                            // (A encoder) or per-64-k-slice column sums [batch][Kp/64][N]
+                            // of B (B^T encoder), of the values the split represents
 };
 
 // Convolution lowering into the transposed fp16 column matrix colT [Pp][Kp].
