@@ -29,16 +29,68 @@ METRIC = "GOPS (2·M·N·K/s) packed INT16/INT32 GEMM; conv & attention-core GOP
 # MI355X datasheet peaks (dense)
 PEAK = {"f16": 2500.0, "i8": 5000.0, "f32": 157.3, "hbm": 8000.0}  # TFLOP/s, TOP/s, GB/s
 
+# HBM bytes per launch of the headline contraction, from two rocprofv3 counter
+# passes (FETCH_SIZE, WRITE_SIZE) over this benchmark, each scaled by what the
+# counter reads for a 1 GiB device copy (`--copy-calibration`).  Valid only for
+# the kernel source they were taken on: the SHA-256 of the contraction
+# kernel's text is compared at run time and the figure is dropped (null) if
+# the kernel has changed since.
+TRAFFIC = {
+    "kernel": "gemm_nt_128x256",
+    "kernel_sha256": "5f342e1d9dced801038c2bd96e08bc3bf5ee1cf5ea44d73d72222c7e7f6ae5e2",
+    "read_bytes": 2149179579,     # FETCH_SIZE 1049435 KiB x 2.0 (copy: 524304 KiB per GiB read)
+    "write_bytes": 268435456,     # WRITE_SIZE 262144 KiB x 1.0 (copy: 1048576 KiB per GiB written)
+}
+KERNEL_SRC = os.path.join(ROOT, "paper_2606_09905_amd", "csrc", "k_gemm_nt.hip")
+
+
+def contraction_sha256():
+    """SHA-256 of the fp16-exact contraction kernel's source text (the
+    k_gemm_nt template up to the builders)."""
+    import hashlib
+    try:
+        src = open(KERNEL_SRC).read()
+        a = src.index("template <int BM, int BN, int NW, bool IMPL>")
+        b = src.index("// Builders", a)
+    except (OSError, ValueError):
+        return None
+    return hashlib.sha256(src[a:b].encode()).hexdigest()
+
+
+def traffic_bytes(kernel, launches):
+    """Measured HBM bytes per launch (read + written), or None."""
+    t = TRAFFIC
+    if kernel != t["kernel"] or t["read_bytes"] is None or launches != 1:
+        return None
+    if t["kernel_sha256"] is None or contraction_sha256() != t["kernel_sha256"]:
+        return None
+    return t["read_bytes"] + t["write_bytes"]
+
+
+def copy_calibration(torch):
+    n = 1 << 28                      # 2^28 float32 = 1 GiB
+    a = torch.ones(n, dtype=torch.float32, device="cuda")
+    b = torch.empty_like(a)
+    torch.cuda.synchronize()
+    for _ in range(2):
+        b.copy_(a)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_calibration": "2 x 1 GiB device-to-device copies"}), flush=True)
+
 
 def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=5)
+    # the GPU needs a few tens of milliseconds of load to reach its steady
+    # clocks: the default warmup covers that
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=50)
     ap.add_argument("--workload", default=HEADLINE)
     ap.add_argument("--all", action="store_true", help="also measure every workload")
     ap.add_argument("--all-out", default=os.path.join(ROOT, "gpurun_out", "bench_all.json"))
     ap.add_argument("--no-cpu", action="store_true", help="skip the oracle CPU baseline")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="only run two 1 GiB device-to-device copies (HBM counter calibration)")
     ap.add_argument("--cpu-rows", type=int, default=8192,
                     help="rows of A in the oracle's CPU sample of the headline GEMM")
     return ap.parse_args()
@@ -135,6 +187,9 @@ def main():
     if not torch.cuda.is_available():
         print(json.dumps({"error": "no GPU visible"}), flush=True)
         sys.exit(1)
+    if args.copy_calibration:
+        copy_calibration(torch)
+        return
     qx.lib()
     w = WORKLOADS[args.workload]
     r = measure(w, args.steps, args.warmup, torch, qx)
@@ -177,7 +232,7 @@ def main():
             "peak": peak,
             "unit": "TFLOP/s" if unit_peak in ("f16", "f32") else "TOP/s",
             "frac": round(achieved_tflops / peak, 4),
-            "traffic": None,
+            "traffic": traffic_bytes(dom_name, dom_launches),
             "kernel": dom_name,
             "kernel_ms": round(dom_ms, 4),
             "kernel_launches": dom_launches,

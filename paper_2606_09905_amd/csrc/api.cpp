@@ -349,28 +349,29 @@ qx_status plan_int_gemm(const GemmSpec& s, Plan* pl, uint64_t* ws_used) {
         const uint64_t b_off = round_up(a_off + (uint64_t)s.batch * P * Mp * Kp, 256);
         *ws_used = b_off + (uint64_t)s.batch * P * Np * Kp;
         const int64_t v16 = s.s24 ? 4 : 8;   // elements per 16 bytes
-        EncParams ea{};
+        EncPairParams ep{};
+        EncParams& ea = ep.a;
         ea.s_src = s.sA; ea.s_dst = P * Mp * Kp;
         ea.M = (int32_t)s.M; ea.K = (int32_t)s.K;
         ea.Mp = (int32_t)Mp; ea.Kp = (int32_t)Kp;
         ea.ld_src = (int32_t)s.lda; ea.batch = (int32_t)s.batch;
         ea.vec = (s.lda % v16 == 0 && s.sA % v16 == 0) ? 1 : 0;
-        LaunchRec r1;
-        build_enc_limb_a(route, s.s24, ea, &r1);
-        r1.bind(offsetof(EncParams, src), s.a_bind);
-        r1.bind(offsetof(EncParams, dst), BIND_WS, a_off);
-        if (offset) r1.bind(offsetof(EncParams, sums), BIND_WS, rs_off);
-        EncParams eb{};
+        EncParams& eb = ep.b;
         eb.s_src = s.sB; eb.s_dst = P * Np * Kp;
         eb.N = (int32_t)s.N; eb.K = (int32_t)s.K;
         eb.Np = (int32_t)Np; eb.Kp = (int32_t)Kp;
         eb.ld_src = (int32_t)s.ldb; eb.batch = (int32_t)s.batch;
         eb.vec = (s.ldb % 4 == 0 && s.sB % 4 == 0) ? 1 : 0;
-        LaunchRec r2;
-        build_enc_limb_bt(route, s.s24, eb, &r2);
-        r2.bind(offsetof(EncParams, src), s.b_bind, s.b_ws_off);
-        r2.bind(offsetof(EncParams, dst), BIND_WS, b_off);
-        if (offset) r2.bind(offsetof(EncParams, sums), BIND_WS, cs_off);
+        LaunchRec r1;
+        build_enc_limb(route, s.s24, ep, &r1);
+        r1.bind(offsetof(EncPairParams, a) + offsetof(EncParams, src), s.a_bind);
+        r1.bind(offsetof(EncPairParams, a) + offsetof(EncParams, dst), BIND_WS, a_off);
+        r1.bind(offsetof(EncPairParams, b) + offsetof(EncParams, src), s.b_bind, s.b_ws_off);
+        r1.bind(offsetof(EncPairParams, b) + offsetof(EncParams, dst), BIND_WS, b_off);
+        if (offset) {
+            r1.bind(offsetof(EncPairParams, a) + offsetof(EncParams, sums), BIND_WS, rs_off);
+            r1.bind(offsetof(EncPairParams, b) + offsetof(EncParams, sums), BIND_WS, cs_off);
+        }
         g.sA = P * Mp * Kp; g.sB = P * Np * Kp;
         g.lda = (int32_t)Kp; g.ldb = (int32_t)Kp;
         g.plane_a = Mp * Kp; g.plane_b = Np * Kp;
@@ -385,7 +386,6 @@ qx_status plan_int_gemm(const GemmSpec& s, Plan* pl, uint64_t* ws_used) {
             r3.bind(offsetof(GemmParams, colsum), BIND_WS, cs_off);
         }
         pl->launches.push_back(r1);
-        pl->launches.push_back(r2);
         pl->launches.push_back(r3);
         info.tile_m = bm; info.tile_n = bn; info.tile_k = 64;
         return QX_OK;

@@ -252,7 +252,8 @@ struct SchemeKaratsuba {  // x in [-8256, 8127]: balanced base 128, h, l, h+l
 struct SchemeOffset4 {  // any int16: x = 256*s1 + s0 + 128, s1 = x>>8, s0 = (x & 255) - 128
     static constexpr int PLANES = 2, GROUPS = 3, PRODUCTS = 4, PAD = 128;
     template <class T> __device__ static int32_t value(T x) { return (int32_t)x; }
-    static constexpr int pa[4] = {0, 0, 1, 1}, pb[4] = {0, 1, 0, 1}, pg[4] = {0, 1, 1, 2};
+    // product order keeps consecutive MFMAs on different accumulators
+    static constexpr int pa[4] = {0, 0, 1, 1}, pb[4] = {0, 1, 1, 0}, pg[4] = {0, 1, 2, 1};
     template <class T> __device__ static void split(T xv, uint32_t* l) {
         const uint32_t x = (uint32_t)(int)xv;
         l[0] = (x >> 8) & 0xFFu;          // s1 (arithmetic high byte of an int16)
@@ -263,9 +264,11 @@ struct SchemeOffset4 {  // any int16: x = 256*s1 + s0 + 128, s1 = x>>8, s0 = (x 
 struct SchemeS24 {  // smul24: u = sext24(x) + 2^23, s_i = byte_i(u) - 128, x = sum 2^(8i) s_i + 32896
     static constexpr int PLANES = 3, GROUPS = 4, PRODUCTS = 8, PAD = 0x8080;
     template <class T> __device__ static int32_t value(T x) { return (int32_t)((uint32_t)(int32_t)x << 8) >> 8; }
-    static constexpr int pa[8] = {0, 0, 1, 0, 1, 2, 1, 2};
-    static constexpr int pb[8] = {0, 1, 0, 2, 1, 0, 2, 1};
-    static constexpr int pg[8] = {0, 1, 1, 2, 2, 2, 3, 3};
+    // limb pairs (i, j) with i + j <= 3 into group i + j, ordered so that
+    // consecutive MFMAs never accumulate into the same group
+    static constexpr int pa[8] = {0, 0, 0, 1, 1, 1, 2, 2};
+    static constexpr int pb[8] = {0, 1, 2, 2, 0, 1, 1, 0};
+    static constexpr int pg[8] = {0, 1, 2, 3, 1, 2, 3, 2};
     template <class T> __device__ static void split(T xv, uint32_t* l) {
         const uint32_t u = ((uint32_t)(int)xv & 0xFFFFFFu) ^ 0x808080u ^ 0x800000u;
         l[0] = u & 0xFFu;
@@ -468,11 +471,11 @@ __global__ __launch_bounds__(NT) void k_gemm_i8limb(const GemmParams p) {
 // product.  Offset schemes also get the row sums of the represented values
 // (wrapping), reduced across the wave.
 template <class S, class T>
-__global__ __launch_bounds__(NT) void k_enc_limb_a(const EncParams p) {
+__device__ __forceinline__ void enc_limb_a(const EncParams& p, int blk) {
     constexpr int P = S::PLANES;
     constexpr bool SUMS = S::PAD != 0;
     const int lane = threadIdx.x & 63;
-    const int64_t rowg = (int64_t)blockIdx.x * (NT / 64) + (threadIdx.x >> 6);
+    const int64_t rowg = (int64_t)blk * (NT / 64) + (threadIdx.x >> 6);
     if (rowg >= (int64_t)p.batch * p.Mp) return;                     // whole wave
     const int b = (int)(rowg / p.Mp), m = (int)(rowg - (int64_t)b * p.Mp);
     const T* src = (const T*)p.src + b * p.s_src + (int64_t)m * p.ld_src;
@@ -516,12 +519,14 @@ __global__ __launch_bounds__(NT) void k_enc_limb_a(const EncParams p) {
 // bytes of each column and plane into one dword, and stages it in LDS; the
 // rows then leave as 16-byte runs along k.
 template <class S, class T>
-__global__ __launch_bounds__(NT) void k_enc_limb_bt(const EncParams p) {
+__device__ __forceinline__ void enc_limb_bt(const EncParams& p, int blk) {
     constexpr int P = S::PLANES, RW = 17;     // LDS row: 16 dwords of k + 1 to spread banks
     constexpr bool SUMS = S::PAD != 0;
     __shared__ uint32_t t[P][64][RW];
     __shared__ uint32_t cs[64];
-    const int n0 = blockIdx.x * 64, k0 = blockIdx.y * 64, b = blockIdx.z;
+    const int nb64 = p.Np / 64, kb64 = p.Kp / 64;
+    const int bx = blk % nb64, by = (blk / nb64) % kb64, b = blk / (nb64 * kb64);
+    const int n0 = bx * 64, k0 = by * 64;
     const T* src = (const T*)p.src + b * p.s_src;
     const int tid = threadIdx.x, kg = tid >> 4, ng = tid & 15;
     const int kb = k0 + kg * 4, nb = n0 + ng * 4;
@@ -566,7 +571,7 @@ __global__ __launch_bounds__(NT) void k_enc_limb_bt(const EncParams p) {
     __syncthreads();
     // column sums of this 64-k slice: [batch][Kp/64][N]
     if (SUMS && tid < 64 && n0 + tid < p.N)
-        p.sums[((int64_t)b * gridDim.y + blockIdx.y) * p.N + n0 + tid] = (int32_t)cs[tid];
+        p.sums[((int64_t)b * kb64 + by) * p.N + n0 + tid] = (int32_t)cs[tid];
     const int nn = tid >> 2, kc = (tid & 3) * 4;
     int8_t* dst = (int8_t*)p.dst + b * p.s_dst + (int64_t)(n0 + nn) * p.Kp + k0 + kc * 4;
 #pragma unroll
@@ -576,14 +581,43 @@ __global__ __launch_bounds__(NT) void k_enc_limb_bt(const EncParams p) {
     }
 }
 
+// Both limb encoders in one launch: blocks [0, blocks_a) encode A (four rows
+// each), the rest encode 64 x 64 blocks of B^T.
+template <class S, class T>
+__global__ __launch_bounds__(NT) void k_enc_limb(const EncPairParams p) {
+    if ((int)blockIdx.x < p.blocks_a) enc_limb_a<S, T>(p.a, blockIdx.x);
+    else enc_limb_bt<S, T>(p.b, blockIdx.x - p.blocks_a);
+}
+
 // 64-byte LDS rows (64 int8) as four 16-byte chunks; the 16 rows of one
 // ds_read_b128 lane group land in distinct banks.
 __device__ __forceinline__ int swz_i8(int row) { return (row >> 2) & 3; }
 
-template <class S, int BM, int BN>
+// Wait until at most n K tiles of LPT direct-to-LDS loads each are still in
+// flight (s_waitcnt takes an immediate; a count past the 6-bit field waits
+// for more, which is still correct).
+template <int LPT>
+__device__ __forceinline__ void wait_tiles(int n) {
+#define QX_WAIT(k)                                                           \
+    {                                                                        \
+        constexpr int c = (k) * LPT > 63 ? 63 : (k) * LPT;                   \
+        __builtin_amdgcn_s_waitcnt((c & 15) | ((c >> 4) << 14) | 0x0F70);   \
+    }
+    switch (n) {
+    case 0: QX_WAIT(0) break;
+    case 1: QX_WAIT(1) break;
+    case 2: QX_WAIT(2) break;
+    case 3: QX_WAIT(3) break;
+    default: QX_WAIT(4) break;
+    }
+#undef QX_WAIT
+}
+
+template <class S, int BM, int BN, int STAGES>
 __global__ __launch_bounds__(NT) void k_gemm_i8nt(const GemmParams p) {
     constexpr int BK = 64, KCH = 4, P = S::PLANES, G = S::GROUPS;
-    constexpr int WM = BM / 2, WN = BN / 2, TM = WM / 32, TN = WN / 32, STAGES = 3;
+    constexpr int WM = BM / 2, WN = BN / 2, TM = WM / 32, TN = WN / 32;
+    static_assert(STAGES >= 3 && STAGES <= 6, "ring depth");
     constexpr int AL = P * BM * KCH / NT, BL = P * BN * KCH / NT, LPT = AL + BL;
     static_assert(AL * NT == P * BM * KCH && BL * NT == P * BN * KCH, "whole loads");
     constexpr unsigned STAGE_A = P * BM * KCH * 16, STAGE_B = P * BN * KCH * 16;
@@ -656,8 +690,8 @@ __global__ __launch_bounds__(NT) void k_gemm_i8nt(const GemmParams p) {
     for (int s = 0; s < STAGES - 1; ++s)
         if (s < ktiles) issue(s);
     for (int t = 0; t < ktiles; ++t) {
-        if (t + 1 < ktiles) __builtin_amdgcn_s_waitcnt((LPT & 15) | ((LPT >> 4) << 14) | 0x0F70);
-        else __builtin_amdgcn_s_waitcnt(0x0F70);
+        // tile t must have landed; the tiles after it may still be in flight
+        wait_tiles<LPT>(min(STAGES - 2, ktiles - 1 - t));
         __syncthreads();
         if (t + STAGES - 1 < ktiles) issue(t + STAGES - 1);
         const int s = t % STAGES;
@@ -887,39 +921,34 @@ void i8nt_tile_shape(int32_t route, int64_t M, int64_t N, int64_t batch, int* bm
 }
 
 template <class S>
-static void enc_limb_recs(bool s24, bool bt, const EncParams& p, LaunchRec* rec, const char* name) {
-    if (bt) {
-        rec->fn = s24 ? (const void*)k_enc_limb_bt<S, int32_t> : (const void*)k_enc_limb_bt<S, int16_t>;
-        rec->grid = dim3((unsigned)(p.Np / 64), (unsigned)(p.Kp / 64), (unsigned)p.batch);
-    } else {
-        const int64_t rows = (int64_t)p.batch * p.Mp;    // one wave per row
-        rec->fn = s24 ? (const void*)k_enc_limb_a<S, int32_t> : (const void*)k_enc_limb_a<S, int16_t>;
-        rec->grid = dim3((unsigned)((rows + NT / 64 - 1) / (NT / 64)), 1, 1);
-    }
+static void enc_limb_rec(bool s24, const EncPairParams& p0, LaunchRec* rec, const char* name) {
+    EncPairParams p = p0;
+    p.blocks_a = (int32_t)(((int64_t)p.a.batch * p.a.Mp + NT / 64 - 1) / (NT / 64));   // a wave per row
+    const int64_t blocks_b = (int64_t)(p.b.Np / 64) * (p.b.Kp / 64) * p.b.batch;
+    rec->fn = s24 ? (const void*)k_enc_limb<S, int32_t> : (const void*)k_enc_limb<S, int16_t>;
+    rec->grid = dim3((unsigned)(p.blocks_a + blocks_b), 1, 1);
     rec->block = dim3(NT, 1, 1);
     rec->shmem = 0;
     rec->name = name;
     rec->set_params(p);
 }
 
-static void enc_limb(int32_t route, bool s24, bool bt, const EncParams& p, LaunchRec* rec) {
+void build_enc_limb(int32_t route, bool s24, const EncPairParams& p, LaunchRec* rec) {
     switch (route) {
-    case R_I8_DIRECT: enc_limb_recs<SchemeDirect>(s24, bt, p, rec, bt ? "enc_limb_bt_direct" : "enc_limb_a_direct"); break;
-    case R_I8_KARATSUBA: enc_limb_recs<SchemeKaratsuba>(s24, bt, p, rec, bt ? "enc_limb_bt_karatsuba" : "enc_limb_a_karatsuba"); break;
-    case R_I8_OFFSET4: enc_limb_recs<SchemeOffset4>(s24, bt, p, rec, bt ? "enc_limb_bt_offset4" : "enc_limb_a_offset4"); break;
-    default: enc_limb_recs<SchemeS24>(s24, bt, p, rec, bt ? "enc_limb_bt_s24" : "enc_limb_a_s24"); break;
+    case R_I8_DIRECT: enc_limb_rec<SchemeDirect>(s24, p, rec, "enc_limb_direct"); break;
+    case R_I8_KARATSUBA: enc_limb_rec<SchemeKaratsuba>(s24, p, rec, "enc_limb_karatsuba"); break;
+    case R_I8_OFFSET4: enc_limb_rec<SchemeOffset4>(s24, p, rec, "enc_limb_offset4"); break;
+    default: enc_limb_rec<SchemeS24>(s24, p, rec, "enc_limb_s24"); break;
     }
 }
-void build_enc_limb_a(int32_t route, bool s24, const EncParams& p, LaunchRec* rec) { enc_limb(route, s24, false, p, rec); }
-void build_enc_limb_bt(int32_t route, bool s24, const EncParams& p, LaunchRec* rec) { enc_limb(route, s24, true, p, rec); }
 
 bool build_gemm_i8nt(int32_t route, const GemmParams& p0, int batch, LaunchRec* rec) {
     int bm, bn;
     i8nt_tile_shape(route, p0.M, p0.N, batch, &bm, &bn);
     const bool big = bm == 128;
 #define QX_NT(S, NAME)                                                                               \
-    if (big) fill_gemm_rec(rec, k_gemm_i8nt<S, 128, 128>, p0, 128, 128, batch, "gemm_i8nt_" NAME "_128x128"); \
-    else fill_gemm_rec(rec, k_gemm_i8nt<S, 64, 64>, p0, 64, 64, batch, "gemm_i8nt_" NAME "_64x64");
+    if (big) fill_gemm_rec(rec, k_gemm_i8nt<S, 128, 128, 3>, p0, 128, 128, batch, "gemm_i8nt_" NAME "_128x128"); \
+    else fill_gemm_rec(rec, k_gemm_i8nt<S, 64, 64, 6>, p0, 64, 64, batch, "gemm_i8nt_" NAME "_64x64");
     switch (route) {
     case R_I8_DIRECT: QX_NT(SchemeDirect, "direct") return true;
     case R_I8_KARATSUBA: QX_NT(SchemeKaratsuba, "karatsuba") return true;

@@ -91,6 +91,13 @@ struct EncParams {
                             // of B (B^T encoder), of the values the split represents
 };
 
+// Both operand encoders of the int8 limb routes in one launch.
+struct EncPairParams {
+    EncParams a;            // A -> A8 [batch][P][Mp][Kp]
+    EncParams b;            // B -> B8T [batch][P][Np][Kp]
+    int32_t blocks_a;       // leading blocks that encode A
+};
+
 // Convolution lowering into the transposed fp16 column matrix colT [Pp][Kp].
 struct Im2colTParams {
     const int16_t* x;
@@ -243,8 +250,7 @@ void build_im2col_t(const Im2colTParams& p, LaunchRec* rec);
 void build_conv_prep(const ConvPrepParams& p, LaunchRec* rec);
 // int8 limb routes for large problems: limb-plane encoders + direct-to-LDS NT GEMM.
 void i8nt_tile_shape(int32_t route, int64_t M, int64_t N, int64_t batch, int* bm, int* bn);
-void build_enc_limb_a(int32_t route, bool s24, const EncParams& p, LaunchRec* rec);
-void build_enc_limb_bt(int32_t route, bool s24, const EncParams& p, LaunchRec* rec);
+void build_enc_limb(int32_t route, bool s24, const EncPairParams& p, LaunchRec* rec);
 bool build_gemm_i8nt(int32_t route, const GemmParams& p, int batch, LaunchRec* rec);
 
 }  // namespace qx
