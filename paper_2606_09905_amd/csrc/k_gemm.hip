@@ -79,7 +79,8 @@ __global__ __launch_bounds__(NT) void k_gemm_f16x(const GemmParams p) {
     static_assert((BM / WM) * (BN / WN) == 4, "four waves");
     constexpr int A_VECS = BM * KCH / NT;         // 16-byte A vectors per thread
     constexpr int B_NBLK = BN / 8;                // B staged as 4(k) x 8(n) blocks
-    static_assert((BK / 4) * B_NBLK == NT, "one B block per thread");
+    constexpr int B_THREADS = (BK / 4) * B_NBLK;  // threads that stage one B block each
+    static_assert(B_THREADS <= NT && NT % B_THREADS == 0, "B blocks");
 
     __shared__ h8 As[2][BM][KCH];
     __shared__ h8 Bs[2][BN][KCH];
@@ -112,6 +113,7 @@ __global__ __launch_bounds__(NT) void k_gemm_f16x(const GemmParams p) {
                     ra[i][e] = (gm < p.M && gk + e < p.K) ? A[(int64_t)gm * p.lda + gk + e] : (short)0;
             }
         }
+        if (B_THREADS < NT && tid >= B_THREADS) return;
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
             const int gk = k0 + bkb * 4 + r, gn = n0 + bnb * 8;
@@ -133,6 +135,7 @@ __global__ __launch_bounds__(NT) void k_gemm_f16x(const GemmParams p) {
             for (int e = 0; e < 8; ++e) h[e] = (_Float16)ra[i][e];
             As[buf][row][swz_a(row, c)] = h;
         }
+        if (B_THREADS < NT && tid >= B_THREADS) return;
 #pragma unroll
         for (int c = 0; c < 8; ++c) {
             const int col = bnb * 8 + c;
@@ -874,10 +877,21 @@ bool build_gemm_mfma(int32_t route, const GemmParams& p, int batch, LaunchRec* r
     *tile_k = 64;
     switch (route) {
     case R_F16_EXACT: {
-        *tile_m = 128;
-        *tile_n = 128;
         const bool al = aligned_for(p, 2, 8);
         const bool step = p.chunk_tiles == 0;  // chunk of 16: flush after every MFMA step
+        // fewer than 64 tiles of 128 x 128: 64 x 64 tiles give 4x the workgroups
+        const int64_t tiles128 = (int64_t)((p.M + 127) / 128) * ((p.N + 127) / 128) * batch;
+        if (tiles128 < 64) {
+            *tile_m = 64;
+            *tile_n = 64;
+            if (al && !step) fill_gemm_rec(rec, k_gemm_f16x<64, 64, 64, 32, 32, true, false>, p, 64, 64, batch, "gemm_f16x_64");
+            else if (al) fill_gemm_rec(rec, k_gemm_f16x<64, 64, 64, 32, 32, true, true>, p, 64, 64, batch, "gemm_f16x_step_64");
+            else if (!step) fill_gemm_rec(rec, k_gemm_f16x<64, 64, 64, 32, 32, false, false>, p, 64, 64, batch, "gemm_f16x_u_64");
+            else fill_gemm_rec(rec, k_gemm_f16x<64, 64, 64, 32, 32, false, true>, p, 64, 64, batch, "gemm_f16x_step_u_64");
+            return true;
+        }
+        *tile_m = 128;
+        *tile_n = 128;
         if (al && !step) fill_gemm_rec(rec, k_gemm_f16x<128, 128, 64, 64, 64, true, false>, p, 128, 128, batch, "gemm_f16x");
         else if (al) fill_gemm_rec(rec, k_gemm_f16x<128, 128, 64, 64, 64, true, true>, p, 128, 128, batch, "gemm_f16x_step");
         else if (!step) fill_gemm_rec(rec, k_gemm_f16x<128, 128, 64, 64, 64, false, false>, p, 128, 128, batch, "gemm_f16x_u");
