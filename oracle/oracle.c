@@ -163,6 +163,76 @@ void oracle_conv2d_im2col(const int16_t* x, const int16_t* w, int32_t* y,
     free(g);
 }
 
+/* Conv2D on INT32 operands (Table 2, Conv2D INT32 row) under the smul24
+ * contract (Methodology): each operand word is read as sext24 of its low 24
+ * bits, products keep their low 32 bits, sums wrap mod 2^32.  Same geometry
+ * and layout as oracle_conv2d_direct. */
+void oracle_conv2d_s24_direct(const int32_t* x, const int32_t* w, int32_t* y,
+                              int64_t N, int64_t Ci, int64_t H, int64_t W, int64_t Co,
+                              int64_t KH, int64_t KW, int64_t stride, int64_t pad) {
+    int64_t Ho = conv_out_dim(H, KH, stride, pad);
+    int64_t Wo = conv_out_dim(W, KW, stride, pad);
+    #pragma omp parallel for collapse(2) schedule(dynamic, 1)
+    for (int64_t n = 0; n < N; ++n) {
+        for (int64_t co = 0; co < Co; ++co) {
+            for (int64_t oh = 0; oh < Ho; ++oh) {
+                for (int64_t ow = 0; ow < Wo; ++ow) {
+                    uint64_t acc = 0;
+                    for (int64_t ci = 0; ci < Ci; ++ci) {
+                        for (int64_t kh = 0; kh < KH; ++kh) {
+                            int64_t ih = oh * stride - pad + kh;
+                            if (ih < 0 || ih >= H) continue;
+                            for (int64_t kw = 0; kw < KW; ++kw) {
+                                int64_t iw = ow * stride - pad + kw;
+                                if (iw < 0 || iw >= W) continue;
+                                int64_t xv = sext24(x[((n * Ci + ci) * H + ih) * W + iw]);
+                                int64_t wv = sext24(w[((co * Ci + ci) * KH + kh) * KW + kw]);
+                                acc += (uint64_t)(xv * wv);
+                            }
+                        }
+                    }
+                    y[((n * Co + co) * Ho + oh) * Wo + ow] = low32(acc);
+                }
+            }
+        }
+    }
+}
+
+/* Conv2D on FP32 operands (Table 2, Conv2D FP32 row), the reference the GPU
+ * result is held to: every product and sum in float64 from the float32
+ * inputs, in the plain (ci, kh, kw) order.  Same geometry and layout as
+ * oracle_conv2d_direct; y is float64. */
+void oracle_conv2d_f64_direct(const float* x, const float* w, double* y,
+                              int64_t N, int64_t Ci, int64_t H, int64_t W, int64_t Co,
+                              int64_t KH, int64_t KW, int64_t stride, int64_t pad) {
+    int64_t Ho = conv_out_dim(H, KH, stride, pad);
+    int64_t Wo = conv_out_dim(W, KW, stride, pad);
+    #pragma omp parallel for collapse(2) schedule(dynamic, 1)
+    for (int64_t n = 0; n < N; ++n) {
+        for (int64_t co = 0; co < Co; ++co) {
+            for (int64_t oh = 0; oh < Ho; ++oh) {
+                for (int64_t ow = 0; ow < Wo; ++ow) {
+                    double acc = 0.0;
+                    for (int64_t ci = 0; ci < Ci; ++ci) {
+                        for (int64_t kh = 0; kh < KH; ++kh) {
+                            int64_t ih = oh * stride - pad + kh;
+                            if (ih < 0 || ih >= H) continue;
+                            for (int64_t kw = 0; kw < KW; ++kw) {
+                                int64_t iw = ow * stride - pad + kw;
+                                if (iw < 0 || iw >= W) continue;
+                                double xv = x[((n * Ci + ci) * H + ih) * W + iw];
+                                double wv = w[((co * Ci + ci) * KH + kh) * KW + kw];
+                                acc += xv * wv;
+                            }
+                        }
+                    }
+                    y[((n * Co + co) * Ho + oh) * Wo + ow] = acc;
+                }
+            }
+        }
+    }
+}
+
 /* Attention core, INT32 (Methodology: O = (Q K^T) V; Table 2, INT32 row).
  * No scale, softmax or mask; one head; Q, K, V, O are [L][d] row-major.
  * S = Q K^T is formed exactly, then O = S V (mod 2^32). */

@@ -43,7 +43,8 @@ def _load():
         i64 = ctypes.c_int64
         for name in ("oracle_gemm_i16i32", "oracle_gemm_i32_s24"):
             getattr(lib, name).argtypes = [p, p, p, i64, i64, i64, i64]
-        for name in ("oracle_conv2d_direct", "oracle_conv2d_im2col"):
+        for name in ("oracle_conv2d_direct", "oracle_conv2d_im2col", "oracle_conv2d_s24_direct",
+                     "oracle_conv2d_f64_direct"):
             getattr(lib, name).argtypes = [p, p, p] + [i64] * 9
         for name in ("oracle_attn_i32", "oracle_attn_i32_assoc", "oracle_attn_f64",
                      "oracle_attn_f64_assoc", "oracle_attn_f32"):
@@ -99,13 +100,13 @@ def conv_out_shape(N, Ci, H, W, Co, KH, KW, stride, pad):
     return (N, Co, Ho, Wo)
 
 
-def _conv(fn, x, w, stride, pad):
-    x = _c(x, np.int16)
-    w = _c(w, np.int16)
+def _conv(fn, x, w, stride, pad, in_dtype=np.int16, out_dtype=np.int32):
+    x = _c(x, in_dtype)
+    w = _c(w, in_dtype)
     N, Ci, H, W = x.shape
     Co, Ci2, KH, KW = w.shape
     assert Ci == Ci2
-    y = np.empty(conv_out_shape(N, Ci, H, W, Co, KH, KW, stride, pad), np.int32)
+    y = np.empty(conv_out_shape(N, Ci, H, W, Co, KH, KW, stride, pad), out_dtype)
     fn(_ptr(x), _ptr(w), _ptr(y), N, Ci, H, W, Co, KH, KW, stride, pad)
     return y
 
@@ -118,6 +119,18 @@ def conv2d_direct(x, w, stride=1, pad=0):
 def conv2d_im2col(x, w, stride=1, pad=0):
     """The same convolution via explicit im2col and the GEMM oracle."""
     return _conv(_load().oracle_conv2d_im2col, x, w, stride, pad)
+
+
+def conv2d_s24(x, w, stride=1, pad=0):
+    """INT32 convolution under the smul24 contract: operands read as sext24 of
+    their low 24 bits, int32 result mod 2^32 (Table 2, Conv2D INT32 row)."""
+    return _conv(_load().oracle_conv2d_s24_direct, x, w, stride, pad, np.int32, np.int32)
+
+
+def conv2d_f64(x, w, stride=1, pad=0):
+    """FP32 convolution's reference: float32 inputs, float64 products and sums
+    (Table 2, Conv2D FP32 row)."""
+    return _conv(_load().oracle_conv2d_f64_direct, x, w, stride, pad, np.float32, np.float64)
 
 
 def _attn(fn, Q, K, V, dtype, out_dtype):

@@ -27,8 +27,10 @@ def gemm(A, B, f=lambda v: v):
              for j in range(N)] for i in range(M)]
 
 
-def conv2d(x, w, stride, pad):
-    """x [N][Ci][H][W], w [Co][Ci][KH][KW] nested lists -> y [N][Co][Ho][Wo]."""
+def conv2d(x, w, stride, pad, f=int, wrap=True):
+    """x [N][Ci][H][W], w [Co][Ci][KH][KW] nested lists -> y [N][Co][Ho][Wo].
+    f maps each operand first (int, sext24 of an int word, or Fraction for
+    exact real arithmetic); wrap reduces the exact sum mod 2^32."""
     N, Ci, H, W = len(x), len(x[0]), len(x[0][0]), len(x[0][0][0])
     Co, KH, KW = len(w), len(w[0][0]), len(w[0][0][0])
     Ho = (H + 2 * pad - KH) // stride + 1
@@ -44,8 +46,8 @@ def conv2d(x, w, stride, pad):
                             for kw in range(KW):
                                 ih, iw = oh * stride - pad + kh, ow * stride - pad + kw
                                 if 0 <= ih < H and 0 <= iw < W:
-                                    s += int(x[n][ci][ih][iw]) * int(w[co][ci][kh][kw])
-                    y[n][co][oh][ow] = wrap32(s)
+                                    s += f(x[n][ci][ih][iw]) * f(w[co][ci][kh][kw])
+                    y[n][co][oh][ow] = wrap32(s) if wrap else s
     return y
 
 

@@ -227,6 +227,82 @@ def test_conv_closed_forms():
     assert (y[1:-1, 1:-1] == 9 * C).all()
 
 
+# ----------------------------------------------------------------------------
+# Conv2D on INT32 operands under the smul24 contract, and on FP32 operands
+# ----------------------------------------------------------------------------
+@pytest.mark.parametrize("cfg", CONV_TINY)
+def test_conv_s24_bruteforce_full_int32_words(cfg):
+    # every bit of the words is random: bits 24..31 must be ignored
+    N, Ci, H, W, Co, KH, KW, s, p = cfg
+    rng = np.random.default_rng(sum(cfg) + 7)
+    x = rng.integers(-(1 << 31), (1 << 31) - 1, (N, Ci, H, W), dtype=np.int32, endpoint=True)
+    w = rng.integers(-(1 << 31), (1 << 31) - 1, (Co, Ci, KH, KW), dtype=np.int32, endpoint=True)
+    ref = brute.conv2d(x.tolist(), w.tolist(), s, p, f=lambda v: brute.sext24(int(v)))
+    assert orc.conv2d_s24(x, w, s, p).tolist() == ref
+
+
+def test_conv_s24_contract_invariants():
+    rng = np.random.default_rng(5)
+    x = rng.integers(-32768, 32767, (2, 6, 9, 8), dtype=np.int16, endpoint=True)
+    w = rng.integers(-32768, 32767, (5, 6, 3, 3), dtype=np.int16, endpoint=True)
+    # int16 values are their own sext24: equals the INT16 convolution
+    y16 = orc.conv2d_direct(x, w, 1, 1)
+    y24 = orc.conv2d_s24(x.astype(np.int32), w.astype(np.int32), 1, 1)
+    assert (y16 == y24).all()
+    # adding multiples of 2^24 to the words changes nothing
+    hi = rng.integers(-128, 127, x.shape, endpoint=True).astype(np.int64) << 24
+    xm = ((x.astype(np.int64) + hi + (1 << 31)) % (1 << 32) - (1 << 31)).astype(np.int32)
+    assert (orc.conv2d_s24(xm, w.astype(np.int32), 1, 1) == y24).all()
+    # closed form: all operands 2^23 - 1, 1x1 kernel: Ci * (2^46 - 2^24 + 1) mod 2^32
+    Ci = 3
+    top = (1 << 23) - 1
+    y = orc.conv2d_s24(np.full((1, Ci, 2, 2), top, np.int32), np.full((1, Ci, 1, 1), top, np.int32), 1, 0)
+    assert (y == brute.wrap32(Ci * ((1 << 46) - (1 << 24) + 1))).all()
+    assert brute.wrap32(Ci * ((1 << 46) - (1 << 24) + 1)) == -3 * 16777215
+    # -2^23 everywhere: each product is 2^46 = 0 mod 2^32
+    bot = -(1 << 23)
+    y = orc.conv2d_s24(np.full((1, 4, 3, 3), bot, np.int32), np.full((2, 4, 3, 3), bot, np.int32), 1, 1)
+    assert (y == 0).all()
+
+
+@pytest.mark.parametrize("cfg", CONV_TINY[:4])
+def test_conv_f64_exact_rationals(cfg):
+    from fractions import Fraction
+    N, Ci, H, W, Co, KH, KW, s, p = cfg
+    rng = np.random.default_rng(sum(cfg) + 11)
+    x = rng.standard_normal((N, Ci, H, W)).astype(np.float32)
+    w = rng.standard_normal((Co, Ci, KH, KW)).astype(np.float32)
+    exact = brute.conv2d(x.tolist(), w.tolist(), s, p, f=lambda v: Fraction(float(v)), wrap=False)
+    y = orc.conv2d_f64(x, w, s, p)
+    # float64 products of float32 inputs are exact; the sums round at most
+    # (terms - 1) times by 2^-53 relative to the sum of |products|
+    absx = np.abs(x).astype(np.float64)
+    absw = np.abs(w).astype(np.float64)
+    bound_sum = orc.conv2d_f64(absx.astype(np.float32), absw.astype(np.float32), s, p)
+    terms = Ci * KH * KW
+    err = np.abs(y - np.array([[[[float(v) for v in r] for r in c] for c in im] for im in exact]))
+    assert (err <= terms * 2.0 ** -52 * bound_sum + 1e-300).all()
+
+
+def test_conv_f64_integer_values_and_numpy():
+    rng = np.random.default_rng(9)
+    xi = rng.integers(-100, 100, (2, 7, 10, 9), dtype=np.int16, endpoint=True)
+    wi = rng.integers(-100, 100, (4, 7, 3, 2), dtype=np.int16, endpoint=True)
+    # integer-valued floats: every partial sum is an exact small integer
+    y = orc.conv2d_f64(xi.astype(np.float32), wi.astype(np.float32), 2, 1)
+    assert (y == orc.conv2d_direct(xi, wi, 2, 1)).all()
+    # independent library route: zero-pad, gather windows, float64 tensordot
+    x = rng.standard_normal((2, 7, 10, 9)).astype(np.float32)
+    w = rng.standard_normal((4, 7, 3, 2)).astype(np.float32)
+    s, p = 2, 1
+    xp = np.pad(x.astype(np.float64), ((0, 0), (0, 0), (p, p), (p, p)))
+    win = np.lib.stride_tricks.sliding_window_view(xp, (3, 2), axis=(2, 3))[:, :, ::s, ::s]
+    ref = np.tensordot(win, w.astype(np.float64), axes=([1, 4, 5], [1, 2, 3])).transpose(0, 3, 1, 2)
+    y = orc.conv2d_f64(x, w, s, p)
+    assert y.shape == ref.shape
+    assert np.max(np.abs(y - ref)) <= 1e-12 * np.max(np.abs(ref))
+
+
 def test_conv_output_shape():
     assert orc.conv_out_shape(8, 64, 56, 56, 128, 3, 3, 1, 1) == (8, 128, 56, 56)
     assert orc.conv_out_shape(1, 1, 7, 6, 1, 3, 2, 2, 0) == (1, 1, 3, 3)
