@@ -105,6 +105,9 @@ def make_executor(w, qx):
     if w.op == "conv2d":
         return qx.Executor.conv2d(d["N"], d["Ci"], d["H"], d["W"], d["Co"], d["KH"], d["KW"],
                                   d["stride"], d["pad"], w.bound, w.bound)
+    if w.op in ("conv2d_f32", "conv2d_i32"):
+        return qx.Executor.conv2d_t("f32" if w.op == "conv2d_f32" else "i32", d["N"], d["Ci"], d["H"], d["W"],
+                                    d["Co"], d["KH"], d["KW"], d["stride"], d["pad"])
     if w.op == "attn_f32":
         return qx.Executor.attn("f32", d["L"], d["d"])
     if w.op == "attn_i32":

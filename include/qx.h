@@ -88,7 +88,10 @@ typedef enum {
     QX_ROUTE_S24_I8LIMB = 7,
     QX_ROUTE_ATTN_F32_MFMA = 8,  /* attention: fp32 MFMA, S tile kept on chip */
     QX_ROUTE_ATTN_I32_MFMA = 9,  /* attention: int8 MFMA for QK^T, S split into int8 limbs */
-    QX_ROUTE_ATTN_I32_VALU = 10  /* attention: vector-ALU int32, any operand range */
+    QX_ROUTE_ATTN_I32_VALU = 10, /* attention: vector-ALU int32, any operand range */
+    QX_ROUTE_ATTN_F32_VALU = 11, /* attention: vector-ALU fp32 (d outside the MFMA shapes) */
+    QX_ROUTE_F32_MFMA = 12,      /* FP32 conv: fp32 matrix cores (C_in a multiple of 32) */
+    QX_ROUTE_F32_VALU = 13       /* FP32 conv: vector-ALU fp32, any shape */
 } qx_route;
 
 /* What the planner decided for one operation (for tests and reporting). */
@@ -135,6 +138,19 @@ qx_status conv2d_gemm(const int16_t* x, const int16_t* w, int32_t* y,
                       int64_t KH, int64_t KW, int64_t stride, int64_t pad,
                       int32_t bound_x, int32_t bound_w, void* stream);
 
+/* Conv2D on FP32 or INT32 operands through the same lowering (Table 2,
+ * Conv2D FP32 and INT32 rows).  Geometry, layouts and size rules as
+ * conv2d_gemm; x, w and y have the element type of dt.
+ *  QX_DT_F32: float32 in and out.  The sum is formed in fp32 (on the fp32
+ *             matrix cores when C_in is a multiple of 32, else on the vector
+ *             ALU) in a fixed order, so repeated runs are bit-identical; it
+ *             meets max|y - R| <= 1e-4 max|R| against the float64 sum R.
+ *  QX_DT_I32: int32 under the smul24 contract (Methodology): each operand
+ *             word is read as sext24 of its low 24 bits; y exact mod 2^32. */
+qx_status conv2d_gemm_t(qx_attn_dtype dt, const void* x, const void* w, void* y,
+                        int64_t N, int64_t C_in, int64_t H, int64_t W, int64_t C_out,
+                        int64_t KH, int64_t KW, int64_t stride, int64_t pad, void* stream);
+
 /* Single-head attention core (Methodology: O = (Q K^T) V; Table 2, attention
  * rows): no scale, softmax or mask.  Q, K, V, O are [L][d] row-major.
  *  QX_DT_F32: float32 in and out.  The association (Q K^T) V is evaluated
@@ -161,10 +177,14 @@ qx_status qx_exec_create_gemm_i32_s24(qx_exec* out, int64_t M, int64_t N, int64_
 qx_status qx_exec_create_conv2d(qx_exec* out, int64_t N, int64_t C_in, int64_t H, int64_t W,
                                 int64_t C_out, int64_t KH, int64_t KW, int64_t stride,
                                 int64_t pad, int32_t bound_x, int32_t bound_w, int32_t route);
+/* dt QX_DT_F32: route AUTO, F32_MFMA or F32_VALU; QX_DT_I32: AUTO, S24_I8LIMB or S24_VALU. */
+qx_status qx_exec_create_conv2d_t(qx_exec* out, qx_attn_dtype dt, int64_t N, int64_t C_in,
+                                  int64_t H, int64_t W, int64_t C_out, int64_t KH, int64_t KW,
+                                  int64_t stride, int64_t pad, int32_t route);
 qx_status qx_exec_create_attn(qx_exec* out, qx_attn_dtype dt, int64_t L, int64_t d,
                               int32_t bound, int32_t route);
 
-/* Enqueue one evaluation: inputs = {A, B} (GEMMs), {x, w} (conv) or
+/* Enqueue one evaluation: inputs = {A, B} (GEMMs), {x, w} (convolutions) or
  * {Q, K, V} (attention), device pointers with the shapes given at create.
  * Allocates nothing.  Calls on one handle must not overlap in time. */
 qx_status qx_exec_run(qx_exec h, const void* const* inputs, void* output, void* stream);
@@ -193,6 +213,9 @@ qx_status qx_plan_gemm_i32_s24(qx_plan_info* out, int64_t M, int64_t N, int64_t 
 qx_status qx_plan_conv2d(qx_plan_info* out, int64_t N, int64_t C_in, int64_t H, int64_t W,
                          int64_t C_out, int64_t KH, int64_t KW, int64_t stride, int64_t pad,
                          int32_t bound_x, int32_t bound_w, int32_t route);
+qx_status qx_plan_conv2d_t(qx_plan_info* out, qx_attn_dtype dt, int64_t N, int64_t C_in,
+                           int64_t H, int64_t W, int64_t C_out, int64_t KH, int64_t KW,
+                           int64_t stride, int64_t pad, int32_t route);
 qx_status qx_plan_attn(qx_plan_info* out, qx_attn_dtype dt, int64_t L, int64_t d,
                        int32_t bound, int32_t route);
 

@@ -50,7 +50,9 @@ constexpr int64_t kMaxDim = (int64_t)1 << 30;
 constexpr int64_t kMaxBatch = 65535;
 constexpr uint32_t kMagic = 0x71786578u;  // "qxex"
 
-enum OpKind : int32_t { OP_GEMM_I16 = 1, OP_GEMM_S24 = 2, OP_CONV = 3, OP_ATTN_F32 = 4, OP_ATTN_I32 = 5 };
+enum OpKind : int32_t {
+    OP_GEMM_I16 = 1, OP_GEMM_S24 = 2, OP_CONV = 3, OP_ATTN_F32 = 4, OP_ATTN_I32 = 5, OP_CONV_F32 = 6, OP_CONV_I32 = 7
+};
 
 // A fully planned operation: route facts plus launch records with unbound
 // pointers.  Built on the host with no device call.
@@ -149,6 +151,9 @@ struct GemmSpec {
     int64_t lda, ldb, ldc, sA, sB, sC;
     int32_t out_mode, hw;
     bool allow_nt;       // plain GEMM: large fp16-exact problems may take encode + NT GEMM
+    bool b_conv;         // B is the im2col matrix of the image bound by b_bind (geometry
+                         // geo), gathered by the limb-plane encoder (NT int8 path only)
+    ConvGeom geo;
 };
 
 // The encode + direct-to-LDS route pays two HBM-bound encoding passes; it is
@@ -315,6 +320,7 @@ qx_status plan_int_gemm(const GemmSpec& s, Plan* pl, uint64_t* ws_used) {
     g.lda = (int32_t)s.lda; g.ldb = (int32_t)s.ldb; g.ldc = (int32_t)s.ldc;
     g.out_mode = s.out_mode; g.hw = s.hw; g.b_mode = B_KN;
     const bool nt8 = s.allow_nt && use_i8nt(route, s.M, s.N, s.K, s.batch);
+    if (s.b_conv && !nt8) return fail(QX_ERR_UNSUPPORTED, "gathered B needs the NT int8 route");
     const bool offset = route == R_I8_OFFSET4 || route == R_S24_I8LIMB;
     uint64_t rs_off = 0, cs_off = 0;
     if (offset) {
@@ -362,6 +368,11 @@ qx_status plan_int_gemm(const GemmSpec& s, Plan* pl, uint64_t* ws_used) {
         eb.Np = (int32_t)Np; eb.Kp = (int32_t)Kp;
         eb.ld_src = (int32_t)s.ldb; eb.batch = (int32_t)s.batch;
         eb.vec = (s.ldb % 4 == 0 && s.sB % 4 == 0) ? 1 : 0;
+        if (s.b_conv) {
+            eb.conv = 1;
+            eb.g = s.geo;
+            eb.vec = 0;
+        }
         LaunchRec r1;
         build_enc_limb(route, s.s24, ep, &r1);
         r1.bind(offsetof(EncPairParams, a) + offsetof(EncParams, src), s.a_bind);
@@ -488,8 +499,10 @@ qx_status plan_gemm(Plan* pl, bool s24, int64_t M, int64_t N, int64_t K, int64_t
     return QX_OK;
 }
 
-qx_status plan_conv(Plan* pl, int64_t N, int64_t Ci, int64_t H, int64_t W, int64_t Co, int64_t KH, int64_t KW,
-                    int64_t stride, int64_t pad, int32_t bound_x, int32_t bound_w, int32_t route) {
+// Geometry shared by every convolution: validates the arguments and gives
+// the output size and the GEMM view (Kd = C_in*KH*KW, P = N*Ho*Wo).
+qx_status conv_shape(int64_t N, int64_t Ci, int64_t H, int64_t W, int64_t Co, int64_t KH, int64_t KW,
+                     int64_t stride, int64_t pad, int64_t* Ho_, int64_t* Wo_, int64_t* Kd_, int64_t* P_) {
     qx_status st = check_dims({{"N", N}, {"C_in", Ci}, {"H", H}, {"W", W}, {"C_out", Co}, {"KH", KH},
                                {"KW", KW}, {"stride", stride}, {"pad", pad}});
     if (st) return st;
@@ -500,14 +513,23 @@ qx_status plan_conv(Plan* pl, int64_t N, int64_t Ci, int64_t H, int64_t W, int64
     if (Ho < 1 || Wo < 1)
         return fail(QX_ERR_INVALID_ARG, "kernel %lldx%lld larger than the padded %lldx%lld input", (long long)KH,
                     (long long)KW, (long long)(H + 2 * pad), (long long)(W + 2 * pad));
-    int64_t ba, bb;
-    if ((st = check_bound16(bound_w, "bound_w", &ba))) return st;
-    if ((st = check_bound16(bound_x, "bound_x", &bb))) return st;
     int64_t Kd, P, t;
     if (!mul_ok(Ci, KH * KW, kMaxDim, &Kd) || !mul_ok(N, Ho * Wo, kMaxDim, &P) ||
         !mul_ok(Kd, P, (int64_t)1 << 40, &t) || !mul_ok(Co, P, (int64_t)1 << 40, &t))
         return fail(QX_ERR_UNSUPPORTED, "convolution too large");
     if (Kd > 65535) return fail(QX_ERR_UNSUPPORTED, "C_in*KH*KW = %lld exceeds 65535", (long long)Kd);
+    *Ho_ = Ho; *Wo_ = Wo; *Kd_ = Kd; *P_ = P;
+    return QX_OK;
+}
+
+qx_status plan_conv(Plan* pl, int64_t N, int64_t Ci, int64_t H, int64_t W, int64_t Co, int64_t KH, int64_t KW,
+                    int64_t stride, int64_t pad, int32_t bound_x, int32_t bound_w, int32_t route) {
+    int64_t Ho, Wo, Kd, P;
+    qx_status st = conv_shape(N, Ci, H, W, Co, KH, KW, stride, pad, &Ho, &Wo, &Kd, &P);
+    if (st) return st;
+    int64_t ba, bb;
+    if ((st = check_bound16(bound_w, "bound_w", &ba))) return st;
+    if ((st = check_bound16(bound_x, "bound_x", &bb))) return st;
     if (route < 0 || route > R_ATTN_I32_VALU) return fail(QX_ERR_INVALID_ARG, "unknown route %d", route);
     pl->op = OP_CONV;
     pl->n_inputs = 2;
@@ -553,6 +575,7 @@ qx_status plan_conv(Plan* pl, int64_t N, int64_t Ci, int64_t H, int64_t W, int64
                            (int32_t)pad, (int32_t)Ho, (int32_t)Wo};
         ConvPrepParams cp{};
         cp.nimg = (int32_t)N; cp.Co = (int32_t)Co; cp.Cop = (int32_t)Mp; cp.Kd = (int32_t)Kd;
+        cp.elem_bytes = 2;
         cp.g = geo;
         LaunchRec r1;
         build_conv_prep(cp, &r1);
@@ -625,6 +648,7 @@ qx_status plan_conv(Plan* pl, int64_t N, int64_t Ci, int64_t H, int64_t W, int64
     Im2colParams ip{};
     ip.P = P;
     ip.Kd = (int32_t)Kd;
+    ip.elem_bytes = 2;
     ip.g = ConvGeom{(int32_t)Ci, (int32_t)H, (int32_t)W, (int32_t)KH, (int32_t)KW, (int32_t)stride, (int32_t)pad,
                     (int32_t)Ho, (int32_t)Wo};
     LaunchRec rec;
@@ -633,6 +657,145 @@ qx_status plan_conv(Plan* pl, int64_t N, int64_t Ci, int64_t H, int64_t W, int64
     rec.bind(offsetof(Im2colParams, col), BIND_WS, 0);
     pl->launches.push_back(rec);
     for (auto& r : g.launches) pl->launches.push_back(r);
+    pl->info.kernels = (int32_t)pl->launches.size();
+    pl->info.workspace_bytes = (int64_t)ws;
+    return QX_OK;
+}
+
+// Conv2D on FP32 or INT32 (smul24 contract) operands (Table 2, Conv2D FP32
+// and INT32 rows): the same lowering onto the FP32 and smul24 GEMMs.
+qx_status plan_conv_t(Plan* pl, qx_attn_dtype dt, int64_t N, int64_t Ci, int64_t H, int64_t W, int64_t Co,
+                      int64_t KH, int64_t KW, int64_t stride, int64_t pad, int32_t route) {
+    int64_t Ho, Wo, Kd, P;
+    qx_status st = conv_shape(N, Ci, H, W, Co, KH, KW, stride, pad, &Ho, &Wo, &Kd, &P);
+    if (st) return st;
+    if (dt != QX_DT_F32 && dt != QX_DT_I32) return fail(QX_ERR_INVALID_ARG, "unknown dtype %d", (int)dt);
+    pl->op = dt == QX_DT_F32 ? OP_CONV_F32 : OP_CONV_I32;
+    pl->n_inputs = 2;
+    pl->in_align = 16;
+    qx_plan_info& info = pl->info;
+    const int64_t Hp = H + 2 * pad, Wp = W + 2 * pad;
+    const ConvGeom geo{(int32_t)Ci, (int32_t)H, (int32_t)W, (int32_t)KH, (int32_t)KW, (int32_t)stride,
+                       (int32_t)pad, (int32_t)Ho, (int32_t)Wo};
+    if (dt == QX_DT_F32) {
+        const bool mfma_ok = Ci % 32 == 0 && 4 * N * Hp * Wp * Ci < ((int64_t)1 << 31);
+        int32_t r = route == R_AUTO ? (mfma_ok ? R_F32_MFMA : R_F32_VALU) : route;
+        if (r != R_F32_MFMA && r != R_F32_VALU)
+            return fail(QX_ERR_INVALID_ARG, "route %d does not apply to an FP32 convolution", route);
+        if (r == R_F32_MFMA && !mfma_ok)
+            return fail(QX_ERR_UNSUPPORTED, "the fp32 MFMA convolution needs C_in a multiple of 32");
+        info.route = r;
+        info.products = 1;
+        info.chunk = 0;
+        info.exact_no_wrap = 0;
+        if (N == 0 || Co == 0) {
+            info.kernels = 0;
+            info.workspace_bytes = 0;
+            return QX_OK;
+        }
+        if (Ci == 0) {
+            add_fill_out(pl, N * Co * Ho * Wo);
+            info.kernels = 1;
+            info.workspace_bytes = 0;
+            return QX_OK;
+        }
+        if (r == R_F32_MFMA) {
+            // bordered NHWC fp32 image + tap-major weights, then the gathering
+            // fp32 NT GEMM with an NCHW scatter
+            int bm, bn;
+            nt_tile_shape(Co, P, 1, &bm, &bn);
+            const int64_t Mp = pad_up(Co, bm);
+            const uint64_t x_off = round_up(4 * (uint64_t)Mp * Kd, 256);
+            ConvPrepParams cp{};
+            cp.nimg = (int32_t)N; cp.Co = (int32_t)Co; cp.Cop = (int32_t)Mp; cp.Kd = (int32_t)Kd;
+            cp.elem_bytes = 4;
+            cp.g = geo;
+            LaunchRec r1;
+            build_conv_prep(cp, &r1);
+            r1.bind(offsetof(ConvPrepParams, x), BIND_IN0);
+            r1.bind(offsetof(ConvPrepParams, w), BIND_IN1);
+            r1.bind(offsetof(ConvPrepParams, xp), BIND_WS, x_off);
+            r1.bind(offsetof(ConvPrepParams, w16), BIND_WS, 0);
+            GemmParams gp{};
+            gp.M = (int32_t)Co; gp.N = (int32_t)P; gp.K = (int32_t)Kd;
+            gp.lda = (int32_t)Kd; gp.ldb = 0; gp.ldc = (int32_t)P;
+            gp.out_mode = OUT_CONV; gp.hw = (int32_t)(Ho * Wo); gp.b_mode = B_NHWC;
+            gp.g = geo;
+            LaunchRec r2;
+            build_gemm_nt_f32(gp, 1, &r2);
+            r2.bind(offsetof(GemmParams, A), BIND_WS, 0);
+            r2.bind(offsetof(GemmParams, B), BIND_WS, x_off);
+            r2.bind(offsetof(GemmParams, C), BIND_OUT);
+            pl->launches = {r1, r2};
+            info.tile_m = bm; info.tile_n = bn; info.tile_k = 32;
+            info.kernels = 2;
+            info.workspace_bytes = (int64_t)(x_off + 4 * (uint64_t)(N * Hp * Wp * Ci));
+            return QX_OK;
+        }
+        // explicit lowering col [Kd][P] fp32, then the vector-ALU fp32 GEMM
+        if ((Co + 63) / 64 > 65535) return fail(QX_ERR_UNSUPPORTED, "C_out too large for the VALU route");
+        Im2colParams ip{};
+        ip.P = P; ip.Kd = (int32_t)Kd; ip.elem_bytes = 4; ip.g = geo;
+        LaunchRec r1;
+        build_im2col(ip, &r1);
+        r1.bind(offsetof(Im2colParams, x), BIND_IN0);
+        r1.bind(offsetof(Im2colParams, col), BIND_WS, 0);
+        ValuGemmParams v{};
+        v.M = (int32_t)Co; v.N = (int32_t)P; v.K = (int32_t)Kd;
+        v.lda = (int32_t)Kd; v.ldb = (int32_t)P; v.ldc = (int32_t)P; v.b_trans = 0;
+        v.out_mode = OUT_CONV; v.hw = (int32_t)(Ho * Wo);
+        LaunchRec r2;
+        build_valu_gemm(VK_F32, v, 1, &r2);
+        r2.bind(offsetof(ValuGemmParams, A), BIND_IN1);
+        r2.bind(offsetof(ValuGemmParams, B), BIND_WS, 0);
+        r2.bind(offsetof(ValuGemmParams, C), BIND_OUT);
+        pl->launches = {r1, r2};
+        info.tile_m = 64; info.tile_n = 64; info.tile_k = 16;
+        info.kernels = 2;
+        info.workspace_bytes = (int64_t)(4 * (uint64_t)Kd * (uint64_t)P);
+        return QX_OK;
+    }
+    // INT32 under smul24.  Large problems: the limb-plane encoder gathers the
+    // im2col columns straight from x, then the NT int8 contraction.  Small
+    // ones: explicit lowering col [Kd][P] int32, then the smul24 GEMM.
+    if (route < 0 || route > R_F32_VALU) return fail(QX_ERR_INVALID_ARG, "unknown route %d", route);
+    const bool gather = (route == R_AUTO || route == R_S24_I8LIMB) && use_i8nt(R_S24_I8LIMB, Co, P, Kd, 1);
+    GemmSpec s{};
+    s.M = Co; s.N = P; s.K = Kd; s.batch = 1; s.s24 = true; s.route = route;
+    s.a_bind = BIND_IN1; s.b_bind = gather ? BIND_IN0 : BIND_WS; s.b_ws_off = 0;
+    s.lda = Kd; s.ldb = P; s.ldc = P; s.sA = 0; s.sB = 0; s.sC = 0;
+    s.out_mode = OUT_CONV; s.hw = (int32_t)(Ho * Wo);
+    s.allow_nt = true;
+    s.b_conv = gather;
+    s.geo = geo;
+    uint64_t ws = gather ? 0 : round_up(4 * (uint64_t)Kd * (uint64_t)P, 256);
+    Plan g;
+    g.info = pl->info;
+    if ((st = plan_int_gemm(s, &g, &ws))) return st;
+    pl->info = g.info;
+    if (N == 0 || Co == 0) {
+        pl->launches.clear();
+        pl->info.kernels = 0;
+        pl->info.workspace_bytes = 0;
+        return QX_OK;
+    }
+    if (Ci == 0) {
+        add_fill_out(pl, N * Co * Ho * Wo);
+        pl->info.kernels = 1;
+        pl->info.workspace_bytes = 0;
+        return QX_OK;
+    }
+    if (!gather) {
+        Im2colParams ip{};
+        ip.P = P; ip.Kd = (int32_t)Kd; ip.elem_bytes = 4; ip.g = geo;
+        LaunchRec rec;
+        build_im2col(ip, &rec);
+        rec.bind(offsetof(Im2colParams, x), BIND_IN0);
+        rec.bind(offsetof(Im2colParams, col), BIND_WS, 0);
+        pl->launches.push_back(rec);
+    }
+    for (auto& r : g.launches) pl->launches.push_back(r);
+    pl->n_events = g.n_events;
     pl->info.kernels = (int32_t)pl->launches.size();
     pl->info.workspace_bytes = (int64_t)ws;
     return QX_OK;
@@ -1083,6 +1246,16 @@ qx_status qx_plan_conv2d(qx_plan_info* out, int64_t N, int64_t C_in, int64_t H, 
     return st;
 }
 
+qx_status qx_plan_conv2d_t(qx_plan_info* out, qx_attn_dtype dt, int64_t N, int64_t C_in, int64_t H, int64_t W,
+                           int64_t C_out, int64_t KH, int64_t KW, int64_t stride, int64_t pad, int32_t route) {
+    g_err.clear();
+    if (!out) return fail(QX_ERR_INVALID_ARG, "out is NULL");
+    Plan pl;
+    qx_status st = plan_conv_t(&pl, dt, N, C_in, H, W, C_out, KH, KW, stride, pad, route);
+    if (!st) *out = pl.info;
+    return st;
+}
+
 qx_status qx_plan_attn(qx_plan_info* out, qx_attn_dtype dt, int64_t L, int64_t d, int32_t bound, int32_t route) {
     g_err.clear();
     if (!out) return fail(QX_ERR_INVALID_ARG, "out is NULL");
@@ -1121,6 +1294,17 @@ qx_status qx_exec_create_conv2d(qx_exec* out, int64_t N, int64_t C_in, int64_t H
     *out = nullptr;
     Plan pl;
     qx_status st = plan_conv(&pl, N, C_in, H, W, C_out, KH, KW, stride, pad, bound_x, bound_w, route);
+    if (st) return st;
+    return make_exec(std::move(pl), out);
+}
+
+qx_status qx_exec_create_conv2d_t(qx_exec* out, qx_attn_dtype dt, int64_t N, int64_t C_in, int64_t H, int64_t W,
+                                  int64_t C_out, int64_t KH, int64_t KW, int64_t stride, int64_t pad, int32_t route) {
+    g_err.clear();
+    if (!out) return fail(QX_ERR_INVALID_ARG, "out is NULL");
+    *out = nullptr;
+    Plan pl;
+    qx_status st = plan_conv_t(&pl, dt, N, C_in, H, W, C_out, KH, KW, stride, pad, route);
     if (st) return st;
     return make_exec(std::move(pl), out);
 }
@@ -1233,6 +1417,24 @@ qx_status conv2d_gemm(const int16_t* x, const int16_t* w, int32_t* y, int64_t N,
                    [&](Plan* pl) {
                        return plan_conv(pl, N, C_in, H, W, C_out, KH, KW, stride, pad, bound_x, bound_w, R_AUTO);
                    },
+                   in, y, stream);
+}
+
+qx_status conv2d_gemm_t(qx_attn_dtype dt, const void* x, const void* w, void* y, int64_t N, int64_t C_in,
+                        int64_t H, int64_t W, int64_t C_out, int64_t KH, int64_t KW, int64_t stride, int64_t pad,
+                        void* stream) {
+    g_err.clear();
+    Plan probe;
+    qx_status st = plan_conv_t(&probe, dt, N, C_in, H, W, C_out, KH, KW, stride, pad, R_AUTO);
+    if (st) return st;
+    if (probe.launches.empty()) return QX_OK;
+    if (!empty_ok(x, N * C_in * H * W) || !empty_ok(w, C_out * C_in * KH * KW) || !y)
+        return fail(QX_ERR_INVALID_ARG, "NULL pointer for a non-empty operand");
+    const void* in[2] = {x, w};
+    Key key{dt == QX_DT_F32 ? OP_CONV_F32 : OP_CONV_I32, 0, N, C_in, H, W, C_out, KH, KW, stride, pad, 0, 0, 0,
+            (uintptr_t)stream};
+    return oneshot(key,
+                   [&](Plan* pl) { return plan_conv_t(pl, dt, N, C_in, H, W, C_out, KH, KW, stride, pad, R_AUTO); },
                    in, y, stream);
 }
 

@@ -538,13 +538,39 @@ __device__ __forceinline__ void enc_limb_bt(const EncParams& p, int blk) {
         __syncthreads();
     }
     uint32_t w[P][4] = {}, csum[4] = {};
+    // conv: pixel coordinates of this thread's four columns
+    int cimg[4], coh[4], cow[4];
+    if (p.conv) {
+        const int hw = p.g.Ho * p.g.Wo;
+#pragma unroll
+        for (int c = 0; c < 4; ++c) {
+            const int n = min(nb + c, p.N - 1);
+            cimg[c] = n / hw;
+            const int rem = n - cimg[c] * hw;
+            coh[c] = rem / p.g.Wo;
+            cow[c] = rem - coh[c] * p.g.Wo;
+        }
+    }
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
         const int k = kb + r;
         const T* row = src + (int64_t)k * p.ld_src + nb;
         T x[4];
         bool ok[4];
-        if (p.vec && k < p.K && nb + 4 <= p.N) {
+        if (p.conv) {
+            // B[k][n] = x[img][ci][oh*s - pad + kh][ow*s - pad + kw], zero outside
+            // the image (a real zero operand), k = (ci*KH + kh)*KW + kw
+            const ConvGeom& g = p.g;
+            const int kk = min(k, p.K - 1);
+            const int kw = kk % g.KW, t2 = kk / g.KW, kh = t2 % g.KH, ci = t2 / g.KH;
+#pragma unroll
+            for (int c = 0; c < 4; ++c) {
+                ok[c] = k < p.K && nb + c < p.N;
+                const int ih = coh[c] * g.stride - g.pad + kh, iw = cow[c] * g.stride - g.pad + kw;
+                const bool in = ok[c] && ih >= 0 && ih < g.H && iw >= 0 && iw < g.W;
+                x[c] = in ? src[(((int64_t)cimg[c] * g.Ci + ci) * g.H + ih) * g.W + iw] : (T)0;
+            }
+        } else if (p.vec && k < p.K && nb + 4 <= p.N) {
             load_vec<T, 4>(row, x);
 #pragma unroll
             for (int c = 0; c < 4; ++c) ok[c] = true;
@@ -813,6 +839,7 @@ __global__ __launch_bounds__(NT) void k_sums(const SumsParams p) {
 // ===========================================================================
 // Explicit im2col (Methodology: convolution through lowering).
 // ===========================================================================
+template <class T>
 __global__ __launch_bounds__(NT) void k_im2col(const Im2colParams p) {
     const int64_t pix = (int64_t)blockIdx.x * NT + threadIdx.x;
     const int k = blockIdx.y;
@@ -823,10 +850,10 @@ __global__ __launch_bounds__(NT) void k_im2col(const Im2colParams p) {
     const int n = (int)(pix / hw), rem = (int)(pix - (int64_t)n * hw);
     const int oh = rem / g.Wo, ow = rem - oh * g.Wo;
     const int ih = oh * g.stride - g.pad + kh, iw = ow * g.stride - g.pad + kw;
-    int16_t v = 0;
+    T v = (T)0;
     if (ih >= 0 && ih < g.H && iw >= 0 && iw < g.W)
-        v = p.x[(((int64_t)n * g.Ci + ci) * g.H + ih) * g.W + iw];
-    p.col[(int64_t)k * p.P + pix] = v;
+        v = ((const T*)p.x)[(((int64_t)n * g.Ci + ci) * g.H + ih) * g.W + iw];
+    ((T*)p.col)[(int64_t)k * p.P + pix] = v;
 }
 
 __global__ __launch_bounds__(NT) void k_fill(const FillParams p) {
@@ -931,7 +958,7 @@ bool build_gemm_mfma(int32_t route, const GemmParams& p, int batch, LaunchRec* r
 void i8nt_tile_shape(int32_t route, int64_t M, int64_t N, int64_t batch, int* bm, int* bn) {
     (void)route;
     const int64_t big = ((M + 127) / 128) * ((N + 127) / 128) * batch;
-    *bm = *bn = big >= 256 ? 128 : 64;
+    *bm = *bn = big >= 128 ? 128 : 64;
 }
 
 template <class S>
@@ -960,9 +987,13 @@ bool build_gemm_i8nt(int32_t route, const GemmParams& p0, int batch, LaunchRec* 
     int bm, bn;
     i8nt_tile_shape(route, p0.M, p0.N, batch, &bm, &bn);
     const bool big = bm == 128;
+    // 64x64 tiles: a 6-deep ring (one workgroup per CU) while the grid fits
+    // the chip in one round, else 3 deep (two per CU)
+    const bool deep = (int64_t)((p0.M + 63) / 64) * ((p0.N + 63) / 64) * batch <= 256;
 #define QX_NT(S, NAME)                                                                               \
     if (big) fill_gemm_rec(rec, k_gemm_i8nt<S, 128, 128, 3>, p0, 128, 128, batch, "gemm_i8nt_" NAME "_128x128"); \
-    else fill_gemm_rec(rec, k_gemm_i8nt<S, 64, 64, 6>, p0, 64, 64, batch, "gemm_i8nt_" NAME "_64x64");
+    else if (deep) fill_gemm_rec(rec, k_gemm_i8nt<S, 64, 64, 6>, p0, 64, 64, batch, "gemm_i8nt_" NAME "_64x64"); \
+    else fill_gemm_rec(rec, k_gemm_i8nt<S, 64, 64, 3>, p0, 64, 64, batch, "gemm_i8nt_" NAME "_64x64_3");
     switch (route) {
     case R_I8_DIRECT: QX_NT(SchemeDirect, "direct") return true;
     case R_I8_KARATSUBA: QX_NT(SchemeKaratsuba, "karatsuba") return true;
@@ -986,7 +1017,7 @@ void build_sums(const SumsParams& p, LaunchRec* rec) {
 }
 
 void build_im2col(const Im2colParams& p, LaunchRec* rec) {
-    rec->fn = (const void*)k_im2col;
+    rec->fn = p.elem_bytes == 4 ? (const void*)k_im2col<uint32_t> : (const void*)k_im2col<uint16_t>;
     rec->grid = dim3((unsigned)((p.P + NT - 1) / NT), (unsigned)p.Kd, 1);
     rec->block = dim3(NT, 1, 1);
     rec->name = "im2col";

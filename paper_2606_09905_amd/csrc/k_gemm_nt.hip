@@ -30,6 +30,7 @@ typedef _Float16 h2 __attribute__((ext_vector_type(2)));
 typedef float f16x __attribute__((ext_vector_type(16)));
 typedef unsigned u16x __attribute__((ext_vector_type(16)));
 typedef short s8v __attribute__((ext_vector_type(8)));
+typedef float f4v __attribute__((ext_vector_type(4)));
 
 // ===========================================================================
 // Stage 1: encoders
@@ -197,9 +198,9 @@ __global__ __launch_bounds__(256) void k_conv_prep(const ConvPrepParams p) {
         const int wl = tid & 63, cq = tid >> 6;
         const int w = wp0 + wl - g.pad;
         const bool in = row_in && w >= 0 && w < g.W;
-        _Float16* dst = p.xp + ((int64_t)n * Hp + hp) * Wp * g.Ci;
+        _Float16* dst = (_Float16*)p.xp + ((int64_t)n * Hp + hp) * Wp * g.Ci;
         for (int c0 = 0; c0 < g.Ci; c0 += 64) {
-            const int16_t* src = p.x + (((int64_t)n * g.Ci + c0) * g.H + h) * g.W + w;
+            const int16_t* src = (const int16_t*)p.x + (((int64_t)n * g.Ci + c0) * g.H + h) * g.W + w;
 #pragma unroll
             for (int r = 0; r < 16; ++r) {
                 const int c = cq + 4 * r;
@@ -230,15 +231,237 @@ __global__ __launch_bounds__(256) void k_conv_prep(const ConvPrepParams p) {
     h8 o;
 #pragma unroll
     for (int e = 0; e < 8; ++e)
-        o[e] = co < p.Co ? (_Float16)p.w[(((int64_t)co * g.Ci + ci0 + e) * g.KH + kh) * g.KW + kw]
+        o[e] = co < p.Co ? (_Float16)((const int16_t*)p.w)[(((int64_t)co * g.Ci + ci0 + e) * g.KH + kh) * g.KW + kw]
                          : (_Float16)0.0f;
-    *(h8*)(p.w16 + (int64_t)co * p.Kd + k0) = o;
+    *(h8*)((_Float16*)p.w16 + (int64_t)co * p.Kd + k0) = o;
+}
+
+// FP32 counterpart of k_conv_prep (C_in a multiple of 32): x NCHW float ->
+// zero-bordered NHWC float xp; w OIHW float -> w32 [Cop][Kd] with
+// k = (kh*KW + kw)*Ci + ci.  Values are copied unchanged.
+__global__ __launch_bounds__(256) void k_conv_prep_f32(const ConvPrepParams p) {
+    const ConvGeom& g = p.g;
+    const int tid = threadIdx.x;
+    if (blockIdx.y == 0) {
+        if ((int)blockIdx.x >= p.xblocks) return;
+        __shared__ float t[32][65];
+        const int Hp = g.H + 2 * g.pad, Wp = g.W + 2 * g.pad;
+        const int wch = (Wp + 63) / 64;
+        const int n = blockIdx.x / (Hp * wch), rem = blockIdx.x - n * Hp * wch;
+        const int hp = rem / wch, wp0 = (rem - hp * wch) * 64;
+        const int h = hp - g.pad;
+        const bool row_in = h >= 0 && h < g.H;
+        const int wl = tid & 63, cq = tid >> 6;
+        const int w = wp0 + wl - g.pad;
+        const bool in = row_in && w >= 0 && w < g.W;
+        float* dst = (float*)p.xp + ((int64_t)n * Hp + hp) * Wp * g.Ci;
+        for (int c0 = 0; c0 < g.Ci; c0 += 32) {
+            const float* src = (const float*)p.x + (((int64_t)n * g.Ci + c0) * g.H + h) * g.W + w;
+#pragma unroll
+            for (int r = 0; r < 8; ++r) {
+                const int c = cq + 4 * r;
+                t[c][wl] = in ? src[(int64_t)c * g.H * g.W] : 0.0f;
+            }
+            __syncthreads();
+#pragma unroll
+            for (int i = 0; i < 2; ++i) {
+                const int q = tid + 256 * i, px = q >> 3, ch = q & 7;
+                if (wp0 + px < Wp) {
+                    f4v o;
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) o[e] = t[ch * 4 + e][px];
+                    *(f4v*)(dst + (int64_t)(wp0 + px) * g.Ci + c0 + ch * 4) = o;
+                }
+            }
+            __syncthreads();
+        }
+        return;
+    }
+    if ((int)blockIdx.x >= p.wblocks) return;
+    const int kc = p.Kd / 4;
+    const int64_t v = (int64_t)blockIdx.x * 256 + tid;
+    if (v >= (int64_t)p.Cop * kc) return;
+    const int co = (int)(v / kc), k0 = (int)(v - (int64_t)co * kc) * 4;
+    const int tap = k0 / g.Ci, ci0 = k0 - tap * g.Ci;
+    const int kh = tap / g.KW, kw = tap - kh * g.KW;
+    f4v o;
+#pragma unroll
+    for (int e = 0; e < 4; ++e)
+        o[e] = co < p.Co ? ((const float*)p.w)[(((int64_t)co * g.Ci + ci0 + e) * g.KH + kh) * g.KW + kw] : 0.0f;
+    *(f4v*)((float*)p.w16 + (int64_t)co * p.Kd + k0) = o;
 }
 
 // ===========================================================================
 // Stage 2: contraction
 // ===========================================================================
 __device__ __forceinline__ int chunk_swz(int r) { return (r >> 1) & 7; }
+
+// FP32 contraction (conv FP32 row) on v_mfma_f32_32x32x2f32 with the same
+// staging: a K tile is 32 fp32 = 128-byte rows of eight 16-byte chunks, same
+// swizzle and direct-to-LDS ring.  In k-step ks (8 k) lane half h reads chunk
+// 2*ks + h of its row / column, and MFMA e of the step takes element e of it:
+// K-slot (h, e) is k = 8*ks + 4*h + e for both operands.  The sum is formed
+// in fp32 in the matrix cores' order.  IMPL gathers B from the bordered NHWC
+// fp32 image, 32 channels of one kernel tap per K tile.
+template <int BM, int BN, int NW, bool IMPL>
+__global__ __launch_bounds__(NW * 64) void k_gemm_nt_f32(const GemmParams p) {
+    constexpr int BK = 32, KCH = 8, WM = 64, WN = 64;
+    constexpr int TM = WM / 32, TN = WN / 32;
+    constexpr int WAVES_N = BN / WN;
+    static_assert((BM / WM) * (BN / WN) == NW, "wave grid");
+    constexpr int NTH = NW * 64;
+    constexpr int AL = BM * KCH / NTH, BL = BN * KCH / NTH, LPT = AL + BL;
+    static_assert(AL * NTH == BM * KCH && BL * NTH == BN * KCH, "whole loads");
+    constexpr int STAGES = 3;
+    constexpr unsigned STAGE_A = BM * KCH * 16, STAGE_B = BN * KCH * 16;
+    __shared__ f4v As[STAGES][BM][KCH];
+    __shared__ f4v Bs[STAGES][BN][KCH];
+
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, l32 = lane & 31, hh = lane >> 5;
+    const int wm = wave / WAVES_N, wn = wave % WAVES_N;
+    const int tiles_m = (p.M + BM - 1) / BM, tiles_n = p.tiles_n;
+    int pid = blockIdx.x;
+    const int total = gridDim.x;
+    if ((total & 7) == 0) pid = (pid & 7) * (total >> 3) + (pid >> 3);
+    int tm, tn;
+    {
+        constexpr int G = 8;
+        const int per_group = G * tiles_n;
+        const int gid = pid / per_group;
+        const int first_m = gid * G;
+        const int gsz = min(tiles_m - first_m, G);
+        const int in = pid - gid * per_group;
+        tm = first_m + in % gsz;
+        tn = in / gsz;
+    }
+    const int m0 = tm * BM, n0 = tn * BN;
+    const int b = blockIdx.z;
+    const float* A = (const float*)p.A + b * p.sA;   // [Mp][lda], lda = Kp
+    const float* B = (const float*)p.B + b * p.sB;   // [Np][ldb] or the NHWC image
+    float* C = (float*)p.C + b * p.sC;
+
+    unsigned oa[AL], ob[BL];
+#pragma unroll
+    for (int i = 0; i < AL; ++i) {
+        const int q = tid + NTH * i, row = q / KCH, pc = q % KCH;
+        oa[i] = (unsigned)(((int64_t)row * p.lda + (pc ^ chunk_swz(row)) * 4) * 4);
+    }
+    const ConvGeom& g = p.g;
+    const int Hp = g.H + 2 * g.pad, Wp = g.W + 2 * g.pad;
+#pragma unroll
+    for (int i = 0; i < BL; ++i) {
+        const int q = tid + NTH * i, row = q / KCH, pc = q % KCH;
+        if (IMPL) {
+            int pix = n0 + row;
+            if (pix >= p.N) pix = 0;     // never stored
+            const int img = pix / p.hw, rem = pix - img * p.hw;
+            const int oh = rem / g.Wo, ow = rem - oh * g.Wo;
+            const int64_t base = (((int64_t)img * Hp + oh * g.stride) * Wp + ow * g.stride) * g.Ci;
+            ob[i] = (unsigned)((base + (pc ^ chunk_swz(row)) * 4) * 4);
+        } else {
+            ob[i] = (unsigned)(((int64_t)row * p.ldb + (pc ^ chunk_swz(row)) * 4) * 4);
+        }
+    }
+    const char* a_panel = (const char*)(A + (int64_t)m0 * p.lda);
+    const char* b_panel = IMPL ? (const char*)B : (const char*)(B + (int64_t)n0 * p.ldb);
+    int tap_h = 0, tap_w = 0, tap_c = 0;
+    const unsigned wave_u = __builtin_amdgcn_readfirstlane(wave);
+    const unsigned lds_a0 = (unsigned)(uintptr_t)&As[0][0][0] + wave_u * 1024;
+    const unsigned lds_b0 = (unsigned)(uintptr_t)&Bs[0][0][0] + wave_u * 1024;
+    auto issue = [&](int t) {
+        const int s = t % STAGES;
+        const char* ab = a_panel + t * BK * 4;
+        const char* bb;
+        if (IMPL) {
+            bb = b_panel + (int64_t)((tap_h * Wp + tap_w) * g.Ci + tap_c) * 4;
+            tap_c += BK;
+            if (tap_c == g.Ci) {
+                tap_c = 0;
+                if (++tap_w == g.KW) {
+                    tap_w = 0;
+                    ++tap_h;
+                }
+            }
+        } else {
+            bb = b_panel + t * BK * 4;
+        }
+        const unsigned la = lds_a0 + s * STAGE_A, lb = lds_b0 + s * STAGE_B;
+#pragma unroll
+        for (int i = 0; i < AL; ++i)
+            asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dwordx4 %0, %1"
+                         :: "v"(oa[i]), "s"(ab), "s"(la + NTH * 16 * i) : "memory", "m0");
+#pragma unroll
+        for (int i = 0; i < BL; ++i)
+            asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dwordx4 %0, %1"
+                         :: "v"(ob[i]), "s"(bb), "s"(lb + NTH * 16 * i) : "memory", "m0");
+    };
+
+    f16x acc[TM][TN];
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j) acc[i][j] = f16x{};
+    auto ldf = [&](int s, int ks, f4v (&a)[TM], f4v (&bv)[TN]) {
+        const int c = ks * 2 + hh;
+#pragma unroll
+        for (int i = 0; i < TM; ++i) {
+            const int row = wm * WM + i * 32 + l32;
+            a[i] = As[s][row][c ^ chunk_swz(row)];
+        }
+#pragma unroll
+        for (int j = 0; j < TN; ++j) {
+            const int col = wn * WN + j * 32 + l32;
+            bv[j] = Bs[s][col][c ^ chunk_swz(col)];
+        }
+    };
+    const int ktiles = p.K / BK;   // K is padded to whole tiles
+#pragma unroll
+    for (int s = 0; s < STAGES - 1; ++s)
+        if (s < ktiles) issue(s);
+    for (int t = 0; t < ktiles; ++t) {
+        if (t + 1 < ktiles) __builtin_amdgcn_s_waitcnt((LPT & 15) | ((LPT >> 4) << 14) | 0x0F70);
+        else __builtin_amdgcn_s_waitcnt(0x0F70);
+        __syncthreads();
+        if (t + STAGES - 1 < ktiles) issue(t + STAGES - 1);
+        const int s = t % STAGES;
+        constexpr int KS = BK / 8;
+        f4v fa[KS][TM], fb[KS][TN];
+        ldf(s, 0, fa[0], fb[0]);
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) {
+            if (ks + 1 < KS) ldf(s, ks + 1, fa[ks + 1], fb[ks + 1]);
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+#pragma unroll
+                for (int i = 0; i < TM; ++i)
+#pragma unroll
+                    for (int j = 0; j < TN; ++j)
+                        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(fa[ks][i][e], fb[ks][j][e], acc[i][j],
+                                                                         0, 0, 0);
+        }
+    }
+#pragma unroll
+    for (int j = 0; j < TN; ++j) {
+        const int gn = n0 + wn * WN + j * 32 + l32;
+        if (gn >= p.N) continue;
+        int64_t col_off, row_stride;
+        if (p.out_mode == OUT_ROWMAJOR) {
+            col_off = gn;
+            row_stride = p.ldc;
+        } else {
+            const int img = gn / p.hw, pix = gn - img * p.hw;
+            col_off = (int64_t)img * p.M * p.hw + pix;
+            row_stride = p.hw;
+        }
+#pragma unroll
+        for (int i = 0; i < TM; ++i)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+                const int gm = m0 + wm * WM + i * 32 + 8 * (r >> 2) + 4 * hh + (r & 3);
+                if (gm < p.M) C[(int64_t)gm * row_stride + col_off] = acc[i][j][r];
+            }
+    }
+}
 
 template <int BM, int BN, int NW, bool IMPL>
 __global__ __launch_bounds__(NW * 64) void k_gemm_nt(const GemmParams p) {
@@ -480,16 +703,41 @@ void build_gemm_nt(const GemmParams& p0, int batch, LaunchRec* rec) {
     rec->set_params(p);
 }
 
+void build_gemm_nt_f32(const GemmParams& p0, int batch, LaunchRec* rec) {
+    int bm, bn;
+    nt_tile_shape(p0.M, p0.N, batch, &bm, &bn);
+    GemmParams p = p0;
+    const int tiles_m = (p.M + bm - 1) / bm;
+    p.tiles_n = (p.N + bn - 1) / bn;
+    rec->grid = dim3((unsigned)(tiles_m * p.tiles_n), 1, (unsigned)batch);
+    const bool impl = p.b_mode == B_NHWC;
+    if (bn == 256) {
+        rec->fn = impl ? (const void*)k_gemm_nt_f32<128, 256, 8, true> : (const void*)k_gemm_nt_f32<128, 256, 8, false>;
+        rec->block = dim3(512, 1, 1);
+        rec->name = impl ? "gemm_nt_f32_conv_128x256" : "gemm_nt_f32_128x256";
+    } else if (bm == 64) {
+        rec->fn = impl ? (const void*)k_gemm_nt_f32<64, 128, 2, true> : (const void*)k_gemm_nt_f32<64, 128, 2, false>;
+        rec->block = dim3(128, 1, 1);
+        rec->name = impl ? "gemm_nt_f32_conv_64x128" : "gemm_nt_f32_64x128";
+    } else {
+        rec->fn = impl ? (const void*)k_gemm_nt_f32<128, 128, 4, true> : (const void*)k_gemm_nt_f32<128, 128, 4, false>;
+        rec->block = dim3(256, 1, 1);
+        rec->name = impl ? "gemm_nt_f32_conv_128x128" : "gemm_nt_f32_128x128";
+    }
+    rec->set_params(p);
+}
+
 void build_conv_prep(const ConvPrepParams& p0, LaunchRec* rec) {
     ConvPrepParams p = p0;
     const ConvGeom& g = p.g;
     const int Hp = g.H + 2 * g.pad, Wp = g.W + 2 * g.pad;
     p.xblocks = p.nimg * Hp * ((Wp + 63) / 64);
-    p.wblocks = (int32_t)(((int64_t)p.Cop * (p.Kd / 8) + 255) / 256);
-    rec->fn = (const void*)k_conv_prep;
+    const bool f32 = p.elem_bytes == 4;
+    p.wblocks = (int32_t)(((int64_t)p.Cop * (p.Kd / (f32 ? 4 : 8)) + 255) / 256);
+    rec->fn = f32 ? (const void*)k_conv_prep_f32 : (const void*)k_conv_prep;
     rec->grid = dim3((unsigned)std::max(p.xblocks, p.wblocks), 2, 1);
     rec->block = dim3(256, 1, 1);
-    rec->name = "conv_prep_nhwc_f16";
+    rec->name = f32 ? "conv_prep_nhwc_f32" : "conv_prep_nhwc_f16";
     rec->set_params(p);
 }
 

@@ -67,12 +67,14 @@ struct SumsParams {
     int32_t batch;
 };
 
-// Explicit im2col: col[k][p] (int16), k = (ci*KH + kh)*KW + kw, p = (n*Ho + oh)*Wo + ow.
+// Explicit im2col: col[k][p], k = (ci*KH + kh)*KW + kw, p = (n*Ho + oh)*Wo + ow,
+// elements of elem_bytes (2: int16, 4: int32 or float32) copied as they are.
 struct Im2colParams {
-    const int16_t* x;
-    int16_t* col;
+    const void* x;
+    void* col;
     int64_t P;              // N*Ho*Wo
     int32_t Kd;             // Ci*KH*KW
+    int32_t elem_bytes;
     ConvGeom g;
 };
 
@@ -89,6 +91,9 @@ struct EncParams {
     int32_t* sums;          // int8 limb routes with an offset: row sums [batch][M] of A
                             // (A encoder) or per-64-k-slice column sums [batch][Kp/64][N]
                             // of B (B^T encoder), of the values the split represents
+    int32_t conv;           // B^T encoder: 1 = B is the im2col matrix of the NCHW image
+                            // src with geometry g (gathered, never materialised)
+    ConvGeom g;
 };
 
 // Both operand encoders of the int8 limb routes in one launch.
@@ -110,13 +115,16 @@ struct Im2colTParams {
 // Implicit lowering of a convolution (C_in a multiple of 64): the input as a
 // zero-bordered NHWC fp16 copy xp [N][H+2pad][W+2pad][Ci] and the weights as
 // w16 [Cop][Kd] fp16 with k = (kh*KW + kw)*Ci + ci, in one launch.
+// elem_bytes 2: int16 in, fp16 out (C_in a multiple of 64); 4: float32
+// copied unchanged (C_in a multiple of 32).
 struct ConvPrepParams {
-    const int16_t* x;       // NCHW
-    const int16_t* w;       // OIHW
-    _Float16* xp;
-    _Float16* w16;
+    const void* x;          // NCHW
+    const void* w;          // OIHW
+    void* xp;
+    void* w16;
     int32_t nimg, Co, Cop, Kd;
     int32_t xblocks, wblocks;
+    int32_t elem_bytes;
     ConvGeom g;
 };
 
@@ -225,7 +233,8 @@ enum Route : int32_t {
     R_AUTO = 0, R_I8_DIRECT = 1, R_F16_EXACT = 2, R_I8_KARATSUBA = 3, R_I8_OFFSET4 = 4,
     R_VALU_DOT2 = 5, R_S24_VALU = 6, R_S24_I8LIMB = 7,
     R_ATTN_F32_MFMA = 8, R_ATTN_I32_MFMA = 9, R_ATTN_I32_VALU = 10,
-    R_ATTN_F32_VALU = 11,   // internal fallback for shapes the fp32 MFMA kernel does not take
+    R_ATTN_F32_VALU = 11,   // fp32 attention on the vector ALU (shapes the MFMA kernel does not take)
+    R_F32_MFMA = 12, R_F32_VALU = 13,   // FP32 convolution: fp32 matrix cores / vector ALU
 };
 
 // Integer GEMM main kernel for an MFMA route; returns false if unsupported.
@@ -248,6 +257,8 @@ void build_enc_a(const EncParams& p, LaunchRec* rec);
 void build_enc_bt(const EncParams& p, LaunchRec* rec);
 void build_im2col_t(const Im2colTParams& p, LaunchRec* rec);
 void build_conv_prep(const ConvPrepParams& p, LaunchRec* rec);
+// FP32 NT GEMM on the fp32 matrix cores (conv FP32 row); same tile shapes.
+void build_gemm_nt_f32(const GemmParams& p, int batch, LaunchRec* rec);
 // int8 limb routes for large problems: limb-plane encoders + direct-to-LDS NT GEMM.
 void i8nt_tile_shape(int32_t route, int64_t M, int64_t N, int64_t batch, int* bm, int* bn);
 void build_enc_limb(int32_t route, bool s24, const EncPairParams& p, LaunchRec* rec);

@@ -26,6 +26,7 @@ ROUTE = {
     "auto": 0, "i8_direct": 1, "f16_exact": 2, "i8_karatsuba": 3, "i8_offset4": 4,
     "valu_dot2": 5, "s24_valu": 6, "s24_i8limb": 7,
     "attn_f32_mfma": 8, "attn_i32_mfma": 9, "attn_i32_valu": 10, "attn_f32_valu": 11,
+    "f32_mfma": 12, "f32_valu": 13,
 }
 ROUTE_NAME = {v: k for k, v in ROUTE.items()}
 
@@ -67,10 +68,12 @@ def lib() -> ctypes.CDLL:
             "qgemm_i16i32": [_p, _p, _p, _i64, _i64, _i64, _i64, _i32, _i32, _p],
             "qgemm_i32_s24": [_p, _p, _p, _i64, _i64, _i64, _i64, _p],
             "conv2d_gemm": [_p, _p, _p] + [_i64] * 9 + [_i32, _i32, _p],
+            "conv2d_gemm_t": [_i32, _p, _p, _p] + [_i64] * 9 + [_p],
             "attn_core": [_i32, _p, _p, _p, _p, _i64, _i64, _i32, _p],
             "qx_exec_create_gemm_i16i32": [_p, _i64, _i64, _i64, _i64, _i32, _i32, _i32],
             "qx_exec_create_gemm_i32_s24": [_p, _i64, _i64, _i64, _i64, _i32],
             "qx_exec_create_conv2d": [_p] + [_i64] * 9 + [_i32, _i32, _i32],
+            "qx_exec_create_conv2d_t": [_p, _i32] + [_i64] * 9 + [_i32],
             "qx_exec_create_attn": [_p, _i32, _i64, _i64, _i32, _i32],
             "qx_exec_run": [_p, _p, _p, _p],
             "qx_exec_plan": [_p, _p],
@@ -79,6 +82,7 @@ def lib() -> ctypes.CDLL:
             "qx_plan_gemm_i16i32": [_p, _i64, _i64, _i64, _i64, _i32, _i32, _i32],
             "qx_plan_gemm_i32_s24": [_p, _i64, _i64, _i64, _i64, _i32],
             "qx_plan_conv2d": [_p] + [_i64] * 9 + [_i32, _i32, _i32],
+            "qx_plan_conv2d_t": [_p, _i32] + [_i64] * 9 + [_i32],
             "qx_plan_attn": [_p, _i32, _i64, _i64, _i32, _i32],
         }
         for name, args in sig.items():
@@ -198,6 +202,29 @@ def conv2d_gemm(x, w, stride: int = 1, pad: int = 0, bound_x: int = 0, bound_w: 
     return out
 
 
+def conv2d_gemm_t(x, w, stride: int = 1, pad: int = 0, out=None, stream=None):
+    """Conv2D on float32 (fp32 sum) or int32 (smul24 contract, exact mod 2^32)
+    NCHW x and OIHW w -> NCHW y of the same dtype."""
+    torch = _torch()
+    if x.dtype == torch.float32:
+        dt = DT_F32
+    elif x.dtype == torch.int32:
+        dt = DT_I32
+    else:
+        raise TypeError("x must be float32 or int32")
+    N, Ci, H, W = x.shape
+    Co, Ci2, KH, KW = w.shape
+    if Ci2 != Ci:
+        raise ValueError("channel mismatch")
+    Ho, Wo = conv_out_hw(H, W, KH, KW, stride, pad)
+    if out is None:
+        out = torch.empty((N, Co, max(Ho, 0), max(Wo, 0)), dtype=x.dtype, device=x.device)
+    check(lib().conv2d_gemm_t(dt, _dev_tensor(x, x.dtype, "x"), _dev_tensor(w, x.dtype, "w"),
+                              _dev_tensor(out, x.dtype, "y"), N, Ci, H, W, Co, KH, KW, stride, pad,
+                              _stream(stream)))
+    return out
+
+
 def attn_core(Q, K, V, bound: int = 0, out=None, stream=None):
     """O = (Q K^T) V for [L, d] float32 or int32 tensors."""
     torch = _torch()
@@ -239,6 +266,13 @@ def plan_conv2d(N, Ci, H, W, Co, KH, KW, stride=1, pad=0, bound_x=0, bound_w=0, 
     info = PlanInfo()
     check(lib().qx_plan_conv2d(ctypes.byref(info), N, Ci, H, W, Co, KH, KW, stride, pad,
                                bound_x, bound_w, _route(route)))
+    return info.as_dict()
+
+
+def plan_conv2d_t(dtype: str, N, Ci, H, W, Co, KH, KW, stride=1, pad=0, route="auto") -> dict:
+    info = PlanInfo()
+    check(lib().qx_plan_conv2d_t(ctypes.byref(info), DT_F32 if dtype == "f32" else DT_I32, N, Ci, H, W,
+                                 Co, KH, KW, stride, pad, _route(route)))
     return info.as_dict()
 
 
@@ -284,6 +318,16 @@ class Executor:
                                           bound_x, bound_w, _route(route)))
         Ho, Wo = conv_out_hw(H, W, KH, KW, stride, pad)
         return cls(h, (N, Co, Ho, Wo), torch.int32, 2)
+
+    @classmethod
+    def conv2d_t(cls, dtype: str, N, Ci, H, W, Co, KH, KW, stride=1, pad=0, route="auto"):
+        torch = _torch()
+        h = ctypes.c_void_p()
+        dt = DT_F32 if dtype == "f32" else DT_I32
+        check(lib().qx_exec_create_conv2d_t(ctypes.byref(h), dt, N, Ci, H, W, Co, KH, KW, stride, pad,
+                                            _route(route)))
+        Ho, Wo = conv_out_hw(H, W, KH, KW, stride, pad)
+        return cls(h, (N, Co, Ho, Wo), torch.float32 if dtype == "f32" else torch.int32, 2)
 
     @classmethod
     def attn(cls, dtype: str, L, d, bound=0, route="auto"):

@@ -5,9 +5,11 @@ arithmetic, so both the HIP path and the CPU oracle can take their inputs from
 it.  The paper gives no shapes for its operator table and uses no dataset, so
 the workloads below are synthetic by definition: a small INT16 GEMM (values in
 [-1024, 1023]), smul24 INT32 GEMMs over the full signed 24-bit range, an INT16
-3x3 convolution, the FP32 and INT32 attention cores, and the large INT16 GEMMs
-(values in [-256, 255]).  Integers are uniform over a closed range; FP32 inputs
-are N(0, 1) / sqrt(d).
+3x3 convolution, the FP32 and INT32 attention cores, the large INT16 GEMMs
+(values in [-256, 255]), and the same 3x3 convolution on FP32 and on smul24
+INT32 operands.  Integers are uniform over a closed range; FP32 attention
+inputs are N(0, 1) / sqrt(d), FP32 convolution inputs N(0, 1) with weights
+N(0, 1) / sqrt(C_in KH KW).
 """
 from __future__ import annotations
 
@@ -29,7 +31,8 @@ def normal_f32(rng: np.random.Generator, shape, scale: float) -> np.ndarray:
 @dataclass(frozen=True)
 class Workload:
     name: str
-    op: str            # "gemm_i16i32" | "gemm_i32_s24" | "conv2d" | "attn_f32" | "attn_i32"
+    op: str            # "gemm_i16i32" | "gemm_i32_s24" | "conv2d" | "conv2d_f32" | "conv2d_i32"
+                       # | "attn_f32" | "attn_i32"
     seed: int
     dims: dict = field(default_factory=dict)
     lo: int = 0
@@ -42,7 +45,7 @@ class Workload:
         d = self.dims
         if self.op in ("gemm_i16i32", "gemm_i32_s24"):
             return 2.0 * d["M"] * d["N"] * d["K"] * d["batch"]
-        if self.op == "conv2d":
+        if self.op in ("conv2d", "conv2d_f32", "conv2d_i32"):
             ho = (d["H"] + 2 * d["pad"] - d["KH"]) // d["stride"] + 1
             wo = (d["W"] + 2 * d["pad"] - d["KW"]) // d["stride"] + 1
             return 2.0 * d["N"] * d["Co"] * ho * wo * d["Ci"] * d["KH"] * d["KW"]
@@ -68,6 +71,14 @@ class Workload:
             x = ints(rng, (d["N"], d["Ci"], d["H"], d["W"]), self.lo, self.hi, np.int16)
             w = ints(rng, (d["Co"], d["Ci"], d["KH"], d["KW"]), self.lo, self.hi, np.int16)
             return x, w
+        if self.op == "conv2d_f32":
+            x = normal_f32(rng, (d["N"], d["Ci"], d["H"], d["W"]), 1.0)
+            w = normal_f32(rng, (d["Co"], d["Ci"], d["KH"], d["KW"]), 1.0 / np.sqrt(d["Ci"] * d["KH"] * d["KW"]))
+            return x, w
+        if self.op == "conv2d_i32":
+            x = ints(rng, (d["N"], d["Ci"], d["H"], d["W"]), self.lo, self.hi, np.int32)
+            w = ints(rng, (d["Co"], d["Ci"], d["KH"], d["KW"]), self.lo, self.hi, np.int32)
+            return x, w
         if self.op == "attn_f32":
             s = 1.0 / np.sqrt(d["d"])
             return tuple(normal_f32(rng, (d["L"], d["d"]), s) for _ in range(3))
@@ -90,4 +101,9 @@ WORKLOADS = {w.name: w for w in [
     Workload("attn_i32_4096x64", "attn_i32", 6, dict(L=4096, d=64), -64, 63, 64),
     _gemm("gemm_i16_8192", "gemm_i16i32", 7, 8192, 8192, 8192, 1, -256, 255),
     _gemm("gemm_i16_64x2048", "gemm_i16i32", 8, 2048, 2048, 2048, 64, -256, 255),
+    Workload("conv_f32_8x64x56x56_128_3x3", "conv2d_f32", 9,
+             dict(N=8, Ci=64, H=56, W=56, Co=128, KH=3, KW=3, stride=1, pad=1)),
+    Workload("conv_i32_8x64x56x56_128_3x3", "conv2d_i32", 10,
+             dict(N=8, Ci=64, H=56, W=56, Co=128, KH=3, KW=3, stride=1, pad=1),
+             -(1 << 23), (1 << 23) - 1, 1 << 23),
 ]}

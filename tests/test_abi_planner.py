@@ -68,6 +68,36 @@ def test_limb_routes_take_the_encode_nt_structure_when_large():
     assert qx.plan_gemm_i16i32(64, 64, 64, 1, 127, 127)["kernels"] == 1
 
 
+def test_conv_f32_i32_plans():
+    # FP32: the fp32 matrix cores when C_in % 32 == 0 (prep launch + gathering
+    # NT GEMM), else explicit lowering + vector-ALU fp32 GEMM
+    p = qx.plan_conv2d_t("f32", 8, 64, 56, 56, 128, 3, 3, 1, 1)
+    assert p["route_name"] == "f32_mfma" and p["kernels"] == 2
+    assert p["workspace_bytes"] >= 4 * 8 * 58 * 58 * 64 + 4 * 128 * 576
+    p = qx.plan_conv2d_t("f32", 2, 3, 20, 20, 8, 3, 3, 1, 1)
+    assert p["route_name"] == "f32_valu" and p["kernels"] == 2
+    with pytest.raises(qx.QxError) as e:
+        qx.plan_conv2d_t("f32", 2, 3, 20, 20, 8, 3, 3, 1, 1, "f32_mfma")
+    assert e.value.status == qx.ERR_UNSUPPORTED
+    with pytest.raises(qx.QxError) as e:
+        qx.plan_conv2d_t("f32", 2, 32, 20, 20, 8, 3, 3, 1, 1, "f16_exact")
+    assert e.value.status == qx.ERR_INVALID_ARG
+    # INT32 (smul24): large problems gather the im2col columns inside the
+    # limb-plane encoder (no column matrix), then the NT int8 contraction;
+    # small ones lower explicitly and run the register-staged smul24 GEMM
+    p = qx.plan_conv2d_t("i32", 8, 64, 56, 56, 128, 3, 3, 1, 1)
+    assert p["route_name"] == "s24_i8limb" and p["kernels"] == 2
+    assert p["workspace_bytes"] < 4 * 576 * 8 * 56 * 56
+    p = qx.plan_conv2d_t("i32", 1, 4, 8, 8, 4, 3, 3, 1, 1)
+    assert p["route_name"] == "s24_i8limb" and p["kernels"] == 3   # im2col, sums, GEMM
+    assert qx.plan_conv2d_t("i32", 1, 2, 5, 5, 3, 3, 3, 1, 1, "s24_valu")["route_name"] == "s24_valu"
+    with pytest.raises(qx.QxError) as e:
+        qx.plan_conv2d_t("i32", 1, 2, 5, 5, 3, 3, 3, 1, 1, "f32_mfma")
+    assert e.value.status == qx.ERR_INVALID_ARG
+    assert qx.plan_conv2d_t("f32", 0, 32, 5, 5, 3, 3, 3, 1, 1)["kernels"] == 0
+    assert qx.plan_conv2d_t("i32", 1, 0, 5, 5, 3, 3, 3, 1, 1)["kernels"] == 1
+
+
 @pytest.mark.parametrize("b,route", [
     (1, "i8_direct"), (127, "i8_direct"), (128, "f16_exact"), (256, "f16_exact"),
     (1024, "f16_exact"), (2048, "i8_karatsuba"), (8127, "i8_karatsuba"),

@@ -499,6 +499,88 @@ def test_workload_conv_full_oracle():
     same(y, orc.conv2d_direct(x, wt, d["stride"], d["pad"]))
 
 
+CONV_T_CASES = [  # N, Ci, H, W, Co, KH, KW, stride, pad: fp32 MFMA needs C_in % 32 == 0
+    (1, 32, 8, 8, 16, 3, 3, 1, 1), (2, 64, 30, 26, 100, 3, 3, 1, 1), (3, 96, 17, 19, 40, 3, 3, 2, 1),
+    (2, 32, 23, 23, 64, 7, 7, 2, 3), (4, 64, 9, 33, 48, 5, 3, 1, 2), (1, 3, 20, 20, 8, 3, 3, 1, 1),
+    (2, 5, 9, 7, 5, 3, 3, 1, 1), (3, 12, 17, 9, 7, 3, 2, 3, 0),
+]
+
+
+@pytest.mark.parametrize("case", CONV_T_CASES)
+def test_conv_f32(case):
+    # FP32 conv (Table 2, Conv2D FP32 row): normwise 1e-4 against the float64
+    # sum, and the elementwise a-priori bound Kd * 2^-24 * (|x| conv |w|) of an
+    # fp32 sum in any order; repeated runs are bit-identical.
+    N, Ci, H, W, Co, KH, KW, s, p = case
+    rng = np.random.default_rng(zlib.crc32(repr(("f32", case)).encode()))
+    x = rng.standard_normal((N, Ci, H, W)).astype(np.float32)
+    w = (rng.standard_normal((Co, Ci, KH, KW)) / np.sqrt(Ci * KH * KW)).astype(np.float32)
+    with qx.Executor.conv2d_t("f32", N, Ci, H, W, Co, KH, KW, s, p) as ex:
+        plan = ex.plan()
+        assert plan["route_name"] == ("f32_mfma" if Ci % 32 == 0 else "f32_valu"), plan
+        y = run_exec(ex, (x, w))
+        y2 = run_exec(ex, (x, w))
+    R = orc.conv2d_f64(x, w, s, p)
+    assert normwise(y, R) <= 1e-4
+    absref = orc.conv2d_f64(np.abs(x), np.abs(w), s, p)
+    assert (np.abs(y - R) <= Ci * KH * KW * 2.0 ** -24 * absref + 1e-30).all()
+    assert np.array_equal(y, y2)
+    if Ci % 32 == 0:   # the vector-ALU route on the same data meets the same bar
+        with qx.Executor.conv2d_t("f32", N, Ci, H, W, Co, KH, KW, s, p, "f32_valu") as ex:
+            yv = run_exec(ex, (x, w))
+        assert normwise(yv, R) <= 1e-4
+
+
+@pytest.mark.parametrize("route", ["s24_i8limb", "s24_valu"])
+@pytest.mark.parametrize("case", CONV_T_CASES[:5] + [(8, 64, 20, 20, 96, 3, 3, 1, 1)])
+def test_conv_i32_smul24(route, case):
+    # INT32 conv under the smul24 contract: full 32-bit words (bits 24..31
+    # ignored), bit-exact mod 2^32 against the oracle.
+    N, Ci, H, W, Co, KH, KW, s, p = case
+    rng = np.random.default_rng(zlib.crc32(repr(("i32", route, case)).encode()))
+    x = rng.integers(-(1 << 31), (1 << 31) - 1, (N, Ci, H, W), dtype=np.int32, endpoint=True)
+    w = rng.integers(-(1 << 31), (1 << 31) - 1, (Co, Ci, KH, KW), dtype=np.int32, endpoint=True)
+    x[0, :, 0, :] = -(1 << 23)
+    w[0] = (1 << 23) - 1
+    with qx.Executor.conv2d_t("i32", N, Ci, H, W, Co, KH, KW, s, p, route) as ex:
+        assert ex.plan()["route_name"] == route
+        y = run_exec(ex, (x, w))
+    same(y, orc.conv2d_s24(x, w, s, p), str((route, case)))
+
+
+def test_conv_t_oneshot_and_empty():
+    rng = np.random.default_rng(4)
+    x = rng.standard_normal((1, 32, 6, 5)).astype(np.float32)
+    w = rng.standard_normal((3, 32, 3, 3)).astype(np.float32)
+    y = host(qx.conv2d_gemm_t(dev(x), dev(w), 1, 1))
+    assert normwise(y, orc.conv2d_f64(x, w, 1, 1)) <= 1e-4
+    xi = rng.integers(-(1 << 23), (1 << 23) - 1, (2, 3, 5, 5), dtype=np.int32)
+    wi = rng.integers(-(1 << 23), (1 << 23) - 1, (4, 3, 2, 2), dtype=np.int32)
+    same(host(qx.conv2d_gemm_t(dev(xi), dev(wi), 2, 0)), orc.conv2d_s24(xi, wi, 2, 0))
+    # C_in == 0 -> zeros
+    z = qx.conv2d_gemm_t(torch.empty((1, 0, 4, 4), dtype=torch.float32, device="cuda"),
+                         torch.empty((2, 0, 3, 3), dtype=torch.float32, device="cuda"), 1, 1)
+    assert z.shape == (1, 2, 4, 4) and float(z.abs().sum()) == 0.0
+
+
+def test_workload_conv_t_full_oracle():
+    wf = WORKLOADS["conv_f32_8x64x56x56_128_3x3"]
+    x, w = wf.generate()
+    d = wf.dims
+    with qx.Executor.conv2d_t("f32", d["N"], d["Ci"], d["H"], d["W"], d["Co"], d["KH"], d["KW"],
+                              d["stride"], d["pad"]) as ex:
+        y = run_exec(ex, (x, w))
+    err = normwise(y, orc.conv2d_f64(x, w, d["stride"], d["pad"]))
+    _say(f"[conv_f32] normwise error {err:.3e}")
+    assert err <= 1e-4
+    wi = WORKLOADS["conv_i32_8x64x56x56_128_3x3"]
+    x, w = wi.generate()
+    with qx.Executor.conv2d_t("i32", d["N"], d["Ci"], d["H"], d["W"], d["Co"], d["KH"], d["KW"],
+                              d["stride"], d["pad"]) as ex:
+        y = run_exec(ex, (x, w))
+    same(y, orc.conv2d_s24(x, w, d["stride"], d["pad"]))
+
+
 def test_workload_attn_full_oracle():
     wf = WORKLOADS["attn_f32_4096x64"]
     Q, K, V = wf.generate()
