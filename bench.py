@@ -225,7 +225,11 @@ def main():
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "i16",
+        # the arithmetic the contraction runs in: fp16 products summed exactly
+        # in fp32 per chunk, chunks added in int32 (the result is the exact
+        # int32 GEMM of the int16 inputs)
+        "dtype": {"f16_exact": "f16", "s24_i8limb": "i8", "i8_direct": "i8", "i8_karatsuba": "i8",
+                  "i8_offset4": "i8"}.get(route, "i32"),
         "data": "synthetic",
         "config": {"workload": w.name, **w.dims, "operand_range": [w.lo, w.hi], "seed": w.seed,
                    "route": route, "chunk": r["plan"]["chunk"]},

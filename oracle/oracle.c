@@ -233,6 +233,59 @@ void oracle_conv2d_f64_direct(const float* x, const float* w, double* y,
     }
 }
 
+/* Min/max reduction (Table 2, Min/max rows): out[0] = min, out[1] = max of
+ * the n values; n >= 1. */
+void oracle_minmax_i32(const int32_t* x, int64_t n, int32_t* out) {
+    int32_t lo = x[0], hi = x[0];
+    for (int64_t i = 1; i < n; ++i) {
+        if (x[i] < lo) lo = x[i];
+        if (x[i] > hi) hi = x[i];
+    }
+    out[0] = lo;
+    out[1] = hi;
+}
+
+void oracle_minmax_i16(const int16_t* x, int64_t n, int16_t* out) {
+    int16_t lo = x[0], hi = x[0];
+    for (int64_t i = 1; i < n; ++i) {
+        if (x[i] < lo) lo = x[i];
+        if (x[i] > hi) hi = x[i];
+    }
+    out[0] = lo;
+    out[1] = hi;
+}
+
+/* 2x2 pooling with stride 2, no padding (Table 2, AvgPool INT32 and MaxPool
+ * FP32 rows): x NCHW [N][C][H][W] -> y [N][C][H/2][W/2] (floor; a trailing
+ * odd row or column is dropped).  The INT32 average is the floor of the
+ * exact sum of the four values divided by 4. */
+void oracle_avgpool2_i32(const int32_t* x, int32_t* y, int64_t N, int64_t C, int64_t H, int64_t W) {
+    const int64_t Ho = H / 2, Wo = W / 2;
+    for (int64_t nc = 0; nc < N * C; ++nc)
+        for (int64_t oh = 0; oh < Ho; ++oh)
+            for (int64_t ow = 0; ow < Wo; ++ow) {
+                const int32_t* p = x + (nc * H + 2 * oh) * W + 2 * ow;
+                int64_t s = (int64_t)p[0] + p[1] + p[W] + p[W + 1];
+                int64_t q = s / 4;
+                if (s % 4 != 0 && s < 0) q -= 1;   /* floor, not truncation */
+                y[(nc * Ho + oh) * Wo + ow] = (int32_t)q;
+            }
+}
+
+void oracle_maxpool2_f32(const float* x, float* y, int64_t N, int64_t C, int64_t H, int64_t W) {
+    const int64_t Ho = H / 2, Wo = W / 2;
+    for (int64_t nc = 0; nc < N * C; ++nc)
+        for (int64_t oh = 0; oh < Ho; ++oh)
+            for (int64_t ow = 0; ow < Wo; ++ow) {
+                const float* p = x + (nc * H + 2 * oh) * W + 2 * ow;
+                float m = p[0];
+                if (p[1] > m) m = p[1];
+                if (p[W] > m) m = p[W];
+                if (p[W + 1] > m) m = p[W + 1];
+                y[(nc * Ho + oh) * Wo + ow] = m;
+            }
+}
+
 /* Attention core, INT32 (Methodology: O = (Q K^T) V; Table 2, INT32 row).
  * No scale, softmax or mask; one head; Q, K, V, O are [L][d] row-major.
  * S = Q K^T is formed exactly, then O = S V (mod 2^32). */

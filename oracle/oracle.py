@@ -49,6 +49,10 @@ def _load():
         for name in ("oracle_attn_i32", "oracle_attn_i32_assoc", "oracle_attn_f64",
                      "oracle_attn_f64_assoc", "oracle_attn_f32"):
             getattr(lib, name).argtypes = [p, p, p, p, i64, i64]
+        lib.oracle_minmax_i32.argtypes = [p, i64, p]
+        lib.oracle_minmax_i16.argtypes = [p, i64, p]
+        for name in ("oracle_avgpool2_i32", "oracle_maxpool2_f32"):
+            getattr(lib, name).argtypes = [p, p, i64, i64, i64, i64]
         _lib = lib
     return _lib
 
@@ -165,3 +169,35 @@ def attn_f64_assoc(Q, K, V):
 def attn_f32(Q, K, V):
     """plain float32, sequential summation order."""
     return _attn(_load().oracle_attn_f32, Q, K, V, np.float32, np.float32)
+
+
+def minmax(x):
+    """(min, max) of a non-empty int32 or int16 array (Table 2, Min/max rows)."""
+    x = np.asarray(x)
+    if x.dtype == np.int16:
+        x = _c(x, np.int16)
+        out = np.empty(2, np.int16)
+        _load().oracle_minmax_i16(_ptr(x), x.size, _ptr(out))
+    else:
+        x = _c(x, np.int32)
+        out = np.empty(2, np.int32)
+        _load().oracle_minmax_i32(_ptr(x), x.size, _ptr(out))
+    return out
+
+
+def _pool(fn, x, dtype):
+    x = _c(x, dtype)
+    N, C, H, W = x.shape
+    y = np.empty((N, C, H // 2, W // 2), dtype)
+    fn(_ptr(x), _ptr(y), N, C, H, W)
+    return y
+
+
+def avgpool2_i32(x):
+    """2x2 / stride 2 average of int32 NCHW: floor(sum of 4 / 4) (Table 2, AvgPool row)."""
+    return _pool(_load().oracle_avgpool2_i32, x, np.int32)
+
+
+def maxpool2_f32(x):
+    """2x2 / stride 2 maximum of float32 NCHW (Table 2, MaxPool row)."""
+    return _pool(_load().oracle_maxpool2_f32, x, np.float32)

@@ -363,3 +363,51 @@ def test_attn_f64_orders_and_numpy_agree():
     absref = (np.abs(Q).astype(np.float64) @ np.abs(K).astype(np.float64).T) @ np.abs(V)
     u = 2.0 ** -24
     assert (np.abs(F - R) <= (d + L) * u * absref + 1e-30).all()
+
+
+# ----------------------------------------------------------------------------
+# Min/max, 2x2 average and max pooling (Table 2 rows)
+# ----------------------------------------------------------------------------
+@pytest.mark.parametrize("n", [1, 2, 7, 1000, 65537])
+def test_minmax_against_numpy(n):
+    rng = np.random.default_rng(n)
+    for dt, lo, hi in ((np.int32, -(1 << 31), (1 << 31) - 1), (np.int16, -32768, 32767)):
+        x = rng.integers(lo, hi, n, dtype=dt, endpoint=True)
+        assert orc.minmax(x).tolist() == [int(x.min()), int(x.max())]
+    # the extremes sit anywhere, including first and last
+    x = np.zeros(9, np.int32)
+    x[0], x[-1] = -(1 << 31), (1 << 31) - 1
+    assert orc.minmax(x).tolist() == [-(1 << 31), (1 << 31) - 1]
+    x = np.full(5, -3, np.int16)
+    assert orc.minmax(x).tolist() == [-3, -3]
+
+
+@pytest.mark.parametrize("shape", [(1, 1, 2, 2), (2, 3, 6, 8), (1, 2, 7, 9), (3, 1, 5, 4)])
+def test_pools_against_numpy(shape):
+    N, C, H, W = shape
+    rng = np.random.default_rng(H * W + C)
+    x = rng.integers(-(1 << 31), (1 << 31) - 1, shape, dtype=np.int32, endpoint=True)
+    Ho, Wo = H // 2, W // 2
+    win = x[:, :, :2 * Ho, :2 * Wo].astype(np.int64).reshape(N, C, Ho, 2, Wo, 2)
+    assert (orc.avgpool2_i32(x) == win.sum(axis=(3, 5)) // 4).all()   # numpy floor division
+    xf = rng.standard_normal(shape).astype(np.float32)
+    winf = xf[:, :, :2 * Ho, :2 * Wo].reshape(N, C, Ho, 2, Wo, 2)
+    assert (orc.maxpool2_f32(xf) == winf.max(axis=(3, 5))).all()
+
+
+def test_pool_closed_forms():
+    # constant input: the average and the maximum are the constant
+    x = np.full((1, 2, 4, 6), -123456789, np.int32)
+    assert (orc.avgpool2_i32(x) == -123456789).all()
+    assert (orc.maxpool2_f32(np.full((1, 1, 4, 4), 2.5, np.float32)) == 2.5).all()
+    # floor of a negative quarter, exact sum beyond int32
+    x = np.array([[[[1, 2], [3, -7]]]], np.int32)
+    assert orc.avgpool2_i32(x)[0, 0, 0, 0] == -1
+    big = (1 << 31) - 1
+    assert orc.avgpool2_i32(np.full((1, 1, 2, 2), big, np.int32))[0, 0, 0, 0] == big
+    assert orc.avgpool2_i32(np.full((1, 1, 2, 2), -big - 1, np.int32))[0, 0, 0, 0] == -big - 1
+    # the maximum of one window picks each position in turn
+    for pos in range(4):
+        v = np.zeros(4, np.float32)
+        v[pos] = 1.0
+        assert orc.maxpool2_f32(v.reshape(1, 1, 2, 2))[0, 0, 0, 0] == 1.0
