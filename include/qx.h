@@ -151,6 +151,23 @@ qx_status conv2d_gemm_t(qx_attn_dtype dt, const void* x, const void* w, void* y,
                         int64_t N, int64_t C_in, int64_t H, int64_t W, int64_t C_out,
                         int64_t KH, int64_t KW, int64_t stride, int64_t pad, void* stream);
 
+/* Min/max (Table 2, Min/max rows): out[0] = min, out[1] = max of the n >= 1
+ * values of x; elem_bytes 4 = int32, 2 = int16.  out is a device pointer to
+ * two elements of the input type (aligned to the element size); x must be
+ * 16-byte aligned.  n == 0 is QX_ERR_INVALID_ARG (no minimum exists). */
+qx_status minmax(const void* x, int64_t n, int32_t elem_bytes, void* out, void* stream);
+
+/* 2x2 / stride 2 pooling without padding (Table 2, AvgPool INT32 and MaxPool
+ * FP32 rows): x NCHW [N][C][H][W] -> y [N][C][H/2][W/2] (a trailing odd row
+ * or column is dropped).
+ *  QX_POOL_AVG_I32: int32; y = floor((x00 + x01 + x10 + x11) / 4) of the exact sum.
+ *  QX_POOL_MAX_F32: float32; y = the window maximum (first value, replaced by
+ *                   each later one in row-major order that compares greater).
+ * x must be 16-byte aligned; with W % 8 == 0 so must y. */
+typedef enum { QX_POOL_AVG_I32 = 0, QX_POOL_MAX_F32 = 1 } qx_pool_kind;
+qx_status pool2x2(int32_t kind, const void* x, void* y, int64_t N, int64_t C, int64_t H, int64_t W,
+                  void* stream);
+
 /* Single-head attention core (Methodology: O = (Q K^T) V; Table 2, attention
  * rows): no scale, softmax or mask.  Q, K, V, O are [L][d] row-major.
  *  QX_DT_F32: float32 in and out.  The association (Q K^T) V is evaluated
@@ -183,8 +200,11 @@ qx_status qx_exec_create_conv2d_t(qx_exec* out, qx_attn_dtype dt, int64_t N, int
                                   int64_t stride, int64_t pad, int32_t route);
 qx_status qx_exec_create_attn(qx_exec* out, qx_attn_dtype dt, int64_t L, int64_t d,
                               int32_t bound, int32_t route);
+qx_status qx_exec_create_minmax(qx_exec* out, int64_t n, int32_t elem_bytes);
+qx_status qx_exec_create_pool2x2(qx_exec* out, int32_t kind, int64_t N, int64_t C, int64_t H, int64_t W);
 
-/* Enqueue one evaluation: inputs = {A, B} (GEMMs), {x, w} (convolutions) or
+/* Enqueue one evaluation: inputs = {A, B} (GEMMs), {x, w} (convolutions), {x}
+ * (min/max, pooling) or
  * {Q, K, V} (attention), device pointers with the shapes given at create.
  * Allocates nothing.  Calls on one handle must not overlap in time. */
 qx_status qx_exec_run(qx_exec h, const void* const* inputs, void* output, void* stream);
@@ -218,6 +238,8 @@ qx_status qx_plan_conv2d_t(qx_plan_info* out, qx_attn_dtype dt, int64_t N, int64
                            int64_t stride, int64_t pad, int32_t route);
 qx_status qx_plan_attn(qx_plan_info* out, qx_attn_dtype dt, int64_t L, int64_t d,
                        int32_t bound, int32_t route);
+qx_status qx_plan_minmax(qx_plan_info* out, int64_t n, int32_t elem_bytes);
+qx_status qx_plan_pool2x2(qx_plan_info* out, int32_t kind, int64_t N, int64_t C, int64_t H, int64_t W);
 
 /* Message of the last failing call on this thread ("" if none).  Valid
  * until the next qx call on the same thread. */

@@ -51,7 +51,8 @@ constexpr int64_t kMaxBatch = 65535;
 constexpr uint32_t kMagic = 0x71786578u;  // "qxex"
 
 enum OpKind : int32_t {
-    OP_GEMM_I16 = 1, OP_GEMM_S24 = 2, OP_CONV = 3, OP_ATTN_F32 = 4, OP_ATTN_I32 = 5, OP_CONV_F32 = 6, OP_CONV_I32 = 7
+    OP_GEMM_I16 = 1, OP_GEMM_S24 = 2, OP_CONV = 3, OP_ATTN_F32 = 4, OP_ATTN_I32 = 5, OP_CONV_F32 = 6, OP_CONV_I32 = 7,
+    OP_MINMAX = 8, OP_POOL = 9
 };
 
 // A fully planned operation: route facts plus launch records with unbound
@@ -71,6 +72,7 @@ struct Plan {
     int n_events = 0;        // cross-lane events used by the launches (0: one stream)
     int n_inputs = 0;
     uint64_t in_align = 16;  // required alignment of every input pointer
+    uint64_t out_align = 4;  // required alignment of the output pointer
 };
 
 bool mul_ok(int64_t a, int64_t b, int64_t lim, int64_t* out) {
@@ -801,6 +803,68 @@ qx_status plan_conv_t(Plan* pl, qx_attn_dtype dt, int64_t N, int64_t Ci, int64_t
     return QX_OK;
 }
 
+// Min/max over n >= 1 int32 or int16 values (Table 2, Min/max rows).
+qx_status plan_minmax(Plan* pl, int64_t n, int32_t elem_bytes) {
+    if (elem_bytes != 2 && elem_bytes != 4) return fail(QX_ERR_INVALID_ARG, "elem_bytes = %d must be 2 or 4", elem_bytes);
+    if (n < 1) return fail(QX_ERR_INVALID_ARG, "min/max needs n >= 1 (n = %lld)", (long long)n);
+    if (n > ((int64_t)1 << 40)) return fail(QX_ERR_UNSUPPORTED, "n = %lld exceeds 2^40", (long long)n);
+    pl->op = OP_MINMAX;
+    pl->n_inputs = 1;
+    pl->in_align = 16;
+    pl->out_align = (uint64_t)elem_bytes;
+    MinMaxParams m{};
+    m.n = n;
+    m.elem_bytes = elem_bytes;
+    minmax_blocks(n, &m.blocks, &m.per);
+    LaunchRec r1, r2;
+    build_minmax(m, &r1, &r2);
+    r1.bind(offsetof(MinMaxParams, x), BIND_IN0);
+    r1.bind(offsetof(MinMaxParams, part), BIND_WS, 0);
+    r2.bind(offsetof(MinMaxParams, part), BIND_WS, 0);
+    r2.bind(offsetof(MinMaxParams, out), BIND_OUT);
+    pl->launches = {r1, r2};
+    qx_plan_info& info = pl->info;
+    info.route = R_AUTO;
+    info.kernels = 2;
+    info.workspace_bytes = 8 * (int64_t)m.blocks;
+    info.tile_m = 1; info.tile_n = (int32_t)std::min<int64_t>(m.per, INT32_MAX); info.tile_k = 1;
+    return QX_OK;
+}
+
+// 2x2 / stride 2 pooling of NCHW tensors (Table 2, AvgPool INT32 and MaxPool
+// FP32 rows): y [N][C][H/2][W/2].
+qx_status plan_pool2(Plan* pl, int32_t kind, int64_t N, int64_t C, int64_t H, int64_t W) {
+    if (kind != POOL_AVG_I32 && kind != POOL_MAX_F32) return fail(QX_ERR_INVALID_ARG, "unknown pool kind %d", kind);
+    qx_status st = check_dims({{"N", N}, {"C", C}, {"H", H}, {"W", W}});
+    if (st) return st;
+    int64_t nc, t;
+    if (!mul_ok(N, C, kMaxDim, &nc) || !mul_ok(nc * H, W, (int64_t)1 << 40, &t))
+        return fail(QX_ERR_UNSUPPORTED, "tensor larger than 2^40 elements");
+    pl->op = OP_POOL;
+    pl->n_inputs = 1;
+    pl->in_align = 16;
+    const int64_t Ho = H / 2, Wo = W / 2;
+    qx_plan_info& info = pl->info;
+    info.route = R_AUTO;
+    info.workspace_bytes = 0;
+    if (nc == 0 || Ho == 0 || Wo == 0) {
+        info.kernels = 0;
+        return QX_OK;
+    }
+    PoolParams pp{};
+    pp.NC = nc; pp.H = (int32_t)H; pp.W = (int32_t)W; pp.Ho = (int32_t)Ho; pp.Wo = (int32_t)Wo;
+    pp.vec = W % 8 == 0 ? 1 : 0;
+    pl->out_align = pp.vec ? 16 : 4;
+    LaunchRec r;
+    build_pool2(kind, pp, &r);
+    r.bind(offsetof(PoolParams, x), BIND_IN0);
+    r.bind(offsetof(PoolParams, y), BIND_OUT);
+    pl->launches = {r};
+    info.kernels = 1;
+    info.tile_m = 2; info.tile_n = 8; info.tile_k = 1;
+    return QX_OK;
+}
+
 qx_status plan_attn(Plan* pl, qx_attn_dtype dt, int64_t L, int64_t d, int32_t bound, int32_t route) {
     qx_status st = check_dims({{"L", L}, {"d", d}});
     if (st) return st;
@@ -1077,6 +1141,8 @@ qx_status run_exec(qx_exec h, const void* const* inputs, void* output, void* str
             return fail(QX_ERR_INVALID_ARG, "input %d is not %llu-byte aligned", i, (unsigned long long)pl.in_align);
     }
     if (!output) return fail(QX_ERR_INVALID_ARG, "output is NULL");
+    if ((uintptr_t)output % pl.out_align)
+        return fail(QX_ERR_INVALID_ARG, "output is not %llu-byte aligned", (unsigned long long)pl.out_align);
     int dev = -1;
     hipError_t e = hipGetDevice(&dev);
     if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
@@ -1256,6 +1322,24 @@ qx_status qx_plan_conv2d_t(qx_plan_info* out, qx_attn_dtype dt, int64_t N, int64
     return st;
 }
 
+qx_status qx_plan_minmax(qx_plan_info* out, int64_t n, int32_t elem_bytes) {
+    g_err.clear();
+    if (!out) return fail(QX_ERR_INVALID_ARG, "out is NULL");
+    Plan pl;
+    qx_status st = plan_minmax(&pl, n, elem_bytes);
+    if (!st) *out = pl.info;
+    return st;
+}
+
+qx_status qx_plan_pool2x2(qx_plan_info* out, int32_t kind, int64_t N, int64_t C, int64_t H, int64_t W) {
+    g_err.clear();
+    if (!out) return fail(QX_ERR_INVALID_ARG, "out is NULL");
+    Plan pl;
+    qx_status st = plan_pool2(&pl, kind, N, C, H, W);
+    if (!st) *out = pl.info;
+    return st;
+}
+
 qx_status qx_plan_attn(qx_plan_info* out, qx_attn_dtype dt, int64_t L, int64_t d, int32_t bound, int32_t route) {
     g_err.clear();
     if (!out) return fail(QX_ERR_INVALID_ARG, "out is NULL");
@@ -1305,6 +1389,26 @@ qx_status qx_exec_create_conv2d_t(qx_exec* out, qx_attn_dtype dt, int64_t N, int
     *out = nullptr;
     Plan pl;
     qx_status st = plan_conv_t(&pl, dt, N, C_in, H, W, C_out, KH, KW, stride, pad, route);
+    if (st) return st;
+    return make_exec(std::move(pl), out);
+}
+
+qx_status qx_exec_create_minmax(qx_exec* out, int64_t n, int32_t elem_bytes) {
+    g_err.clear();
+    if (!out) return fail(QX_ERR_INVALID_ARG, "out is NULL");
+    *out = nullptr;
+    Plan pl;
+    qx_status st = plan_minmax(&pl, n, elem_bytes);
+    if (st) return st;
+    return make_exec(std::move(pl), out);
+}
+
+qx_status qx_exec_create_pool2x2(qx_exec* out, int32_t kind, int64_t N, int64_t C, int64_t H, int64_t W) {
+    g_err.clear();
+    if (!out) return fail(QX_ERR_INVALID_ARG, "out is NULL");
+    *out = nullptr;
+    Plan pl;
+    qx_status st = plan_pool2(&pl, kind, N, C, H, W);
     if (st) return st;
     return make_exec(std::move(pl), out);
 }
@@ -1436,6 +1540,29 @@ qx_status conv2d_gemm_t(qx_attn_dtype dt, const void* x, const void* w, void* y,
     return oneshot(key,
                    [&](Plan* pl) { return plan_conv_t(pl, dt, N, C_in, H, W, C_out, KH, KW, stride, pad, R_AUTO); },
                    in, y, stream);
+}
+
+qx_status minmax(const void* x, int64_t n, int32_t elem_bytes, void* out, void* stream) {
+    g_err.clear();
+    Plan probe;
+    qx_status st = plan_minmax(&probe, n, elem_bytes);
+    if (st) return st;
+    if (!x || !out) return fail(QX_ERR_INVALID_ARG, "NULL pointer");
+    const void* in[1] = {x};
+    Key key{OP_MINMAX, 0, n, elem_bytes, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, (uintptr_t)stream};
+    return oneshot(key, [&](Plan* pl) { return plan_minmax(pl, n, elem_bytes); }, in, out, stream);
+}
+
+qx_status pool2x2(int32_t kind, const void* x, void* y, int64_t N, int64_t C, int64_t H, int64_t W, void* stream) {
+    g_err.clear();
+    Plan probe;
+    qx_status st = plan_pool2(&probe, kind, N, C, H, W);
+    if (st) return st;
+    if (probe.launches.empty()) return QX_OK;
+    if (!x || !y) return fail(QX_ERR_INVALID_ARG, "NULL pointer for a non-empty operand");
+    const void* in[1] = {x};
+    Key key{OP_POOL, 0, kind, N, C, H, W, 0, 0, 0, 0, 0, 0, 0, (uintptr_t)stream};
+    return oneshot(key, [&](Plan* pl) { return plan_pool2(pl, kind, N, C, H, W); }, in, y, stream);
 }
 
 qx_status attn_core(qx_attn_dtype dt, const void* Q, const void* K, const void* V, void* O, int64_t L, int64_t d,

@@ -1,0 +1,192 @@
+// k_reduce.hip -- the HBM-bound operators of the operator table (Table 2):
+// min/max over an INT32 or INT16 array, and 2x2 / stride 2 pooling of NCHW
+// tensors (INT32 average, FP32 maximum).  One pass over the input with
+// 16-byte loads; their roofline is HBM bandwidth.
+#include <algorithm>
+
+#include "qx_internal.h"
+
+namespace qx {
+
+typedef int i4v __attribute__((ext_vector_type(4)));
+typedef short s8m __attribute__((ext_vector_type(8)));
+typedef float f4m __attribute__((ext_vector_type(4)));
+
+constexpr int RT = 256;   // threads per workgroup
+
+// ---------------------------------------------------------------------------
+// min/max: pass 1 -- workgroup b reduces elements [b*per, min((b+1)*per, n))
+// (per is a multiple of 64 elements) and writes its pair to part[2b .. 2b+1];
+// pass 2 -- one workgroup reduces the pairs into out[0] = min, out[1] = max.
+// ---------------------------------------------------------------------------
+template <class T>
+__device__ __forceinline__ void minmax_vec(const T* src, int32_t& lo, int32_t& hi) {
+    if (sizeof(T) == 4) {
+        const i4v v = *(const i4v*)src;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            lo = min(lo, (int32_t)v[e]);
+            hi = max(hi, (int32_t)v[e]);
+        }
+    } else {
+        const s8m v = *(const s8m*)src;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+            lo = min(lo, (int32_t)v[e]);
+            hi = max(hi, (int32_t)v[e]);
+        }
+    }
+}
+
+__device__ __forceinline__ void block_minmax(int32_t& lo, int32_t& hi) {
+    __shared__ int32_t red[2][RT / 64];
+    for (int off = 32; off > 0; off >>= 1) {
+        lo = min(lo, __shfl_xor(lo, off, 64));
+        hi = max(hi, __shfl_xor(hi, off, 64));
+    }
+    const int wave = threadIdx.x >> 6;
+    if ((threadIdx.x & 63) == 0) {
+        red[0][wave] = lo;
+        red[1][wave] = hi;
+    }
+    __syncthreads();
+    lo = red[0][0];
+    hi = red[1][0];
+#pragma unroll
+    for (int w = 1; w < RT / 64; ++w) {
+        lo = min(lo, red[0][w]);
+        hi = max(hi, red[1][w]);
+    }
+}
+
+template <class T>
+__global__ __launch_bounds__(RT) void k_minmax_partial(const MinMaxParams p) {
+    constexpr int V = 16 / sizeof(T);
+    const T* x = (const T*)p.x;
+    const int64_t start = (int64_t)blockIdx.x * p.per;
+    const int64_t end = min(start + p.per, p.n);
+    int32_t lo = INT32_MAX, hi = INT32_MIN;
+    const int64_t vend = start + (end - start) / (RT * V) * (RT * V);
+    // whole rounds of 256 vectors, four in flight per thread
+    int64_t i = start + threadIdx.x * V;
+    for (; i + 3 * RT * V < vend; i += 4 * RT * V) {
+        minmax_vec<T>(x + i, lo, hi);
+        minmax_vec<T>(x + i + RT * V, lo, hi);
+        minmax_vec<T>(x + i + 2 * RT * V, lo, hi);
+        minmax_vec<T>(x + i + 3 * RT * V, lo, hi);
+    }
+    for (; i < vend; i += RT * V) minmax_vec<T>(x + i, lo, hi);
+    for (int64_t j = vend + threadIdx.x; j < end; j += RT) {
+        lo = min(lo, (int32_t)x[j]);
+        hi = max(hi, (int32_t)x[j]);
+    }
+    block_minmax(lo, hi);
+    if (threadIdx.x == 0) {
+        p.part[2 * blockIdx.x] = lo;
+        p.part[2 * blockIdx.x + 1] = hi;
+    }
+}
+
+__global__ __launch_bounds__(RT) void k_minmax_final(const MinMaxParams p) {
+    int32_t lo = INT32_MAX, hi = INT32_MIN;
+    for (int b = threadIdx.x; b < p.blocks; b += RT) {
+        lo = min(lo, p.part[2 * b]);
+        hi = max(hi, p.part[2 * b + 1]);
+    }
+    block_minmax(lo, hi);
+    if (threadIdx.x == 0) {
+        if (p.elem_bytes == 4) {
+            ((int32_t*)p.out)[0] = lo;
+            ((int32_t*)p.out)[1] = hi;
+        } else {
+            ((int16_t*)p.out)[0] = (int16_t)lo;
+            ((int16_t*)p.out)[1] = (int16_t)hi;
+        }
+    }
+}
+
+// ---------------------------------------------------------------------------
+// 2x2 / stride 2 pooling, no padding (a trailing odd row or column is
+// dropped).  A thread makes four consecutive outputs of one output row from
+// two 8-element input row segments.  INT32 average: floor of the exact sum
+// of the four values over 4 (the int64 sum shifted right by 2).  FP32
+// maximum: the first window value, replaced by each later one that compares
+// greater (row-major window order).
+// ---------------------------------------------------------------------------
+template <bool AVG>
+__device__ __forceinline__ uint32_t pool4(const uint32_t* a, const uint32_t* b) {
+    if (AVG) {
+        const int64_t s = (int64_t)(int32_t)a[0] + (int32_t)a[1] + (int32_t)b[0] + (int32_t)b[1];
+        return (uint32_t)(int32_t)(s >> 2);
+    }
+    float m = __uint_as_float(a[0]);
+    const float c1 = __uint_as_float(a[1]), c2 = __uint_as_float(b[0]), c3 = __uint_as_float(b[1]);
+    if (c1 > m) m = c1;
+    if (c2 > m) m = c2;
+    if (c3 > m) m = c3;
+    return __float_as_uint(m);
+}
+
+template <bool AVG>
+__global__ __launch_bounds__(RT) void k_pool2(const PoolParams p) {
+    const int wq = (p.Wo + 3) / 4;
+    const int64_t t = (int64_t)blockIdx.x * RT + threadIdx.x;
+    if (t >= p.NC * p.Ho * wq) return;
+    const int q = (int)(t % wq);
+    const int64_t r = t / wq;            // (nc, oh)
+    const int oh = (int)(r % p.Ho);
+    const int64_t nc = r / p.Ho;
+    const int ow0 = q * 4;
+    const uint32_t* row0 = (const uint32_t*)p.x + (nc * p.H + 2 * oh) * p.W + 2 * ow0;
+    const uint32_t* row1 = row0 + p.W;
+    uint32_t* out = (uint32_t*)p.y + (nc * p.Ho + oh) * p.Wo + ow0;
+    if (p.vec && ow0 + 4 <= p.Wo) {
+        const i4v a0 = *(const i4v*)row0, a1 = *(const i4v*)(row0 + 4);
+        const i4v b0 = *(const i4v*)row1, b1 = *(const i4v*)(row1 + 4);
+        const uint32_t a[8] = {(uint32_t)a0[0], (uint32_t)a0[1], (uint32_t)a0[2], (uint32_t)a0[3],
+                               (uint32_t)a1[0], (uint32_t)a1[1], (uint32_t)a1[2], (uint32_t)a1[3]};
+        const uint32_t b[8] = {(uint32_t)b0[0], (uint32_t)b0[1], (uint32_t)b0[2], (uint32_t)b0[3],
+                               (uint32_t)b1[0], (uint32_t)b1[1], (uint32_t)b1[2], (uint32_t)b1[3]};
+        i4v o;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) o[e] = (int)pool4<AVG>(a + 2 * e, b + 2 * e);
+        *(i4v*)out = o;
+    } else {
+        for (int e = 0; e < 4 && ow0 + e < p.Wo; ++e) out[e] = pool4<AVG>(row0 + 2 * e, row1 + 2 * e);
+    }
+}
+
+// ---------------------------------------------------------------------------
+// Builders
+// ---------------------------------------------------------------------------
+void minmax_blocks(int64_t n, int32_t* blocks, int64_t* per) {
+    const int64_t want = std::min<int64_t>(std::max<int64_t>((n + 65535) / 65536, 1), 2048);
+    int64_t pe = (n + want - 1) / want;
+    pe = (pe + 63) / 64 * 64;   // whole 16-byte vectors at every workgroup start
+    *per = pe;
+    *blocks = (int32_t)((n + pe - 1) / pe);
+}
+
+void build_minmax(const MinMaxParams& p, LaunchRec* partial, LaunchRec* final_rec) {
+    partial->fn = p.elem_bytes == 4 ? (const void*)k_minmax_partial<int32_t> : (const void*)k_minmax_partial<int16_t>;
+    partial->grid = dim3((unsigned)p.blocks, 1, 1);
+    partial->block = dim3(RT, 1, 1);
+    partial->name = p.elem_bytes == 4 ? "minmax_i32" : "minmax_i16";
+    partial->set_params(p);
+    final_rec->fn = (const void*)k_minmax_final;
+    final_rec->grid = dim3(1, 1, 1);
+    final_rec->block = dim3(RT, 1, 1);
+    final_rec->name = "minmax_final";
+    final_rec->set_params(p);
+}
+
+void build_pool2(int32_t kind, const PoolParams& p, LaunchRec* rec) {
+    const int64_t threads = p.NC * p.Ho * ((p.Wo + 3) / 4);
+    rec->fn = kind == POOL_AVG_I32 ? (const void*)k_pool2<true> : (const void*)k_pool2<false>;
+    rec->grid = dim3((unsigned)std::max<int64_t>((threads + RT - 1) / RT, 1), 1, 1);
+    rec->block = dim3(RT, 1, 1);
+    rec->name = kind == POOL_AVG_I32 ? "avgpool2_i32" : "maxpool2_f32";
+    rec->set_params(p);
+}
+
+}  // namespace qx

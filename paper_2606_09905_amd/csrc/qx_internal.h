@@ -158,6 +158,26 @@ struct RangeParams {
     uint32_t bit;           // value or-ed into *flag
 };
 
+// Min/max: pass 1 writes one (min, max) pair per workgroup into part.
+struct MinMaxParams {
+    const void* x;
+    int32_t* part;          // [blocks][2]
+    void* out;              // two elements of the input type
+    int64_t n, per;         // elements; elements per workgroup (multiple of 64)
+    int32_t blocks;
+    int32_t elem_bytes;     // 4 (int32) or 2 (int16)
+};
+
+// 2x2 / stride 2 pooling of NCHW 32-bit elements.
+enum PoolKind : int32_t { POOL_AVG_I32 = 0, POOL_MAX_F32 = 1 };
+struct PoolParams {
+    const void* x;
+    void* y;
+    int64_t NC;
+    int32_t H, W, Ho, Wo;
+    int32_t vec;            // W % 8 == 0: 16-byte loads and stores
+};
+
 struct FillParams {
     void* ptr;
     int64_t n32;            // number of 32-bit words
@@ -250,6 +270,10 @@ bool build_attn_i32(const AttnParams& p, LaunchRec* rec);
 void build_reduce(const ReduceParams& p, LaunchRec* rec);
 void build_fill(const FillParams& p, LaunchRec* rec);
 void build_range(const RangeParams& p, LaunchRec* rec);
+// Min/max reduction (two launches) and 2x2 pooling.
+void minmax_blocks(int64_t n, int32_t* blocks, int64_t* per);
+void build_minmax(const MinMaxParams& p, LaunchRec* partial, LaunchRec* final_rec);
+void build_pool2(int32_t kind, const PoolParams& p, LaunchRec* rec);
 // fp16-exact route for large problems: encoders + direct-to-LDS NT GEMM.
 void nt_tile_shape(int64_t M, int64_t N, int64_t batch, int* bm, int* bn);
 void build_gemm_nt(const GemmParams& p, int batch, LaunchRec* rec);

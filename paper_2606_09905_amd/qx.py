@@ -20,6 +20,8 @@ STATUS_NAMES = ["OK", "INVALID_ARG", "UNSUPPORTED", "RANGE", "OUT_OF_MEMORY", "D
 
 # qx_attn_dtype
 DT_F32, DT_I32 = 0, 1
+# qx_pool_kind
+POOL_AVG_I32, POOL_MAX_F32 = 0, 1
 
 # qx_route
 ROUTE = {
@@ -84,6 +86,12 @@ def lib() -> ctypes.CDLL:
             "qx_plan_conv2d": [_p] + [_i64] * 9 + [_i32, _i32, _i32],
             "qx_plan_conv2d_t": [_p, _i32] + [_i64] * 9 + [_i32],
             "qx_plan_attn": [_p, _i32, _i64, _i64, _i32, _i32],
+            "minmax": [_p, _i64, _i32, _p, _p],
+            "pool2x2": [_i32, _p, _p, _i64, _i64, _i64, _i64, _p],
+            "qx_exec_create_minmax": [_p, _i64, _i32],
+            "qx_exec_create_pool2x2": [_p, _i32, _i64, _i64, _i64, _i64],
+            "qx_plan_minmax": [_p, _i64, _i32],
+            "qx_plan_pool2x2": [_p, _i32, _i64, _i64, _i64, _i64],
         }
         for name, args in sig.items():
             fn = getattr(L, name)
@@ -243,6 +251,35 @@ def attn_core(Q, K, V, bound: int = 0, out=None, stream=None):
     return out
 
 
+def minmax(x, out=None, stream=None):
+    """(min, max) of a non-empty int32 or int16 tensor, as a 2-element tensor."""
+    torch = _torch()
+    if x.dtype not in (torch.int32, torch.int16):
+        raise TypeError("x must be int32 or int16")
+    if out is None:
+        out = torch.empty(2, dtype=x.dtype, device=x.device)
+    check(lib().minmax(_dev_tensor(x, x.dtype, "x"), x.numel(), x.element_size(),
+                       _dev_tensor(out, x.dtype, "out"), _stream(stream)))
+    return out
+
+
+def pool2x2(x, out=None, stream=None):
+    """2x2 / stride 2 pooling of an NCHW tensor: int32 -> floor average, float32 -> maximum."""
+    torch = _torch()
+    if x.dtype == torch.int32:
+        kind = POOL_AVG_I32
+    elif x.dtype == torch.float32:
+        kind = POOL_MAX_F32
+    else:
+        raise TypeError("x must be int32 (average) or float32 (maximum)")
+    N, C, H, W = x.shape
+    if out is None:
+        out = torch.empty((N, C, H // 2, W // 2), dtype=x.dtype, device=x.device)
+    check(lib().pool2x2(kind, _dev_tensor(x, x.dtype, "x"), _dev_tensor(out, x.dtype, "y"),
+                        N, C, H, W, _stream(stream)))
+    return out
+
+
 # ---------------------------------------------------------------------------
 # planner queries (host only)
 # ---------------------------------------------------------------------------
@@ -273,6 +310,19 @@ def plan_conv2d_t(dtype: str, N, Ci, H, W, Co, KH, KW, stride=1, pad=0, route="a
     info = PlanInfo()
     check(lib().qx_plan_conv2d_t(ctypes.byref(info), DT_F32 if dtype == "f32" else DT_I32, N, Ci, H, W,
                                  Co, KH, KW, stride, pad, _route(route)))
+    return info.as_dict()
+
+
+def plan_minmax(n, elem_bytes) -> dict:
+    info = PlanInfo()
+    check(lib().qx_plan_minmax(ctypes.byref(info), n, elem_bytes))
+    return info.as_dict()
+
+
+def plan_pool2x2(kind: str, N, C, H, W) -> dict:
+    info = PlanInfo()
+    check(lib().qx_plan_pool2x2(ctypes.byref(info), POOL_AVG_I32 if kind == "avg_i32" else POOL_MAX_F32,
+                                N, C, H, W))
     return info.as_dict()
 
 
@@ -328,6 +378,23 @@ class Executor:
                                             _route(route)))
         Ho, Wo = conv_out_hw(H, W, KH, KW, stride, pad)
         return cls(h, (N, Co, Ho, Wo), torch.float32 if dtype == "f32" else torch.int32, 2)
+
+    @classmethod
+    def minmax(cls, n, dtype: str):
+        """dtype "i32" or "i16"; the output is 2 elements (min, max)."""
+        torch = _torch()
+        h = ctypes.c_void_p()
+        check(lib().qx_exec_create_minmax(ctypes.byref(h), n, 4 if dtype == "i32" else 2))
+        return cls(h, (2,), torch.int32 if dtype == "i32" else torch.int16, 1)
+
+    @classmethod
+    def pool2x2(cls, kind: str, N, C, H, W):
+        """kind "avg_i32" or "max_f32"."""
+        torch = _torch()
+        h = ctypes.c_void_p()
+        k = POOL_AVG_I32 if kind == "avg_i32" else POOL_MAX_F32
+        check(lib().qx_exec_create_pool2x2(ctypes.byref(h), k, N, C, H, W))
+        return cls(h, (N, C, H // 2, W // 2), torch.int32 if k == POOL_AVG_I32 else torch.float32, 1)
 
     @classmethod
     def attn(cls, dtype: str, L, d, bound=0, route="auto"):

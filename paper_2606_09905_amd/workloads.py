@@ -7,9 +7,11 @@ the workloads below are synthetic by definition: a small INT16 GEMM (values in
 [-1024, 1023]), smul24 INT32 GEMMs over the full signed 24-bit range, an INT16
 3x3 convolution, the FP32 and INT32 attention cores, the large INT16 GEMMs
 (values in [-256, 255]), and the same 3x3 convolution on FP32 and on smul24
-INT32 operands.  Integers are uniform over a closed range; FP32 attention
-inputs are N(0, 1) / sqrt(d), FP32 convolution inputs N(0, 1) with weights
-N(0, 1) / sqrt(C_in KH KW).
+INT32 operands, and the HBM-bound rows: min/max over INT32 and INT16 arrays,
+2x2 INT32 average pooling and FP32 max pooling.  Integers are uniform over a
+closed range; FP32 attention inputs are N(0, 1) / sqrt(d), FP32 convolution
+inputs N(0, 1) with weights N(0, 1) / sqrt(C_in KH KW), pooling inputs
+N(0, 1).
 """
 from __future__ import annotations
 
@@ -51,7 +53,22 @@ class Workload:
             return 2.0 * d["N"] * d["Co"] * ho * wo * d["Ci"] * d["KH"] * d["KW"]
         if self.op in ("attn_f32", "attn_i32"):
             return 4.0 * d["L"] * d["L"] * d["d"]
+        if self.op in ("minmax_i32", "minmax_i16", "avgpool_i32", "maxpool_f32"):
+            return 0.0      # measured in bytes per second (see in_bytes)
         raise ValueError(self.op)
+
+    @property
+    def in_bytes(self) -> int:
+        """Bytes of input one evaluation reads (the GiB/s metric of the
+        min/max and pooling rows)."""
+        d = self.dims
+        if self.op == "minmax_i32":
+            return 4 * d["n"]
+        if self.op == "minmax_i16":
+            return 2 * d["n"]
+        if self.op in ("avgpool_i32", "maxpool_f32"):
+            return 4 * d["N"] * d["C"] * d["H"] * d["W"]
+        return 0
 
     def generate(self):
         """Inputs as NumPy arrays, drawn in a fixed order from default_rng(seed)."""
@@ -79,6 +96,14 @@ class Workload:
             x = ints(rng, (d["N"], d["Ci"], d["H"], d["W"]), self.lo, self.hi, np.int32)
             w = ints(rng, (d["Co"], d["Ci"], d["KH"], d["KW"]), self.lo, self.hi, np.int32)
             return x, w
+        if self.op == "minmax_i32":
+            return (ints(rng, (d["n"],), self.lo, self.hi, np.int32),)
+        if self.op == "minmax_i16":
+            return (ints(rng, (d["n"],), self.lo, self.hi, np.int16),)
+        if self.op == "avgpool_i32":
+            return (ints(rng, (d["N"], d["C"], d["H"], d["W"]), self.lo, self.hi, np.int32),)
+        if self.op == "maxpool_f32":
+            return (normal_f32(rng, (d["N"], d["C"], d["H"], d["W"]), 1.0),)
         if self.op == "attn_f32":
             s = 1.0 / np.sqrt(d["d"])
             return tuple(normal_f32(rng, (d["L"], d["d"]), s) for _ in range(3))
@@ -106,4 +131,9 @@ WORKLOADS = {w.name: w for w in [
     Workload("conv_i32_8x64x56x56_128_3x3", "conv2d_i32", 10,
              dict(N=8, Ci=64, H=56, W=56, Co=128, KH=3, KW=3, stride=1, pad=1),
              -(1 << 23), (1 << 23) - 1, 1 << 23),
+    Workload("minmax_i32_128Mi", "minmax_i32", 11, dict(n=1 << 27), -(1 << 31), (1 << 31) - 1),
+    Workload("minmax_i16_256Mi", "minmax_i16", 12, dict(n=1 << 28), -32768, 32767),
+    Workload("avgpool_i32_16x64x224x224", "avgpool_i32", 13, dict(N=16, C=64, H=224, W=224),
+             -(1 << 31), (1 << 31) - 1),
+    Workload("maxpool_f32_16x64x224x224", "maxpool_f32", 14, dict(N=16, C=64, H=224, W=224)),
 ]}

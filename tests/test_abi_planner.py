@@ -98,6 +98,21 @@ def test_conv_f32_i32_plans():
     assert qx.plan_conv2d_t("i32", 1, 0, 5, 5, 3, 3, 3, 1, 1)["kernels"] == 1
 
 
+def test_minmax_pool_plans():
+    p = qx.plan_minmax(1 << 27, 4)
+    assert p["kernels"] == 2 and p["workspace_bytes"] == 8 * 2048
+    assert qx.plan_minmax(1, 2)["kernels"] == 2
+    for bad in ((0, 4), (10, 3), (-1, 2)):
+        with pytest.raises(qx.QxError) as e:
+            qx.plan_minmax(*bad)
+        assert e.value.status == qx.ERR_INVALID_ARG
+    assert qx.plan_pool2x2("avg_i32", 16, 64, 224, 224)["kernels"] == 1
+    assert qx.plan_pool2x2("max_f32", 1, 1, 3, 3)["kernels"] == 1
+    assert qx.plan_pool2x2("max_f32", 1, 1, 1, 3)["kernels"] == 0
+    with pytest.raises(qx.QxError):
+        qx.plan_pool2x2("avg_i32", -1, 1, 4, 4)
+
+
 @pytest.mark.parametrize("b,route", [
     (1, "i8_direct"), (127, "i8_direct"), (128, "f16_exact"), (256, "f16_exact"),
     (1024, "f16_exact"), (2048, "i8_karatsuba"), (8127, "i8_karatsuba"),

@@ -581,6 +581,65 @@ def test_workload_conv_t_full_oracle():
     same(y, orc.conv2d_s24(x, w, d["stride"], d["pad"]))
 
 
+# ---------------------------------------------------------------------------
+# Min/max and 2x2 pooling (Table 2 rows)
+# ---------------------------------------------------------------------------
+@pytest.mark.parametrize("n", [1, 5, 63, 64, 1000, 65537, 3 * (1 << 20) + 7])
+def test_minmax(n):
+    rng = np.random.default_rng(n)
+    for dt, lo, hi in ((np.int32, -(1 << 31), (1 << 31) - 1), (np.int16, -32768, 32767)):
+        x = rng.integers(lo // 2, hi // 2, n, dtype=dt, endpoint=True)
+        # the extremes at random positions, including the very last element
+        x[rng.integers(0, n)] = lo
+        x[-1] = hi
+        got = host(qx.minmax(dev(x)))
+        same(got, orc.minmax(x), f"{dt.__name__} n={n}")
+
+
+@pytest.mark.parametrize("shape", [(1, 1, 2, 2), (2, 3, 6, 8), (1, 2, 7, 9), (3, 1, 5, 4), (2, 4, 16, 40),
+                                   (1, 8, 33, 64), (4, 3, 224, 224)])
+def test_pools(shape):
+    rng = np.random.default_rng(sum(shape))
+    x = rng.integers(-(1 << 31), (1 << 31) - 1, shape, dtype=np.int32, endpoint=True)
+    same(host(qx.pool2x2(dev(x))), orc.avgpool2_i32(x), f"avg {shape}")
+    xf = rng.standard_normal(shape).astype(np.float32)
+    xf.reshape(-1)[::7] = -0.0          # signed zeros and ties take the oracle's order
+    same(host(qx.pool2x2(dev(xf))).view(np.uint32), orc.maxpool2_f32(xf).view(np.uint32), f"max {shape}")
+
+
+def test_minmax_pool_executors_and_errors():
+    with pytest.raises(qx.QxError) as e:
+        qx.plan_minmax(0, 4)
+    assert e.value.status == qx.ERR_INVALID_ARG
+    x = np.arange(-50, 50, dtype=np.int32)
+    with qx.Executor.minmax(100, "i32") as ex:
+        assert ex.plan()["kernels"] == 2
+        same(run_exec(ex, (x,)), np.array([-50, 49], np.int32))
+        same(run_exec(ex, (x[::-1].copy(),)), np.array([-50, 49], np.int32))
+    with qx.Executor.pool2x2("max_f32", 1, 1, 4, 8) as ex:
+        xf = np.arange(32, dtype=np.float32).reshape(1, 1, 4, 8)
+        same(run_exec(ex, (xf,)), orc.maxpool2_f32(xf))
+    # H or W below 2: empty output, nothing launched
+    assert qx.plan_pool2x2("avg_i32", 2, 3, 1, 8)["kernels"] == 0
+
+
+@pytest.mark.parametrize("name", ["minmax_i32_128Mi", "minmax_i16_256Mi", "avgpool_i32_16x64x224x224",
+                                  "maxpool_f32_16x64x224x224"])
+def test_workload_hbm_rows_full_oracle(name):
+    w = WORKLOADS[name]
+    (x,) = w.generate()
+    d = w.dims
+    if w.op.startswith("minmax"):
+        with qx.Executor.minmax(d["n"], w.op[-3:]) as ex:
+            same(run_exec(ex, (x,)), orc.minmax(x))
+        return
+    kind = "avg_i32" if w.op == "avgpool_i32" else "max_f32"
+    with qx.Executor.pool2x2(kind, d["N"], d["C"], d["H"], d["W"]) as ex:
+        y = run_exec(ex, (x,))
+    ref = orc.avgpool2_i32(x) if kind == "avg_i32" else orc.maxpool2_f32(x)
+    same(y.view(np.uint32), ref.view(np.uint32))
+
+
 def test_workload_attn_full_oracle():
     wf = WORKLOADS["attn_f32_4096x64"]
     Q, K, V = wf.generate()
