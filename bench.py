@@ -108,6 +108,8 @@ def make_executor(w, qx):
     if w.op in ("conv2d_f32", "conv2d_i32"):
         return qx.Executor.conv2d_t("f32" if w.op == "conv2d_f32" else "i32", d["N"], d["Ci"], d["H"], d["W"],
                                     d["Co"], d["KH"], d["KW"], d["stride"], d["pad"])
+    if w.op == "lenet_i32":
+        return qx.Executor.lenet_i32(d["B"])
     if w.op in ("minmax_i32", "minmax_i16"):
         return qx.Executor.minmax(d["n"], w.op[-3:])
     if w.op in ("avgpool_i32", "maxpool_f32"):

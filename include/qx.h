@@ -201,11 +201,21 @@ qx_status qx_exec_create_conv2d_t(qx_exec* out, qx_attn_dtype dt, int64_t N, int
 qx_status qx_exec_create_attn(qx_exec* out, qx_attn_dtype dt, int64_t L, int64_t d,
                               int32_t bound, int32_t route);
 qx_status qx_exec_create_minmax(qx_exec* out, int64_t n, int32_t elem_bytes);
+/* LeNet-5-shaped INT32 pipeline (Results: end-to-end CNN), every layer one
+ * of this library's operators chained through the workspace on one stream:
+ *   x [B][1][32][32] -> conv 6@5x5 -> ReLU -> 2x2 avg -> conv 16@5x5 -> ReLU
+ *   -> 2x2 avg -> [B][400] -> FC 120 -> ReLU -> FC 84 -> ReLU -> FC 10.
+ * Convolutions and FC layers are INT32 under the smul24 contract (operand
+ * words read as sext24 of their low 24 bits, results mod 2^32); pools are
+ * the INT32 floor average; ReLU is max(x, 0).  inputs = {x, w1 [6][1][5][5],
+ * w2 [16][6][5][5], f1 [400][120], f2 [120][84], f3 [84][10]} (FC weights
+ * [in][out]); output [B][10] int32.  0 <= batch <= 2^20. */
+qx_status qx_exec_create_lenet_i32(qx_exec* out, int64_t batch);
 qx_status qx_exec_create_pool2x2(qx_exec* out, int32_t kind, int64_t N, int64_t C, int64_t H, int64_t W);
 
 /* Enqueue one evaluation: inputs = {A, B} (GEMMs), {x, w} (convolutions), {x}
- * (min/max, pooling) or
- * {Q, K, V} (attention), device pointers with the shapes given at create.
+ * (min/max, pooling), {Q, K, V} (attention) or {x, w1, w2, f1, f2, f3}
+ * (LeNet pipeline), device pointers with the shapes given at create.
  * Allocates nothing.  Calls on one handle must not overlap in time. */
 qx_status qx_exec_run(qx_exec h, const void* const* inputs, void* output, void* stream);
 
@@ -239,6 +249,7 @@ qx_status qx_plan_conv2d_t(qx_plan_info* out, qx_attn_dtype dt, int64_t N, int64
 qx_status qx_plan_attn(qx_plan_info* out, qx_attn_dtype dt, int64_t L, int64_t d,
                        int32_t bound, int32_t route);
 qx_status qx_plan_minmax(qx_plan_info* out, int64_t n, int32_t elem_bytes);
+qx_status qx_plan_lenet_i32(qx_plan_info* out, int64_t batch);
 qx_status qx_plan_pool2x2(qx_plan_info* out, int32_t kind, int64_t N, int64_t C, int64_t H, int64_t W);
 
 /* Message of the last failing call on this thread ("" if none).  Valid

@@ -201,3 +201,19 @@ def avgpool2_i32(x):
 def maxpool2_f32(x):
     """2x2 / stride 2 maximum of float32 NCHW (Table 2, MaxPool row)."""
     return _pool(_load().oracle_maxpool2_f32, x, np.float32)
+
+
+def lenet_i32(x, w1, w2, f1, f2, f3):
+    """LeNet-5-shaped INT32 pipeline (Results: end-to-end CNN), composed of
+    the functions above: conv (smul24) -> ReLU -> 2x2 floor average -> conv
+    -> ReLU -> 2x2 average -> FC -> ReLU -> FC -> ReLU -> FC, every layer
+    int32 mod 2^32 with its operands read under the smul24 contract.
+    x [B][1][32][32]; FC weights [in][out]; returns [B][10] int32."""
+    B = x.shape[0]
+    a = conv2d_s24(x, w1, 1, 0)
+    a = avgpool2_i32(np.maximum(a, 0))
+    a = conv2d_s24(a, w2, 1, 0)
+    a = avgpool2_i32(np.maximum(a, 0)).reshape(1, B, 400)
+    h = np.maximum(gemm_i32_s24(a, np.asarray(f1, np.int32)[None]), 0)
+    h = np.maximum(gemm_i32_s24(h, np.asarray(f2, np.int32)[None]), 0)
+    return gemm_i32_s24(h, np.asarray(f3, np.int32)[None])[0]

@@ -52,7 +52,7 @@ constexpr uint32_t kMagic = 0x71786578u;  // "qxex"
 
 enum OpKind : int32_t {
     OP_GEMM_I16 = 1, OP_GEMM_S24 = 2, OP_CONV = 3, OP_ATTN_F32 = 4, OP_ATTN_I32 = 5, OP_CONV_F32 = 6, OP_CONV_I32 = 7,
-    OP_MINMAX = 8, OP_POOL = 9
+    OP_MINMAX = 8, OP_POOL = 9, OP_LENET = 10
 };
 
 // A fully planned operation: route facts plus launch records with unbound
@@ -762,6 +762,36 @@ qx_status plan_conv_t(Plan* pl, qx_attn_dtype dt, int64_t N, int64_t Ci, int64_t
     // ones: explicit lowering col [Kd][P] int32, then the smul24 GEMM.
     if (route < 0 || route > R_F32_VALU) return fail(QX_ERR_INVALID_ARG, "unknown route %d", route);
     const bool gather = (route == R_AUTO || route == R_S24_I8LIMB) && use_i8nt(R_S24_I8LIMB, Co, P, Kd, 1);
+    // few output channels: a direct vector-ALU kernel (a GEMM tile would be
+    // mostly empty)
+    const bool direct = Co <= 16 && Kd <= 1024 && KW <= 8 && (route == R_S24_VALU || (route == R_AUTO && !gather));
+    if (direct) {
+        info.route = R_S24_VALU;
+        info.products = 1;
+        info.chunk = 0;
+        info.exact_no_wrap = 0;
+        info.workspace_bytes = 0;
+        if (N == 0 || Co == 0) {
+            info.kernels = 0;
+            return QX_OK;
+        }
+        if (Ci == 0) {
+            add_fill_out(pl, N * Co * Ho * Wo);
+            info.kernels = 1;
+            return QX_OK;
+        }
+        ConvDirectParams cd{};
+        cd.P = P; cd.Co = (int32_t)Co; cd.Kd = (int32_t)Kd; cd.g = geo;
+        LaunchRec r;
+        build_conv_direct_s24(cd, &r);
+        r.bind(offsetof(ConvDirectParams, x), BIND_IN0);
+        r.bind(offsetof(ConvDirectParams, w), BIND_IN1);
+        r.bind(offsetof(ConvDirectParams, y), BIND_OUT);
+        pl->launches = {r};
+        info.kernels = 1;
+        info.tile_m = 1; info.tile_n = 256; info.tile_k = 1;
+        return QX_OK;
+    }
     GemmSpec s{};
     s.M = Co; s.N = P; s.K = Kd; s.batch = 1; s.s24 = true; s.route = route;
     s.a_bind = BIND_IN1; s.b_bind = gather ? BIND_IN0 : BIND_WS; s.b_ws_off = 0;
@@ -862,6 +892,114 @@ qx_status plan_pool2(Plan* pl, int32_t kind, int64_t N, int64_t C, int64_t H, in
     pl->launches = {r};
     info.kernels = 1;
     info.tile_m = 2; info.tile_n = 8; info.tile_k = 1;
+    return QX_OK;
+}
+
+// Where a sub-plan's input or output binding goes when plans are chained.
+struct Target {
+    Bind bind;
+    uint64_t add;
+};
+
+// Appends the launches of sub-plan sp to pl: its workspace moves to
+// [base, base + its size) of pl's workspace, its inputs and output are
+// rebound to the given targets.
+void append_plan(Plan* pl, const Plan& sp, uint64_t base, std::initializer_list<Target> ins, Target out) {
+    const Target* in = ins.begin();
+    for (const LaunchRec& r0 : sp.launches) {
+        LaunchRec r = r0;
+        for (int i = 0; i < r.nslots; ++i) {
+            Slot& sl = r.slots[i];
+            if (sl.bind == BIND_WS) {
+                sl.add += base;
+            } else if (sl.bind == BIND_OUT) {
+                sl.bind = out.bind;
+                sl.add += out.add;
+            } else {
+                sl.add += in[sl.bind].add;
+                sl.bind = in[sl.bind].bind;
+            }
+        }
+        pl->launches.push_back(r);
+    }
+}
+
+// LeNet-5-shaped INT32 pipeline (Results: end-to-end CNN on the substrate),
+// every layer an executor-planned operator of this library, chained on one
+// stream through the workspace:
+//   x [B][1][32][32] -> conv 6@5x5 -> ReLU -> 2x2 avg -> conv 16@5x5 -> ReLU
+//   -> 2x2 avg -> [B][400] -> FC 120 -> ReLU -> FC 84 -> ReLU -> FC 10.
+// Convolutions and FC layers are INT32 under the smul24 contract (each
+// operand word read as sext24, results mod 2^32); the pools are the INT32
+// floor average of the ReLU'd values.  Inputs: x, w1 [6][1][5][5],
+// w2 [16][6][5][5], f1 [400][120], f2 [120][84], f3 [84][10]; output [B][10].
+qx_status plan_lenet(Plan* pl, int64_t B) {
+    qx_status st = check_dims({{"batch", B}});
+    if (st) return st;
+    if (B > (1 << 20)) return fail(QX_ERR_UNSUPPORTED, "batch = %lld exceeds 2^20", (long long)B);
+    pl->op = OP_LENET;
+    pl->n_inputs = 6;
+    pl->in_align = 16;
+    qx_plan_info& info = pl->info;
+    info.route = R_S24_I8LIMB;
+    info.products = products_of(R_S24_I8LIMB);
+    info.exact_no_wrap = 0;
+    if (B == 0) {
+        info.kernels = 0;
+        info.workspace_bytes = 0;
+        return QX_OK;
+    }
+    uint64_t off = 0;
+    auto take = [&](uint64_t bytes) {
+        const uint64_t o = round_up(off, 256);
+        off = o + bytes;
+        return o;
+    };
+    const uint64_t o_a1 = take(4 * (uint64_t)B * 6 * 28 * 28), o_p1 = take(4 * (uint64_t)B * 6 * 14 * 14);
+    const uint64_t o_a2 = take(4 * (uint64_t)B * 16 * 10 * 10), o_p2 = take(4 * (uint64_t)B * 400);
+    const uint64_t o_h1 = take(4 * (uint64_t)B * 120), o_h2 = take(4 * (uint64_t)B * 84);
+    auto sub = [&](Plan& sp, std::initializer_list<Target> ins, Target out) -> qx_status {
+        if (sp.n_events) return fail(QX_ERR_UNSUPPORTED, "chained plans must use one stream");
+        append_plan(pl, sp, take((uint64_t)sp.info.workspace_bytes), ins, out);
+        return QX_OK;
+    };
+    auto pool = [&](uint64_t from, uint64_t to, int64_t C, int32_t H) {
+        PoolParams pp{};
+        pp.NC = B * C; pp.H = H; pp.W = H; pp.Ho = H / 2; pp.Wo = H / 2;
+        pp.vec = H % 8 == 0 ? 1 : 0;
+        pp.relu = 1;
+        LaunchRec r;
+        build_pool2(POOL_AVG_I32, pp, &r);
+        r.bind(offsetof(PoolParams, x), BIND_WS, from);
+        r.bind(offsetof(PoolParams, y), BIND_WS, to);
+        pl->launches.push_back(r);
+    };
+    auto relu = [&](uint64_t at, int64_t n) {
+        ReluParams rp{};
+        rp.n = n;
+        LaunchRec r;
+        build_relu(rp, &r);
+        r.bind(offsetof(ReluParams, p), BIND_WS, at);
+        pl->launches.push_back(r);
+    };
+    Plan c1, c2, g1, g2, g3;
+    if ((st = plan_conv_t(&c1, QX_DT_I32, B, 1, 32, 32, 6, 5, 5, 1, 0, R_AUTO))) return st;
+    if ((st = sub(c1, {{BIND_IN0, 0}, {BIND_IN1, 0}}, {BIND_WS, o_a1}))) return st;
+    pool(o_a1, o_p1, 6, 28);
+    if ((st = plan_conv_t(&c2, QX_DT_I32, B, 6, 14, 14, 16, 5, 5, 1, 0, R_AUTO))) return st;
+    if ((st = sub(c2, {{BIND_WS, o_p1}, {BIND_IN2, 0}}, {BIND_WS, o_a2}))) return st;
+    pool(o_a2, o_p2, 16, 10);
+    if ((st = plan_gemm(&g1, true, B, 120, 400, 1, 0, 0, R_AUTO))) return st;
+    if ((st = sub(g1, {{BIND_WS, o_p2}, {BIND_IN3, 0}}, {BIND_WS, o_h1}))) return st;
+    relu(o_h1, B * 120);
+    if ((st = plan_gemm(&g2, true, B, 84, 120, 1, 0, 0, R_AUTO))) return st;
+    if ((st = sub(g2, {{BIND_WS, o_h1}, {BIND_IN4, 0}}, {BIND_WS, o_h2}))) return st;
+    relu(o_h2, B * 84);
+    if ((st = plan_gemm(&g3, true, B, 10, 84, 1, 0, 0, R_AUTO))) return st;
+    if ((st = sub(g3, {{BIND_WS, o_h2}, {BIND_IN5, 0}}, {BIND_OUT, 0}))) return st;
+    info.kernels = (int32_t)pl->launches.size();
+    info.workspace_bytes = (int64_t)round_up(off, 256);
+    info.tile_m = info.tile_n = info.tile_k = 0;
     return QX_OK;
 }
 
@@ -1132,7 +1270,7 @@ qx_status run_exec(qx_exec h, const void* const* inputs, void* output, void* str
     unsigned used = 0;
     for (const LaunchRec& r : pl.launches)
         for (int i = 0; i < r.nslots; ++i)
-            if (r.slots[i].bind <= BIND_IN2) used |= 1u << r.slots[i].bind;
+            if (r.slots[i].bind < BIND_OUT) used |= 1u << r.slots[i].bind;
     if (used && !inputs) return fail(QX_ERR_INVALID_ARG, "inputs is NULL");
     for (int i = 0; i < pl.n_inputs; ++i) {
         if (!(used & (1u << i))) continue;
@@ -1167,13 +1305,9 @@ qx_status run_exec(qx_exec h, const void* const* inputs, void* output, void* str
         for (int i = 0; i < r.nslots; ++i) {
             const Slot& sl = r.slots[i];
             const char* ptr = nullptr;
-            switch (sl.bind) {
-            case BIND_IN0: ptr = (const char*)inputs[0]; break;
-            case BIND_IN1: ptr = (const char*)inputs[1]; break;
-            case BIND_IN2: ptr = (const char*)inputs[2]; break;
-            case BIND_OUT: ptr = (const char*)output; break;
-            case BIND_WS: ptr = (const char*)h->ws; break;
-            }
+            if (sl.bind < BIND_OUT) ptr = (const char*)inputs[sl.bind];
+            else if (sl.bind == BIND_OUT) ptr = (const char*)output;
+            else ptr = (const char*)h->ws;
             ptr += sl.add;
             memcpy(r.blob + sl.off, &ptr, sizeof(void*));
         }
@@ -1340,6 +1474,15 @@ qx_status qx_plan_pool2x2(qx_plan_info* out, int32_t kind, int64_t N, int64_t C,
     return st;
 }
 
+qx_status qx_plan_lenet_i32(qx_plan_info* out, int64_t batch) {
+    g_err.clear();
+    if (!out) return fail(QX_ERR_INVALID_ARG, "out is NULL");
+    Plan pl;
+    qx_status st = plan_lenet(&pl, batch);
+    if (!st) *out = pl.info;
+    return st;
+}
+
 qx_status qx_plan_attn(qx_plan_info* out, qx_attn_dtype dt, int64_t L, int64_t d, int32_t bound, int32_t route) {
     g_err.clear();
     if (!out) return fail(QX_ERR_INVALID_ARG, "out is NULL");
@@ -1409,6 +1552,16 @@ qx_status qx_exec_create_pool2x2(qx_exec* out, int32_t kind, int64_t N, int64_t 
     *out = nullptr;
     Plan pl;
     qx_status st = plan_pool2(&pl, kind, N, C, H, W);
+    if (st) return st;
+    return make_exec(std::move(pl), out);
+}
+
+qx_status qx_exec_create_lenet_i32(qx_exec* out, int64_t batch) {
+    g_err.clear();
+    if (!out) return fail(QX_ERR_INVALID_ARG, "out is NULL");
+    *out = nullptr;
+    Plan pl;
+    qx_status st = plan_lenet(&pl, batch);
     if (st) return st;
     return make_exec(std::move(pl), out);
 }

@@ -114,10 +114,16 @@ __global__ __launch_bounds__(RT) void k_minmax_final(const MinMaxParams p) {
 // greater (row-major window order).
 // ---------------------------------------------------------------------------
 template <bool AVG>
-__device__ __forceinline__ uint32_t pool4(const uint32_t* a, const uint32_t* b) {
+__device__ __forceinline__ uint32_t pool4(const uint32_t* a, const uint32_t* b, bool relu) {
     if (AVG) {
-        const int64_t s = (int64_t)(int32_t)a[0] + (int32_t)a[1] + (int32_t)b[0] + (int32_t)b[1];
-        return (uint32_t)(int32_t)(s >> 2);
+        int64_t v0 = (int32_t)a[0], v1 = (int32_t)a[1], v2 = (int32_t)b[0], v3 = (int32_t)b[1];
+        if (relu) {
+            v0 = v0 > 0 ? v0 : 0;
+            v1 = v1 > 0 ? v1 : 0;
+            v2 = v2 > 0 ? v2 : 0;
+            v3 = v3 > 0 ? v3 : 0;
+        }
+        return (uint32_t)(int32_t)((v0 + v1 + v2 + v3) >> 2);
     }
     float m = __uint_as_float(a[0]);
     const float c1 = __uint_as_float(a[1]), c2 = __uint_as_float(b[0]), c3 = __uint_as_float(b[1]);
@@ -149,11 +155,73 @@ __global__ __launch_bounds__(RT) void k_pool2(const PoolParams p) {
                                (uint32_t)b1[0], (uint32_t)b1[1], (uint32_t)b1[2], (uint32_t)b1[3]};
         i4v o;
 #pragma unroll
-        for (int e = 0; e < 4; ++e) o[e] = (int)pool4<AVG>(a + 2 * e, b + 2 * e);
+        for (int e = 0; e < 4; ++e) o[e] = (int)pool4<AVG>(a + 2 * e, b + 2 * e, p.relu);
         *(i4v*)out = o;
     } else {
-        for (int e = 0; e < 4 && ow0 + e < p.Wo; ++e) out[e] = pool4<AVG>(row0 + 2 * e, row1 + 2 * e);
+        for (int e = 0; e < 4 && ow0 + e < p.Wo; ++e) out[e] = pool4<AVG>(row0 + 2 * e, row1 + 2 * e, p.relu);
     }
+}
+
+__global__ __launch_bounds__(RT) void k_relu_i32(const ReluParams p) {
+    const int64_t i = (int64_t)blockIdx.x * RT + threadIdx.x;
+    if (i < p.n) p.p[i] = max(p.p[i], 0);
+}
+
+// ---------------------------------------------------------------------------
+// Direct INT32 convolution under the smul24 contract for few output
+// channels, where a GEMM tile would be mostly empty: every thread owns one
+// output pixel and accumulates all C_out channels with v_mul_i32_i24 (low 32
+// bits of the product of the sign-extended low 24 bits), wrapping mod 2^32.
+// ---------------------------------------------------------------------------
+constexpr int DKW = 8;   // KW limit; C_out <= 16 and C_in*KH*KW <= 1024 (64 KB of LDS)
+
+template <int DCO>   // output channels per thread (8 or 16)
+__global__ __launch_bounds__(RT) void k_conv_direct_s24(const ConvDirectParams p) {
+    // weights [k][co], zero past C_out; sized Kd * DCO at launch so that
+    // small filters leave room for many workgroups per CU
+    extern __shared__ int32_t wsh[];
+    int32_t(*ws)[DCO] = (int32_t(*)[DCO])wsh;
+    const ConvGeom& g = p.g;
+    for (int i = threadIdx.x; i < p.Kd * DCO; i += RT) {
+        const int k = i / DCO, c = i % DCO;
+        ws[k][c] = c < p.Co ? p.w[(int64_t)c * p.Kd + k] : 0;
+    }
+    __syncthreads();
+    const int64_t pix = (int64_t)blockIdx.x * RT + threadIdx.x;
+    const int64_t pc = min(pix, p.P - 1);
+    const int hw = g.Ho * g.Wo;
+    const int n = (int)(pc / hw), rem = (int)(pc - (int64_t)n * hw);
+    const int oh = rem / g.Wo, ow = rem - oh * g.Wo;
+    const int32_t* xb = p.x + (int64_t)n * g.Ci * g.H * g.W;
+    uint32_t acc[DCO];
+#pragma unroll
+    for (int c = 0; c < DCO; ++c) acc[c] = 0u;
+    int k = 0;
+    for (int ci = 0; ci < g.Ci; ++ci)
+        for (int kh = 0; kh < g.KH; ++kh, k += g.KW) {
+            const int ih = oh * g.stride - g.pad + kh;
+            const bool rin = ih >= 0 && ih < g.H;
+            const int32_t* xr = xb + ((int64_t)ci * g.H + ih) * g.W;
+            // the KW inputs of this kernel row first (independent loads), then
+            // every output channel
+            int32_t xv[DKW];
+#pragma unroll
+            for (int kw = 0; kw < DKW; ++kw) {
+                const int iw = ow * g.stride - g.pad + kw;
+                xv[kw] = (kw < g.KW && rin && iw >= 0 && iw < g.W) ? xr[iw] : 0;
+            }
+#pragma unroll
+            for (int kw = 0; kw < DKW; ++kw) {
+                if (kw >= g.KW) break;
+                const int32_t* wk = ws[k + kw];
+#pragma unroll
+                for (int c = 0; c < DCO; ++c) acc[c] += (uint32_t)__mul24(xv[kw], wk[c]);
+            }
+        }
+    if (pix < p.P)
+#pragma unroll
+        for (int c = 0; c < DCO; ++c)
+            if (c < p.Co) p.y[((int64_t)n * p.Co + c) * hw + rem] = (int32_t)acc[c];
 }
 
 // ---------------------------------------------------------------------------
@@ -178,6 +246,24 @@ void build_minmax(const MinMaxParams& p, LaunchRec* partial, LaunchRec* final_re
     final_rec->block = dim3(RT, 1, 1);
     final_rec->name = "minmax_final";
     final_rec->set_params(p);
+}
+
+void build_conv_direct_s24(const ConvDirectParams& p, LaunchRec* rec) {
+    const int dco = p.Co <= 8 ? 8 : 16;
+    rec->fn = dco == 8 ? (const void*)k_conv_direct_s24<8> : (const void*)k_conv_direct_s24<16>;
+    rec->grid = dim3((unsigned)std::max<int64_t>((p.P + RT - 1) / RT, 1), 1, 1);
+    rec->block = dim3(RT, 1, 1);
+    rec->shmem = (uint32_t)(p.Kd * dco * sizeof(int32_t));
+    rec->name = "conv_direct_s24";
+    rec->set_params(p);
+}
+
+void build_relu(const ReluParams& p, LaunchRec* rec) {
+    rec->fn = (const void*)k_relu_i32;
+    rec->grid = dim3((unsigned)std::max<int64_t>((p.n + RT - 1) / RT, 1), 1, 1);
+    rec->block = dim3(RT, 1, 1);
+    rec->name = "relu_i32";
+    rec->set_params(p);
 }
 
 void build_pool2(int32_t kind, const PoolParams& p, LaunchRec* rec) {

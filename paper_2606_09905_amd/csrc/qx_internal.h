@@ -128,6 +128,18 @@ struct ConvPrepParams {
     ConvGeom g;
 };
 
+// Direct smul24 convolution on the vector ALU for few output channels
+// (C_out <= 16, C_in*KH*KW <= 1024, KW <= 8): a thread makes every output
+// channel of one output pixel; the weights sit in LDS.
+struct ConvDirectParams {
+    const int32_t* x;       // NCHW
+    const int32_t* w;       // OIHW
+    int32_t* y;             // NCHW
+    int64_t P;              // N*Ho*Wo
+    int32_t Co, Kd;
+    ConvGeom g;
+};
+
 // Attention core O = (Q K^T) V.
 struct AttnParams {
     const void* Q;
@@ -176,6 +188,13 @@ struct PoolParams {
     int64_t NC;
     int32_t H, W, Ho, Wo;
     int32_t vec;            // W % 8 == 0: 16-byte loads and stores
+    int32_t relu;           // average of max(x, 0) (a ReLU fused ahead of the pool)
+};
+
+// In-place ReLU of int32 values: p[i] = max(p[i], 0).
+struct ReluParams {
+    int32_t* p;
+    int64_t n;
 };
 
 struct FillParams {
@@ -206,7 +225,11 @@ struct ValuGemmParams {
 // ---------------------------------------------------------------------------
 // Cached launch records.
 // ---------------------------------------------------------------------------
-enum Bind : uint8_t { BIND_IN0 = 0, BIND_IN1 = 1, BIND_IN2 = 2, BIND_OUT = 3, BIND_WS = 4 };
+enum Bind : uint8_t {
+    BIND_IN0 = 0, BIND_IN1 = 1, BIND_IN2 = 2, BIND_IN3 = 3, BIND_IN4 = 4, BIND_IN5 = 5,
+    BIND_OUT = 6, BIND_WS = 7
+};
+constexpr int kMaxInputs = 6;
 
 struct Slot {
     uint16_t off;           // byte offset of a pointer field in the parameter blob
@@ -274,6 +297,8 @@ void build_range(const RangeParams& p, LaunchRec* rec);
 void minmax_blocks(int64_t n, int32_t* blocks, int64_t* per);
 void build_minmax(const MinMaxParams& p, LaunchRec* partial, LaunchRec* final_rec);
 void build_pool2(int32_t kind, const PoolParams& p, LaunchRec* rec);
+void build_relu(const ReluParams& p, LaunchRec* rec);
+void build_conv_direct_s24(const ConvDirectParams& p, LaunchRec* rec);
 // fp16-exact route for large problems: encoders + direct-to-LDS NT GEMM.
 void nt_tile_shape(int64_t M, int64_t N, int64_t batch, int* bm, int* bn);
 void build_gemm_nt(const GemmParams& p, int batch, LaunchRec* rec);

@@ -91,6 +91,8 @@ def lib() -> ctypes.CDLL:
             "qx_exec_create_minmax": [_p, _i64, _i32],
             "qx_exec_create_pool2x2": [_p, _i32, _i64, _i64, _i64, _i64],
             "qx_plan_minmax": [_p, _i64, _i32],
+            "qx_plan_lenet_i32": [_p, _i64],
+            "qx_exec_create_lenet_i32": [_p, _i64],
             "qx_plan_pool2x2": [_p, _i32, _i64, _i64, _i64, _i64],
         }
         for name, args in sig.items():
@@ -326,6 +328,12 @@ def plan_pool2x2(kind: str, N, C, H, W) -> dict:
     return info.as_dict()
 
 
+def plan_lenet_i32(batch) -> dict:
+    info = PlanInfo()
+    check(lib().qx_plan_lenet_i32(ctypes.byref(info), batch))
+    return info.as_dict()
+
+
 def plan_attn(dtype: str, L, d, bound=0, route="auto") -> dict:
     info = PlanInfo()
     check(lib().qx_plan_attn(ctypes.byref(info), DT_F32 if dtype == "f32" else DT_I32, L, d,
@@ -395,6 +403,14 @@ class Executor:
         k = POOL_AVG_I32 if kind == "avg_i32" else POOL_MAX_F32
         check(lib().qx_exec_create_pool2x2(ctypes.byref(h), k, N, C, H, W))
         return cls(h, (N, C, H // 2, W // 2), torch.int32 if k == POOL_AVG_I32 else torch.float32, 1)
+
+    @classmethod
+    def lenet_i32(cls, batch):
+        """inputs (x, w1, w2, f1, f2, f3) int32; output [batch][10] int32."""
+        torch = _torch()
+        h = ctypes.c_void_p()
+        check(lib().qx_exec_create_lenet_i32(ctypes.byref(h), batch))
+        return cls(h, (batch, 10), torch.int32, 6)
 
     @classmethod
     def attn(cls, dtype: str, L, d, bound=0, route="auto"):

@@ -8,7 +8,9 @@ the workloads below are synthetic by definition: a small INT16 GEMM (values in
 3x3 convolution, the FP32 and INT32 attention cores, the large INT16 GEMMs
 (values in [-256, 255]), and the same 3x3 convolution on FP32 and on smul24
 INT32 operands, and the HBM-bound rows: min/max over INT32 and INT16 arrays,
-2x2 INT32 average pooling and FP32 max pooling.  Integers are uniform over a
+2x2 INT32 average pooling and FP32 max pooling, and a LeNet-5-shaped INT32
+pipeline with synthetic weights (images in [0, 255], weights in [-3, 3]).
+Integers are uniform over a
 closed range; FP32 attention inputs are N(0, 1) / sqrt(d), FP32 convolution
 inputs N(0, 1) with weights N(0, 1) / sqrt(C_in KH KW), pooling inputs
 N(0, 1).
@@ -55,6 +57,10 @@ class Workload:
             return 4.0 * d["L"] * d["L"] * d["d"]
         if self.op in ("minmax_i32", "minmax_i16", "avgpool_i32", "maxpool_f32"):
             return 0.0      # measured in bytes per second (see in_bytes)
+        if self.op == "lenet_i32":
+            # conv 6@5x5 on 32x32, conv 16@5x5 on 14x14, FC 400-120-84-10
+            per_image = 2 * (6 * 28 * 28 * 25 + 16 * 10 * 10 * 150 + 400 * 120 + 120 * 84 + 84 * 10)
+            return float(per_image) * d["B"]
         raise ValueError(self.op)
 
     @property
@@ -96,6 +102,10 @@ class Workload:
             x = ints(rng, (d["N"], d["Ci"], d["H"], d["W"]), self.lo, self.hi, np.int32)
             w = ints(rng, (d["Co"], d["Ci"], d["KH"], d["KW"]), self.lo, self.hi, np.int32)
             return x, w
+        if self.op == "lenet_i32":
+            x = ints(rng, (d["B"], 1, 32, 32), 0, 255, np.int32)
+            shapes = ((6, 1, 5, 5), (16, 6, 5, 5), (400, 120), (120, 84), (84, 10))
+            return (x,) + tuple(ints(rng, s, self.lo, self.hi, np.int32) for s in shapes)
         if self.op == "minmax_i32":
             return (ints(rng, (d["n"],), self.lo, self.hi, np.int32),)
         if self.op == "minmax_i16":
@@ -136,4 +146,5 @@ WORKLOADS = {w.name: w for w in [
     Workload("avgpool_i32_16x64x224x224", "avgpool_i32", 13, dict(N=16, C=64, H=224, W=224),
              -(1 << 31), (1 << 31) - 1),
     Workload("maxpool_f32_16x64x224x224", "maxpool_f32", 14, dict(N=16, C=64, H=224, W=224)),
+    Workload("lenet_i32_b4096", "lenet_i32", 15, dict(B=4096), -3, 3, 3),
 ]}

@@ -67,3 +67,27 @@ def attn_exact(Q, K, V):
     v = [[Fraction(float(x)) for x in r] for r in V]
     S = [[sum(q[i][t] * k[j][t] for t in range(d)) for j in range(L)] for i in range(L)]
     return [[sum(S[i][j] * v[j][t] for j in range(L)) for t in range(d)] for i in range(L)]
+
+
+def lenet_i32(x, w1, w2, f1, f2, f3):
+    """The LeNet-5-shaped INT32 pipeline for one image, layer by layer in
+    Python integers: smul24 operand reading, wrap to int32 after every
+    layer, ReLU, floor average of 2x2 windows."""
+    s24 = lambda v: sext24(int(v))
+
+    def relu_pool(y):
+        C, H, W = len(y), len(y[0]), len(y[0][0])
+        return [[[(max(y[c][2 * i][2 * j], 0) + max(y[c][2 * i][2 * j + 1], 0) +
+                   max(y[c][2 * i + 1][2 * j], 0) + max(y[c][2 * i + 1][2 * j + 1], 0)) // 4
+                  for j in range(W // 2)] for i in range(H // 2)] for c in range(C)]
+
+    a = conv2d([x], w1, 1, 0, f=s24)[0]
+    a = relu_pool(a)
+    a = conv2d([a], w2, 1, 0, f=s24)[0]
+    a = relu_pool(a)
+    v = [a[c][i][j] for c in range(16) for i in range(5) for j in range(5)]
+    for f, last in ((f1, False), (f2, False), (f3, True)):
+        v = [wrap32(sum(s24(v[k]) * s24(f[k][n]) for k in range(len(v)))) for n in range(len(f[0]))]
+        if not last:
+            v = [max(t, 0) for t in v]
+    return v

@@ -88,14 +88,28 @@ def test_conv_f32_i32_plans():
     p = qx.plan_conv2d_t("i32", 8, 64, 56, 56, 128, 3, 3, 1, 1)
     assert p["route_name"] == "s24_i8limb" and p["kernels"] == 2
     assert p["workspace_bytes"] < 4 * 576 * 8 * 56 * 56
-    p = qx.plan_conv2d_t("i32", 1, 4, 8, 8, 4, 3, 3, 1, 1)
+    p = qx.plan_conv2d_t("i32", 1, 4, 8, 8, 40, 3, 3, 1, 1)
     assert p["route_name"] == "s24_i8limb" and p["kernels"] == 3   # im2col, sums, GEMM
+    # few output channels: one direct vector-ALU kernel
+    p = qx.plan_conv2d_t("i32", 1, 4, 8, 8, 4, 3, 3, 1, 1)
+    assert p["route_name"] == "s24_valu" and p["kernels"] == 1 and p["workspace_bytes"] == 0
+    assert qx.plan_conv2d_t("i32", 1, 4, 8, 8, 4, 3, 3, 1, 1, "s24_i8limb")["kernels"] == 3
     assert qx.plan_conv2d_t("i32", 1, 2, 5, 5, 3, 3, 3, 1, 1, "s24_valu")["route_name"] == "s24_valu"
     with pytest.raises(qx.QxError) as e:
         qx.plan_conv2d_t("i32", 1, 2, 5, 5, 3, 3, 3, 1, 1, "f32_mfma")
     assert e.value.status == qx.ERR_INVALID_ARG
     assert qx.plan_conv2d_t("f32", 0, 32, 5, 5, 3, 3, 3, 1, 1)["kernels"] == 0
     assert qx.plan_conv2d_t("i32", 1, 0, 5, 5, 3, 3, 3, 1, 1)["kernels"] == 1
+
+
+def test_lenet_plan_chains_the_operators():
+    p = qx.plan_lenet_i32(4096)
+    # conv1 (im2col, sums, GEMM), pool, conv2 (im2col, sums, GEMM), pool,
+    # 3 FC GEMMs with their sums and limb encoders, 2 ReLUs
+    assert p["kernels"] >= 12 and p["workspace_bytes"] >= 4 * 4096 * 6 * 28 * 28
+    assert qx.plan_lenet_i32(0)["kernels"] == 0
+    with pytest.raises(qx.QxError):
+        qx.plan_lenet_i32(-1)
 
 
 def test_minmax_pool_plans():

@@ -532,7 +532,8 @@ def test_conv_f32(case):
 
 
 @pytest.mark.parametrize("route", ["s24_i8limb", "s24_valu"])
-@pytest.mark.parametrize("case", CONV_T_CASES[:5] + [(8, 64, 20, 20, 96, 3, 3, 1, 1)])
+@pytest.mark.parametrize("case", CONV_T_CASES[:5] + [(8, 64, 20, 20, 96, 3, 3, 1, 1), (3, 6, 14, 14, 16, 5, 5, 1, 0),
+                                                     (2, 5, 11, 9, 3, 3, 2, 2, 1), (2, 150, 6, 6, 16, 1, 1, 1, 0)])
 def test_conv_i32_smul24(route, case):
     # INT32 conv under the smul24 contract: full 32-bit words (bits 24..31
     # ignored), bit-exact mod 2^32 against the oracle.
@@ -638,6 +639,30 @@ def test_workload_hbm_rows_full_oracle(name):
         y = run_exec(ex, (x,))
     ref = orc.avgpool2_i32(x) if kind == "avg_i32" else orc.maxpool2_f32(x)
     same(y.view(np.uint32), ref.view(np.uint32))
+
+
+@pytest.mark.parametrize("B,wb", [(1, 3), (7, 300), (64, 3), (300, 300)])
+def test_lenet_pipeline(B, wb):
+    # every layer chained through the executor's workspace; weights of 300
+    # make the sums wrap and later layers read only the low 24 bits
+    rng = np.random.default_rng(B * 1000 + wb)
+    x = rng.integers(0, 255, (B, 1, 32, 32), dtype=np.int32, endpoint=True)
+    ws = [rng.integers(-wb, wb, s, dtype=np.int32, endpoint=True)
+          for s in ((6, 1, 5, 5), (16, 6, 5, 5), (400, 120), (120, 84), (84, 10))]
+    with qx.Executor.lenet_i32(B) as ex:
+        y = run_exec(ex, (x, *ws))
+        y2 = run_exec(ex, (x, *ws))
+    ref = orc.lenet_i32(x, *ws)
+    same(y, ref)
+    same(y2, ref, "second run")
+
+
+def test_workload_lenet_full_oracle():
+    w = WORKLOADS["lenet_i32_b4096"]
+    inputs = w.generate()
+    with qx.Executor.lenet_i32(w.dims["B"]) as ex:
+        y = run_exec(ex, inputs)
+    same(y, orc.lenet_i32(*inputs))
 
 
 def test_workload_attn_full_oracle():

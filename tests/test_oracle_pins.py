@@ -411,3 +411,33 @@ def test_pool_closed_forms():
         v = np.zeros(4, np.float32)
         v[pos] = 1.0
         assert orc.maxpool2_f32(v.reshape(1, 1, 2, 2))[0, 0, 0, 0] == 1.0
+
+
+# ----------------------------------------------------------------------------
+# LeNet-5-shaped INT32 pipeline (Results: end-to-end CNN)
+# ----------------------------------------------------------------------------
+def _lenet_inputs(rng, B, lo=-300, hi=300):
+    x = rng.integers(0, 255, (B, 1, 32, 32), dtype=np.int32, endpoint=True)
+    ws = [rng.integers(lo, hi, s, dtype=np.int32, endpoint=True)
+          for s in ((6, 1, 5, 5), (16, 6, 5, 5), (400, 120), (120, 84), (84, 10))]
+    return x, ws
+
+
+def test_lenet_bruteforce_single_images():
+    # layer-by-layer Python integers; the weights are large enough that the
+    # FC sums wrap mod 2^32 and later layers read only the low 24 bits
+    rng = np.random.default_rng(21)
+    x, ws = _lenet_inputs(rng, 2)
+    got = orc.lenet_i32(x, *ws)
+    for b in range(2):
+        ref = brute.lenet_i32(x[b].tolist(), ws[0].tolist(), ws[1].tolist(),
+                              ws[2].tolist(), ws[3].tolist(), ws[4].tolist())
+        assert got[b].tolist() == ref
+
+
+def test_lenet_batch_is_per_image():
+    rng = np.random.default_rng(22)
+    x, ws = _lenet_inputs(rng, 5, -3, 3)
+    full = orc.lenet_i32(x, *ws)
+    for b in range(5):
+        assert (orc.lenet_i32(x[b:b + 1], *ws)[0] == full[b]).all()
