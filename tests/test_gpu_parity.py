@@ -456,6 +456,27 @@ def test_executor_reuse_and_errors():
         assert e.value.status == qx.ERR_INVALID_ARG
 
 
+def test_size_limits():
+    # the largest batch the grid takes (65535 in grid z), a grid of 2^14
+    # row tiles, and the one-element and one-row degenerate shapes
+    rng = np.random.default_rng(6)
+    A = rand_int(rng, (65535, 2, 3), 127, np.int16)
+    B = rand_int(rng, (65535, 3, 2), 127, np.int16)
+    with qx.Executor.gemm_i16i32(2, 2, 3, 65535, 127, 127) as ex:
+        same(run_exec(ex, (A, B)), orc.gemm_i16i32(A, B))
+    A = rand_int(rng, (1, 1 << 20, 5), 2048, np.int16)
+    B = rand_int(rng, (1, 5, 3), 16, np.int16)
+    with qx.Executor.gemm_i16i32(1 << 20, 3, 5, 1, 2048, 16) as ex:
+        same(run_exec(ex, (A, B)), orc.gemm_i16i32(A, B))
+    A = rng.integers(-(1 << 31), (1 << 31) - 1, (3, 1, 1), dtype=np.int32, endpoint=True)
+    B = rng.integers(-(1 << 31), (1 << 31) - 1, (3, 1, 1), dtype=np.int32, endpoint=True)
+    with qx.Executor.gemm_i32_s24(1, 1, 1, 3) as ex:
+        same(run_exec(ex, (A, B)), orc.gemm_i32_s24(A, B))
+    x = rand_int(rng, (1, 1, 1, 1), 256, np.int16)
+    w = rand_int(rng, (1, 1, 1, 1), 256, np.int16)
+    same(host(qx.conv2d_gemm(dev(x), dev(w), 1, 0, 256, 256)), orc.conv2d_direct(x, w, 1, 0))
+
+
 # ---------------------------------------------------------------------------
 # Full-size workloads (the benchmark's launch configuration)
 # ---------------------------------------------------------------------------
