@@ -23,6 +23,7 @@
  * Pins: every function here is checked against brute force in Python
  * integers, closed forms and invariants by tests/test_oracle_pins.py.
  */
+#include <math.h>
 #include <stdint.h>
 #include <stdlib.h>
 #include <string.h>
@@ -284,6 +285,46 @@ void oracle_maxpool2_f32(const float* x, float* y, int64_t N, int64_t C, int64_t
                 if (p[W + 1] > m) m = p[W + 1];
                 y[(nc * Ho + oh) * Wo + ow] = m;
             }
+}
+
+/* Scaled dot-product attention with softmax (Table 2 footnote: the FP32
+ * attention baseline is SDPA with softmax; the attention core extended by
+ * the softmax, Discussion), the float64 reference: for each of the BH heads
+ * and each query i,
+ *   s_j = scale * sum_t Q[i][t] K[j][t]   over keys j (j <= i if causal),
+ *   O[i] = sum_j exp(s_j - max_j s_j) V[j] / sum_j exp(s_j - max_j s_j).
+ * Q, K, V float32 [BH][L][d]; O float64 [BH][L][d]. */
+void oracle_sdpa_f64(const float* Q, const float* K, const float* V, double* O,
+                     int64_t BH, int64_t L, int64_t d, double scale, int32_t causal) {
+    #pragma omp parallel for collapse(2) schedule(dynamic, 4)
+    for (int64_t h = 0; h < BH; ++h) {
+        for (int64_t i = 0; i < L; ++i) {
+            const float* q = Q + (h * L + i) * d;
+            const int64_t nk = causal ? i + 1 : L;
+            double* s = (double*)malloc((size_t)(nk > 0 ? nk : 1) * sizeof(double));
+            double mx = -INFINITY;
+            for (int64_t j = 0; j < nk; ++j) {
+                const float* k = K + (h * L + j) * d;
+                double acc = 0.0;
+                for (int64_t t = 0; t < d; ++t) acc += (double)q[t] * (double)k[t];
+                s[j] = scale * acc;
+                if (s[j] > mx) mx = s[j];
+            }
+            double den = 0.0;
+            for (int64_t j = 0; j < nk; ++j) {
+                s[j] = exp(s[j] - mx);
+                den += s[j];
+            }
+            double* o = O + (h * L + i) * d;
+            for (int64_t t = 0; t < d; ++t) o[t] = 0.0;
+            for (int64_t j = 0; j < nk; ++j) {
+                const float* v = V + (h * L + j) * d;
+                for (int64_t t = 0; t < d; ++t) o[t] += s[j] * (double)v[t];
+            }
+            for (int64_t t = 0; t < d; ++t) o[t] /= den;
+            free(s);
+        }
+    }
 }
 
 /* Attention core, INT32 (Methodology: O = (Q K^T) V; Table 2, INT32 row).

@@ -28,7 +28,7 @@ def build(force: bool = True) -> str:
         tmp = _LIB + ".tmp"
         subprocess.check_call(
             ["gcc", "-O2", "-fopenmp", "-fPIC", "-shared", "-std=c11",
-             "-Wall", "-Wextra", "-o", tmp, _SRC])
+             "-Wall", "-Wextra", "-o", tmp, _SRC, "-lm"])
         os.replace(tmp, _LIB)
     return _LIB
 
@@ -49,6 +49,7 @@ def _load():
         for name in ("oracle_attn_i32", "oracle_attn_i32_assoc", "oracle_attn_f64",
                      "oracle_attn_f64_assoc", "oracle_attn_f32"):
             getattr(lib, name).argtypes = [p, p, p, p, i64, i64]
+        lib.oracle_sdpa_f64.argtypes = [p, p, p, p, i64, i64, i64, ctypes.c_double, ctypes.c_int32]
         lib.oracle_minmax_i32.argtypes = [p, i64, p]
         lib.oracle_minmax_i16.argtypes = [p, i64, p]
         for name in ("oracle_avgpool2_i32", "oracle_maxpool2_f32"):
@@ -217,3 +218,13 @@ def lenet_i32(x, w1, w2, f1, f2, f3):
     h = np.maximum(gemm_i32_s24(a, np.asarray(f1, np.int32)[None]), 0)
     h = np.maximum(gemm_i32_s24(h, np.asarray(f2, np.int32)[None]), 0)
     return gemm_i32_s24(h, np.asarray(f3, np.int32)[None])[0]
+
+
+def sdpa_f64(Q, K, V, scale=1.0, causal=False):
+    """softmax(scale Q K^T [causal mask]) V per head, float64 from float32
+    inputs [BH][L][d] (the softmax attention of Table 2's FP32 baseline)."""
+    Q, K, V = (_c(t, np.float32) for t in (Q, K, V))
+    BH, L, d = Q.shape
+    O = np.empty((BH, L, d), np.float64)
+    _load().oracle_sdpa_f64(_ptr(Q), _ptr(K), _ptr(V), _ptr(O), BH, L, d, float(scale), 1 if causal else 0)
+    return O

@@ -366,6 +366,86 @@ def test_attn_f64_orders_and_numpy_agree():
 
 
 # ----------------------------------------------------------------------------
+# Softmax attention (the SDPA baseline of Table 2's footnote; Discussion)
+# ----------------------------------------------------------------------------
+@pytest.mark.parametrize("BH,L,d,scale,causal", [(1, 1, 1, 1.0, False), (2, 5, 3, 0.7, True),
+                                                 (3, 17, 8, 1.0, False), (2, 33, 16, 0.25, True),
+                                                 (1, 64, 64, -0.5, False)])
+def test_sdpa_f64_matches_torch_float64(BH, L, d, scale, causal):
+    torch = pytest.importorskip("torch")
+    rng = np.random.default_rng(BH + L + d)
+    Q, K, V = (rng.standard_normal((BH, L, d)).astype(np.float32) for _ in range(3))
+    R = orc.sdpa_f64(Q, K, V, scale, causal)
+    T = torch.nn.functional.scaled_dot_product_attention(
+        *(torch.from_numpy(a.astype(np.float64)) for a in (Q, K, V)), is_causal=causal, scale=scale).numpy()
+    assert np.abs(R - T).max() <= 1e-13 * max(np.abs(T).max(), 1.0)
+
+
+def test_sdpa_f64_closed_forms():
+    rng = np.random.default_rng(7)
+    L, d = 9, 4
+    Q, K, V = (rng.standard_normal((1, L, d)).astype(np.float32) for _ in range(3))
+    V64 = V[0].astype(np.float64)
+    # scale 0: uniform weights over the keys a query sees (all keys, or the prefix)
+    R = orc.sdpa_f64(Q, K, V, 0.0, False)[0]
+    assert np.abs(R - V64.mean(axis=0)).max() <= 1e-14
+    R = orc.sdpa_f64(Q, K, V, 0.0, True)[0]
+    prefix = np.cumsum(V64, axis=0) / np.arange(1, L + 1)[:, None]
+    assert np.abs(R - prefix).max() <= 1e-14
+    # the first query under the mask sees only key 0; one key is the identity
+    assert (orc.sdpa_f64(Q, K, V, 3.0, True)[0, 0] == V64[0]).all()
+    assert (orc.sdpa_f64(Q[:, :1], K[:, :1], V[:, :1], 3.0, False)[0, 0] == V64[0]).all()
+    # Q = t I and K a permutation matrix: the score of query i is t on key
+    # pi(i) and 0 elsewhere, so O[i] = (e^t V[pi(i)] + sum_{j != pi(i)} V[j]) / (e^t + L - 1)
+    n, t = 6, 2.5
+    perm = np.array([3, 0, 5, 1, 4, 2])
+    Qm = (t * np.eye(n)).astype(np.float32)[None]
+    Km = np.eye(n, dtype=np.float32)[perm][None]        # row i of K is e_perm(i)
+    Vm = rng.standard_normal((1, n, n)).astype(np.float32)
+    R = orc.sdpa_f64(Qm, Km, Vm, 1.0, False)[0]
+    Vd = Vm[0].astype(np.float64)
+    inv = np.argsort(perm)                               # key j carries e_perm(j); query i matches j = inv[i]
+    for i in range(n):
+        j = inv[i]
+        want = (np.exp(t) * Vd[j] + (Vd.sum(axis=0) - Vd[j])) / (np.exp(t) + n - 1)
+        assert np.abs(R[i] - want).max() <= 1e-14
+
+
+def test_sdpa_f64_invariants():
+    rng = np.random.default_rng(8)
+    BH, L, d = 3, 20, 6
+    Q, K, V = (rng.standard_normal((BH, L, d)).astype(np.float32) for _ in range(3))
+    for causal in (False, True):
+        R = orc.sdpa_f64(Q, K, V, 0.8, causal)
+        # heads are independent
+        for b in range(BH):
+            assert np.array_equal(R[b], orc.sdpa_f64(Q[b:b + 1], K[b:b + 1], V[b:b + 1], 0.8, causal)[0])
+        # a shift of every key by u adds q.u to every score of a query: no change
+        u = np.float32(0.5) * np.ones(d, np.float32)
+        Rs = orc.sdpa_f64(Q, K + u, V, 0.8, causal)
+        assert np.abs(R - Rs).max() <= 1e-5 * np.abs(R).max()
+        # the weights are a convex combination: each output within V's column range
+        for b in range(BH):
+            for i in range(L):
+                seen = V[b, : i + 1] if causal else V[b]
+                assert (R[b, i] >= seen.min(axis=0) - 1e-12).all() and (R[b, i] <= seen.max(axis=0) + 1e-12).all()
+    # without the mask, permuting keys and values together changes nothing
+    perm = rng.permutation(L)
+    R = orc.sdpa_f64(Q, K, V, 0.8, False)
+    Rp = orc.sdpa_f64(Q, K[:, perm], V[:, perm], 0.8, False)
+    assert np.abs(R - Rp).max() <= 1e-13 * np.abs(R).max()
+    # under the mask, query i ignores keys after it: changing the last key
+    # and value changes the last row only
+    K2, V2 = K.copy(), V.copy()
+    K2[:, -1] += 3.0
+    V2[:, -1] -= 2.0
+    R1 = orc.sdpa_f64(Q, K, V, 0.8, True)
+    R2 = orc.sdpa_f64(Q, K2, V2, 0.8, True)
+    assert np.array_equal(R1[:, :-1], R2[:, :-1])
+    assert not np.array_equal(R1[:, -1], R2[:, -1])
+
+
+# ----------------------------------------------------------------------------
 # Min/max, 2x2 average and max pooling (Table 2 rows)
 # ----------------------------------------------------------------------------
 @pytest.mark.parametrize("n", [1, 2, 7, 1000, 65537])
