@@ -50,7 +50,8 @@ def contraction_sha256():
     import hashlib
     try:
         src = open(KERNEL_SRC).read()
-        a = src.index("template <int BM, int BN, int NW, bool IMPL>")
+        sig = src.index("void k_gemm_nt(const GemmParams p)")
+        a = src.rindex("template <", 0, sig)
         b = src.index("// Builders", a)
     except (OSError, ValueError):
         return None
@@ -118,6 +119,8 @@ def make_executor(w, qx):
         return qx.Executor.attn("f32", d["L"], d["d"])
     if w.op == "attn_i32":
         return qx.Executor.attn("i32", d["L"], d["d"], w.bound)
+    if w.op == "sdpa_f32":
+        return qx.Executor.sdpa_f32(d["BH"], d["L"], d["d"], d["scale"], bool(d["causal"]))
     raise ValueError(w.op)
 
 
@@ -218,7 +221,8 @@ def main():
     achieved_tflops = w.ops / (dom_ms / 1e3) / 1e12
     route = r["plan"]["route_name"]
     unit_peak = {"f16_exact": "f16", "i8_direct": "i8", "i8_karatsuba": "i8", "i8_offset4": "i8",
-                 "s24_i8limb": "i8", "attn_f32_mfma": "f32", "attn_i32_mfma": "i8"}.get(route, "f16")
+                 "s24_i8limb": "i8", "attn_f32_mfma": "f32", "attn_i32_mfma": "i8",
+                 "f32_mfma": "f32"}.get(route, "f16")
     peak = PEAK[unit_peak]
     line = {
         "metric": METRIC,
@@ -235,7 +239,8 @@ def main():
         # in fp32 per chunk, chunks added in int32 (the result is the exact
         # int32 GEMM of the int16 inputs)
         "dtype": {"f16_exact": "f16", "s24_i8limb": "i8", "i8_direct": "i8", "i8_karatsuba": "i8",
-                  "i8_offset4": "i8"}.get(route, "i32"),
+                  "i8_offset4": "i8", "attn_f32_mfma": "f32", "attn_i32_mfma": "i8",
+                  "f32_mfma": "f32", "f32_valu": "f32", "attn_f32_valu": "f32"}.get(route, "i32"),
         "data": "synthetic",
         "config": {"workload": w.name, **w.dims, "operand_range": [w.lo, w.hi], "seed": w.seed,
                    "route": route, "chunk": r["plan"]["chunk"]},

@@ -179,6 +179,24 @@ qx_status pool2x2(int32_t kind, const void* x, void* y, int64_t N, int64_t C, in
 qx_status attn_core(qx_attn_dtype dt, const void* Q, const void* K, const void* V, void* O,
                     int64_t L, int64_t d, int32_t bound, void* stream);
 
+/* Multi-head scaled dot-product attention with softmax, FP32 (the SDPA
+ * attention baseline of Table 2, whose footnote gives scale 1.0; the
+ * attention core with a softmax, Discussion).  For every head b < BH:
+ *   O[b] = softmax_rows(scale * Q[b] K[b]^T [+ causal mask]) V[b]
+ * Q, K, V, O float32 [BH][L][d] row-major (heads outermost; a [B][H][L][d]
+ * tensor is BH = B*H heads).  causal = 1 lets query i see keys j <= i only;
+ * causal = 0 sees all L keys.  scale: any finite value (1/sqrt(d) is the
+ * usual one).  The softmax is taken online over 32-key blocks with a
+ * running maximum; key splits (used when BH * ceil(L/128) < 512) are merged
+ * in a fixed order, so repeated runs are bit-identical.
+ * BH in [0, 65535], L in [0, 2^20], d in [0, 128]; BH*L*d <= 2^34; any 0
+ * size is a no-op.  Q, K, V 16-byte aligned when d % 32 == 0, 4-byte
+ * otherwise.  Returns QX_ERR_INVALID_ARG for a non-finite scale or
+ * causal outside {0, 1}. */
+qx_status sdpa_f32(const float* Q, const float* K, const float* V, float* O,
+                   int64_t BH, int64_t L, int64_t d, float scale, int32_t causal,
+                   void* stream);
+
 /* ---- persistent executor (Methodology: assemble and allocate once, cache
  *      launch metadata, re-dispatch) ---------------------------------------- */
 
@@ -233,6 +251,9 @@ qx_status qx_exec_profile(qx_exec h, const void* const* inputs, void* output, vo
 
 /* Free the workspace and the handle (waits for the device to finish any
  * work that may use the workspace).  NULL is accepted. */
+/* inputs {Q, K, V}, output O, as sdpa_f32 */
+qx_status qx_exec_create_sdpa_f32(qx_exec* out, int64_t BH, int64_t L, int64_t d, float scale,
+                                  int32_t causal);
 qx_status qx_exec_destroy(qx_exec h);
 
 /* ---- planner queries (pure host logic, no device needed) ---------------- */
@@ -248,6 +269,8 @@ qx_status qx_plan_conv2d_t(qx_plan_info* out, qx_attn_dtype dt, int64_t N, int64
                            int64_t stride, int64_t pad, int32_t route);
 qx_status qx_plan_attn(qx_plan_info* out, qx_attn_dtype dt, int64_t L, int64_t d,
                        int32_t bound, int32_t route);
+qx_status qx_plan_sdpa_f32(qx_plan_info* out, int64_t BH, int64_t L, int64_t d, float scale,
+                           int32_t causal);
 qx_status qx_plan_minmax(qx_plan_info* out, int64_t n, int32_t elem_bytes);
 qx_status qx_plan_lenet_i32(qx_plan_info* out, int64_t batch);
 qx_status qx_plan_pool2x2(qx_plan_info* out, int32_t kind, int64_t N, int64_t C, int64_t H, int64_t W);

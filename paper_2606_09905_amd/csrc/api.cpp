@@ -14,6 +14,8 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <cmath>
+#include <cstring>
 #include <cstdarg>
 #include <cstdio>
 #include <map>
@@ -52,7 +54,7 @@ constexpr uint32_t kMagic = 0x71786578u;  // "qxex"
 
 enum OpKind : int32_t {
     OP_GEMM_I16 = 1, OP_GEMM_S24 = 2, OP_CONV = 3, OP_ATTN_F32 = 4, OP_ATTN_I32 = 5, OP_CONV_F32 = 6, OP_CONV_I32 = 7,
-    OP_MINMAX = 8, OP_POOL = 9, OP_LENET = 10
+    OP_MINMAX = 8, OP_POOL = 9, OP_LENET = 10, OP_SDPA = 11
 };
 
 // A fully planned operation: route facts plus launch records with unbound
@@ -1123,6 +1125,74 @@ qx_status plan_attn(Plan* pl, qx_attn_dtype dt, int64_t L, int64_t d, int32_t bo
     return QX_OK;
 }
 
+qx_status plan_sdpa(Plan* pl, int64_t BH, int64_t L, int64_t d, float scale, int32_t causal) {
+    qx_status st = check_dims({{"BH", BH}, {"L", L}, {"d", d}});
+    if (st) return st;
+    if (d > 128) return fail(QX_ERR_UNSUPPORTED, "d = %lld exceeds 128", (long long)d);
+    if (L > (1 << 20)) return fail(QX_ERR_UNSUPPORTED, "L = %lld exceeds 2^20", (long long)L);
+    if (BH > 65535) return fail(QX_ERR_UNSUPPORTED, "BH = %lld exceeds 65535", (long long)BH);
+    if (!std::isfinite(scale)) return fail(QX_ERR_INVALID_ARG, "scale must be finite");
+    if (causal != 0 && causal != 1) return fail(QX_ERR_INVALID_ARG, "causal = %d must be 0 or 1", causal);
+    int64_t n;
+    if (!mul_ok(BH, L, (int64_t)1 << 40, &n) || !mul_ok(n, d, (int64_t)1 << 34, &n))
+        return fail(QX_ERR_UNSUPPORTED, "BH*L*d exceeds 2^34");
+    pl->op = OP_SDPA;
+    pl->n_inputs = 3;
+    pl->in_align = d % 32 == 0 ? 16 : 4;
+    qx_plan_info& info = pl->info;
+    info.route = R_ATTN_F32_MFMA;
+    info.products = 1;
+    info.chunk = 0;
+    info.exact_no_wrap = 0;
+    if (BH == 0 || L == 0 || d == 0) {
+        info.kernels = 0;
+        info.workspace_bytes = 0;
+        return QX_OK;
+    }
+    // Key splits only while the query blocks of all heads leave the chip
+    // short of 512 workgroups; split boundaries on 32-key blocks.
+    const int64_t wgs = (L + 127) / 128 * BH;
+    const int64_t kblocks = (L + 31) / 32;
+    int64_t splits = std::min<int64_t>(std::max<int64_t>((512 + wgs - 1) / wgs, 1), kblocks);
+    const int64_t kps = ((kblocks + splits - 1) / splits) * 32;
+    splits = (L + kps - 1) / kps;
+    SdpaParams a{};
+    a.L = (int32_t)L; a.d = (int32_t)d; a.BH = (int32_t)BH;
+    a.splits = (int32_t)splits; a.keys_per_split = (int32_t)kps;
+    a.causal = causal;
+    a.c = (float)((double)scale * 1.4426950408889634);   // log2(e)
+    LaunchRec rec;
+    if (!build_sdpa_f32(a, &rec)) return fail(QX_ERR_UNSUPPORTED, "no attention kernel for d = %lld", (long long)d);
+    rec.bind(offsetof(SdpaParams, Q), BIND_IN0);
+    rec.bind(offsetof(SdpaParams, K), BIND_IN1);
+    rec.bind(offsetof(SdpaParams, V), BIND_IN2);
+    rec.bind(offsetof(SdpaParams, O), BIND_OUT);
+    uint64_t ws = 0;
+    if (splits > 1) {
+        const uint64_t part_bytes = round_up(4 * (uint64_t)splits * (uint64_t)n, 256);
+        ws = part_bytes + 8 * (uint64_t)splits * (uint64_t)BH * (uint64_t)L;
+        rec.bind(offsetof(SdpaParams, part), BIND_WS, 0);
+        rec.bind(offsetof(SdpaParams, stat), BIND_WS, part_bytes);
+        pl->launches.push_back(rec);
+        SdpaCombineParams cp{};
+        cp.rows = BH * L;
+        cp.d = (int32_t)d;
+        cp.splits = (int32_t)splits;
+        LaunchRec rc;
+        build_sdpa_combine(cp, &rc);
+        rc.bind(offsetof(SdpaCombineParams, part), BIND_WS, 0);
+        rc.bind(offsetof(SdpaCombineParams, stat), BIND_WS, part_bytes);
+        rc.bind(offsetof(SdpaCombineParams, O), BIND_OUT);
+        pl->launches.push_back(rc);
+    } else {
+        pl->launches.push_back(rec);
+    }
+    info.tile_m = 128; info.tile_n = (int32_t)d; info.tile_k = (int32_t)kps;
+    info.kernels = (int32_t)pl->launches.size();
+    info.workspace_bytes = (int64_t)ws;
+    return QX_OK;
+}
+
 }  // namespace
 
 // ---------------------------------------------------------------------------
@@ -1492,6 +1562,25 @@ qx_status qx_plan_attn(qx_plan_info* out, qx_attn_dtype dt, int64_t L, int64_t d
     return st;
 }
 
+qx_status qx_plan_sdpa_f32(qx_plan_info* out, int64_t BH, int64_t L, int64_t d, float scale, int32_t causal) {
+    g_err.clear();
+    if (!out) return fail(QX_ERR_INVALID_ARG, "out is NULL");
+    Plan pl;
+    qx_status st = plan_sdpa(&pl, BH, L, d, scale, causal);
+    if (!st) *out = pl.info;
+    return st;
+}
+
+qx_status qx_exec_create_sdpa_f32(qx_exec* out, int64_t BH, int64_t L, int64_t d, float scale, int32_t causal) {
+    g_err.clear();
+    if (!out) return fail(QX_ERR_INVALID_ARG, "out is NULL");
+    *out = nullptr;
+    Plan pl;
+    qx_status st = plan_sdpa(&pl, BH, L, d, scale, causal);
+    if (st) return st;
+    return make_exec(std::move(pl), out);
+}
+
 qx_status qx_exec_create_gemm_i16i32(qx_exec* out, int64_t M, int64_t N, int64_t K, int64_t batch, int32_t bound_a,
                                      int32_t bound_b, int32_t route) {
     g_err.clear();
@@ -1730,6 +1819,21 @@ qx_status attn_core(qx_attn_dtype dt, const void* Q, const void* K, const void* 
     Key key{dt == QX_DT_F32 ? OP_ATTN_F32 : OP_ATTN_I32, 0, L, d, bound, 0, 0, 0, 0, 0, 0, 0, 0, 0,
             (uintptr_t)stream};
     return oneshot(key, [&](Plan* pl) { return plan_attn(pl, dt, L, d, bound, R_AUTO); }, in, O, stream);
+}
+
+qx_status sdpa_f32(const float* Q, const float* K, const float* V, float* O, int64_t BH, int64_t L, int64_t d,
+                   float scale, int32_t causal, void* stream) {
+    g_err.clear();
+    Plan probe;
+    qx_status st = plan_sdpa(&probe, BH, L, d, scale, causal);
+    if (st) return st;
+    if (probe.launches.empty()) return QX_OK;
+    if (!Q || !K || !V || !O) return fail(QX_ERR_INVALID_ARG, "NULL pointer for a non-empty operand");
+    const void* in[3] = {Q, K, V};
+    uint32_t sbits;
+    std::memcpy(&sbits, &scale, 4);
+    Key key{OP_SDPA, 0, BH, L, d, (int64_t)sbits, causal, 0, 0, 0, 0, 0, 0, 0, (uintptr_t)stream};
+    return oneshot(key, [&](Plan* pl) { return plan_sdpa(pl, BH, L, d, scale, causal); }, in, O, stream);
 }
 
 }  // extern "C"

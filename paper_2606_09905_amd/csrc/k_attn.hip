@@ -275,6 +275,200 @@ __global__ __launch_bounds__(AT) void k_attn_i32(const AttnParams p) {
 }
 
 // ---------------------------------------------------------------------------
+// Softmax attention, FP32, BH heads (the SDPA-with-softmax form of the
+// attention baseline, Table 2 footnote; the attention core with a softmax,
+// Discussion).  Same S^T = K_blk Q^T layout as k_attn_f32: lane (query l32,
+// half h) holds 16 of the 32 scores of its query in a key block.  Per block
+// the running maximum m (base-2 exponent domain, t = scale*log2(e)*s) and the
+// running sum are updated online; the exponentials are the A operand of
+// O += P V, and O's rows (registers, not lanes) are rescaled by the factor of
+// their query, fetched from the lane that owns it.  With key splits every
+// split writes unnormalised O, its maximum and its sum; k_sdpa_combine merges
+// them in split order, so repeated runs are bit-identical.
+// RAG: d < D, columns d..D-1 read as zeros and are not written.
+// ---------------------------------------------------------------------------
+template <int D, bool RAG>
+__global__ __launch_bounds__(AT) void k_sdpa_f32(const SdpaParams p) {
+    constexpr int DP = D + 4;
+    constexpr int HALF = D / 2;
+    constexpr int NTO = D / 32;
+    constexpr int LD4 = AKB * D / 4 / AT;
+    __shared__ float Ks[AKB][DP];
+    __shared__ float Vs[AKB][DP];
+
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, h = lane >> 5, l32 = lane & 31;
+    // Under the mask a query block's work grows with its index: the dispatch
+    // order (x fastest, then z) hands out the longest blocks of every head
+    // first, so that the short ones fill in behind them.
+    int qblk = blockIdx.x;
+    int64_t head = blockIdx.z;
+    if (p.causal) {
+        const int id = (int)blockIdx.x + (int)gridDim.x * (int)blockIdx.z;
+        qblk = (int)gridDim.x - 1 - id / (int)gridDim.z;
+        head = id % (int)gridDim.z;
+    }
+    const int qb = qblk * AQ;
+    const int q0 = qb + wave * AQW;
+    const int split = blockIdx.y;
+    const int d = RAG ? p.d : D;
+    const int key_lo = split * p.keys_per_split;
+    int key_hi = min(p.L, key_lo + p.keys_per_split);
+    if (p.causal) key_hi = min(key_hi, qb + AQ);
+    const int64_t hoff = head * p.L * d;
+    const float* Q = p.Q + hoff;
+    const float* Kp = p.K + hoff;
+    const float* Vp = p.V + hoff;
+
+    auto ld4 = [&](const float* base, int row, int c4) -> f4 {
+        if (!RAG) return *(const f4*)(base + (int64_t)row * D + c4 * 4);
+        f4 v;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            const int col = c4 * 4 + e;
+            v[e] = col < d ? base[(int64_t)row * d + col] : 0.f;
+        }
+        return v;
+    };
+
+    const int q = q0 + l32;           // this lane's query in the S^T layout
+    float qf[HALF];
+#pragma unroll
+    for (int t = 0; t < HALF; t += 4) {
+        const f4 v = q < p.L ? ld4(Q, q, (HALF * h + t) / 4) : f4{};
+        qf[t] = v[0]; qf[t + 1] = v[1]; qf[t + 2] = v[2]; qf[t + 3] = v[3];
+    }
+    f16x o[NTO];
+#pragma unroll
+    for (int n = 0; n < NTO; ++n) o[n] = f16x{};
+    float m = -INFINITY;              // running maximum of t for query q
+    float lsum = 0.f;                 // this half's share of the running sum
+
+    f4 rk[LD4], rv[LD4];
+    auto load = [&](int kb) {
+#pragma unroll
+        for (int i = 0; i < LD4; ++i) {
+            const int v = tid + AT * i, row = v / (D / 4), c4 = v % (D / 4);
+            const int key = kb + row;
+            const bool in = key < key_hi;
+            rk[i] = in ? ld4(Kp, key, c4) : f4{};
+            rv[i] = in ? ld4(Vp, key, c4) : f4{};
+        }
+    };
+    auto stash = [&]() {
+#pragma unroll
+        for (int i = 0; i < LD4; ++i) {
+            const int v = tid + AT * i, row = v / (D / 4), c4 = v % (D / 4);
+            *(f4*)&Ks[row][c4 * 4] = rk[i];
+            *(f4*)&Vs[row][c4 * 4] = rv[i];
+        }
+    };
+
+    const float c = p.c;
+    if (key_lo < key_hi) load(key_lo);
+    for (int kb = key_lo; kb < key_hi; kb += AKB) {
+        __syncthreads();
+        stash();
+        __syncthreads();
+        if (kb + AKB < key_hi) load(kb + AKB);
+        if (p.causal && kb > q0 + AQW - 1) continue;   // every key after every query of this wave
+        f16x s = f16x{};
+#pragma unroll
+        for (int t = 0; t < HALF; t += 4) {
+            const f4 kv = *(const f4*)&Ks[l32][HALF * h + t];
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+                s = __builtin_amdgcn_mfma_f32_32x32x2f32(kv[e], qf[t + e], s, 0, 0, 0);
+        }
+        // register r holds key kb + 8*(r/4) + 4*h + r%4
+        // keys at or past key_lim are masked for this lane's query
+        const int key_lim = p.causal ? min(key_hi, q + 1) : key_hi;
+        const int kl = key_lim - kb - 4 * h;    // register r is kept iff 8*(r/4) + r%4 < kl
+        float mx = -INFINITY;
+#pragma unroll
+        for (int r = 0; r < 16; ++r)
+            if (8 * (r >> 2) + (r & 3) < kl) mx = fmaxf(mx, s[r] * c);
+        mx = fmaxf(mx, __shfl_xor(mx, 32));
+        const float m_new = fmaxf(m, mx);
+        const float m_use = m_new == -INFINITY ? 0.f : m_new;
+        const float alpha = exp2f(m - m_use);
+        m = m_new;
+        float ps = 0.f;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+            s[r] = 8 * (r >> 2) + (r & 3) < kl ? exp2f(fmaf(s[r], c, -m_use)) : 0.f;
+            ps += s[r];
+        }
+        lsum = lsum * alpha + ps;
+        if (__ballot(alpha != 1.f) != 0) {
+            // row r of O is query 8*(r/4) + 4*h + r%4, whose factor lane that index holds
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+                const float a = __shfl(alpha, 8 * (r >> 2) + 4 * h + (r & 3));
+#pragma unroll
+                for (int n = 0; n < NTO; ++n) o[n][r] *= a;
+            }
+        }
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+            const int key = 8 * (r >> 2) + 4 * h + (r & 3);
+#pragma unroll
+            for (int n = 0; n < NTO; ++n)
+                o[n] = __builtin_amdgcn_mfma_f32_32x32x2f32(s[r], Vs[key][n * 32 + l32], o[n], 0, 0, 0);
+        }
+    }
+
+    const float l = lsum + __shfl_xor(lsum, 32);
+    const int64_t rows = (int64_t)p.BH * p.L;
+    if (p.splits > 1) {
+        float* part = p.part + ((int64_t)split * rows + head * p.L) * d;
+#pragma unroll
+        for (int n = 0; n < NTO; ++n)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+                const int qr = q0 + 8 * (r >> 2) + 4 * h + (r & 3), col = n * 32 + l32;
+                if (qr < p.L && (!RAG || col < d)) part[(int64_t)qr * d + col] = o[n][r];
+            }
+        if (h == 0 && q < p.L) {
+            float* st = p.stat + ((int64_t)split * rows + head * p.L + q) * 2;
+            st[0] = m;
+            st[1] = l;
+        }
+    } else {
+        const float inv = l > 0.f ? 1.f / l : 0.f;
+        float* O = p.O + hoff;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+            const int qi = 8 * (r >> 2) + 4 * h + (r & 3);
+            const float f = __shfl(inv, qi);
+            const int qr = q0 + qi;
+#pragma unroll
+            for (int n = 0; n < NTO; ++n) {
+                const int col = n * 32 + l32;
+                if (qr < p.L && (!RAG || col < d)) O[(int64_t)qr * d + col] = o[n][r] * f;
+            }
+        }
+    }
+}
+
+// Merge of the key splits, one thread per output element, splits in order:
+// O = sum_s 2^(m_s - M) O_s / sum_s 2^(m_s - M) l_s with M = max_s m_s.
+__global__ __launch_bounds__(AT) void k_sdpa_combine(const SdpaCombineParams p) {
+    const int64_t i = (int64_t)blockIdx.x * AT + threadIdx.x;
+    if (i >= p.rows * p.d) return;
+    const int64_t row = i / p.d;
+    float M = -INFINITY;
+    for (int s = 0; s < p.splits; ++s) M = fmaxf(M, p.stat[((int64_t)s * p.rows + row) * 2]);
+    float num = 0.f, den = 0.f;
+    for (int s = 0; s < p.splits; ++s) {
+        const float* st = p.stat + ((int64_t)s * p.rows + row) * 2;
+        const float w = exp2f(st[0] - M);
+        num += w * p.part[(int64_t)s * p.rows * p.d + i];
+        den += w * st[1];
+    }
+    p.O[i] = num / den;
+}
+
+// ---------------------------------------------------------------------------
 // Builders
 // ---------------------------------------------------------------------------
 bool build_attn_f32(const AttnParams& p, LaunchRec* rec) {
@@ -312,6 +506,34 @@ void build_reduce(const ReduceParams& p, LaunchRec* rec) {
     rec->grid = dim3((unsigned)((p.n + AT - 1) / AT), 1, 1);
     rec->block = dim3(AT, 1, 1);
     rec->name = "reduce_splits";
+    rec->set_params(p);
+}
+
+bool build_sdpa_f32(const SdpaParams& p, LaunchRec* rec) {
+    const int D = (p.d + 31) / 32 * 32;
+    const bool rag = p.d != D;
+#define QX_SDPA_CASE(DD) \
+    case DD: rec->fn = rag ? (const void*)k_sdpa_f32<DD, true> : (const void*)k_sdpa_f32<DD, false>; break;
+    switch (D) {
+    QX_SDPA_CASE(32)
+    QX_SDPA_CASE(64)
+    QX_SDPA_CASE(96)
+    QX_SDPA_CASE(128)
+    default: return false;
+    }
+#undef QX_SDPA_CASE
+    rec->name = "sdpa_f32";
+    rec->grid = dim3((unsigned)((p.L + AQ - 1) / AQ), (unsigned)p.splits, (unsigned)p.BH);
+    rec->block = dim3(AT, 1, 1);
+    rec->set_params(p);
+    return true;
+}
+
+void build_sdpa_combine(const SdpaCombineParams& p, LaunchRec* rec) {
+    rec->fn = (const void*)k_sdpa_combine;
+    rec->grid = dim3((unsigned)((p.rows * p.d + AT - 1) / AT), 1, 1);
+    rec->block = dim3(AT, 1, 1);
+    rec->name = "sdpa_combine";
     rec->set_params(p);
 }
 

@@ -153,6 +153,30 @@ struct AttnParams {
     int32_t limbs;          // I32: int8 limbs of S
 };
 
+// Softmax attention over BH heads (FP32): O = softmax(scale Q K^T [mask]) V.
+struct SdpaParams {
+    const float* Q;         // [BH][L][d]
+    const float* K;
+    const float* V;
+    float* O;               // [BH][L][d]
+    float* part;            // splits > 1: unnormalised outputs [splits][BH][L][d]
+    float* stat;            // splits > 1: (max, sum) per row [splits][BH][L][2]
+    int32_t L, d, BH;
+    int32_t splits;         // key splits
+    int32_t keys_per_split;
+    int32_t causal;         // key j is seen by query i only when j <= i
+    float c;                // scale * log2(e): scores in the base-2 exponent domain
+};
+
+struct SdpaCombineParams {
+    const float* part;
+    const float* stat;
+    float* O;
+    int64_t rows;           // BH * L
+    int32_t d;
+    int32_t splits;
+};
+
 struct ReduceParams {
     const float* part;      // [splits][n]
     float* out;             // [n]
@@ -291,6 +315,8 @@ void build_valu_gemm(int32_t kind, const ValuGemmParams& p, int batch, LaunchRec
 bool build_attn_f32(const AttnParams& p, LaunchRec* rec);
 bool build_attn_i32(const AttnParams& p, LaunchRec* rec);
 void build_reduce(const ReduceParams& p, LaunchRec* rec);
+bool build_sdpa_f32(const SdpaParams& p, LaunchRec* rec);
+void build_sdpa_combine(const SdpaCombineParams& p, LaunchRec* rec);
 void build_fill(const FillParams& p, LaunchRec* rec);
 void build_range(const RangeParams& p, LaunchRec* rec);
 // Min/max reduction (two launches) and 2x2 pooling.

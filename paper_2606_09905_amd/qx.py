@@ -7,6 +7,7 @@ If the library is missing, every call raises; there is no fallback.
 from __future__ import annotations
 
 import ctypes
+import math
 import os
 import re
 
@@ -55,7 +56,7 @@ class PlanInfo(ctypes.Structure):
 
 
 _lib = None
-_i64, _i32, _p = ctypes.c_int64, ctypes.c_int32, ctypes.c_void_p
+_i64, _i32, _p, _f32 = ctypes.c_int64, ctypes.c_int32, ctypes.c_void_p, ctypes.c_float
 
 
 def lib() -> ctypes.CDLL:
@@ -94,6 +95,9 @@ def lib() -> ctypes.CDLL:
             "qx_plan_lenet_i32": [_p, _i64],
             "qx_exec_create_lenet_i32": [_p, _i64],
             "qx_plan_pool2x2": [_p, _i32, _i64, _i64, _i64, _i64],
+            "sdpa_f32": [_p, _p, _p, _p, _i64, _i64, _i64, _f32, _i32, _p],
+            "qx_exec_create_sdpa_f32": [_p, _i64, _i64, _i64, _f32, _i32],
+            "qx_plan_sdpa_f32": [_p, _i64, _i64, _i64, _f32, _i32],
         }
         for name, args in sig.items():
             fn = getattr(L, name)
@@ -253,6 +257,24 @@ def attn_core(Q, K, V, bound: int = 0, out=None, stream=None):
     return out
 
 
+def sdpa_f32(Q, K, V, scale: float = 1.0, causal: bool = False, out=None, stream=None):
+    """softmax(scale Q K^T [causal mask]) V per head for float32 [..., L, d]
+    tensors; leading dimensions are flattened into heads."""
+    torch = _torch()
+    if Q.dtype != torch.float32:
+        raise TypeError("Q must be float32")
+    if Q.dim() < 2 or K.shape != Q.shape or V.shape != Q.shape:
+        raise ValueError("Q, K, V must share one shape [..., L, d]")
+    L, d = Q.shape[-2], Q.shape[-1]
+    BH = math.prod(Q.shape[:-2])
+    if out is None:
+        out = torch.empty(Q.shape, dtype=Q.dtype, device=Q.device)
+    check(lib().sdpa_f32(_dev_tensor(Q, Q.dtype, "Q"), _dev_tensor(K, Q.dtype, "K"),
+                         _dev_tensor(V, Q.dtype, "V"), _dev_tensor(out, Q.dtype, "O"), BH, L, d,
+                         float(scale), 1 if causal else 0, _stream(stream)))
+    return out
+
+
 def minmax(x, out=None, stream=None):
     """(min, max) of a non-empty int32 or int16 tensor, as a 2-element tensor."""
     torch = _torch()
@@ -331,6 +353,12 @@ def plan_pool2x2(kind: str, N, C, H, W) -> dict:
 def plan_lenet_i32(batch) -> dict:
     info = PlanInfo()
     check(lib().qx_plan_lenet_i32(ctypes.byref(info), batch))
+    return info.as_dict()
+
+
+def plan_sdpa_f32(BH, L, d, scale=1.0, causal=False) -> dict:
+    info = PlanInfo()
+    check(lib().qx_plan_sdpa_f32(ctypes.byref(info), BH, L, d, float(scale), 1 if causal else 0))
     return info.as_dict()
 
 
@@ -419,6 +447,14 @@ class Executor:
         check(lib().qx_exec_create_attn(ctypes.byref(h), DT_F32 if dtype == "f32" else DT_I32, L, d,
                                         bound, _route(route)))
         return cls(h, (L, d), torch.float32 if dtype == "f32" else torch.int32, 3)
+
+    @classmethod
+    def sdpa_f32(cls, BH, L, d, scale=1.0, causal=False):
+        """inputs (Q, K, V) float32 [BH][L][d]; output [BH][L][d]."""
+        torch = _torch()
+        h = ctypes.c_void_p()
+        check(lib().qx_exec_create_sdpa_f32(ctypes.byref(h), BH, L, d, float(scale), 1 if causal else 0))
+        return cls(h, (BH, L, d), torch.float32, 3)
 
     def plan(self) -> dict:
         info = PlanInfo()

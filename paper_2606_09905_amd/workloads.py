@@ -9,11 +9,13 @@ the workloads below are synthetic by definition: a small INT16 GEMM (values in
 (values in [-256, 255]), and the same 3x3 convolution on FP32 and on smul24
 INT32 operands, and the HBM-bound rows: min/max over INT32 and INT16 arrays,
 2x2 INT32 average pooling and FP32 max pooling, and a LeNet-5-shaped INT32
-pipeline with synthetic weights (images in [0, 255], weights in [-3, 3]).
+pipeline with synthetic weights (images in [0, 255], weights in [-3, 3]),
+and multi-head softmax attention (32 heads of 4096 x 64, plain and causal).
 Integers are uniform over a
-closed range; FP32 attention inputs are N(0, 1) / sqrt(d), FP32 convolution
-inputs N(0, 1) with weights N(0, 1) / sqrt(C_in KH KW), pooling inputs
-N(0, 1).
+closed range; FP32 attention-core inputs are N(0, 1) / sqrt(d), FP32
+convolution inputs N(0, 1) with weights N(0, 1) / sqrt(C_in KH KW), pooling
+inputs N(0, 1), softmax-attention inputs N(0, 1) * d^(-1/4), so that at
+scale 1 the scores have unit variance.
 """
 from __future__ import annotations
 
@@ -36,7 +38,7 @@ def normal_f32(rng: np.random.Generator, shape, scale: float) -> np.ndarray:
 class Workload:
     name: str
     op: str            # "gemm_i16i32" | "gemm_i32_s24" | "conv2d" | "conv2d_f32" | "conv2d_i32"
-                       # | "attn_f32" | "attn_i32"
+                       # | "attn_f32" | "attn_i32" | "sdpa_f32" | ...
     seed: int
     dims: dict = field(default_factory=dict)
     lo: int = 0
@@ -55,6 +57,10 @@ class Workload:
             return 2.0 * d["N"] * d["Co"] * ho * wo * d["Ci"] * d["KH"] * d["KW"]
         if self.op in ("attn_f32", "attn_i32"):
             return 4.0 * d["L"] * d["L"] * d["d"]
+        if self.op == "sdpa_f32":
+            # two products per (query, key) pair seen: all L^2, or L(L+1)/2 under the mask
+            pairs = d["L"] * (d["L"] + 1) / 2 if d["causal"] else d["L"] * d["L"]
+            return 4.0 * d["BH"] * pairs * d["d"]
         if self.op in ("minmax_i32", "minmax_i16", "avgpool_i32", "maxpool_f32"):
             return 0.0      # measured in bytes per second (see in_bytes)
         if self.op == "lenet_i32":
@@ -119,6 +125,9 @@ class Workload:
             return tuple(normal_f32(rng, (d["L"], d["d"]), s) for _ in range(3))
         if self.op == "attn_i32":
             return tuple(ints(rng, (d["L"], d["d"]), self.lo, self.hi, np.int32) for _ in range(3))
+        if self.op == "sdpa_f32":
+            s = d["d"] ** -0.25
+            return tuple(normal_f32(rng, (d["BH"], d["L"], d["d"]), s) for _ in range(3))
         raise ValueError(self.op)
 
 
@@ -147,4 +156,6 @@ WORKLOADS = {w.name: w for w in [
              -(1 << 31), (1 << 31) - 1),
     Workload("maxpool_f32_16x64x224x224", "maxpool_f32", 14, dict(N=16, C=64, H=224, W=224)),
     Workload("lenet_i32_b4096", "lenet_i32", 15, dict(B=4096), -3, 3, 3),
+    Workload("sdpa_f32_32x4096x64", "sdpa_f32", 16, dict(BH=32, L=4096, d=64, scale=1.0, causal=0)),
+    Workload("sdpa_f32_causal_32x4096x64", "sdpa_f32", 17, dict(BH=32, L=4096, d=64, scale=1.0, causal=1)),
 ]}

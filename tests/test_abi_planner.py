@@ -249,6 +249,33 @@ def test_attention_plans():
     assert p["tile_k"] % 32 == 0 and (4096 // 128) * (4096 // p["tile_k"]) >= 512
 
 
+def test_sdpa_plans():
+    # 32 heads x 32 query blocks fill the chip: one launch, no workspace
+    p = qx.plan_sdpa_f32(32, 4096, 64, 1.0, False)
+    assert p["kernels"] == 1 and p["workspace_bytes"] == 0 and p["tile_k"] == 4096
+    # one head: key splits on 32-key boundaries, merged by a second launch;
+    # the workspace holds unnormalised outputs plus (max, sum) per row
+    p = qx.plan_sdpa_f32(1, 4096, 64, 0.125, True)
+    splits = 4096 // p["tile_k"]
+    assert p["kernels"] == 2 and p["tile_k"] % 32 == 0 and 32 * splits >= 512
+    assert p["workspace_bytes"] >= splits * 4096 * (64 + 2) * 4
+    # any d up to 128 (ragged d pads to the next multiple of 32 on chip)
+    for d in (1, 17, 40, 100, 128):
+        assert qx.plan_sdpa_f32(2, 100, d)["kernels"] >= 1
+    for args, status in (((1, 10, 129), qx.ERR_UNSUPPORTED), ((65536, 10, 64), qx.ERR_UNSUPPORTED),
+                         ((1, (1 << 20) + 1, 64), qx.ERR_UNSUPPORTED), ((-1, 10, 64), qx.ERR_INVALID_ARG),
+                         ((1, 10, 64, float("nan")), qx.ERR_INVALID_ARG),
+                         ((1, 10, 64, float("inf")), qx.ERR_INVALID_ARG)):
+        with pytest.raises(qx.QxError) as e:
+            qx.plan_sdpa_f32(*args)
+        assert e.value.status == status, args
+    info = qx.PlanInfo()
+    assert qx.lib().qx_plan_sdpa_f32(qx.ctypes.byref(info), 1, 10, 64, 1.0, 2) == qx.ERR_INVALID_ARG
+    assert qx.lib().qx_plan_sdpa_f32(None, 1, 10, 64, 1.0, 0) == qx.ERR_INVALID_ARG
+    for args in ((0, 10, 64), (2, 0, 64), (2, 10, 0)):
+        assert qx.plan_sdpa_f32(*args)["kernels"] == 0
+
+
 def test_null_pointer_validation_before_device():
     # Validation returns before any HIP call, so this runs without a GPU.
     L = qx.lib()

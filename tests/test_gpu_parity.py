@@ -702,6 +702,74 @@ def test_workload_attn_full_oracle():
     same(O, orc.attn_i32(Q, K, V))
 
 
+# ---------------------------------------------------------------------------
+# Softmax attention over heads (FP32): normwise 1e-4 against the float64 oracle
+# ---------------------------------------------------------------------------
+SDPA_CASES = [  # BH, L, d, scale, causal, input sigma (None: d^-1/4, unit-variance scores)
+    (1, 1, 64, 1.0, False, None), (1, 1, 64, 1.0, True, None), (2, 31, 32, 1.0, False, None),
+    (3, 100, 64, 0.125, True, 1.0), (2, 257, 64, 1.0, False, 1.0), (4, 300, 128, 0.088, True, None),
+    (2, 77, 96, 0.5, False, None), (2, 100, 40, 0.3, True, None), (1, 50, 1, 2.0, False, 1.0),
+    (3, 129, 17, -0.7, True, None), (1, 4096, 64, 1.0, True, None), (1, 2000, 128, 0.1, False, 1.0),
+    (40, 130, 64, 1.0, True, None), (2, 64, 64, 0.0, False, 1.0), (5, 33, 100, 0.1, False, None),
+]
+
+
+def sdpa_inputs(BH, L, d, sigma, seed):
+    rng = np.random.default_rng(seed)
+    s = d ** -0.25 if sigma is None else sigma
+    return tuple((rng.standard_normal((BH, L, d)) * s).astype(np.float32) for _ in range(3))
+
+
+@pytest.mark.parametrize("case", SDPA_CASES)
+def test_sdpa_f32(case):
+    BH, L, d, scale, causal, sigma = case
+    _say(f"[sdpa] BH={BH} L={L} d={d} scale={scale} causal={causal}")
+    Q, K, V = sdpa_inputs(BH, L, d, sigma, BH * 1000 + L + d)
+    plan = qx.plan_sdpa_f32(BH, L, d, scale, causal)
+    O = host(qx.sdpa_f32(dev(Q), dev(K), dev(V), scale, causal))
+    R = orc.sdpa_f64(Q, K, V, scale, causal)
+    err = normwise(O, R)
+    assert err <= 1e-4, (err, plan)
+    # key splits merge in a fixed order: a second run is bit-identical
+    O2 = host(qx.sdpa_f32(dev(Q), dev(K), dev(V), scale, causal))
+    assert np.array_equal(O, O2)
+
+
+def test_sdpa_executor_oneshot_and_errors():
+    BH, L, d = 3, 200, 64
+    Q, K, V = sdpa_inputs(BH, L, d, None, 5)
+    with qx.Executor.sdpa_f32(BH, L, d, 1.0, True) as ex:
+        assert ex.plan()["kernels"] == 2
+        O = run_exec(ex, (Q, K, V))
+    assert np.array_equal(O, host(qx.sdpa_f32(dev(Q), dev(K), dev(V), 1.0, True)))
+    # [B][H][L][d] is BH = B*H heads
+    O4 = host(qx.sdpa_f32(*(dev(a.reshape(1, BH, L, d)) for a in (Q, K, V)), 1.0, True))
+    assert np.array_equal(O4.reshape(BH, L, d), O)
+    # empty sizes are no-ops; a NULL operand of a non-empty call is refused
+    e = torch.empty((0, 5, 64), dtype=torch.float32, device="cuda")
+    assert qx.sdpa_f32(e, e, e).shape == (0, 5, 64)
+    assert qx.lib().sdpa_f32(None, None, None, None, 1, 4, 64, 1.0, 0, None) == qx.ERR_INVALID_ARG
+    assert qx.lib().sdpa_f32(None, None, None, None, 0, 4, 64, 1.0, 0, None) == 0
+
+
+@pytest.mark.parametrize("name,heads", [("sdpa_f32_32x4096x64", (0, 13, 31)),
+                                        ("sdpa_f32_causal_32x4096x64", (0, 31))])
+def test_workload_sdpa_sampled_heads(name, heads):
+    w = WORKLOADS[name]
+    d = w.dims
+    _say(f"[{name}] generate")
+    Q, K, V = w.generate()
+    with qx.Executor.sdpa_f32(d["BH"], d["L"], d["d"], d["scale"], bool(d["causal"])) as ex:
+        O = run_exec(ex, (Q, K, V))
+    _say(f"[{name}] heads {heads} against the oracle")
+    hs = list(heads)
+    R = orc.sdpa_f64(Q[hs], K[hs], V[hs], d["scale"], bool(d["causal"]))
+    err = normwise(O[hs], R)
+    _say(f"[{name}] normwise error {err:.3e}")
+    assert err <= 1e-4
+    assert np.isfinite(O).all()
+
+
 @pytest.mark.parametrize("name", ["gemm_i16_8192", "gemm_i16_64x2048"])
 def test_workload_large_gemm(name):
     w = WORKLOADS[name]
