@@ -21,6 +21,8 @@
 // global side (each lane fetches the chunk that belongs at its LDS slot).
 #include <algorithm>
 
+#include <type_traits>
+
 #include "qx_internal.h"
 
 namespace qx {
@@ -610,6 +612,85 @@ __global__ __launch_bounds__(NW * 64) void k_gemm_nt(const GemmParams p) {
 
     const int ktiles = p.K / BK;   // K is padded to whole tiles
     const int CT = p.chunk_tiles;
+    if constexpr (NW == 8) {
+        // Ping-pong: the waves form two groups, one wave of each per SIMD.
+        // Phases alternate between barriers; in every phase one group reads
+        // a whole tile's fragments from LDS and issues its share of the DMA
+        // while the other runs the MFMAs of the tile it read in the phase
+        // before, so the matrix cores and the LDS work side by side instead
+        // of in turns.  Group 1 runs one phase behind group 0:
+        //   phase 2t:   group 0 reads tile t      group 1 computes tile t-1
+        //   phase 2t+1: group 0 computes tile t   group 1 reads tile t
+        // Tile u is issued by each wave in its read phase of tile u-2 (tiles
+        // 0 and 1 before the loop) into the stage of tile u-3, which both
+        // groups finished reading by then; it must have landed before phase
+        // 2u, so every wave ends phase 2t+1 with tile t+1 complete.
+        constexpr int KS = BK / 16;
+        // s_waitcnt immediates: vmcnt(n) with lgkmcnt(0)
+        constexpr unsigned WAIT_VM_LPT = (LPT & 15) | ((LPT >> 4) << 14) | 0x0070;
+        constexpr unsigned WAIT_VM_0 = 0x0070;
+        const int grp = wave >> 2;
+        // a phase boundary: no instruction moves across it
+        auto phase_end = [] {
+            __builtin_amdgcn_sched_barrier(0);
+            __syncthreads();
+            __builtin_amdgcn_sched_barrier(0);
+        };
+        h8 fa[KS][TM], fb[KS][TN];
+        issue(0);
+        if (1 < ktiles) {
+            issue(1);
+            __builtin_amdgcn_s_waitcnt(WAIT_VM_LPT);
+        } else {
+            __builtin_amdgcn_s_waitcnt(WAIT_VM_0);
+        }
+        phase_end();
+        if (grp == 1) phase_end();
+        // One tile: its read phase, then its compute phase.  ZERO (the first
+        // tile of a flush chunk) starts the fp32 accumulators from zero; the
+        // last tile of a chunk adds them into the int32 accumulators.
+        auto ptile = [&](int tc, auto zero, bool flush) {
+            constexpr bool ZERO = decltype(zero)::value;
+            const int s = tc % STAGES;
+#pragma unroll
+            for (int ks = 0; ks < KS; ++ks) ldf(s, ks, fa[ks], fb[ks]);
+            if (tc + 2 < ktiles) issue(tc + 2);
+            if (grp == 1) {
+                if (tc + 2 < ktiles) __builtin_amdgcn_s_waitcnt(WAIT_VM_LPT);
+                else __builtin_amdgcn_s_waitcnt(WAIT_VM_0);
+            } else {
+                __builtin_amdgcn_s_waitcnt(0xC07F);   // lgkmcnt(0)
+            }
+            phase_end();
+#pragma unroll
+            for (int ks = 0; ks < KS; ++ks)
+#pragma unroll
+                for (int i = 0; i < TM; ++i)
+#pragma unroll
+                    for (int j = 0; j < TN; ++j)
+                        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_f16(fa[ks][i], fb[ks][j],
+                                        (ZERO && ks == 0) ? f16x{} : acc[i][j], 0, 0, 0);
+            if (flush) {
+#pragma unroll
+                for (int i = 0; i < TM; ++i)
+#pragma unroll
+                    for (int j = 0; j < TN; ++j)
+#pragma unroll
+                        for (int r = 0; r < 16; ++r) iacc[i][j][r] += (uint32_t)(int32_t)acc[i][j][r];
+            }
+            if (grp == 0) {
+                if (tc + 2 < ktiles) __builtin_amdgcn_s_waitcnt(WAIT_VM_LPT);
+                else __builtin_amdgcn_s_waitcnt(WAIT_VM_0);
+            }
+            phase_end();
+        };
+        for (int tc = 0; tc < ktiles;) {
+            const int cend = min(tc + CT, ktiles);
+            ptile(tc, std::true_type{}, tc + 1 == cend);
+            for (++tc; tc < cend; ++tc) ptile(tc, std::false_type{}, tc + 1 == cend);
+        }
+        if (grp == 0) phase_end();
+    } else {
 #pragma unroll
     for (int s = 0; s < STAGES - 1; ++s)
         if (s < ktiles) issue(s);
@@ -631,6 +712,7 @@ __global__ __launch_bounds__(NW * 64) void k_gemm_nt(const GemmParams p) {
             for (int j = 0; j < TN; ++j)
 #pragma unroll
                 for (int r = 0; r < 16; ++r) iacc[i][j][r] += (uint32_t)(int32_t)acc[i][j][r];
+    }
     }
 
     // 32x32 accumulator layout: lane holds column (lane & 31), rows
