@@ -37,8 +37,8 @@ PEAK = {"f16": 2500.0, "i8": 5000.0, "f32": 157.3, "hbm": 8000.0}  # TFLOP/s, TO
 # the kernel has changed since.
 TRAFFIC = {
     "kernel": "gemm_nt_128x256",
-    "kernel_sha256": "5f342e1d9dced801038c2bd96e08bc3bf5ee1cf5ea44d73d72222c7e7f6ae5e2",
-    "read_bytes": 2149179579,     # FETCH_SIZE 1049435 KiB x 2.0 (copy: 524304 KiB per GiB read)
+    "kernel_sha256": "f56454229bbabb49d43ec5f701e9ce545f0e91f2e26f5421966c41662a23ed84",
+    "read_bytes": 2148625373,     # FETCH_SIZE 1049166 KiB x 2.0 (copy: 524304 KiB per GiB read)
     "write_bytes": 268435456,     # WRITE_SIZE 262144 KiB x 1.0 (copy: 1048576 KiB per GiB written)
 }
 KERNEL_SRC = os.path.join(ROOT, "paper_2606_09905_amd", "csrc", "k_gemm_nt.hip")
