@@ -30,9 +30,16 @@ FLAGS = [
 ]
 
 
+# Per-source additions.  The attention kernels keep their MFMA accumulators
+# in ordinary VGPRs: the online softmax rescales the output accumulators
+# with vector ALU multiplies, and accumulators placed in AGPRs would be
+# copied out and back around every key block.
+EXTRA = {"k_attn.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"]}
+
+
 def _compile(src: str) -> str:
     obj = os.path.join(BUILD_DIR, os.path.basename(src) + ".o")
-    cmd = [HIPCC, *FLAGS, "-c", os.path.join(CSRC, src), "-o", obj]
+    cmd = [HIPCC, *FLAGS, *EXTRA.get(src, []), "-c", os.path.join(CSRC, src), "-o", obj]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError(f"hipcc failed for {src}:\n{r.stdout}\n{r.stderr}")

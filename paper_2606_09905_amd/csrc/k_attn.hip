@@ -331,11 +331,14 @@ __global__ __launch_bounds__(AT) void k_sdpa_f32(const SdpaParams p) {
     };
 
     const int q = q0 + l32;           // this lane's query in the S^T layout
+    // Q is taken pre-multiplied by c = scale*log2(e), so the scores come out
+    // of the MFMAs already in the base-2 exponent domain.
+    const float c = p.c;
     float qf[HALF];
 #pragma unroll
     for (int t = 0; t < HALF; t += 4) {
         const f4 v = q < p.L ? ld4(Q, q, (HALF * h + t) / 4) : f4{};
-        qf[t] = v[0]; qf[t + 1] = v[1]; qf[t + 2] = v[2]; qf[t + 3] = v[3];
+        qf[t] = v[0] * c; qf[t + 1] = v[1] * c; qf[t + 2] = v[2] * c; qf[t + 3] = v[3] * c;
     }
     f16x o[NTO];
 #pragma unroll
@@ -363,7 +366,6 @@ __global__ __launch_bounds__(AT) void k_sdpa_f32(const SdpaParams p) {
         }
     };
 
-    const float c = p.c;
     if (key_lo < key_hi) load(key_lo);
     for (int kb = key_lo; kb < key_hi; kb += AKB) {
         __syncthreads();
@@ -379,23 +381,31 @@ __global__ __launch_bounds__(AT) void k_sdpa_f32(const SdpaParams p) {
             for (int e = 0; e < 4; ++e)
                 s = __builtin_amdgcn_mfma_f32_32x32x2f32(kv[e], qf[t + e], s, 0, 0, 0);
         }
-        // register r holds key kb + 8*(r/4) + 4*h + r%4
-        // keys at or past key_lim are masked for this lane's query
-        const int key_lim = p.causal ? min(key_hi, q + 1) : key_hi;
-        const int kl = key_lim - kb - 4 * h;    // register r is kept iff 8*(r/4) + r%4 < kl
-        float mx = -INFINITY;
+        // Register r holds key kb + 8*(r/4) + 4*h + r%4.  In a block that
+        // reaches past key_hi or (causal) past a query of this wave, keys at
+        // or past key_lim are set to -inf, whose exponential is 0.
+        if (kb + AKB > key_hi || (p.causal && kb + AKB - 1 > q0)) {
+            const int key_lim = p.causal ? min(key_hi, q + 1) : key_hi;
+            const int kl = key_lim - kb - 4 * h;    // register r is kept iff 8*(r/4) + r%4 < kl
 #pragma unroll
-        for (int r = 0; r < 16; ++r)
-            if (8 * (r >> 2) + (r & 3) < kl) mx = fmaxf(mx, s[r] * c);
+            for (int r = 0; r < 16; ++r)
+                if (8 * (r >> 2) + (r & 3) >= kl) s[r] = -INFINITY;
+        }
+        float mx = fmaxf(fmaxf(s[0], s[1]), s[2]);
+#pragma unroll
+        for (int r = 3; r < 15; r += 2) mx = fmaxf(fmaxf(mx, s[r]), s[r + 1]);
+        mx = fmaxf(mx, s[15]);
         mx = fmaxf(mx, __shfl_xor(mx, 32));
         const float m_new = fmaxf(m, mx);
         const float m_use = m_new == -INFINITY ? 0.f : m_new;
-        const float alpha = exp2f(m - m_use);
+        // v_exp_f32 directly: arguments are <= 0 here, results below 2^-126
+        // flush to 0, which no sum of a row with its maximum term 1 can see
+        const float alpha = __builtin_amdgcn_exp2f(m - m_use);
         m = m_new;
         float ps = 0.f;
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
-            s[r] = 8 * (r >> 2) + (r & 3) < kl ? exp2f(fmaf(s[r], c, -m_use)) : 0.f;
+            s[r] = __builtin_amdgcn_exp2f(s[r] - m_use);
             ps += s[r];
         }
         lsum = lsum * alpha + ps;
