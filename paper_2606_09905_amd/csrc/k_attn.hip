@@ -293,8 +293,10 @@ __global__ __launch_bounds__(AT) void k_sdpa_f32(const SdpaParams p) {
     constexpr int HALF = D / 2;
     constexpr int NTO = D / 32;
     constexpr int LD4 = AKB * D / 4 / AT;
-    __shared__ float Ks[AKB][DP];
-    __shared__ float Vs[AKB][DP];
+    // two LDS buffers: block j is staged into buffer j&1 while the other
+    // holds block j-1, so one barrier per block suffices
+    __shared__ float Ksb[2][AKB][DP];
+    __shared__ float Vsb[2][AKB][DP];
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, h = lane >> 5, l32 = lane & 31;
     // Under the mask a query block's work grows with its index: the dispatch
@@ -357,21 +359,25 @@ __global__ __launch_bounds__(AT) void k_sdpa_f32(const SdpaParams p) {
             rv[i] = in ? ld4(Vp, key, c4) : f4{};
         }
     };
-    auto stash = [&]() {
+    auto stash = [&](int buf) {
 #pragma unroll
         for (int i = 0; i < LD4; ++i) {
             const int v = tid + AT * i, row = v / (D / 4), c4 = v % (D / 4);
-            *(f4*)&Ks[row][c4 * 4] = rk[i];
-            *(f4*)&Vs[row][c4 * 4] = rv[i];
+            *(f4*)&Ksb[buf][row][c4 * 4] = rk[i];
+            *(f4*)&Vsb[buf][row][c4 * 4] = rv[i];
         }
     };
 
     if (key_lo < key_hi) load(key_lo);
-    for (int kb = key_lo; kb < key_hi; kb += AKB) {
-        __syncthreads();
-        stash();
+    int buf = 0;
+    for (int kb = key_lo; kb < key_hi; kb += AKB, buf ^= 1) {
+        // Buffer buf was last read two blocks ago: every wave finished that
+        // block before the previous iteration's barrier.
+        stash(buf);
         __syncthreads();
         if (kb + AKB < key_hi) load(kb + AKB);
+        float (&Ks)[AKB][DP] = Ksb[buf];
+        float (&Vs)[AKB][DP] = Vsb[buf];
         if (p.causal && kb > q0 + AQW - 1) continue;   // every key after every query of this wave
         f16x s = f16x{};
 #pragma unroll
