@@ -956,9 +956,12 @@ bool build_gemm_mfma(int32_t route, const GemmParams& p, int batch, LaunchRec* r
 // int8 NT route: 128x128 workgroup tiles (four 64x64 waves) when they fill
 // the chip, else 64x64 (four 32x32 waves).
 void i8nt_tile_shape(int32_t route, int64_t M, int64_t N, int64_t batch, int* bm, int* bn) {
-    (void)route;
     const int64_t big = ((M + 127) / 128) * ((N + 127) / 128) * batch;
-    *bm = *bn = big >= 128 ? 128 : 64;
+    // smul24 keeps four accumulator groups: a 128x128 tile needs all 512
+    // registers of a lane (one wave per SIMD), so it takes 64x64 tiles (two
+    // workgroups per CU) unless there are tiles for several rounds
+    const int64_t min_big = route == R_S24_I8LIMB ? 1024 : 128;
+    *bm = *bn = big >= min_big ? 128 : 64;
 }
 
 template <class S>
