@@ -90,6 +90,8 @@ def parse():
     ap.add_argument("--all", action="store_true", help="also measure every workload")
     ap.add_argument("--all-out", default=os.path.join(ROOT, "gpurun_out", "bench_all.json"))
     ap.add_argument("--no-cpu", action="store_true", help="skip the oracle CPU baseline")
+    ap.add_argument("--oracle-all", action="store_true",
+                    help="time the CPU oracle on every workload (host only) and exit")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run two 1 GiB device-to-device copies (HBM counter calibration)")
     ap.add_argument("--cpu-rows", type=int, default=8192,
@@ -187,8 +189,74 @@ def cpu_baseline(w, rows):
     }
 
 
+def oracle_timings(workloads):
+    """Wall time of the CPU oracle on every workload, on the host cores: the
+    whole workload where it finishes in seconds, else a stated sample (rows of
+    A, images, heads).  Rates are in the workload's unit (GOPS, or GiB/s of
+    input for the memory-bound rows)."""
+    from oracle import oracle as orc
+    orc.gemm_i16i32(np.zeros((1, 1, 1), np.int16), np.zeros((1, 1, 1), np.int16))   # build/load
+    cores = int(os.environ.get("OMP_NUM_THREADS", 0)) or len(os.sched_getaffinity(0))
+    out = {}
+    for name, w in workloads.items():
+        d = w.dims
+        inputs = w.generate()
+        frac, sample = 1.0, "whole workload"
+        if w.op == "gemm_i16i32":
+            A, B = inputs
+            budget = 1 << 34                      # multiply-adds the sample may take
+            per_batch = d["M"] * d["N"] * d["K"]
+            nb = max(1, min(d["batch"], budget // per_batch))
+            rows = d["M"] if per_batch <= budget else max(1, budget // (d["N"] * d["K"]))
+            if rows < d["M"] or nb < d["batch"]:
+                sample = f"{rows} of {d['M']} rows of A in {nb} of {d['batch']} batches"
+            frac = rows * nb / (d["M"] * d["batch"])
+            fn = lambda: orc.gemm_i16i32(np.ascontiguousarray(A[:nb, :rows]), B[:nb])
+        elif w.op == "gemm_i32_s24":
+            A, B = inputs
+            fn = lambda: orc.gemm_i32_s24(A, B)
+        elif w.op in ("conv2d", "conv2d_i32", "conv2d_f32"):
+            x, wt = inputs
+            f = {"conv2d": orc.conv2d_direct, "conv2d_i32": orc.conv2d_s24, "conv2d_f32": orc.conv2d_f64}[w.op]
+            fn = lambda: f(x, wt, d["stride"], d["pad"])
+        elif w.op == "attn_f32":
+            fn = lambda: orc.attn_f64(*inputs)
+        elif w.op == "attn_i32":
+            fn = lambda: orc.attn_i32(*inputs)
+        elif w.op in ("minmax_i32", "minmax_i16"):
+            fn = lambda: orc.minmax(inputs[0])
+        elif w.op == "avgpool_i32":
+            fn = lambda: orc.avgpool2_i32(inputs[0])
+        elif w.op == "maxpool_f32":
+            fn = lambda: orc.maxpool2_f32(inputs[0])
+        elif w.op == "lenet_i32":
+            fn = lambda: orc.lenet_i32(*inputs)
+        elif w.op == "sdpa_f32":
+            Q, K, V = inputs
+            frac, sample = 2 / d["BH"], f"2 of {d['BH']} heads"
+            fn = lambda: orc.sdpa_f64(Q[:2], K[:2], V[:2], d["scale"], bool(d["causal"]))
+        else:
+            continue
+        t0 = time.perf_counter()
+        fn()
+        dt = time.perf_counter() - t0
+        if w.ops:
+            rate, unit = w.ops * frac / dt / 1e9, "GOPS"
+        else:
+            rate, unit = w.in_bytes * frac / dt / 2 ** 30, "GiB/s"
+        out[name] = {"value": rate, "unit": unit, "seconds": dt, "sample": sample, "cores": cores}
+        print(f"[oracle] {name}: {rate:.3g} {unit} ({dt:.2f} s, {sample}, {cores} threads)",
+              file=sys.stderr, flush=True)
+    return out
+
+
 def main():
     args = parse()
+    if args.oracle_all:
+        from paper_2606_09905_amd.workloads import WORKLOADS
+        res = oracle_timings(WORKLOADS)
+        print(json.dumps({"oracle": res}), flush=True)
+        return
     if args.gpus != 1:
         print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1",
                           "n_gpus": args.gpus}), flush=True)
