@@ -303,10 +303,10 @@ def main():
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        # the arithmetic the contraction runs in: fp16 products summed exactly
-        # in fp32 per chunk, chunks added in int32 (the result is the exact
-        # int32 GEMM of the int16 inputs)
-        "dtype": {"f16_exact": "f16", "s24_i8limb": "i8", "i8_direct": "i8", "i8_karatsuba": "i8",
+        # the arithmetic the contraction runs in: bf16 (bounds <= 256) or fp16
+        # products summed exactly in fp32 per chunk, chunks added in int32
+        # (the result is the exact int32 GEMM of the int16 inputs)
+        "dtype": {"f16_exact": "bf16" if r["plan"].get("operand_format") == 1 else "f16", "s24_i8limb": "i8", "i8_direct": "i8", "i8_karatsuba": "i8",
                   "i8_offset4": "i8", "attn_f32_mfma": "f32", "attn_i32_mfma": "i8",
                   "f32_mfma": "f32", "f32_valu": "f32", "attn_f32_valu": "f32"}.get(route, "i32"),
         "data": "synthetic",

@@ -68,7 +68,9 @@ typedef enum { QX_DT_F32 = 0, QX_DT_I32 = 1 } qx_attn_dtype;
  *  I8_DIRECT    operands in [-127, 127]: one int8 MFMA product per multiply-add.
  *  F16_EXACT    |a|, |b| <= 2048 and chunk*|a|max*|b|max <= 2^24: fp16 MFMA with
  *               fp32 partial sums over `chunk` K-steps (every partial is an exactly
- *               representable integer), flushed into int32.
+ *               representable integer), flushed into int32.  Large problems whose
+ *               bounds are both <= 256 encode the operands as bf16 instead (also
+ *               exact there) and run the bf16 MFMA; operand_format reports it.
  *  I8_KARATSUBA operands in [-8127, 8127]: balanced base-128 limbs h, l and h+l,
  *               three int8 MFMA products.
  *  I8_OFFSET4   any int16: offset base-256 limbs, four int8 MFMA products plus a
@@ -102,6 +104,9 @@ typedef struct {
     int32_t tile_m, tile_n, tile_k;  /* workgroup tile of the main kernel */
     int32_t kernels;          /* kernel launches per run */
     int32_t exact_no_wrap;    /* 1: contract proves |result| < 2^31; 0: defined mod 2^32 */
+    int32_t operand_format;   /* F16_EXACT with encoded operands: 1 = bf16 (both bounds
+                                 <= 256, exact in bf16), 0 = fp16 (or not applicable) */
+    int32_t reserved;         /* 0 */
     int64_t workspace_bytes;  /* device workspace owned by the plan */
 } qx_plan_info;
 

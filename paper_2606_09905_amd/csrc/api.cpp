@@ -238,6 +238,11 @@ qx_status plan_int_gemm(const GemmSpec& s, Plan* pl, uint64_t* ws_used) {
 
     if (s.allow_nt && use_nt(route, f16_chunk(s.ba, s.bb), s.M, s.N, s.K, s.batch)) {
         const int64_t chunk = f16_chunk(s.ba, s.bb);
+        // Operands within [-256, 256] are exact in bf16 as well (eight
+        // significant bits); the bf16 matrix cores sustain a slightly higher
+        // clock on such data, so the encoders write bf16 then.
+        const int32_t bf = std::max(s.ba, s.bb) <= 256 ? 1 : 0;
+        info.operand_format = bf;
         int bm, bn;
         nt_tile_shape(s.M, s.N, s.batch, &bm, &bn);
         // A and B^T are padded to whole 128-row / 256-column tiles so that
@@ -267,6 +272,7 @@ qx_status plan_int_gemm(const GemmSpec& s, Plan* pl, uint64_t* ws_used) {
             ea.Mp = (int32_t)Mp; ea.Np = 0; ea.Kp = (int32_t)Kp;
             ea.ld_src = (int32_t)s.lda; ea.batch = (int32_t)cnt;
             ea.vec = (s.lda % 8 == 0 && s.sA % 8 == 0) ? 1 : 0;
+            ea.bf16 = bf;
             LaunchRec r;
             build_enc_a(ea, &r);
             r.bind(offsetof(EncParams, src), s.a_bind, 2 * (uint64_t)(b0 * s.sA));
@@ -283,6 +289,7 @@ qx_status plan_int_gemm(const GemmSpec& s, Plan* pl, uint64_t* ws_used) {
             eb.Mp = 0; eb.Np = (int32_t)nwp; eb.Kp = (int32_t)Kp;
             eb.ld_src = (int32_t)s.ldb; eb.batch = (int32_t)cnt;
             eb.vec = (s.ldb % 8 == 0 && s.sB % 8 == 0 && n0 % 8 == 0) ? 1 : 0;
+            eb.bf16 = bf;
             LaunchRec r2;
             build_enc_bt(eb, &r2);
             const uint64_t bt_add = b_off + 2 * (uint64_t)(b0 * Np * Kp + n0 * Kp);
@@ -294,6 +301,7 @@ qx_status plan_int_gemm(const GemmSpec& s, Plan* pl, uint64_t* ws_used) {
             g.lda = (int32_t)Kp; g.ldb = (int32_t)Kp; g.ldc = (int32_t)s.ldc;
             g.out_mode = s.out_mode; g.hw = s.hw; g.b_mode = B_KN;
             g.chunk_tiles = (int32_t)(chunk / 64);
+            g.bf16 = bf;
             LaunchRec r3;
             build_gemm_nt(g, (int)cnt, &r3);
             r3.bind(offsetof(GemmParams, A), BIND_WS, a_off + 2 * (uint64_t)(b0 * Mp * Kp));

@@ -37,16 +37,33 @@ typedef float f4v __attribute__((ext_vector_type(4)));
 // ===========================================================================
 // Stage 1: encoders
 // ===========================================================================
-// 8 int16 -> 8 fp16 (exact for |x| <= 2048).
+typedef __bf16 b8v __attribute__((ext_vector_type(8)));
+
+// 8 int16 -> 8 fp16 (exact for |x| <= 2048), or with BF 8 bf16 (exact for
+// |x| <= 256: eight significant bits) carried in the same 16-bit lanes.
+template <bool BF>
 __device__ __forceinline__ h8 to_h8(s8v v) {
-    h8 o;
+    if constexpr (BF) {
+        b8v o;
 #pragma unroll
-    for (int e = 0; e < 8; ++e) o[e] = (_Float16)v[e];
-    return o;
+        for (int e = 0; e < 8; ++e) o[e] = (__bf16)(float)v[e];
+        return __builtin_bit_cast(h8, o);
+    } else {
+        h8 o;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) o[e] = (_Float16)v[e];
+        return o;
+    }
+}
+template <bool BF>
+__device__ __forceinline__ _Float16 to_h1(int v) {
+    if constexpr (BF) return __builtin_bit_cast(_Float16, (__bf16)(float)v);
+    else return (_Float16)v;
 }
 
-// A [batch][M][lda] int16 -> A16 [batch][Mp][Kp] fp16; one thread = 8 k,
-// four vectors per thread.
+// A [batch][M][lda] int16 -> A16 [batch][Mp][Kp] fp16 (bf16 with BF); one
+// thread = 8 k, four vectors per thread.
+template <bool BF>
 __global__ __launch_bounds__(256) void k_enc_a(const EncParams p) {
     const int kv = p.Kp / 8;
     const int64_t per_b = (int64_t)p.Mp * kv;
@@ -61,18 +78,19 @@ __global__ __launch_bounds__(256) void k_enc_a(const EncParams p) {
         const int16_t* src = (const int16_t*)p.src + b * p.s_src + (int64_t)m * p.ld_src + k0;
         h8 out;
         if (p.vec && m < p.M && k0 + 8 <= p.K) {
-            out = to_h8(*(const s8v*)src);
+            out = to_h8<BF>(*(const s8v*)src);
         } else {
 #pragma unroll
-            for (int e = 0; e < 8; ++e)
-                out[e] = (m < p.M && k0 + e < p.K) ? (_Float16)src[e] : (_Float16)0.0f;
+            for (int e = 0; e < 8; ++e) out[e] = to_h1<BF>((m < p.M && k0 + e < p.K) ? src[e] : 0);
         }
         *(h8*)((_Float16*)p.dst + b * p.s_dst + (int64_t)m * p.Kp + k0) = out;
     }
 }
 
-// B [batch][K][ldb] int16 -> BT16 [batch][Np][Kp] fp16 through a 64(k) x
-// 128(n) LDS transpose; 16-byte reads along n and 16-byte writes along k.
+// B [batch][K][ldb] int16 -> BT16 [batch][Np][Kp] fp16 (bf16 with BF)
+// through a 64(k) x 64(n) LDS transpose; 16-byte reads along n and 16-byte
+// writes along k.
+template <bool BF>
 __global__ __launch_bounds__(256) void k_enc_bt(const EncParams p) {
     // 64 x 64 blocks keep the LDS footprint at 9 KB, so these workgroups can
     // share a CU with a resident 144 KB contraction workgroup.
@@ -87,10 +105,10 @@ __global__ __launch_bounds__(256) void k_enc_bt(const EncParams p) {
         const int16_t* s = src + (int64_t)k * p.ld_src + n;
         h8 h;
         if (p.vec && k < p.K && n + 8 <= p.N) {
-            h = to_h8(*(const s8v*)s);
+            h = to_h8<BF>(*(const s8v*)s);
         } else {
 #pragma unroll
-            for (int e = 0; e < 8; ++e) h[e] = (k < p.K && n + e < p.N) ? (_Float16)s[e] : (_Float16)0.0f;
+            for (int e = 0; e < 8; ++e) h[e] = to_h1<BF>((k < p.K && n + e < p.N) ? s[e] : 0);
         }
 #pragma unroll
         for (int e = 0; e < 8; ++e) t[nv + e][kk] = h[e];
@@ -465,7 +483,18 @@ __global__ __launch_bounds__(NW * 64) void k_gemm_nt_f32(const GemmParams p) {
     }
 }
 
-template <int BM, int BN, int NW, bool IMPL>
+// One 32x32x16 MFMA step of the fp16-exact route: fp16 operands, or bf16
+// ones (the same 16-bit lanes) with BF; fp32 accumulation either way.
+template <bool BF>
+__device__ __forceinline__ f16x mfma_h(h8 a, h8 b, f16x c) {
+    if constexpr (BF)
+        return __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(b8v, a), __builtin_bit_cast(b8v, b), c,
+                                                       0, 0, 0);
+    else
+        return __builtin_amdgcn_mfma_f32_32x32x16_f16(a, b, c, 0, 0, 0);
+}
+
+template <int BM, int BN, int NW, bool IMPL, bool BF>
 __global__ __launch_bounds__(NW * 64) void k_gemm_nt(const GemmParams p) {
     constexpr int BK = 64, KCH = 8, WM = 64, WN = 64;
     constexpr int TM = WM / 32, TN = WN / 32;
@@ -604,8 +633,7 @@ __global__ __launch_bounds__(NW * 64) void k_gemm_nt(const GemmParams p) {
             for (int i = 0; i < TM; ++i)
 #pragma unroll
                 for (int j = 0; j < TN; ++j)
-                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_f16(fa[ks][i], fb[ks][j],
-                                    (first && ks == 0) ? f16x{} : acc[i][j], 0, 0, 0);
+                    acc[i][j] = mfma_h<BF>(fa[ks][i], fb[ks][j], (first && ks == 0) ? f16x{} : acc[i][j]);
             __builtin_amdgcn_s_setprio(0);
         }
     };
@@ -668,8 +696,7 @@ __global__ __launch_bounds__(NW * 64) void k_gemm_nt(const GemmParams p) {
                 for (int i = 0; i < TM; ++i)
 #pragma unroll
                     for (int j = 0; j < TN; ++j)
-                        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_f16(fa[ks][i], fb[ks][j],
-                                        (ZERO && ks == 0) ? f16x{} : acc[i][j], 0, 0, 0);
+                        acc[i][j] = mfma_h<BF>(fa[ks][i], fb[ks][j], (ZERO && ks == 0) ? f16x{} : acc[i][j]);
             if (flush) {
 #pragma unroll
                 for (int i = 0; i < TM; ++i)
@@ -736,7 +763,10 @@ __global__ __launch_bounds__(NW * 64) void k_gemm_nt(const GemmParams p) {
 #pragma unroll
             for (int r = 0; r < 16; ++r) {
                 const int gm = m0 + wm * WM + i * 32 + 8 * (r >> 2) + 4 * hh + (r & 3);
-                if (gm < p.M) C[(int64_t)gm * row_stride + col_off] = (int32_t)iacc[i][j][r];
+                // non-temporal: the output is not re-read here, and kept out
+                // of L2 it does not evict the operand tiles other
+                // workgroups are still streaming
+                if (gm < p.M) __builtin_nontemporal_store((int32_t)iacc[i][j][r], &C[(int64_t)gm * row_stride + col_off]);
             }
     }
 }
@@ -769,18 +799,22 @@ void build_gemm_nt(const GemmParams& p0, int batch, LaunchRec* rec) {
     p.tiles_n = (p.N + bn - 1) / bn;
     rec->grid = dim3((unsigned)(tiles_m * p.tiles_n), 1, (unsigned)batch);
     const bool impl = p.b_mode == B_NHWC;
+    const bool bf = p.bf16 != 0 && !impl;   // the conv image copy is fp16
     if (bn == 256) {
-        rec->fn = impl ? (const void*)k_gemm_nt<128, 256, 8, true> : (const void*)k_gemm_nt<128, 256, 8, false>;
+        rec->fn = impl ? (const void*)k_gemm_nt<128, 256, 8, true, false>
+                       : bf ? (const void*)k_gemm_nt<128, 256, 8, false, true> : (const void*)k_gemm_nt<128, 256, 8, false, false>;
         rec->block = dim3(512, 1, 1);
-        rec->name = impl ? "gemm_nt_conv_128x256" : "gemm_nt_128x256";
+        rec->name = impl ? "gemm_nt_conv_128x256" : bf ? "gemm_nt_bf16_128x256" : "gemm_nt_128x256";
     } else if (bm == 64) {
-        rec->fn = impl ? (const void*)k_gemm_nt<64, 128, 2, true> : (const void*)k_gemm_nt<64, 128, 2, false>;
+        rec->fn = impl ? (const void*)k_gemm_nt<64, 128, 2, true, false>
+                       : bf ? (const void*)k_gemm_nt<64, 128, 2, false, true> : (const void*)k_gemm_nt<64, 128, 2, false, false>;
         rec->block = dim3(128, 1, 1);
-        rec->name = impl ? "gemm_nt_conv_64x128" : "gemm_nt_64x128";
+        rec->name = impl ? "gemm_nt_conv_64x128" : bf ? "gemm_nt_bf16_64x128" : "gemm_nt_64x128";
     } else {
-        rec->fn = impl ? (const void*)k_gemm_nt<128, 128, 4, true> : (const void*)k_gemm_nt<128, 128, 4, false>;
+        rec->fn = impl ? (const void*)k_gemm_nt<128, 128, 4, true, false>
+                       : bf ? (const void*)k_gemm_nt<128, 128, 4, false, true> : (const void*)k_gemm_nt<128, 128, 4, false, false>;
         rec->block = dim3(256, 1, 1);
-        rec->name = impl ? "gemm_nt_conv_128x128" : "gemm_nt_128x128";
+        rec->name = impl ? "gemm_nt_conv_128x128" : bf ? "gemm_nt_bf16_128x128" : "gemm_nt_128x128";
     }
     rec->set_params(p);
 }
@@ -825,18 +859,18 @@ void build_conv_prep(const ConvPrepParams& p0, LaunchRec* rec) {
 
 void build_enc_a(const EncParams& p, LaunchRec* rec) {
     const int64_t n = (int64_t)p.batch * p.Mp * (p.Kp / 8);
-    rec->fn = (const void*)k_enc_a;
+    rec->fn = p.bf16 ? (const void*)k_enc_a<true> : (const void*)k_enc_a<false>;
     rec->grid = dim3((unsigned)((n + 1023) / 1024), 1, 1);
     rec->block = dim3(256, 1, 1);
-    rec->name = "enc_a_f16";
+    rec->name = p.bf16 ? "enc_a_bf16" : "enc_a_f16";
     rec->set_params(p);
 }
 
 void build_enc_bt(const EncParams& p, LaunchRec* rec) {
-    rec->fn = (const void*)k_enc_bt;
+    rec->fn = p.bf16 ? (const void*)k_enc_bt<true> : (const void*)k_enc_bt<false>;
     rec->grid = dim3((unsigned)(p.Np / 64), (unsigned)(p.Kp / 64), (unsigned)p.batch);
     rec->block = dim3(256, 1, 1);
-    rec->name = "enc_bt_f16";
+    rec->name = p.bf16 ? "enc_bt_bf16" : "enc_bt_f16";
     rec->set_params(p);
 }
 

@@ -50,6 +50,7 @@ struct GemmParams {
     int32_t hw;             // OUT_CONV: Ho*Wo
     int32_t tiles_n;        // number of N tiles (grid swizzle)
     int32_t cs_slices;      // colsum holds this many partial rows per batch
+    int32_t bf16;           // F16_EXACT NT contraction: operands are bf16 (|x| <= 256), else fp16
     int64_t plane_a;        // int8 NT route: bytes between limb planes of A and of B
     int64_t plane_b;
     ConvGeom g;
@@ -93,6 +94,7 @@ struct EncParams {
                             // of B (B^T encoder), of the values the split represents
     int32_t conv;           // B^T encoder: 1 = B is the im2col matrix of the NCHW image
                             // src with geometry g (gathered, never materialised)
+    int32_t bf16;           // fp16 encoders: write bf16 (exact for |x| <= 256) instead of fp16
     ConvGeom g;
 };
 
@@ -269,7 +271,7 @@ struct LaunchRec {
     dim3 grid{1, 1, 1};
     dim3 block{1, 1, 1};
     uint32_t shmem = 0;
-    alignas(16) unsigned char blob[256];
+    alignas(16) unsigned char blob[320];
     uint32_t blob_size = 0;
     Slot slots[8];
     int nslots = 0;

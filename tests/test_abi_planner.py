@@ -298,3 +298,17 @@ def test_null_pointer_validation_before_device():
     assert L.qx_exec_destroy(None) == qx.OK
     info = qx.PlanInfo()
     assert L.qx_exec_plan(None, ctypes.byref(info)) == qx.ERR_INVALID_ARG
+
+
+def test_bf16_operand_format_for_small_bounds():
+    # Large fp16-exact problems whose bounds are both <= 256 encode the
+    # operands as bf16 (integers up to 256 need eight significant bits);
+    # wider bounds, the register-staged small-problem kernel and the conv
+    # image copy stay fp16.
+    for ba, bb, fmt in ((256, 256, 1), (128, 256, 1), (1, 200, 1), (257, 256, 0), (300, 300, 0), (1024, 16, 0)):
+        p = qx.plan_gemm_i16i32(4096, 4096, 4096, 1, ba, bb)
+        assert p["route_name"] == "f16_exact" and p["operand_format"] == fmt, (ba, bb, p)
+    assert qx.plan_gemm_i16i32(64, 64, 64, 1, 256, 256)["operand_format"] == 0
+    assert qx.plan_conv2d(8, 64, 56, 56, 128, 3, 3, 1, 1, 256, 256)["operand_format"] == 0
+    # the chunk rule does not depend on the operand format
+    assert qx.plan_gemm_i16i32(4096, 4096, 4096, 1, 256, 256)["chunk"] == 256

@@ -201,6 +201,29 @@ def test_f16_exact_mixed_magnitudes():
     same(got, orc.gemm_i16i32(A, B))
 
 
+@pytest.mark.parametrize("K", [256, 4096, 4100])
+def test_bf16_operands_extremes(K):
+    # bf16-encoded operands (bounds <= 256): +-256, +-255 and +-1 in patterns
+    # that make full 256-element partial sums reach 2^24 exactly and mix
+    # 2^16-sized products with unit ones.
+    M = N = 64 if K >= 4096 else 1024
+    vals = np.array([-256, 256, -255, 255, -1, 1], np.int16)
+    rng = np.random.default_rng(K)
+    A = vals[rng.integers(0, 6, (1, M, K))]
+    B = vals[rng.integers(0, 6, (1, K, N))]
+    A[0, 0, :] = -256
+    B[0, :, 0] = -256
+    A[0, 1, :] = 256
+    B[0, :, 1] = -256
+    with qx.Executor.gemm_i16i32(M, N, K, 1, 256, 256) as ex:
+        plan = ex.plan()
+        assert plan["route_name"] == "f16_exact" and plan["operand_format"] == 1, plan
+        got = run_exec(ex, (A, B))
+    want = orc.gemm_i16i32(A, B)
+    assert want[0, 0, 0] == K * 65536 and want[0, 1, 1] == -K * 65536
+    same(got, want)
+
+
 def test_gemm_i16_oneshot_and_empty():
     rng = np.random.default_rng(3)
     A = rand_int(rng, (96, 80), 1024, np.int16)
@@ -395,7 +418,8 @@ def test_executor_profile_times_every_launch():
     with qx.Executor.gemm_i16i32(512, 768, 1024, 1, 256, 256) as ex:
         prof = ex.profile([ta, tb], out, reps=3)
     names = [n for n, _ in prof]
-    assert names[:2] == ["enc_a_f16", "enc_bt_f16"] and names[2].startswith("gemm_nt_")
+    # operands within [-256, 256]: the encoders write bf16
+    assert names[:2] == ["enc_a_bf16", "enc_bt_bf16"] and names[2].startswith("gemm_nt_bf16_")
     assert all(ms > 0 for _, ms in prof)
     same(host(out), orc.gemm_i16i32(A, B))
 
