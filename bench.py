@@ -36,22 +36,22 @@ PEAK = {"f16": 2500.0, "i8": 5000.0, "f32": 157.3, "hbm": 8000.0}  # TFLOP/s, TO
 # kernel's text is compared at run time and the figure is dropped (null) if
 # the kernel has changed since.
 TRAFFIC = {
-    "kernel": "gemm_nt_128x256",
-    "kernel_sha256": "f56454229bbabb49d43ec5f701e9ce545f0e91f2e26f5421966c41662a23ed84",
-    "read_bytes": 2148625373,     # FETCH_SIZE 1049166 KiB x 2.0 (copy: 524304 KiB per GiB read)
-    "write_bytes": 268435456,     # WRITE_SIZE 262144 KiB x 1.0 (copy: 1048576 KiB per GiB written)
+    "kernel": "gemm_nt_bf16_128x256",
+    "kernel_sha256": "7564f64eb892fd982e04e162505d4ee22a6bf620531cd24b4c9dd3d453e7d370",
+    "read_bytes": 2147642880,     # FETCH_SIZE 1048653.75 KiB x 2.0 (copy: 524304 KiB per GiB read)
+    "write_bytes": 268454894,     # WRITE_SIZE 262162.98 KiB x 1.0 (copy: 1048576 KiB per GiB written)
 }
 KERNEL_SRC = os.path.join(ROOT, "paper_2606_09905_amd", "csrc", "k_gemm_nt.hip")
 
 
 def contraction_sha256():
-    """SHA-256 of the fp16-exact contraction kernel's source text (the
-    k_gemm_nt template up to the builders)."""
+    """SHA-256 of the fp16-exact contraction kernel's source text (its MFMA
+    step helper and the k_gemm_nt template, up to the builders)."""
     import hashlib
     try:
         src = open(KERNEL_SRC).read()
-        sig = src.index("void k_gemm_nt(const GemmParams p)")
-        a = src.rindex("template <", 0, sig)
+        a = src.index("// One 32x32x16 MFMA step of the fp16-exact route")
+        src.index("void k_gemm_nt(const GemmParams p)", a)
         b = src.index("// Builders", a)
     except (OSError, ValueError):
         return None
