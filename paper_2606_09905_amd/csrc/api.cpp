@@ -1088,7 +1088,13 @@ qx_status plan_attn(Plan* pl, qx_attn_dtype dt, int64_t L, int64_t d, int32_t bo
         const int64_t qgroups = (L + 127) / 128;
         const int64_t kblocks = (L + 31) / 32;
         int64_t splits = std::min<int64_t>(std::max<int64_t>((512 + qgroups - 1) / qgroups, 1), kblocks);
-        const int64_t kps = ((kblocks + splits - 1) / splits) * 32;
+        int64_t kps = ((kblocks + splits - 1) / splits) * 32;
+        if (r == R_ATTN_I32_MFMA && (d == 32 || d == 64 || d == 128)) {
+            // resident splits: kps * d a multiple of 4096 (whole 1 KB loads
+            // per wave) and both int8 tiles within 48 KiB of LDS
+            const int64_t g = std::max<int64_t>(32, 4096 / d), cap = 24576 / d / g * g;
+            kps = std::min((kps + g - 1) / g * g, cap);
+        }
         splits = (L + kps - 1) / kps;
         AttnParams a{};
         a.L = (int32_t)L; a.d = (int32_t)d; a.splits = (int32_t)splits; a.keys_per_split = (int32_t)kps;
@@ -1115,6 +1121,31 @@ qx_status plan_attn(Plan* pl, qx_attn_dtype dt, int64_t L, int64_t d, int32_t bo
             } else {
                 pl->launches.push_back(rec);
             }
+        } else if (resident_attn_i32(d, kps)) {
+            // prep: int8 K rows and reordered V^T rows in the workspace, O
+            // cleared for split accumulation; then every workgroup loads its
+            // whole key split into LDS once (and forms the V column sums of
+            // the offset correction from it)
+            a.Lp = (int32_t)(splits * kps);
+            a.clear_o = splits > 1 ? 1 : 0;
+            a.prep_k = (int64_t)a.Lp * d / 16;
+            a.prep_v = d * (int64_t)a.Lp / 16;
+            const uint64_t v8_off = round_up((uint64_t)a.Lp * (uint64_t)d, 256);
+            ws = v8_off + (uint64_t)a.Lp * (uint64_t)d;
+            LaunchRec r1;
+            build_attn_i32_prep(a, &r1);
+            r1.bind(offsetof(AttnParams, K), BIND_IN1);
+            r1.bind(offsetof(AttnParams, V), BIND_IN2);
+            r1.bind(offsetof(AttnParams, O), BIND_OUT);
+            r1.bind(offsetof(AttnParams, k8), BIND_WS, 0);
+            r1.bind(offsetof(AttnParams, v8), BIND_WS, v8_off);
+            pl->launches.push_back(r1);
+            build_attn_i32r(a, &rec);
+            rec.bind(offsetof(AttnParams, Q), BIND_IN0);
+            rec.bind(offsetof(AttnParams, O), BIND_OUT);
+            rec.bind(offsetof(AttnParams, k8), BIND_WS, 0);
+            rec.bind(offsetof(AttnParams, v8), BIND_WS, v8_off);
+            pl->launches.push_back(rec);
         } else {
             // the output cleared for split accumulation, then the kernel
             // (which also forms the V column sums of the offset correction)

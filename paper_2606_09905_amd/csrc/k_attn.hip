@@ -275,6 +275,191 @@ __global__ __launch_bounds__(AT) void k_attn_i32(const AttnParams p) {
 }
 
 // ---------------------------------------------------------------------------
+// INT32 with resident key splits.  A prep launch writes int8 copies of K
+// (rows) and V^T (rows of keys, each 32-key block reordered as in the V
+// operand gather below) into the workspace and clears O; then each workgroup
+// loads its whole key split -- kps keys of K8 and of V8 -- into LDS with
+// direct-to-LDS loads in one batch, and runs every key block from LDS with
+// no further global loads or barriers.  The S^T tile and the limb split are
+// those of k_attn_i32.
+// ---------------------------------------------------------------------------
+template <int D>
+__global__ __launch_bounds__(AT) void k_attn_i32_prep(const AttnParams p) {
+    const int64_t i = (int64_t)blockIdx.x * AT + threadIdx.x;
+    const int32_t* Kp = (const int32_t*)p.K;
+    const int32_t* Vp = (const int32_t*)p.V;
+    auto pack4 = [](i4 v) -> uint32_t {
+        return ((uint32_t)v[0] & 0xFFu) | (((uint32_t)v[1] & 0xFFu) << 8) |
+               (((uint32_t)v[2] & 0xFFu) << 16) | ((uint32_t)v[3] << 24);
+    };
+    if (i < p.prep_k) {
+        // 16 consecutive d of one key row
+        const int key = (int)(i / (D / 16)), c0 = (int)(i % (D / 16)) * 16;
+        i4 o = i4{};
+        if (key < p.L) {
+#pragma unroll
+            for (int w = 0; w < 4; ++w) o[w] = (int)pack4(*(const i4*)(Kp + (int64_t)key * D + c0 + 4 * w));
+        }
+        *(i4*)((int8_t*)p.k8 + (int64_t)key * D + c0) = o;
+        return;
+    }
+    const int64_t iv = i - p.prep_k;
+    if (iv < p.prep_v) {
+        // column c, half-block hb (16 keys): byte 4w + e holds key
+        // 32*(hb/2) + 8w + 4*(hb%2) + e
+        const int c = (int)(iv % D);
+        const int hb = (int)(iv / D);
+        const int kb = (hb >> 1) * 32 + 4 * (hb & 1);
+        i4 o;
+#pragma unroll
+        for (int w = 0; w < 4; ++w) {
+            uint32_t x = 0;
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                const int key = kb + 8 * w + e;
+                const uint32_t v = key < p.L ? (uint32_t)Vp[(int64_t)key * D + c] : 0u;
+                x |= (v & 0xFFu) << (8 * e);
+            }
+            o[w] = (int)x;
+        }
+        *(i4*)((int8_t*)p.v8 + (int64_t)c * p.Lp + 16 * (int64_t)hb) = o;
+        return;
+    }
+    const int64_t io = iv - p.prep_v;
+    if (p.clear_o && io < (int64_t)p.L * D / 4) ((i4*)p.O)[io] = i4{};
+}
+
+// chunk swizzles of the resident tiles: K rows of D bytes (16 lanes of one
+// ds_read_b128 read 16 rows at one chunk: spread them over the 64 banks), and
+// V rows of kps bytes (swizzle within the largest power-of-two group of
+// chunks that divides the row, at most 16)
+template <int D>
+__device__ __forceinline__ int swz_k(int row) { return (row / (256 / D)) & (D / 16 - 1); }
+__device__ __forceinline__ int swz_v(int row, int vmask) { return row & vmask; }
+
+template <int D>
+__global__ __launch_bounds__(AT) void k_attn_i32r(const AttnParams p) {
+    constexpr int NTO = D / 32;
+    constexpr int CK = D / 16;                   // 16-byte chunks per K row
+    extern __shared__ __attribute__((aligned(16))) char smem[];
+    const int kps = p.keys_per_split;
+    char* Ks = smem;                             // [kps][D] int8
+    char* Vs = smem + (int64_t)kps * D;          // [D][kps] int8
+    __shared__ uint32_t vsum[D];
+
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, h = lane >> 5, l32 = lane & 31;
+    const int q0 = blockIdx.x * AQ + wave * AQW;
+    const int split = blockIdx.y;
+    const int key_lo = split * kps;
+    const int CV = kps / 16;                     // 16-byte chunks per V row
+    const int vmask = min(CV & -CV, 16) - 1;
+    const unsigned wave_u = __builtin_amdgcn_readfirstlane(wave);
+
+    // the split's K8 rows and V8 columns, 1 KB per wave instruction
+    {
+        const char* k8 = (const char*)p.k8 + (int64_t)key_lo * D;
+        const char* v8 = (const char*)p.v8 + key_lo;
+        const unsigned lds_k = (unsigned)(uintptr_t)Ks, lds_v = (unsigned)(uintptr_t)Vs;
+        const int nk = kps * D / 1024, nv = D * kps / 1024;
+        for (int I = (int)wave_u; I < nk; I += 4) {
+            const int q = I * 64 + lane, row = q / CK, pos = q % CK;
+            const unsigned off = (unsigned)(row * D + ((pos ^ swz_k<D>(row)) * 16));
+            asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dwordx4 %0, %1"
+                         :: "v"(off), "s"(k8), "s"(lds_k + I * 1024) : "memory", "m0");
+        }
+        for (int I = (int)wave_u; I < nv; I += 4) {
+            const int q = I * 64 + lane, row = q / CV, pos = q % CV;
+            const unsigned off = (unsigned)(row * p.Lp + ((pos ^ swz_v(row, vmask)) * 16));
+            asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dwordx4 %0, %1"
+                         :: "v"(off), "s"(v8), "s"(lds_v + I * 1024) : "memory", "m0");
+        }
+    }
+    const int32_t* Q = (const int32_t*)p.Q;
+    auto pack4 = [](i4 v) -> uint32_t {
+        return ((uint32_t)v[0] & 0xFFu) | (((uint32_t)v[1] & 0xFFu) << 8) |
+               (((uint32_t)v[2] & 0xFFu) << 16) | ((uint32_t)v[3] << 24);
+    };
+    i4 qf[NTO];
+    {
+        const int q = q0 + l32;
+#pragma unroll
+        for (int t = 0; t < NTO; ++t) {
+#pragma unroll
+            for (int w = 0; w < 4; ++w) {
+                const i4 v = (q < p.L) ? *(const i4*)(Q + (int64_t)q * D + 32 * t + 16 * h + 4 * w) : i4{};
+                qf[t][w] = (int)pack4(v);
+            }
+        }
+    }
+    if (tid < D) vsum[tid] = 0u;
+    __builtin_amdgcn_s_waitcnt(0x0070);          // vmcnt(0), lgkmcnt(0): the tiles have landed
+    __syncthreads();
+    // column sums of V over the split's keys (padding keys are zero)
+    {
+        constexpr int TPR = AT / D;              // threads per V row
+        const int row = tid / TPR, part = tid % TPR;
+        const uint32_t* vr = (const uint32_t*)(Vs + (int64_t)row * kps);
+        // thread `part` sums words [part*per, (part+1)*per), visited in an
+        // order rotated by the row so that lanes on different rows (whose
+        // rows start in the same bank) read different banks
+        const int per = kps / 4 / TPR;
+        int acc = 0;
+        for (int i = 0; i < per; ++i)
+            acc = __builtin_amdgcn_sdot4((int)vr[part * per + (i + row) % per], 0x01010101, acc, false);
+        atomicAdd(&vsum[row], (uint32_t)acc);
+    }
+
+    i16x o[3][NTO];
+#pragma unroll
+    for (int j = 0; j < 3; ++j)
+#pragma unroll
+        for (int n = 0; n < NTO; ++n) o[j][n] = i16x{};
+    for (int blk = 0; blk < kps / 32; ++blk) {
+        const int krow = blk * 32 + l32;
+        i16x s = i16x{};
+#pragma unroll
+        for (int t = 0; t < NTO; ++t) {
+            const i4 kf = *(const i4*)(Ks + (int64_t)krow * D + (((2 * t + h) ^ swz_k<D>(krow)) * 16));
+            s = __builtin_amdgcn_mfma_i32_32x32x32_i8(kf, qf[t], s, 0, 0, 0);
+        }
+        uint32_t x[16];
+#pragma unroll
+        for (int r = 0; r < 16; ++r) x[r] = (uint32_t)s[r] ^ 0x8080u;
+        i4 limb[3];
+#pragma unroll
+        for (int jj = 0; jj < 3; ++jj)
+#pragma unroll
+            for (int w = 0; w < 4; ++w)
+                limb[jj][w] = (int)gather_byte(x[4 * w], x[4 * w + 1], x[4 * w + 2], x[4 * w + 3], jj);
+#pragma unroll
+        for (int n = 0; n < NTO; ++n) {
+            const int vrow = n * 32 + l32;
+            const i4 vb = *(const i4*)(Vs + (int64_t)vrow * kps + (((2 * blk + h) ^ swz_v(vrow, vmask)) * 16));
+#pragma unroll
+            for (int jj = 0; jj < 3; ++jj)
+                o[jj][n] = __builtin_amdgcn_mfma_i32_32x32x32_i8(limb[jj], vb, o[jj][n], 0, 0, 0);
+        }
+    }
+    __syncthreads();                             // vsum complete
+
+    int32_t* O = (int32_t*)p.O;
+#pragma unroll
+    for (int n = 0; n < NTO; ++n) {
+        const int c = n * 32 + l32;
+        const uint32_t corr = 32896u * vsum[c];
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+            const int q = q0 + 8 * (r >> 2) + 4 * h + (r & 3);
+            if (q >= p.L) continue;
+            const uint32_t v = (uint32_t)o[0][n][r] + ((uint32_t)o[1][n][r] << 8) +
+                               ((uint32_t)o[2][n][r] << 16) + corr;
+            if (p.splits > 1) atomicAdd(O + (int64_t)q * D + c, (int)v);
+            else O[(int64_t)q * D + c] = (int32_t)v;
+        }
+    }
+}
+
+// ---------------------------------------------------------------------------
 // Softmax attention, FP32, BH heads (the SDPA-with-softmax form of the
 // attention baseline, Table 2 footnote; the attention core with a softmax,
 // Discussion).  Same S^T = K_blk Q^T layout as k_attn_f32: lane (query l32,
@@ -513,6 +698,40 @@ bool build_attn_i32(const AttnParams& p, LaunchRec* rec) {
     rec->name = "attn_i32";
     rec->grid = dim3((unsigned)((p.L + AQ - 1) / AQ), (unsigned)p.splits, 1);
     rec->block = dim3(AT, 1, 1);
+    rec->set_params(p);
+    return true;
+}
+
+bool resident_attn_i32(int64_t d, int64_t kps) {
+    return (d == 32 || d == 64 || d == 128) && kps % 32 == 0 && (kps * d) % 4096 == 0 && 2 * kps * d <= 49152;
+}
+
+bool build_attn_i32_prep(const AttnParams& p, LaunchRec* rec) {
+    switch (p.d) {
+    case 32: rec->fn = (const void*)k_attn_i32_prep<32>; break;
+    case 64: rec->fn = (const void*)k_attn_i32_prep<64>; break;
+    case 128: rec->fn = (const void*)k_attn_i32_prep<128>; break;
+    default: return false;
+    }
+    const int64_t items = p.prep_k + p.prep_v + (p.clear_o ? (int64_t)p.L * p.d / 4 : 0);
+    rec->name = "attn_i32_prep";
+    rec->grid = dim3((unsigned)((items + AT - 1) / AT), 1, 1);
+    rec->block = dim3(AT, 1, 1);
+    rec->set_params(p);
+    return true;
+}
+
+bool build_attn_i32r(const AttnParams& p, LaunchRec* rec) {
+    switch (p.d) {
+    case 32: rec->fn = (const void*)k_attn_i32r<32>; break;
+    case 64: rec->fn = (const void*)k_attn_i32r<64>; break;
+    case 128: rec->fn = (const void*)k_attn_i32r<128>; break;
+    default: return false;
+    }
+    rec->name = "attn_i32_resident";
+    rec->grid = dim3((unsigned)((p.L + AQ - 1) / AQ), (unsigned)p.splits, 1);
+    rec->block = dim3(AT, 1, 1);
+    rec->shmem = (uint32_t)(2 * (int64_t)p.keys_per_split * p.d);
     rec->set_params(p);
     return true;
 }

@@ -153,6 +153,13 @@ struct AttnParams {
     int32_t splits;         // key splits
     int32_t keys_per_split;
     int32_t limbs;          // I32: int8 limbs of S
+    // I32 with resident key splits: int8 copies made by the prep launch
+    void* k8;               // [Lp][d] int8 rows of K
+    void* v8;               // [d][Lp] int8 rows of V^T, keys of every 32-key block reordered
+                            // so a lane half's 16 keys of one S V product are contiguous
+    int32_t Lp;             // splits * keys_per_split (>= L), zero-padded keys
+    int32_t clear_o;        // prep also clears O (split partials are added with atomics)
+    int64_t prep_k, prep_v; // prep work items: 16-byte K8 chunks, 16-byte V8 chunks
 };
 
 // Softmax attention over BH heads (FP32): O = softmax(scale Q K^T [mask]) V.
@@ -316,6 +323,11 @@ void build_im2col(const Im2colParams& p, LaunchRec* rec);
 void build_valu_gemm(int32_t kind, const ValuGemmParams& p, int batch, LaunchRec* rec);
 bool build_attn_f32(const AttnParams& p, LaunchRec* rec);
 bool build_attn_i32(const AttnParams& p, LaunchRec* rec);
+// INT32 attention with resident key splits: applicable for d in {32, 64, 128}
+// and splits of kps keys with kps * d a multiple of 4096 and 2 * kps * d <= 48 KiB
+bool resident_attn_i32(int64_t d, int64_t kps);
+bool build_attn_i32_prep(const AttnParams& p, LaunchRec* rec);
+bool build_attn_i32r(const AttnParams& p, LaunchRec* rec);
 void build_reduce(const ReduceParams& p, LaunchRec* rec);
 bool build_sdpa_f32(const SdpaParams& p, LaunchRec* rec);
 void build_sdpa_combine(const SdpaCombineParams& p, LaunchRec* rec);

@@ -362,8 +362,11 @@ def test_attn_f32(L, d):
 
 
 @pytest.mark.parametrize("L,d,b", [(1, 32, 64), (33, 64, 64), (128, 64, 127), (300, 32, 100),
-                                   (1024, 128, 127), (257, 96, 64), (1000, 64, 64)])
+                                   (1024, 128, 127), (257, 96, 64), (1000, 64, 64), (4100, 128, 100),
+                                   (5000, 32, 127), (2049, 64, 127)])
 def test_attn_i32_mfma(L, d, b):
+    # d in {32, 64, 128}: the prep launch plus the resident-split kernel
+    # (ragged last split, zero-padded keys); d = 96: the streaming kernel
     rng = np.random.default_rng(L * 3 + d + b)
     Q, K, V = (rand_int(rng, (L, d), b, np.int32) for _ in range(3))
     O = host(qx.attn_core(dev(Q), dev(K), dev(V), bound=b))
@@ -379,8 +382,9 @@ def test_attn_i32_valu_full_range(L, d):
     same(O, orc.attn_i32(Q, K, V))
 
 
-def test_attn_i32_extremes():
-    L, d, b = 512, 64, 127
+@pytest.mark.parametrize("L,d", [(512, 64), (700, 128), (333, 32)])
+def test_attn_i32_extremes(L, d):
+    b = 127
     Q = np.full((L, d), -b, np.int32)
     K = np.full((L, d), -b, np.int32)
     V = np.full((L, d), b, np.int32)
