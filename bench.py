@@ -88,7 +88,7 @@ def parse():
     ap.add_argument("--warmup", type=int, default=50)
     ap.add_argument("--workload", default=HEADLINE)
     ap.add_argument("--all", action="store_true", help="also measure every workload")
-    ap.add_argument("--all-out", default=os.path.join(ROOT, "gpurun_out", "bench_all.json"))
+    ap.add_argument("--all-out", default="bench_all.json", help="where --all writes its per-workload results")
     ap.add_argument("--no-cpu", action="store_true", help="skip the oracle CPU baseline")
     ap.add_argument("--oracle-all", action="store_true",
                     help="time the CPU oracle on every workload (host only) and exit")
@@ -258,7 +258,7 @@ def main():
         print(json.dumps({"oracle": res}), flush=True)
         return
     if args.gpus != 1:
-        print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1",
+        print(json.dumps({"error": "the benchmark runs on one GPU only; --gpus must be 1",
                           "n_gpus": args.gpus}), flush=True)
         sys.exit(2)
     import torch
@@ -347,7 +347,8 @@ def main():
                         f"({m['gibs_cached'] * 2 ** 30 / 1e12 / PEAK['hbm'] * 1e3:.2f} of HBM peak)")
             res[name] = m
             print(f"[bench] {name}: {rate}, route {m['plan']['route_name']}", file=sys.stderr, flush=True)
-        os.makedirs(os.path.dirname(args.all_out), exist_ok=True)
+        if os.path.dirname(args.all_out):
+            os.makedirs(os.path.dirname(args.all_out), exist_ok=True)
         with open(args.all_out, "w") as f:
             json.dump(res, f, indent=1)
     print(json.dumps(line), flush=True)

@@ -55,7 +55,7 @@ extern "C" {
 typedef enum {
     QX_OK = 0,
     QX_ERR_INVALID_ARG = 1,   /* null pointer, negative size, size overflow, bad enum */
-    QX_ERR_UNSUPPORTED = 2,   /* valid request this build cannot run (device, route, shape) */
+    QX_ERR_UNSUPPORTED = 2,   /* valid request the library cannot run (device, route, shape) */
     QX_ERR_RANGE = 3,         /* declared bound outside what the operation accepts,
                                  or (QX_VALIDATE=1) an operand outside its declared bound */
     QX_ERR_OUT_OF_MEMORY = 4, /* workspace allocation failed */
