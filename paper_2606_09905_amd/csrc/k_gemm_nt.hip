@@ -88,36 +88,38 @@ __global__ __launch_bounds__(256) void k_enc_a(const EncParams p) {
 }
 
 // B [batch][K][ldb] int16 -> BT16 [batch][Np][Kp] fp16 (bf16 with BF)
-// through a 64(k) x 64(n) LDS transpose; 16-byte reads along n and 16-byte
-// writes along k.
+// transposed in registers.  A wave owns a 64(k) x 64(n) tile; lane
+// (kb, nb) = (lane / 8, lane % 8) reads eight 16-byte rows k = 8kb + r
+// (n = 8nb .. 8nb + 7) and writes eight 16-byte rows n = 8nb + e
+// (k = 8kb .. 8kb + 7): both sides move whole 128-byte lines per eight
+// lanes, and no LDS is involved.  A block is four waves along k.
 template <bool BF>
-__global__ __launch_bounds__(256) void k_enc_bt(const EncParams p) {
-    // 64 x 64 blocks keep the LDS footprint at 9 KB, so these workgroups can
-    // share a CU with a resident 144 KB contraction workgroup.
-    __shared__ __attribute__((aligned(16))) _Float16 t[64][64 + 8];
-    const int n0 = blockIdx.x * 64, k0 = blockIdx.y * 64, b = blockIdx.z;
+__global__ __launch_bounds__(256) void k_enc_bt2(const EncParams p) {
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int kb = lane >> 3, nb = lane & 7;
+    const int n0 = blockIdx.x * 64, k0 = (blockIdx.y * 4 + wave) * 64, b = blockIdx.z;
+    if (k0 >= p.Kp) return;
     const int16_t* src = (const int16_t*)p.src + b * p.s_src;
-    const int tid = threadIdx.x;
+    s8v in[8];
+    const int n = n0 + nb * 8;
 #pragma unroll
-    for (int q = 0; q < 2; ++q) {
-        const int idx = tid + 256 * q, kk = idx / 8, nv = (idx % 8) * 8;
-        const int k = k0 + kk, n = n0 + nv;
-        const int16_t* s = src + (int64_t)k * p.ld_src + n;
-        h8 h;
+    for (int r = 0; r < 8; ++r) {
+        const int k = k0 + kb * 8 + r;
+        const int16_t* sp = src + (int64_t)k * p.ld_src + n;
         if (p.vec && k < p.K && n + 8 <= p.N) {
-            h = to_h8<BF>(*(const s8v*)s);
+            in[r] = *(const s8v*)sp;
         } else {
 #pragma unroll
-            for (int e = 0; e < 8; ++e) h[e] = to_h1<BF>((k < p.K && n + e < p.N) ? s[e] : 0);
+            for (int e = 0; e < 8; ++e) in[r][e] = (k < p.K && n + e < p.N) ? sp[e] : (short)0;
         }
-#pragma unroll
-        for (int e = 0; e < 8; ++e) t[nv + e][kk] = h[e];
     }
-    __syncthreads();
+    _Float16* dst = (_Float16*)p.dst + b * p.s_dst + (int64_t)n * p.Kp + k0 + kb * 8;
 #pragma unroll
-    for (int q = 0; q < 2; ++q) {
-        const int idx = tid + 256 * q, nn = idx / 8, kc = (idx % 8) * 8;
-        *(h8*)((_Float16*)p.dst + b * p.s_dst + (int64_t)(n0 + nn) * p.Kp + k0 + kc) = *(const h8*)&t[nn][kc];
+    for (int e = 0; e < 8; ++e) {
+        s8v col;
+#pragma unroll
+        for (int r = 0; r < 8; ++r) col[r] = in[r][e];
+        *(h8*)(dst + (int64_t)e * p.Kp) = to_h8<BF>(col);
     }
 }
 
@@ -867,8 +869,8 @@ void build_enc_a(const EncParams& p, LaunchRec* rec) {
 }
 
 void build_enc_bt(const EncParams& p, LaunchRec* rec) {
-    rec->fn = p.bf16 ? (const void*)k_enc_bt<true> : (const void*)k_enc_bt<false>;
-    rec->grid = dim3((unsigned)(p.Np / 64), (unsigned)(p.Kp / 64), (unsigned)p.batch);
+    rec->fn = p.bf16 ? (const void*)k_enc_bt2<true> : (const void*)k_enc_bt2<false>;
+    rec->grid = dim3((unsigned)(p.Np / 64), (unsigned)((p.Kp / 64 + 3) / 4), (unsigned)p.batch);
     rec->block = dim3(256, 1, 1);
     rec->name = p.bf16 ? "enc_bt_bf16" : "enc_bt_f16";
     rec->set_params(p);
