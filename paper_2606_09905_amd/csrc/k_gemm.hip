@@ -652,6 +652,11 @@ __global__ __launch_bounds__(NT) void k_gemm_i8nt(const GemmParams p) {
     constexpr unsigned STAGE_A = P * BM * KCH * 16, STAGE_B = P * BN * KCH * 16;
     __shared__ i4 As[STAGES][P][BM][KCH];
     __shared__ i4 Bs[STAGES][P][BN][KCH];
+    // offset routes: the tile's row sums and per-slice column sums, loaded
+    // into LDS ahead of the first K tile (their latency hides behind the
+    // tile loads); the slices are added once, before the K loop
+    constexpr int MAX_SLICES = 16;
+    __shared__ uint32_t rs_l[BM], cs_l[MAX_SLICES][BN], csum_l[BN];
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, l32 = lane & 31, hh = lane >> 5;
     const int wm = wave >> 1, wn = wave & 1;
@@ -715,13 +720,45 @@ __global__ __launch_bounds__(NT) void k_gemm_i8nt(const GemmParams p) {
             for (int j = 0; j < TN; ++j) acc[g][i][j] = i16x{};
 
     const int ktiles = (p.K + BK - 1) / BK;   // planes are zero-limb padded to whole tiles
+    const bool sums_lds = p.corr_c != 0 && p.cs_slices <= MAX_SLICES;
+    if (sums_lds) {
+        // one 4-byte direct-to-LDS load per lane, 64 values per wave
+        // instruction; indices past M or N re-read the last valid element
+        // (those rows and columns are never stored)
+        const int32_t* rsg = p.rowsum + (int64_t)b * p.M;
+        const int32_t* csg = p.colsum + (int64_t)b * p.cs_slices * p.N;
+        constexpr int RI = BM / 64, CI = BN / 64;
+        const int n_inst = RI + p.cs_slices * CI;
+        for (int I = (int)wave_u; I < n_inst; I += NT / 64) {
+            const int32_t* base;
+            unsigned off, lds;
+            if (I < RI) {
+                base = rsg;
+                off = (unsigned)min(m0 + I * 64 + lane, p.M - 1) * 4u;
+                lds = (unsigned)(uintptr_t)&rs_l[I * 64];
+            } else {
+                const int sl = (I - RI) / CI, ci = (I - RI) % CI;
+                base = csg + (int64_t)sl * p.N;
+                off = (unsigned)min(n0 + ci * 64 + lane, p.N - 1) * 4u;
+                lds = (unsigned)(uintptr_t)&cs_l[sl][ci * 64];
+            }
+            asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dword %0, %1"
+                         :: "v"(off), "s"(base), "s"(lds) : "memory", "m0");
+        }
+    }
 #pragma unroll
     for (int s = 0; s < STAGES - 1; ++s)
         if (s < ktiles) issue(s);
     for (int t = 0; t < ktiles; ++t) {
         // tile t must have landed; the tiles after it may still be in flight
+        // (and the sums, issued before tile 0, have landed with it)
         wait_tiles<LPT>(min(STAGES - 2, ktiles - 1 - t));
         __syncthreads();
+        if (t == 0 && sums_lds && tid < BN) {
+            uint32_t c = 0;
+            for (int sl = 0; sl < p.cs_slices; ++sl) c += cs_l[sl][tid];
+            csum_l[tid] = c;   // read after the epilogue's barrier-ordered loop
+        }
         if (t + STAGES - 1 < ktiles) issue(t + STAGES - 1);
         const int s = t % STAGES;
 #pragma unroll
@@ -752,6 +789,7 @@ __global__ __launch_bounds__(NT) void k_gemm_i8nt(const GemmParams p) {
         }
     }
 
+    if (sums_lds) __syncthreads();   // csum_l complete (also with a single K tile)
     int32_t* C = (int32_t*)p.C + b * p.sC;
     const uint32_t cc = (uint32_t)p.corr_c;
     const uint32_t kcc = (uint32_t)p.K * cc * cc;
@@ -762,7 +800,9 @@ __global__ __launch_bounds__(NT) void k_gemm_i8nt(const GemmParams p) {
         const int gn = n0 + wn * WN + j * 32 + l32;
         if (gn >= p.N) continue;
         uint32_t csum = 0;
-        if (cc)
+        if (sums_lds)
+            csum = csum_l[wn * WN + j * 32 + l32];
+        else if (cc)
             for (int sl = 0; sl < p.cs_slices; ++sl) csum += (uint32_t)cs[(int64_t)sl * p.N + gn];
 #pragma unroll
         for (int i = 0; i < TM; ++i)
@@ -774,7 +814,11 @@ __global__ __launch_bounds__(NT) void k_gemm_i8nt(const GemmParams p) {
 #pragma unroll
                 for (int q = 0; q < G; ++q) gv[q] = (uint32_t)acc[q][i][j][r];
                 uint32_t v = S::combine(gv);
-                if (cc) v += cc * ((uint32_t)rs[gm] + csum) - kcc;
+                if (cc) {
+                    const uint32_t rsum = sums_lds ? rs_l[wm * WM + i * 32 + 8 * (r >> 2) + 4 * hh + (r & 3)]
+                                                   : (uint32_t)rs[gm];
+                    v += cc * (rsum + csum) - kcc;
+                }
                 store_c(p, C, gm, gn, v);
             }
     }
