@@ -106,7 +106,9 @@ typedef struct {
     int32_t exact_no_wrap;    /* 1: contract proves |result| < 2^31; 0: defined mod 2^32 */
     int32_t operand_format;   /* F16_EXACT with encoded operands: 1 = bf16 (both bounds
                                  <= 256, exact in bf16), 0 = fp16 (or not applicable) */
-    int32_t reserved;         /* 0 */
+    int32_t k_splits;         /* int8 limb routes: K slices of the main kernel, added into
+                                 the output (cleared first) with wrapping int32 atomics,
+                                 exact mod 2^32; 0: K is not sliced */
     int64_t workspace_bytes;  /* device workspace owned by the plan */
 } qx_plan_info;
 

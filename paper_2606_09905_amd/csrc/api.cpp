@@ -193,6 +193,8 @@ bool use_i8nt(int32_t route, int64_t M, int64_t N, int64_t K, int64_t batch) {
     return P * pad_up(M, bm) * Kp < lim && P * pad_up(N, bn) * Kp < lim;
 }
 
+void add_fill_out(Plan* pl, int64_t n32);
+
 // Appends the launches of one integer GEMM; ws_used is the workspace end.
 qx_status plan_int_gemm(const GemmSpec& s, Plan* pl, uint64_t* ws_used) {
     int32_t route = s.route;
@@ -363,6 +365,26 @@ qx_status plan_int_gemm(const GemmSpec& s, Plan* pl, uint64_t* ws_used) {
         i8nt_tile_shape(route, s.M, s.N, s.batch, &bm, &bn);
         const int64_t P = planes_of(route);
         const int64_t Mp = pad_up(s.M, bm), Np = pad_up(s.N, bn), Kp = pad_up(s.K, 64);
+        // K slices: a grid with fewer 64x64 tiles than the chip has CUs
+        // leaves CUs idle while each tile walks all of K; slicing K (at least
+        // four K tiles per slice, at most 16 slices) fills the CUs once.  Two
+        // slices per CU do not pay: a CU's throughput on these tiles is the
+        // same with one workgroup or two.  The slices add into the output,
+        // cleared first, so it must be one dense block.
+        int32_t ksplit = 1;
+        {
+            const int64_t tiles = (Mp / bm) * (Np / bn) * s.batch, kt = Kp / 64;
+            const bool dense_out = s.out_mode == OUT_ROWMAJOR && s.ldc == s.N &&
+                                   (s.batch == 1 || s.sC == s.M * s.N);
+            if (bm == 64 && dense_out && tiles <= 128 && kt >= 8) {
+                const int64_t want = std::min<int64_t>({256 / tiles, 16, kt / 4});
+                const int64_t per = (kt + want - 1) / want;
+                ksplit = (int32_t)((kt + per - 1) / per);   // no empty slice
+            }
+        }
+        g.ksplit = ksplit;
+        info.k_splits = ksplit > 1 ? ksplit : 0;
+        if (ksplit > 1) add_fill_out(pl, s.M * s.N * s.batch);
         const uint64_t a_off = round_up(*ws_used, 256);
         const uint64_t b_off = round_up(a_off + (uint64_t)s.batch * P * Mp * Kp, 256);
         *ws_used = b_off + (uint64_t)s.batch * P * Np * Kp;

@@ -51,14 +51,15 @@ __device__ __forceinline__ void tile_coords(int tiles_m, int tiles_n, int& tm, i
 }
 
 // Store one int32 result with the epilogue's layout.
+__device__ __forceinline__ int64_t c_index(const GemmParams& p, int gm, int gn) {
+    if (p.out_mode == OUT_ROWMAJOR) return (int64_t)gm * p.ldc + gn;
+    const int img = gn / p.hw, pix = gn - img * p.hw;
+    return ((int64_t)img * p.M + gm) * p.hw + pix;
+}
+
 __device__ __forceinline__ void store_c(const GemmParams& p, int32_t* C, int gm, int gn, uint32_t v) {
     if (gm >= p.M || gn >= p.N) return;
-    if (p.out_mode == OUT_ROWMAJOR) {
-        C[(int64_t)gm * p.ldc + gn] = (int32_t)v;
-    } else {
-        const int img = gn / p.hw, pix = gn - img * p.hw;
-        C[((int64_t)img * p.M + gm) * p.hw + pix] = (int32_t)v;
-    }
+    C[c_index(p, gm, gn)] = (int32_t)v;
 }
 
 // ===========================================================================
@@ -647,16 +648,20 @@ __global__ __launch_bounds__(NT) void k_gemm_i8nt(const GemmParams p) {
     constexpr int BK = 64, KCH = 4, P = S::PLANES, G = S::GROUPS;
     constexpr int WM = BM / 2, WN = BN / 2, TM = WM / 32, TN = WN / 32;
     static_assert(STAGES >= 3 && STAGES <= 6, "ring depth");
-    constexpr int AL = P * BM * KCH / NT, BL = P * BN * KCH / NT, LPT = AL + BL;
+    // offset routes: besides its share of the two operand tiles, every wave
+    // loads one dword per lane of the K tile's column-sum row (the encoder
+    // writes one row of column sums per 64 K), so the column sums add up
+    // alongside the K loop for any K; only the first BN/64 waves' values
+    // are used
+    constexpr bool OFFS = S::PAD != 0;
+    constexpr int AL = P * BM * KCH / NT, BL = P * BN * KCH / NT, LPT = AL + BL + (OFFS ? 1 : 0);
     static_assert(AL * NT == P * BM * KCH && BL * NT == P * BN * KCH, "whole loads");
+    static_assert(BN <= NT, "one column-sum dword per thread");
     constexpr unsigned STAGE_A = P * BM * KCH * 16, STAGE_B = P * BN * KCH * 16;
     __shared__ i4 As[STAGES][P][BM][KCH];
     __shared__ i4 Bs[STAGES][P][BN][KCH];
-    // offset routes: the tile's row sums and per-slice column sums, loaded
-    // into LDS ahead of the first K tile (their latency hides behind the
-    // tile loads); the slices are added once, before the K loop
-    constexpr int MAX_SLICES = 16;
-    __shared__ uint32_t rs_l[BM], cs_l[MAX_SLICES][BN], csum_l[BN];
+    __shared__ uint32_t cs_ring[OFFS ? STAGES : 1][NT];
+    __shared__ uint32_t rs_l[BM], csum_l[BN];
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, l32 = lane & 31, hh = lane >> 5;
     const int wm = wave >> 1, wn = wave & 1;
@@ -677,9 +682,24 @@ __global__ __launch_bounds__(NT) void k_gemm_i8nt(const GemmParams p) {
     }
     const int m0 = tm * BM, n0 = tn * BN;
     const int b = blockIdx.z;
+    // K slices: slice y covers K tiles [y*per, y*per + ktiles); every slice
+    // adds its partial products and the column-sum part of the offset
+    // correction over its own K tiles into C (cleared beforehand) with
+    // wrapping int32 atomics, which is exact mod 2^32 in any order; slice 0
+    // also adds the row-sum part and subtracts K c^2
+    const int ktiles_all = (p.K + BK - 1) / BK;   // planes are zero-limb padded to whole tiles
+    const bool split = p.ksplit > 1;
+    int kt0 = 0, ktiles = ktiles_all;
+    if (split) {
+        const int per = (ktiles_all + p.ksplit - 1) / p.ksplit;
+        kt0 = (int)blockIdx.y * per;
+        ktiles = min(per, ktiles_all - kt0);
+        if (ktiles <= 0) return;   // whole workgroup, before any barrier; never slice 0
+    }
+    const bool lead = blockIdx.y == 0;
     // planes: A8 [batch][P][Mp][Kp] (sA = P*Mp*Kp, lda = Kp, plane_a = Mp*Kp), B8T likewise
-    const char* a_panel = (const char*)p.A + b * p.sA + (int64_t)m0 * p.lda;
-    const char* b_panel = (const char*)p.B + b * p.sB + (int64_t)n0 * p.ldb;
+    const char* a_panel = (const char*)p.A + b * p.sA + (int64_t)m0 * p.lda + kt0 * BK;
+    const char* b_panel = (const char*)p.B + b * p.sB + (int64_t)n0 * p.ldb + kt0 * BK;
     unsigned oa[AL], ob[BL];
 #pragma unroll
     for (int i = 0; i < AL; ++i) {
@@ -696,6 +716,11 @@ __global__ __launch_bounds__(NT) void k_gemm_i8nt(const GemmParams p) {
     const unsigned wave_u = __builtin_amdgcn_readfirstlane(wave);
     const unsigned lds_a0 = (unsigned)(uintptr_t)&As[0][0][0][0] + wave_u * 1024;
     const unsigned lds_b0 = (unsigned)(uintptr_t)&Bs[0][0][0][0] + wave_u * 1024;
+    // column sums [batch][K/64][N]: this thread's column, clamped into N
+    // (columns past N are never stored)
+    const int32_t* csg = OFFS ? p.colsum + ((int64_t)b * p.cs_slices + kt0) * p.N : nullptr;
+    const unsigned cs_off = (unsigned)min(n0 + tid, p.N - 1) * 4u;
+    const unsigned lds_cs0 = (unsigned)(uintptr_t)&cs_ring[0][0] + wave_u * 256;
     auto issue = [&](int t) {
         const int s = t % STAGES;
         const char* ab = a_panel + t * BK;
@@ -709,6 +734,9 @@ __global__ __launch_bounds__(NT) void k_gemm_i8nt(const GemmParams p) {
         for (int i = 0; i < BL; ++i)
             asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dwordx4 %0, %1"
                          :: "v"(ob[i]), "s"(bb), "s"(lb + NT * 16 * i) : "memory", "m0");
+        if constexpr (OFFS)
+            asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dword %0, %1"
+                         :: "v"(cs_off), "s"(csg + (int64_t)t * p.N), "s"(lds_cs0 + s * NT * 4) : "memory", "m0");
     };
 
     i16x acc[G][TM][TN];
@@ -719,33 +747,19 @@ __global__ __launch_bounds__(NT) void k_gemm_i8nt(const GemmParams p) {
 #pragma unroll
             for (int j = 0; j < TN; ++j) acc[g][i][j] = i16x{};
 
-    const int ktiles = (p.K + BK - 1) / BK;   // planes are zero-limb padded to whole tiles
-    const bool sums_lds = p.corr_c != 0 && p.cs_slices <= MAX_SLICES;
-    if (sums_lds) {
-        // one 4-byte direct-to-LDS load per lane, 64 values per wave
-        // instruction; indices past M or N re-read the last valid element
-        // (those rows and columns are never stored)
+    if (OFFS && lead) {
+        // the tile's row sums, one 4-byte direct-to-LDS load per lane ahead
+        // of the first K tile; rows past M re-read the last valid one (they
+        // are never stored)
         const int32_t* rsg = p.rowsum + (int64_t)b * p.M;
-        const int32_t* csg = p.colsum + (int64_t)b * p.cs_slices * p.N;
-        constexpr int RI = BM / 64, CI = BN / 64;
-        const int n_inst = RI + p.cs_slices * CI;
-        for (int I = (int)wave_u; I < n_inst; I += NT / 64) {
-            const int32_t* base;
-            unsigned off, lds;
-            if (I < RI) {
-                base = rsg;
-                off = (unsigned)min(m0 + I * 64 + lane, p.M - 1) * 4u;
-                lds = (unsigned)(uintptr_t)&rs_l[I * 64];
-            } else {
-                const int sl = (I - RI) / CI, ci = (I - RI) % CI;
-                base = csg + (int64_t)sl * p.N;
-                off = (unsigned)min(n0 + ci * 64 + lane, p.N - 1) * 4u;
-                lds = (unsigned)(uintptr_t)&cs_l[sl][ci * 64];
-            }
+        for (int I = (int)wave_u; I < BM / 64; I += NT / 64) {
+            const unsigned off = (unsigned)min(m0 + I * 64 + lane, p.M - 1) * 4u;
+            const unsigned lds = (unsigned)(uintptr_t)&rs_l[I * 64];
             asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dword %0, %1"
-                         :: "v"(off), "s"(base), "s"(lds) : "memory", "m0");
+                         :: "v"(off), "s"(rsg), "s"(lds) : "memory", "m0");
         }
     }
+    uint32_t csum_acc = 0;   // this thread's column sum over the K tiles seen
 #pragma unroll
     for (int s = 0; s < STAGES - 1; ++s)
         if (s < ktiles) issue(s);
@@ -754,13 +768,9 @@ __global__ __launch_bounds__(NT) void k_gemm_i8nt(const GemmParams p) {
         // (and the sums, issued before tile 0, have landed with it)
         wait_tiles<LPT>(min(STAGES - 2, ktiles - 1 - t));
         __syncthreads();
-        if (t == 0 && sums_lds && tid < BN) {
-            uint32_t c = 0;
-            for (int sl = 0; sl < p.cs_slices; ++sl) c += cs_l[sl][tid];
-            csum_l[tid] = c;   // read after the epilogue's barrier-ordered loop
-        }
-        if (t + STAGES - 1 < ktiles) issue(t + STAGES - 1);
         const int s = t % STAGES;
+        if (OFFS && tid < BN) csum_acc += cs_ring[s][tid];   // before the stage is refilled
+        if (t + STAGES - 1 < ktiles) issue(t + STAGES - 1);
 #pragma unroll
         for (int ks = 0; ks < BK / 32; ++ks) {
             const int c = ks * 2 + hh;
@@ -789,37 +799,35 @@ __global__ __launch_bounds__(NT) void k_gemm_i8nt(const GemmParams p) {
         }
     }
 
-    if (sums_lds) __syncthreads();   // csum_l complete (also with a single K tile)
+    if (OFFS) {
+        if (tid < BN) csum_l[tid] = csum_acc;
+        __syncthreads();
+    }
     int32_t* C = (int32_t*)p.C + b * p.sC;
     const uint32_t cc = (uint32_t)p.corr_c;
     const uint32_t kcc = (uint32_t)p.K * cc * cc;
-    const int32_t* rs = p.rowsum ? p.rowsum + (int64_t)b * p.M : nullptr;
-    const int32_t* cs = p.colsum ? p.colsum + (int64_t)b * p.cs_slices * p.N : nullptr;
 #pragma unroll
     for (int j = 0; j < TN; ++j) {
         const int gn = n0 + wn * WN + j * 32 + l32;
         if (gn >= p.N) continue;
-        uint32_t csum = 0;
-        if (sums_lds)
-            csum = csum_l[wn * WN + j * 32 + l32];
-        else if (cc)
-            for (int sl = 0; sl < p.cs_slices; ++sl) csum += (uint32_t)cs[(int64_t)sl * p.N + gn];
+        const uint32_t ccol = OFFS ? cc * csum_l[wn * WN + j * 32 + l32] : 0u;
 #pragma unroll
         for (int i = 0; i < TM; ++i)
 #pragma unroll
             for (int r = 0; r < 16; ++r) {
-                const int gm = m0 + wm * WM + i * 32 + 8 * (r >> 2) + 4 * hh + (r & 3);
+                const int lr = wm * WM + i * 32 + 8 * (r >> 2) + 4 * hh + (r & 3);
+                const int gm = m0 + lr;
                 if (gm >= p.M) continue;
                 uint32_t gv[G];
 #pragma unroll
                 for (int q = 0; q < G; ++q) gv[q] = (uint32_t)acc[q][i][j][r];
                 uint32_t v = S::combine(gv);
-                if (cc) {
-                    const uint32_t rsum = sums_lds ? rs_l[wm * WM + i * 32 + 8 * (r >> 2) + 4 * hh + (r & 3)]
-                                                   : (uint32_t)rs[gm];
-                    v += cc * (rsum + csum) - kcc;
+                if (OFFS) {
+                    v += ccol;
+                    if (lead) v += cc * rs_l[lr] - kcc;
                 }
-                store_c(p, C, gm, gn, v);
+                if (split) atomicAdd((uint32_t*)C + c_index(p, gm, gn), v);
+                else C[c_index(p, gm, gn)] = (int32_t)v;
             }
     }
 }
@@ -1034,21 +1042,23 @@ bool build_gemm_i8nt(int32_t route, const GemmParams& p0, int batch, LaunchRec* 
     int bm, bn;
     i8nt_tile_shape(route, p0.M, p0.N, batch, &bm, &bn);
     const bool big = bm == 128;
-    // 64x64 tiles: a 6-deep ring (one workgroup per CU) while the grid fits
-    // the chip in one round, else 3 deep (two per CU)
-    const bool deep = (int64_t)((p0.M + 63) / 64) * ((p0.N + 63) / 64) * batch <= 256;
+    // 64x64 tiles: a 6-deep ring (one workgroup per CU) while the grid,
+    // K slices included, fits the chip in one round, else 3 deep (two per CU)
+    const bool deep = (int64_t)((p0.M + 63) / 64) * ((p0.N + 63) / 64) * batch * std::max(p0.ksplit, 1) <= 256;
 #define QX_NT(S, NAME)                                                                               \
     if (big) fill_gemm_rec(rec, k_gemm_i8nt<S, 128, 128, 3>, p0, 128, 128, batch, "gemm_i8nt_" NAME "_128x128"); \
     else if (deep) fill_gemm_rec(rec, k_gemm_i8nt<S, 64, 64, 6>, p0, 64, 64, batch, "gemm_i8nt_" NAME "_64x64"); \
     else fill_gemm_rec(rec, k_gemm_i8nt<S, 64, 64, 3>, p0, 64, 64, batch, "gemm_i8nt_" NAME "_64x64_3");
     switch (route) {
-    case R_I8_DIRECT: QX_NT(SchemeDirect, "direct") return true;
-    case R_I8_KARATSUBA: QX_NT(SchemeKaratsuba, "karatsuba") return true;
-    case R_I8_OFFSET4: QX_NT(SchemeOffset4, "offset4") return true;
-    case R_S24_I8LIMB: QX_NT(SchemeS24, "s24") return true;
+    case R_I8_DIRECT: QX_NT(SchemeDirect, "direct") break;
+    case R_I8_KARATSUBA: QX_NT(SchemeKaratsuba, "karatsuba") break;
+    case R_I8_OFFSET4: QX_NT(SchemeOffset4, "offset4") break;
+    case R_S24_I8LIMB: QX_NT(SchemeS24, "s24") break;
     default: return false;
     }
 #undef QX_NT
+    if (p0.ksplit > 1) rec->grid.y = (unsigned)p0.ksplit;
+    return true;
 }
 
 int sums_slices(int K) { return std::max((K + SUM_SLICE - 1) / SUM_SLICE, 1); }

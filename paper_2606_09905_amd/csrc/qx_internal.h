@@ -51,6 +51,9 @@ struct GemmParams {
     int32_t tiles_n;        // number of N tiles (grid swizzle)
     int32_t cs_slices;      // colsum holds this many partial rows per batch
     int32_t bf16;           // F16_EXACT NT contraction: operands are bf16 (|x| <= 256), else fp16
+    int32_t ksplit;         // int8 NT route: K slices (grid y) added into a cleared C with
+                            // wrapping int32 atomics; <= 1: one slice, plain stores
+    int32_t pad0;
     int64_t plane_a;        // int8 NT route: bytes between limb planes of A and of B
     int64_t plane_b;
     ConvGeom g;

@@ -46,7 +46,7 @@ class PlanInfo(ctypes.Structure):
         ("route", ctypes.c_int32), ("chunk", ctypes.c_int32), ("products", ctypes.c_int32),
         ("tile_m", ctypes.c_int32), ("tile_n", ctypes.c_int32), ("tile_k", ctypes.c_int32),
         ("kernels", ctypes.c_int32), ("exact_no_wrap", ctypes.c_int32),
-        ("operand_format", ctypes.c_int32), ("reserved", ctypes.c_int32),
+        ("operand_format", ctypes.c_int32), ("k_splits", ctypes.c_int32),
         ("workspace_bytes", ctypes.c_int64),
     ]
 

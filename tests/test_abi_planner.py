@@ -55,19 +55,32 @@ def test_limb_routes_take_the_encode_nt_structure_when_large():
     # NT int8 contraction runs on 64x64 tiles (64 tiles of 128x128 would
     # leave most of the chip idle).
     p = qx.plan_gemm_i32_s24(1024, 1024, 1024, 1)
-    assert p["kernels"] == 2 and (p["tile_m"], p["tile_n"]) == (64, 64)
+    assert p["kernels"] == 2 and (p["tile_m"], p["tile_n"]) == (64, 64) and p["k_splits"] == 0, p
     # three int8 planes of each operand (padded to 64) after the sums
     assert p["workspace_bytes"] >= 2 * 3 * 1024 * 1024
     # 16 x 512^3: 256 tiles of 128x128 are fewer than the 1024 a smul24
     # contraction needs before it takes them (four accumulator groups fill
     # every register of a lane at 128x128), so 64x64 again
     p = qx.plan_gemm_i32_s24(512, 512, 512, 16)
-    assert p["kernels"] == 2 and (p["tile_m"], p["tile_n"]) == (64, 64)
+    assert p["kernels"] == 2 and (p["tile_m"], p["tile_n"]) == (64, 64) and p["k_splits"] == 0
     p = qx.plan_gemm_i32_s24(4096, 4096, 512, 1)
-    assert p["kernels"] == 2 and (p["tile_m"], p["tile_n"]) == (128, 128)
+    assert p["kernels"] == 2 and (p["tile_m"], p["tile_n"]) == (128, 128) and p["k_splits"] == 0
     for route, b, kernels in (("i8_direct", 127, 2), ("i8_karatsuba", 8127, 2), ("i8_offset4", 0, 2)):
         p = qx.plan_gemm_i16i32(2048, 2048, 2048, 1, b, b, route)
         assert p["kernels"] == kernels and p["tile_m"] == 128, (route, p)
+    # K slices when there are at most 128 tiles: enough slices to give each
+    # CU one workgroup, at most 16, each of at least four 64-wide K tiles,
+    # none empty (132 K tiles: 16 slices of 9 would leave the last empty,
+    # so 15; 79 K tiles in 12 slices of 7 leave 2 for the last)
+    for (M, N, K, b), splits in (((300, 200, 5000, 1), 12), ((64, 1024, 4096, 1), 16),
+                                 ((33, 700, 999, 2), 4), ((640, 640, 640, 1), 2),
+                                 ((640, 640, 448, 1), 0), ((700, 900, 1000, 1), 0),
+                                 ((64, 64, 8448, 1), 15), ((1024, 1024, 256, 1), 0),
+                                 ((2048, 1024, 4096, 1), 0)):
+        p = qx.plan_gemm_i32_s24(M, N, K, b)
+        assert p["k_splits"] == splits and p["kernels"] == (3 if splits else 2), ((M, N, K, b), p)
+    p = qx.plan_gemm_i16i32(257, 129, 1000, 1, 32768, 32768, "i8_offset4")
+    assert p["k_splits"] == 4 and p["kernels"] == 3, p
     # small problems keep the single-pass register-staged kernel
     assert qx.plan_gemm_i32_s24(64, 64, 64, 1)["kernels"] == 2
     assert qx.plan_gemm_i16i32(64, 64, 64, 1, 127, 127)["kernels"] == 1
