@@ -21,6 +21,8 @@
 // feasible tiling, packing and accumulation).
 #include <algorithm>
 
+#include <type_traits>
+
 #include "qx_internal.h"
 
 namespace qx {
@@ -469,6 +471,48 @@ __global__ __launch_bounds__(NT) void k_gemm_i8limb(const GemmParams p) {
 // int8 limb routes for large problems: encode to limb planes, then an NT
 // int8 GEMM staged global -> LDS with global_load_lds_dwordx4.
 // ===========================================================================
+// smul24 limbs of four operands packed per plane with byte permutes: the
+// dword of plane q holds limb q of u0..u3 in bytes 0..3.  Limb q is byte q
+// of (x mod 2^24) ^ 0x008080 (bytes 0 and 1 flipped by 0x80), so the padding
+// value 0x8080 packs to zero bytes.
+__device__ __forceinline__ void pack_s24(uint32_t u0, uint32_t u1, uint32_t u2, uint32_t u3, uint32_t* d) {
+    const uint32_t lo = __builtin_amdgcn_perm(u1, u0, 0x05010400u);   // (u0.b0, u1.b0, u0.b1, u1.b1)
+    const uint32_t hi = __builtin_amdgcn_perm(u3, u2, 0x05010400u);   // (u2.b0, u3.b0, u2.b1, u3.b1)
+    d[0] = __builtin_amdgcn_perm(hi, lo, 0x05040100u) ^ 0x80808080u;
+    d[1] = __builtin_amdgcn_perm(hi, lo, 0x07060302u) ^ 0x80808080u;
+    const uint32_t lo2 = __builtin_amdgcn_perm(u1, u0, 0x0C0C0602u);  // (u0.b2, u1.b2, 0, 0)
+    const uint32_t hi2 = __builtin_amdgcn_perm(u3, u2, 0x0C0C0602u);
+    d[2] = __builtin_amdgcn_perm(hi2, lo2, 0x05040100u);
+}
+
+// Limb dwords of four k-consecutive elements x[0..3] (ok[r] false: padding,
+// all-zero limbs) for every plane, and their represented values' sum.
+template <class S, class T>
+__device__ __forceinline__ uint32_t pack4(const T* x, const bool* ok, uint32_t* w) {
+    uint32_t sum = 0;
+    if constexpr (std::is_same<S, SchemeS24>::value && sizeof(T) == 4) {
+        uint32_t u[4];
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            u[r] = ok[r] ? (uint32_t)x[r] : (uint32_t)S::PAD;
+            sum += ok[r] ? (uint32_t)S::value(x[r]) : 0u;
+        }
+        pack_s24(u[0], u[1], u[2], u[3], w);
+    } else {
+#pragma unroll
+        for (int q = 0; q < S::PLANES; ++q) w[q] = 0;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            uint32_t l[S::PLANES];
+            S::split(x[r], l);
+#pragma unroll
+            for (int q = 0; q < S::PLANES; ++q) w[q] |= (ok[r] ? l[q] : 0u) << (8 * r);
+            sum += ok[r] ? (uint32_t)S::value(x[r]) : 0u;
+        }
+    }
+    return sum;
+}
+
 // A [batch][M][lda] (T) -> A8 [batch][P][Mp][Kp] int8 limb planes.  One wave
 // per row; a lane splits 16 consecutive k per step.  Elements outside M x K
 // become all-zero limbs (the split of S::PAD), which add nothing to any limb
@@ -499,18 +543,12 @@ __device__ __forceinline__ void enc_limb_a(const EncParams& p, int blk) {
                 x[e] = ok[e] ? src[k0 + e] : (T)0;
             }
         }
-        uint32_t w[P][4] = {};
+        uint32_t w[4][P];
 #pragma unroll
-        for (int e = 0; e < 16; ++e) {
-            uint32_t l[P];
-            S::split(x[e], l);
-#pragma unroll
-            for (int q = 0; q < P; ++q) w[q][e >> 2] |= (ok[e] ? l[q] : 0u) << (8 * (e & 3));
-            if (SUMS && ok[e]) sum += (uint32_t)S::value(x[e]);
-        }
+        for (int g4 = 0; g4 < 4; ++g4) sum += pack4<S, T>(x + 4 * g4, ok + 4 * g4, w[g4]);
 #pragma unroll
         for (int q = 0; q < P; ++q)
-            *(i4*)(dst + (int64_t)q * p.Mp * p.Kp + k0) = i4{(int)w[q][0], (int)w[q][1], (int)w[q][2], (int)w[q][3]};
+            *(i4*)(dst + (int64_t)q * p.Mp * p.Kp + k0) = i4{(int)w[0][q], (int)w[1][q], (int)w[2][q], (int)w[3][q]};
     }
     if (SUMS) {
         for (int off = 32; off > 0; off >>= 1) sum += __shfl_xor(sum, off, 64);
@@ -519,89 +557,113 @@ __device__ __forceinline__ void enc_limb_a(const EncParams& p, int blk) {
 }
 
 // B [batch][K][ldb] (T) -> B8T [batch][P][Np][Kp]: a workgroup transposes a
-// 64(k) x 64(n) block.  A thread splits a 4 x 4 sub-block, packs the four k
-// bytes of each column and plane into one dword, and stages it in LDS; the
-// rows then leave as 16-byte runs along k.
+// 64(k) x 64(n) block.  A thread takes four k rows of four columns, packs
+// the four k bytes of each column and plane into one dword and stages it in
+// LDS; the rows then leave as 16-byte runs along k.  Plain B: a thread's
+// columns are consecutive (one 16-byte load per row).  Conv (B gathered
+// from the NCHW input, k = (ci*KH + kh)*KW + kw, n = (img*Ho + oh)*Wo + ow):
+// a thread's columns are 16 apart so that 16 lanes gather 16 consecutive
+// pixels, and the workgroup first tabulates its 64 rows' tap offsets and its
+// 64 columns' window origins in LDS, which leaves two adds, a bounds test
+// and a load per element.
 template <class S, class T>
 __device__ __forceinline__ void enc_limb_bt(const EncParams& p, int blk) {
     constexpr int P = S::PLANES, RW = 17;     // LDS row: 16 dwords of k + 1 to spread banks
     constexpr bool SUMS = S::PAD != 0;
     __shared__ uint32_t t[P][64][RW];
-    __shared__ uint32_t cs[64];
+    __shared__ uint32_t cpart[SUMS ? 16 : 1][64];
+    __shared__ int64_t tab_base[64], tab_off[64];
+    __shared__ int32_t tab_ih[64], tab_iw[64], tab_kh[64], tab_kw[64];
     const int nb64 = p.Np / 64, kb64 = p.Kp / 64;
     const int bx = blk % nb64, by = (blk / nb64) % kb64, b = blk / (nb64 * kb64);
     const int n0 = bx * 64, k0 = by * 64;
     const T* src = (const T*)p.src + b * p.s_src;
     const int tid = threadIdx.x, kg = tid >> 4, ng = tid & 15;
-    const int kb = k0 + kg * 4, nb = n0 + ng * 4;
-    if (SUMS) {
-        if (tid < 64) cs[tid] = 0;
-        __syncthreads();
-    }
-    uint32_t w[P][4] = {}, csum[4] = {};
-    // conv: pixel coordinates of this thread's four columns
-    int cimg[4], coh[4], cow[4];
+    const int kb = k0 + kg * 4;
+    T x[4][4];
+    bool ok[4][4];
+    int col[4];
     if (p.conv) {
-        const int hw = p.g.Ho * p.g.Wo;
+        const ConvGeom& g = p.g;
+        if (tid < 64) {
+            // column n0 + tid: window origin (clamped into N; columns past N are padding)
+            const int hw = g.Ho * g.Wo;
+            const int n = min(n0 + tid, p.N - 1);
+            const int img = n / hw, rem = n - img * hw, oh = rem / g.Wo, ow = rem - oh * g.Wo;
+            const int ih0 = oh * g.stride - g.pad, iw0 = ow * g.stride - g.pad;
+            tab_base[tid] = ((int64_t)img * g.Ci * g.H + ih0) * g.W + iw0;
+            tab_ih[tid] = ih0;
+            tab_iw[tid] = iw0;
+        } else if (tid < 128) {
+            // row k0 + i: tap (ci, kh, kw) (clamped into K; rows past K are padding)
+            const int i = tid - 64, k = min(k0 + i, p.K - 1);
+            const int kw = k % g.KW, t2 = k / g.KW, kh = t2 % g.KH, ci = t2 / g.KH;
+            tab_off[i] = ((int64_t)ci * g.H + kh) * g.W + kw;
+            tab_kh[i] = kh;
+            tab_kw[i] = kw;
+        }
+        __syncthreads();
+        int64_t cb[4];
+        int cih[4], ciw[4];
 #pragma unroll
         for (int c = 0; c < 4; ++c) {
-            const int n = min(nb + c, p.N - 1);
-            cimg[c] = n / hw;
-            const int rem = n - cimg[c] * hw;
-            coh[c] = rem / p.g.Wo;
-            cow[c] = rem - coh[c] * p.g.Wo;
+            col[c] = ng + 16 * c;
+            cb[c] = tab_base[col[c]];
+            cih[c] = tab_ih[col[c]];
+            ciw[c] = tab_iw[col[c]];
+        }
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            const int i = kg * 4 + r;
+            const int64_t off = tab_off[i];
+            const int kh = tab_kh[i], kw = tab_kw[i];
+#pragma unroll
+            for (int c = 0; c < 4; ++c) {
+                ok[r][c] = kb + r < p.K && n0 + col[c] < p.N;
+                const int ih = cih[c] + kh, iw = ciw[c] + kw;
+                const bool in = ok[r][c] && (unsigned)ih < (unsigned)g.H && (unsigned)iw < (unsigned)g.W;
+                x[r][c] = in ? src[cb[c] + off] : (T)0;   // outside the image: a real zero operand
+            }
+        }
+    } else {
+#pragma unroll
+        for (int c = 0; c < 4; ++c) col[c] = ng * 4 + c;
+        const int nb = n0 + ng * 4;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            const int k = kb + r;
+            const T* row = src + (int64_t)k * p.ld_src + nb;
+            if (p.vec && k < p.K && nb + 4 <= p.N) {
+                load_vec<T, 4>(row, x[r]);
+#pragma unroll
+                for (int c = 0; c < 4; ++c) ok[r][c] = true;
+            } else {
+#pragma unroll
+                for (int c = 0; c < 4; ++c) {
+                    ok[r][c] = k < p.K && nb + c < p.N;
+                    x[r][c] = ok[r][c] ? row[c] : (T)0;
+                }
+            }
         }
     }
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
-        const int k = kb + r;
-        const T* row = src + (int64_t)k * p.ld_src + nb;
-        T x[4];
-        bool ok[4];
-        if (p.conv) {
-            // B[k][n] = x[img][ci][oh*s - pad + kh][ow*s - pad + kw], zero outside
-            // the image (a real zero operand), k = (ci*KH + kh)*KW + kw
-            const ConvGeom& g = p.g;
-            const int kk = min(k, p.K - 1);
-            const int kw = kk % g.KW, t2 = kk / g.KW, kh = t2 % g.KH, ci = t2 / g.KH;
+    for (int c = 0; c < 4; ++c) {
+        const T xc[4] = {x[0][c], x[1][c], x[2][c], x[3][c]};
+        const bool oc[4] = {ok[0][c], ok[1][c], ok[2][c], ok[3][c]};
+        uint32_t w[P];
+        const uint32_t cs = pack4<S, T>(xc, oc, w);
 #pragma unroll
-            for (int c = 0; c < 4; ++c) {
-                ok[c] = k < p.K && nb + c < p.N;
-                const int ih = coh[c] * g.stride - g.pad + kh, iw = cow[c] * g.stride - g.pad + kw;
-                const bool in = ok[c] && ih >= 0 && ih < g.H && iw >= 0 && iw < g.W;
-                x[c] = in ? src[(((int64_t)cimg[c] * g.Ci + ci) * g.H + ih) * g.W + iw] : (T)0;
-            }
-        } else if (p.vec && k < p.K && nb + 4 <= p.N) {
-            load_vec<T, 4>(row, x);
-#pragma unroll
-            for (int c = 0; c < 4; ++c) ok[c] = true;
-        } else {
-#pragma unroll
-            for (int c = 0; c < 4; ++c) {
-                ok[c] = k < p.K && nb + c < p.N;
-                x[c] = ok[c] ? row[c] : (T)0;
-            }
-        }
-#pragma unroll
-        for (int c = 0; c < 4; ++c) {
-            uint32_t l[P];
-            S::split(x[c], l);
-#pragma unroll
-            for (int q = 0; q < P; ++q) w[q][c] |= (ok[c] ? l[q] : 0u) << (8 * r);
-            if (SUMS && ok[c]) csum[c] += (uint32_t)S::value(x[c]);
-        }
+        for (int q = 0; q < P; ++q) t[q][col[c]][kg] = w[q];
+        if (SUMS) cpart[kg][col[c]] = cs;
     }
-#pragma unroll
-    for (int q = 0; q < P; ++q)
-#pragma unroll
-        for (int c = 0; c < 4; ++c) t[q][ng * 4 + c][kg] = w[q][c];
-    if (SUMS)
-#pragma unroll
-        for (int c = 0; c < 4; ++c) atomicAdd(&cs[ng * 4 + c], csum[c]);
     __syncthreads();
     // column sums of this 64-k slice: [batch][Kp/64][N]
-    if (SUMS && tid < 64 && n0 + tid < p.N)
-        p.sums[((int64_t)b * kb64 + by) * p.N + n0 + tid] = (int32_t)cs[tid];
+    if (SUMS && tid < 64 && n0 + tid < p.N) {
+        uint32_t cs = 0;
+#pragma unroll
+        for (int i = 0; i < 16; ++i) cs += cpart[i][tid];
+        p.sums[((int64_t)b * kb64 + by) * p.N + n0 + tid] = (int32_t)cs;
+    }
     const int nn = tid >> 2, kc = (tid & 3) * 4;
     int8_t* dst = (int8_t*)p.dst + b * p.s_dst + (int64_t)(n0 + nn) * p.Kp + k0 + kc * 4;
 #pragma unroll
