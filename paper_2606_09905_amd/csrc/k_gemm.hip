@@ -705,10 +705,15 @@ __device__ __forceinline__ void wait_tiles(int n) {
 #undef QX_WAIT
 }
 
-template <class S, int BM, int BN, int STAGES>
-__global__ __launch_bounds__(NT) void k_gemm_i8nt(const GemmParams p) {
+// WAVES = 4: a 2 x 2 grid of waves; WAVES = 8: 2 (M) x 4 (N), two waves per
+// SIMD, which halves a 128 x 128 tile's per-wave accumulators.
+template <class S, int BM, int BN, int STAGES, int WAVES>
+__global__ __launch_bounds__(64 * WAVES) void k_gemm_i8nt(const GemmParams p) {
+    constexpr int NTH = 64 * WAVES, WGN = WAVES / 2;
     constexpr int BK = 64, KCH = 4, P = S::PLANES, G = S::GROUPS;
-    constexpr int WM = BM / 2, WN = BN / 2, TM = WM / 32, TN = WN / 32;
+    constexpr int WM = BM / 2, WN = BN / WGN, TM = WM / 32, TN = WN / 32;
+    static_assert(WAVES == 4 || WAVES == 8, "wave grid");
+    static_assert(TM >= 1 && TN >= 1, "whole 32 x 32 blocks per wave");
     static_assert(STAGES >= 3 && STAGES <= 6, "ring depth");
     // offset routes: besides its share of the two operand tiles, every wave
     // loads one dword per lane of the K tile's column-sum row (the encoder
@@ -716,17 +721,17 @@ __global__ __launch_bounds__(NT) void k_gemm_i8nt(const GemmParams p) {
     // alongside the K loop for any K; only the first BN/64 waves' values
     // are used
     constexpr bool OFFS = S::PAD != 0;
-    constexpr int AL = P * BM * KCH / NT, BL = P * BN * KCH / NT, LPT = AL + BL + (OFFS ? 1 : 0);
-    static_assert(AL * NT == P * BM * KCH && BL * NT == P * BN * KCH, "whole loads");
-    static_assert(BN <= NT, "one column-sum dword per thread");
+    constexpr int AL = P * BM * KCH / NTH, BL = P * BN * KCH / NTH, LPT = AL + BL + (OFFS ? 1 : 0);
+    static_assert(AL * NTH == P * BM * KCH && BL * NTH == P * BN * KCH, "whole loads");
+    static_assert(BN <= NTH, "one column-sum dword per thread");
     constexpr unsigned STAGE_A = P * BM * KCH * 16, STAGE_B = P * BN * KCH * 16;
     __shared__ i4 As[STAGES][P][BM][KCH];
     __shared__ i4 Bs[STAGES][P][BN][KCH];
-    __shared__ uint32_t cs_ring[OFFS ? STAGES : 1][NT];
+    __shared__ uint32_t cs_ring[OFFS ? STAGES : 1][NTH];
     __shared__ uint32_t rs_l[BM], csum_l[BN];
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, l32 = lane & 31, hh = lane >> 5;
-    const int wm = wave >> 1, wn = wave & 1;
+    const int wm = wave / WGN, wn = wave % WGN;
     const int tiles_m = (p.M + BM - 1) / BM;
     int pid = blockIdx.x;
     const int total = gridDim.x;
@@ -765,13 +770,13 @@ __global__ __launch_bounds__(NT) void k_gemm_i8nt(const GemmParams p) {
     unsigned oa[AL], ob[BL];
 #pragma unroll
     for (int i = 0; i < AL; ++i) {
-        const int q = tid + NT * i, plane = q / (BM * KCH), rem = q % (BM * KCH);
+        const int q = tid + NTH * i, plane = q / (BM * KCH), rem = q % (BM * KCH);
         const int row = rem / KCH, pc = rem % KCH;
         oa[i] = (unsigned)((int64_t)plane * p.plane_a + row * p.lda + (pc ^ swz_i8(row)) * 16);
     }
 #pragma unroll
     for (int i = 0; i < BL; ++i) {
-        const int q = tid + NT * i, plane = q / (BN * KCH), rem = q % (BN * KCH);
+        const int q = tid + NTH * i, plane = q / (BN * KCH), rem = q % (BN * KCH);
         const int row = rem / KCH, pc = rem % KCH;
         ob[i] = (unsigned)((int64_t)plane * p.plane_b + row * p.ldb + (pc ^ swz_i8(row)) * 16);
     }
@@ -791,14 +796,14 @@ __global__ __launch_bounds__(NT) void k_gemm_i8nt(const GemmParams p) {
 #pragma unroll
         for (int i = 0; i < AL; ++i)
             asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dwordx4 %0, %1"
-                         :: "v"(oa[i]), "s"(ab), "s"(la + NT * 16 * i) : "memory", "m0");
+                         :: "v"(oa[i]), "s"(ab), "s"(la + NTH * 16 * i) : "memory", "m0");
 #pragma unroll
         for (int i = 0; i < BL; ++i)
             asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dwordx4 %0, %1"
-                         :: "v"(ob[i]), "s"(bb), "s"(lb + NT * 16 * i) : "memory", "m0");
+                         :: "v"(ob[i]), "s"(bb), "s"(lb + NTH * 16 * i) : "memory", "m0");
         if constexpr (OFFS)
             asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dword %0, %1"
-                         :: "v"(cs_off), "s"(csg + (int64_t)t * p.N), "s"(lds_cs0 + s * NT * 4) : "memory", "m0");
+                         :: "v"(cs_off), "s"(csg + (int64_t)t * p.N), "s"(lds_cs0 + s * NTH * 4) : "memory", "m0");
     };
 
     i16x acc[G][TM][TN];
@@ -814,7 +819,7 @@ __global__ __launch_bounds__(NT) void k_gemm_i8nt(const GemmParams p) {
         // of the first K tile; rows past M re-read the last valid one (they
         // are never stored)
         const int32_t* rsg = p.rowsum + (int64_t)b * p.M;
-        for (int I = (int)wave_u; I < BM / 64; I += NT / 64) {
+        for (int I = (int)wave_u; I < BM / 64; I += NTH / 64) {
             const unsigned off = (unsigned)min(m0 + I * 64 + lane, p.M - 1) * 4u;
             const unsigned lds = (unsigned)(uintptr_t)&rs_l[I * 64];
             asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dword %0, %1"
@@ -1070,12 +1075,12 @@ bool build_gemm_mfma(int32_t route, const GemmParams& p, int batch, LaunchRec* r
 // int8 NT route: 128x128 workgroup tiles (four 64x64 waves) when they fill
 // the chip, else 64x64 (four 32x32 waves).
 void i8nt_tile_shape(int32_t route, int64_t M, int64_t N, int64_t batch, int* bm, int* bn) {
+    // 128x128 tiles (eight waves, two per SIMD, 64x32 each) move half the
+    // operand bytes per product of 64x64 tiles; they take over once there
+    // are 128 of them
+    (void)route;
     const int64_t big = ((M + 127) / 128) * ((N + 127) / 128) * batch;
-    // smul24 keeps four accumulator groups: a 128x128 tile needs all 512
-    // registers of a lane (one wave per SIMD), so it takes 64x64 tiles (two
-    // workgroups per CU) unless there are tiles for several rounds
-    const int64_t min_big = route == R_S24_I8LIMB ? 1024 : 128;
-    *bm = *bn = big >= min_big ? 128 : 64;
+    *bm = *bn = big >= 128 ? 128 : 64;
 }
 
 template <class S>
@@ -1108,9 +1113,9 @@ bool build_gemm_i8nt(int32_t route, const GemmParams& p0, int batch, LaunchRec* 
     // K slices included, fits the chip in one round, else 3 deep (two per CU)
     const bool deep = (int64_t)((p0.M + 63) / 64) * ((p0.N + 63) / 64) * batch * std::max(p0.ksplit, 1) <= 256;
 #define QX_NT(S, NAME)                                                                               \
-    if (big) fill_gemm_rec(rec, k_gemm_i8nt<S, 128, 128, 3>, p0, 128, 128, batch, "gemm_i8nt_" NAME "_128x128"); \
-    else if (deep) fill_gemm_rec(rec, k_gemm_i8nt<S, 64, 64, 6>, p0, 64, 64, batch, "gemm_i8nt_" NAME "_64x64"); \
-    else fill_gemm_rec(rec, k_gemm_i8nt<S, 64, 64, 3>, p0, 64, 64, batch, "gemm_i8nt_" NAME "_64x64_3");
+    if (big) fill_gemm_rec(rec, k_gemm_i8nt<S, 128, 128, 3, 8>, p0, 128, 128, batch, "gemm_i8nt_" NAME "_128x128"); \
+    else if (deep) fill_gemm_rec(rec, k_gemm_i8nt<S, 64, 64, 6, 4>, p0, 64, 64, batch, "gemm_i8nt_" NAME "_64x64"); \
+    else fill_gemm_rec(rec, k_gemm_i8nt<S, 64, 64, 3, 4>, p0, 64, 64, batch, "gemm_i8nt_" NAME "_64x64_3");
     switch (route) {
     case R_I8_DIRECT: QX_NT(SchemeDirect, "direct") break;
     case R_I8_KARATSUBA: QX_NT(SchemeKaratsuba, "karatsuba") break;
@@ -1119,6 +1124,7 @@ bool build_gemm_i8nt(int32_t route, const GemmParams& p0, int batch, LaunchRec* 
     default: return false;
     }
 #undef QX_NT
+    if (big) rec->block = dim3(512, 1, 1);
     if (p0.ksplit > 1) rec->grid.y = (unsigned)p0.ksplit;
     return true;
 }

@@ -58,11 +58,10 @@ def test_limb_routes_take_the_encode_nt_structure_when_large():
     assert p["kernels"] == 2 and (p["tile_m"], p["tile_n"]) == (64, 64) and p["k_splits"] == 0, p
     # three int8 planes of each operand (padded to 64) after the sums
     assert p["workspace_bytes"] >= 2 * 3 * 1024 * 1024
-    # 16 x 512^3: 256 tiles of 128x128 are fewer than the 1024 a smul24
-    # contraction needs before it takes them (four accumulator groups fill
-    # every register of a lane at 128x128), so 64x64 again
+    # 16 x 512^3: 256 tiles of 128x128 (at least 128 of them), run by eight
+    # waves of 64x32 each
     p = qx.plan_gemm_i32_s24(512, 512, 512, 16)
-    assert p["kernels"] == 2 and (p["tile_m"], p["tile_n"]) == (64, 64) and p["k_splits"] == 0
+    assert p["kernels"] == 2 and (p["tile_m"], p["tile_n"]) == (128, 128) and p["k_splits"] == 0
     p = qx.plan_gemm_i32_s24(4096, 4096, 512, 1)
     assert p["kernels"] == 2 and (p["tile_m"], p["tile_n"]) == (128, 128) and p["k_splits"] == 0
     for route, b, kernels in (("i8_direct", 127, 2), ("i8_karatsuba", 8127, 2), ("i8_offset4", 0, 2)):
