@@ -735,7 +735,16 @@ __global__ __launch_bounds__(64 * WAVES) void k_gemm_i8nt(const GemmParams p) {
     const int tiles_m = (p.M + BM - 1) / BM;
     int pid = blockIdx.x;
     const int total = gridDim.x;
+    // consecutive workgroup IDs go to the eight XCDs in turn: give each XCD
+    // a contiguous run of tiles (with a folded batch, whole batches), whose
+    // operand panels then share that XCD's L2
     if ((total & 7) == 0) pid = (pid & 7) * (total >> 3) + (pid >> 3);
+    int b = blockIdx.z;
+    if (p.flat_batch) {
+        const int tpb = tiles_m * p.tiles_n;
+        b = pid / tpb;
+        pid -= b * tpb;
+    }
     int tm, tn;
     {
         constexpr int GR = 8;
@@ -748,7 +757,6 @@ __global__ __launch_bounds__(64 * WAVES) void k_gemm_i8nt(const GemmParams p) {
         tn = in / gsz;
     }
     const int m0 = tm * BM, n0 = tn * BN;
-    const int b = blockIdx.z;
     // K slices: slice y covers K tiles [y*per, y*per + ktiles); every slice
     // adds its partial products and the column-sum part of the offset
     // correction over its own K tiles into C (cleared beforehand) with
@@ -1126,6 +1134,13 @@ bool build_gemm_i8nt(int32_t route, const GemmParams& p0, int batch, LaunchRec* 
 #undef QX_NT
     if (big) rec->block = dim3(512, 1, 1);
     if (p0.ksplit > 1) rec->grid.y = (unsigned)p0.ksplit;
+    if (batch > 1 && (int64_t)rec->grid.x * batch < ((int64_t)1 << 31)) {
+        GemmParams p = *(const GemmParams*)rec->blob;
+        p.flat_batch = 1;
+        rec->set_params(p);
+        rec->grid.x *= (unsigned)batch;
+        rec->grid.z = 1;
+    }
     return true;
 }
 

@@ -53,7 +53,7 @@ struct GemmParams {
     int32_t bf16;           // F16_EXACT NT contraction: operands are bf16 (|x| <= 256), else fp16
     int32_t ksplit;         // int8 NT route: K slices (grid y) added into a cleared C with
                             // wrapping int32 atomics; <= 1: one slice, plain stores
-    int32_t pad0;
+    int32_t flat_batch;     // int8 NT route: batch folded into grid x (each XCD gets whole batches)
     int64_t plane_a;        // int8 NT route: bytes between limb planes of A and of B
     int64_t plane_b;
     ConvGeom g;
