@@ -1105,11 +1105,14 @@ qx_status plan_attn(Plan* pl, qx_attn_dtype dt, int64_t L, int64_t d, int32_t bo
         pl->launches.push_back(r2);
         info.tile_m = 64; info.tile_n = 64; info.tile_k = 16;
     } else {
-        // Key splits: enough workgroups to cover the chip (>= 512), split
-        // boundaries on 32-key blocks.
+        // Key splits: enough workgroups for one per CU (>= 256), split
+        // boundaries on 32-key blocks.  Twice that many (shorter splits)
+        // measured 10% slower on L = 4096, d = 64 (more per-workgroup
+        // set-up and more partial outputs to combine); half as many left
+        // CUs idle (FP32 1.6x slower).
         const int64_t qgroups = (L + 127) / 128;
         const int64_t kblocks = (L + 31) / 32;
-        int64_t splits = std::min<int64_t>(std::max<int64_t>((512 + qgroups - 1) / qgroups, 1), kblocks);
+        int64_t splits = std::min<int64_t>(std::max<int64_t>((256 + qgroups - 1) / qgroups, 1), kblocks);
         int64_t kps = ((kblocks + splits - 1) / splits) * 32;
         if (r == R_ATTN_I32_MFMA && (d == 32 || d == 64 || d == 128)) {
             // resident splits: kps * d a multiple of 4096 (whole 1 KB loads

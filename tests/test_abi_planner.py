@@ -261,9 +261,14 @@ def test_attention_plans():
     with pytest.raises(qx.QxError) as e:
         qx.plan_attn("f32", 100, 300)
     assert e.value.status == qx.ERR_UNSUPPORTED
-    # key splits: every split boundary on a 32-key block, enough workgroups
+    # key splits: every split boundary on a 32-key block, one workgroup per
+    # CU (32 query blocks x 8 splits of 512 keys)
     p = qx.plan_attn("f32", 4096, 64)
-    assert p["tile_k"] % 32 == 0 and (4096 // 128) * (4096 // p["tile_k"]) >= 512
+    assert p["tile_k"] % 32 == 0 and (4096 // 128) * (4096 // p["tile_k"]) >= 256
+    assert p["tile_k"] == 512
+    # INT32 resident splits: both int8 tiles within 48 KiB of LDS caps a
+    # split at 384 keys for d = 64 (11 splits)
+    assert qx.plan_attn("i32", 4096, 64, 64)["tile_k"] == 384
 
 
 def test_sdpa_plans():
