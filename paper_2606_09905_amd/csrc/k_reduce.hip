@@ -175,10 +175,18 @@ __global__ __launch_bounds__(RT) void k_relu_i32(const ReluParams p) {
 // ---------------------------------------------------------------------------
 constexpr int DKW = 8;   // KW limit; C_out <= 16 and C_in*KH*KW <= 1024 (64 KB of LDS)
 
-template <int DCO>   // output channels per thread (8 or 16)
+// KWT: the kernel width when it is 3 or 5, else DKW for any KW <= DKW (the
+// taps past KW then multiply a zero input).  PXT: output pixels per thread,
+// consecutive along a row (Wo % PXT == 0): each weight read from LDS (a
+// broadcast, the same address in every lane) feeds PXT * DCO multiply-adds.
+// IMGS > 0: a workgroup takes IMGS whole images (IMGS * Ho * Wo <= RT * PXT)
+// and first copies their inputs into LDS with coalesced loads, so the
+// window reads (scattered across rows and cache lines) come from LDS;
+// IMGS == 0 reads the windows from global memory.
+template <int DCO, int KWT, int PXT, bool STAGE>
 __global__ __launch_bounds__(RT) void k_conv_direct_s24(const ConvDirectParams p) {
-    // weights [k][co], zero past C_out; sized Kd * DCO at launch so that
-    // small filters leave room for many workgroups per CU
+    // LDS: weights [Kd][DCO], zero past C_out, then (STAGE) the inputs of
+    // this workgroup's images [imgs][Ci][H][W]
     extern __shared__ int32_t wsh[];
     int32_t(*ws)[DCO] = (int32_t(*)[DCO])wsh;
     const ConvGeom& g = p.g;
@@ -186,42 +194,79 @@ __global__ __launch_bounds__(RT) void k_conv_direct_s24(const ConvDirectParams p
         const int k = i / DCO, c = i % DCO;
         ws[k][c] = c < p.Co ? p.w[(int64_t)c * p.Kd + k] : 0;
     }
-    __syncthreads();
-    const int64_t pix = (int64_t)blockIdx.x * RT + threadIdx.x;
-    const int64_t pc = min(pix, p.P - 1);
     const int hw = g.Ho * g.Wo;
-    const int n = (int)(pc / hw), rem = (int)(pc - (int64_t)n * hw);
-    const int oh = rem / g.Wo, ow = rem - oh * g.Wo;
-    const int32_t* xb = p.x + (int64_t)n * g.Ci * g.H * g.W;
-    uint32_t acc[DCO];
+    const int64_t groups = p.P / PXT;
+    int64_t t;
+    const int32_t* xb;
+    int n, rem;
+    bool live;
+    if constexpr (STAGE) {
+        // images [img0, img0 + imgs) of the batch; thread -> PXT pixels
+        const int imgs = p.imgs, nimg = (int)(p.P / hw);
+        const int img0 = (int)blockIdx.x * imgs, cnt = min(imgs, nimg - img0);
+        const int chw = g.Ci * g.H * g.W;
+        int32_t* xs = wsh + p.Kd * DCO;
+        const int32_t* src = p.x + (int64_t)img0 * chw;
+        for (int i = threadIdx.x; i < cnt * chw; i += RT) xs[i] = src[i];
+        const int local = (int)threadIdx.x * PXT;             // pixel within the images
+        live = local < cnt * hw;
+        const int li = min(local, cnt * hw - PXT);
+        const int limg = li / hw;
+        rem = li - limg * hw;
+        n = img0 + limg;
+        t = (int64_t)n * (hw / PXT) + rem / PXT;
+        xb = xs + (int64_t)limg * chw;
+        __syncthreads();
+    } else {
+        t = (int64_t)blockIdx.x * RT + threadIdx.x;
+        live = t < groups;
+        const int64_t pc = min(t, groups - 1) * PXT;
+        n = (int)(pc / hw);
+        rem = (int)(pc - (int64_t)n * hw);
+        xb = p.x + (int64_t)n * g.Ci * g.H * g.W;
+        __syncthreads();
+    }
+    const int oh = rem / g.Wo, ow0 = rem - oh * g.Wo;
+    uint32_t acc[PXT][DCO];
 #pragma unroll
-    for (int c = 0; c < DCO; ++c) acc[c] = 0u;
+    for (int j = 0; j < PXT; ++j)
+#pragma unroll
+        for (int c = 0; c < DCO; ++c) acc[j][c] = 0u;
     int k = 0;
     for (int ci = 0; ci < g.Ci; ++ci)
         for (int kh = 0; kh < g.KH; ++kh, k += g.KW) {
             const int ih = oh * g.stride - g.pad + kh;
             const bool rin = ih >= 0 && ih < g.H;
             const int32_t* xr = xb + ((int64_t)ci * g.H + ih) * g.W;
-            // the KW inputs of this kernel row first (independent loads), then
-            // every output channel
-            int32_t xv[DKW];
+            // the inputs of this kernel row for all PXT pixels first
+            // (independent loads), then every tap and output channel
+            int32_t xv[PXT][KWT];
 #pragma unroll
-            for (int kw = 0; kw < DKW; ++kw) {
-                const int iw = ow * g.stride - g.pad + kw;
-                xv[kw] = (kw < g.KW && rin && iw >= 0 && iw < g.W) ? xr[iw] : 0;
-            }
+            for (int j = 0; j < PXT; ++j)
 #pragma unroll
-            for (int kw = 0; kw < DKW; ++kw) {
-                if (kw >= g.KW) break;
-                const int32_t* wk = ws[k + kw];
+                for (int kw = 0; kw < KWT; ++kw) {
+                    const int iw = (ow0 + j) * g.stride - g.pad + kw;
+                    xv[j][kw] = (kw < g.KW && rin && iw >= 0 && iw < g.W) ? xr[iw] : 0;
+                }
 #pragma unroll
-                for (int c = 0; c < DCO; ++c) acc[c] += (uint32_t)__mul24(xv[kw], wk[c]);
+            for (int kw = 0; kw < KWT; ++kw) {
+                const int32_t* wk = ws[k + (KWT == DKW ? min(kw, g.KW - 1) : kw)];
+                int32_t wv[DCO];
+#pragma unroll
+                for (int c = 0; c < DCO; ++c) wv[c] = wk[c];
+#pragma unroll
+                for (int j = 0; j < PXT; ++j)
+#pragma unroll
+                    for (int c = 0; c < DCO; ++c) acc[j][c] += (uint32_t)__mul24(xv[j][kw], wv[c]);
             }
         }
-    if (pix < p.P)
+    (void)t;
+    if (live)
 #pragma unroll
         for (int c = 0; c < DCO; ++c)
-            if (c < p.Co) p.y[((int64_t)n * p.Co + c) * hw + rem] = (int32_t)acc[c];
+            if (c < p.Co)
+#pragma unroll
+                for (int j = 0; j < PXT; ++j) p.y[((int64_t)n * p.Co + c) * hw + rem + j] = (int32_t)acc[j][c];
 }
 
 // ---------------------------------------------------------------------------
@@ -248,12 +293,38 @@ void build_minmax(const MinMaxParams& p, LaunchRec* partial, LaunchRec* final_re
     final_rec->set_params(p);
 }
 
-void build_conv_direct_s24(const ConvDirectParams& p, LaunchRec* rec) {
+void build_conv_direct_s24(const ConvDirectParams& p0, LaunchRec* rec) {
+    ConvDirectParams p = p0;
+    const int kw = p.g.KW, wo = p.g.Wo;
+    const int pxt = wo % 4 == 0 ? 4 : wo % 2 == 0 ? 2 : 1;
     const int dco = p.Co <= 8 ? 8 : 16;
-    rec->fn = dco == 8 ? (const void*)k_conv_direct_s24<8> : (const void*)k_conv_direct_s24<16>;
-    rec->grid = dim3((unsigned)std::max<int64_t>((p.P + RT - 1) / RT, 1), 1, 1);
+    const int64_t hw = (int64_t)p.g.Ho * wo;
+    const int64_t chw = (int64_t)p.g.Ci * p.g.H * p.g.W;
+    // whole images per workgroup when at least one fits the threads and
+    // LDS (weights + inputs within 64 KB)
+    const int64_t by_threads = hw > 0 ? (int64_t)RT * pxt / hw : 0;
+    const int64_t by_lds = chw > 0 ? (16384 - (int64_t)p.Kd * dco) / chw : 0;
+    const int64_t imgs = std::min<int64_t>(by_threads, by_lds);
+    const bool stage = imgs >= 1 && p.P > 0;
+    p.imgs = stage ? (int32_t)imgs : 0;
+#define QX_DC4(DCO, KWT, PX) (stage ? (const void*)k_conv_direct_s24<DCO, KWT, PX, true> \
+                                    : (const void*)k_conv_direct_s24<DCO, KWT, PX, false>)
+#define QX_DC3(DCO, KWT) (pxt == 4 ? QX_DC4(DCO, KWT, 4) : pxt == 2 ? QX_DC4(DCO, KWT, 2) : QX_DC4(DCO, KWT, 1))
+#define QX_DC(DCO) (kw == 5 ? QX_DC3(DCO, 5) : kw == 3 ? QX_DC3(DCO, 3) : QX_DC3(DCO, DKW))
+    rec->fn = p.Co <= 8 ? QX_DC(8) : QX_DC(16);
+#undef QX_DC
+#undef QX_DC3
+#undef QX_DC4
+    int64_t blocks;
+    if (stage) {
+        const int64_t nimg = p.P / hw;
+        blocks = (nimg + imgs - 1) / imgs;
+    } else {
+        blocks = (p.P / pxt + RT - 1) / RT;
+    }
+    rec->grid = dim3((unsigned)std::max<int64_t>(blocks, 1), 1, 1);
     rec->block = dim3(RT, 1, 1);
-    rec->shmem = (uint32_t)(p.Kd * dco * sizeof(int32_t));
+    rec->shmem = (uint32_t)((p.Kd * dco + (stage ? imgs * chw : 0)) * sizeof(int32_t));
     rec->name = "conv_direct_s24";
     rec->set_params(p);
 }

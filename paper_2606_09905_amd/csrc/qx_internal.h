@@ -142,6 +142,7 @@ struct ConvDirectParams {
     int32_t* y;             // NCHW
     int64_t P;              // N*Ho*Wo
     int32_t Co, Kd;
+    int32_t imgs;           // > 0: whole images per workgroup, staged in LDS
     ConvGeom g;
 };
 
