@@ -187,7 +187,7 @@ template <int DCO, int KWT, int PXT, bool STAGE>
 __global__ __launch_bounds__(RT) void k_conv_direct_s24(const ConvDirectParams p) {
     // LDS: weights [Kd][DCO], zero past C_out, then (STAGE) the inputs of
     // this workgroup's images [imgs][Ci][H][W]
-    extern __shared__ int32_t wsh[];
+    extern __shared__ __align__(16) int32_t wsh[];
     int32_t(*ws)[DCO] = (int32_t(*)[DCO])wsh;
     const ConvGeom& g = p.g;
     for (int i = threadIdx.x; i < p.Kd * DCO; i += RT) {
@@ -250,10 +250,16 @@ __global__ __launch_bounds__(RT) void k_conv_direct_s24(const ConvDirectParams p
                 }
 #pragma unroll
             for (int kw = 0; kw < KWT; ++kw) {
-                const int32_t* wk = ws[k + (KWT == DKW ? min(kw, g.KW - 1) : kw)];
+                // DCO weights as 16-byte LDS reads (rows of DCO ints from a
+                // 16-byte aligned base)
+                const i4v* wk = (const i4v*)ws[k + (KWT == DKW ? min(kw, g.KW - 1) : kw)];
                 int32_t wv[DCO];
 #pragma unroll
-                for (int c = 0; c < DCO; ++c) wv[c] = wk[c];
+                for (int c4 = 0; c4 < DCO / 4; ++c4) {
+                    const i4v w4 = wk[c4];
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) wv[4 * c4 + e] = w4[e];
+                }
 #pragma unroll
                 for (int j = 0; j < PXT; ++j)
 #pragma unroll
