@@ -987,8 +987,7 @@ qx_status plan_lenet(Plan* pl, int64_t B) {
         off = o + bytes;
         return o;
     };
-    const uint64_t o_a1 = take(4 * (uint64_t)B * 6 * 28 * 28), o_p1 = take(4 * (uint64_t)B * 6 * 14 * 14);
-    const uint64_t o_a2 = take(4 * (uint64_t)B * 16 * 10 * 10), o_p2 = take(4 * (uint64_t)B * 400);
+    const uint64_t o_p1 = take(4 * (uint64_t)B * 6 * 14 * 14), o_p2 = take(4 * (uint64_t)B * 400);
     const uint64_t o_h1 = take(4 * (uint64_t)B * 120), o_h2 = take(4 * (uint64_t)B * 84);
     auto sub = [&](Plan& sp, std::initializer_list<Target> ins, Target out) -> qx_status {
         if (sp.n_events) return fail(QX_ERR_UNSUPPORTED, "chained plans must use one stream");
@@ -1006,6 +1005,27 @@ qx_status plan_lenet(Plan* pl, int64_t B) {
         r.bind(offsetof(PoolParams, y), BIND_WS, to);
         pl->launches.push_back(r);
     };
+    // conv 5x5 (smul24, few output channels: the direct kernel), ReLU and the
+    // 2x2 average pool into the workspace.  One launch when the pooled map
+    // (one thread per pooled pixel) still gives every SIMD four waves and an
+    // image fits the kernel's LDS; else the conv (four pixels per thread)
+    // and the pool as two launches.
+    auto conv_pool = [&](Target x, Bind w, uint64_t to, int64_t Ci, int32_t H, int64_t Co) {
+        const int32_t Ho = H - 4;
+        ConvDirectParams cd{};
+        cd.P = B * Ho * Ho; cd.Co = (int32_t)Co; cd.Kd = (int32_t)(Ci * 25);
+        cd.g = ConvGeom{(int32_t)Ci, H, H, 5, 5, 1, 0, Ho, Ho};
+        const bool fuse = B * (Ho / 2) * (Ho / 2) >= 4 * 1024 * 64 && conv_pool_images(cd) > 0;
+        cd.pool = fuse ? 1 : 0;
+        const uint64_t y = fuse ? to : take(4 * (uint64_t)B * Co * Ho * Ho);
+        LaunchRec r;
+        build_conv_direct_s24(cd, &r);
+        r.bind(offsetof(ConvDirectParams, x), x.bind, x.add);
+        r.bind(offsetof(ConvDirectParams, w), w);
+        r.bind(offsetof(ConvDirectParams, y), BIND_WS, y);
+        pl->launches.push_back(r);
+        if (!fuse) pool(y, to, Co, Ho);
+    };
     auto relu = [&](uint64_t at, int64_t n) {
         ReluParams rp{};
         rp.n = n;
@@ -1014,13 +1034,9 @@ qx_status plan_lenet(Plan* pl, int64_t B) {
         r.bind(offsetof(ReluParams, p), BIND_WS, at);
         pl->launches.push_back(r);
     };
-    Plan c1, c2, g1, g2, g3;
-    if ((st = plan_conv_t(&c1, QX_DT_I32, B, 1, 32, 32, 6, 5, 5, 1, 0, R_AUTO))) return st;
-    if ((st = sub(c1, {{BIND_IN0, 0}, {BIND_IN1, 0}}, {BIND_WS, o_a1}))) return st;
-    pool(o_a1, o_p1, 6, 28);
-    if ((st = plan_conv_t(&c2, QX_DT_I32, B, 6, 14, 14, 16, 5, 5, 1, 0, R_AUTO))) return st;
-    if ((st = sub(c2, {{BIND_WS, o_p1}, {BIND_IN2, 0}}, {BIND_WS, o_a2}))) return st;
-    pool(o_a2, o_p2, 16, 10);
+    Plan g1, g2, g3;
+    conv_pool({BIND_IN0, 0}, BIND_IN1, o_p1, 1, 32, 6);
+    conv_pool({BIND_WS, o_p1}, BIND_IN2, o_p2, 6, 14, 16);
     if ((st = plan_gemm(&g1, true, B, 120, 400, 1, 0, 0, R_AUTO))) return st;
     if ((st = sub(g1, {{BIND_WS, o_p2}, {BIND_IN3, 0}}, {BIND_WS, o_h1}))) return st;
     relu(o_h1, B * 120);

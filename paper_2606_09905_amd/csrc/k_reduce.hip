@@ -275,6 +275,90 @@ __global__ __launch_bounds__(RT) void k_conv_direct_s24(const ConvDirectParams p
                 for (int j = 0; j < PXT; ++j) p.y[((int64_t)n * p.Co + c) * hw + rem + j] = (int32_t)acc[j][c];
 }
 
+// The direct convolution fused with ReLU and a 2x2 average pool (the
+// sequence of the LeNet-shaped pipeline): a thread computes one 2x2 block of
+// conv outputs for every output channel (four pixels share each weight
+// read, as above) and writes only the pooled value, floor((relu(a) +
+// relu(b) + relu(c) + relu(d)) / 4) summed in 64 bits, the pool kernel's
+// arithmetic.  Ho and Wo even; the output is [N][C_out][Ho/2][Wo/2].  A
+// workgroup takes p.imgs whole images, staged in LDS as above.
+template <int DCO, int KWT>
+__global__ __launch_bounds__(RT) void k_conv_pool_s24(const ConvDirectParams p) {
+    extern __shared__ __align__(16) int32_t wsh[];
+    int32_t(*ws)[DCO] = (int32_t(*)[DCO])wsh;
+    const ConvGeom& g = p.g;
+    for (int i = threadIdx.x; i < p.Kd * DCO; i += RT) {
+        const int k = i / DCO, c = i % DCO;
+        ws[k][c] = c < p.Co ? p.w[(int64_t)c * p.Kd + k] : 0;
+    }
+    const int Wq = g.Wo / 2, hwq = (g.Ho / 2) * Wq;
+    const int64_t pq = p.P / 4;   // pooled pixels
+    // images [img0, img0 + cnt) of the batch; thread -> one pooled pixel
+    const int imgs = p.imgs, nimg = (int)(pq / hwq);
+    const int img0 = (int)blockIdx.x * imgs, cnt = min(imgs, nimg - img0);
+    const int chw = g.Ci * g.H * g.W;
+    int32_t* xs = wsh + p.Kd * DCO;
+    const int32_t* src = p.x + (int64_t)img0 * chw;
+    for (int i = threadIdx.x; i < cnt * chw; i += RT) xs[i] = src[i];
+    const int local = (int)threadIdx.x;
+    const bool live = local < cnt * hwq;
+    const int li = min(local, cnt * hwq - 1);
+    const int limg = li / hwq;
+    const int remq = li - limg * hwq;
+    const int n = img0 + limg;
+    const int32_t* xb = xs + (int64_t)limg * chw;
+    __syncthreads();
+    const int qh = remq / Wq, qw = remq - qh * Wq;
+    const int oh0 = 2 * qh, ow0 = 2 * qw;
+    uint32_t acc[4][DCO];
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+#pragma unroll
+        for (int c = 0; c < DCO; ++c) acc[j][c] = 0u;
+    int k = 0;
+    for (int ci = 0; ci < g.Ci; ++ci)
+        for (int kh = 0; kh < g.KH; ++kh, k += g.KW) {
+            int32_t xv[4][KWT];
+#pragma unroll
+            for (int dy = 0; dy < 2; ++dy) {
+                const int ih = (oh0 + dy) * g.stride - g.pad + kh;
+                const bool rin = ih >= 0 && ih < g.H;
+                const int32_t* xr = xb + ((int64_t)ci * g.H + ih) * g.W;
+#pragma unroll
+                for (int dx = 0; dx < 2; ++dx)
+#pragma unroll
+                    for (int kw = 0; kw < KWT; ++kw) {
+                        const int iw = (ow0 + dx) * g.stride - g.pad + kw;
+                        xv[2 * dy + dx][kw] = (kw < g.KW && rin && iw >= 0 && iw < g.W) ? xr[iw] : 0;
+                    }
+            }
+#pragma unroll
+            for (int kw = 0; kw < KWT; ++kw) {
+                const i4v* wk = (const i4v*)ws[k + (KWT == DKW ? min(kw, g.KW - 1) : kw)];
+                int32_t wv[DCO];
+#pragma unroll
+                for (int c4 = 0; c4 < DCO / 4; ++c4) {
+                    const i4v w4 = wk[c4];
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) wv[4 * c4 + e] = w4[e];
+                }
+#pragma unroll
+                for (int j = 0; j < 4; ++j)
+#pragma unroll
+                    for (int c = 0; c < DCO; ++c) acc[j][c] += (uint32_t)__mul24(xv[j][kw], wv[c]);
+            }
+        }
+    if (live)
+#pragma unroll
+        for (int c = 0; c < DCO; ++c)
+            if (c < p.Co) {
+                int64_t sum = 0;
+#pragma unroll
+                for (int j = 0; j < 4; ++j) sum += max((int64_t)(int32_t)acc[j][c], (int64_t)0);
+                p.y[((int64_t)n * p.Co + c) * hwq + remq] = (int32_t)(sum >> 2);
+            }
+}
+
 // ---------------------------------------------------------------------------
 // Builders
 // ---------------------------------------------------------------------------
@@ -299,8 +383,39 @@ void build_minmax(const MinMaxParams& p, LaunchRec* partial, LaunchRec* final_re
     final_rec->set_params(p);
 }
 
+// Whole images per workgroup for the fused conv + ReLU + pool kernel: as
+// many as its threads (one per pooled pixel) and 64 KB of LDS (weights and
+// inputs) hold; 0 when not even one fits.
+int32_t conv_pool_images(const ConvDirectParams& p) {
+    const int dco = p.Co <= 8 ? 8 : 16;
+    const int64_t hwq = (int64_t)(p.g.Ho / 2) * (p.g.Wo / 2);
+    const int64_t chw = (int64_t)p.g.Ci * p.g.H * p.g.W;
+    if (hwq <= 0 || chw <= 0 || p.P <= 0) return 0;
+    return (int32_t)std::max<int64_t>(std::min<int64_t>(RT / hwq, (16384 - (int64_t)p.Kd * dco) / chw), 0);
+}
+
 void build_conv_direct_s24(const ConvDirectParams& p0, LaunchRec* rec) {
     ConvDirectParams p = p0;
+    if (p.pool) {
+        // fused ReLU + 2x2 average: one thread per pooled pixel, whole
+        // images staged in LDS (the caller checked conv_pool_images > 0)
+        const int kw = p.g.KW;
+        const int dco = p.Co <= 8 ? 8 : 16;
+        const int64_t hwq = (int64_t)(p.g.Ho / 2) * (p.g.Wo / 2);
+        const int64_t chw = (int64_t)p.g.Ci * p.g.H * p.g.W;
+        p.imgs = conv_pool_images(p);
+#define QX_CP(DCO) (kw == 5 ? (const void*)k_conv_pool_s24<DCO, 5> \
+                    : kw == 3 ? (const void*)k_conv_pool_s24<DCO, 3> : (const void*)k_conv_pool_s24<DCO, DKW>)
+        rec->fn = p.Co <= 8 ? QX_CP(8) : QX_CP(16);
+#undef QX_CP
+        const int64_t blocks = (p.P / 4 / hwq + p.imgs - 1) / p.imgs;
+        rec->grid = dim3((unsigned)std::max<int64_t>(blocks, 1), 1, 1);
+        rec->block = dim3(RT, 1, 1);
+        rec->shmem = (uint32_t)((p.Kd * dco + p.imgs * chw) * sizeof(int32_t));
+        rec->name = "conv_relu_pool_s24";
+        rec->set_params(p);
+        return;
+    }
     const int kw = p.g.KW, wo = p.g.Wo;
     const int pxt = wo % 4 == 0 ? 4 : wo % 2 == 0 ? 2 : 1;
     const int dco = p.Co <= 8 ? 8 : 16;

@@ -143,6 +143,7 @@ struct ConvDirectParams {
     int64_t P;              // N*Ho*Wo
     int32_t Co, Kd;
     int32_t imgs;           // > 0: whole images per workgroup, staged in LDS
+    int32_t pool;           // 1: ReLU + 2x2 average fused, y is [N][C_out][Ho/2][Wo/2]
     ConvGeom g;
 };
 
@@ -342,6 +343,7 @@ void minmax_blocks(int64_t n, int32_t* blocks, int64_t* per);
 void build_minmax(const MinMaxParams& p, LaunchRec* partial, LaunchRec* final_rec);
 void build_pool2(int32_t kind, const PoolParams& p, LaunchRec* rec);
 void build_relu(const ReluParams& p, LaunchRec* rec);
+int32_t conv_pool_images(const ConvDirectParams& p);
 void build_conv_direct_s24(const ConvDirectParams& p, LaunchRec* rec);
 // fp16-exact route for large problems: encoders + direct-to-LDS NT GEMM.
 void nt_tile_shape(int64_t M, int64_t N, int64_t batch, int* bm, int* bn);
