@@ -169,20 +169,21 @@ __global__ __launch_bounds__(RT) void k_relu_i32(const ReluParams p) {
 
 // ---------------------------------------------------------------------------
 // Direct INT32 convolution under the smul24 contract for few output
-// channels, where a GEMM tile would be mostly empty: every thread owns one
-// output pixel and accumulates all C_out channels with v_mul_i32_i24 (low 32
-// bits of the product of the sign-extended low 24 bits), wrapping mod 2^32.
+// channels, where a GEMM tile would be mostly empty: a thread owns a few
+// output pixels and accumulates all C_out channels of each with
+// v_mad_i32_i24 (low 32 bits of the product of the sign-extended low 24
+// bits), wrapping mod 2^32.
 // ---------------------------------------------------------------------------
 constexpr int DKW = 8;   // KW limit; C_out <= 16 and C_in*KH*KW <= 1024 (64 KB of LDS)
 
 // KWT: the kernel width when it is 3 or 5, else DKW for any KW <= DKW (the
 // taps past KW then multiply a zero input).  PXT: output pixels per thread,
 // consecutive along a row (Wo % PXT == 0): each weight read from LDS (a
-// broadcast, the same address in every lane) feeds PXT * DCO multiply-adds.
-// IMGS > 0: a workgroup takes IMGS whole images (IMGS * Ho * Wo <= RT * PXT)
+// broadcast, the same address in every lane) feeds PXT multiply-adds.
+// STAGE: a workgroup takes p.imgs whole images (imgs * Ho * Wo <= RT * PXT)
 // and first copies their inputs into LDS with coalesced loads, so the
 // window reads (scattered across rows and cache lines) come from LDS;
-// IMGS == 0 reads the windows from global memory.
+// otherwise the windows are read from global memory.
 template <int DCO, int KWT, int PXT, bool STAGE>
 __global__ __launch_bounds__(RT) void k_conv_direct_s24(const ConvDirectParams p) {
     // LDS: weights [Kd][DCO], zero past C_out, then (STAGE) the inputs of
