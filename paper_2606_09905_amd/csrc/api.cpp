@@ -1026,7 +1026,20 @@ qx_status plan_lenet(Plan* pl, int64_t B) {
         pl->launches.push_back(r);
         if (!fuse) pool(y, to, Co, Ho);
     };
+    // ReLU after a fully connected layer: folded into the int8 NT
+    // contraction's stores when that is the layer's last launch (and K is
+    // not sliced), else a launch of its own
     auto relu = [&](uint64_t at, int64_t n) {
+        LaunchRec& last = pl->launches.back();
+        if (strncmp(last.name, "gemm_i8nt_", 10) == 0) {
+            GemmParams gp;
+            memcpy(&gp, last.blob, sizeof(gp));
+            if (gp.ksplit <= 1) {
+                gp.relu = 1;
+                memcpy(last.blob, &gp, sizeof(gp));
+                return;
+            }
+        }
         ReluParams rp{};
         rp.n = n;
         LaunchRec r;

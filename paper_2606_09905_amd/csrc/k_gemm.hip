@@ -902,7 +902,7 @@ __global__ __launch_bounds__(64 * WAVES) void k_gemm_i8nt(const GemmParams p) {
                     if (lead) v += cc * rs_l[lr] - kcc;
                 }
                 if (split) atomicAdd((uint32_t*)C + c_index(p, gm, gn), v);
-                else C[c_index(p, gm, gn)] = (int32_t)v;
+                else C[c_index(p, gm, gn)] = p.relu ? max((int32_t)v, 0) : (int32_t)v;
             }
     }
 }

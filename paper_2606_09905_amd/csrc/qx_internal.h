@@ -54,6 +54,8 @@ struct GemmParams {
     int32_t ksplit;         // int8 NT route: K slices (grid y) added into a cleared C with
                             // wrapping int32 atomics; <= 1: one slice, plain stores
     int32_t flat_batch;     // int8 NT route: batch folded into grid x (each XCD gets whole batches)
+    int32_t relu;           // int8 NT route without K slices: store max(C, 0)
+    int32_t pad1;
     int64_t plane_a;        // int8 NT route: bytes between limb planes of A and of B
     int64_t plane_b;
     ConvGeom g;
