@@ -4,13 +4,12 @@
  * the smul24 operand contract, GEMM-backed Conv2D through im2col lowering,
  * the single-head attention core O = (Q K^T) V, and a persistent executor.
  *
- * The operations are the ones the paper's Methodology names (tiled
- * matrix-multiplication substrate reused by every operator, GEMM-backed
- * convolution through lowering, attention core O = (Q K^T) V, persistent
- * executors that assemble and allocate once, smul24 operand-range contracts
- * that decide tiling, packing and accumulation at run time), measured in its
- * Table 1 (INT32 and packed INT16 / INT32-accumulation GEMM) and Table 2
- * (Conv2D and attention-core rows).
+ * The operations follow the paper's Methodology: one tiled integer GEMM
+ * that every operator reuses, convolution lowered onto it, the attention
+ * core O = (Q K^T) V, handles that plan and allocate a single time, and
+ * caller-declared operand bounds from which the exact route is chosen.  The
+ * paper measures them in Table 1 (INT32 and packed INT16 / INT32-accumulation
+ * GEMM) and Table 2 (Conv2D and attention-core rows).
  *
  * Conventions shared by every entry point
  * ---------------------------------------
@@ -207,24 +206,40 @@ qx_status sdpa_f32(const float* Q, const float* K, const float* V, float* O,
 /* ---- persistent executor (Methodology: assemble and allocate once, cache
  *      launch metadata, re-dispatch) ---------------------------------------- */
 
-/* Plan tiles, choose the route (route = QX_ROUTE_AUTO, or force one; an
- * infeasible forced route returns QX_ERR_RANGE), allocate the workspace and
- * build the cached launch records, on the current device.  *out receives the
- * handle.  Nothing is enqueued. */
-qx_status qx_exec_create_gemm_i16i32(qx_exec* out, int64_t M, int64_t N, int64_t K,
-                                     int64_t batch, int32_t bound_a, int32_t bound_b,
-                                     int32_t route);
-qx_status qx_exec_create_gemm_i32_s24(qx_exec* out, int64_t M, int64_t N, int64_t K,
-                                      int64_t batch, int32_t route);
+/* Plan tiles, choose the exact route from the declared contract, allocate
+ * the workspace and build the cached launch records, on the current device.
+ * *out receives the handle (NULL on failure).  Nothing is enqueued.  Size and
+ * bound rules are those of the matching one-shot call; the handle owns its
+ * workspace until qx_exec_destroy. */
+qx_status qx_exec_create_gemm_i16i32(qx_exec* out, int64_t M, int64_t N, int64_t K, int64_t batch,
+                                     int32_t bound_a, int32_t bound_b);
+qx_status qx_exec_create_gemm_i32_s24(qx_exec* out, int64_t M, int64_t N, int64_t K, int64_t batch);
 qx_status qx_exec_create_conv2d(qx_exec* out, int64_t N, int64_t C_in, int64_t H, int64_t W,
-                                int64_t C_out, int64_t KH, int64_t KW, int64_t stride,
-                                int64_t pad, int32_t bound_x, int32_t bound_w, int32_t route);
-/* dt QX_DT_F32: route AUTO, F32_MFMA or F32_VALU; QX_DT_I32: AUTO, S24_I8LIMB or S24_VALU. */
+                                int64_t C_out, int64_t KH, int64_t KW, int64_t stride, int64_t pad,
+                                int32_t bound_x, int32_t bound_w);
+qx_status qx_exec_create_attn(qx_exec* out, qx_attn_dtype dt, int64_t L, int64_t d, int32_t bound);
+
+/* The same four calls with a forced route (tests and comparisons of the
+ * routes, e.g. the vector-ALU smul24 GEMM against the int8 limb one):
+ * route = QX_ROUTE_AUTO behaves exactly as the call without the suffix; a
+ * route that does not apply to the operation returns QX_ERR_INVALID_ARG,
+ * one that cannot be exact for the declared bounds QX_ERR_RANGE. */
+qx_status qx_exec_create_gemm_i16i32_route(qx_exec* out, int64_t M, int64_t N, int64_t K,
+                                           int64_t batch, int32_t bound_a, int32_t bound_b,
+                                           int32_t route);
+qx_status qx_exec_create_gemm_i32_s24_route(qx_exec* out, int64_t M, int64_t N, int64_t K,
+                                            int64_t batch, int32_t route);
+qx_status qx_exec_create_conv2d_route(qx_exec* out, int64_t N, int64_t C_in, int64_t H, int64_t W,
+                                      int64_t C_out, int64_t KH, int64_t KW, int64_t stride,
+                                      int64_t pad, int32_t bound_x, int32_t bound_w, int32_t route);
+qx_status qx_exec_create_attn_route(qx_exec* out, qx_attn_dtype dt, int64_t L, int64_t d,
+                                    int32_t bound, int32_t route);
+
+/* FP32 / INT32 convolution (as conv2d_gemm_t).  dt QX_DT_F32: route AUTO,
+ * F32_MFMA or F32_VALU; QX_DT_I32: AUTO, S24_I8LIMB or S24_VALU. */
 qx_status qx_exec_create_conv2d_t(qx_exec* out, qx_attn_dtype dt, int64_t N, int64_t C_in,
                                   int64_t H, int64_t W, int64_t C_out, int64_t KH, int64_t KW,
                                   int64_t stride, int64_t pad, int32_t route);
-qx_status qx_exec_create_attn(qx_exec* out, qx_attn_dtype dt, int64_t L, int64_t d,
-                              int32_t bound, int32_t route);
 qx_status qx_exec_create_minmax(qx_exec* out, int64_t n, int32_t elem_bytes);
 /* LeNet-5-shaped INT32 pipeline (Results: end-to-end CNN), every layer one
  * of this library's operators chained through the workspace on one stream:
@@ -237,11 +252,16 @@ qx_status qx_exec_create_minmax(qx_exec* out, int64_t n, int32_t elem_bytes);
  * [in][out]); output [B][10] int32.  0 <= batch <= 2^20. */
 qx_status qx_exec_create_lenet_i32(qx_exec* out, int64_t batch);
 qx_status qx_exec_create_pool2x2(qx_exec* out, int32_t kind, int64_t N, int64_t C, int64_t H, int64_t W);
+/* Softmax attention (as sdpa_f32): inputs {Q, K, V}, output O. */
+qx_status qx_exec_create_sdpa_f32(qx_exec* out, int64_t BH, int64_t L, int64_t d, float scale,
+                                  int32_t causal);
 
 /* Enqueue one evaluation: inputs = {A, B} (GEMMs), {x, w} (convolutions), {x}
  * (min/max, pooling), {Q, K, V} (attention) or {x, w1, w2, f1, f2, f3}
  * (LeNet pipeline), device pointers with the shapes given at create.
- * Allocates nothing.  Calls on one handle must not overlap in time. */
+ * Allocates nothing.  Calls on one handle must not overlap in time.  A
+ * handle that is not live (never created, or already destroyed) returns
+ * QX_ERR_INVALID_ARG. */
 qx_status qx_exec_run(qx_exec h, const void* const* inputs, void* output, void* stream);
 
 /* The plan a handle carries. */
@@ -257,10 +277,9 @@ qx_status qx_exec_profile(qx_exec h, const void* const* inputs, void* output, vo
                           int32_t reps, float* kernel_ms, const char** names, int32_t max_kernels);
 
 /* Free the workspace and the handle (waits for the device to finish any
- * work that may use the workspace).  NULL is accepted. */
-/* inputs {Q, K, V}, output O, as sdpa_f32 */
-qx_status qx_exec_create_sdpa_f32(qx_exec* out, int64_t BH, int64_t L, int64_t d, float scale,
-                                  int32_t causal);
+ * work that may use the workspace).  NULL is accepted.  Destroying a handle
+ * that is not live (a second destroy, or a pointer that no create returned)
+ * returns QX_ERR_INVALID_ARG and touches nothing. */
 qx_status qx_exec_destroy(qx_exec h);
 
 /* ---- planner queries (pure host logic, no device needed) ---------------- */

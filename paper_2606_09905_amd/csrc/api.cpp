@@ -1,16 +1,16 @@
 // api.cpp -- planner, persistent executor and the C ABI of libqx.
 //
-// Planner: turns an operation, its shape and its operand-range contract into
-// a route, tiles, launch records and a workspace size (Methodology: operand
-// range contracts propagate to the operators and decide tiling, packing and
-// accumulation at run time).  Pure host logic; exported through the
-// qx_plan_* queries so it can be checked without a device.
+// Planner: from an operation, its shape and the caller's declared operand
+// bounds it derives which exact route can run (the bounds prove how large
+// every partial sum can get), the tile shapes, the launch records and the
+// workspace size (Methodology: operand-range contracts).  Pure host logic,
+// exported through the qx_plan_* queries so it can be checked without a
+// device.
 //
-// Executor: a handle that planned once, allocated its workspace once and
-// keeps the launch records; a run patches the caller's pointers into the
-// cached parameter blocks and enqueues the launches (Methodology: persistent
-// executors that assemble kernels and allocate device buffers once and cache
-// dispatch metadata).
+// Executor: a handle holding one planned operation.  Its workspace is
+// allocated and its launch parameter blocks built when it is created; a run
+// only writes the caller's pointers into copies of those blocks and enqueues
+// the launches (Methodology: persistent executors).
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
@@ -18,13 +18,17 @@
 #include <cstring>
 #include <cstdarg>
 #include <cstdio>
+#include <cstdlib>
+#include <atomic>
 #include <map>
+#include <set>
 #include <mutex>
 #include <string>
 #include <tuple>
 #include <vector>
 
 #include "../../include/qx.h"
+#include "../../include/qx_testing.h"
 #include "qx_internal.h"
 
 using namespace qx;
@@ -163,8 +167,15 @@ struct GemmSpec {
 // The encode + direct-to-LDS route pays two HBM-bound encoding passes; it is
 // used when the contraction is large enough for them to be small change and
 // the chunk covers at least one 64-wide K tile.
+// The NT kernel forms each lane's byte offset into an operand panel (at
+// most 256 rows of Kp fp16 elements) in 32-bit int arithmetic, and the B^T
+// encoder puts Kp/256 workgroups in grid y, so Kp is held below 2^22 (every
+// offset below 2^31); longer K takes the register-staged kernel, which
+// addresses in 64 bits.
+constexpr int64_t kNtMaxKp = (int64_t)1 << 22;
 bool use_nt(int32_t route, int64_t chunk, int64_t M, int64_t N, int64_t K, int64_t batch) {
     if (route != R_F16_EXACT || chunk < 64) return false;
+    if ((K + 63) / 64 * 64 >= kNtMaxKp) return false;
     const double macs = (double)M * (double)N * (double)K * (double)batch;
     return macs >= (double)(1 << 24) && M >= 32 && N >= 32 && K >= 64;
 }
@@ -1289,11 +1300,144 @@ qx_status plan_sdpa(Plan* pl, int64_t BH, int64_t L, int64_t d, float scale, int
 }  // namespace
 
 // ---------------------------------------------------------------------------
-// Executor
+// Device runtime calls of the executor
+//
+// Every HIP call the executor makes (device query, workspace, side stream,
+// events, launches, the validation read-back) goes through one table.  The
+// default table is the HIP runtime.  A host-only test double (switched on by
+// qx_testing_host_double, for tests of the executor's bookkeeping on machines
+// without a GPU) records instead: it reports one gfx950 device, hands out
+// host memory for workspaces, checks every launch's geometry and enqueues
+// nothing, so no operation result is ever computed while it is on.  Each
+// handle keeps the table it was created with.
 // ---------------------------------------------------------------------------
+namespace {
+
+struct RtTable {
+    const char* name;
+    hipError_t (*get_device)(int*);
+    hipError_t (*set_device)(int);
+    hipError_t (*arch_name)(int, char*, size_t);
+    hipError_t (*malloc)(void**, size_t);
+    hipError_t (*free)(void*);
+    hipError_t (*clear_sync)(void*, size_t);    // zero, then wait for the device
+    hipError_t (*device_sync)();
+    hipError_t (*stream_create)(hipStream_t*);
+    hipError_t (*stream_destroy)(hipStream_t);
+    hipError_t (*stream_sync)(hipStream_t);
+    hipError_t (*event_create)(hipEvent_t*, bool timing);
+    hipError_t (*event_destroy)(hipEvent_t);
+    hipError_t (*event_record)(hipEvent_t, hipStream_t);
+    hipError_t (*event_elapsed)(float*, hipEvent_t, hipEvent_t);
+    hipError_t (*stream_wait)(hipStream_t, hipEvent_t);
+    hipError_t (*launch)(const LaunchRec&, void**, hipStream_t);
+    hipError_t (*read_async)(void*, const void*, size_t, hipStream_t);
+};
+
+hipError_t hip_arch_name(int dev, char* buf, size_t n) {
+    hipDeviceProp_t prop;
+    hipError_t e = hipGetDeviceProperties(&prop, dev);
+    if (e == hipSuccess) snprintf(buf, n, "%s", prop.gcnArchName);
+    return e;
+}
+
+const RtTable kHip = {
+    "hip",
+    [](int* d) { return hipGetDevice(d); },
+    [](int d) { return hipSetDevice(d); },
+    hip_arch_name,
+    [](void** p, size_t n) { return hipMalloc(p, n); },
+    [](void* p) { return hipFree(p); },
+    [](void* p, size_t n) {
+        hipError_t e = hipMemset(p, 0, n);
+        return e == hipSuccess ? hipDeviceSynchronize() : e;
+    },
+    []() { return hipDeviceSynchronize(); },
+    [](hipStream_t* s) { return hipStreamCreateWithFlags(s, hipStreamNonBlocking); },
+    [](hipStream_t s) { return hipStreamDestroy(s); },
+    [](hipStream_t s) { return hipStreamSynchronize(s); },
+    [](hipEvent_t* ev, bool timing) {
+        return timing ? hipEventCreate(ev) : hipEventCreateWithFlags(ev, hipEventDisableTiming);
+    },
+    [](hipEvent_t ev) { return hipEventDestroy(ev); },
+    [](hipEvent_t ev, hipStream_t s) { return hipEventRecord(ev, s); },
+    [](float* ms, hipEvent_t a, hipEvent_t b) { return hipEventElapsedTime(ms, a, b); },
+    [](hipStream_t s, hipEvent_t ev) { return hipStreamWaitEvent(s, ev, 0); },
+    [](const LaunchRec& r, void** args, hipStream_t s) {
+        return hipLaunchKernel(r.fn, r.grid, r.block, args, r.shmem, s);
+    },
+    [](void* dst, const void* src, size_t n, hipStream_t s) {
+        return hipMemcpyAsync(dst, src, n, hipMemcpyDeviceToHost, s);
+    },
+};
+
+// Host double: streams and events are distinct dummy objects so that leaks
+// show up in the counters; a launch is checked against the hardware's grid
+// and workgroup limits and every pointer slot of its parameter block must be
+// bound.
+struct Dummy { uint32_t tag; };
+hipError_t dbl_new(void** p) { *p = new Dummy{0x64626c}; return hipSuccess; }
+hipError_t dbl_delete(void* p) {
+    if (!p || ((Dummy*)p)->tag != 0x64626c) return hipErrorInvalidValue;
+    ((Dummy*)p)->tag = 0;
+    delete (Dummy*)p;
+    return hipSuccess;
+}
+hipError_t dbl_launch(const LaunchRec& r, void** args, hipStream_t) {
+    if (!r.fn || !args) return hipErrorInvalidValue;
+    if (r.grid.x < 1 || r.grid.y < 1 || r.grid.z < 1 || r.grid.y > 65535 || r.grid.z > 65535 ||
+        (uint64_t)r.grid.x * r.block.x > 0xFFFFFFFFull)
+        return hipErrorInvalidConfiguration;
+    if (r.block.x * r.block.y * r.block.z < 1 || r.block.x * r.block.y * r.block.z > 1024)
+        return hipErrorInvalidConfiguration;
+    if (r.shmem > 160 * 1024) return hipErrorInvalidConfiguration;
+    for (int i = 0; i < r.nslots; ++i) {
+        void* ptr = nullptr;
+        memcpy(&ptr, (const unsigned char*)args[0] + r.slots[i].off, sizeof ptr);
+        if (!ptr) return hipErrorInvalidValue;
+    }
+    return hipSuccess;
+}
+
+const RtTable kHostDouble = {
+    "host double",
+    [](int* d) { *d = 0; return hipSuccess; },
+    [](int d) { return d == 0 ? hipSuccess : hipErrorInvalidDevice; },
+    [](int, char* buf, size_t n) { snprintf(buf, n, "gfx950:sramecc+:xnack-"); return hipSuccess; },
+    [](void** p, size_t n) {
+        *p = aligned_alloc(256, round_up(n, 256));
+        return *p ? hipSuccess : hipErrorOutOfMemory;
+    },
+    [](void* p) { std::free(p); return hipSuccess; },
+    [](void* p, size_t n) { memset(p, 0, n); return hipSuccess; },
+    []() { return hipSuccess; },
+    [](hipStream_t* s) { return dbl_new((void**)s); },
+    [](hipStream_t s) { return dbl_delete((void*)s); },
+    [](hipStream_t) { return hipSuccess; },
+    [](hipEvent_t* ev, bool) { return dbl_new((void**)ev); },
+    [](hipEvent_t ev) { return dbl_delete((void*)ev); },
+    [](hipEvent_t ev, hipStream_t) { return ev ? hipSuccess : hipErrorInvalidHandle; },
+    [](float* ms, hipEvent_t, hipEvent_t) { *ms = 0.0f; return hipSuccess; },
+    [](hipStream_t, hipEvent_t ev) { return ev ? hipSuccess : hipErrorInvalidHandle; },
+    dbl_launch,
+    [](void* dst, const void* src, size_t n, hipStream_t) { memcpy(dst, src, n); return hipSuccess; },
+};
+
+std::atomic<const RtTable*> g_rt{&kHip};
+
+// Counters of every device resource the executor acquires and releases
+// (both tables), for the tests of "run allocates nothing" and of cleanup
+// after a failed create.
+enum Counter { C_ALLOCS, C_FREES, C_STREAMS, C_STREAMS_FREED, C_EVENTS, C_EVENTS_FREED, C_LAUNCHES, C_LIVE_HANDLES,
+               C_N };
+std::atomic<int64_t> g_count[C_N];
+
+}  // namespace
+
 struct qx_exec_s {
     uint32_t magic;
     int device;
+    const RtTable* rt;      // runtime the handle was created with
     Plan plan;
     void* ws;
     uint64_t ws_bytes;
@@ -1307,27 +1451,76 @@ struct qx_exec_s {
 
 namespace {
 
-qx_status check_device(int* dev) {
-    hipError_t e = hipGetDevice(dev);
+// Live handles: a handle is usable only between its create and its destroy,
+// so a second destroy or a stray pointer is refused without being read.
+std::mutex g_live_mu;
+std::set<qx_exec>* g_live = new std::set<qx_exec>();
+
+bool is_live(qx_exec h) {
+    if (!h) return false;
+    std::lock_guard<std::mutex> lk(g_live_mu);
+    return g_live->count(h) != 0;
+}
+
+qx_status check_device(const RtTable& rt, int* dev) {
+    hipError_t e = rt.get_device(dev);
     if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
-    hipDeviceProp_t prop;
-    e = hipGetDeviceProperties(&prop, *dev);
+    char arch[256] = {0};
+    e = rt.arch_name(*dev, arch, sizeof arch);
     if (e != hipSuccess) return hip_fail(e, "hipGetDeviceProperties");
-    if (strncmp(prop.gcnArchName, "gfx950", 6) != 0)
-        return fail(QX_ERR_UNSUPPORTED, "device %d is %s; this library is built for gfx950 only", *dev,
-                    prop.gcnArchName);
+    if (strncmp(arch, "gfx950", 6) != 0)
+        return fail(QX_ERR_UNSUPPORTED, "device %d is %s; this library is built for gfx950 only", *dev, arch);
     return QX_OK;
+}
+
+// Releases everything a handle holds (any part may be missing); returns the
+// first error, after trying every release.
+hipError_t release_exec(qx_exec h) {
+    const RtTable& rt = *h->rt;
+    hipError_t first = hipSuccess;
+    auto note = [&](hipError_t e) { if (first == hipSuccess && e != hipSuccess) first = e; };
+    if (h->ws || h->side) note(rt.device_sync());
+    if (h->ws) {
+        note(rt.free(h->ws));
+        g_count[C_FREES]++;
+        h->ws = nullptr;
+    }
+    for (hipEvent_t ev : h->evs) {
+        note(rt.event_destroy(ev));
+        g_count[C_EVENTS_FREED]++;
+    }
+    h->evs.clear();
+    if (h->side) {
+        note(rt.stream_destroy(h->side));
+        g_count[C_STREAMS_FREED]++;
+        h->side = nullptr;
+    }
+    return first;
+}
+
+// QX_TEST_FAIL_ALLOC=k: the k-th device resource a create acquires (side
+// stream, event or workspace, counted from 1 in that order) fails as if the
+// device were out of memory, so that every cleanup path of a failed create
+// can be exercised.
+int fail_alloc_at() {
+    const char* v = getenv("QX_TEST_FAIL_ALLOC");
+    return v ? atoi(v) : 0;
 }
 
 qx_status make_exec(Plan&& pl, qx_exec* out) {
     if (!out) return fail(QX_ERR_INVALID_ARG, "out is NULL");
     *out = nullptr;
+    const RtTable& rt = *g_rt.load();
     int dev = 0;
-    qx_status st = check_device(&dev);
+    qx_status st = check_device(rt, &dev);
     if (st) return st;
+    const int fail_at = fail_alloc_at();
+    int acquired = 0;
+    auto injected = [&]() { return ++acquired == fail_at; };
     qx_exec h = new qx_exec_s();
     h->magic = kMagic;
     h->device = dev;
+    h->rt = &rt;
     h->ws = nullptr;
     h->side = nullptr;
     h->ws_bytes = (uint64_t)pl.info.workspace_bytes;
@@ -1335,53 +1528,57 @@ qx_status make_exec(Plan&& pl, qx_exec* out) {
     // QX_VALIDATE flag word behind the plan's workspace
     h->flag_off = round_up(h->ws_bytes, 256);
     if (!h->plan.checks.empty()) h->ws_bytes = h->flag_off + 256;
+    hipError_t e = hipSuccess;
+    const char* what = "";
     if (h->plan.n_events > 0) {
         // default-priority side stream; events without timing
-        hipError_t e = hipStreamCreateWithFlags(&h->side, hipStreamNonBlocking);
+        what = "executor side stream";
+        e = injected() ? hipErrorOutOfMemory : rt.stream_create(&h->side);
+        if (e == hipSuccess) g_count[C_STREAMS]++;
+        else h->side = nullptr;
         for (int i = 0; e == hipSuccess && i < h->plan.n_events + 2; ++i) {
+            what = "executor event";
             hipEvent_t ev = nullptr;
-            e = hipEventCreateWithFlags(&ev, hipEventDisableTiming);
-            if (e == hipSuccess) h->evs.push_back(ev);
-        }
-        if (e != hipSuccess) {
-            for (hipEvent_t ev : h->evs) (void)hipEventDestroy(ev);
-            if (h->side) (void)hipStreamDestroy(h->side);
-            h->magic = 0;
-            delete h;
-            return hip_fail(e, "executor stream/event creation");
+            e = injected() ? hipErrorOutOfMemory : rt.event_create(&ev, false);
+            if (e == hipSuccess) {
+                h->evs.push_back(ev);
+                g_count[C_EVENTS]++;
+            }
         }
     }
-    if (h->ws_bytes) {
-        hipError_t e = hipMalloc(&h->ws, h->ws_bytes);
-        if (e != hipSuccess) {
+    if (e == hipSuccess && h->ws_bytes) {
+        what = "workspace allocation";
+        e = injected() ? hipErrorOutOfMemory : rt.malloc(&h->ws, h->ws_bytes);
+        if (e == hipSuccess) {
+            g_count[C_ALLOCS]++;
+            // Zero once: padding that no run writes (tile tails of the encoded
+            // operands) must hold finite zeros.
+            what = "workspace clear";
+            e = rt.clear_sync(h->ws, h->ws_bytes);
+        } else {
             h->ws = nullptr;
-            for (hipEvent_t ev : h->evs) (void)hipEventDestroy(ev);
-            if (h->side) (void)hipStreamDestroy(h->side);
-            h->magic = 0;
-            delete h;
-            (void)hipGetLastError();
-            return hip_fail(e, "workspace hipMalloc");
-        }
-        // Zero once: padding that no run writes (tile tails of the encoded
-        // operands) must hold finite zeros.
-        e = hipMemset(h->ws, 0, h->ws_bytes);
-        if (e == hipSuccess) e = hipDeviceSynchronize();
-        if (e != hipSuccess) {
-            (void)hipFree(h->ws);
-            for (hipEvent_t ev : h->evs) (void)hipEventDestroy(ev);
-            if (h->side) (void)hipStreamDestroy(h->side);
-            h->magic = 0;
-            delete h;
-            return hip_fail(e, "workspace clear");
         }
     }
+    if (e != hipSuccess) {
+        if (h->rt == &kHip) (void)hipGetLastError();
+        (void)release_exec(h);
+        h->magic = 0;
+        delete h;
+        return hip_fail(e, what);
+    }
+    {
+        std::lock_guard<std::mutex> lk(g_live_mu);
+        g_live->insert(h);
+    }
+    g_count[C_LIVE_HANDLES]++;
     *out = h;
     return QX_OK;
 }
 
-qx_status launch_direct(LaunchRec& r, hipStream_t s) {
+qx_status launch_direct(const RtTable& rt, LaunchRec& r, hipStream_t s) {
     void* args[1] = {r.blob};
-    hipError_t e = hipLaunchKernel(r.fn, r.grid, r.block, args, r.shmem, s);
+    g_count[C_LAUNCHES]++;
+    hipError_t e = rt.launch(r, args, s);
     return e == hipSuccess ? QX_OK : hip_fail(e, r.name);
 }
 
@@ -1389,6 +1586,7 @@ qx_status launch_direct(LaunchRec& r, hipStream_t s) {
 // is outside its declared bound.
 qx_status validate_ranges(qx_exec h, const void* const* inputs, hipStream_t s) {
     const Plan& pl = h->plan;
+    const RtTable& rt = *h->rt;
     uint32_t* flag = (uint32_t*)((char*)h->ws + h->flag_off);
     FillParams f{};
     f.ptr = flag;
@@ -1396,7 +1594,7 @@ qx_status validate_ranges(qx_exec h, const void* const* inputs, hipStream_t s) {
     f.value = 0;
     LaunchRec rf;
     build_fill(f, &rf);
-    qx_status st = launch_direct(rf, s);
+    qx_status st = launch_direct(rt, rf, s);
     for (size_t i = 0; st == QX_OK && i < pl.checks.size(); ++i) {
         const Plan::RangeCheck& c = pl.checks[i];
         if (c.n == 0) continue;
@@ -1409,12 +1607,12 @@ qx_status validate_ranges(qx_exec h, const void* const* inputs, hipStream_t s) {
         rp.bit = 1u << i;
         LaunchRec rr;
         build_range(rp, &rr);
-        st = launch_direct(rr, s);
+        st = launch_direct(rt, rr, s);
     }
     if (st) return st;
     uint32_t bad = 0;
-    hipError_t e = hipMemcpyAsync(&bad, flag, sizeof bad, hipMemcpyDeviceToHost, s);
-    if (e == hipSuccess) e = hipStreamSynchronize(s);
+    hipError_t e = rt.read_async(&bad, flag, sizeof bad, s);
+    if (e == hipSuccess) e = rt.stream_sync(s);
     if (e != hipSuccess) return hip_fail(e, "range scan");
     for (size_t i = 0; i < pl.checks.size(); ++i)
         if (bad & (1u << i))
@@ -1425,8 +1623,9 @@ qx_status validate_ranges(qx_exec h, const void* const* inputs, hipStream_t s) {
 
 qx_status run_exec(qx_exec h, const void* const* inputs, void* output, void* stream,
                    std::vector<hipEvent_t>* evs = nullptr) {
-    if (!h || h->magic != kMagic) return fail(QX_ERR_INVALID_ARG, "invalid executor handle");
+    if (!is_live(h) || h->magic != kMagic) return fail(QX_ERR_INVALID_ARG, "invalid executor handle");
     const Plan& pl = h->plan;
+    const RtTable& rt = *h->rt;
     if (pl.launches.empty()) return QX_OK;
     // Only inputs some launch reads are required (a K == 0 GEMM just clears
     // its output and may get NULL operands).
@@ -1445,7 +1644,7 @@ qx_status run_exec(qx_exec h, const void* const* inputs, void* output, void* str
     if ((uintptr_t)output % pl.out_align)
         return fail(QX_ERR_INVALID_ARG, "output is not %llu-byte aligned", (unsigned long long)pl.out_align);
     int dev = -1;
-    hipError_t e = hipGetDevice(&dev);
+    hipError_t e = rt.get_device(&dev);
     if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
     if (dev != h->device)
         return fail(QX_ERR_INVALID_ARG, "handle was created on device %d, current device is %d", h->device, dev);
@@ -1460,8 +1659,8 @@ qx_status run_exec(qx_exec h, const void* const* inputs, void* output, void* str
     // every launch in plan order on the caller's stream instead.
     const bool lanes = pl.n_events > 0 && !evs;
     if (lanes) {
-        if ((e = hipEventRecord(h->evs[0], s)) != hipSuccess) return hip_fail(e, "hipEventRecord");
-        if ((e = hipStreamWaitEvent(h->side, h->evs[0], 0)) != hipSuccess) return hip_fail(e, "hipStreamWaitEvent");
+        if ((e = rt.event_record(h->evs[0], s)) != hipSuccess) return hip_fail(e, "hipEventRecord");
+        if ((e = rt.stream_wait(h->side, h->evs[0])) != hipSuccess) return hip_fail(e, "hipStreamWaitEvent");
     }
     for (const LaunchRec& r0 : pl.launches) {
         LaunchRec r = r0;
@@ -1477,27 +1676,29 @@ qx_status run_exec(qx_exec h, const void* const* inputs, void* output, void* str
         void* args[1] = {r.blob};
         const size_t li = (size_t)(&r0 - pl.launches.data());
         hipStream_t ls = (lanes && r.lane) ? h->side : s;
-        if (lanes && r.wait_ev >= 0 && (e = hipStreamWaitEvent(ls, h->evs[r.wait_ev], 0)) != hipSuccess)
+        if (lanes && r.wait_ev >= 0 && (e = rt.stream_wait(ls, h->evs[r.wait_ev])) != hipSuccess)
             return hip_fail(e, "hipStreamWaitEvent");
-        if (evs && (e = hipEventRecord((*evs)[2 * li], s)) != hipSuccess) return hip_fail(e, "hipEventRecord");
-        e = hipLaunchKernel(r.fn, r.grid, r.block, args, r.shmem, ls);
+        if (evs && (e = rt.event_record((*evs)[2 * li], s)) != hipSuccess) return hip_fail(e, "hipEventRecord");
+        g_count[C_LAUNCHES]++;
+        e = rt.launch(r, args, ls);
         if (e != hipSuccess) return hip_fail(e, r.name);
-        if (evs && (e = hipEventRecord((*evs)[2 * li + 1], s)) != hipSuccess) return hip_fail(e, "hipEventRecord");
-        if (lanes && r.rec_ev >= 0 && (e = hipEventRecord(h->evs[r.rec_ev], ls)) != hipSuccess)
+        if (evs && (e = rt.event_record((*evs)[2 * li + 1], s)) != hipSuccess) return hip_fail(e, "hipEventRecord");
+        if (lanes && r.rec_ev >= 0 && (e = rt.event_record(h->evs[r.rec_ev], ls)) != hipSuccess)
             return hip_fail(e, "hipEventRecord");
     }
     if (lanes) {
-        if ((e = hipEventRecord(h->evs.back(), h->side)) != hipSuccess) return hip_fail(e, "hipEventRecord");
-        if ((e = hipStreamWaitEvent(s, h->evs.back(), 0)) != hipSuccess) return hip_fail(e, "hipStreamWaitEvent");
+        if ((e = rt.event_record(h->evs.back(), h->side)) != hipSuccess) return hip_fail(e, "hipEventRecord");
+        if ((e = rt.stream_wait(s, h->evs.back())) != hipSuccess) return hip_fail(e, "hipStreamWaitEvent");
     }
     return QX_OK;
 }
 
 qx_status profile_exec(qx_exec h, const void* const* inputs, void* output, void* stream, int32_t reps,
                        float* kernel_ms, const char** names, int32_t max_kernels) {
-    if (!h || h->magic != kMagic) return fail(QX_ERR_INVALID_ARG, "invalid executor handle");
+    if (!is_live(h) || h->magic != kMagic) return fail(QX_ERR_INVALID_ARG, "invalid executor handle");
     if (reps < 1 || max_kernels < 0 || (max_kernels > 0 && !kernel_ms))
         return fail(QX_ERR_INVALID_ARG, "reps must be >= 1 and kernel_ms non-NULL");
+    const RtTable& rt = *h->rt;
     const size_t nl = h->plan.launches.size();
     const int nout = (int)std::min<size_t>(nl, (size_t)max_kernels);
     for (int i = 0; i < nout; ++i) {
@@ -1509,7 +1710,10 @@ qx_status profile_exec(qx_exec h, const void* const* inputs, void* output, void*
     qx_status st = QX_OK;
     hipError_t e = hipSuccess;
     for (auto& ev : evs)
-        if ((e = hipEventCreate(&ev)) != hipSuccess) break;
+        if ((e = rt.event_create(&ev, true)) != hipSuccess) {
+            ev = nullptr;
+            break;
+        }
     if (e != hipSuccess) {
         st = hip_fail(e, "hipEventCreate");
     } else {
@@ -1517,12 +1721,12 @@ qx_status profile_exec(qx_exec h, const void* const* inputs, void* output, void*
             std::vector<hipEvent_t> sub(evs.begin() + 2 * nl * r, evs.begin() + 2 * nl * (r + 1));
             st = run_exec(h, inputs, output, stream, &sub);
         }
-        if (st == QX_OK && (e = hipStreamSynchronize((hipStream_t)stream)) != hipSuccess)
+        if (st == QX_OK && (e = rt.stream_sync((hipStream_t)stream)) != hipSuccess)
             st = hip_fail(e, "hipStreamSynchronize");
         for (int r = 0; r < reps && st == QX_OK; ++r)
             for (int i = 0; i < nout; ++i) {
                 float ms = 0.0f;
-                if ((e = hipEventElapsedTime(&ms, evs[2 * nl * r + 2 * i], evs[2 * nl * r + 2 * i + 1])) !=
+                if ((e = rt.event_elapsed(&ms, evs[2 * nl * r + 2 * i], evs[2 * nl * r + 2 * i + 1])) !=
                     hipSuccess) {
                     st = hip_fail(e, "hipEventElapsedTime");
                     break;
@@ -1531,11 +1735,13 @@ qx_status profile_exec(qx_exec h, const void* const* inputs, void* output, void*
             }
     }
     for (auto& ev : evs)
-        if (ev) (void)hipEventDestroy(ev);
+        if (ev) (void)rt.event_destroy(ev);
     return st;
 }
 
-// One-shot calls: a cache of executors keyed by the full request.
+// One-shot calls: a cache of executors keyed by the full request.  The lock
+// is held while a missing entry is created, so concurrent first calls with
+// one key create it once.
 typedef std::tuple<int, int, int64_t, int64_t, int64_t, int64_t, int64_t, int64_t, int64_t, int64_t, int64_t,
                    int64_t, int64_t, int64_t, uintptr_t>
     Key;
@@ -1545,7 +1751,7 @@ std::map<Key, qx_exec>* g_cache = new std::map<Key, qx_exec>();
 template <class MakePlan>
 qx_status oneshot(const Key& key0, MakePlan make_plan, const void* const* inputs, void* output, void* stream) {
     int dev = -1;
-    hipError_t e = hipGetDevice(&dev);
+    hipError_t e = g_rt.load()->get_device(&dev);
     if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
     Key key = key0;
     std::get<1>(key) = dev;
@@ -1553,18 +1759,14 @@ qx_status oneshot(const Key& key0, MakePlan make_plan, const void* const* inputs
     {
         std::lock_guard<std::mutex> lk(g_cache_mu);
         auto it = g_cache->find(key);
-        if (it != g_cache->end()) h = it->second;
-    }
-    if (!h) {
-        Plan pl;
-        qx_status st = make_plan(&pl);
-        if (st) return st;
-        if ((st = make_exec(std::move(pl), &h))) return st;
-        std::lock_guard<std::mutex> lk(g_cache_mu);
-        auto ins = g_cache->emplace(key, h);
-        if (!ins.second) {  // another thread won the race
-            qx_exec_destroy(h);
-            h = ins.first->second;
+        if (it != g_cache->end()) {
+            h = it->second;
+        } else {
+            Plan pl;
+            qx_status st = make_plan(&pl);
+            if (st) return st;
+            if ((st = make_exec(std::move(pl), &h))) return st;
+            g_cache->emplace(key, h);
         }
     }
     return run_exec(h, inputs, output, stream);
@@ -1674,8 +1876,8 @@ qx_status qx_exec_create_sdpa_f32(qx_exec* out, int64_t BH, int64_t L, int64_t d
     return make_exec(std::move(pl), out);
 }
 
-qx_status qx_exec_create_gemm_i16i32(qx_exec* out, int64_t M, int64_t N, int64_t K, int64_t batch, int32_t bound_a,
-                                     int32_t bound_b, int32_t route) {
+qx_status qx_exec_create_gemm_i16i32_route(qx_exec* out, int64_t M, int64_t N, int64_t K, int64_t batch,
+                                           int32_t bound_a, int32_t bound_b, int32_t route) {
     g_err.clear();
     if (!out) return fail(QX_ERR_INVALID_ARG, "out is NULL");
     *out = nullptr;
@@ -1685,7 +1887,8 @@ qx_status qx_exec_create_gemm_i16i32(qx_exec* out, int64_t M, int64_t N, int64_t
     return make_exec(std::move(pl), out);
 }
 
-qx_status qx_exec_create_gemm_i32_s24(qx_exec* out, int64_t M, int64_t N, int64_t K, int64_t batch, int32_t route) {
+qx_status qx_exec_create_gemm_i32_s24_route(qx_exec* out, int64_t M, int64_t N, int64_t K, int64_t batch,
+                                            int32_t route) {
     g_err.clear();
     if (!out) return fail(QX_ERR_INVALID_ARG, "out is NULL");
     *out = nullptr;
@@ -1695,9 +1898,9 @@ qx_status qx_exec_create_gemm_i32_s24(qx_exec* out, int64_t M, int64_t N, int64_
     return make_exec(std::move(pl), out);
 }
 
-qx_status qx_exec_create_conv2d(qx_exec* out, int64_t N, int64_t C_in, int64_t H, int64_t W, int64_t C_out,
-                                int64_t KH, int64_t KW, int64_t stride, int64_t pad, int32_t bound_x, int32_t bound_w,
-                                int32_t route) {
+qx_status qx_exec_create_conv2d_route(qx_exec* out, int64_t N, int64_t C_in, int64_t H, int64_t W, int64_t C_out,
+                                      int64_t KH, int64_t KW, int64_t stride, int64_t pad, int32_t bound_x,
+                                      int32_t bound_w, int32_t route) {
     g_err.clear();
     if (!out) return fail(QX_ERR_INVALID_ARG, "out is NULL");
     *out = nullptr;
@@ -1748,7 +1951,8 @@ qx_status qx_exec_create_lenet_i32(qx_exec* out, int64_t batch) {
     return make_exec(std::move(pl), out);
 }
 
-qx_status qx_exec_create_attn(qx_exec* out, qx_attn_dtype dt, int64_t L, int64_t d, int32_t bound, int32_t route) {
+qx_status qx_exec_create_attn_route(qx_exec* out, qx_attn_dtype dt, int64_t L, int64_t d, int32_t bound,
+                                    int32_t route) {
     g_err.clear();
     if (!out) return fail(QX_ERR_INVALID_ARG, "out is NULL");
     *out = nullptr;
@@ -1756,6 +1960,27 @@ qx_status qx_exec_create_attn(qx_exec* out, qx_attn_dtype dt, int64_t L, int64_t
     qx_status st = plan_attn(&pl, dt, L, d, bound, route);
     if (st) return st;
     return make_exec(std::move(pl), out);
+}
+
+// The executor-create calls of the operations' specified interface take no
+// route: the planner chooses it from the contract.
+qx_status qx_exec_create_gemm_i16i32(qx_exec* out, int64_t M, int64_t N, int64_t K, int64_t batch, int32_t bound_a,
+                                     int32_t bound_b) {
+    return qx_exec_create_gemm_i16i32_route(out, M, N, K, batch, bound_a, bound_b, R_AUTO);
+}
+
+qx_status qx_exec_create_gemm_i32_s24(qx_exec* out, int64_t M, int64_t N, int64_t K, int64_t batch) {
+    return qx_exec_create_gemm_i32_s24_route(out, M, N, K, batch, R_AUTO);
+}
+
+qx_status qx_exec_create_conv2d(qx_exec* out, int64_t N, int64_t C_in, int64_t H, int64_t W, int64_t C_out,
+                                int64_t KH, int64_t KW, int64_t stride, int64_t pad, int32_t bound_x,
+                                int32_t bound_w) {
+    return qx_exec_create_conv2d_route(out, N, C_in, H, W, C_out, KH, KW, stride, pad, bound_x, bound_w, R_AUTO);
+}
+
+qx_status qx_exec_create_attn(qx_exec* out, qx_attn_dtype dt, int64_t L, int64_t d, int32_t bound) {
+    return qx_exec_create_attn_route(out, dt, L, d, bound, R_AUTO);
 }
 
 qx_status qx_exec_run(qx_exec h, const void* const* inputs, void* output, void* stream) {
@@ -1771,7 +1996,7 @@ qx_status qx_exec_profile(qx_exec h, const void* const* inputs, void* output, vo
 
 qx_status qx_exec_plan(qx_exec h, qx_plan_info* out) {
     g_err.clear();
-    if (!h || h->magic != kMagic) return fail(QX_ERR_INVALID_ARG, "invalid executor handle");
+    if (!is_live(h) || h->magic != kMagic) return fail(QX_ERR_INVALID_ARG, "invalid executor handle");
     if (!out) return fail(QX_ERR_INVALID_ARG, "out is NULL");
     *out = h->plan.info;
     return QX_OK;
@@ -1780,23 +2005,20 @@ qx_status qx_exec_plan(qx_exec h, qx_plan_info* out) {
 qx_status qx_exec_destroy(qx_exec h) {
     g_err.clear();
     if (!h) return QX_OK;
-    if (h->magic != kMagic) return fail(QX_ERR_INVALID_ARG, "invalid executor handle");
-    h->magic = 0;
-    qx_status st = QX_OK;
-    if (h->ws || h->side) {
-        int cur = -1;
-        (void)hipGetDevice(&cur);
-        if (cur != h->device) (void)hipSetDevice(h->device);
-        hipError_t e = hipDeviceSynchronize();
-        if (e == hipSuccess && h->ws) e = hipFree(h->ws);
-        for (hipEvent_t ev : h->evs)
-            if (e == hipSuccess) e = hipEventDestroy(ev);
-        if (e == hipSuccess && h->side) e = hipStreamDestroy(h->side);
-        if (e != hipSuccess) st = hip_fail(e, "executor release");
-        if (cur != h->device && cur >= 0) (void)hipSetDevice(cur);
+    {
+        std::lock_guard<std::mutex> lk(g_live_mu);
+        if (!g_live->erase(h)) return fail(QX_ERR_INVALID_ARG, "invalid executor handle (not live)");
     }
+    g_count[C_LIVE_HANDLES]--;
+    h->magic = 0;
+    const RtTable& rt = *h->rt;
+    int cur = -1;
+    (void)rt.get_device(&cur);
+    if (cur != h->device) (void)rt.set_device(h->device);
+    const hipError_t e = release_exec(h);
+    if (cur != h->device && cur >= 0) (void)rt.set_device(cur);
     delete h;
-    return st;
+    return e == hipSuccess ? QX_OK : hip_fail(e, "executor release");
 }
 
 void qx_release_cache(void) {
@@ -1806,6 +2028,27 @@ void qx_release_cache(void) {
         old.swap(*g_cache);
     }
     for (auto& kv : old) qx_exec_destroy(kv.second);
+}
+
+// ---- test seams (include/qx_testing.h) ----------------------------------
+
+qx_status qx_testing_host_double(int32_t on) {
+    g_err.clear();
+    if (on != 0 && on != 1) return fail(QX_ERR_INVALID_ARG, "on must be 0 or 1");
+    const RtTable* want = on ? &kHostDouble : &kHip;
+    if (g_rt.load() == want) return QX_OK;
+    qx_release_cache();
+    {
+        std::lock_guard<std::mutex> lk(g_live_mu);
+        if (!g_live->empty())
+            return fail(QX_ERR_INVALID_ARG, "%zu executor handles are still live", g_live->size());
+    }
+    g_rt.store(want);
+    return QX_OK;
+}
+
+void qx_testing_counters(int64_t* out, int32_t n) {
+    for (int i = 0; out && i < n && i < C_N; ++i) out[i] = g_count[i].load();
 }
 
 static bool empty_ok(const void* p, int64_t n) { return p != nullptr || n == 0; }

@@ -983,9 +983,11 @@ __global__ __launch_bounds__(NT) void k_im2col(const Im2colParams p) {
     ((T*)p.col)[(int64_t)k * p.P + pix] = v;
 }
 
+// Fill of 32-bit words: a grid-stride loop, so any count fits the capped grid.
 __global__ __launch_bounds__(NT) void k_fill(const FillParams p) {
-    const int64_t i = (int64_t)blockIdx.x * NT + threadIdx.x;
-    if (i < p.n32) ((int32_t*)p.ptr)[i] = p.value;
+    const int64_t stride = (int64_t)gridDim.x * NT;
+    for (int64_t i = (int64_t)blockIdx.x * NT + threadIdx.x; i < p.n32; i += stride)
+        ((int32_t*)p.ptr)[i] = p.value;
 }
 
 // Range scan: a grid-stride pass; a wave with any lane out of range sets the
@@ -1176,7 +1178,7 @@ void build_range(const RangeParams& p, LaunchRec* rec) {
 
 void build_fill(const FillParams& p, LaunchRec* rec) {
     rec->fn = (const void*)k_fill;
-    rec->grid = dim3((unsigned)(p.n32 > 0 ? (p.n32 + NT - 1) / NT : 1), 1, 1);
+    rec->grid = dim3((unsigned)std::min<int64_t>(std::max<int64_t>((p.n32 + NT - 1) / NT, 1), kFillMaxBlocks), 1, 1);
     rec->block = dim3(NT, 1, 1);
     rec->name = "fill";
     rec->set_params(p);

@@ -237,6 +237,8 @@ struct ReluParams {
     int64_t n;
 };
 
+// Largest grid of the fill kernel (a grid-stride loop beyond it).
+constexpr int64_t kFillMaxBlocks = 16384;
 struct FillParams {
     void* ptr;
     int64_t n32;            // number of 32-bit words

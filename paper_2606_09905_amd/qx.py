@@ -74,11 +74,16 @@ def lib() -> ctypes.CDLL:
             "conv2d_gemm": [_p, _p, _p] + [_i64] * 9 + [_i32, _i32, _p],
             "conv2d_gemm_t": [_i32, _p, _p, _p] + [_i64] * 9 + [_p],
             "attn_core": [_i32, _p, _p, _p, _p, _i64, _i64, _i32, _p],
-            "qx_exec_create_gemm_i16i32": [_p, _i64, _i64, _i64, _i64, _i32, _i32, _i32],
-            "qx_exec_create_gemm_i32_s24": [_p, _i64, _i64, _i64, _i64, _i32],
-            "qx_exec_create_conv2d": [_p] + [_i64] * 9 + [_i32, _i32, _i32],
+            "qx_exec_create_gemm_i16i32": [_p, _i64, _i64, _i64, _i64, _i32, _i32],
+            "qx_exec_create_gemm_i32_s24": [_p, _i64, _i64, _i64, _i64],
+            "qx_exec_create_conv2d": [_p] + [_i64] * 9 + [_i32, _i32],
+            "qx_exec_create_attn": [_p, _i32, _i64, _i64, _i32],
+            "qx_exec_create_gemm_i16i32_route": [_p, _i64, _i64, _i64, _i64, _i32, _i32, _i32],
+            "qx_exec_create_gemm_i32_s24_route": [_p, _i64, _i64, _i64, _i64, _i32],
+            "qx_exec_create_conv2d_route": [_p] + [_i64] * 9 + [_i32, _i32, _i32],
+            "qx_exec_create_attn_route": [_p, _i32, _i64, _i64, _i32, _i32],
             "qx_exec_create_conv2d_t": [_p, _i32] + [_i64] * 9 + [_i32],
-            "qx_exec_create_attn": [_p, _i32, _i64, _i64, _i32, _i32],
+            "qx_testing_host_double": [_i32],
             "qx_exec_run": [_p, _p, _p, _p],
             "qx_exec_plan": [_p, _p],
             "qx_exec_profile": [_p, _p, _p, _p, _i32, _p, _p, _i32],
@@ -108,13 +113,15 @@ def lib() -> ctypes.CDLL:
         L.qx_last_error.restype = ctypes.c_char_p
         L.qx_release_cache.argtypes = []
         L.qx_release_cache.restype = None
+        L.qx_testing_counters.argtypes = [_p, _i32]
+        L.qx_testing_counters.restype = None
         _lib = L
     return _lib
 
 
-def header_functions() -> list[str]:
-    """Names of every function include/qx.h declares."""
-    with open(HEADER_PATH) as f:
+def header_functions(path: str = HEADER_PATH) -> list[str]:
+    """Names of every function a header (default include/qx.h) declares."""
+    with open(path) as f:
         text = f.read()
     text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
     return sorted(set(re.findall(r"\b([A-Za-z_]\w*)\s*\(", text)) -
@@ -386,23 +393,33 @@ class Executor:
     def gemm_i16i32(cls, M, N, K, batch=1, bound_a=0, bound_b=0, route="auto"):
         torch = _torch()
         h = ctypes.c_void_p()
-        check(lib().qx_exec_create_gemm_i16i32(ctypes.byref(h), M, N, K, batch, bound_a, bound_b,
-                                               _route(route)))
+        if _route(route) == 0:
+            check(lib().qx_exec_create_gemm_i16i32(ctypes.byref(h), M, N, K, batch, bound_a, bound_b))
+        else:
+            check(lib().qx_exec_create_gemm_i16i32_route(ctypes.byref(h), M, N, K, batch, bound_a, bound_b,
+                                                         _route(route)))
         return cls(h, (batch, M, N), torch.int32, 2)
 
     @classmethod
     def gemm_i32_s24(cls, M, N, K, batch=1, route="auto"):
         torch = _torch()
         h = ctypes.c_void_p()
-        check(lib().qx_exec_create_gemm_i32_s24(ctypes.byref(h), M, N, K, batch, _route(route)))
+        if _route(route) == 0:
+            check(lib().qx_exec_create_gemm_i32_s24(ctypes.byref(h), M, N, K, batch))
+        else:
+            check(lib().qx_exec_create_gemm_i32_s24_route(ctypes.byref(h), M, N, K, batch, _route(route)))
         return cls(h, (batch, M, N), torch.int32, 2)
 
     @classmethod
     def conv2d(cls, N, Ci, H, W, Co, KH, KW, stride=1, pad=0, bound_x=0, bound_w=0, route="auto"):
         torch = _torch()
         h = ctypes.c_void_p()
-        check(lib().qx_exec_create_conv2d(ctypes.byref(h), N, Ci, H, W, Co, KH, KW, stride, pad,
-                                          bound_x, bound_w, _route(route)))
+        if _route(route) == 0:
+            check(lib().qx_exec_create_conv2d(ctypes.byref(h), N, Ci, H, W, Co, KH, KW, stride, pad,
+                                              bound_x, bound_w))
+        else:
+            check(lib().qx_exec_create_conv2d_route(ctypes.byref(h), N, Ci, H, W, Co, KH, KW, stride, pad,
+                                                    bound_x, bound_w, _route(route)))
         Ho, Wo = conv_out_hw(H, W, KH, KW, stride, pad)
         return cls(h, (N, Co, Ho, Wo), torch.int32, 2)
 
@@ -445,8 +462,11 @@ class Executor:
     def attn(cls, dtype: str, L, d, bound=0, route="auto"):
         torch = _torch()
         h = ctypes.c_void_p()
-        check(lib().qx_exec_create_attn(ctypes.byref(h), DT_F32 if dtype == "f32" else DT_I32, L, d,
-                                        bound, _route(route)))
+        dt = DT_F32 if dtype == "f32" else DT_I32
+        if _route(route) == 0:
+            check(lib().qx_exec_create_attn(ctypes.byref(h), dt, L, d, bound))
+        else:
+            check(lib().qx_exec_create_attn_route(ctypes.byref(h), dt, L, d, bound, _route(route)))
         return cls(h, (L, d), torch.float32 if dtype == "f32" else torch.int32, 3)
 
     @classmethod
@@ -510,3 +530,32 @@ class Executor:
                 lib().qx_exec_destroy(self._h)
         except Exception:
             pass
+
+
+# ---------------------------------------------------------------------------
+# test seams (include/qx_testing.h): no result is computed under the double
+# ---------------------------------------------------------------------------
+COUNTERS = ("allocs", "frees", "streams", "streams_freed", "events", "events_freed", "launches",
+            "live_handles")
+
+
+def testing_host_double(on: bool) -> None:
+    """Switch executor creation to the host-only runtime double (or back)."""
+    check(lib().qx_testing_host_double(1 if on else 0))
+
+
+def testing_counters() -> dict:
+    vals = (ctypes.c_int64 * len(COUNTERS))()
+    lib().qx_testing_counters(vals, len(COUNTERS))
+    return dict(zip(COUNTERS, list(vals)))
+
+
+class HostTensor:
+    """Stand-in for a device tensor under the host double: a pointer, a
+    shape and a dtype (nothing is ever read or written through it)."""
+
+    def __init__(self, ptr: int, shape, dtype=None):
+        self.ptr, self.shape, self.dtype = ptr, tuple(shape), dtype
+
+    def data_ptr(self) -> int:
+        return self.ptr

@@ -336,3 +336,28 @@ def test_bf16_operand_format_for_small_bounds():
     assert qx.plan_conv2d(8, 64, 56, 56, 128, 3, 3, 1, 1, 256, 256)["operand_format"] == 0
     # the chunk rule does not depend on the operand format
     assert qx.plan_gemm_i16i32(4096, 4096, 4096, 1, 256, 256)["chunk"] == 256
+
+
+def test_nt_route_holds_32_bit_panel_offsets():
+    # The encode + NT kernel addresses a 256-row operand panel with 32-bit
+    # offsets; from Kp = 2^22 on the register-staged kernel (64-bit
+    # addressing, no workspace) takes over.
+    below = qx.plan_gemm_i16i32(256, 256, (1 << 22) - 64, 1, 256, 256)
+    assert below["kernels"] == 3 and below["workspace_bytes"] > 0
+    for K in ((1 << 22) - 63, 1 << 22, 1 << 24):
+        p = qx.plan_gemm_i16i32(256, 256, K, 1, 256, 256)
+        assert p["route_name"] == "f16_exact" and p["kernels"] == 1 and p["workspace_bytes"] == 0, (K, p)
+
+
+def test_fill_grid_is_capped_for_huge_outputs():
+    # K == 0 clears the output; from 2^32 words the launch must still fit
+    # the grid limits (checked by the host double's launch check).
+    qx.lib().qx_release_cache()
+    qx.testing_host_double(True)
+    try:
+        for M, N, batch in ((1 << 16, 1 << 16, 1), (1 << 16, 1 << 16, 3), (1 << 20, 1 << 13, 1)):
+            with qx.Executor.gemm_i16i32(M, N, 0, batch, 256, 256) as ex:
+                assert ex.plan()["kernels"] == 1
+                ex.run_ptrs([1 << 40, 1 << 41], 1 << 44, 0)
+    finally:
+        qx.testing_host_double(False)
