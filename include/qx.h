@@ -185,6 +185,25 @@ qx_status pool2x2(int32_t kind, const void* x, void* y, int64_t N, int64_t C, in
 qx_status attn_core(qx_attn_dtype dt, const void* Q, const void* K, const void* V, void* O,
                     int64_t L, int64_t d, int32_t bound, void* stream);
 
+/* qgemm_i16i32 for callers that cannot allocate device memory: code under
+ * HIP graph capture, serving loops and harnesses that forbid allocation.
+ * Same arguments, layouts, result (bit for bit) and errors as qgemm_i16i32,
+ * and it calls no allocation routine: its workspace is a fixed per-device
+ * scratch array of QX_NOALLOC_SCRATCH_BYTES, reserved when the library is
+ * loaded on that device and held until the process ends.  Problems whose
+ * encoded operands do not fit the scratch run the register-staged kernels
+ * (no operand copies); one that needs more scratch even then returns
+ * QX_ERR_UNSUPPORTED before anything is enqueued.  Every launch rewrites the
+ * scratch it reads, so earlier calls' contents never leak into a result.
+ * All calls on one GPU share its scratch: calls that overlap in time on that
+ * GPU (other streams, other threads) race and must be serialised by the
+ * caller.  Batched problems run every launch on `stream` in order (no side
+ * stream).  The host keeps a small plan per distinct request. */
+#define QX_NOALLOC_SCRATCH_BYTES (64u << 20)
+qx_status qgemm_i16i32_noalloc(const int16_t* A, const int16_t* B, int32_t* C,
+                               int64_t M, int64_t N, int64_t K, int64_t batch,
+                               int32_t bound_a, int32_t bound_b, void* stream);
+
 /* Multi-head scaled dot-product attention with softmax, FP32 (the SDPA
  * attention baseline of Table 2, whose footnote gives scale 1.0; the
  * attention core with a softmax, Discussion).  For every head b < BH:

@@ -18,7 +18,8 @@ ROOT = os.path.dirname(HERE)
 OUT = os.path.join(HERE, "libqx.so")
 BUILD_DIR = os.path.join(ROOT, "_build")
 
-SOURCES = ["api.cpp", "k_gemm.hip", "k_gemm_nt.hip", "k_valu.hip", "k_attn.hip", "k_reduce.hip"]
+SOURCES = ["api.cpp", "k_gemm.hip", "k_gemm_nt.hip", "k_valu.hip", "k_attn.hip", "k_reduce.hip",
+           "scratch.hip"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = [

@@ -487,7 +487,7 @@ qx_status check_dims(std::initializer_list<std::pair<const char*, int64_t>> dims
 }
 
 qx_status plan_gemm(Plan* pl, bool s24, int64_t M, int64_t N, int64_t K, int64_t batch, int32_t bound_a,
-                    int32_t bound_b, int32_t route) {
+                    int32_t bound_b, int32_t route, bool allow_nt = true) {
     qx_status st = check_dims({{"M", M}, {"N", N}, {"K", K}, {"batch", batch}});
     if (st) return st;
     if (batch > kMaxBatch) return fail(QX_ERR_UNSUPPORTED, "batch = %lld exceeds 65535", (long long)batch);
@@ -515,7 +515,7 @@ qx_status plan_gemm(Plan* pl, bool s24, int64_t M, int64_t N, int64_t K, int64_t
     s.a_bind = BIND_IN0; s.b_bind = BIND_IN1; s.b_ws_off = 0;
     s.lda = K; s.ldb = N; s.ldc = N; s.sA = M * K; s.sB = K * N; s.sC = M * N;
     s.out_mode = OUT_ROWMAJOR; s.hw = 1;
-    s.allow_nt = true;
+    s.allow_nt = allow_nt;
     uint64_t ws = 0;
     Plan scratch;
     scratch.info = pl->info;
@@ -1575,6 +1575,20 @@ qx_status make_exec(Plan&& pl, qx_exec* out) {
     return QX_OK;
 }
 
+// What a run needs: the plan, the runtime, the workspace (with the
+// validation flag word at flag_off) and, for plans that overlap launches, the
+// side stream and events.  Without a side stream every launch goes to the
+// caller's stream in plan order.
+struct RunCtx {
+    const Plan* plan;
+    const RtTable* rt;
+    void* ws;
+    uint64_t flag_off;
+    hipStream_t side;
+    const hipEvent_t* evs;
+    int device;
+};
+
 qx_status launch_direct(const RtTable& rt, LaunchRec& r, hipStream_t s) {
     void* args[1] = {r.blob};
     g_count[C_LAUNCHES]++;
@@ -1584,10 +1598,10 @@ qx_status launch_direct(const RtTable& rt, LaunchRec& r, hipStream_t s) {
 
 // QX_VALIDATE: scan every bounded operand, wait, and refuse the run if one
 // is outside its declared bound.
-qx_status validate_ranges(qx_exec h, const void* const* inputs, hipStream_t s) {
-    const Plan& pl = h->plan;
-    const RtTable& rt = *h->rt;
-    uint32_t* flag = (uint32_t*)((char*)h->ws + h->flag_off);
+qx_status validate_ranges(const RunCtx& c, const void* const* inputs, hipStream_t s) {
+    const Plan& pl = *c.plan;
+    const RtTable& rt = *c.rt;
+    uint32_t* flag = (uint32_t*)((char*)c.ws + c.flag_off);
     FillParams f{};
     f.ptr = flag;
     f.n32 = 1;
@@ -1621,11 +1635,10 @@ qx_status validate_ranges(qx_exec h, const void* const* inputs, hipStream_t s) {
     return QX_OK;
 }
 
-qx_status run_exec(qx_exec h, const void* const* inputs, void* output, void* stream,
-                   std::vector<hipEvent_t>* evs = nullptr) {
-    if (!is_live(h) || h->magic != kMagic) return fail(QX_ERR_INVALID_ARG, "invalid executor handle");
-    const Plan& pl = h->plan;
-    const RtTable& rt = *h->rt;
+qx_status run_plan(const RunCtx& c, const void* const* inputs, void* output, void* stream,
+                   std::vector<hipEvent_t>* evs) {
+    const Plan& pl = *c.plan;
+    const RtTable& rt = *c.rt;
     if (pl.launches.empty()) return QX_OK;
     // Only inputs some launch reads are required (a K == 0 GEMM just clears
     // its output and may get NULL operands).
@@ -1646,21 +1659,21 @@ qx_status run_exec(qx_exec h, const void* const* inputs, void* output, void* str
     int dev = -1;
     hipError_t e = rt.get_device(&dev);
     if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
-    if (dev != h->device)
-        return fail(QX_ERR_INVALID_ARG, "handle was created on device %d, current device is %d", h->device, dev);
+    if (dev != c.device)
+        return fail(QX_ERR_INVALID_ARG, "plan was made for device %d, current device is %d", c.device, dev);
     hipStream_t s = (hipStream_t)stream;
     const char* val = getenv("QX_VALIDATE");
     if (val && val[0] == '1' && !pl.checks.empty()) {
-        const qx_status st = validate_ranges(h, inputs, s);
+        const qx_status st = validate_ranges(c, inputs, s);
         if (st) return st;
     }
     // Overlapped plans fork to the side stream after everything already on
     // the caller's stream and join back at the end.  Per-launch timing runs
     // every launch in plan order on the caller's stream instead.
-    const bool lanes = pl.n_events > 0 && !evs;
+    const bool lanes = pl.n_events > 0 && !evs && c.side;
     if (lanes) {
-        if ((e = rt.event_record(h->evs[0], s)) != hipSuccess) return hip_fail(e, "hipEventRecord");
-        if ((e = rt.stream_wait(h->side, h->evs[0])) != hipSuccess) return hip_fail(e, "hipStreamWaitEvent");
+        if ((e = rt.event_record(c.evs[0], s)) != hipSuccess) return hip_fail(e, "hipEventRecord");
+        if ((e = rt.stream_wait(c.side, c.evs[0])) != hipSuccess) return hip_fail(e, "hipStreamWaitEvent");
     }
     for (const LaunchRec& r0 : pl.launches) {
         LaunchRec r = r0;
@@ -1669,28 +1682,36 @@ qx_status run_exec(qx_exec h, const void* const* inputs, void* output, void* str
             const char* ptr = nullptr;
             if (sl.bind < BIND_OUT) ptr = (const char*)inputs[sl.bind];
             else if (sl.bind == BIND_OUT) ptr = (const char*)output;
-            else ptr = (const char*)h->ws;
+            else ptr = (const char*)c.ws;
             ptr += sl.add;
             memcpy(r.blob + sl.off, &ptr, sizeof(void*));
         }
         void* args[1] = {r.blob};
         const size_t li = (size_t)(&r0 - pl.launches.data());
-        hipStream_t ls = (lanes && r.lane) ? h->side : s;
-        if (lanes && r.wait_ev >= 0 && (e = rt.stream_wait(ls, h->evs[r.wait_ev])) != hipSuccess)
+        hipStream_t ls = (lanes && r.lane) ? c.side : s;
+        if (lanes && r.wait_ev >= 0 && (e = rt.stream_wait(ls, c.evs[r.wait_ev])) != hipSuccess)
             return hip_fail(e, "hipStreamWaitEvent");
         if (evs && (e = rt.event_record((*evs)[2 * li], s)) != hipSuccess) return hip_fail(e, "hipEventRecord");
         g_count[C_LAUNCHES]++;
         e = rt.launch(r, args, ls);
         if (e != hipSuccess) return hip_fail(e, r.name);
         if (evs && (e = rt.event_record((*evs)[2 * li + 1], s)) != hipSuccess) return hip_fail(e, "hipEventRecord");
-        if (lanes && r.rec_ev >= 0 && (e = rt.event_record(h->evs[r.rec_ev], ls)) != hipSuccess)
+        if (lanes && r.rec_ev >= 0 && (e = rt.event_record(c.evs[r.rec_ev], ls)) != hipSuccess)
             return hip_fail(e, "hipEventRecord");
     }
     if (lanes) {
-        if ((e = rt.event_record(h->evs.back(), h->side)) != hipSuccess) return hip_fail(e, "hipEventRecord");
-        if ((e = rt.stream_wait(s, h->evs.back())) != hipSuccess) return hip_fail(e, "hipStreamWaitEvent");
+        const hipEvent_t join = c.evs[pl.n_events + 1];
+        if ((e = rt.event_record(join, c.side)) != hipSuccess) return hip_fail(e, "hipEventRecord");
+        if ((e = rt.stream_wait(s, join)) != hipSuccess) return hip_fail(e, "hipStreamWaitEvent");
     }
     return QX_OK;
+}
+
+qx_status run_exec(qx_exec h, const void* const* inputs, void* output, void* stream,
+                   std::vector<hipEvent_t>* evs = nullptr) {
+    if (!is_live(h) || h->magic != kMagic) return fail(QX_ERR_INVALID_ARG, "invalid executor handle");
+    const RunCtx c{&h->plan, h->rt, h->ws, h->flag_off, h->side, h->evs.data(), h->device};
+    return run_plan(c, inputs, output, stream, evs);
 }
 
 qx_status profile_exec(qx_exec h, const void* const* inputs, void* output, void* stream, int32_t reps,
@@ -1772,6 +1793,23 @@ qx_status oneshot(const Key& key0, MakePlan make_plan, const void* const* inputs
     return run_exec(h, inputs, output, stream);
 }
 
+}  // namespace
+
+// Allocation-free GEMM: plans are cached on the host per request; the
+// workspace is the per-device scratch array, whose device address is looked
+// up (and the device checked) on the first call on each device.
+namespace {
+typedef std::tuple<int64_t, int64_t, int64_t, int64_t, int32_t, int32_t> NoAllocKey;
+std::mutex g_noalloc_mu;
+std::map<NoAllocKey, Plan>* g_noalloc_plans = new std::map<NoAllocKey, Plan>();
+std::atomic<bool> g_noalloc_dev_ok[64];
+
+static_assert(QX_NOALLOC_SCRATCH_BYTES == kScratchBytes, "scratch size in the header and the library");
+
+uint64_t scratch_need(const Plan& pl) {
+    const uint64_t ws = (uint64_t)pl.info.workspace_bytes;
+    return pl.checks.empty() ? ws : round_up(ws, 256) + 256;
+}
 }  // namespace
 
 // ---------------------------------------------------------------------------
@@ -2155,6 +2193,54 @@ qx_status attn_core(qx_attn_dtype dt, const void* Q, const void* K, const void* 
     Key key{dt == QX_DT_F32 ? OP_ATTN_F32 : OP_ATTN_I32, 0, L, d, bound, 0, 0, 0, 0, 0, 0, 0, 0, 0,
             (uintptr_t)stream};
     return oneshot(key, [&](Plan* pl) { return plan_attn(pl, dt, L, d, bound, R_AUTO); }, in, O, stream);
+}
+
+qx_status qgemm_i16i32_noalloc(const int16_t* A, const int16_t* B, int32_t* C, int64_t M, int64_t N, int64_t K,
+                               int64_t batch, int32_t bound_a, int32_t bound_b, void* stream) {
+    g_err.clear();
+    const Plan* pl = nullptr;
+    {
+        std::lock_guard<std::mutex> lk(g_noalloc_mu);
+        const NoAllocKey key{M, N, K, batch, bound_a, bound_b};
+        auto it = g_noalloc_plans->find(key);
+        if (it == g_noalloc_plans->end()) {
+            Plan p;
+            qx_status st = plan_gemm(&p, false, M, N, K, batch, bound_a, bound_b, R_AUTO);
+            if (st) return st;
+            if (scratch_need(p) > kScratchBytes) {
+                // the encoded operands do not fit: the register-staged
+                // kernels convert while staging and need only the row and
+                // column sums of the offset routes
+                Plan q;
+                if ((st = plan_gemm(&q, false, M, N, K, batch, bound_a, bound_b, R_AUTO, false))) return st;
+                p = std::move(q);
+            }
+            if (scratch_need(p) > kScratchBytes)
+                return fail(QX_ERR_UNSUPPORTED,
+                            "this GEMM needs %llu bytes of workspace; the allocation-free entry point has %llu",
+                            (unsigned long long)scratch_need(p), (unsigned long long)kScratchBytes);
+            it = g_noalloc_plans->emplace(key, std::move(p)).first;
+        }
+        pl = &it->second;
+    }
+    if (!empty_ok(A, M * K * batch) || !empty_ok(B, K * N * batch) || !empty_ok(C, M * N * batch))
+        return fail(QX_ERR_INVALID_ARG, "NULL pointer for a non-empty operand");
+    if (pl->launches.empty()) return QX_OK;
+    int dev = -1;
+    hipError_t e = kHip.get_device(&dev);
+    if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+    if (dev < 0 || dev >= 64) return fail(QX_ERR_UNSUPPORTED, "device %d: at most 64 devices", dev);
+    if (!g_noalloc_dev_ok[dev].load()) {
+        int d2 = dev;
+        qx_status st = check_device(kHip, &d2);
+        if (st) return st;
+        g_noalloc_dev_ok[dev].store(true);
+    }
+    void* ws = nullptr;
+    if ((e = scratch_device_ptr(dev, &ws)) != hipSuccess) return hip_fail(e, "scratch lookup");
+    const void* in[2] = {A, B};
+    const RunCtx c{pl, &kHip, ws, round_up((uint64_t)pl->info.workspace_bytes, 256), nullptr, nullptr, dev};
+    return run_plan(c, in, C, stream, nullptr);
 }
 
 qx_status sdpa_f32(const float* Q, const float* K, const float* V, float* O, int64_t BH, int64_t L, int64_t d,

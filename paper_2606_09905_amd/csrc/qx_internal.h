@@ -322,6 +322,12 @@ enum Route : int32_t {
     R_F32_MFMA = 12, R_F32_VALU = 13,   // FP32 convolution: fp32 matrix cores / vector ALU
 };
 
+// Fixed device scratch of the allocation-free GEMM entry point: its size,
+// and its device address on device `dev` (looked up once per device, with
+// that device current).
+constexpr uint64_t kScratchBytes = (uint64_t)64 << 20;
+hipError_t scratch_device_ptr(int dev, void** out);
+
 // Integer GEMM main kernel for an MFMA route; returns false if unsupported.
 bool build_gemm_mfma(int32_t route, const GemmParams& p, int batch, LaunchRec* rec,
                      int* tile_m, int* tile_n, int* tile_k);

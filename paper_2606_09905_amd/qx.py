@@ -71,6 +71,7 @@ def lib() -> ctypes.CDLL:
         sig = {
             "qgemm_i16i32": [_p, _p, _p, _i64, _i64, _i64, _i64, _i32, _i32, _p],
             "qgemm_i32_s24": [_p, _p, _p, _i64, _i64, _i64, _i64, _p],
+            "qgemm_i16i32_noalloc": [_p, _p, _p, _i64, _i64, _i64, _i64, _i32, _i32, _p],
             "conv2d_gemm": [_p, _p, _p] + [_i64] * 9 + [_i32, _i32, _p],
             "conv2d_gemm_t": [_i32, _p, _p, _p] + [_i64] * 9 + [_p],
             "attn_core": [_i32, _p, _p, _p, _p, _i64, _i64, _i32, _p],
@@ -124,6 +125,7 @@ def header_functions(path: str = HEADER_PATH) -> list[str]:
     with open(path) as f:
         text = f.read()
     text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    text = re.sub(r"^\s*#.*$", "", text, flags=re.M)     # preprocessor lines
     return sorted(set(re.findall(r"\b([A-Za-z_]\w*)\s*\(", text)) -
                   {"if", "defined", "sizeof"})
 
@@ -189,6 +191,19 @@ def qgemm_i16i32(A, B, bound_a: int = 0, bound_b: int = 0, out=None, stream=None
     check(lib().qgemm_i16i32(_dev_tensor(A, torch.int16, "A"), _dev_tensor(B, torch.int16, "B"),
                              _dev_tensor(out, torch.int32, "C"), M, N, K, batch,
                              int(bound_a), int(bound_b), _stream(stream)))
+    return out
+
+
+def qgemm_i16i32_noalloc(A, B, out, bound_a: int = 0, bound_b: int = 0, stream=None):
+    """qgemm_i16i32 into a caller-provided `out`, with no device allocation
+    (the library's fixed per-device scratch serves as workspace)."""
+    torch = _torch()
+    batch, M, N, K, shape = _gemm_shapes(A, B)
+    if tuple(out.shape) != tuple(shape):
+        raise ValueError(f"out must have shape {shape}")
+    check(lib().qgemm_i16i32_noalloc(_dev_tensor(A, torch.int16, "A"), _dev_tensor(B, torch.int16, "B"),
+                                     _dev_tensor(out, torch.int32, "C"), M, N, K, batch,
+                                     int(bound_a), int(bound_b), _stream(stream)))
     return out
 
 
