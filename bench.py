@@ -90,6 +90,8 @@ def parse():
     ap.add_argument("--all", action="store_true", help="also measure every workload")
     ap.add_argument("--all-out", default="bench_all.json", help="where --all writes its per-workload results")
     ap.add_argument("--no-cpu", action="store_true", help="skip the oracle CPU baseline")
+    ap.add_argument("--no-configs", action="store_true",
+                    help="skip the per-configuration measurements of the other workloads")
     ap.add_argument("--oracle-all", action="store_true",
                     help="time the CPU oracle on every workload (host only) and exit")
     ap.add_argument("--copy-calibration", action="store_true",
@@ -99,12 +101,12 @@ def parse():
     return ap.parse_args()
 
 
-def make_executor(w, qx):
+def make_executor(w, qx, route="auto"):
     d = w.dims
     if w.op == "gemm_i16i32":
-        return qx.Executor.gemm_i16i32(d["M"], d["N"], d["K"], d["batch"], w.bound, w.bound)
+        return qx.Executor.gemm_i16i32(d["M"], d["N"], d["K"], d["batch"], w.bound, w.bound, route)
     if w.op == "gemm_i32_s24":
-        return qx.Executor.gemm_i32_s24(d["M"], d["N"], d["K"], d["batch"])
+        return qx.Executor.gemm_i32_s24(d["M"], d["N"], d["K"], d["batch"], route)
     if w.op == "conv2d":
         return qx.Executor.conv2d(d["N"], d["Ci"], d["H"], d["W"], d["Co"], d["KH"], d["KW"],
                                   d["stride"], d["pad"], w.bound, w.bound)
@@ -126,12 +128,15 @@ def make_executor(w, qx):
     raise ValueError(w.op)
 
 
-def measure(w, steps, warmup, torch, qx):
-    """Setup, cached steady state and execute-only time of one workload."""
-    inputs = [torch.from_numpy(np.ascontiguousarray(a)).cuda() for a in w.generate()]
+def measure(w, steps, warmup, torch, qx, route="auto", inputs=None, sustain_ms=0.0):
+    """Setup, cached steady state and execute-only time of one workload.
+    With sustain_ms > 0 a further back-to-back loop of at least that many
+    milliseconds (and 20 runs) gives the sustained-clock step time."""
+    if inputs is None:
+        inputs = [torch.from_numpy(np.ascontiguousarray(a)).cuda() for a in w.generate()]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    ex = make_executor(w, qx)
+    ex = make_executor(w, qx, route)
     setup_ms = (time.perf_counter() - t0) * 1e3
     plan = ex.plan()
     out = torch.empty(ex.out_shape, dtype=ex.out_dtype, device="cuda")
@@ -146,6 +151,15 @@ def measure(w, steps, warmup, torch, qx):
         ex.run_ptrs(ptrs, out.data_ptr(), stream)
     torch.cuda.synchronize()
     cached_s = (time.perf_counter() - t0) / steps
+    sustained = None
+    if sustain_ms > 0:
+        reps = max(20, int(np.ceil(sustain_ms / max(cached_s * 1e3, 1e-3))))
+        t0 = time.perf_counter()
+        for _ in range(reps):
+            ex.run_ptrs(ptrs, out.data_ptr(), stream)
+        torch.cuda.synchronize()
+        dt = time.perf_counter() - t0
+        sustained = {"runs": reps, "total_ms": dt * 1e3, "ms_per_step": dt * 1e3 / reps}
     # execute-only: events around each run on the same stream
     evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
            for _ in range(steps)]
@@ -161,6 +175,7 @@ def measure(w, steps, warmup, torch, qx):
     ex.close()
     return {
         "setup_ms": setup_ms,
+        "sustained": sustained,
         "cached_ms": cached_s * 1e3,
         "exec_ms_mean": float(np.mean(exec_ms)),
         "exec_ms_median": float(np.median(exec_ms)),
@@ -170,10 +185,26 @@ def measure(w, steps, warmup, torch, qx):
     }
 
 
+def cpu_model() -> str:
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
 def cpu_baseline(w, rows):
     """The oracle on a bounded sample of the headline GEMM: `rows` rows of A
-    against the full B, on the host cores (OpenMP)."""
+    against the full B, on the host cores (OpenMP); then the oracle on one
+    thread over the whole of the small GEMM workloads (256^3 INT16, 1024^3
+    and 16 x 512^3 smul24)."""
     from oracle import oracle as orc
+    from paper_2606_09905_amd.workloads import WORKLOADS
+    cores = int(os.environ.get("OMP_NUM_THREADS", 0)) or len(os.sched_getaffinity(0))
+    orc.set_threads(cores)
     A, B = w.generate()
     A = np.ascontiguousarray(A[0, :rows])
     orc.gemm_i16i32(A[:2], B[0])          # build/load outside the timed region
@@ -182,10 +213,24 @@ def cpu_baseline(w, rows):
     dt = time.perf_counter() - t0
     d = w.dims
     ops = 2.0 * rows * d["N"] * d["K"]
-    cores = int(os.environ.get("OMP_NUM_THREADS", 0)) or len(os.sched_getaffinity(0))
+    one = {}
+    for name in ("gemm_i16_256", "gemm_s24_1024", "gemm_s24_16x512"):
+        sw = WORKLOADS[name]
+        a, b = sw.generate()
+        f = orc.gemm_i16i32 if sw.op == "gemm_i16i32" else orc.gemm_i32_s24
+        for threads in (1, cores):
+            orc.set_threads(threads)
+            t1 = time.perf_counter()
+            f(a, b)
+            t = time.perf_counter() - t1
+            one.setdefault(name, {})["threads_1" if threads == 1 else f"threads_{cores}"] = {
+                "seconds": round(t, 4), "gops": round(sw.ops / t / 1e9, 3)}
+    orc.set_threads(cores)
     return {
         "value": ops / dt / 1e9, "unit": "GOPS", "cores": cores, "kind": "oracle",
         "sample": f"{rows} of {d['M']} rows of A x full B ({ops:.3e} ops, {dt:.1f} s)",
+        "cpu_model": cpu_model(),
+        "small_gemms_whole": one,
     }
 
 
@@ -250,6 +295,88 @@ def oracle_timings(workloads):
     return out
 
 
+# Unit and peak of the dominant kernel for each route: the MFMA peak of the
+# operand type the matrix cores run, or the vector ALU's integer rate
+# (256 CUs x 64 lanes x 2.4 GHz; v_mad_i32_i24 is 2 ops per lane and cycle,
+# v_dot2_i32_i16 4).
+ROUTE_PEAK = {
+    "f16_exact": ("mfma", "f16"), "i8_direct": ("mfma", "i8"), "i8_karatsuba": ("mfma", "i8"),
+    "i8_offset4": ("mfma", "i8"), "s24_i8limb": ("mfma", "i8"), "attn_i32_mfma": ("mfma", "i8"),
+    "attn_f32_mfma": ("mfma", "f32"), "f32_mfma": ("mfma", "f32"),
+    "s24_valu": ("alu", "i32_valu"), "valu_dot2": ("alu", "dot2_valu"), "attn_i32_valu": ("alu", "i32_valu"),
+}
+PEAK.update({"i32_valu": 78.6, "dot2_valu": 157.3})
+PEAK_UNIT = {"f16": "TFLOP/s", "f32": "TFLOP/s", "i8": "TOP/s", "i32_valu": "TOP/s", "dot2_valu": "TOP/s"}
+
+# The configurations the metric is quoted on, by workload, and the forced
+# vector-ALU routes measured beside the matrix-core ones.
+CONFIGS = [
+    ("C1", "gemm_i16_256", "auto"), ("C1_valu", "gemm_i16_256", "valu_dot2"),
+    ("C2a", "gemm_s24_1024", "auto"), ("C2a_valu", "gemm_s24_1024", "s24_valu"),
+    ("C2b", "gemm_s24_16x512", "auto"), ("C2b_valu", "gemm_s24_16x512", "s24_valu"),
+    ("C3", "conv_8x64x56x56_128_3x3", "auto"),
+    ("C4f", "attn_f32_4096x64", "auto"), ("C4i", "attn_i32_4096x64", "auto"),
+    ("C5a", "gemm_i16_8192", "auto"), ("C5b", "gemm_i16_64x2048", "auto"),
+]
+
+
+def summarize(w, r):
+    """Dominant kernel of a measured workload (the one with the most
+    execute-only time per step) and its rate against its unit's peak.  A step
+    may split it into several launches (column panels or batch groups);
+    together they do the whole algorithmic work, so the achieved rate is that
+    work over their summed duration."""
+    per_name = {}
+    for n, v in r["kernels"]:
+        c = per_name.setdefault(n, [0.0, 0])
+        c[0] += v
+        c[1] += 1
+    dom_name, (dom_ms, dom_launches) = max(per_name.items(), key=lambda kv: kv[1][0])
+    route = r["plan"]["route_name"]
+    bound, unit = ROUTE_PEAK.get(route, ("mfma", "f16"))
+    achieved = w.ops / (dom_ms / 1e3) / 1e12
+    products = 2.0 if route == "attn_i32_mfma" else float(max(r["plan"]["products"], 1))
+    return {"route": route, "bound": bound, "peak_name": unit, "peak": PEAK[unit], "peak_unit": PEAK_UNIT[unit],
+            "achieved": achieved, "frac": achieved / PEAK[unit],
+            "issued_frac": achieved * products / PEAK[unit] if bound == "mfma" and unit == "i8" else None,
+            "kernel": dom_name, "kernel_ms": dom_ms, "kernel_launches": dom_launches,
+            "kernels_ms": {n: round(v[0], 4) for n, v in per_name.items()},
+            "launches": {n: v[1] for n, v in per_name.items()}}
+
+
+def measure_configs(args, torch, qx, workloads, headline, head_sm, head_gops):
+    """Every configuration the metric is quoted on: cached and execute-only
+    GOPS and the dominant kernel's fraction of its unit's peak."""
+    out = {}
+    cache = {}
+    for tag, name, route in CONFIGS:
+        wl = workloads[name]
+        if name == headline and route == "auto":
+            sm, gops_c, gops_e = head_sm, head_gops, None
+        else:
+            if name not in cache:
+                cache.clear()
+                torch.cuda.empty_cache()
+                cache[name] = [torch.from_numpy(np.ascontiguousarray(a)).cuda() for a in wl.generate()]
+            m = measure(wl, max(args.steps, 20), max(args.warmup, 5), torch, qx, route=route, inputs=cache[name])
+            sm = summarize(wl, m)
+            gops_c = wl.ops / (m["cached_ms"] / 1e3) / 1e9
+            gops_e = wl.ops / (m["exec_ms_mean"] / 1e3) / 1e9
+        e = {"workload": name, "route": sm["route"], "gops_cached": round(gops_c, 1),
+             "gops_exec": None if gops_e is None else round(gops_e, 1),
+             "kernel": sm["kernel"], "kernel_ms": round(sm["kernel_ms"], 4),
+             "bound": sm["bound"], "peak": sm["peak"], "peak_unit": sm["peak_unit"],
+             "kernel_frac": round(sm["frac"], 4)}
+        if sm["issued_frac"] is not None:
+            e["kernel_issued_frac"] = round(sm["issued_frac"], 4)
+        out[tag] = e
+        print(f"[bench] {tag} {name} ({sm['route']}): {gops_c:.1f} GOPS cached, kernel {sm['kernel']} "
+              f"{sm['kernel_ms'] * 1e3:.1f} us = {sm['frac']:.3f} of {sm['peak_name']} peak",
+              file=sys.stderr, flush=True)
+    cache.clear()
+    return out
+
+
 def main():
     args = parse()
     if args.oracle_all:
@@ -272,26 +399,11 @@ def main():
         return
     qx.lib()
     w = WORKLOADS[args.workload]
-    r = measure(w, args.steps, args.warmup, torch, qx)
+    r = measure(w, args.steps, args.warmup, torch, qx, sustain_ms=200.0)
     ms = r["cached_ms"]
     gops = w.ops / (ms / 1e3) / 1e9
-    # dominant kernel: the one with the most execute-only time per step (the
-    # contraction).  A step may split it into several launches (column panels
-    # or batch groups); together they do the whole 2*M*N*K*batch, so the
-    # achieved rate is that work over their summed duration (equivalently:
-    # work per launch over the mean launch duration).
-    per_name = {}
-    for n, v in r["kernels"]:
-        c = per_name.setdefault(n, [0.0, 0])
-        c[0] += v
-        c[1] += 1
-    dom_name, (dom_ms, dom_launches) = max(per_name.items(), key=lambda kv: kv[1][0])
-    achieved_tflops = w.ops / (dom_ms / 1e3) / 1e12
-    route = r["plan"]["route_name"]
-    unit_peak = {"f16_exact": "f16", "i8_direct": "i8", "i8_karatsuba": "i8", "i8_offset4": "i8",
-                 "s24_i8limb": "i8", "attn_f32_mfma": "f32", "attn_i32_mfma": "i8",
-                 "f32_mfma": "f32"}.get(route, "f16")
-    peak = PEAK[unit_peak]
+    sm = summarize(w, r)
+    route = sm["route"]
     line = {
         "metric": METRIC,
         "value": round(gops, 1),
@@ -313,23 +425,29 @@ def main():
         "config": {"workload": w.name, **w.dims, "operand_range": [w.lo, w.hi], "seed": w.seed,
                    "route": route, "chunk": r["plan"]["chunk"]},
         "roofline": {
-            "bound": "mfma",
-            "achieved": round(achieved_tflops, 1),
-            "peak": peak,
-            "unit": "TFLOP/s" if unit_peak in ("f16", "f32") else "TOP/s",
-            "frac": round(achieved_tflops / peak, 4),
-            "traffic": traffic_bytes(dom_name, dom_launches),
-            "kernel": dom_name,
-            "kernel_ms": round(dom_ms, 4),
-            "kernel_launches": dom_launches,
-            "frac_of_int8_peak": round(achieved_tflops / PEAK["i8"], 4),
+            "bound": sm["bound"],
+            "achieved": round(sm["achieved"], 1),
+            "peak": sm["peak"],
+            "unit": sm["peak_unit"],
+            "frac": round(sm["frac"], 4),
+            "traffic": traffic_bytes(sm["kernel"], sm["kernel_launches"]),
+            "kernel": sm["kernel"],
+            "kernel_ms": round(sm["kernel_ms"], 4),
+            "kernel_launches": sm["kernel_launches"],
+            "frac_of_int8_peak": round(sm["achieved"] / PEAK["i8"], 4),
         },
         "timing": {"setup_ms": round(r["setup_ms"], 2), "cached_ms": round(ms, 4),
                    "exec_ms": round(r["exec_ms_mean"], 4),
-                   "kernels_ms": {n: round(v[0], 4) for n, v in per_name.items()},
-                   "launches": {n: v[1] for n, v in per_name.items()},
-                   "end_to_end_frac_of_int8_peak": round(gops / 1e3 / PEAK["i8"], 4)},
+                   "kernels_ms": sm["kernels_ms"],
+                   "launches": sm["launches"],
+                   "end_to_end_frac_of_int8_peak": round(gops / 1e3 / PEAK["i8"], 4),
+                   # a further >= 200 ms back-to-back loop (sustained clocks),
+                   # outside the K timed steps
+                   "sustained": {k: round(v, 4) if isinstance(v, float) else v
+                                 for k, v in (r["sustained"] or {}).items()}},
     }
+    if not args.no_configs:
+        line["configs"] = measure_configs(args, torch, qx, WORKLOADS, w.name, sm, gops)
     if not args.no_cpu:
         line["cpu_baseline"] = cpu_baseline(w, args.cpu_rows)
     if args.all:

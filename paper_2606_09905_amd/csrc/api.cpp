@@ -90,6 +90,16 @@ bool mul_ok(int64_t a, int64_t b, int64_t lim, int64_t* out) {
 
 uint64_t round_up(uint64_t v, uint64_t a) { return (v + a - 1) / a * a; }
 
+// The dtype argument as the caller passed it.  A C caller may pass any int;
+// reading it through the enum type would be undefined for values outside
+// the enumerators, so its bytes are copied and validated as an int32.
+int32_t dt_raw(const qx_attn_dtype& dt) {
+    int32_t v;
+    static_assert(sizeof(qx_attn_dtype) == sizeof(int32_t), "enum passed as int");
+    memcpy(&v, &dt, sizeof v);
+    return v;
+}
+
 // ---------------------------------------------------------------------------
 // Exactness rules of the integer routes.
 // ---------------------------------------------------------------------------
@@ -709,7 +719,7 @@ qx_status plan_conv(Plan* pl, int64_t N, int64_t Ci, int64_t H, int64_t W, int64
 
 // Conv2D on FP32 or INT32 (smul24 contract) operands (Table 2, Conv2D FP32
 // and INT32 rows): the same lowering onto the FP32 and smul24 GEMMs.
-qx_status plan_conv_t(Plan* pl, qx_attn_dtype dt, int64_t N, int64_t Ci, int64_t H, int64_t W, int64_t Co,
+qx_status plan_conv_t(Plan* pl, int32_t dt, int64_t N, int64_t Ci, int64_t H, int64_t W, int64_t Co,
                       int64_t KH, int64_t KW, int64_t stride, int64_t pad, int32_t route) {
     int64_t Ho, Wo, Kd, P;
     qx_status st = conv_shape(N, Ci, H, W, Co, KH, KW, stride, pad, &Ho, &Wo, &Kd, &P);
@@ -1075,7 +1085,7 @@ qx_status plan_lenet(Plan* pl, int64_t B) {
     return QX_OK;
 }
 
-qx_status plan_attn(Plan* pl, qx_attn_dtype dt, int64_t L, int64_t d, int32_t bound, int32_t route) {
+qx_status plan_attn(Plan* pl, int32_t dt, int64_t L, int64_t d, int32_t bound, int32_t route) {
     qx_status st = check_dims({{"L", L}, {"d", d}});
     if (st) return st;
     if (dt != QX_DT_F32 && dt != QX_DT_I32) return fail(QX_ERR_INVALID_ARG, "unknown attention dtype %d", (int)dt);
@@ -1854,7 +1864,7 @@ qx_status qx_plan_conv2d_t(qx_plan_info* out, qx_attn_dtype dt, int64_t N, int64
     g_err.clear();
     if (!out) return fail(QX_ERR_INVALID_ARG, "out is NULL");
     Plan pl;
-    qx_status st = plan_conv_t(&pl, dt, N, C_in, H, W, C_out, KH, KW, stride, pad, route);
+    qx_status st = plan_conv_t(&pl, dt_raw(dt), N, C_in, H, W, C_out, KH, KW, stride, pad, route);
     if (!st) *out = pl.info;
     return st;
 }
@@ -1890,7 +1900,7 @@ qx_status qx_plan_attn(qx_plan_info* out, qx_attn_dtype dt, int64_t L, int64_t d
     g_err.clear();
     if (!out) return fail(QX_ERR_INVALID_ARG, "out is NULL");
     Plan pl;
-    qx_status st = plan_attn(&pl, dt, L, d, bound, route);
+    qx_status st = plan_attn(&pl, dt_raw(dt), L, d, bound, route);
     if (!st) *out = pl.info;
     return st;
 }
@@ -1954,7 +1964,7 @@ qx_status qx_exec_create_conv2d_t(qx_exec* out, qx_attn_dtype dt, int64_t N, int
     if (!out) return fail(QX_ERR_INVALID_ARG, "out is NULL");
     *out = nullptr;
     Plan pl;
-    qx_status st = plan_conv_t(&pl, dt, N, C_in, H, W, C_out, KH, KW, stride, pad, route);
+    qx_status st = plan_conv_t(&pl, dt_raw(dt), N, C_in, H, W, C_out, KH, KW, stride, pad, route);
     if (st) return st;
     return make_exec(std::move(pl), out);
 }
@@ -1995,7 +2005,7 @@ qx_status qx_exec_create_attn_route(qx_exec* out, qx_attn_dtype dt, int64_t L, i
     if (!out) return fail(QX_ERR_INVALID_ARG, "out is NULL");
     *out = nullptr;
     Plan pl;
-    qx_status st = plan_attn(&pl, dt, L, d, bound, route);
+    qx_status st = plan_attn(&pl, dt_raw(dt), L, d, bound, route);
     if (st) return st;
     return make_exec(std::move(pl), out);
 }
@@ -2018,7 +2028,13 @@ qx_status qx_exec_create_conv2d(qx_exec* out, int64_t N, int64_t C_in, int64_t H
 }
 
 qx_status qx_exec_create_attn(qx_exec* out, qx_attn_dtype dt, int64_t L, int64_t d, int32_t bound) {
-    return qx_exec_create_attn_route(out, dt, L, d, bound, R_AUTO);
+    g_err.clear();
+    if (!out) return fail(QX_ERR_INVALID_ARG, "out is NULL");
+    *out = nullptr;
+    Plan pl;
+    qx_status st = plan_attn(&pl, dt_raw(dt), L, d, bound, R_AUTO);
+    if (st) return st;
+    return make_exec(std::move(pl), out);
 }
 
 qx_status qx_exec_run(qx_exec h, const void* const* inputs, void* output, void* stream) {
@@ -2145,16 +2161,16 @@ qx_status conv2d_gemm_t(qx_attn_dtype dt, const void* x, const void* w, void* y,
                         void* stream) {
     g_err.clear();
     Plan probe;
-    qx_status st = plan_conv_t(&probe, dt, N, C_in, H, W, C_out, KH, KW, stride, pad, R_AUTO);
+    qx_status st = plan_conv_t(&probe, dt_raw(dt), N, C_in, H, W, C_out, KH, KW, stride, pad, R_AUTO);
     if (st) return st;
     if (probe.launches.empty()) return QX_OK;
     if (!empty_ok(x, N * C_in * H * W) || !empty_ok(w, C_out * C_in * KH * KW) || !y)
         return fail(QX_ERR_INVALID_ARG, "NULL pointer for a non-empty operand");
     const void* in[2] = {x, w};
-    Key key{dt == QX_DT_F32 ? OP_CONV_F32 : OP_CONV_I32, 0, N, C_in, H, W, C_out, KH, KW, stride, pad, 0, 0, 0,
+    Key key{dt_raw(dt) == QX_DT_F32 ? OP_CONV_F32 : OP_CONV_I32, 0, N, C_in, H, W, C_out, KH, KW, stride, pad, 0, 0, 0,
             (uintptr_t)stream};
     return oneshot(key,
-                   [&](Plan* pl) { return plan_conv_t(pl, dt, N, C_in, H, W, C_out, KH, KW, stride, pad, R_AUTO); },
+                   [&](Plan* pl) { return plan_conv_t(pl, dt_raw(dt), N, C_in, H, W, C_out, KH, KW, stride, pad, R_AUTO); },
                    in, y, stream);
 }
 
@@ -2185,14 +2201,14 @@ qx_status attn_core(qx_attn_dtype dt, const void* Q, const void* K, const void* 
                     int32_t bound, void* stream) {
     g_err.clear();
     Plan probe;
-    qx_status st = plan_attn(&probe, dt, L, d, bound, R_AUTO);
+    qx_status st = plan_attn(&probe, dt_raw(dt), L, d, bound, R_AUTO);
     if (st) return st;
     if (probe.launches.empty()) return QX_OK;
     if (!Q || !K || !V || !O) return fail(QX_ERR_INVALID_ARG, "NULL pointer for a non-empty operand");
     const void* in[3] = {Q, K, V};
-    Key key{dt == QX_DT_F32 ? OP_ATTN_F32 : OP_ATTN_I32, 0, L, d, bound, 0, 0, 0, 0, 0, 0, 0, 0, 0,
+    Key key{dt_raw(dt) == QX_DT_F32 ? OP_ATTN_F32 : OP_ATTN_I32, 0, L, d, bound, 0, 0, 0, 0, 0, 0, 0, 0, 0,
             (uintptr_t)stream};
-    return oneshot(key, [&](Plan* pl) { return plan_attn(pl, dt, L, d, bound, R_AUTO); }, in, O, stream);
+    return oneshot(key, [&](Plan* pl) { return plan_attn(pl, dt_raw(dt), L, d, bound, R_AUTO); }, in, O, stream);
 }
 
 qx_status qgemm_i16i32_noalloc(const int16_t* A, const int16_t* B, int32_t* C, int64_t M, int64_t N, int64_t K,
