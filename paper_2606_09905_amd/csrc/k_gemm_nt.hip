@@ -713,10 +713,100 @@ __global__ __launch_bounds__(NW * 64) void k_gemm_nt(const GemmParams p) {
             }
             phase_end();
         };
-        for (int tc = 0; tc < ktiles;) {
-            const int cend = min(tc + CT, ktiles);
-            ptile(tc, std::true_type{}, tc + 1 == cend);
-            for (++tc; tc < cend; ++tc) ptile(tc, std::false_type{}, tc + 1 == cend);
+        if (CT >= 4 && TM * TN == 4) {
+            // Staggered flushes: the four 32x32 blocks of a wave close their
+            // chunks on different tiles -- block b on every tile t with
+            // t % 4 == b (t >= 1) -- so each compute phase converts and adds
+            // one block (32 vector ops) while the same wave's 16 MFMAs run,
+            // instead of all four blocks (128 vector ops, as long as the
+            // MFMAs themselves) after every fourth tile.  Every chunk spans
+            // at most four tiles (256 K), within the exactness bound since
+            // CT >= 4.  FB = the block closed and restarted on this tile; 4 =
+            // the first tile, where every block starts from zero.
+            // Fragment reads at a stage offset the optimiser cannot see
+            // through, so the per-lane addresses of the three stages are not
+            // all precomputed and kept live (that alone would cost 48
+            // registers).
+            auto ldf_at = [&](unsigned soff_a, unsigned soff_b, int ks, h8 (&a)[TM], h8 (&bv)[TN]) {
+                const int c = ks * 2 + hh;
+#pragma unroll
+                for (int i = 0; i < TM; ++i) {
+                    const int row = wm * WM + i * 32 + l32;
+                    a[i] = *(const h8*)((const char*)&As[0][row][c ^ chunk_swz(row)] + soff_a);
+                }
+#pragma unroll
+                for (int j = 0; j < TN; ++j) {
+                    const int col = wn * WN + j * 32 + l32;
+                    bv[j] = *(const h8*)((const char*)&Bs[0][col][c ^ chunk_swz(col)] + soff_b);
+                }
+            };
+            auto stile = [&](int tc, auto fb_c) {
+                constexpr int FB = decltype(fb_c)::value;
+                unsigned soff = (unsigned)(tc % STAGES);
+                asm volatile("" : "+s"(soff));
+#pragma unroll
+                for (int ks = 0; ks < KS; ++ks) ldf_at(soff * STAGE_A, soff * STAGE_B, ks, fa[ks], fb[ks]);
+                if (tc + 2 < ktiles) issue(tc + 2);
+                if (grp == 1) {
+                    if (tc + 2 < ktiles) __builtin_amdgcn_s_waitcnt(WAIT_VM_LPT);
+                    else __builtin_amdgcn_s_waitcnt(WAIT_VM_0);
+                } else {
+                    __builtin_amdgcn_s_waitcnt(0xC07F);   // lgkmcnt(0)
+                }
+                phase_end();
+                if constexpr (FB < 4) {
+#pragma unroll
+                    for (int r = 0; r < 16; ++r)
+                        iacc[FB / 2][FB % 2][r] += (uint32_t)(int32_t)acc[FB / 2][FB % 2][r];
+                    // pin the conversion to this phase: left to itself the
+                    // optimiser sinks it past later tiles, which keeps the
+                    // old fp32 block alive beside the restarted one
+                    asm volatile("" : "+v"(iacc[FB / 2][FB % 2]));
+                }
+                // the restarted block comes last in the first k-step, so its
+                // conversion has the other blocks' MFMAs to run beside
+#pragma unroll
+                for (int ks = 0; ks < KS; ++ks)
+#pragma unroll
+                    for (int q = 1; q <= 4; ++q) {
+                        const int b = FB < 4 ? (FB + q) & 3 : q - 1;
+                        const int i = b >> 1, j = b & 1;
+                        const bool zero = ks == 0 && (FB == 4 || b == FB);
+                        acc[i][j] = mfma_h<BF>(fa[ks][i], fb[ks][j], zero ? f16x{} : acc[i][j]);
+                    }
+                if (grp == 0) {
+                    if (tc + 2 < ktiles) __builtin_amdgcn_s_waitcnt(WAIT_VM_LPT);
+                    else __builtin_amdgcn_s_waitcnt(WAIT_VM_0);
+                }
+                phase_end();
+            };
+            using I0 = std::integral_constant<int, 0>;
+            using I1 = std::integral_constant<int, 1>;
+            using I2 = std::integral_constant<int, 2>;
+            using I3 = std::integral_constant<int, 3>;
+            stile(0, std::integral_constant<int, 4>{});
+            int tc = 1;
+            for (; tc + 3 < ktiles; tc += 4) {
+                stile(tc, I1{});
+                stile(tc + 1, I2{});
+                stile(tc + 2, I3{});
+                stile(tc + 3, I0{});
+            }
+            if (tc < ktiles) stile(tc, I1{});
+            if (tc + 1 < ktiles) stile(tc + 1, I2{});
+            if (tc + 2 < ktiles) stile(tc + 2, I3{});
+#pragma unroll
+            for (int i = 0; i < TM; ++i)
+#pragma unroll
+                for (int j = 0; j < TN; ++j)
+#pragma unroll
+                    for (int r = 0; r < 16; ++r) iacc[i][j][r] += (uint32_t)(int32_t)acc[i][j][r];
+        } else {
+            for (int tc = 0; tc < ktiles;) {
+                const int cend = min(tc + CT, ktiles);
+                ptile(tc, std::true_type{}, tc + 1 == cend);
+                for (++tc; tc < cend; ++tc) ptile(tc, std::false_type{}, tc + 1 == cend);
+            }
         }
         if (grp == 0) phase_end();
     } else {
