@@ -1164,7 +1164,12 @@ qx_status plan_attn(Plan* pl, int32_t dt, int64_t L, int64_t d, int32_t bound, i
         const int64_t kblocks = (L + 31) / 32;
         int64_t splits = std::min<int64_t>(std::max<int64_t>((256 + qgroups - 1) / qgroups, 1), kblocks);
         int64_t kps = ((kblocks + splits - 1) / splits) * 32;
-        if (r == R_ATTN_I32_MFMA && (d == 32 || d == 64 || d == 128)) {
+        const bool stream = r == R_ATTN_I32_MFMA && (d == 32 || d == 64);
+        if (stream) {
+            // streaming kernel: each split is two halves of an even number of
+            // whole 32-key blocks
+            kps = (kps + 127) / 128 * 128;
+        } else if (r == R_ATTN_I32_MFMA && d == 128) {
             // resident splits: kps * d a multiple of 4096 (whole 1 KB loads
             // per wave) and both int8 tiles within 48 KiB of LDS
             const int64_t g = std::max<int64_t>(32, 4096 / d), cap = 24576 / d / g * g;
@@ -1196,6 +1201,35 @@ qx_status plan_attn(Plan* pl, int32_t dt, int64_t L, int64_t d, int32_t bound, i
             } else {
                 pl->launches.push_back(rec);
             }
+        } else if (stream) {
+            // prep: int8 K rows and block-major int8 V in the workspace, O
+            // cleared for split accumulation; then eight waves per
+            // workgroup stream their keys from them (no LDS staging)
+            a.Lp = (int32_t)(splits * kps);
+            a.clear_o = splits > 1 ? 1 : 0;
+            a.v_blocks = 1;
+            a.prep_k = (int64_t)a.Lp * d / 16;
+            a.prep_v = d * (int64_t)a.Lp / 16;
+            a.prep_q = L * d / 16;
+            const uint64_t v8_off = round_up((uint64_t)a.Lp * (uint64_t)d, 256);
+            const uint64_t q8_off = round_up(v8_off + (uint64_t)a.Lp * (uint64_t)d, 256);
+            ws = q8_off + (uint64_t)L * (uint64_t)d;
+            LaunchRec r1;
+            build_attn_i32_prep(a, &r1);
+            r1.bind(offsetof(AttnParams, Q), BIND_IN0);
+            r1.bind(offsetof(AttnParams, K), BIND_IN1);
+            r1.bind(offsetof(AttnParams, V), BIND_IN2);
+            r1.bind(offsetof(AttnParams, O), BIND_OUT);
+            r1.bind(offsetof(AttnParams, k8), BIND_WS, 0);
+            r1.bind(offsetof(AttnParams, v8), BIND_WS, v8_off);
+            r1.bind(offsetof(AttnParams, q8), BIND_WS, q8_off);
+            pl->launches.push_back(r1);
+            if (!build_attn_i32s(a, &rec)) return fail(QX_ERR_UNSUPPORTED, "no streaming attention kernel");
+            rec.bind(offsetof(AttnParams, O), BIND_OUT);
+            rec.bind(offsetof(AttnParams, k8), BIND_WS, 0);
+            rec.bind(offsetof(AttnParams, v8), BIND_WS, v8_off);
+            rec.bind(offsetof(AttnParams, q8), BIND_WS, q8_off);
+            pl->launches.push_back(rec);
         } else if (resident_attn_i32(d, kps)) {
             // prep: int8 K rows and reordered V^T rows in the workspace, O
             // cleared for split accumulation; then every workgroup loads its

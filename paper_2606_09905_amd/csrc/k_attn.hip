@@ -322,10 +322,23 @@ __global__ __launch_bounds__(AT) void k_attn_i32_prep(const AttnParams p) {
             }
             o[w] = (int)x;
         }
-        *(i4*)((int8_t*)p.v8 + (int64_t)c * p.Lp + 16 * (int64_t)hb) = o;
+        int8_t* dst = p.v_blocks ? (int8_t*)p.v8 + ((int64_t)(hb >> 1) * D + c) * 32 + 16 * (hb & 1)
+                                 : (int8_t*)p.v8 + (int64_t)c * p.Lp + 16 * (int64_t)hb;
+        *(i4*)dst = o;
         return;
     }
-    const int64_t io = iv - p.prep_v;
+    const int64_t iq = iv - p.prep_v;
+    if (iq < p.prep_q) {
+        // 16 consecutive d of one query row
+        const int q = (int)(iq / (D / 16)), c0 = (int)(iq % (D / 16)) * 16;
+        const int32_t* Qp = (const int32_t*)p.Q;
+        i4 o;
+#pragma unroll
+        for (int w = 0; w < 4; ++w) o[w] = (int)pack4(*(const i4*)(Qp + (int64_t)q * D + c0 + 4 * w));
+        *(i4*)((int8_t*)p.q8 + (int64_t)q * D + c0) = o;
+        return;
+    }
+    const int64_t io = iq - p.prep_q;
     if (p.clear_o && io < (int64_t)p.L * D / 4) ((i4*)p.O)[io] = i4{};
 }
 
@@ -455,6 +468,183 @@ __global__ __launch_bounds__(AT) void k_attn_i32r(const AttnParams p) {
                                ((uint32_t)o[2][n][r] << 16) + corr;
             if (p.splits > 1) atomicAdd(O + (int64_t)q * D + c, (int)v);
             else O[(int64_t)q * D + c] = (int32_t)v;
+        }
+    }
+}
+
+// ---------------------------------------------------------------------------
+// INT32, streaming.  A workgroup of eight waves takes 128 queries and one key
+// split: wave w holds query tile w % 4 and the key half w / 4 of the split,
+// and streams its own 32-key blocks of K8 rows and block-major V8 straight
+// from global memory (L2) into registers, two blocks ahead, so no wave ever
+// waits on another until the end.  Per block: S^T on the int8 matrix cores,
+// the offset limb split of S, three limb products into O, and the block's V
+// column sums (for the offset correction) from the same V registers.  The
+// two key halves of a query tile are added through LDS, then one wrapping
+// int32 atomic per output joins the splits (exact mod 2^32 in any order).
+// ---------------------------------------------------------------------------
+template <int D>
+__global__ __launch_bounds__(512) void k_attn_i32s(const AttnParams p) {
+    constexpr int NTO = D / 32;
+    constexpr int BLK = 2 * NTO * 1024;          // bytes of one block's K and V
+    // two key halves x two pairs of blocks; after the loop a half's ring
+    // also carries its sums to the other half
+    __shared__ __attribute__((aligned(16))) char ring[2][2][2][BLK];
+
+    const int tid = threadIdx.x, lane = tid & 63, h = lane >> 5, l32 = lane & 31;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);   // uniform: block addresses stay scalar
+    const int qw = wave & 3, kh = wave >> 2;
+    const int q0 = blockIdx.x * AQ + qw * AQW;
+    const int kps = p.keys_per_split;            // a multiple of 128
+    const int npair = kps / 128;                 // pairs of 32-key blocks per key half
+    const int blk0 = (int)(((int64_t)blockIdx.y * kps + kh * (kps / 2)) / 32);
+    const char* K8 = (const char*)p.k8;          // [Lp][D]
+    const char* V8 = (const char*)p.v8;          // [Lp/32][D][32]
+
+    // The four waves of a key half stage its blocks in a shared LDS ring
+    // (two pairs deep) with direct-to-LDS loads, one pair ahead, each wave a
+    // quarter of every pair.  A lane's 16 bytes land where the MFMA operand
+    // layout reads them (lane (key | column l32, half h): K row chunk
+    // 2t + h, V 16 keys of column n*32 + l32), which is the same for all
+    // four query tiles, so the ring reads are contiguous.
+    const unsigned koff = (unsigned)(l32 * D + h * 16), voff = (unsigned)(l32 * 32 + h * 16);
+    constexpr int PER_PAIR = 2 * 2 * NTO;        // 1 KB loads per pair (K and V of two blocks)
+    static_assert(PER_PAIR % 4 == 0, "a pair splits over the four waves");
+    auto issue = [&](int pr) {
+        const unsigned lds = (unsigned)(uintptr_t)&ring[kh][pr & 1][0][0];
+#pragma unroll
+        for (int u = 0; u < PER_PAIR / 4; ++u) {
+            const int l = qw * (PER_PAIR / 4) + u;           // 0 .. PER_PAIR-1
+            const int e = l / (2 * NTO), part = l % (2 * NTO);   // block of the pair, 1 KB part
+            const int64_t bg = blk0 + 2 * pr + e;
+            const unsigned dst = lds + (unsigned)(e * BLK + part * 1024);
+            if (part < NTO) {
+                const char* kb = K8 + bg * 32 * D;
+                asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dwordx4 %0, %1"
+                             :: "v"(koff + part * 32), "s"(kb), "s"(dst) : "memory", "m0");
+            } else {
+                const char* vb = V8 + bg * D * 32;
+                asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dwordx4 %0, %1"
+                             :: "v"(voff + (part - NTO) * 1024), "s"(vb), "s"(dst) : "memory", "m0");
+            }
+        }
+    };
+    // Q rows as int8 (written by the prep launch): lane (query l32, half h),
+    // MFMA t: Q[query][32t + 16h + e]; queued ahead of the key blocks
+    i4 qf[NTO];
+    {
+        const int q = min(q0 + l32, p.L - 1);
+#pragma unroll
+        for (int t = 0; t < NTO; ++t) qf[t] = *(const i4*)((const char*)p.q8 + (int64_t)q * D + 32 * t + 16 * h);
+    }
+    if (npair > 0) issue(0);
+    i16x o[3][NTO];
+#pragma unroll
+    for (int j = 0; j < 3; ++j)
+#pragma unroll
+        for (int n = 0; n < NTO; ++n) o[j][n] = i16x{};
+    int vs[NTO];                                 // V column n*32 + l32, keys of half h
+#pragma unroll
+    for (int n = 0; n < NTO; ++n) vs[n] = 0;
+
+    // the offset limbs of S (bytes of S ^ 0x8080, read as int8): K-slot
+    // (h, e) of the second product is key 8*(e/4) + 4*h + e%4, as the S^T
+    // accumulator layout gives
+    auto limbs = [](const i16x& s, i4 (&limb)[3]) {
+        uint32_t x[16];
+#pragma unroll
+        for (int r = 0; r < 16; ++r) x[r] = (uint32_t)s[r] ^ 0x8080u;
+#pragma unroll
+        for (int jj = 0; jj < 3; ++jj)
+#pragma unroll
+            for (int w = 0; w < 4; ++w)
+                limb[jj][w] = (int)gather_byte(x[4 * w], x[4 * w + 1], x[4 * w + 2], x[4 * w + 3], jj);
+    };
+    for (int pr = 0; pr < npair; ++pr) {
+        __builtin_amdgcn_s_waitcnt(0x0F70);      // this wave's part of pair pr landed
+        __syncthreads();                         // every part landed; slot (pr+1)&1 read by all
+        if (pr + 1 < npair) issue(pr + 1);       // one pair ahead, into the slot freed above
+        const char* st0 = &ring[kh][pr & 1][0][0];
+        const char* st1 = &ring[kh][pr & 1][1][0];
+        i4 kf0[NTO], kf1[NTO], vf0[NTO], vf1[NTO];
+#pragma unroll
+        for (int t = 0; t < NTO; ++t) {
+            kf0[t] = *(const i4*)(st0 + t * 1024 + lane * 16);
+            kf1[t] = *(const i4*)(st1 + t * 1024 + lane * 16);
+        }
+#pragma unroll
+        for (int n = 0; n < NTO; ++n) {
+            vf0[n] = *(const i4*)(st0 + (NTO + n) * 1024 + lane * 16);
+            vf1[n] = *(const i4*)(st1 + (NTO + n) * 1024 + lane * 16);
+        }
+        // two independent S^T chains, then each block's limbs beside the
+        // other's matrix products
+        i16x s0 = i16x{}, s1 = i16x{};
+#pragma unroll
+        for (int t = 0; t < NTO; ++t) {
+            s0 = __builtin_amdgcn_mfma_i32_32x32x32_i8(kf0[t], qf[t], s0, 0, 0, 0);
+            s1 = __builtin_amdgcn_mfma_i32_32x32x32_i8(kf1[t], qf[t], s1, 0, 0, 0);
+        }
+        i4 l0[3], l1[3];
+        limbs(s0, l0);
+#pragma unroll
+        for (int n = 0; n < NTO; ++n)
+#pragma unroll
+            for (int jj = 0; jj < 3; ++jj)
+                o[jj][n] = __builtin_amdgcn_mfma_i32_32x32x32_i8(l0[jj], vf0[n], o[jj][n], 0, 0, 0);
+        limbs(s1, l1);
+#pragma unroll
+        for (int n = 0; n < NTO; ++n) {
+#pragma unroll
+            for (int w = 0; w < 4; ++w) {
+                vs[n] = __builtin_amdgcn_sdot4(vf0[n][w], 0x01010101, vs[n], false);
+                vs[n] = __builtin_amdgcn_sdot4(vf1[n][w], 0x01010101, vs[n], false);
+            }
+#pragma unroll
+            for (int jj = 0; jj < 3; ++jj)
+                o[jj][n] = __builtin_amdgcn_mfma_i32_32x32x32_i8(l1[jj], vf1[n], o[jj][n], 0, 0, 0);
+        }
+    }
+
+    // recombine the limbs and add the offset correction of this wave's keys
+    uint32_t v[NTO][16];
+#pragma unroll
+    for (int n = 0; n < NTO; ++n) {
+        const uint32_t cs = (uint32_t)(vs[n] + __shfl_xor(vs[n], 32, 64));
+        const uint32_t corr = 32896u * cs;
+#pragma unroll
+        for (int r = 0; r < 16; ++r)
+            v[n][r] = (uint32_t)o[0][n][r] + ((uint32_t)o[1][n][r] << 8) + ((uint32_t)o[2][n][r] << 16) + corr;
+    }
+    // key half 1 hands its sums to key half 0 through the ring, once every
+    // wave is done reading it: a quarter of the ring per query tile
+    uint32_t* red = (uint32_t*)&ring[0][0][0][0] + qw * (NTO * 16 * 64);   // [NTO][16][64]
+    static_assert(4 * NTO * 16 * 64 * 4 <= (int)sizeof(ring), "exchange fits the ring");
+    __syncthreads();
+    if (kh == 1) {
+#pragma unroll
+        for (int n = 0; n < NTO; ++n)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) red[(n * 16 + r) * 64 + lane] = v[n][r];
+    }
+    __syncthreads();
+    if (kh == 1) return;
+#pragma unroll
+    for (int n = 0; n < NTO; ++n)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) v[n][r] += red[(n * 16 + r) * 64 + lane];
+    int32_t* dst = (int32_t*)p.O;
+#pragma unroll
+    for (int n = 0; n < NTO; ++n) {
+        const int c = n * 32 + l32;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+            const int q = q0 + 8 * (r >> 2) + 4 * h + (r & 3);
+            if (q >= p.L) continue;
+            // splits add into the output cleared by the prep launch:
+            // wrapping int32 atomics, exact mod 2^32 in any order
+            if (p.splits > 1) atomicAdd(dst + (int64_t)q * D + c, (int)v[n][r]);
+            else dst[(int64_t)q * D + c] = (int32_t)v[n][r];
         }
     }
 }
@@ -713,7 +903,7 @@ bool build_attn_i32_prep(const AttnParams& p, LaunchRec* rec) {
     case 128: rec->fn = (const void*)k_attn_i32_prep<128>; break;
     default: return false;
     }
-    const int64_t items = p.prep_k + p.prep_v + (p.clear_o ? (int64_t)p.L * p.d / 4 : 0);
+    const int64_t items = p.prep_k + p.prep_v + p.prep_q + (p.clear_o ? (int64_t)p.L * p.d / 4 : 0);
     rec->name = "attn_i32_prep";
     rec->grid = dim3((unsigned)((items + AT - 1) / AT), 1, 1);
     rec->block = dim3(AT, 1, 1);
@@ -732,6 +922,20 @@ bool build_attn_i32r(const AttnParams& p, LaunchRec* rec) {
     rec->grid = dim3((unsigned)((p.L + AQ - 1) / AQ), (unsigned)p.splits, 1);
     rec->block = dim3(AT, 1, 1);
     rec->shmem = (uint32_t)(2 * (int64_t)p.keys_per_split * p.d);
+    rec->set_params(p);
+    return true;
+}
+
+bool build_attn_i32s(const AttnParams& p, LaunchRec* rec) {
+    switch (p.d) {
+    case 32: rec->fn = (const void*)k_attn_i32s<32>; break;
+    case 64: rec->fn = (const void*)k_attn_i32s<64>; break;
+    default: return false;
+    }
+    if (p.keys_per_split % 128 != 0 || !p.v_blocks) return false;
+    rec->name = "attn_i32_stream";
+    rec->grid = dim3((unsigned)((p.L + AQ - 1) / AQ), (unsigned)p.splits, 1);
+    rec->block = dim3(512, 1, 1);
     rec->set_params(p);
     return true;
 }

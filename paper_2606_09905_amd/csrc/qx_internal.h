@@ -167,6 +167,12 @@ struct AttnParams {
     int32_t Lp;             // splits * keys_per_split (>= L), zero-padded keys
     int32_t clear_o;        // prep also clears O (split partials are added with atomics)
     int64_t prep_k, prep_v; // prep work items: 16-byte K8 chunks, 16-byte V8 chunks
+    int32_t v_blocks;       // prep: 1 = write V8 block-major, [Lp/32][d][32] (each 32-key block of
+                            // every column contiguous, keys reordered as above), for the
+                            // streaming kernel; 0 = [d][Lp]
+    int32_t pad0;
+    void* q8;               // prep_q > 0: int8 rows of Q, [L][d]
+    int64_t prep_q;         // prep work items: 16-byte Q8 chunks (0: none)
 };
 
 // Softmax attention over BH heads (FP32): O = softmax(scale Q K^T [mask]) V.
@@ -343,6 +349,9 @@ bool build_attn_i32(const AttnParams& p, LaunchRec* rec);
 bool resident_attn_i32(int64_t d, int64_t kps);
 bool build_attn_i32_prep(const AttnParams& p, LaunchRec* rec);
 bool build_attn_i32r(const AttnParams& p, LaunchRec* rec);
+// INT32 attention streaming its keys from the int8 copies into registers:
+// d in {32, 64}, keys_per_split a multiple of 128, V8 block-major
+bool build_attn_i32s(const AttnParams& p, LaunchRec* rec);
 void build_reduce(const ReduceParams& p, LaunchRec* rec);
 bool build_sdpa_f32(const SdpaParams& p, LaunchRec* rec);
 void build_sdpa_combine(const SdpaCombineParams& p, LaunchRec* rec);

@@ -273,9 +273,12 @@ def test_attention_plans():
     p = qx.plan_attn("f32", 4096, 64)
     assert p["tile_k"] % 32 == 0 and (4096 // 128) * (4096 // p["tile_k"]) >= 256
     assert p["tile_k"] == 512
-    # INT32 resident splits: both int8 tiles within 48 KiB of LDS caps a
-    # split at 384 keys for d = 64 (11 splits)
-    assert qx.plan_attn("i32", 4096, 64, 64)["tile_k"] == 384
+    # INT32, d = 64: the streaming kernel takes splits of whole 64-key
+    # pairs of blocks, one workgroup per CU (32 query groups x 8 splits of
+    # 512 keys); d = 128 keeps the LDS-resident splits, both int8 tiles
+    # within 48 KiB of LDS (192 keys)
+    assert qx.plan_attn("i32", 4096, 64, 64)["tile_k"] == 512
+    assert qx.plan_attn("i32", 4096, 128, 64)["tile_k"] == 192
 
 
 def test_sdpa_plans():

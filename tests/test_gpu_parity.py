@@ -367,10 +367,13 @@ def test_attn_f32(L, d):
 
 @pytest.mark.parametrize("L,d,b", [(1, 32, 64), (33, 64, 64), (128, 64, 127), (300, 32, 100),
                                    (1024, 128, 127), (257, 96, 64), (1000, 64, 64), (4100, 128, 100),
-                                   (5000, 32, 127), (2049, 64, 127)])
+                                   (5000, 32, 127), (2049, 64, 127), (4096, 64, 127), (63, 32, 127),
+                                   (64, 64, 1), (65, 64, 127), (8191, 64, 64)])
 def test_attn_i32_mfma(L, d, b):
-    # d in {32, 64, 128}: the prep launch plus the resident-split kernel
-    # (ragged last split, zero-padded keys); d = 96: the streaming kernel
+    # d in {32, 64}: the prep launch plus the register-streaming kernel
+    # (eight waves, two key halves per split joined in LDS; ragged last
+    # split, zero-padded keys; one split -> plain stores); d = 128: the
+    # prep plus the LDS-resident splits; d = 96: the LDS-staged loop kernel
     rng = np.random.default_rng(L * 3 + d + b)
     Q, K, V = (rand_int(rng, (L, d), b, np.int32) for _ in range(3))
     O = host(qx.attn_core(dev(Q), dev(K), dev(V), bound=b))
