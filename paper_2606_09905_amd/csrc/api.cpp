@@ -1085,6 +1085,17 @@ qx_status plan_lenet(Plan* pl, int64_t B) {
     return QX_OK;
 }
 
+// Query tiles of 32 per workgroup of the streaming INT32 attention core
+// (eight waves: qt query tiles x 8/qt key parts).  At L = 4096, d = 64 two
+// tiles (64 queries x 4 splits of 1024 keys) measured best: four (8
+// splits) doubled the wrapping atomics that join the splits, and one (2
+// splits of 2048 keys) doubled each workgroup's key traffic and left its
+// LDS ring one pair deep.
+static int attn_stream_qt(int64_t L) {
+    (void)L;
+    return 2;
+}
+
 qx_status plan_attn(Plan* pl, int32_t dt, int64_t L, int64_t d, int32_t bound, int32_t route) {
     qx_status st = check_dims({{"L", L}, {"d", d}});
     if (st) return st;
@@ -1160,15 +1171,17 @@ qx_status plan_attn(Plan* pl, int32_t dt, int64_t L, int64_t d, int32_t bound, i
         // measured 10% slower on L = 4096, d = 64 (more per-workgroup
         // set-up and more partial outputs to combine); half as many left
         // CUs idle (FP32 1.6x slower).
-        const int64_t qgroups = (L + 127) / 128;
+        const bool stream = r == R_ATTN_I32_MFMA && (d == 32 || d == 64);
+        const int qt = stream ? attn_stream_qt(L) : 4;       // query tiles of 32 per workgroup
+        const int64_t qgroups = (L + 32 * qt - 1) / (32 * qt);
         const int64_t kblocks = (L + 31) / 32;
         int64_t splits = std::min<int64_t>(std::max<int64_t>((256 + qgroups - 1) / qgroups, 1), kblocks);
         int64_t kps = ((kblocks + splits - 1) / splits) * 32;
-        const bool stream = r == R_ATTN_I32_MFMA && (d == 32 || d == 64);
         if (stream) {
-            // streaming kernel: each split is two halves of an even number of
-            // whole 32-key blocks
-            kps = (kps + 127) / 128 * 128;
+            // streaming kernel: each split is 8 / qt key parts of an even
+            // number of whole 32-key blocks
+            const int64_t g = 64 * (8 / qt);
+            kps = (kps + g - 1) / g * g;
         } else if (r == R_ATTN_I32_MFMA && d == 128) {
             // resident splits: kps * d a multiple of 4096 (whole 1 KB loads
             // per wave) and both int8 tiles within 48 KiB of LDS
@@ -1179,6 +1192,7 @@ qx_status plan_attn(Plan* pl, int32_t dt, int64_t L, int64_t d, int32_t bound, i
         AttnParams a{};
         a.L = (int32_t)L; a.d = (int32_t)d; a.splits = (int32_t)splits; a.keys_per_split = (int32_t)kps;
         a.limbs = 3;
+        a.qt = qt;
         LaunchRec rec;
         if (r == R_ATTN_F32_MFMA) {
             build_attn_f32(a, &rec);

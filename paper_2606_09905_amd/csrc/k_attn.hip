@@ -473,48 +473,78 @@ __global__ __launch_bounds__(AT) void k_attn_i32r(const AttnParams p) {
 }
 
 // ---------------------------------------------------------------------------
-// INT32, streaming.  A workgroup of eight waves takes 128 queries and one key
-// split: wave w holds query tile w % 4 and the key half w / 4 of the split,
-// and streams its own 32-key blocks of K8 rows and block-major V8 straight
-// from global memory (L2) into registers, two blocks ahead, so no wave ever
-// waits on another until the end.  Per block: S^T on the int8 matrix cores,
-// the offset limb split of S, three limb products into O, and the block's V
-// column sums (for the offset correction) from the same V registers.  The
-// two key halves of a query tile are added through LDS, then one wrapping
-// int32 atomic per output joins the splits (exact mod 2^32 in any order).
+// INT32, streaming.  A workgroup of eight waves takes QT query tiles of 32
+// queries and one key split, cut into KQ = 8 / QT key parts: wave w holds
+// query tile w % QT over key part w / QT.  Per 32-key block: S^T on the int8
+// matrix cores, the offset limb split of S, three limb products into O, and
+// the block's V column sums (for the offset correction) from the same V
+// registers.  The KQ partial outputs of a query tile are added through LDS,
+// each wave adding a slice of the tile, and one wrapping int32 atomic per
+// output joins the key splits (exact mod 2^32 in any order).
 // ---------------------------------------------------------------------------
-template <int D>
+template <int D, int QT>
+struct AttnStream {
+    static constexpr int NTO = D / 32;
+    static constexpr int KQ = 8 / QT;                    // key parts
+    static constexpr int BLK = 2 * NTO * 1024;           // bytes of one block's K and V
+    static constexpr int PER_PAIR = 4 * NTO;             // 1 KB loads per pair of blocks
+    static constexpr int PW = PER_PAIR / QT;             // of them issued by each wave
+    static constexpr int R0 = (128 * 1024) / (KQ * 2 * BLK);
+    static constexpr int R = R0 > 8 ? 8 : R0;            // ring depth in pairs
+    static_assert(PER_PAIR % QT == 0 && R >= 2 && (R & (R - 1)) == 0, "ring geometry");
+    static_assert(PW * (R - 2) < 64, "loads in flight fit the vmcnt counter");
+    static constexpr int KEYS = 64 * KQ;                 // keys_per_split is a multiple of this
+};
+
+// s_waitcnt vmcnt(N) (expcnt and lgkmcnt left alone), N in [0, 63]
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+    static_assert(N >= 0 && N < 64, "vmcnt range");
+    __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
+}
+// wait until at most STEP * n of this wave's vector memory loads are in flight,
+// n in [0, NMAX] (the immediate is a constant: dispatch on n)
+template <int STEP, int NMAX>
+__device__ __forceinline__ void wait_vmcnt_steps(int n) {
+    if constexpr (NMAX <= 0) {
+        wait_vmcnt<0>();
+    } else {
+        if (n >= NMAX) wait_vmcnt<STEP * NMAX>();
+        else wait_vmcnt_steps<STEP, NMAX - 1>(n);
+    }
+}
+
+template <int D, int QT>
 __global__ __launch_bounds__(512) void k_attn_i32s(const AttnParams p) {
-    constexpr int NTO = D / 32;
-    constexpr int BLK = 2 * NTO * 1024;          // bytes of one block's K and V
-    // two key halves x two pairs of blocks; after the loop a half's ring
-    // also carries its sums to the other half
-    __shared__ __attribute__((aligned(16))) char ring[2][2][2][BLK];
+    using G = AttnStream<D, QT>;
+    constexpr int NTO = G::NTO, KQ = G::KQ, BLK = G::BLK, PW = G::PW, R = G::R;
+    // per key part a ring of R pairs of blocks; after the loop the ring
+    // carries the partial outputs between the waves of a query tile
+    __shared__ __attribute__((aligned(16))) char ring[KQ][R][2][BLK];
+    __shared__ __attribute__((aligned(16))) char qs[8][NTO * 1024];
 
     const int tid = threadIdx.x, lane = tid & 63, h = lane >> 5, l32 = lane & 31;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);   // uniform: block addresses stay scalar
-    const int qw = wave & 3, kh = wave >> 2;
-    const int q0 = blockIdx.x * AQ + qw * AQW;
-    const int kps = p.keys_per_split;            // a multiple of 128
-    const int npair = kps / 128;                 // pairs of 32-key blocks per key half
-    const int blk0 = (int)(((int64_t)blockIdx.y * kps + kh * (kps / 2)) / 32);
+    const int qw = wave % QT, kp = wave / QT;
+    const int q0 = blockIdx.x * (32 * QT) + qw * 32;
+    const int kps = p.keys_per_split;            // a multiple of G::KEYS
+    const int npair = kps / G::KEYS;             // pairs of 32-key blocks per key part
+    const int blk0 = (int)(((int64_t)blockIdx.y * kps + (int64_t)kp * (kps / KQ)) / 32);
     const char* K8 = (const char*)p.k8;          // [Lp][D]
     const char* V8 = (const char*)p.v8;          // [Lp/32][D][32]
 
-    // The four waves of a key half stage its blocks in a shared LDS ring
-    // (two pairs deep) with direct-to-LDS loads, one pair ahead, each wave a
-    // quarter of every pair.  A lane's 16 bytes land where the MFMA operand
-    // layout reads them (lane (key | column l32, half h): K row chunk
-    // 2t + h, V 16 keys of column n*32 + l32), which is the same for all
-    // four query tiles, so the ring reads are contiguous.
+    // The QT waves of a key part stage its blocks in the part's ring with
+    // direct-to-LDS loads, R-1 pairs ahead, each wave PW of the 1 KB loads
+    // of every pair.  A lane's 16 bytes land where the MFMA operand layout
+    // reads them (lane (key | column l32, half h): K row chunk 2t + h, V 16
+    // keys of column n*32 + l32), which is the same for every query tile,
+    // so the ring reads are contiguous.
     const unsigned koff = (unsigned)(l32 * D + h * 16), voff = (unsigned)(l32 * 32 + h * 16);
-    constexpr int PER_PAIR = 2 * 2 * NTO;        // 1 KB loads per pair (K and V of two blocks)
-    static_assert(PER_PAIR % 4 == 0, "a pair splits over the four waves");
     auto issue = [&](int pr) {
-        const unsigned lds = (unsigned)(uintptr_t)&ring[kh][pr & 1][0][0];
+        const unsigned lds = (unsigned)(uintptr_t)&ring[kp][pr & (R - 1)][0][0];
 #pragma unroll
-        for (int u = 0; u < PER_PAIR / 4; ++u) {
-            const int l = qw * (PER_PAIR / 4) + u;           // 0 .. PER_PAIR-1
+        for (int u = 0; u < PW; ++u) {
+            const int l = qw * PW + u;                           // 0 .. PER_PAIR-1
             const int e = l / (2 * NTO), part = l % (2 * NTO);   // block of the pair, 1 KB part
             const int64_t bg = blk0 + 2 * pr + e;
             const unsigned dst = lds + (unsigned)(e * BLK + part * 1024);
@@ -529,15 +559,21 @@ __global__ __launch_bounds__(512) void k_attn_i32s(const AttnParams p) {
             }
         }
     };
-    // Q rows as int8 (written by the prep launch): lane (query l32, half h),
-    // MFMA t: Q[query][32t + 16h + e]; queued ahead of the key blocks
-    i4 qf[NTO];
+    // this wave's Q rows as int8 (written by the prep launch), staged the
+    // same way ahead of the key blocks: lane (query l32, half h), MFMA t
+    // reads Q[query][32t + 16h + e]; rows past L repeat the last row
     {
-        const int q = min(q0 + l32, p.L - 1);
+        const int qr = min(q0, p.L - 1);         // a tile past L (last workgroup) reads row L-1
+        const char* qb = (const char*)p.q8 + (int64_t)qr * D;
+        const unsigned qoff = (unsigned)((min(q0 + l32, p.L - 1) - qr) * D + 16 * h);
+        const unsigned dst = (unsigned)(uintptr_t)&qs[wave][0];
 #pragma unroll
-        for (int t = 0; t < NTO; ++t) qf[t] = *(const i4*)((const char*)p.q8 + (int64_t)q * D + 32 * t + 16 * h);
+        for (int t = 0; t < NTO; ++t)
+            asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dwordx4 %0, %1"
+                         :: "v"(qoff + 32 * t), "s"(qb), "s"(dst + t * 1024) : "memory", "m0");
     }
-    if (npair > 0) issue(0);
+    for (int pr = 0; pr < R - 1 && pr < npair; ++pr) issue(pr);
+
     i16x o[3][NTO];
 #pragma unroll
     for (int j = 0; j < 3; ++j)
@@ -546,26 +582,40 @@ __global__ __launch_bounds__(512) void k_attn_i32s(const AttnParams p) {
     int vs[NTO];                                 // V column n*32 + l32, keys of half h
 #pragma unroll
     for (int n = 0; n < NTO; ++n) vs[n] = 0;
+    i4 qf[NTO];
 
     // the offset limbs of S (bytes of S ^ 0x8080, read as int8): K-slot
     // (h, e) of the second product is key 8*(e/4) + 4*h + e%4, as the S^T
-    // accumulator layout gives
+    // accumulator layout gives.  Per four elements a, b, c, d a byte
+    // transpose: (a0 b0 a1 b1), (c0 d0 c1 d1), (a2 b2 - -), (c2 d2 - -), then
+    // limb j = (a_j b_j c_j d_j); the XOR with 0x80 of bytes 0 and 1 is done
+    // on the transposed words.
     auto limbs = [](const i16x& s, i4 (&limb)[3]) {
-        uint32_t x[16];
 #pragma unroll
-        for (int r = 0; r < 16; ++r) x[r] = (uint32_t)s[r] ^ 0x8080u;
-#pragma unroll
-        for (int jj = 0; jj < 3; ++jj)
-#pragma unroll
-            for (int w = 0; w < 4; ++w)
-                limb[jj][w] = (int)gather_byte(x[4 * w], x[4 * w + 1], x[4 * w + 2], x[4 * w + 3], jj);
+        for (int w = 0; w < 4; ++w) {
+            const uint32_t a = (uint32_t)s[4 * w], b = (uint32_t)s[4 * w + 1];
+            const uint32_t c = (uint32_t)s[4 * w + 2], d = (uint32_t)s[4 * w + 3];
+            const uint32_t ab01 = __builtin_amdgcn_perm(b, a, 0x05010400u);
+            const uint32_t cd01 = __builtin_amdgcn_perm(d, c, 0x05010400u);
+            const uint32_t ab2 = __builtin_amdgcn_perm(b, a, 0x0C0C0602u);
+            const uint32_t cd2 = __builtin_amdgcn_perm(d, c, 0x0C0C0602u);
+            limb[0][w] = (int)(__builtin_amdgcn_perm(cd01, ab01, 0x05040100u) ^ 0x80808080u);
+            limb[1][w] = (int)(__builtin_amdgcn_perm(cd01, ab01, 0x07060302u) ^ 0x80808080u);
+            limb[2][w] = (int)__builtin_amdgcn_perm(cd2, ab2, 0x05040100u);
+        }
     };
     for (int pr = 0; pr < npair; ++pr) {
-        __builtin_amdgcn_s_waitcnt(0x0F70);      // this wave's part of pair pr landed
-        __syncthreads();                         // every part landed; slot (pr+1)&1 read by all
-        if (pr + 1 < npair) issue(pr + 1);       // one pair ahead, into the slot freed above
-        const char* st0 = &ring[kh][pr & 1][0][0];
-        const char* st1 = &ring[kh][pr & 1][1][0];
+        // this wave's loads of pair pr (and, before them, its Q rows) have
+        // landed once no more than those of the later pairs are in flight
+        wait_vmcnt_steps<PW, R - 2>(npair - 1 - pr);
+        __syncthreads();                         // every part landed; slot of pair pr-1 read by all
+        if (pr + R - 1 < npair) issue(pr + R - 1);
+        if (pr == 0) {
+#pragma unroll
+            for (int t = 0; t < NTO; ++t) qf[t] = *(const i4*)(&qs[wave][t * 1024 + lane * 16]);
+        }
+        const char* st0 = &ring[kp][pr & (R - 1)][0][0];
+        const char* st1 = &ring[kp][pr & (R - 1)][1][0];
         i4 kf0[NTO], kf1[NTO], vf0[NTO], vf1[NTO];
 #pragma unroll
         for (int t = 0; t < NTO; ++t) {
@@ -579,20 +629,33 @@ __global__ __launch_bounds__(512) void k_attn_i32s(const AttnParams p) {
         }
         // two independent S^T chains, then each block's limbs beside the
         // other's matrix products
+        // both S^T chains are issued before any limb work (pinned: left
+        // alone, the scheduler ran the second chain after the first block's
+        // products, so every limb split waited on its own chain)
         i16x s0 = i16x{}, s1 = i16x{};
 #pragma unroll
         for (int t = 0; t < NTO; ++t) {
             s0 = __builtin_amdgcn_mfma_i32_32x32x32_i8(kf0[t], qf[t], s0, 0, 0, 0);
             s1 = __builtin_amdgcn_mfma_i32_32x32x32_i8(kf1[t], qf[t], s1, 0, 0, 0);
         }
+        asm volatile("" : "+v"(s1));
+        __builtin_amdgcn_sched_barrier(0);
         i4 l0[3], l1[3];
         limbs(s0, l0);
+        __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
         for (int n = 0; n < NTO; ++n)
 #pragma unroll
             for (int jj = 0; jj < 3; ++jj)
                 o[jj][n] = __builtin_amdgcn_mfma_i32_32x32x32_i8(l0[jj], vf0[n], o[jj][n], 0, 0, 0);
         limbs(s1, l1);
+        // the second block's limb split between the first block's products
+#pragma unroll
+        for (int g = 0; g < 3 * NTO; ++g) {
+            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);          // one MFMA
+            __builtin_amdgcn_sched_group_barrier(0x002, 36 / (3 * NTO), 0);   // VALU
+        }
+        __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
         for (int n = 0; n < NTO; ++n) {
 #pragma unroll
@@ -616,36 +679,37 @@ __global__ __launch_bounds__(512) void k_attn_i32s(const AttnParams p) {
         for (int r = 0; r < 16; ++r)
             v[n][r] = (uint32_t)o[0][n][r] + ((uint32_t)o[1][n][r] << 8) + ((uint32_t)o[2][n][r] << 16) + corr;
     }
-    // key half 1 hands its sums to key half 0 through the ring, once every
-    // wave is done reading it: a quarter of the ring per query tile
-    uint32_t* red = (uint32_t*)&ring[0][0][0][0] + qw * (NTO * 16 * 64);   // [NTO][16][64]
-    static_assert(4 * NTO * 16 * 64 * 4 <= (int)sizeof(ring), "exchange fits the ring");
+    // the partial outputs of the KQ key parts, [QT][KQ][32][D], through the
+    // ring once every wave is done reading it
+    uint32_t* red = (uint32_t*)&ring[0][0][0][0];
+    static_assert(8 * 32 * D * 4 <= (int)sizeof(ring), "partial outputs fit the ring");
     __syncthreads();
-    if (kh == 1) {
+    {
+        uint32_t* mine = red + (qw * KQ + kp) * (32 * D);
 #pragma unroll
         for (int n = 0; n < NTO; ++n)
 #pragma unroll
-            for (int r = 0; r < 16; ++r) red[(n * 16 + r) * 64 + lane] = v[n][r];
+            for (int r = 0; r < 16; ++r)
+                mine[(8 * (r >> 2) + 4 * h + (r & 3)) * D + n * 32 + l32] = v[n][r];
     }
     __syncthreads();
-    if (kh == 1) return;
-#pragma unroll
-    for (int n = 0; n < NTO; ++n)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) v[n][r] += red[(n * 16 + r) * 64 + lane];
+    // wave (qw, kp) adds slice kp of query tile qw: 64 consecutive outputs
+    // (row-major, query by column) per step, one atomic per output
+    constexpr int PERW = 32 * D / 64 / KQ;
+    const uint32_t* tile = red + qw * KQ * (32 * D);
     int32_t* dst = (int32_t*)p.O;
 #pragma unroll
-    for (int n = 0; n < NTO; ++n) {
-        const int c = n * 32 + l32;
+    for (int i = 0; i < PERW; ++i) {
+        const int e = (kp * PERW + i) * 64 + lane;
+        uint32_t t = 0;
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-            const int q = q0 + 8 * (r >> 2) + 4 * h + (r & 3);
-            if (q >= p.L) continue;
-            // splits add into the output cleared by the prep launch:
-            // wrapping int32 atomics, exact mod 2^32 in any order
-            if (p.splits > 1) atomicAdd(dst + (int64_t)q * D + c, (int)v[n][r]);
-            else dst[(int64_t)q * D + c] = (int32_t)v[n][r];
-        }
+        for (int k = 0; k < KQ; ++k) t += tile[k * 32 * D + e];
+        const int q = q0 + e / D, c = e % D;
+        if (q >= p.L) continue;
+        // splits add into the output cleared by the prep launch:
+        // wrapping int32 atomics, exact mod 2^32 in any order
+        if (p.splits > 1) atomicAdd(dst + (int64_t)q * D + c, (int)t);
+        else dst[(int64_t)q * D + c] = (int32_t)t;
     }
 }
 
@@ -927,14 +991,14 @@ bool build_attn_i32r(const AttnParams& p, LaunchRec* rec) {
 }
 
 bool build_attn_i32s(const AttnParams& p, LaunchRec* rec) {
-    switch (p.d) {
-    case 32: rec->fn = (const void*)k_attn_i32s<32>; break;
-    case 64: rec->fn = (const void*)k_attn_i32s<64>; break;
-    default: return false;
-    }
-    if (p.keys_per_split % 128 != 0 || !p.v_blocks) return false;
+    int keys = 0;
+#define QX_ATTN_S(DD, QQ) \
+    if (p.d == DD && p.qt == QQ) { rec->fn = (const void*)k_attn_i32s<DD, QQ>; keys = AttnStream<DD, QQ>::KEYS; }
+    QX_ATTN_S(32, 2) QX_ATTN_S(64, 2)
+#undef QX_ATTN_S
+    if (keys == 0 || p.keys_per_split % keys != 0 || !p.v_blocks) return false;
     rec->name = "attn_i32_stream";
-    rec->grid = dim3((unsigned)((p.L + AQ - 1) / AQ), (unsigned)p.splits, 1);
+    rec->grid = dim3((unsigned)((p.L + 32 * p.qt - 1) / (32 * p.qt)), (unsigned)p.splits, 1);
     rec->block = dim3(512, 1, 1);
     rec->set_params(p);
     return true;

@@ -170,7 +170,7 @@ struct AttnParams {
     int32_t v_blocks;       // prep: 1 = write V8 block-major, [Lp/32][d][32] (each 32-key block of
                             // every column contiguous, keys reordered as above), for the
                             // streaming kernel; 0 = [d][Lp]
-    int32_t pad0;
+    int32_t qt;             // streaming kernel: query tiles of 32 per workgroup (1, 2 or 4)
     void* q8;               // prep_q > 0: int8 rows of Q, [L][d]
     int64_t prep_q;         // prep work items: 16-byte Q8 chunks (0: none)
 };

@@ -273,11 +273,16 @@ def test_attention_plans():
     p = qx.plan_attn("f32", 4096, 64)
     assert p["tile_k"] % 32 == 0 and (4096 // 128) * (4096 // p["tile_k"]) >= 256
     assert p["tile_k"] == 512
-    # INT32, d = 64: the streaming kernel takes splits of whole 64-key
-    # pairs of blocks, one workgroup per CU (32 query groups x 8 splits of
-    # 512 keys); d = 128 keeps the LDS-resident splits, both int8 tiles
-    # within 48 KiB of LDS (192 keys)
-    assert qx.plan_attn("i32", 4096, 64, 64)["tile_k"] == 512
+    # INT32, d = 32 and 64: the streaming kernel (64 queries per workgroup,
+    # four key parts of whole 64-key pairs of blocks) fills the chip with 64
+    # query groups x 4 splits of 1024 keys; short sequences round the split
+    # up to 256 keys; d = 128 keeps the LDS-resident splits, both int8
+    # tiles within 48 KiB of LDS (192 keys)
+    assert qx.plan_attn("i32", 4096, 64, 64)["tile_k"] == 1024
+    assert qx.plan_attn("i32", 4096, 32, 64)["tile_k"] == 1024
+    for L in (1, 63, 65, 300, 2049, 8191):
+        kps = qx.plan_attn("i32", L, 64, 64)["tile_k"]
+        assert kps % 256 == 0 and kps >= 256
     assert qx.plan_attn("i32", 4096, 128, 64)["tile_k"] == 192
 
 

@@ -370,9 +370,10 @@ def test_attn_f32(L, d):
                                    (5000, 32, 127), (2049, 64, 127), (4096, 64, 127), (63, 32, 127),
                                    (64, 64, 1), (65, 64, 127), (8191, 64, 64)])
 def test_attn_i32_mfma(L, d, b):
-    # d in {32, 64}: the prep launch plus the register-streaming kernel
-    # (eight waves, two key halves per split joined in LDS; ragged last
-    # split, zero-padded keys; one split -> plain stores); d = 128: the
+    # d in {32, 64}: the prep launch plus the streaming kernel (eight
+    # waves: two query tiles x four key parts per split, joined in LDS;
+    # query tiles past L, ragged last split, zero-padded keys; one split ->
+    # plain stores); d = 128: the
     # prep plus the LDS-resident splits; d = 96: the LDS-staged loop kernel
     rng = np.random.default_rng(L * 3 + d + b)
     Q, K, V = (rand_int(rng, (L, d), b, np.int32) for _ in range(3))
