@@ -604,6 +604,13 @@ __global__ __launch_bounds__(512) void k_attn_i32s(const AttnParams p) {
             limb[2][w] = (int)__builtin_amdgcn_perm(cd2, ab2, 0x05040100u);
         }
     };
+    // Software pipeline: the second block's limb products of pair pr run at
+    // the start of pair pr+1, beside its S^T chains and first limb split
+    // (zero limbs stand in before the first pair: they add nothing).
+    i4 lp[3] = {i4{}, i4{}, i4{}};
+    i4 vp[NTO];
+#pragma unroll
+    for (int n = 0; n < NTO; ++n) vp[n] = i4{};
     for (int pr = 0; pr < npair; ++pr) {
         // this wave's loads of pair pr (and, before them, its Q rows) have
         // landed once no more than those of the later pairs are in flight
@@ -627,11 +634,9 @@ __global__ __launch_bounds__(512) void k_attn_i32s(const AttnParams p) {
             vf0[n] = *(const i4*)(st0 + (NTO + n) * 1024 + lane * 16);
             vf1[n] = *(const i4*)(st1 + (NTO + n) * 1024 + lane * 16);
         }
-        // two independent S^T chains, then each block's limbs beside the
-        // other's matrix products
-        // both S^T chains are issued before any limb work (pinned: left
-        // alone, the scheduler ran the second chain after the first block's
-        // products, so every limb split waited on its own chain)
+        // both S^T chains first (pinned: left alone, the scheduler ran the
+        // second chain after the first block's products, so every limb split
+        // waited on its own chain)
         i16x s0 = i16x{}, s1 = i16x{};
 #pragma unroll
         for (int t = 0; t < NTO; ++t) {
@@ -640,34 +645,51 @@ __global__ __launch_bounds__(512) void k_attn_i32s(const AttnParams p) {
         }
         asm volatile("" : "+v"(s1));
         __builtin_amdgcn_sched_barrier(0);
+        // the previous pair's second-block products beside this pair's first
+        // limb split
         i4 l0[3], l1[3];
+#pragma unroll
+        for (int n = 0; n < NTO; ++n)
+#pragma unroll
+            for (int jj = 0; jj < 3; ++jj)
+                o[jj][n] = __builtin_amdgcn_mfma_i32_32x32x32_i8(lp[jj], vp[n], o[jj][n], 0, 0, 0);
         limbs(s0, l0);
+#pragma unroll
+        for (int g = 0; g < 3 * NTO; ++g) {
+            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+            __builtin_amdgcn_sched_group_barrier(0x002, 36 / (3 * NTO), 0);
+        }
         __builtin_amdgcn_sched_barrier(0);
+        // the first block's products beside the second block's limb split
 #pragma unroll
         for (int n = 0; n < NTO; ++n)
 #pragma unroll
             for (int jj = 0; jj < 3; ++jj)
                 o[jj][n] = __builtin_amdgcn_mfma_i32_32x32x32_i8(l0[jj], vf0[n], o[jj][n], 0, 0, 0);
         limbs(s1, l1);
-        // the second block's limb split between the first block's products
 #pragma unroll
         for (int g = 0; g < 3 * NTO; ++g) {
-            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);          // one MFMA
-            __builtin_amdgcn_sched_group_barrier(0x002, 36 / (3 * NTO), 0);   // VALU
+            __builtin_amdgcn_sched_group_barrier(0x008, 1, 1);
+            __builtin_amdgcn_sched_group_barrier(0x002, 36 / (3 * NTO), 1);
         }
         __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-        for (int n = 0; n < NTO; ++n) {
+        for (int n = 0; n < NTO; ++n)
 #pragma unroll
             for (int w = 0; w < 4; ++w) {
                 vs[n] = __builtin_amdgcn_sdot4(vf0[n][w], 0x01010101, vs[n], false);
                 vs[n] = __builtin_amdgcn_sdot4(vf1[n][w], 0x01010101, vs[n], false);
             }
 #pragma unroll
-            for (int jj = 0; jj < 3; ++jj)
-                o[jj][n] = __builtin_amdgcn_mfma_i32_32x32x32_i8(l1[jj], vf1[n], o[jj][n], 0, 0, 0);
-        }
+        for (int jj = 0; jj < 3; ++jj) lp[jj] = l1[jj];
+#pragma unroll
+        for (int n = 0; n < NTO; ++n) vp[n] = vf1[n];
     }
+#pragma unroll
+    for (int n = 0; n < NTO; ++n)
+#pragma unroll
+        for (int jj = 0; jj < 3; ++jj)
+            o[jj][n] = __builtin_amdgcn_mfma_i32_32x32x32_i8(lp[jj], vp[n], o[jj][n], 0, 0, 0);
 
     // recombine the limbs and add the offset correction of this wave's keys
     uint32_t v[NTO][16];
