@@ -496,9 +496,9 @@ __device__ __forceinline__ f16x mfma_h(h8 a, h8 b, f16x c) {
         return __builtin_amdgcn_mfma_f32_32x32x16_f16(a, b, c, 0, 0, 0);
 }
 
-template <int BM, int BN, int NW, bool IMPL, bool BF>
+template <int BM, int BN, int NW, bool IMPL, bool BF, int WN = 64>
 __global__ __launch_bounds__(NW * 64) void k_gemm_nt(const GemmParams p) {
-    constexpr int BK = 64, KCH = 8, WM = 64, WN = 64;
+    constexpr int BK = 64, KCH = 8, WM = 64;
     constexpr int TM = WM / 32, TN = WN / 32;
     constexpr int WAVES_N = BN / WN;
     static_assert((BM / WM) * (BN / WN) == NW, "wave grid");
@@ -898,9 +898,11 @@ void build_gemm_nt(const GemmParams& p0, int batch, LaunchRec* rec) {
         rec->block = dim3(512, 1, 1);
         rec->name = impl ? "gemm_nt_conv_128x256" : bf ? "gemm_nt_bf16_128x256" : "gemm_nt_128x256";
     } else if (bm == 64) {
-        rec->fn = impl ? (const void*)k_gemm_nt<64, 128, 2, true, false>
+        // the conv gather runs four 64x32 waves (more loads in flight per
+        // CU than two 64x64 ones: 14.0 -> 12.2 us on 8x64x56x56 -> 128)
+        rec->fn = impl ? (const void*)k_gemm_nt<64, 128, 4, true, false, 32>
                        : bf ? (const void*)k_gemm_nt<64, 128, 2, false, true> : (const void*)k_gemm_nt<64, 128, 2, false, false>;
-        rec->block = dim3(128, 1, 1);
+        rec->block = dim3(impl ? 256 : 128, 1, 1);
         rec->name = impl ? "gemm_nt_conv_64x128" : bf ? "gemm_nt_bf16_64x128" : "gemm_nt_64x128";
     } else {
         rec->fn = impl ? (const void*)k_gemm_nt<128, 128, 4, true, false>

@@ -321,6 +321,10 @@ CONV_IMPLICIT_CASES = [  # C_in a multiple of 64: implicit lowering from the NHW
     (2, 64, 30, 26, 100, 3, 3, 1, 1, 256), (3, 128, 17, 19, 64, 3, 3, 2, 1, 256),
     (2, 64, 23, 23, 64, 7, 7, 2, 3, 128), (1, 192, 14, 14, 256, 3, 3, 1, 0, 256),
     (4, 64, 9, 33, 48, 5, 3, 1, 2, 255), (8, 256, 32, 32, 64, 1, 1, 2, 0, 256),
+    # 128 channels (two K tiles per tap), stride 2, 1x1 and 5x5 kernels,
+    # pixel tiles ending mid-row and short images
+    (2, 128, 12, 10, 70, 3, 3, 1, 1, 256), (8, 64, 9, 24, 64, 3, 3, 2, 1, 256),
+    (12, 64, 16, 16, 130, 1, 1, 1, 0, 256), (1, 64, 19, 23, 64, 5, 5, 1, 2, 255),
 ]
 
 
