@@ -705,33 +705,38 @@ __device__ __forceinline__ void wait_tiles(int n) {
 #undef QX_WAIT
 }
 
-// WAVES = 4: a 2 x 2 grid of waves; WAVES = 8: 2 (M) x 4 (N), two waves per
-// SIMD, which halves a 128 x 128 tile's per-wave accumulators.
-template <class S, int BM, int BN, int STAGES, int WAVES>
+// WAVES / KG = 4: a 2 x 2 grid of waves; 8: 2 (M) x 4 (N), two waves per
+// SIMD, which halves a 128 x 128 tile's per-wave accumulators.  KG = 2: two
+// such grids take alternate K tiles of the same output tile (two waves per
+// SIMD for 64 x 64 tiles) and are added through LDS at the end.
+template <class S, int BM, int BN, int STAGES, int WAVES, int KG = 1>
 __global__ __launch_bounds__(64 * WAVES) void k_gemm_i8nt(const GemmParams p) {
-    constexpr int NTH = 64 * WAVES, WGN = WAVES / 2;
+    constexpr int NTH = 64 * WAVES, GW = WAVES / KG, WGN = GW / 2;
     constexpr int BK = 64, KCH = 4, P = S::PLANES, G = S::GROUPS;
     constexpr int WM = BM / 2, WN = BN / WGN, TM = WM / 32, TN = WN / 32;
-    static_assert(WAVES == 4 || WAVES == 8, "wave grid");
+    static_assert(GW == 4 || GW == 8, "wave grid");
+    static_assert(KG == 1 || KG == 2, "K groups");
     static_assert(TM >= 1 && TN >= 1, "whole 32 x 32 blocks per wave");
-    static_assert(STAGES >= 3 && STAGES <= 6, "ring depth");
+    static_assert(STAGES >= 2 * KG + 1 && STAGES <= 6, "ring depth");
     // offset routes: besides its share of the two operand tiles, every wave
     // loads one dword per lane of the K tile's column-sum row (the encoder
     // writes one row of column sums per 64 K), so the column sums add up
     // alongside the K loop for any K; only the first BN/64 waves' values
     // are used
     constexpr bool OFFS = S::PAD != 0;
-    constexpr int AL = P * BM * KCH / NTH, BL = P * BN * KCH / NTH, LPT = AL + BL + (OFFS ? 1 : 0);
-    static_assert(AL * NTH == P * BM * KCH && BL * NTH == P * BN * KCH, "whole loads");
+    // a stage holds the A planes' tile then the B planes' tile, 16-byte
+    // chunks; every wave issues LAB of its wave-wide (1 KB) loads
+    constexpr int CH_A = P * BM * KCH, CH_B = P * BN * KCH, CH = CH_A + CH_B;
+    constexpr int LAB = CH / NTH, LPT = LAB + (OFFS ? 1 : 0);
+    static_assert(LAB * NTH == CH && CH_A % 64 == 0, "whole, wave-uniform loads");
     static_assert(BN <= NTH, "one column-sum dword per thread");
-    constexpr unsigned STAGE_A = P * BM * KCH * 16, STAGE_B = P * BN * KCH * 16;
-    __shared__ i4 As[STAGES][P][BM][KCH];
-    __shared__ i4 Bs[STAGES][P][BN][KCH];
+    __shared__ i4 Stg[STAGES][CH];
     __shared__ uint32_t cs_ring[OFFS ? STAGES : 1][NTH];
     __shared__ uint32_t rs_l[BM], csum_l[BN];
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, l32 = lane & 31, hh = lane >> 5;
-    const int wm = wave / WGN, wn = wave % WGN;
+    const int kg = wave / GW, wl = wave % GW;
+    const int wm = wl / WGN, wn = wl % WGN;
     const int tiles_m = (p.M + BM - 1) / BM;
     int pid = blockIdx.x;
     const int total = gridDim.x;
@@ -775,22 +780,22 @@ __global__ __launch_bounds__(64 * WAVES) void k_gemm_i8nt(const GemmParams p) {
     // planes: A8 [batch][P][Mp][Kp] (sA = P*Mp*Kp, lda = Kp, plane_a = Mp*Kp), B8T likewise
     const char* a_panel = (const char*)p.A + b * p.sA + (int64_t)m0 * p.lda + kt0 * BK;
     const char* b_panel = (const char*)p.B + b * p.sB + (int64_t)n0 * p.ldb + kt0 * BK;
-    unsigned oa[AL], ob[BL];
-#pragma unroll
-    for (int i = 0; i < AL; ++i) {
-        const int q = tid + NTH * i, plane = q / (BM * KCH), rem = q % (BM * KCH);
-        const int row = rem / KCH, pc = rem % KCH;
-        oa[i] = (unsigned)((int64_t)plane * p.plane_a + row * p.lda + (pc ^ swz_i8(row)) * 16);
-    }
-#pragma unroll
-    for (int i = 0; i < BL; ++i) {
-        const int q = tid + NTH * i, plane = q / (BN * KCH), rem = q % (BN * KCH);
-        const int row = rem / KCH, pc = rem % KCH;
-        ob[i] = (unsigned)((int64_t)plane * p.plane_b + row * p.ldb + (pc ^ swz_i8(row)) * 16);
-    }
     const unsigned wave_u = __builtin_amdgcn_readfirstlane(wave);
-    const unsigned lds_a0 = (unsigned)(uintptr_t)&As[0][0][0][0] + wave_u * 1024;
-    const unsigned lds_b0 = (unsigned)(uintptr_t)&Bs[0][0][0][0] + wave_u * 1024;
+    // load k of this wave covers stage chunks (wave + WAVES*k)*64 + lane
+    unsigned ol[LAB];
+#pragma unroll
+    for (int k = 0; k < LAB; ++k) {
+        const int q = (wave + WAVES * k) * 64 + lane;
+        if (q < CH_A) {
+            const int plane = q / (BM * KCH), rem = q % (BM * KCH), row = rem / KCH, pc = rem % KCH;
+            ol[k] = (unsigned)((int64_t)plane * p.plane_a + row * p.lda + (pc ^ swz_i8(row)) * 16);
+        } else {
+            const int qb = q - CH_A;
+            const int plane = qb / (BN * KCH), rem = qb % (BN * KCH), row = rem / KCH, pc = rem % KCH;
+            ol[k] = (unsigned)((int64_t)plane * p.plane_b + row * p.ldb + (pc ^ swz_i8(row)) * 16);
+        }
+    }
+    const unsigned lds_s0 = (unsigned)(uintptr_t)&Stg[0][0];
     // column sums [batch][K/64][N]: this thread's column, clamped into N
     // (columns past N are never stored)
     const int32_t* csg = OFFS ? p.colsum + ((int64_t)b * p.cs_slices + kt0) * p.N : nullptr;
@@ -800,15 +805,14 @@ __global__ __launch_bounds__(64 * WAVES) void k_gemm_i8nt(const GemmParams p) {
         const int s = t % STAGES;
         const char* ab = a_panel + t * BK;
         const char* bb = b_panel + t * BK;
-        const unsigned la = lds_a0 + s * STAGE_A, lb = lds_b0 + s * STAGE_B;
+        const unsigned ls = lds_s0 + (unsigned)(s * CH * 16);
 #pragma unroll
-        for (int i = 0; i < AL; ++i)
+        for (int k = 0; k < LAB; ++k) {
+            const unsigned blk = wave_u + WAVES * k;
+            const char* base = (int)blk * 64 < CH_A ? ab : bb;
             asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dwordx4 %0, %1"
-                         :: "v"(oa[i]), "s"(ab), "s"(la + NTH * 16 * i) : "memory", "m0");
-#pragma unroll
-        for (int i = 0; i < BL; ++i)
-            asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dwordx4 %0, %1"
-                         :: "v"(ob[i]), "s"(bb), "s"(lb + NTH * 16 * i) : "memory", "m0");
+                         :: "v"(ol[k]), "s"(base), "s"(ls + blk * 1024) : "memory", "m0");
+        }
         if constexpr (OFFS)
             asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dword %0, %1"
                          :: "v"(cs_off), "s"(csg + (int64_t)t * p.N), "s"(lds_cs0 + s * NTH * 4) : "memory", "m0");
@@ -836,16 +840,25 @@ __global__ __launch_bounds__(64 * WAVES) void k_gemm_i8nt(const GemmParams p) {
     }
     uint32_t csum_acc = 0;   // this thread's column sum over the K tiles seen
 #pragma unroll
-    for (int s = 0; s < STAGES - 1; ++s)
+    for (int s = 0; s < STAGES - KG; ++s)
         if (s < ktiles) issue(s);
-    for (int t = 0; t < ktiles; ++t) {
-        // tile t must have landed; the tiles after it may still be in flight
-        // (and the sums, issued before tile 0, have landed with it)
-        wait_tiles<LPT>(min(STAGES - 2, ktiles - 1 - t));
+    for (int t = 0; t < ktiles; t += KG) {
+        // tiles t .. t+KG-1 must have landed; up to STAGES-2KG after them
+        // may still be in flight (and the sums, issued before tile 0, have
+        // landed with them)
+        const int last = min(t + KG, ktiles) - 1;
+        wait_tiles<LPT>(min(STAGES - 2 * KG, ktiles - 1 - last));
         __syncthreads();
-        const int s = t % STAGES;
-        if (OFFS && tid < BN) csum_acc += cs_ring[s][tid];   // before the stage is refilled
-        if (t + STAGES - 1 < ktiles) issue(t + STAGES - 1);
+        if (OFFS && tid < BN)
+            for (int u = t; u <= last; ++u) csum_acc += cs_ring[u % STAGES][tid];   // before refills
+        // the slots of the previous KG tiles are free: every wave is past
+        // the barrier, so done with them
+#pragma unroll
+        for (int u = 0; u < KG; ++u)
+            if (t + STAGES - KG + u < ktiles) issue(t + STAGES - KG + u);
+        const int tt = t + kg;               // this wave group's tile
+        if (tt >= ktiles) continue;
+        const int s = tt % STAGES;
 #pragma unroll
         for (int ks = 0; ks < BK / 32; ++ks) {
             const int c = ks * 2 + hh;
@@ -855,12 +868,12 @@ __global__ __launch_bounds__(64 * WAVES) void k_gemm_i8nt(const GemmParams p) {
 #pragma unroll
                 for (int i = 0; i < TM; ++i) {
                     const int row = wm * WM + i * 32 + l32;
-                    a[q][i] = As[s][q][row][c ^ swz_i8(row)];
+                    a[q][i] = Stg[s][(q * BM + row) * KCH + (c ^ swz_i8(row))];
                 }
 #pragma unroll
                 for (int j = 0; j < TN; ++j) {
                     const int col = wn * WN + j * 32 + l32;
-                    bv[q][j] = Bs[s][q][col][c ^ swz_i8(col)];
+                    bv[q][j] = Stg[s][CH_A + (q * BN + col) * KCH + (c ^ swz_i8(col))];
                 }
             }
 #pragma unroll
@@ -874,7 +887,43 @@ __global__ __launch_bounds__(64 * WAVES) void k_gemm_i8nt(const GemmParams p) {
         }
     }
 
-    if (OFFS) {
+    // limb groups recombined per output (wrapping int32: the sum of the K
+    // groups' combinations is the combination of their sums)
+    uint32_t vs[TM][TN][16];
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+                uint32_t gv[G];
+#pragma unroll
+                for (int q = 0; q < G; ++q) gv[q] = (uint32_t)acc[q][i][j][r];
+                vs[i][j][r] = S::combine(gv);
+            }
+    if constexpr (KG == 2) {
+        // group 1 hands its sums to group 0 through the (drained) stage ring
+        static_assert(GW * TM * TN * 16 * 64 * 4 <= (int)sizeof(Stg), "exchange fits the ring");
+        uint32_t* xch = (uint32_t*)&Stg[0][0] + wl * (TM * TN * 16 * 64);
+        __syncthreads();
+        if (kg == 1) {
+#pragma unroll
+            for (int i = 0; i < TM; ++i)
+#pragma unroll
+                for (int j = 0; j < TN; ++j)
+#pragma unroll
+                    for (int r = 0; r < 16; ++r) xch[((i * TN + j) * 16 + r) * 64 + lane] = vs[i][j][r];
+        }
+        if (OFFS && tid < BN) csum_l[tid] = csum_acc;
+        __syncthreads();
+        if (kg == 1) return;
+#pragma unroll
+        for (int i = 0; i < TM; ++i)
+#pragma unroll
+            for (int j = 0; j < TN; ++j)
+#pragma unroll
+                for (int r = 0; r < 16; ++r) vs[i][j][r] += xch[((i * TN + j) * 16 + r) * 64 + lane];
+    } else if (OFFS) {
         if (tid < BN) csum_l[tid] = csum_acc;
         __syncthreads();
     }
@@ -893,10 +942,7 @@ __global__ __launch_bounds__(64 * WAVES) void k_gemm_i8nt(const GemmParams p) {
                 const int lr = wm * WM + i * 32 + 8 * (r >> 2) + 4 * hh + (r & 3);
                 const int gm = m0 + lr;
                 if (gm >= p.M) continue;
-                uint32_t gv[G];
-#pragma unroll
-                for (int q = 0; q < G; ++q) gv[q] = (uint32_t)acc[q][i][j][r];
-                uint32_t v = S::combine(gv);
+                uint32_t v = vs[i][j][r];
                 if (OFFS) {
                     v += ccol;
                     if (lead) v += cc * rs_l[lr] - kcc;
@@ -1124,7 +1170,7 @@ bool build_gemm_i8nt(int32_t route, const GemmParams& p0, int batch, LaunchRec* 
     const bool deep = (int64_t)((p0.M + 63) / 64) * ((p0.N + 63) / 64) * batch * std::max(p0.ksplit, 1) <= 256;
 #define QX_NT(S, NAME)                                                                               \
     if (big) fill_gemm_rec(rec, k_gemm_i8nt<S, 128, 128, 3, 8>, p0, 128, 128, batch, "gemm_i8nt_" NAME "_128x128"); \
-    else if (deep) fill_gemm_rec(rec, k_gemm_i8nt<S, 64, 64, 6, 4>, p0, 64, 64, batch, "gemm_i8nt_" NAME "_64x64"); \
+    else if (deep) fill_gemm_rec(rec, k_gemm_i8nt<S, 64, 64, 6, 8, 2>, p0, 64, 64, batch, "gemm_i8nt_" NAME "_64x64"); \
     else fill_gemm_rec(rec, k_gemm_i8nt<S, 64, 64, 3, 4>, p0, 64, 64, batch, "gemm_i8nt_" NAME "_64x64_3");
     switch (route) {
     case R_I8_DIRECT: QX_NT(SchemeDirect, "direct") break;
@@ -1134,7 +1180,7 @@ bool build_gemm_i8nt(int32_t route, const GemmParams& p0, int batch, LaunchRec* 
     default: return false;
     }
 #undef QX_NT
-    if (big) rec->block = dim3(512, 1, 1);
+    if (big || deep) rec->block = dim3(512, 1, 1);
     if (p0.ksplit > 1) rec->grid.y = (unsigned)p0.ksplit;
     if (batch > 1 && (int64_t)rec->grid.x * batch < ((int64_t)1 << 31)) {
         GemmParams p = *(const GemmParams*)rec->blob;
