@@ -37,9 +37,9 @@ PEAK = {"f16": 2500.0, "i8": 5000.0, "f32": 157.3, "hbm": 8000.0}  # TFLOP/s, TO
 # the kernel has changed since.
 TRAFFIC = {
     "kernel": "gemm_nt_bf16_128x256",
-    "kernel_sha256": "43954b6e7b2f25293ff5badfb5601621a4283eb531564e0a2f8be35c36f728cc",
-    "read_bytes": 2147791043,     # FETCH_SIZE 1048757.8 KiB x 2.0 (copy: 524304 KiB per GiB read)
-    "write_bytes": 268485120,     # WRITE_SIZE 262192.5 KiB x 1.0 (copy: 1048576 KiB per GiB written)
+    "kernel_sha256": "0bb74a1223cec68350a328ba966c67024fd244d9e30b741bd6387b409294faca",
+    "read_bytes": 2147840000,     # FETCH_SIZE 1048750 KiB x 2.0 (copy: 524304 KiB per GiB read)
+    "write_bytes": 268495872,     # WRITE_SIZE 262203 KiB x 1.0 (copy: 1048576 KiB per GiB written)
 }
 KERNEL_SRC = os.path.join(ROOT, "paper_2606_09905_amd", "csrc", "k_gemm_nt.hip")
 
