@@ -87,24 +87,28 @@ __global__ __launch_bounds__(256) void k_enc_a(const EncParams p) {
     }
 }
 
-// B [batch][K][ldb] int16 -> BT16 [batch][Np][Kp] fp16 (bf16 with BF)
-// transposed in registers.  A wave owns a 64(k) x 64(n) tile; lane
-// (kb, nb) = (lane / 8, lane % 8) reads eight 16-byte rows k = 8kb + r
-// (n = 8nb .. 8nb + 7) and writes eight 16-byte rows n = 8nb + e
-// (k = 8kb .. 8kb + 7): both sides move whole 128-byte lines per eight
-// lanes, and no LDS is involved.  A block is four waves along k.
+// B [batch][K][ldb] int16 -> BT16 [batch][Np][Kp] fp16 (bf16 with BF),
+// transposed through LDS with 256-byte segments on both sides (128-byte
+// ones, transposing in registers only, took 57 us against 48 us for an
+// 8192 x 8192 operand): a workgroup takes 128 (k) x 128 (n); wave w reads rows k = 32w .. 32w+31, lane (kb, nb)
+// = (lane / 16, lane % 16) eight 16-byte rows k = 32w + 8kb + r (n = 8nb ..
+// 8nb+7, sixteen lanes per 256-byte row segment), transposes its 8 x 8 block
+// in registers and puts its eight 16-byte rows n = 8nb + e into the LDS
+// tile [n][k]; the tile then leaves as 128 rows of 256 bytes.  Chunk c of
+// tile row n sits at c ^ ((n / 8) & 15), so both sides are conflict-free.
 template <bool BF>
-__global__ __launch_bounds__(256) void k_enc_bt2(const EncParams p) {
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    const int kb = lane >> 3, nb = lane & 7;
-    const int n0 = blockIdx.x * 64, k0 = (blockIdx.y * 4 + wave) * 64, b = blockIdx.z;
-    if (k0 >= p.Kp) return;
+__global__ __launch_bounds__(256) void k_enc_bt(const EncParams p) {
+    __shared__ h8 t[128][16];
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int kb = lane >> 4, nb = lane & 15;
+    const int n0 = blockIdx.x * 128, k0 = blockIdx.y * 128, b = blockIdx.z;
     const int16_t* src = (const int16_t*)p.src + b * p.s_src;
     s8v in[8];
     const int n = n0 + nb * 8;
+    const int kr = k0 + wave * 32 + kb * 8;
 #pragma unroll
     for (int r = 0; r < 8; ++r) {
-        const int k = k0 + kb * 8 + r;
+        const int k = kr + r;
         const int16_t* sp = src + (int64_t)k * p.ld_src + n;
         if (p.vec && k < p.K && n + 8 <= p.N) {
             in[r] = *(const s8v*)sp;
@@ -113,13 +117,22 @@ __global__ __launch_bounds__(256) void k_enc_bt2(const EncParams p) {
             for (int e = 0; e < 8; ++e) in[r][e] = (k < p.K && n + e < p.N) ? sp[e] : (short)0;
         }
     }
-    _Float16* dst = (_Float16*)p.dst + b * p.s_dst + (int64_t)n * p.Kp + k0 + kb * 8;
+    const int c = wave * 4 + kb;              // this lane's k chunk of the tile
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
         s8v col;
 #pragma unroll
         for (int r = 0; r < 8; ++r) col[r] = in[r][e];
-        *(h8*)(dst + (int64_t)e * p.Kp) = to_h8<BF>(col);
+        const int row = nb * 8 + e;
+        t[row][c ^ ((row >> 3) & 15)] = to_h8<BF>(col);
+    }
+    __syncthreads();
+    _Float16* dst = (_Float16*)p.dst + b * p.s_dst;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+        const int q = tid + 256 * i, row = q >> 4, cc = q & 15;
+        const int gn = n0 + row, gk = k0 + cc * 8;
+        if (gn < p.Np && gk < p.Kp) *(h8*)(dst + (int64_t)gn * p.Kp + gk) = t[row][cc ^ ((row >> 3) & 15)];
     }
 }
 
@@ -961,8 +974,8 @@ void build_enc_a(const EncParams& p, LaunchRec* rec) {
 }
 
 void build_enc_bt(const EncParams& p, LaunchRec* rec) {
-    rec->fn = p.bf16 ? (const void*)k_enc_bt2<true> : (const void*)k_enc_bt2<false>;
-    rec->grid = dim3((unsigned)(p.Np / 64), (unsigned)((p.Kp / 64 + 3) / 4), (unsigned)p.batch);
+    rec->fn = p.bf16 ? (const void*)k_enc_bt<true> : (const void*)k_enc_bt<false>;
+    rec->grid = dim3((unsigned)((p.Np + 127) / 128), (unsigned)((p.Kp + 127) / 128), (unsigned)p.batch);
     rec->block = dim3(256, 1, 1);
     rec->name = p.bf16 ? "enc_bt_bf16" : "enc_bt_f16";
     rec->set_params(p);
