@@ -708,16 +708,19 @@ __device__ __forceinline__ void wait_tiles(int n) {
 // WAVES / KG = 4: a 2 x 2 grid of waves; 8: 2 (M) x 4 (N), two waves per
 // SIMD, which halves a 128 x 128 tile's per-wave accumulators.  KG = 2: two
 // such grids take alternate K tiles of the same output tile (two waves per
-// SIMD for 64 x 64 tiles) and are added through LDS at the end.
+// SIMD for 64 x 64 tiles), each with its own STAGES-deep ring and its own
+// barrier (a counter in LDS), so the two groups run out of step: one
+// group's loads and barrier waits overlap the other's matrix products.
+// The groups are added through LDS at the end.
 template <class S, int BM, int BN, int STAGES, int WAVES, int KG = 1>
 __global__ __launch_bounds__(64 * WAVES) void k_gemm_i8nt(const GemmParams p) {
-    constexpr int NTH = 64 * WAVES, GW = WAVES / KG, WGN = GW / 2;
+    constexpr int NTH = 64 * WAVES, GW = WAVES / KG, GTH = 64 * GW, WGN = GW / 2;
     constexpr int BK = 64, KCH = 4, P = S::PLANES, G = S::GROUPS;
     constexpr int WM = BM / 2, WN = BN / WGN, TM = WM / 32, TN = WN / 32;
     static_assert(GW == 4 || GW == 8, "wave grid");
     static_assert(KG == 1 || KG == 2, "K groups");
     static_assert(TM >= 1 && TN >= 1, "whole 32 x 32 blocks per wave");
-    static_assert(STAGES >= 2 * KG + 1 && STAGES <= 6, "ring depth");
+    static_assert(STAGES >= 3 && STAGES <= 6, "ring depth");
     // offset routes: besides its share of the two operand tiles, every wave
     // loads one dword per lane of the K tile's column-sum row (the encoder
     // writes one row of column sums per 64 K), so the column sums add up
@@ -725,17 +728,19 @@ __global__ __launch_bounds__(64 * WAVES) void k_gemm_i8nt(const GemmParams p) {
     // are used
     constexpr bool OFFS = S::PAD != 0;
     // a stage holds the A planes' tile then the B planes' tile, 16-byte
-    // chunks; every wave issues LAB of its wave-wide (1 KB) loads
+    // chunks; every wave of a group issues LAB of its wave-wide (1 KB) loads
     constexpr int CH_A = P * BM * KCH, CH_B = P * BN * KCH, CH = CH_A + CH_B;
-    constexpr int LAB = CH / NTH, LPT = LAB + (OFFS ? 1 : 0);
-    static_assert(LAB * NTH == CH && CH_A % 64 == 0, "whole, wave-uniform loads");
-    static_assert(BN <= NTH, "one column-sum dword per thread");
-    __shared__ i4 Stg[STAGES][CH];
-    __shared__ uint32_t cs_ring[OFFS ? STAGES : 1][NTH];
-    __shared__ uint32_t rs_l[BM], csum_l[BN];
+    constexpr int LAB = CH / GTH, LPT = LAB + (OFFS ? 1 : 0);
+    static_assert(LAB * GTH == CH && CH_A % 64 == 0, "whole, wave-uniform loads");
+    static_assert(BN <= GTH, "one column-sum dword per thread of a group");
+    __shared__ i4 Stg[KG][STAGES][CH];
+    __shared__ uint32_t cs_ring[OFFS ? KG : 1][OFFS ? STAGES : 1][GTH];
+    __shared__ uint32_t rs_l[BM], csum_l[KG][BN];
+    __shared__ uint32_t gbar[KG];
 
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, l32 = lane & 31, hh = lane >> 5;
-    const int kg = wave / GW, wl = wave % GW;
+    const int tid = threadIdx.x, lane = tid & 63, l32 = lane & 31, hh = lane >> 5;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);   // uniform: loop bounds and bases stay scalar
+    const int kg = wave / GW, wl = wave % GW, tg = tid % GTH;
     const int wm = wl / WGN, wn = wl % WGN;
     const int tiles_m = (p.M + BM - 1) / BM;
     int pid = blockIdx.x;
@@ -780,12 +785,12 @@ __global__ __launch_bounds__(64 * WAVES) void k_gemm_i8nt(const GemmParams p) {
     // planes: A8 [batch][P][Mp][Kp] (sA = P*Mp*Kp, lda = Kp, plane_a = Mp*Kp), B8T likewise
     const char* a_panel = (const char*)p.A + b * p.sA + (int64_t)m0 * p.lda + kt0 * BK;
     const char* b_panel = (const char*)p.B + b * p.sB + (int64_t)n0 * p.ldb + kt0 * BK;
-    const unsigned wave_u = __builtin_amdgcn_readfirstlane(wave);
-    // load k of this wave covers stage chunks (wave + WAVES*k)*64 + lane
+    const unsigned wave_u = (unsigned)wave, wl_u = (unsigned)wl, kg_u = (unsigned)kg;
+    // load k of this wave covers stage chunks (wl + GW*k)*64 + lane
     unsigned ol[LAB];
 #pragma unroll
     for (int k = 0; k < LAB; ++k) {
-        const int q = (wave + WAVES * k) * 64 + lane;
+        const int q = (wl + GW * k) * 64 + lane;
         if (q < CH_A) {
             const int plane = q / (BM * KCH), rem = q % (BM * KCH), row = rem / KCH, pc = rem % KCH;
             ol[k] = (unsigned)((int64_t)plane * p.plane_a + row * p.lda + (pc ^ swz_i8(row)) * 16);
@@ -795,27 +800,46 @@ __global__ __launch_bounds__(64 * WAVES) void k_gemm_i8nt(const GemmParams p) {
             ol[k] = (unsigned)((int64_t)plane * p.plane_b + row * p.ldb + (pc ^ swz_i8(row)) * 16);
         }
     }
-    const unsigned lds_s0 = (unsigned)(uintptr_t)&Stg[0][0];
+    const unsigned lds_s0 = (unsigned)(uintptr_t)&Stg[0][0][0] + kg_u * (unsigned)(STAGES * CH * 16);
     // column sums [batch][K/64][N]: this thread's column, clamped into N
     // (columns past N are never stored)
     const int32_t* csg = OFFS ? p.colsum + ((int64_t)b * p.cs_slices + kt0) * p.N : nullptr;
-    const unsigned cs_off = (unsigned)min(n0 + tid, p.N - 1) * 4u;
-    const unsigned lds_cs0 = (unsigned)(uintptr_t)&cs_ring[0][0] + wave_u * 256;
-    auto issue = [&](int t) {
-        const int s = t % STAGES;
+    const unsigned cs_off = (unsigned)min(n0 + tg, p.N - 1) * 4u;
+    const unsigned lds_cs0 = (unsigned)(uintptr_t)&cs_ring[0][0][0] + (OFFS ? kg_u * (STAGES * GTH * 4) : 0u) + wl_u * 256;
+    // this group's local tile u is K tile KG*u + kg, in slot u % STAGES
+    auto issue = [&](int u) {
+        const int s = u % STAGES, t = KG * u + (int)kg_u;
         const char* ab = a_panel + t * BK;
         const char* bb = b_panel + t * BK;
         const unsigned ls = lds_s0 + (unsigned)(s * CH * 16);
 #pragma unroll
         for (int k = 0; k < LAB; ++k) {
-            const unsigned blk = wave_u + WAVES * k;
+            const unsigned blk = wl_u + GW * k;
             const char* base = (int)blk * 64 < CH_A ? ab : bb;
             asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dwordx4 %0, %1"
                          :: "v"(ol[k]), "s"(base), "s"(ls + blk * 1024) : "memory", "m0");
         }
         if constexpr (OFFS)
             asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dword %0, %1"
-                         :: "v"(cs_off), "s"(csg + (int64_t)t * p.N), "s"(lds_cs0 + s * NTH * 4) : "memory", "m0");
+                         :: "v"(cs_off), "s"(csg + (int64_t)t * p.N), "s"(lds_cs0 + s * GTH * 4) : "memory", "m0");
+    };
+    // barrier of this group's waves: all of them have waited for their part
+    // of the current tile and have finished reading the slot about to be
+    // refilled.  KG = 2: a counter in LDS (the group's waves are resident
+    // together, so the wait ends); the data a wave's loads put in LDS has
+    // landed before its vmcnt wait ends, hence before its increment
+    uint32_t gen = 0;
+    auto group_barrier = [&]() {
+        if constexpr (KG == 1) {
+            __syncthreads();
+        } else {
+            gen += GW;
+            __builtin_amdgcn_s_waitcnt(0xC07F);          // lgkmcnt(0): this wave's LDS reads are done
+            if (lane == 0) __hip_atomic_fetch_add(&gbar[kg], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+            while (__hip_atomic_load(&gbar[kg], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP) < gen)
+                __builtin_amdgcn_s_sleep(1);
+            asm volatile("" ::: "memory");
+        }
     };
 
     i16x acc[G][TM][TN];
@@ -838,27 +862,23 @@ __global__ __launch_bounds__(64 * WAVES) void k_gemm_i8nt(const GemmParams p) {
                          :: "v"(off), "s"(rsg), "s"(lds) : "memory", "m0");
         }
     }
-    uint32_t csum_acc = 0;   // this thread's column sum over the K tiles seen
+    if (KG > 1 && tid < KG) gbar[tid] = 0;
+    if constexpr (KG > 1) __syncthreads();
+    uint32_t csum_acc = 0;   // this thread's column sum over its group's K tiles
+    const int nloc = (ktiles - kg + KG - 1) / KG;   // this group's K tiles
 #pragma unroll
-    for (int s = 0; s < STAGES - KG; ++s)
-        if (s < ktiles) issue(s);
-    for (int t = 0; t < ktiles; t += KG) {
-        // tiles t .. t+KG-1 must have landed; up to STAGES-2KG after them
-        // may still be in flight (and the sums, issued before tile 0, have
-        // landed with them)
-        const int last = min(t + KG, ktiles) - 1;
-        wait_tiles<LPT>(min(STAGES - 2 * KG, ktiles - 1 - last));
-        __syncthreads();
-        if (OFFS && tid < BN)
-            for (int u = t; u <= last; ++u) csum_acc += cs_ring[u % STAGES][tid];   // before refills
-        // the slots of the previous KG tiles are free: every wave is past
-        // the barrier, so done with them
-#pragma unroll
-        for (int u = 0; u < KG; ++u)
-            if (t + STAGES - KG + u < ktiles) issue(t + STAGES - KG + u);
-        const int tt = t + kg;               // this wave group's tile
-        if (tt >= ktiles) continue;
-        const int s = tt % STAGES;
+    for (int u = 0; u < STAGES - 1; ++u)
+        if (u < nloc) issue(u);
+    for (int u = 0; u < nloc; ++u) {
+        // local tile u must have landed; the ones after it may still be in
+        // flight (and the sums, issued before tile 0, have landed with it)
+        wait_tiles<LPT>(min(STAGES - 2, nloc - 1 - u));
+        group_barrier();
+        const int s = u % STAGES;
+        if (OFFS && tg < BN) csum_acc += cs_ring[OFFS ? kg : 0][s][tg];   // before the slot is refilled
+        // the slot of local tile u-1 is free: every wave of the group is
+        // past the barrier, so done with it
+        if (u + STAGES - 1 < nloc) issue(u + STAGES - 1);
 #pragma unroll
         for (int ks = 0; ks < BK / 32; ++ks) {
             const int c = ks * 2 + hh;
@@ -868,12 +888,12 @@ __global__ __launch_bounds__(64 * WAVES) void k_gemm_i8nt(const GemmParams p) {
 #pragma unroll
                 for (int i = 0; i < TM; ++i) {
                     const int row = wm * WM + i * 32 + l32;
-                    a[q][i] = Stg[s][(q * BM + row) * KCH + (c ^ swz_i8(row))];
+                    a[q][i] = Stg[kg][s][(q * BM + row) * KCH + (c ^ swz_i8(row))];
                 }
 #pragma unroll
                 for (int j = 0; j < TN; ++j) {
                     const int col = wn * WN + j * 32 + l32;
-                    bv[q][j] = Stg[s][CH_A + (q * BN + col) * KCH + (c ^ swz_i8(col))];
+                    bv[q][j] = Stg[kg][s][CH_A + (q * BN + col) * KCH + (c ^ swz_i8(col))];
                 }
             }
 #pragma unroll
@@ -901,10 +921,11 @@ __global__ __launch_bounds__(64 * WAVES) void k_gemm_i8nt(const GemmParams p) {
                 for (int q = 0; q < G; ++q) gv[q] = (uint32_t)acc[q][i][j][r];
                 vs[i][j][r] = S::combine(gv);
             }
+    if (OFFS && tg < BN) csum_l[kg][tg] = csum_acc;
     if constexpr (KG == 2) {
         // group 1 hands its sums to group 0 through the (drained) stage ring
         static_assert(GW * TM * TN * 16 * 64 * 4 <= (int)sizeof(Stg), "exchange fits the ring");
-        uint32_t* xch = (uint32_t*)&Stg[0][0] + wl * (TM * TN * 16 * 64);
+        uint32_t* xch = (uint32_t*)&Stg[0][0][0] + wl * (TM * TN * 16 * 64);
         __syncthreads();
         if (kg == 1) {
 #pragma unroll
@@ -914,7 +935,6 @@ __global__ __launch_bounds__(64 * WAVES) void k_gemm_i8nt(const GemmParams p) {
 #pragma unroll
                     for (int r = 0; r < 16; ++r) xch[((i * TN + j) * 16 + r) * 64 + lane] = vs[i][j][r];
         }
-        if (OFFS && tid < BN) csum_l[tid] = csum_acc;
         __syncthreads();
         if (kg == 1) return;
 #pragma unroll
@@ -924,7 +944,6 @@ __global__ __launch_bounds__(64 * WAVES) void k_gemm_i8nt(const GemmParams p) {
 #pragma unroll
                 for (int r = 0; r < 16; ++r) vs[i][j][r] += xch[((i * TN + j) * 16 + r) * 64 + lane];
     } else if (OFFS) {
-        if (tid < BN) csum_l[tid] = csum_acc;
         __syncthreads();
     }
     int32_t* C = (int32_t*)p.C + b * p.sC;
@@ -934,7 +953,8 @@ __global__ __launch_bounds__(64 * WAVES) void k_gemm_i8nt(const GemmParams p) {
     for (int j = 0; j < TN; ++j) {
         const int gn = n0 + wn * WN + j * 32 + l32;
         if (gn >= p.N) continue;
-        const uint32_t ccol = OFFS ? cc * csum_l[wn * WN + j * 32 + l32] : 0u;
+        const uint32_t ccol = OFFS ? cc * (KG == 2 ? csum_l[0][wn * WN + j * 32 + l32] + csum_l[KG - 1][wn * WN + j * 32 + l32]
+                                               : csum_l[0][wn * WN + j * 32 + l32]) : 0u;
 #pragma unroll
         for (int i = 0; i < TM; ++i)
 #pragma unroll
@@ -1170,7 +1190,7 @@ bool build_gemm_i8nt(int32_t route, const GemmParams& p0, int batch, LaunchRec* 
     const bool deep = (int64_t)((p0.M + 63) / 64) * ((p0.N + 63) / 64) * batch * std::max(p0.ksplit, 1) <= 256;
 #define QX_NT(S, NAME)                                                                               \
     if (big) fill_gemm_rec(rec, k_gemm_i8nt<S, 128, 128, 3, 8>, p0, 128, 128, batch, "gemm_i8nt_" NAME "_128x128"); \
-    else if (deep) fill_gemm_rec(rec, k_gemm_i8nt<S, 64, 64, 6, 8, 2>, p0, 64, 64, batch, "gemm_i8nt_" NAME "_64x64"); \
+    else if (deep) fill_gemm_rec(rec, k_gemm_i8nt<S, 64, 64, 3, 8, 2>, p0, 64, 64, batch, "gemm_i8nt_" NAME "_64x64"); \
     else fill_gemm_rec(rec, k_gemm_i8nt<S, 64, 64, 3, 4>, p0, 64, 64, batch, "gemm_i8nt_" NAME "_64x64_3");
     switch (route) {
     case R_I8_DIRECT: QX_NT(SchemeDirect, "direct") break;
