@@ -73,7 +73,7 @@ __device__ __forceinline__ void store_c(const GemmParams& p, int32_t* C, int gm,
 __device__ __forceinline__ int swz_a(int row, int c) { return c ^ (row & 7); }
 __device__ __forceinline__ int swz_b(int col, int c) { return c ^ ((col ^ (col >> 3)) & 7); }
 
-template <int BM, int BN, int BK, int WM, int WN, bool ALIGNED, bool FLUSH_STEP>
+template <int BM, int BN, int BK, int WM, int WN, bool ALIGNED, bool FLUSH_STEP, bool ALLK = false>
 __global__ __launch_bounds__(NT) void k_gemm_f16x(const GemmParams p) {
     static_assert(BK == 64, "chunk swizzle assumes 8 chunks per row");
     constexpr int KCH = BK / 8;
@@ -103,7 +103,7 @@ __global__ __launch_bounds__(NT) void k_gemm_f16x(const GemmParams p) {
     s8 rb[4];
     const int bkb = tid / B_NBLK, bnb = tid % B_NBLK;
 
-    auto load = [&](int k0) {
+    auto load_to = [&](int k0, s8 (&ra)[A_VECS], s8 (&rb)[4]) {
 #pragma unroll
         for (int i = 0; i < A_VECS; ++i) {
             const int v = tid + NT * i, row = v / KCH, c = v % KCH;
@@ -129,7 +129,8 @@ __global__ __launch_bounds__(NT) void k_gemm_f16x(const GemmParams p) {
             }
         }
     };
-    auto stash = [&](int buf) {
+    auto load = [&](int k0) { load_to(k0, ra, rb); };
+    auto stash_from = [&](int buf, const s8 (&ra)[A_VECS], const s8 (&rb)[4]) {
 #pragma unroll
         for (int i = 0; i < A_VECS; ++i) {
             const int v = tid + NT * i, row = v / KCH, c = v % KCH;
@@ -159,6 +160,7 @@ __global__ __launch_bounds__(NT) void k_gemm_f16x(const GemmParams p) {
             acc[i][j] = f16x{};
             iacc[i][j] = u16x{};
         }
+    auto stash = [&](int buf) { stash_from(buf, ra, rb); };
     auto flush = [&]() {
 #pragma unroll
         for (int i = 0; i < TM; ++i)
@@ -171,13 +173,10 @@ __global__ __launch_bounds__(NT) void k_gemm_f16x(const GemmParams p) {
     };
 
     const int ktiles = (p.K + BK - 1) / BK;
-    load(0);
-    stash(0);
-    __syncthreads();
-    int since_flush = 0;
-    for (int t = 0; t < ktiles; ++t) {
-        const int buf = t & 1;
-        if (t + 1 < ktiles) load((t + 1) * BK);
+    // The MFMA steps of one staged K tile.  With FLUSH_STEP each step's
+    // product block is a whole chunk (16 k): it starts from zero and is
+    // converted and added on its own.
+    auto compute = [&](int buf) {
 #pragma unroll
         for (int ks = 0; ks < BK / 16; ++ks) {
             h8 a[TM], bv[TN];
@@ -195,16 +194,55 @@ __global__ __launch_bounds__(NT) void k_gemm_f16x(const GemmParams p) {
 #pragma unroll
             for (int i = 0; i < TM; ++i)
 #pragma unroll
-                for (int j = 0; j < TN; ++j)
-                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_f16(a[i], bv[j], acc[i][j], 0, 0, 0);
-            if (FLUSH_STEP) flush();
+                for (int j = 0; j < TN; ++j) {
+                    if (FLUSH_STEP) {
+                        const f16x r = __builtin_amdgcn_mfma_f32_32x32x16_f16(a[i], bv[j], f16x{}, 0, 0, 0);
+#pragma unroll
+                        for (int e = 0; e < 16; ++e) iacc[i][j][e] += (uint32_t)(int32_t)r[e];
+                    } else {
+                        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_f16(a[i], bv[j], acc[i][j], 0, 0, 0);
+                    }
+                }
         }
-        if (!FLUSH_STEP && ++since_flush == p.chunk_tiles) {
-            flush();
-            since_flush = 0;
-        }
-        if (t + 1 < ktiles) stash(buf ^ 1);
+    };
+    int since_flush = 0;
+    if constexpr (ALLK) {
+        // K of at most four tiles (the builder checks): every tile's loads
+        // are issued up front, so the workgroup waits on memory once
+        // instead of once per tile.
+        s8 xa[4][A_VECS], xb[4][4];
+#pragma unroll
+        for (int t = 0; t < 4; ++t)
+            if (t < ktiles) load_to(t * BK, xa[t], xb[t]);
+        stash_from(0, xa[0], xb[0]);
         __syncthreads();
+#pragma unroll
+        for (int t = 0; t < 4; ++t) {
+            if (t < ktiles) {
+                compute(t & 1);
+                if (!FLUSH_STEP && ++since_flush == p.chunk_tiles) {
+                    flush();
+                    since_flush = 0;
+                }
+                if (t + 1 < 4 && t + 1 < ktiles) stash_from((t + 1) & 1, xa[t + 1], xb[t + 1]);
+                __syncthreads();
+            }
+        }
+    } else {
+        load(0);
+        stash(0);
+        __syncthreads();
+        for (int t = 0; t < ktiles; ++t) {
+            const int buf = t & 1;
+            if (t + 1 < ktiles) load((t + 1) * BK);
+            compute(buf);
+            if (!FLUSH_STEP && ++since_flush == p.chunk_tiles) {
+                flush();
+                since_flush = 0;
+            }
+            if (t + 1 < ktiles) stash(buf ^ 1);
+            __syncthreads();
+        }
     }
     if (!FLUSH_STEP) flush();
 
@@ -1106,6 +1144,15 @@ bool build_gemm_mfma(int32_t route, const GemmParams& p, int batch, LaunchRec* r
         if (tiles128 < 64) {
             *tile_m = 64;
             *tile_n = 64;
+            // K within four tiles: all of it loaded up front (the 64 x 64
+            // tile's registers hold four tiles of operands)
+            if (p.K <= 4 * 64) {
+                if (al && !step) fill_gemm_rec(rec, k_gemm_f16x<64, 64, 64, 32, 32, true, false, true>, p, 64, 64, batch, "gemm_f16x_64_k4");
+                else if (al) fill_gemm_rec(rec, k_gemm_f16x<64, 64, 64, 32, 32, true, true, true>, p, 64, 64, batch, "gemm_f16x_step_64_k4");
+                else if (!step) fill_gemm_rec(rec, k_gemm_f16x<64, 64, 64, 32, 32, false, false, true>, p, 64, 64, batch, "gemm_f16x_u_64_k4");
+                else fill_gemm_rec(rec, k_gemm_f16x<64, 64, 64, 32, 32, false, true, true>, p, 64, 64, batch, "gemm_f16x_step_u_64_k4");
+                return true;
+            }
             if (al && !step) fill_gemm_rec(rec, k_gemm_f16x<64, 64, 64, 32, 32, true, false>, p, 64, 64, batch, "gemm_f16x_64");
             else if (al) fill_gemm_rec(rec, k_gemm_f16x<64, 64, 64, 32, 32, true, true>, p, 64, 64, batch, "gemm_f16x_step_64");
             else if (!step) fill_gemm_rec(rec, k_gemm_f16x<64, 64, 64, 32, 32, false, false>, p, 64, 64, batch, "gemm_f16x_u_64");
