@@ -73,7 +73,7 @@ __device__ __forceinline__ void store_c(const GemmParams& p, int32_t* C, int gm,
 __device__ __forceinline__ int swz_a(int row, int c) { return c ^ (row & 7); }
 __device__ __forceinline__ int swz_b(int col, int c) { return c ^ ((col ^ (col >> 3)) & 7); }
 
-template <int BM, int BN, int BK, int WM, int WN, bool ALIGNED, bool FLUSH_STEP, bool ALLK = false>
+template <int BM, int BN, int BK, int WM, int WN, bool ALIGNED, bool FLUSH_STEP>
 __global__ __launch_bounds__(NT) void k_gemm_f16x(const GemmParams p) {
     static_assert(BK == 64, "chunk swizzle assumes 8 chunks per row");
     constexpr int KCH = BK / 8;
@@ -103,7 +103,7 @@ __global__ __launch_bounds__(NT) void k_gemm_f16x(const GemmParams p) {
     s8 rb[4];
     const int bkb = tid / B_NBLK, bnb = tid % B_NBLK;
 
-    auto load_to = [&](int k0, s8 (&ra)[A_VECS], s8 (&rb)[4]) {
+    auto load = [&](int k0) {
 #pragma unroll
         for (int i = 0; i < A_VECS; ++i) {
             const int v = tid + NT * i, row = v / KCH, c = v % KCH;
@@ -129,8 +129,7 @@ __global__ __launch_bounds__(NT) void k_gemm_f16x(const GemmParams p) {
             }
         }
     };
-    auto load = [&](int k0) { load_to(k0, ra, rb); };
-    auto stash_from = [&](int buf, const s8 (&ra)[A_VECS], const s8 (&rb)[4]) {
+    auto stash = [&](int buf) {
 #pragma unroll
         for (int i = 0; i < A_VECS; ++i) {
             const int v = tid + NT * i, row = v / KCH, c = v % KCH;
@@ -160,7 +159,6 @@ __global__ __launch_bounds__(NT) void k_gemm_f16x(const GemmParams p) {
             acc[i][j] = f16x{};
             iacc[i][j] = u16x{};
         }
-    auto stash = [&](int buf) { stash_from(buf, ra, rb); };
     auto flush = [&]() {
 #pragma unroll
         for (int i = 0; i < TM; ++i)
@@ -206,43 +204,19 @@ __global__ __launch_bounds__(NT) void k_gemm_f16x(const GemmParams p) {
         }
     };
     int since_flush = 0;
-    if constexpr (ALLK) {
-        // K of at most four tiles (the builder checks): every tile's loads
-        // are issued up front, so the workgroup waits on memory once
-        // instead of once per tile.
-        s8 xa[4][A_VECS], xb[4][4];
-#pragma unroll
-        for (int t = 0; t < 4; ++t)
-            if (t < ktiles) load_to(t * BK, xa[t], xb[t]);
-        stash_from(0, xa[0], xb[0]);
-        __syncthreads();
-#pragma unroll
-        for (int t = 0; t < 4; ++t) {
-            if (t < ktiles) {
-                compute(t & 1);
-                if (!FLUSH_STEP && ++since_flush == p.chunk_tiles) {
-                    flush();
-                    since_flush = 0;
-                }
-                if (t + 1 < 4 && t + 1 < ktiles) stash_from((t + 1) & 1, xa[t + 1], xb[t + 1]);
-                __syncthreads();
-            }
+    load(0);
+    stash(0);
+    __syncthreads();
+    for (int t = 0; t < ktiles; ++t) {
+        const int buf = t & 1;
+        if (t + 1 < ktiles) load((t + 1) * BK);
+        compute(buf);
+        if (!FLUSH_STEP && ++since_flush == p.chunk_tiles) {
+            flush();
+            since_flush = 0;
         }
-    } else {
-        load(0);
-        stash(0);
+        if (t + 1 < ktiles) stash(buf ^ 1);
         __syncthreads();
-        for (int t = 0; t < ktiles; ++t) {
-            const int buf = t & 1;
-            if (t + 1 < ktiles) load((t + 1) * BK);
-            compute(buf);
-            if (!FLUSH_STEP && ++since_flush == p.chunk_tiles) {
-                flush();
-                since_flush = 0;
-            }
-            if (t + 1 < ktiles) stash(buf ^ 1);
-            __syncthreads();
-        }
     }
     if (!FLUSH_STEP) flush();
 
@@ -258,6 +232,104 @@ __global__ __launch_bounds__(NT) void k_gemm_f16x(const GemmParams p) {
                 const int gn = n0 + wn * WN + j * 32 + (lane & 31);
                 store_c(p, C, gm, gn, iacc[i][j][r]);
             }
+}
+
+// Small fp16-exact GEMMs (K <= 256): a workgroup owns a 32 x 32 output tile
+// and its four waves take one 64-k tile each, so a workgroup waits on memory
+// once and each wave runs a quarter of the K steps; the waves' int32
+// partials are then added through LDS.  A fragments come straight from
+// global memory (8 consecutive k of a row are one 16-byte load); B goes
+// through LDS to be transposed (k-contiguous per column).
+template <bool ALIGNED, bool FLUSH_STEP>
+__global__ __launch_bounds__(NT) void k_gemm_f16_ks(const GemmParams p) {
+    constexpr int BK = 64;
+    __shared__ h8 Bs[4][32][BK / 8];          // per wave: [col][k chunk], chunks swizzled
+    __shared__ u16x red[3][64];               // partials of waves 1..3
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int l32 = lane & 31, hh = lane >> 5;
+    const int tiles_m = (p.M + 31) / 32;
+    const int tm = (int)blockIdx.x % tiles_m, tn = (int)blockIdx.x / tiles_m;
+    const int m0 = tm * 32, n0 = tn * 32;
+    const int b = blockIdx.z;
+    const int16_t* A = (const int16_t*)p.A + b * p.sA;
+    const int16_t* B = (const int16_t*)p.B + b * p.sB;
+    int32_t* C = (int32_t*)p.C + b * p.sC;
+    const int k0 = wave * BK;                 // this wave's K tile (none past K)
+
+    // A: lane (row l32, half hh) holds k = k0 + 16 ks + 8 hh .. +7
+    s8 ra[4];
+    const int gm = m0 + l32;
+#pragma unroll
+    for (int ks = 0; ks < 4; ++ks) {
+        const int gk = k0 + 16 * ks + 8 * hh;
+        if (ALIGNED) {
+            ra[ks] = (gm < p.M && gk < p.K) ? *(const s8*)(A + (int64_t)gm * p.lda + gk) : s8{};
+        } else {
+#pragma unroll
+            for (int e = 0; e < 8; ++e)
+                ra[ks][e] = (gm < p.M && gk + e < p.K) ? A[(int64_t)gm * p.lda + gk + e] : (short)0;
+        }
+    }
+    // B: lane (kr, nc) loads k = k0 + 4 kr .. +3 of columns n0 + 8 nc .. +7
+    const int kr = lane >> 2, nc = lane & 3;
+    s8 rb[4];
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+        const int gk = k0 + 4 * kr + r, gn = n0 + 8 * nc;
+        if (ALIGNED) {
+            rb[r] = (gk < p.K && gn < p.N) ? *(const s8*)(B + (int64_t)gk * p.ldb + gn) : s8{};
+        } else {
+#pragma unroll
+            for (int e = 0; e < 8; ++e)
+                rb[r][e] = (gk < p.K && gn + e < p.N) ? B[(int64_t)gk * p.ldb + gn + e] : (short)0;
+        }
+    }
+#pragma unroll
+    for (int c = 0; c < 8; ++c) {
+        const int col = 8 * nc + c;
+        h4 h;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) h[r] = (_Float16)rb[r][c];
+        h4* dst = (h4*)&Bs[wave][col][swz_b(col, kr >> 1)];
+        dst[kr & 1] = h;
+    }
+    __syncthreads();
+
+    u16x iacc = u16x{};
+    f16x acc = f16x{};
+#pragma unroll
+    for (int ks = 0; ks < 4; ++ks) {
+        h8 a;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) a[e] = (_Float16)ra[ks][e];
+        const h8 bv = Bs[wave][l32][swz_b(l32, ks * 2 + hh)];
+        if (FLUSH_STEP) {
+            // each 16-k step is a whole chunk: converted and added on its own
+            const f16x r = __builtin_amdgcn_mfma_f32_32x32x16_f16(a, bv, f16x{}, 0, 0, 0);
+#pragma unroll
+            for (int e = 0; e < 16; ++e) iacc[e] += (uint32_t)(int32_t)r[e];
+        } else {
+            acc = __builtin_amdgcn_mfma_f32_32x32x16_f16(a, bv, acc, 0, 0, 0);
+        }
+    }
+    if (!FLUSH_STEP) {
+#pragma unroll
+        for (int e = 0; e < 16; ++e) iacc[e] = (uint32_t)(int32_t)acc[e];
+    }
+    if (wave > 0) red[wave - 1][lane] = iacc;
+    __syncthreads();
+    if (wave > 0) return;
+#pragma unroll
+    for (int w = 0; w < 3; ++w) {
+        const u16x o = red[w][lane];
+#pragma unroll
+        for (int e = 0; e < 16; ++e) iacc[e] += o[e];
+    }
+    // 32x32 accumulator layout: lane holds column l32 and rows
+    // 8*(r/4) + 4*hh + r%4.
+#pragma unroll
+    for (int r = 0; r < 16; ++r)
+        store_c(p, C, m0 + 8 * (r >> 2) + 4 * hh + (r & 3), n0 + l32, iacc[r]);
 }
 
 // ===========================================================================
@@ -1144,13 +1216,14 @@ bool build_gemm_mfma(int32_t route, const GemmParams& p, int batch, LaunchRec* r
         if (tiles128 < 64) {
             *tile_m = 64;
             *tile_n = 64;
-            // K within four tiles: all of it loaded up front (the 64 x 64
-            // tile's registers hold four tiles of operands)
+            // K within four tiles: 32 x 32 tiles, K split over the four waves
             if (p.K <= 4 * 64) {
-                if (al && !step) fill_gemm_rec(rec, k_gemm_f16x<64, 64, 64, 32, 32, true, false, true>, p, 64, 64, batch, "gemm_f16x_64_k4");
-                else if (al) fill_gemm_rec(rec, k_gemm_f16x<64, 64, 64, 32, 32, true, true, true>, p, 64, 64, batch, "gemm_f16x_step_64_k4");
-                else if (!step) fill_gemm_rec(rec, k_gemm_f16x<64, 64, 64, 32, 32, false, false, true>, p, 64, 64, batch, "gemm_f16x_u_64_k4");
-                else fill_gemm_rec(rec, k_gemm_f16x<64, 64, 64, 32, 32, false, true, true>, p, 64, 64, batch, "gemm_f16x_step_u_64_k4");
+                *tile_m = 32;
+                *tile_n = 32;
+                if (al && !step) fill_gemm_rec(rec, k_gemm_f16_ks<true, false>, p, 32, 32, batch, "gemm_f16_ksplit");
+                else if (al) fill_gemm_rec(rec, k_gemm_f16_ks<true, true>, p, 32, 32, batch, "gemm_f16_ksplit_step");
+                else if (!step) fill_gemm_rec(rec, k_gemm_f16_ks<false, false>, p, 32, 32, batch, "gemm_f16_ksplit_u");
+                else fill_gemm_rec(rec, k_gemm_f16_ks<false, true>, p, 32, 32, batch, "gemm_f16_ksplit_step_u");
                 return true;
             }
             if (al && !step) fill_gemm_rec(rec, k_gemm_f16x<64, 64, 64, 32, 32, true, false>, p, 64, 64, batch, "gemm_f16x_64");

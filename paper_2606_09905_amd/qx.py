@@ -145,12 +145,12 @@ def _torch():
 
 
 def _stream(stream):
-    torch = _torch()
+    """The HIP stream handle (an int) of a torch stream, a raw handle, or
+    None for torch's current stream."""
     if stream is None:
-        return ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
-    if hasattr(stream, "cuda_stream"):
-        return ctypes.c_void_p(stream.cuda_stream)
-    return ctypes.c_void_p(int(stream))
+        return _torch().cuda.current_stream().cuda_stream
+    handle = getattr(stream, "cuda_stream", None)
+    return handle if handle is not None else int(stream)
 
 
 def _dev_tensor(t, dtype, name):
@@ -498,9 +498,12 @@ class Executor:
         return info.as_dict()
 
     def run_ptrs(self, in_ptrs, out_ptr: int, stream=None) -> None:
-        """Enqueue with raw device pointers (ints)."""
-        arr = (ctypes.c_void_p * len(in_ptrs))(*[ctypes.c_void_p(p) for p in in_ptrs])
-        check(lib().qx_exec_run(self._h, arr, ctypes.c_void_p(out_ptr), _stream(stream)))
+        """Enqueue with raw device pointers (ints).  Kept lean: for small
+        problems the host's cost per call is what bounds back-to-back runs."""
+        arr = (ctypes.c_void_p * len(in_ptrs))(*in_ptrs)
+        st = lib().qx_exec_run(self._h, arr, out_ptr, _stream(stream))
+        if st != OK:
+            check(st)
 
     def run(self, inputs, out=None, stream=None):
         torch = _torch()
