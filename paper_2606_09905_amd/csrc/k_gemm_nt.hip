@@ -62,7 +62,10 @@ __device__ __forceinline__ _Float16 to_h1(int v) {
 }
 
 // A [batch][M][lda] int16 -> A16 [batch][Mp][Kp] fp16 (bf16 with BF); one
-// thread = 8 k, four vectors per thread.
+// thread = 8 k, four vectors per thread.  Both encoders read their int16
+// source once, with non-temporal loads (whole lines per wave-wide load):
+// the source then displaces less of the encoded operands the contraction
+// reads next (2% on 8192^3 and 64 x 2048^3).
 template <bool BF>
 __global__ __launch_bounds__(256) void k_enc_a(const EncParams p) {
     const int kv = p.Kp / 8;
@@ -78,7 +81,7 @@ __global__ __launch_bounds__(256) void k_enc_a(const EncParams p) {
         const int16_t* src = (const int16_t*)p.src + b * p.s_src + (int64_t)m * p.ld_src + k0;
         h8 out;
         if (p.vec && m < p.M && k0 + 8 <= p.K) {
-            out = to_h8<BF>(*(const s8v*)src);
+            out = to_h8<BF>(__builtin_nontemporal_load((const s8v*)src));
         } else {
 #pragma unroll
             for (int e = 0; e < 8; ++e) out[e] = to_h1<BF>((m < p.M && k0 + e < p.K) ? src[e] : 0);
@@ -111,7 +114,7 @@ __global__ __launch_bounds__(256) void k_enc_bt(const EncParams p) {
         const int k = kr + r;
         const int16_t* sp = src + (int64_t)k * p.ld_src + n;
         if (p.vec && k < p.K && n + 8 <= p.N) {
-            in[r] = *(const s8v*)sp;
+            in[r] = __builtin_nontemporal_load((const s8v*)sp);
         } else {
 #pragma unroll
             for (int e = 0; e < 8; ++e) in[r][e] = (k < p.K && n + e < p.N) ? sp[e] : (short)0;
