@@ -20,7 +20,7 @@ extern "C" {
 
 /* on = 1: every later executor create (and one-shot call) uses a host-only
  * double of the device runtime: it reports one gfx950 device, gives
- * workspaces host memory, creates dummy streams and events, and for every
+ * workspaces host memory, creates dummy timing events, and for every
  * launch checks the grid against the hardware limits (x * block <= 2^32 - 1,
  * y, z <= 65535, 1..1024 threads per workgroup, <= 160 KiB of LDS) and that
  * every pointer slot of the parameter block is bound, instead of enqueueing
@@ -31,17 +31,16 @@ extern "C" {
 qx_status qx_testing_host_double(int32_t on);
 
 /* Counters since the library was loaded, both runtimes together:
- * out[0] workspace allocations, out[1] workspace frees, out[2] side streams
- * created, out[3] side streams destroyed, out[4] events created, out[5]
- * events destroyed, out[6] kernel launches enqueued (or checked, under the
- * double), out[7] live executor handles.  Writes min(n, 8) values.
+ * out[0] workspace allocations, out[1] workspace frees, out[2] timing events
+ * created (qx_exec_profile), out[3] timing events destroyed, out[4] kernel
+ * launches enqueued (or checked, under the double), out[5] live executor
+ * handles.  Writes min(n, 6) values.
  *
  * Fault injection: with the environment variable QX_TEST_FAIL_ALLOC=k
  * (read at every executor create), the k-th device resource that create
- * acquires -- side stream, then its events, then the workspace, counted
- * from 1 -- fails as if the device were out of memory: the create returns
- * QX_ERR_OUT_OF_MEMORY, *out is NULL, and everything acquired before it has
- * been released. */
+ * acquires (counted from 1; a create acquires at most one, its workspace)
+ * fails as if the device were out of memory: the create returns
+ * QX_ERR_OUT_OF_MEMORY, *out is NULL, and nothing stays allocated. */
 void qx_testing_counters(int64_t* out, int32_t n);
 
 #ifdef __cplusplus

@@ -75,7 +75,6 @@ struct Plan {
         int32_t bound;
     };
     std::vector<RangeCheck> checks;
-    int n_events = 0;        // cross-lane events used by the launches (0: one stream)
     int n_inputs = 0;
     uint64_t in_align = 16;  // required alignment of every input pointer
     uint64_t out_align = 4;  // required alignment of the output pointer
@@ -274,9 +273,13 @@ qx_status plan_int_gemm(const GemmSpec& s, Plan* pl, uint64_t* ws_used) {
         const uint64_t a_off = round_up(*ws_used, 256);
         const uint64_t b_off = round_up(a_off + 2 * (uint64_t)s.batch * Mp * Kp, 256);
         *ws_used = b_off + 2 * (uint64_t)s.batch * Np * Kp;
-        // Overlap: the operands of the next batch group are encoded on the
-        // side stream while the current group's contraction runs on the
-        // caller's stream.
+        // Batch groups: above 2^32 multiply-adds the batches run in up to 8
+        // groups, each encoded and then contracted, so that a group's
+        // encoded operands are still in the last-level cache when its
+        // contraction reads them.  Encoding the next group on a second
+        // stream while the current one contracts measured 4% slower on
+        // 64 x 2048^3 (the encoders then take CUs between the contraction's
+        // workgroups).
         const double macs = (double)s.M * (double)s.N * (double)s.K * (double)s.batch;
         int64_t groups = 1;
         if (s.batch >= 2 && macs >= (double)(1LL << 32)) {
@@ -285,9 +288,6 @@ qx_status plan_int_gemm(const GemmSpec& s, Plan* pl, uint64_t* ws_used) {
             groups = (s.batch + per - 1) / per;
         }
         const int64_t per_group = (s.batch + groups - 1) / groups;
-        const bool lanes = groups > 1;
-        std::vector<LaunchRec> side, main;
-        int ev = 0;
         auto enc_a = [&](int64_t b0, int64_t cnt) {
             EncParams ea{};
             ea.s_src = s.sA; ea.s_dst = Mp * Kp;
@@ -300,7 +300,6 @@ qx_status plan_int_gemm(const GemmSpec& s, Plan* pl, uint64_t* ws_used) {
             build_enc_a(ea, &r);
             r.bind(offsetof(EncParams, src), s.a_bind, 2 * (uint64_t)(b0 * s.sA));
             r.bind(offsetof(EncParams, dst), BIND_WS, a_off + 2 * (uint64_t)(b0 * Mp * Kp));
-            r.lane = lanes ? 1 : 0;
             return r;
         };
         // encode B^T columns [n0, n0 + nw) of batches [b0, b0 + cnt), then contract them
@@ -330,11 +329,6 @@ qx_status plan_int_gemm(const GemmSpec& s, Plan* pl, uint64_t* ws_used) {
             r3.bind(offsetof(GemmParams, A), BIND_WS, a_off + 2 * (uint64_t)(b0 * Mp * Kp));
             r3.bind(offsetof(GemmParams, B), BIND_WS, bt_add);
             r3.bind(offsetof(GemmParams, C), BIND_OUT, 4 * (uint64_t)(b0 * s.sC + n0));
-            if (lanes) {
-                r2.lane = 1;
-                r2.rec_ev = (int16_t)++ev;
-                r3.wait_ev = (int16_t)ev;
-            }
             pl->launches.push_back(r2);
             pl->launches.push_back(r3);
         };
@@ -343,7 +337,6 @@ qx_status plan_int_gemm(const GemmSpec& s, Plan* pl, uint64_t* ws_used) {
             pl->launches.push_back(enc_a(b0, cnt));
             enc_b_and_gemm(b0, cnt, 0, s.N);
         }
-        pl->n_events = ev;
         info.chunk = (int32_t)(chunk / 64 * 64);
         info.tile_m = bm; info.tile_n = bn; info.tile_k = 64;
         return QX_OK;
@@ -544,7 +537,6 @@ qx_status plan_gemm(Plan* pl, bool s24, int64_t M, int64_t N, int64_t K, int64_t
         return QX_OK;
     }
     pl->launches = scratch.launches;
-    pl->n_events = scratch.n_events;
     if (!s24) {
         if (ba < 32768) pl->checks.push_back({0, 2, M * K * batch, (int32_t)ba});
         if (bb < 32768) pl->checks.push_back({1, 2, K * N * batch, (int32_t)bb});
@@ -880,7 +872,6 @@ qx_status plan_conv_t(Plan* pl, int32_t dt, int64_t N, int64_t Ci, int64_t H, in
         pl->launches.push_back(rec);
     }
     for (auto& r : g.launches) pl->launches.push_back(r);
-    pl->n_events = g.n_events;
     pl->info.kernels = (int32_t)pl->launches.size();
     pl->info.workspace_bytes = (int64_t)ws;
     return QX_OK;
@@ -1011,7 +1002,6 @@ qx_status plan_lenet(Plan* pl, int64_t B) {
     const uint64_t o_p1 = take(4 * (uint64_t)B * 6 * 14 * 14), o_p2 = take(4 * (uint64_t)B * 400);
     const uint64_t o_h1 = take(4 * (uint64_t)B * 120), o_h2 = take(4 * (uint64_t)B * 84);
     auto sub = [&](Plan& sp, std::initializer_list<Target> ins, Target out) -> qx_status {
-        if (sp.n_events) return fail(QX_ERR_UNSUPPORTED, "chained plans must use one stream");
         append_plan(pl, sp, take((uint64_t)sp.info.workspace_bytes), ins, out);
         return QX_OK;
     };
@@ -1360,7 +1350,7 @@ qx_status plan_sdpa(Plan* pl, int64_t BH, int64_t L, int64_t d, float scale, int
 // ---------------------------------------------------------------------------
 // Device runtime calls of the executor
 //
-// Every HIP call the executor makes (device query, workspace, side stream,
+// Every HIP call the executor makes (device query, workspace, timing
 // events, launches, the validation read-back) goes through one table.  The
 // default table is the HIP runtime.  A host-only test double (switched on by
 // qx_testing_host_double, for tests of the executor's bookkeeping on machines
@@ -1380,14 +1370,11 @@ struct RtTable {
     hipError_t (*free)(void*);
     hipError_t (*clear_sync)(void*, size_t);    // zero, then wait for the device
     hipError_t (*device_sync)();
-    hipError_t (*stream_create)(hipStream_t*);
-    hipError_t (*stream_destroy)(hipStream_t);
     hipError_t (*stream_sync)(hipStream_t);
     hipError_t (*event_create)(hipEvent_t*, bool timing);
     hipError_t (*event_destroy)(hipEvent_t);
     hipError_t (*event_record)(hipEvent_t, hipStream_t);
     hipError_t (*event_elapsed)(float*, hipEvent_t, hipEvent_t);
-    hipError_t (*stream_wait)(hipStream_t, hipEvent_t);
     hipError_t (*launch)(const LaunchRec&, void**, hipStream_t);
     hipError_t (*read_async)(void*, const void*, size_t, hipStream_t);
 };
@@ -1411,8 +1398,6 @@ const RtTable kHip = {
         return e == hipSuccess ? hipDeviceSynchronize() : e;
     },
     []() { return hipDeviceSynchronize(); },
-    [](hipStream_t* s) { return hipStreamCreateWithFlags(s, hipStreamNonBlocking); },
-    [](hipStream_t s) { return hipStreamDestroy(s); },
     [](hipStream_t s) { return hipStreamSynchronize(s); },
     [](hipEvent_t* ev, bool timing) {
         return timing ? hipEventCreate(ev) : hipEventCreateWithFlags(ev, hipEventDisableTiming);
@@ -1420,7 +1405,6 @@ const RtTable kHip = {
     [](hipEvent_t ev) { return hipEventDestroy(ev); },
     [](hipEvent_t ev, hipStream_t s) { return hipEventRecord(ev, s); },
     [](float* ms, hipEvent_t a, hipEvent_t b) { return hipEventElapsedTime(ms, a, b); },
-    [](hipStream_t s, hipEvent_t ev) { return hipStreamWaitEvent(s, ev, 0); },
     [](const LaunchRec& r, void** args, hipStream_t s) {
         return hipLaunchKernel(r.fn, r.grid, r.block, args, r.shmem, s);
     },
@@ -1469,14 +1453,11 @@ const RtTable kHostDouble = {
     [](void* p) { std::free(p); return hipSuccess; },
     [](void* p, size_t n) { memset(p, 0, n); return hipSuccess; },
     []() { return hipSuccess; },
-    [](hipStream_t* s) { return dbl_new((void**)s); },
-    [](hipStream_t s) { return dbl_delete((void*)s); },
     [](hipStream_t) { return hipSuccess; },
     [](hipEvent_t* ev, bool) { return dbl_new((void**)ev); },
     [](hipEvent_t ev) { return dbl_delete((void*)ev); },
     [](hipEvent_t ev, hipStream_t) { return ev ? hipSuccess : hipErrorInvalidHandle; },
     [](float* ms, hipEvent_t, hipEvent_t) { *ms = 0.0f; return hipSuccess; },
-    [](hipStream_t, hipEvent_t ev) { return ev ? hipSuccess : hipErrorInvalidHandle; },
     dbl_launch,
     [](void* dst, const void* src, size_t n, hipStream_t) { memcpy(dst, src, n); return hipSuccess; },
 };
@@ -1486,8 +1467,7 @@ std::atomic<const RtTable*> g_rt{&kHip};
 // Counters of every device resource the executor acquires and releases
 // (both tables), for the tests of "run allocates nothing" and of cleanup
 // after a failed create.
-enum Counter { C_ALLOCS, C_FREES, C_STREAMS, C_STREAMS_FREED, C_EVENTS, C_EVENTS_FREED, C_LAUNCHES, C_LIVE_HANDLES,
-               C_N };
+enum Counter { C_ALLOCS, C_FREES, C_EVENTS, C_EVENTS_FREED, C_LAUNCHES, C_LIVE_HANDLES, C_N };
 std::atomic<int64_t> g_count[C_N];
 
 }  // namespace
@@ -1499,11 +1479,6 @@ struct qx_exec_s {
     Plan plan;
     void* ws;
     uint64_t ws_bytes;
-    // side stream and events of plans that overlap launches (operand
-    // encoding of the next batch group or column panel with the current
-    // contraction): evs[0] = run start, evs[1..n] = plan events, last = join
-    hipStream_t side;
-    std::vector<hipEvent_t> evs;
     uint64_t flag_off;      // QX_VALIDATE flag word in the workspace
 };
 
@@ -1537,28 +1512,18 @@ hipError_t release_exec(qx_exec h) {
     const RtTable& rt = *h->rt;
     hipError_t first = hipSuccess;
     auto note = [&](hipError_t e) { if (first == hipSuccess && e != hipSuccess) first = e; };
-    if (h->ws || h->side) note(rt.device_sync());
     if (h->ws) {
+        note(rt.device_sync());
         note(rt.free(h->ws));
         g_count[C_FREES]++;
         h->ws = nullptr;
     }
-    for (hipEvent_t ev : h->evs) {
-        note(rt.event_destroy(ev));
-        g_count[C_EVENTS_FREED]++;
-    }
-    h->evs.clear();
-    if (h->side) {
-        note(rt.stream_destroy(h->side));
-        g_count[C_STREAMS_FREED]++;
-        h->side = nullptr;
-    }
     return first;
 }
 
-// QX_TEST_FAIL_ALLOC=k: the k-th device resource a create acquires (side
-// stream, event or workspace, counted from 1 in that order) fails as if the
-// device were out of memory, so that every cleanup path of a failed create
+// QX_TEST_FAIL_ALLOC=k: the k-th device resource a create acquires (counted
+// from 1; a create acquires at most one, its workspace) fails as if the
+// device were out of memory, so that the cleanup path of a failed create
 // can be exercised.
 int fail_alloc_at() {
     const char* v = getenv("QX_TEST_FAIL_ALLOC");
@@ -1580,7 +1545,6 @@ qx_status make_exec(Plan&& pl, qx_exec* out) {
     h->device = dev;
     h->rt = &rt;
     h->ws = nullptr;
-    h->side = nullptr;
     h->ws_bytes = (uint64_t)pl.info.workspace_bytes;
     h->plan = std::move(pl);
     // QX_VALIDATE flag word behind the plan's workspace
@@ -1588,23 +1552,7 @@ qx_status make_exec(Plan&& pl, qx_exec* out) {
     if (!h->plan.checks.empty()) h->ws_bytes = h->flag_off + 256;
     hipError_t e = hipSuccess;
     const char* what = "";
-    if (h->plan.n_events > 0) {
-        // default-priority side stream; events without timing
-        what = "executor side stream";
-        e = injected() ? hipErrorOutOfMemory : rt.stream_create(&h->side);
-        if (e == hipSuccess) g_count[C_STREAMS]++;
-        else h->side = nullptr;
-        for (int i = 0; e == hipSuccess && i < h->plan.n_events + 2; ++i) {
-            what = "executor event";
-            hipEvent_t ev = nullptr;
-            e = injected() ? hipErrorOutOfMemory : rt.event_create(&ev, false);
-            if (e == hipSuccess) {
-                h->evs.push_back(ev);
-                g_count[C_EVENTS]++;
-            }
-        }
-    }
-    if (e == hipSuccess && h->ws_bytes) {
+    if (h->ws_bytes) {
         what = "workspace allocation";
         e = injected() ? hipErrorOutOfMemory : rt.malloc(&h->ws, h->ws_bytes);
         if (e == hipSuccess) {
@@ -1633,17 +1581,14 @@ qx_status make_exec(Plan&& pl, qx_exec* out) {
     return QX_OK;
 }
 
-// What a run needs: the plan, the runtime, the workspace (with the
-// validation flag word at flag_off) and, for plans that overlap launches, the
-// side stream and events.  Without a side stream every launch goes to the
-// caller's stream in plan order.
+// What a run needs: the plan, the runtime and the workspace (with the
+// validation flag word at flag_off).  Every launch goes to the caller's
+// stream in plan order.
 struct RunCtx {
     const Plan* plan;
     const RtTable* rt;
     void* ws;
     uint64_t flag_off;
-    hipStream_t side;
-    const hipEvent_t* evs;
     int device;
 };
 
@@ -1725,14 +1670,6 @@ qx_status run_plan(const RunCtx& c, const void* const* inputs, void* output, voi
         const qx_status st = validate_ranges(c, inputs, s);
         if (st) return st;
     }
-    // Overlapped plans fork to the side stream after everything already on
-    // the caller's stream and join back at the end.  Per-launch timing runs
-    // every launch in plan order on the caller's stream instead.
-    const bool lanes = pl.n_events > 0 && !evs && c.side;
-    if (lanes) {
-        if ((e = rt.event_record(c.evs[0], s)) != hipSuccess) return hip_fail(e, "hipEventRecord");
-        if ((e = rt.stream_wait(c.side, c.evs[0])) != hipSuccess) return hip_fail(e, "hipStreamWaitEvent");
-    }
     for (const LaunchRec& r0 : pl.launches) {
         LaunchRec r = r0;
         for (int i = 0; i < r.nslots; ++i) {
@@ -1746,21 +1683,11 @@ qx_status run_plan(const RunCtx& c, const void* const* inputs, void* output, voi
         }
         void* args[1] = {r.blob};
         const size_t li = (size_t)(&r0 - pl.launches.data());
-        hipStream_t ls = (lanes && r.lane) ? c.side : s;
-        if (lanes && r.wait_ev >= 0 && (e = rt.stream_wait(ls, c.evs[r.wait_ev])) != hipSuccess)
-            return hip_fail(e, "hipStreamWaitEvent");
         if (evs && (e = rt.event_record((*evs)[2 * li], s)) != hipSuccess) return hip_fail(e, "hipEventRecord");
         g_count[C_LAUNCHES]++;
-        e = rt.launch(r, args, ls);
+        e = rt.launch(r, args, s);
         if (e != hipSuccess) return hip_fail(e, r.name);
         if (evs && (e = rt.event_record((*evs)[2 * li + 1], s)) != hipSuccess) return hip_fail(e, "hipEventRecord");
-        if (lanes && r.rec_ev >= 0 && (e = rt.event_record(c.evs[r.rec_ev], ls)) != hipSuccess)
-            return hip_fail(e, "hipEventRecord");
-    }
-    if (lanes) {
-        const hipEvent_t join = c.evs[pl.n_events + 1];
-        if ((e = rt.event_record(join, c.side)) != hipSuccess) return hip_fail(e, "hipEventRecord");
-        if ((e = rt.stream_wait(s, join)) != hipSuccess) return hip_fail(e, "hipStreamWaitEvent");
     }
     return QX_OK;
 }
@@ -1768,7 +1695,7 @@ qx_status run_plan(const RunCtx& c, const void* const* inputs, void* output, voi
 qx_status run_exec(qx_exec h, const void* const* inputs, void* output, void* stream,
                    std::vector<hipEvent_t>* evs = nullptr) {
     if (!is_live(h) || h->magic != kMagic) return fail(QX_ERR_INVALID_ARG, "invalid executor handle");
-    const RunCtx c{&h->plan, h->rt, h->ws, h->flag_off, h->side, h->evs.data(), h->device};
+    const RunCtx c{&h->plan, h->rt, h->ws, h->flag_off, h->device};
     return run_plan(c, inputs, output, stream, evs);
 }
 
@@ -1788,11 +1715,13 @@ qx_status profile_exec(qx_exec h, const void* const* inputs, void* output, void*
     std::vector<hipEvent_t> evs(2 * nl * (size_t)reps, nullptr);
     qx_status st = QX_OK;
     hipError_t e = hipSuccess;
-    for (auto& ev : evs)
+    for (auto& ev : evs) {
         if ((e = rt.event_create(&ev, true)) != hipSuccess) {
             ev = nullptr;
             break;
         }
+        g_count[C_EVENTS]++;
+    }
     if (e != hipSuccess) {
         st = hip_fail(e, "hipEventCreate");
     } else {
@@ -1814,7 +1743,10 @@ qx_status profile_exec(qx_exec h, const void* const* inputs, void* output, void*
             }
     }
     for (auto& ev : evs)
-        if (ev) (void)rt.event_destroy(ev);
+        if (ev) {
+            (void)rt.event_destroy(ev);
+            g_count[C_EVENTS_FREED]++;
+        }
     return st;
 }
 
@@ -2303,7 +2235,7 @@ qx_status qgemm_i16i32_noalloc(const int16_t* A, const int16_t* B, int32_t* C, i
     void* ws = nullptr;
     if ((e = scratch_device_ptr(dev, &ws)) != hipSuccess) return hip_fail(e, "scratch lookup");
     const void* in[2] = {A, B};
-    const RunCtx c{pl, &kHip, ws, round_up((uint64_t)pl->info.workspace_bytes, 256), nullptr, nullptr, dev};
+    const RunCtx c{pl, &kHip, ws, round_up((uint64_t)pl->info.workspace_bytes, 256), dev};
     return run_plan(c, in, C, stream, nullptr);
 }
 

@@ -285,9 +285,9 @@ struct Slot {
     uint64_t add;           // byte offset added to the bound pointer
 };
 
-// A launch runs on the caller's stream (lane 0) or on the executor's side
-// stream (lane 1).  Cross-lane order is explicit: a launch may wait for an
-// executor event before it starts and record one when it is enqueued.
+// One kernel launch of a plan: kernel, geometry and parameter block, with
+// the pointer fields bound at run time through slots.  Every launch of a
+// plan goes to the caller's stream, in plan order.
 struct LaunchRec {
     const void* fn = nullptr;
     dim3 grid{1, 1, 1};
@@ -298,9 +298,6 @@ struct LaunchRec {
     Slot slots[8];
     int nslots = 0;
     const char* name = "";
-    uint8_t lane = 0;
-    int16_t wait_ev = -1;
-    int16_t rec_ev = -1;
 
     template <class P>
     void set_params(const P& p) {

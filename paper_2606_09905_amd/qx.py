@@ -553,8 +553,7 @@ class Executor:
 # ---------------------------------------------------------------------------
 # test seams (include/qx_testing.h): no result is computed under the double
 # ---------------------------------------------------------------------------
-COUNTERS = ("allocs", "frees", "streams", "streams_freed", "events", "events_freed", "launches",
-            "live_handles")
+COUNTERS = ("allocs", "frees", "events", "events_freed", "launches", "live_handles")
 
 
 def testing_host_double(on: bool) -> None:

@@ -111,19 +111,17 @@ static void executors() {
     cycle(qx_exec_create_lenet_i32(&h, 4096), h, "lenet");
     cycle(qx_exec_create_minmax(&h, 1 << 27, 4), h, "minmax");
     cycle(qx_exec_create_pool2x2(&h, 0, 16, 64, 224, 224), h, "pool");
-    // injected failures at every acquisition of an overlapped plan
-    for (int k = 1; k <= 12; ++k) {
-        char v[16];
-        snprintf(v, sizeof v, "%d", k);
-        setenv("QX_TEST_FAIL_ALLOC", v, 1);
-        qx_exec f = (qx_exec)(uintptr_t)1;
-        const qx_status st = qx_exec_create_gemm_i16i32(&f, 2048, 2048, 2048, 64, 256, 256);
-        CHECK(st == QX_ERR_OUT_OF_MEMORY && f == nullptr, "injected failure %d", k);
-    }
+    // an injected failure of the one acquisition (the workspace), then past it
+    setenv("QX_TEST_FAIL_ALLOC", "1", 1);
+    qx_exec f = (qx_exec)(uintptr_t)1;
+    CHECK(qx_exec_create_gemm_i16i32(&f, 2048, 2048, 2048, 64, 256, 256) == QX_ERR_OUT_OF_MEMORY && f == nullptr,
+          "injected failure");
+    setenv("QX_TEST_FAIL_ALLOC", "2", 1);
+    cycle(qx_exec_create_gemm_i16i32(&f, 2048, 2048, 2048, 64, 256, 256), f, "past the injected failure");
     unsetenv("QX_TEST_FAIL_ALLOC");
-    int64_t c[8];
-    qx_testing_counters(c, 8);
-    CHECK(c[0] == c[1] && c[2] == c[3] && c[4] == c[5] && c[7] == 0, "every resource released");
+    int64_t c[6];
+    qx_testing_counters(c, 6);
+    CHECK(c[0] == c[1] && c[2] == c[3] && c[5] == 0, "every resource released");
     // one-shot calls under the double
     for (int r = 0; r < 3; ++r)
         CHECK(qgemm_i16i32((const int16_t*)in[0], (const int16_t*)in[1], (int32_t*)out, 512, 512, 512, 1, 256, 256,

@@ -174,9 +174,9 @@ def test_gemm_s24_encode_nt_path(shape):
 
 
 @pytest.mark.parametrize("shape", [(1000, 1100, 1400, 3), (520, 700, 1000, 13)])
-def test_gemm_overlapped_batch_groups(shape):
-    # Large enough for the side-stream overlap: batch groups of 1 and of 2
-    # (13 batches in 7 groups, the last one short).
+def test_gemm_batch_groups(shape):
+    # Large enough to run in batch groups: groups of 1 and of 2 (13 batches
+    # in 7 groups, the last one short), each encoded and then contracted.
     M, N, K, batch = shape
     rng = np.random.default_rng(zlib.crc32(repr(("lanes", shape)).encode()))
     A = rand_int(rng, (batch, M, K), 256, np.int16)
