@@ -273,20 +273,20 @@ qx_status plan_int_gemm(const GemmSpec& s, Plan* pl, uint64_t* ws_used) {
         const uint64_t a_off = round_up(*ws_used, 256);
         const uint64_t b_off = round_up(a_off + 2 * (uint64_t)s.batch * Mp * Kp, 256);
         *ws_used = b_off + 2 * (uint64_t)s.batch * Np * Kp;
-        // Batch groups: above 2^32 multiply-adds the batches run in up to 8
-        // groups, each encoded and then contracted, so that a group's
-        // encoded operands are still in the last-level cache when its
-        // contraction reads them.  Encoding the next group on a second
-        // stream while the current one contracts measured 4% slower on
-        // 64 x 2048^3 (the encoders then take CUs between the contraction's
-        // workgroups).
-        const double macs = (double)s.M * (double)s.N * (double)s.K * (double)s.batch;
-        int64_t groups = 1;
-        if (s.batch >= 2 && macs >= (double)(1LL << 32)) {
-            groups = std::min<int64_t>(s.batch, 8);
-            const int64_t per = (s.batch + groups - 1) / groups;
-            groups = (s.batch + per - 1) / per;
-        }
+        // Batch groups: the batches run in groups whose encoded operands
+        // fill at most the 256 MiB last-level cache, each group encoded and
+        // then contracted, so that the contraction reads operands the
+        // encoders have just left in that cache.  64 x 2048^3 (1 GiB
+        // encoded, 16 MiB per batch): 4 groups 1.42 ms per step, 8 groups
+        // 1.48, 2 groups 1.50, one 1.50 (the contraction slows once a
+        // group outgrows the cache; smaller groups pay more encoder tails).
+        // Encoding the next group on a second stream while the current one
+        // contracts measured 4% slower still (the encoders then take CUs
+        // between the contraction's workgroups).
+        constexpr uint64_t kGroupBytes = (uint64_t)256 << 20;
+        const uint64_t batch_bytes = 2 * (uint64_t)(Mp + Np) * (uint64_t)Kp;
+        const int64_t fit = std::max<int64_t>((int64_t)(kGroupBytes / batch_bytes), 1);
+        const int64_t groups = (s.batch + fit - 1) / fit;
         const int64_t per_group = (s.batch + groups - 1) / groups;
         auto enc_a = [&](int64_t b0, int64_t cnt) {
             EncParams ea{};

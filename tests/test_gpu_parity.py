@@ -173,22 +173,29 @@ def test_gemm_s24_encode_nt_path(shape):
     same(got, orc.gemm_i32_s24(A, B), str(shape))
 
 
-@pytest.mark.parametrize("shape", [(1000, 1100, 1400, 3), (520, 700, 1000, 13)])
-def test_gemm_batch_groups(shape):
-    # Large enough to run in batch groups: groups of 1 and of 2 (13 batches
-    # in 7 groups, the last one short), each encoded and then contracted.
+@pytest.mark.parametrize("shape,groups", [((2048, 2048, 2048, 17), [9, 8]), ((3000, 2900, 3000, 9), [5, 4])])
+def test_gemm_batch_groups(shape, groups):
+    # Encoded operands beyond 256 MiB: the batches run in groups (the last
+    # one short), each encoded and then contracted.  Sampled rows of the
+    # batches at every group boundary against the oracle, Freivalds' check
+    # on every batch, and a second run of the same executor.
     M, N, K, batch = shape
-    rng = np.random.default_rng(zlib.crc32(repr(("lanes", shape)).encode()))
+    rng = np.random.default_rng(zlib.crc32(repr(("groups", shape)).encode()))
     A = rand_int(rng, (batch, M, K), 256, np.int16)
     B = rand_int(rng, (batch, K, N), 256, np.int16)
-    groups = -(-batch // -(-batch // min(batch, 8)))
+    A[0, 0, :] = -256
+    B[-1, :, -1] = -256
     with qx.Executor.gemm_i16i32(M, N, K, batch, 256, 256) as ex:
         plan = ex.plan()
-        assert plan["kernels"] == 3 * groups, plan
+        assert plan["kernels"] == 3 * len(groups), plan
         C = run_exec(ex, (A, B))
         C2 = run_exec(ex, (A, B))
     same(C2, C, "second run")
-    same(C, orc.gemm_i16i32(A, B))
+    edges = sorted({0, groups[0] - 1, groups[0], batch - 1})
+    for b in edges:
+        rows = np.unique(np.concatenate([np.sort(rng.choice(M, size=6, replace=False)), [0, M - 1]]))
+        same(C[b, rows], orc.gemm_i16i32(np.ascontiguousarray(A[b, rows]), B[b]), f"batch {b}")
+    assert freivalds(A, B, C, trials=2)
 
 
 def test_f16_exact_mixed_magnitudes():
