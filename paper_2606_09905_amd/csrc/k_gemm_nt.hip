@@ -341,9 +341,9 @@ __device__ __forceinline__ int chunk_swz(int r) { return (r >> 1) & 7; }
 // K-slot (h, e) is k = 8*ks + 4*h + e for both operands.  The sum is formed
 // in fp32 in the matrix cores' order.  IMPL gathers B from the bordered NHWC
 // fp32 image, 32 channels of one kernel tap per K tile.
-template <int BM, int BN, int NW, bool IMPL>
+template <int BM, int BN, int NW, bool IMPL, int WN = 64>
 __global__ __launch_bounds__(NW * 64) void k_gemm_nt_f32(const GemmParams p) {
-    constexpr int BK = 32, KCH = 8, WM = 64, WN = 64;
+    constexpr int BK = 32, KCH = 8, WM = 64;
     constexpr int TM = WM / 32, TN = WN / 32;
     constexpr int WAVES_N = BN / WN;
     static_assert((BM / WM) * (BN / WN) == NW, "wave grid");
@@ -942,8 +942,9 @@ void build_gemm_nt_f32(const GemmParams& p0, int batch, LaunchRec* rec) {
         rec->block = dim3(512, 1, 1);
         rec->name = impl ? "gemm_nt_f32_conv_128x256" : "gemm_nt_f32_128x256";
     } else if (bm == 64) {
-        rec->fn = impl ? (const void*)k_gemm_nt_f32<64, 128, 2, true> : (const void*)k_gemm_nt_f32<64, 128, 2, false>;
-        rec->block = dim3(128, 1, 1);
+        // the conv gather runs four 64x32 waves, as the fp16 one does
+        rec->fn = impl ? (const void*)k_gemm_nt_f32<64, 128, 4, true, 32> : (const void*)k_gemm_nt_f32<64, 128, 2, false>;
+        rec->block = dim3(impl ? 256 : 128, 1, 1);
         rec->name = impl ? "gemm_nt_f32_conv_64x128" : "gemm_nt_f32_64x128";
     } else {
         rec->fn = impl ? (const void*)k_gemm_nt_f32<128, 128, 4, true> : (const void*)k_gemm_nt_f32<128, 128, 4, false>;
