@@ -178,7 +178,7 @@ struct GemmSpec {
 // the chunk covers at least one 64-wide K tile.
 // The NT kernel forms each lane's byte offset into an operand panel (at
 // most 256 rows of Kp fp16 elements) in 32-bit int arithmetic, and the B^T
-// encoder puts Kp/256 workgroups in grid y, so Kp is held below 2^22 (every
+// encoder puts Kp/128 workgroups in grid y, so Kp is held below 2^22 (every
 // offset below 2^31); longer K takes the register-staged kernel, which
 // addresses in 64 bits.
 constexpr int64_t kNtMaxKp = (int64_t)1 << 22;
@@ -350,6 +350,19 @@ qx_status plan_int_gemm(const GemmSpec& s, Plan* pl, uint64_t* ws_used) {
     const bool nt8 = s.allow_nt && use_i8nt(route, s.M, s.N, s.K, s.batch);
     if (s.b_conv && !nt8) return fail(QX_ERR_UNSUPPORTED, "gathered B needs the NT int8 route");
     const bool offset = route == R_I8_OFFSET4 || route == R_S24_I8LIMB;
+    // Implicit INT32 convolution (C_in a multiple of 64): one launch writes
+    // the image as bordered NHWC limb planes with per-chunk position sums and
+    // the weights as limb planes in (kh, kw, ci) order with their row sums;
+    // the contraction then gathers each 64-k tile of B^T (64 channels of one
+    // tap per pixel) from the planes, as the fp16 conv does from its NHWC
+    // copy, instead of reading a materialised column matrix (9x the image
+    // for a 3x3 kernel).  Offsets into the planes are 32-bit.
+    const ConvGeom& cgeo = s.geo;
+    const int64_t conv_hp = cgeo.H + 2 * cgeo.pad, conv_wp = cgeo.W + 2 * cgeo.pad;
+    const int64_t conv_imgs = s.hw > 0 ? s.N / s.hw : 0;
+    const int64_t plane_x = conv_imgs * conv_hp * conv_wp * cgeo.Ci;
+    const bool conv_nhwc = nt8 && s.b_conv && s.s24 && route == R_S24_I8LIMB && cgeo.Ci % 64 == 0 &&
+                           s.batch == 1 && 3 * plane_x < ((int64_t)1 << 31);
     uint64_t rs_off = 0, cs_off = 0;
     if (offset) {
         g.corr_c = route == R_I8_OFFSET4 ? 128 : 32896;
@@ -357,7 +370,11 @@ qx_status plan_int_gemm(const GemmSpec& s, Plan* pl, uint64_t* ws_used) {
         g.cs_slices = slices;
         rs_off = round_up(*ws_used, 256);
         cs_off = round_up(rs_off + 4 * (uint64_t)s.batch * (uint64_t)s.M, 256);
-        *ws_used = cs_off + 4 * (uint64_t)s.batch * (uint64_t)slices * (uint64_t)s.N;
+        // column sums: [batch][K/64][N], or for the implicit convolution the
+        // per-chunk position sums [N_img][C_in/64][H+2p][W+2p]
+        const uint64_t cs_n = conv_nhwc ? (uint64_t)(conv_imgs * (cgeo.Ci / 64) * conv_hp * conv_wp)
+                                        : (uint64_t)s.batch * (uint64_t)slices * (uint64_t)s.N;
+        *ws_used = cs_off + 4 * cs_n;
         if (!nt8) {  // the limb-plane encoders produce the sums themselves
             SumsParams sp{};
             sp.sA = s.sA; sp.sB = s.sB;
@@ -399,6 +416,40 @@ qx_status plan_int_gemm(const GemmSpec& s, Plan* pl, uint64_t* ws_used) {
         g.ksplit = ksplit;
         info.k_splits = ksplit > 1 ? ksplit : 0;
         if (ksplit > 1) add_fill_out(pl, s.M * s.N * s.batch);
+        if (conv_nhwc) {
+            const uint64_t a_off = round_up(*ws_used, 256);
+            const uint64_t x_off = round_up(a_off + (uint64_t)P * Mp * Kp, 256);
+            *ws_used = x_off + (uint64_t)P * plane_x;
+            ConvLimbPrepParams cp{};
+            cp.plane_x = plane_x;
+            cp.plane_a = Mp * Kp;
+            cp.nimg = (int32_t)conv_imgs; cp.Co = (int32_t)s.M; cp.Kd = (int32_t)s.K;
+            cp.g = cgeo;
+            LaunchRec r1;
+            build_conv_prep_limb(cp, &r1);
+            r1.bind(offsetof(ConvLimbPrepParams, x), s.b_bind, s.b_ws_off);
+            r1.bind(offsetof(ConvLimbPrepParams, w), s.a_bind);
+            r1.bind(offsetof(ConvLimbPrepParams, xp8), BIND_WS, x_off);
+            r1.bind(offsetof(ConvLimbPrepParams, s), BIND_WS, cs_off);
+            r1.bind(offsetof(ConvLimbPrepParams, a8), BIND_WS, a_off);
+            r1.bind(offsetof(ConvLimbPrepParams, rowsum), BIND_WS, rs_off);
+            g.b_mode = B_NHWC;
+            g.g = cgeo;
+            g.sA = P * Mp * Kp; g.sB = 0;
+            g.lda = (int32_t)Kp; g.ldb = 0;
+            g.plane_a = Mp * Kp; g.plane_b = plane_x;
+            LaunchRec r3;
+            if (!build_gemm_i8nt(route, g, 1, &r3)) return fail(QX_ERR_UNSUPPORTED, "no kernel for route %d", route);
+            r3.bind(offsetof(GemmParams, A), BIND_WS, a_off);
+            r3.bind(offsetof(GemmParams, B), BIND_WS, x_off);
+            r3.bind(offsetof(GemmParams, C), BIND_OUT);
+            r3.bind(offsetof(GemmParams, rowsum), BIND_WS, rs_off);
+            r3.bind(offsetof(GemmParams, colsum), BIND_WS, cs_off);
+            pl->launches.push_back(r1);
+            pl->launches.push_back(r3);
+            info.tile_m = bm; info.tile_n = bn; info.tile_k = 64;
+            return QX_OK;
+        }
         const uint64_t a_off = round_up(*ws_used, 256);
         const uint64_t b_off = round_up(a_off + (uint64_t)s.batch * P * Mp * Kp, 256);
         *ws_used = b_off + (uint64_t)s.batch * P * Np * Kp;

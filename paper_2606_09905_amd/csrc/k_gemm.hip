@@ -791,6 +791,97 @@ __global__ __launch_bounds__(NT) void k_enc_limb(const EncPairParams p) {
     else enc_limb_bt<S, T>(p.b, blockIdx.x - p.blocks_a);
 }
 
+// Implicit lowering of an INT32 convolution onto the int8 limb route
+// (smul24 split, C_in a multiple of 64).  blockIdx.y == 0: a block takes
+// one bordered image row (n, hp) and 64 of its positions, and for every
+// 64-channel chunk stages the chunk's NCHW values in LDS (coalesced along
+// W), then writes each position's 64 channels as three 64-byte limb rows
+// (8 channels per thread) and the chunk's sum of the represented values at
+// that position (positions outside the image hold the value 0).
+// blockIdx.y == 1: one wave per output channel writes its weight row in
+// (kh, kw, ci) order as limb planes and its row sum.
+__global__ __launch_bounds__(NT) void k_conv_prep_limb(const ConvLimbPrepParams p) {
+    const ConvGeom& g = p.g;
+    const int tid = threadIdx.x;
+    if (blockIdx.y == 0) {
+        if ((int)blockIdx.x >= p.xblocks) return;
+        __shared__ int32_t t[64][65];
+        const int Hp = g.H + 2 * g.pad, Wp = g.W + 2 * g.pad;
+        const int wch = (Wp + 63) / 64, CC = g.Ci / 64;
+        const int n = blockIdx.x / (Hp * wch), rem = blockIdx.x - n * Hp * wch;
+        const int hp = rem / wch, wp0 = (rem - hp * wch) * 64;
+        const int h = hp - g.pad;
+        const bool row_in = h >= 0 && h < g.H;
+        const int wl = tid & 63, cq = tid >> 6;
+        const int w = wp0 + wl - g.pad;
+        const bool in = row_in && w >= 0 && w < g.W;
+        const int64_t pos0 = ((int64_t)n * Hp + hp) * Wp;           // position of (n, hp, 0)
+        for (int c0 = 0; c0 < g.Ci; c0 += 64) {
+            const int32_t* src = p.x + (((int64_t)n * g.Ci + c0) * g.H + h) * g.W + w;
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+                const int c = cq + 4 * r;
+                t[c][wl] = in ? src[(int64_t)c * g.H * g.W] : 0;
+            }
+            __syncthreads();
+#pragma unroll
+            for (int i = 0; i < 2; ++i) {
+                const int q = tid + NT * i, px = q >> 3, cg = q & 7;
+                uint32_t u[8];
+                uint32_t sum = 0;
+#pragma unroll
+                for (int e = 0; e < 8; ++e) {
+                    u[e] = (uint32_t)t[cg * 8 + e][px];
+                    sum += (uint32_t)SchemeS24::value((int32_t)u[e]);
+                }
+                uint32_t lo[3], hi[3];
+                pack_s24(u[0], u[1], u[2], u[3], lo);
+                pack_s24(u[4], u[5], u[6], u[7], hi);
+                // the eight threads of one position are eight consecutive lanes
+                sum += __shfl_xor(sum, 1, 64);
+                sum += __shfl_xor(sum, 2, 64);
+                sum += __shfl_xor(sum, 4, 64);
+                if (wp0 + px < Wp) {
+                    const int64_t pos = pos0 + wp0 + px;
+#pragma unroll
+                    for (int pl = 0; pl < 3; ++pl) {
+                        typedef uint32_t u2v __attribute__((ext_vector_type(2)));
+                        *(u2v*)(p.xp8 + pl * p.plane_x + pos * g.Ci + c0 + cg * 8) = u2v{lo[pl], hi[pl]};
+                    }
+                    if (cg == 0)
+                        p.s[(((int64_t)n * CC + c0 / 64) * Hp + hp) * Wp + wp0 + px] = (int32_t)sum;
+                }
+            }
+            __syncthreads();
+        }
+        return;
+    }
+    // weights: wave -> output channel; lane -> 16 consecutive k (one tap, 16 channels)
+    const int co = (int)blockIdx.x * (NT / 64) + (tid >> 6), lane = tid & 63;
+    if ((int)blockIdx.x >= p.wblocks || co >= p.Co) return;   // whole wave
+    const int taps = g.KH * g.KW;
+    uint32_t sum = 0;
+    for (int k0 = lane * 16; k0 < p.Kd; k0 += 64 * 16) {
+        const int tap = k0 / g.Ci, ci0 = k0 - tap * g.Ci;
+        const int32_t* src = p.w + ((int64_t)co * g.Ci + ci0) * taps + tap;
+        uint32_t u[16];
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+            u[e] = (uint32_t)src[(int64_t)e * taps];
+            sum += (uint32_t)SchemeS24::value((int32_t)u[e]);
+        }
+        uint32_t d[4][3];
+#pragma unroll
+        for (int g4 = 0; g4 < 4; ++g4) pack_s24(u[4 * g4], u[4 * g4 + 1], u[4 * g4 + 2], u[4 * g4 + 3], d[g4]);
+#pragma unroll
+        for (int pl = 0; pl < 3; ++pl)
+            *(i4*)(p.a8 + pl * p.plane_a + (int64_t)co * p.Kd + k0) =
+                i4{(int)d[0][pl], (int)d[1][pl], (int)d[2][pl], (int)d[3][pl]};
+    }
+    for (int off = 32; off > 0; off >>= 1) sum += __shfl_xor(sum, off, 64);
+    if (lane == 0) p.rowsum[co] = (int32_t)sum;
+}
+
 // 64-byte LDS rows (64 int8) as four 16-byte chunks; the 16 rows of one
 // ds_read_b128 lane group land in distinct banks.
 __device__ __forceinline__ int swz_i8(int row) { return (row >> 2) & 3; }
@@ -894,7 +985,26 @@ __global__ __launch_bounds__(64 * WAVES) void k_gemm_i8nt(const GemmParams p) {
     const bool lead = blockIdx.y == 0;
     // planes: A8 [batch][P][Mp][Kp] (sA = P*Mp*Kp, lda = Kp, plane_a = Mp*Kp), B8T likewise
     const char* a_panel = (const char*)p.A + b * p.sA + (int64_t)m0 * p.lda + kt0 * BK;
-    const char* b_panel = (const char*)p.B + b * p.sB + (int64_t)n0 * p.ldb + kt0 * BK;
+    // B_NHWC (implicit convolution, one image batch, no K slices): B^T column
+    // n is output pixel n, and its K tile t is the 64 channels of chunk t % CC
+    // of kernel tap t / CC at that pixel's window in the bordered NHWC limb
+    // planes; the pixel's window origin goes into the lane offsets, the tap
+    // and chunk into the tile's base
+    const bool nhwc = p.b_mode == B_NHWC;
+    const ConvGeom& cg = p.g;
+    const int Hp = cg.H + 2 * cg.pad, Wp = cg.W + 2 * cg.pad, CC = cg.Ci / 64;
+    auto win_origin = [&](int n) {   // (img, oh*stride, ow*stride) of output pixel n, as a bordered position
+        const int pix = n < p.N ? n : 0;   // columns past N are never stored
+        const int img = pix / p.hw, rem = pix - img * p.hw;
+        const int oh = rem / cg.Wo, ow = rem - oh * cg.Wo;
+        return ((int64_t)img * CC * Hp + oh * cg.stride) * Wp + ow * cg.stride;   // S index, chunk 0
+    };
+    auto tile_tap = [&](int t, int64_t& x_off, int64_t& s_off) {   // K tile t's offsets in xp8 (bytes) and s
+        const int chunk = t % CC, tap = t / CC, kh = tap / cg.KW, kw = tap - kh * cg.KW;
+        x_off = ((int64_t)kh * Wp + kw) * cg.Ci + chunk * 64;
+        s_off = ((int64_t)chunk * Hp + kh) * Wp + kw;
+    };
+    const char* b_panel = nhwc ? (const char*)p.B : (const char*)p.B + b * p.sB + (int64_t)n0 * p.ldb + kt0 * BK;
     const unsigned wave_u = (unsigned)wave, wl_u = (unsigned)wl, kg_u = (unsigned)kg;
     // load k of this wave covers stage chunks (wl + GW*k)*64 + lane
     unsigned ol[LAB];
@@ -907,20 +1017,32 @@ __global__ __launch_bounds__(64 * WAVES) void k_gemm_i8nt(const GemmParams p) {
         } else {
             const int qb = q - CH_A;
             const int plane = qb / (BN * KCH), rem = qb % (BN * KCH), row = rem / KCH, pc = rem % KCH;
-            ol[k] = (unsigned)((int64_t)plane * p.plane_b + row * p.ldb + (pc ^ swz_i8(row)) * 16);
+            if (nhwc) {
+                // window origin of pixel n0 + row in the NHWC planes: its S
+                // index with the image's chunk stride taken out
+                const int pix = n0 + row < p.N ? n0 + row : 0;
+                const int img = pix / p.hw, prem = pix - img * p.hw;
+                const int oh = prem / cg.Wo, ow = prem - oh * cg.Wo;
+                const int64_t pos = ((int64_t)img * Hp + oh * cg.stride) * Wp + ow * cg.stride;
+                ol[k] = (unsigned)((int64_t)plane * p.plane_b + pos * cg.Ci + (pc ^ swz_i8(row)) * 16);
+            } else {
+                ol[k] = (unsigned)((int64_t)plane * p.plane_b + row * p.ldb + (pc ^ swz_i8(row)) * 16);
+            }
         }
     }
     const unsigned lds_s0 = (unsigned)(uintptr_t)&Stg[0][0][0] + kg_u * (unsigned)(STAGES * CH * 16);
     // column sums [batch][K/64][N]: this thread's column, clamped into N
     // (columns past N are never stored)
-    const int32_t* csg = OFFS ? p.colsum + ((int64_t)b * p.cs_slices + kt0) * p.N : nullptr;
-    const unsigned cs_off = (unsigned)min(n0 + tg, p.N - 1) * 4u;
+    const int32_t* csg = !OFFS ? nullptr : nhwc ? p.colsum : p.colsum + ((int64_t)b * p.cs_slices + kt0) * p.N;
+    const unsigned cs_off = (unsigned)(nhwc ? win_origin(n0 + tg) : (int64_t)min(n0 + tg, p.N - 1)) * 4u;
     const unsigned lds_cs0 = (unsigned)(uintptr_t)&cs_ring[0][0][0] + (OFFS ? kg_u * (STAGES * GTH * 4) : 0u) + wl_u * 256;
     // this group's local tile u is K tile KG*u + kg, in slot u % STAGES
     auto issue = [&](int u) {
         const int s = u % STAGES, t = KG * u + (int)kg_u;
         const char* ab = a_panel + t * BK;
-        const char* bb = b_panel + t * BK;
+        int64_t x_off = 0, s_off = 0;
+        if (nhwc) tile_tap(t, x_off, s_off);
+        const char* bb = nhwc ? b_panel + x_off : b_panel + t * BK;
         const unsigned ls = lds_s0 + (unsigned)(s * CH * 16);
 #pragma unroll
         for (int k = 0; k < LAB; ++k) {
@@ -931,7 +1053,8 @@ __global__ __launch_bounds__(64 * WAVES) void k_gemm_i8nt(const GemmParams p) {
         }
         if constexpr (OFFS)
             asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dword %0, %1"
-                         :: "v"(cs_off), "s"(csg + (int64_t)t * p.N), "s"(lds_cs0 + s * GTH * 4) : "memory", "m0");
+                         :: "v"(cs_off), "s"(nhwc ? csg + s_off : csg + (int64_t)t * p.N), "s"(lds_cs0 + s * GTH * 4)
+                         : "memory", "m0");
     };
     // barrier of this group's waves: all of them have waited for their part
     // of the current tile and have finished reading the slot about to be
@@ -1299,6 +1422,19 @@ void build_enc_limb(int32_t route, bool s24, const EncPairParams& p, LaunchRec* 
     case R_I8_OFFSET4: enc_limb_rec<SchemeOffset4>(s24, p, rec, "enc_limb_offset4"); break;
     default: enc_limb_rec<SchemeS24>(s24, p, rec, "enc_limb_s24"); break;
     }
+}
+
+void build_conv_prep_limb(const ConvLimbPrepParams& p0, LaunchRec* rec) {
+    ConvLimbPrepParams p = p0;
+    const ConvGeom& g = p.g;
+    const int Hp = g.H + 2 * g.pad, Wp = g.W + 2 * g.pad;
+    p.xblocks = p.nimg * Hp * ((Wp + 63) / 64);
+    p.wblocks = (p.Co + NT / 64 - 1) / (NT / 64);
+    rec->fn = (const void*)k_conv_prep_limb;
+    rec->grid = dim3((unsigned)std::max(p.xblocks, p.wblocks), 2, 1);
+    rec->block = dim3(NT, 1, 1);
+    rec->name = "conv_prep_limb_s24";
+    rec->set_params(p);
 }
 
 bool build_gemm_i8nt(int32_t route, const GemmParams& p0, int batch, LaunchRec* rec) {

@@ -46,7 +46,8 @@ struct GemmParams {
     int32_t chunk_tiles;    // F16_EXACT: flush fp32 partials every chunk_tiles K-tiles
     int32_t corr_c;         // offset constant c of the limb split (0: none)
     int32_t out_mode;       // OutMode
-    int32_t b_mode;         // BMode
+    int32_t b_mode;         // BMode (int8 NT route: B_KN planes, or B_NHWC: gathered from the
+                            // bordered NHWC limb planes of ConvLimbPrepParams, colsum from s)
     int32_t hw;             // OUT_CONV: Ho*Wo
     int32_t tiles_n;        // number of N tiles (grid swizzle)
     int32_t cs_slices;      // colsum holds this many partial rows per batch
@@ -132,6 +133,28 @@ struct ConvPrepParams {
     int32_t nimg, Co, Cop, Kd;
     int32_t xblocks, wblocks;
     int32_t elem_bytes;
+    ConvGeom g;
+};
+
+// Implicit lowering of an INT32 (smul24) convolution for the int8 limb route
+// (C_in a multiple of 64), in one launch: the input as three int8 limb
+// planes of a zero-bordered NHWC image xp8 [3][N][H+2pad][W+2pad][Ci] (the
+// border holds the limbs of 0), the per-position sums of the represented
+// values over each 64-channel chunk s [N][Ci/64][H+2pad][W+2pad] (the column
+// sums of the offset correction, gathered per K tile like the columns), and
+// the weights as limb planes a8 [3][Mp][Kd], k = (kh*KW + kw)*Ci + ci, with
+// their row sums.
+struct ConvLimbPrepParams {
+    const int32_t* x;       // NCHW
+    const int32_t* w;       // OIHW
+    int8_t* xp8;
+    int32_t* s;
+    int8_t* a8;
+    int32_t* rowsum;        // [Co]
+    int64_t plane_x;        // bytes between the image planes
+    int64_t plane_a;        // bytes between the weight planes (Mp * Kd)
+    int32_t nimg, Co, Kd;
+    int32_t xblocks, wblocks;
     ConvGeom g;
 };
 
@@ -373,6 +396,7 @@ void build_gemm_nt_f32(const GemmParams& p, int batch, LaunchRec* rec);
 // int8 limb routes for large problems: limb-plane encoders + direct-to-LDS NT GEMM.
 void i8nt_tile_shape(int32_t route, int64_t M, int64_t N, int64_t batch, int* bm, int* bn);
 void build_enc_limb(int32_t route, bool s24, const EncPairParams& p, LaunchRec* rec);
+void build_conv_prep_limb(const ConvLimbPrepParams& p, LaunchRec* rec);
 bool build_gemm_i8nt(int32_t route, const GemmParams& p, int batch, LaunchRec* rec);
 
 }  // namespace qx

@@ -99,12 +99,18 @@ def test_conv_f32_i32_plans():
     with pytest.raises(qx.QxError) as e:
         qx.plan_conv2d_t("f32", 2, 32, 20, 20, 8, 3, 3, 1, 1, "f16_exact")
     assert e.value.status == qx.ERR_INVALID_ARG
-    # INT32 (smul24): large problems gather the im2col columns inside the
-    # limb-plane encoder (no column matrix), then the NT int8 contraction;
-    # small ones lower explicitly and run the register-staged smul24 GEMM
+    # INT32 (smul24): large problems with C_in a multiple of 64 write the
+    # image once as bordered NHWC limb planes and the contraction gathers its
+    # column tiles from them (workspace about 3 bytes per bordered image
+    # element); other C_in gather the im2col columns inside the limb-plane
+    # encoder (3 bytes per column-matrix element); small ones lower
+    # explicitly and run the register-staged smul24 GEMM
     p = qx.plan_conv2d_t("i32", 8, 64, 56, 56, 128, 3, 3, 1, 1)
     assert p["route_name"] == "s24_i8limb" and p["kernels"] == 2
-    assert p["workspace_bytes"] < 4 * 576 * 8 * 56 * 56
+    assert p["workspace_bytes"] < 3 * 8 * 58 * 58 * 64 + 3 * 128 * 576 + 4 * 8 * 58 * 58 + 4 * 128 + 4096
+    p = qx.plan_conv2d_t("i32", 8, 48, 56, 56, 128, 3, 3, 1, 1)
+    assert p["route_name"] == "s24_i8limb" and p["kernels"] == 2
+    assert p["workspace_bytes"] > 3 * 432 * 8 * 56 * 56
     p = qx.plan_conv2d_t("i32", 1, 4, 8, 8, 40, 3, 3, 1, 1)
     assert p["route_name"] == "s24_i8limb" and p["kernels"] == 3   # im2col, sums, GEMM
     # few output channels: one direct vector-ALU kernel

@@ -638,6 +638,34 @@ def test_conv_t_oneshot_and_empty():
     assert z.shape == (1, 2, 4, 4) and float(z.abs().sum()) == 0.0
 
 
+@pytest.mark.parametrize("case", CONV_IMPLICIT_CASES)
+def test_conv_i32_implicit_lowering(case):
+    # INT32 conv with C_in a multiple of 64 on the int8 limb route: one
+    # launch writes the bordered NHWC limb planes (border = the limbs of 0),
+    # the per-chunk position sums and the (kh, kw, ci)-ordered weight planes;
+    # the contraction gathers its column tiles from the planes, so the
+    # workspace holds about the image, not the 9x larger column matrix.
+    # Strides 1-2, pads 0-3, 1x1 to 7x7 and rectangular kernels, 64-192
+    # channels, pixel tiles ending mid-row; bit-exact mod 2^32.
+    N, Ci, H, W, Co, KH, KW, s, p, _ = case
+    rng = np.random.default_rng(zlib.crc32(repr(("i32 implicit", case)).encode()))
+    x = rng.integers(-(1 << 31), (1 << 31) - 1, (N, Ci, H, W), dtype=np.int32, endpoint=True)
+    w = rng.integers(-(1 << 31), (1 << 31) - 1, (Co, Ci, KH, KW), dtype=np.int32, endpoint=True)
+    x[0, :, 0, :] = -(1 << 23)
+    x[-1, :, -1, :] = (1 << 23) - 1
+    w[0] = (1 << 23) - 1
+    w[-1] = -(1 << 23)
+    Ho, Wo = (H + 2 * p - KH) // s + 1, (W + 2 * p - KW) // s + 1
+    with qx.Executor.conv2d_t("i32", N, Ci, H, W, Co, KH, KW, s, p, "s24_i8limb") as ex:
+        plan = ex.plan()
+        assert plan["kernels"] == 2, plan
+        planes = 3 * N * (H + 2 * p) * (W + 2 * p) * Ci
+        assert plan["workspace_bytes"] < planes + 3 * (Co + 128) * KH * KW * Ci + 4 * N * (H + 2 * p) * (W + 2 * p) * Ci // 64 + 4 * Co + 4096, plan
+        y = run_exec(ex, (x, w))
+    assert y.shape == (N, Co, Ho, Wo)
+    same(y, orc.conv2d_s24(x, w, s, p), str(case))
+
+
 def test_workload_conv_t_full_oracle():
     wf = WORKLOADS["conv_f32_8x64x56x56_128_3x3"]
     x, w = wf.generate()
