@@ -215,6 +215,13 @@ bool use_i8nt(int32_t route, int64_t M, int64_t N, int64_t K, int64_t batch) {
 
 void add_fill_out(Plan* pl, int64_t n32);
 
+// The skinny smul24 kernel (one row per thread, eight columns per
+// workgroup) takes GEMMs of at most 128 columns with at least 1024 rows over
+// the batch, enough workgroups to occupy the chip, and K up to 4096.
+static bool skinny_s24(const GemmSpec& s) {
+    return s.s24 && s.N <= 128 && s.M * s.batch >= 1024 && s.K <= 4096;
+}
+
 // Appends the launches of one integer GEMM; ws_used is the workspace end.
 qx_status plan_int_gemm(const GemmSpec& s, Plan* pl, uint64_t* ws_used) {
     int32_t route = s.route;
@@ -226,7 +233,17 @@ qx_status plan_int_gemm(const GemmSpec& s, Plan* pl, uint64_t* ws_used) {
             return fail(QX_ERR_RANGE, "route %d cannot be exact for bounds %lld x %lld", route,
                         (long long)s.ba, (long long)s.bb);
     } else {
-        if (route == R_AUTO) route = R_S24_I8LIMB;
+        // Few output columns, many rows and at most 2^26 multiply-adds (the
+        // last two fully connected layers of a LeNet-shaped network): the
+        // skinny vector-ALU kernel, one launch without encoders or sums.
+        // Through the limb planes / skinny kernel: 4096 x 10 x 84 18.1 /
+        // 5.2 us, 4096 x 84 x 120 11.7 / 7.1, 4096 x 64 x 120 11.5 / 8.9;
+        // larger ones favour the matrix cores: 4096 x 120 x 400 16.6 /
+        // 16.7, 16384 x 128 x 512 35.6 / 73.9.
+        if (route == R_AUTO) {
+            const double macs = (double)s.M * (double)s.N * (double)s.K * (double)s.batch;
+            route = (skinny_s24(s) && macs <= (double)(1 << 26) && !s.b_conv) ? R_S24_VALU : R_S24_I8LIMB;
+        }
         if (route != R_S24_I8LIMB && route != R_S24_VALU)
             return fail(QX_ERR_INVALID_ARG, "route %d does not apply to the smul24 GEMM", route);
     }
@@ -249,12 +266,15 @@ qx_status plan_int_gemm(const GemmSpec& s, Plan* pl, uint64_t* ws_used) {
         v.lda = (int32_t)s.lda; v.ldb = (int32_t)s.ldb; v.ldc = (int32_t)s.ldc;
         v.b_trans = 0; v.out_mode = s.out_mode; v.hw = s.hw;
         LaunchRec rec;
-        build_valu_gemm(route == R_VALU_DOT2 ? VK_I16_DOT2 : VK_S24, v, (int)s.batch, &rec);
+        const bool skinny = route == R_S24_VALU && skinny_s24(s);
+        if (skinny) build_valu_skinny_s24(v, (int)s.batch, &rec);
+        else build_valu_gemm(route == R_VALU_DOT2 ? VK_I16_DOT2 : VK_S24, v, (int)s.batch, &rec);
         rec.bind(offsetof(ValuGemmParams, A), s.a_bind);
         rec.bind(offsetof(ValuGemmParams, B), s.b_bind, s.b_ws_off);
         rec.bind(offsetof(ValuGemmParams, C), BIND_OUT);
         pl->launches.push_back(rec);
-        info.tile_m = 64; info.tile_n = 64; info.tile_k = 16;
+        if (skinny) { info.tile_m = 64; info.tile_n = 8; info.tile_k = 32; }
+        else { info.tile_m = 64; info.tile_n = 64; info.tile_k = 16; }
         return QX_OK;
     }
 
@@ -1088,11 +1108,18 @@ qx_status plan_lenet(Plan* pl, int64_t B) {
         pl->launches.push_back(r);
         if (!fuse) pool(y, to, Co, Ho);
     };
-    // ReLU after a fully connected layer: folded into the int8 NT
-    // contraction's stores when that is the layer's last launch (and K is
-    // not sliced), else a launch of its own
+    // ReLU after a fully connected layer: folded into the stores of the
+    // layer's last launch when that is the int8 NT contraction (K not
+    // sliced) or the skinny vector-ALU kernel, else a launch of its own
     auto relu = [&](uint64_t at, int64_t n) {
         LaunchRec& last = pl->launches.back();
+        if (strcmp(last.name, "valu_s24_skinny") == 0) {
+            ValuGemmParams vp;
+            memcpy(&vp, last.blob, sizeof(vp));
+            vp.relu = 1;
+            memcpy(last.blob, &vp, sizeof(vp));
+            return;
+        }
         if (strncmp(last.name, "gemm_i8nt_", 10) == 0) {
             GemmParams gp;
             memcpy(&gp, last.blob, sizeof(gp));

@@ -291,6 +291,7 @@ struct ValuGemmParams {
     int32_t b_trans;
     int32_t out_mode;
     int32_t hw;
+    int32_t relu;           // skinny smul24 kernel only: max(c, 0) on store
 };
 
 // ---------------------------------------------------------------------------
@@ -362,6 +363,7 @@ void build_sums(const SumsParams& p, LaunchRec* rec);
 int sums_slices(int K);
 void build_im2col(const Im2colParams& p, LaunchRec* rec);
 void build_valu_gemm(int32_t kind, const ValuGemmParams& p, int batch, LaunchRec* rec);
+void build_valu_skinny_s24(const ValuGemmParams& p, int batch, LaunchRec* rec);   // N of a few tens
 bool build_attn_f32(const AttnParams& p, LaunchRec* rec);
 bool build_attn_i32(const AttnParams& p, LaunchRec* rec);
 // INT32 attention with resident key splits: applicable for d in {32, 64, 128}

@@ -34,6 +34,17 @@ def test_auto_routes_for_the_workloads():
     p = qx.plan_gemm_i32_s24(1024, 1024, 1024, 1)
     assert p["route_name"] == "s24_i8limb" and p["products"] == 8 and p["exact_no_wrap"] == 0
     assert p["workspace_bytes"] >= 4 * 2048
+    # few columns, many rows, at most 2^26 multiply-adds: one skinny
+    # vector-ALU launch, no workspace
+    for M, N, K in ((4096, 84, 120), (4096, 10, 84), (4096, 64, 120)):
+        p = qx.plan_gemm_i32_s24(M, N, K, 1)
+        assert p["route_name"] == "s24_valu" and p["kernels"] == 1 and p["workspace_bytes"] == 0, p
+        assert (p["tile_m"], p["tile_n"]) == (64, 8)
+    # more work (or few rows) keeps the matrix cores
+    assert qx.plan_gemm_i32_s24(4096, 120, 400, 1)["route_name"] == "s24_i8limb"
+    assert qx.plan_gemm_i32_s24(64, 64, 8448, 1)["route_name"] == "s24_i8limb"
+    # the vector-ALU route asked for by name takes the skinny kernel too
+    assert qx.plan_gemm_i32_s24(4096, 120, 400, 1, "s24_valu")["tile_n"] == 8
     d = w["conv_8x64x56x56_128_3x3"].dims
     p = qx.plan_conv2d(d["N"], d["Ci"], d["H"], d["W"], d["Co"], d["KH"], d["KW"], 1, 1, 256, 256)
     # one launch writes the bordered NHWC fp16 image and the fp16 weights,
@@ -130,11 +141,12 @@ def test_lenet_plan_chains_the_operators():
     # conv1: one direct launch with ReLU and the 2x2 average fused (its
     # 4096 x 14 x 14 pooled pixels give every SIMD four waves; only the pooled
     # map reaches the workspace); conv2 (4096 x 5 x 5 pooled pixels) keeps
-    # conv and pool apart; then 3 FC GEMMs with their limb encoders or sums,
-    # the first two storing through their ReLU (int8 NT contractions without
-    # K slices).  A small batch fuses none of these: 2 pools and 2 ReLU
-    # launches more.
-    assert p["kernels"] == 9, p
+    # conv and pool apart; then 3 FC GEMMs: the first through its limb
+    # encoder and the int8 contraction, the other two one skinny vector-ALU
+    # launch each; the first two store through their ReLU.  A small batch
+    # fuses none of these and runs every FC layer through the limb planes:
+    # 2 pools, 2 encoders or sums and 2 ReLU launches more.
+    assert p["kernels"] == 7, p
     assert qx.plan_lenet_i32(7)["kernels"] == 12
     assert 4 * 4096 * (6 * 14 * 14 + 400) <= p["workspace_bytes"] < 4 * 4096 * 6 * 28 * 28
     assert qx.plan_lenet_i32(0)["kernels"] == 0

@@ -280,6 +280,32 @@ def test_gemm_s24_extremes_and_accumulator_wrap(route):
     same(got, orc.gemm_i32_s24(A, B))
 
 
+SKINNY_S24_SHAPES = [  # M, N, K, batch: at most 128 columns, at least 1024 rows over the batch
+    (4096, 120, 400, 1), (4096, 10, 84, 1), (1100, 84, 120, 1), (1030, 127, 37, 2),
+    (2000, 9, 130, 1), (1500, 128, 1, 1), (1024, 128, 4096, 1), (600, 65, 64, 3),
+]
+
+
+@pytest.mark.parametrize("route", ["auto", "s24_valu"])
+@pytest.mark.parametrize("shape", SKINNY_S24_SHAPES)
+def test_gemm_s24_skinny(route, shape):
+    # One row per thread, eight columns per workgroup: ragged rows (M not a
+    # multiple of 256), ragged column groups, K not a multiple of 4 (the
+    # element-wise A loads) or of 64 (a short last B stage), batches.
+    M, N, K, batch = shape
+    rng = np.random.default_rng(zlib.crc32(repr(("skinny", shape)).encode()))
+    A = rng.integers(-(1 << 31), (1 << 31) - 1, (batch, M, K), dtype=np.int32, endpoint=True)
+    B = rng.integers(-(1 << 31), (1 << 31) - 1, (batch, K, N), dtype=np.int32, endpoint=True)
+    A[0, 0, :] = -(1 << 23)
+    B[0, :, 0] = -(1 << 23)
+    with qx.Executor.gemm_i32_s24(M, N, K, batch, route) as ex:
+        plan = ex.plan()
+        if route == "s24_valu" or M * N * K * batch <= 1 << 26:
+            assert plan["route_name"] == "s24_valu" and plan["tile_n"] == 8, plan
+        got = run_exec(ex, (A, B))
+    same(got, orc.gemm_i32_s24(A, B), str(shape))
+
+
 # ---------------------------------------------------------------------------
 # Conv2D
 # ---------------------------------------------------------------------------
