@@ -152,8 +152,16 @@ __global__ __launch_bounds__(VT) void k_valu_skinny_s24(const ValuGemmParams p) 
     __shared__ __align__(16) int32_t As[NWV][WR][AP];
     const int lane = threadIdx.x & 63;
     const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-    const int m0 = blockIdx.x * WR, m = m0 + lane;
-    const int n0g = blockIdx.y * NG;
+    // Workgroups (row block, column group), column groups fastest.  The
+    // dispatcher deals consecutive workgroups to the eight XCDs in turn;
+    // when their count is a multiple of 8, XCD x is given the x-th eighth of
+    // them instead, whole row blocks with all their column groups, so that
+    // a block of A is fetched into that XCD's L2 once, not once per group.
+    const int groups = (p.N + NG - 1) / NG, nwg = gridDim.x;
+    int lin = blockIdx.x;
+    if ((nwg & 7) == 0) lin = (lin & 7) * (nwg >> 3) + (lin >> 3);
+    const int m0 = (lin / groups) * WR, m = m0 + lane;
+    const int n0g = (lin % groups) * NG;
     // The last column group moves left to end at column N - 1 (it overlaps
     // the previous group and stores only its own columns), so every scalar
     // load of B reads NG contiguous words inside the matrix (N >= NG).
@@ -191,11 +199,18 @@ __global__ __launch_bounds__(VT) void k_valu_skinny_s24(const ValuGemmParams p) 
         __builtin_amdgcn_wave_barrier();
         __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
     };
-    auto load_b = [&](int k, int32_t* r) {
-        const cptr row = B + (int64_t)k * p.ldb;
+    // B rows are addressed by a 32-bit byte offset from B (K x ldb words
+    // of B, K <= 4096 and ldb <= 2^17: under 2^31 bytes), stepped by one row
+    // per load, which keeps the scalar address arithmetic to one add per row
+    typedef const __attribute__((address_space(4))) char* cbptr;
+    const cbptr Bb = (cbptr)B;
+    const uint32_t row_bytes = 4u * (uint32_t)p.ldb;
+    auto load_b_at = [&](uint32_t off, int32_t* r) {
+        const cptr row = (cptr)(Bb + off);
 #pragma unroll
         for (int j = 0; j < NG; ++j) r[j] = row[j];
     };
+    auto load_b = [&](int k, int32_t* r) { load_b_at((uint32_t)k * row_bytes, r); };
     uint32_t acc[NG];
 #pragma unroll
     for (int j = 0; j < NG; ++j) acc[j] = 0u;
@@ -210,11 +225,15 @@ __global__ __launch_bounds__(VT) void k_valu_skinny_s24(const ValuGemmParams p) 
             // whole chunk, four k at a time: one wait covers the scalar
             // loads of four B rows (scalar loads return out of order, so
             // any wait for one of them waits for all)
+            uint32_t boff = (uint32_t)k0 * row_bytes;
 #pragma unroll
             for (int q = 0; q < KC / 4; ++q) {
                 int32_t bq[4][NG];
 #pragma unroll
-                for (int e = 0; e < 4; ++e) load_b(k0 + 4 * q + e, bq[e]);
+                for (int e = 0; e < 4; ++e) {
+                    load_b_at(boff, bq[e]);
+                    boff += row_bytes;
+                }
                 const i4v a4 = *(const i4v*)&as[lane][4 * q];
 #pragma unroll
                 for (int e = 0; e < 4; ++e)
@@ -262,7 +281,7 @@ void build_valu_skinny_s24(const ValuGemmParams& p, int batch, LaunchRec* rec) {
     rec->fn = ng == 8 ? (const void*)k_valu_skinny_s24<8> : ng == 4 ? (const void*)k_valu_skinny_s24<4>
             : ng == 2 ? (const void*)k_valu_skinny_s24<2> : (const void*)k_valu_skinny_s24<1>;
     rec->name = "valu_s24_skinny";
-    rec->grid = dim3((unsigned)((p.M + 63) / 64), (unsigned)((p.N + ng - 1) / ng), (unsigned)batch);
+    rec->grid = dim3((unsigned)(((p.M + 63) / 64) * ((p.N + ng - 1) / ng)), 1u, (unsigned)batch);
     rec->block = dim3(VT, 1, 1);
     rec->set_params(p);
 }
