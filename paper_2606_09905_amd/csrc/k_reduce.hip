@@ -186,7 +186,7 @@ constexpr int DKW = 8;   // KW limit; C_out <= 16 and C_in*KH*KW <= 1024 (64 KB 
 // and first copies their inputs into LDS with coalesced loads, so the
 // window reads (scattered across rows and cache lines) come from LDS;
 // otherwise the windows are read from global memory.
-template <int DCO, int KWT, int PXT, bool STAGE>
+template <int DCO, int KWT, int PXT, bool STAGE, bool S1P0>
 __global__ __launch_bounds__(RT) void k_conv_direct_s24(const ConvDirectParams p) {
     // LDS: weights [Kd][DCO], zero past C_out, then (STAGE) the inputs of
     // this workgroup's images [imgs][Ci][H][W]
@@ -238,19 +238,33 @@ __global__ __launch_bounds__(RT) void k_conv_direct_s24(const ConvDirectParams p
     int k = 0;
     for (int ci = 0; ci < g.Ci; ++ci)
         for (int kh = 0; kh < g.KH; ++kh, k += g.KW) {
-            const int ih = oh * g.stride - g.pad + kh;
-            const bool rin = ih >= 0 && ih < g.H;
-            const int32_t* xr = xb + ((int64_t)ci * g.H + ih) * g.W;
             // the inputs of this kernel row for all PXT pixels first
             // (independent loads), then every tap and output channel
             int32_t xv[PXT][KWT];
+            if constexpr (S1P0) {
+                // stride 1, no padding: every window lies inside the image
+                // and neighbouring pixels share PXT + KW - 2 of their inputs
+                const int32_t* xr = xb + ((int64_t)ci * g.H + oh + kh) * g.W + ow0;
+                int32_t xrow[PXT + KWT - 1];
 #pragma unroll
-            for (int j = 0; j < PXT; ++j)
+                for (int i = 0; i < PXT + KWT - 1; ++i)
+                    xrow[i] = (KWT != DKW || i < PXT + g.KW - 1) ? xr[i] : 0;
 #pragma unroll
-                for (int kw = 0; kw < KWT; ++kw) {
-                    const int iw = (ow0 + j) * g.stride - g.pad + kw;
-                    xv[j][kw] = (kw < g.KW && rin && iw >= 0 && iw < g.W) ? xr[iw] : 0;
-                }
+                for (int j = 0; j < PXT; ++j)
+#pragma unroll
+                    for (int kw = 0; kw < KWT; ++kw) xv[j][kw] = (KWT != DKW || kw < g.KW) ? xrow[j + kw] : 0;
+            } else {
+                const int ih = oh * g.stride - g.pad + kh;
+                const bool rin = ih >= 0 && ih < g.H;
+                const int32_t* xr = xb + ((int64_t)ci * g.H + ih) * g.W;
+#pragma unroll
+                for (int j = 0; j < PXT; ++j)
+#pragma unroll
+                    for (int kw = 0; kw < KWT; ++kw) {
+                        const int iw = (ow0 + j) * g.stride - g.pad + kw;
+                        xv[j][kw] = (kw < g.KW && rin && iw >= 0 && iw < g.W) ? xr[iw] : 0;
+                    }
+            }
 #pragma unroll
             for (int kw = 0; kw < KWT; ++kw) {
                 // DCO weights as 16-byte LDS reads (rows of DCO ints from a
@@ -285,7 +299,7 @@ __global__ __launch_bounds__(RT) void k_conv_direct_s24(const ConvDirectParams p
 // relu(b) + relu(c) + relu(d)) / 4) summed in 64 bits, the pool kernel's
 // arithmetic.  Ho and Wo even; the output is [N][C_out][Ho/2][Wo/2].  A
 // workgroup takes p.imgs whole images, staged in LDS as above.
-template <int DCO, int KWT>
+template <int DCO, int KWT, bool S1P0>
 __global__ __launch_bounds__(RT) void k_conv_pool_s24(const ConvDirectParams p) {
     extern __shared__ __align__(16) int32_t wsh[];
     int32_t(*ws)[DCO] = (int32_t(*)[DCO])wsh;
@@ -324,16 +338,30 @@ __global__ __launch_bounds__(RT) void k_conv_pool_s24(const ConvDirectParams p) 
             int32_t xv[4][KWT];
 #pragma unroll
             for (int dy = 0; dy < 2; ++dy) {
-                const int ih = (oh0 + dy) * g.stride - g.pad + kh;
-                const bool rin = ih >= 0 && ih < g.H;
-                const int32_t* xr = xb + ((int64_t)ci * g.H + ih) * g.W;
+                if constexpr (S1P0) {
+                    // stride 1, no padding: the two pixels of a row share
+                    // KW - 1 of their inputs, all inside the image
+                    const int32_t* xr = xb + ((int64_t)ci * g.H + oh0 + dy + kh) * g.W + ow0;
+                    int32_t xrow[KWT + 1];
 #pragma unroll
-                for (int dx = 0; dx < 2; ++dx)
+                    for (int i = 0; i < KWT + 1; ++i) xrow[i] = (KWT != DKW || i < g.KW + 1) ? xr[i] : 0;
 #pragma unroll
-                    for (int kw = 0; kw < KWT; ++kw) {
-                        const int iw = (ow0 + dx) * g.stride - g.pad + kw;
-                        xv[2 * dy + dx][kw] = (kw < g.KW && rin && iw >= 0 && iw < g.W) ? xr[iw] : 0;
-                    }
+                    for (int dx = 0; dx < 2; ++dx)
+#pragma unroll
+                        for (int kw = 0; kw < KWT; ++kw)
+                            xv[2 * dy + dx][kw] = (KWT != DKW || kw < g.KW) ? xrow[dx + kw] : 0;
+                } else {
+                    const int ih = (oh0 + dy) * g.stride - g.pad + kh;
+                    const bool rin = ih >= 0 && ih < g.H;
+                    const int32_t* xr = xb + ((int64_t)ci * g.H + ih) * g.W;
+#pragma unroll
+                    for (int dx = 0; dx < 2; ++dx)
+#pragma unroll
+                        for (int kw = 0; kw < KWT; ++kw) {
+                            const int iw = (ow0 + dx) * g.stride - g.pad + kw;
+                            xv[2 * dy + dx][kw] = (kw < g.KW && rin && iw >= 0 && iw < g.W) ? xr[iw] : 0;
+                        }
+                }
             }
 #pragma unroll
             for (int kw = 0; kw < KWT; ++kw) {
@@ -407,10 +435,12 @@ void build_conv_direct_s24(const ConvDirectParams& p0, LaunchRec* rec) {
         const int64_t hwq = (int64_t)(p.g.Ho / 2) * (p.g.Wo / 2);
         const int64_t chw = (int64_t)p.g.Ci * p.g.H * p.g.W;
         p.imgs = conv_pool_images(p);
-#define QX_CP(DCO) (kw == 5 ? (const void*)k_conv_pool_s24<DCO, 5> \
-                    : kw == 3 ? (const void*)k_conv_pool_s24<DCO, 3> : (const void*)k_conv_pool_s24<DCO, DKW>)
+        const bool s1p0 = p.g.stride == 1 && p.g.pad == 0;
+#define QX_CP2(DCO, KWT) (s1p0 ? (const void*)k_conv_pool_s24<DCO, KWT, true> : (const void*)k_conv_pool_s24<DCO, KWT, false>)
+#define QX_CP(DCO) (kw == 5 ? QX_CP2(DCO, 5) : kw == 3 ? QX_CP2(DCO, 3) : QX_CP2(DCO, DKW))
         rec->fn = p.Co <= 8 ? QX_CP(8) : QX_CP(16);
 #undef QX_CP
+#undef QX_CP2
         const int64_t blocks = (p.P / 4 / hwq + p.imgs - 1) / p.imgs;
         rec->grid = dim3((unsigned)std::max<int64_t>(blocks, 1), 1, 1);
         rec->block = dim3(RT, 1, 1);
@@ -431,14 +461,17 @@ void build_conv_direct_s24(const ConvDirectParams& p0, LaunchRec* rec) {
     const int64_t imgs = std::min<int64_t>(by_threads, by_lds);
     const bool stage = imgs >= 1 && p.P > 0;
     p.imgs = stage ? (int32_t)imgs : 0;
-#define QX_DC4(DCO, KWT, PX) (stage ? (const void*)k_conv_direct_s24<DCO, KWT, PX, true> \
-                                    : (const void*)k_conv_direct_s24<DCO, KWT, PX, false>)
+    const bool s1p0 = p.g.stride == 1 && p.g.pad == 0;
+#define QX_DC5(DCO, KWT, PX, ST) (s1p0 ? (const void*)k_conv_direct_s24<DCO, KWT, PX, ST, true> \
+                                       : (const void*)k_conv_direct_s24<DCO, KWT, PX, ST, false>)
+#define QX_DC4(DCO, KWT, PX) (stage ? QX_DC5(DCO, KWT, PX, true) : QX_DC5(DCO, KWT, PX, false))
 #define QX_DC3(DCO, KWT) (pxt == 4 ? QX_DC4(DCO, KWT, 4) : pxt == 2 ? QX_DC4(DCO, KWT, 2) : QX_DC4(DCO, KWT, 1))
 #define QX_DC(DCO) (kw == 5 ? QX_DC3(DCO, 5) : kw == 3 ? QX_DC3(DCO, 3) : QX_DC3(DCO, DKW))
     rec->fn = p.Co <= 8 ? QX_DC(8) : QX_DC(16);
 #undef QX_DC
 #undef QX_DC3
 #undef QX_DC4
+#undef QX_DC5
     int64_t blocks;
     if (stage) {
         const int64_t nimg = p.P / hw;

@@ -629,14 +629,19 @@ def test_conv_f32(case):
 @pytest.mark.parametrize("case", CONV_T_CASES[:5] + [(8, 64, 20, 20, 96, 3, 3, 1, 1), (3, 6, 14, 14, 16, 5, 5, 1, 0),
                                                      (2, 5, 11, 9, 3, 3, 2, 2, 1), (2, 150, 6, 6, 16, 1, 1, 1, 0),
                                                      (7, 6, 14, 14, 16, 5, 5, 1, 0), (1, 16, 40, 40, 4, 3, 3, 1, 0),
-                                                     (2, 3, 70, 70, 6, 5, 5, 2, 2)])
+                                                     (2, 3, 70, 70, 6, 5, 5, 2, 2), (2, 3, 12, 12, 8, 5, 5, 1, 0),
+                                                     (3, 4, 9, 10, 5, 4, 4, 1, 0), (2, 2, 8, 14, 16, 2, 7, 1, 0),
+                                                     (1, 3, 50, 50, 6, 3, 3, 1, 0), (2, 2, 9, 9, 3, 3, 3, 1, 0)])
 def test_conv_i32_smul24(route, case):
     # INT32 conv under the smul24 contract: full 32-bit words (bits 24..31
     # ignored), bit-exact mod 2^32 against the oracle.  On the vector-ALU
     # route the direct kernel stages whole images in LDS when they fit
     # (7 images of 14x14x6 in groups of 5 leave a partial group) and reads
     # the windows from global memory when an image has more output pixels
-    # than a workgroup's threads cover (40x40 and 70x70 inputs).
+    # than a workgroup's threads cover (40x40, 50x50 and 70x70 inputs).
+    # Stride 1 without padding takes unguarded window reads shared between
+    # a thread's pixels: 4, 2 and 1 pixels per thread, kernel widths 3 and 5
+    # and the generic width path (1, 4, 7).
     N, Ci, H, W, Co, KH, KW, s, p = case
     rng = np.random.default_rng(zlib.crc32(repr(("i32", route, case)).encode()))
     x = rng.integers(-(1 << 31), (1 << 31) - 1, (N, Ci, H, W), dtype=np.int32, endpoint=True)
