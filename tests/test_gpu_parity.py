@@ -283,6 +283,9 @@ def test_gemm_s24_extremes_and_accumulator_wrap(route):
 SKINNY_S24_SHAPES = [  # M, N, K, batch: at most 128 columns, at least 1024 rows over the batch
     (4096, 120, 400, 1), (4096, 10, 84, 1), (1100, 84, 120, 1), (1030, 127, 37, 2),
     (2000, 9, 130, 1), (1500, 128, 1, 1), (1024, 128, 4096, 1), (600, 65, 64, 3),
+    # fewer than 8 columns: 4, 2 or 1 column per workgroup, the last group
+    # shifted left over the previous one
+    (1500, 7, 37, 1), (1100, 5, 64, 2), (1024, 3, 100, 1), (1030, 2, 33, 1), (2048, 1, 96, 1),
 ]
 
 
