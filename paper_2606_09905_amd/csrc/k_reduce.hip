@@ -299,7 +299,7 @@ __global__ __launch_bounds__(RT) void k_conv_direct_s24(const ConvDirectParams p
 // relu(b) + relu(c) + relu(d)) / 4) summed in 64 bits, the pool kernel's
 // arithmetic.  Ho and Wo even; the output is [N][C_out][Ho/2][Wo/2].  A
 // workgroup takes p.imgs whole images, staged in LDS as above.
-template <int DCO, int KWT, bool S1P0>
+template <int DCO, int KWT, bool S1P0, int DCU>
 __global__ __launch_bounds__(RT) void k_conv_pool_s24(const ConvDirectParams p) {
     extern __shared__ __align__(16) int32_t wsh[];
     int32_t(*ws)[DCO] = (int32_t(*)[DCO])wsh;
@@ -327,11 +327,14 @@ __global__ __launch_bounds__(RT) void k_conv_pool_s24(const ConvDirectParams p) 
     __syncthreads();
     const int qh = remq / Wq, qw = remq - qh * Wq;
     const int oh0 = 2 * qh, ow0 = 2 * qw;
-    uint32_t acc[4][DCO];
+    // DCU: output channels computed (C_out <= DCU <= DCO; the LDS weight
+    // rows stay DCO wide)
+    static_assert(DCU <= DCO, "computed channels fit the weight rows");
+    uint32_t acc[4][DCU];
 #pragma unroll
     for (int j = 0; j < 4; ++j)
 #pragma unroll
-        for (int c = 0; c < DCO; ++c) acc[j][c] = 0u;
+        for (int c = 0; c < DCU; ++c) acc[j][c] = 0u;
     int k = 0;
     for (int ci = 0; ci < g.Ci; ++ci)
         for (int kh = 0; kh < g.KH; ++kh, k += g.KW) {
@@ -368,7 +371,7 @@ __global__ __launch_bounds__(RT) void k_conv_pool_s24(const ConvDirectParams p) 
                 const i4v* wk = (const i4v*)ws[k + (KWT == DKW ? min(kw, g.KW - 1) : kw)];
                 int32_t wv[DCO];
 #pragma unroll
-                for (int c4 = 0; c4 < DCO / 4; ++c4) {
+                for (int c4 = 0; c4 < (DCU + 3) / 4; ++c4) {
                     const i4v w4 = wk[c4];
 #pragma unroll
                     for (int e = 0; e < 4; ++e) wv[4 * c4 + e] = w4[e];
@@ -376,12 +379,12 @@ __global__ __launch_bounds__(RT) void k_conv_pool_s24(const ConvDirectParams p) 
 #pragma unroll
                 for (int j = 0; j < 4; ++j)
 #pragma unroll
-                    for (int c = 0; c < DCO; ++c) acc[j][c] += (uint32_t)__mul24(xv[j][kw], wv[c]);
+                    for (int c = 0; c < DCU; ++c) acc[j][c] += (uint32_t)__mul24(xv[j][kw], wv[c]);
             }
         }
     if (live)
 #pragma unroll
-        for (int c = 0; c < DCO; ++c)
+        for (int c = 0; c < DCU; ++c)
             if (c < p.Co) {
                 int64_t sum = 0;
 #pragma unroll
@@ -436,11 +439,16 @@ void build_conv_direct_s24(const ConvDirectParams& p0, LaunchRec* rec) {
         const int64_t chw = (int64_t)p.g.Ci * p.g.H * p.g.W;
         p.imgs = conv_pool_images(p);
         const bool s1p0 = p.g.stride == 1 && p.g.pad == 0;
-#define QX_CP2(DCO, KWT) (s1p0 ? (const void*)k_conv_pool_s24<DCO, KWT, true> : (const void*)k_conv_pool_s24<DCO, KWT, false>)
+        // channels computed: C_out rounded up to 4, 6, 8 or 16
+#define QX_CP3(DCO, KWT, DCU) (s1p0 ? (const void*)k_conv_pool_s24<DCO, KWT, true, DCU> \
+                                    : (const void*)k_conv_pool_s24<DCO, KWT, false, DCU>)
+#define QX_CP2(DCO, KWT) (DCO == 16 ? QX_CP3(DCO, KWT, DCO) : p.Co <= 4 ? QX_CP3(DCO, KWT, 4) \
+                          : p.Co <= 6 ? QX_CP3(DCO, KWT, 6) : QX_CP3(DCO, KWT, DCO))
 #define QX_CP(DCO) (kw == 5 ? QX_CP2(DCO, 5) : kw == 3 ? QX_CP2(DCO, 3) : QX_CP2(DCO, DKW))
         rec->fn = p.Co <= 8 ? QX_CP(8) : QX_CP(16);
 #undef QX_CP
 #undef QX_CP2
+#undef QX_CP3
         const int64_t blocks = (p.P / 4 / hwq + p.imgs - 1) / p.imgs;
         rec->grid = dim3((unsigned)std::max<int64_t>(blocks, 1), 1, 1);
         rec->block = dim3(RT, 1, 1);
