@@ -178,6 +178,65 @@ __global__ __launch_bounds__(RT) void k_relu_i32(const ReluParams p) {
 // ---------------------------------------------------------------------------
 constexpr int DKW = 8;   // KW limit; C_out <= 16 and C_in*KH*KW <= 1024 (64 KB of LDS)
 
+// The workgroup copies n int32 from global memory into LDS with several
+// loads in flight per thread before any wait (16-byte loads when both
+// sides are 16-byte aligned): a loop of single loads each waited for costs
+// one memory latency per element a thread copies.
+__device__ __forceinline__ void copy_to_lds(int32_t* dst, const int32_t* src, int n) {
+    int done = 0;
+    if ((((uintptr_t)src | (uintptr_t)dst) & 15) == 0) {
+        const int n4 = n >> 2;
+        const i4v* s4 = (const i4v*)src;
+        i4v* d4 = (i4v*)dst;
+        for (int i0 = (int)threadIdx.x; i0 < n4; i0 += RT * 4) {
+            i4v v[4];
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                const int i = i0 + u * RT;
+                v[u] = i < n4 ? s4[i] : i4v{0, 0, 0, 0};
+            }
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                const int i = i0 + u * RT;
+                if (i < n4) d4[i] = v[u];
+            }
+        }
+        done = 4 * n4;
+    }
+    for (int i0 = done + (int)threadIdx.x; i0 < n; i0 += RT * 8) {
+        int32_t v[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+            const int i = i0 + u * RT;
+            v[u] = i < n ? src[i] : 0;
+        }
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+            const int i = i0 + u * RT;
+            if (i < n) dst[i] = v[u];
+        }
+    }
+}
+
+// Weights [C_out][Kd] -> LDS [Kd][DCO] (zero past C_out), eight loads in
+// flight per thread.
+template <int DCO>
+__device__ __forceinline__ void stage_weights(int32_t (*ws)[DCO], const int32_t* w, int Co, int Kd) {
+    for (int i0 = (int)threadIdx.x; i0 < Kd * DCO; i0 += RT * 8) {
+        int32_t v[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+            const int i = i0 + u * RT, k = i / DCO, c = i % DCO;
+            v[u] = (i < Kd * DCO && c < Co) ? w[(int64_t)c * Kd + k] : 0;
+        }
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+            const int i = i0 + u * RT;
+            if (i < Kd * DCO) ws[i / DCO][i % DCO] = v[u];
+        }
+    }
+}
+
 // KWT: the kernel width when it is 3 or 5, else DKW for any KW <= DKW (the
 // taps past KW then multiply a zero input).  PXT: output pixels per thread,
 // consecutive along a row (Wo % PXT == 0): each weight read from LDS (a
@@ -187,16 +246,14 @@ constexpr int DKW = 8;   // KW limit; C_out <= 16 and C_in*KH*KW <= 1024 (64 KB 
 // window reads (scattered across rows and cache lines) come from LDS;
 // otherwise the windows are read from global memory.
 template <int DCO, int KWT, int PXT, bool STAGE, bool S1P0>
-__global__ __launch_bounds__(RT) void k_conv_direct_s24(const ConvDirectParams p) {
+__global__ __launch_bounds__(RT) __attribute__((amdgpu_waves_per_eu(1, 4)))
+void k_conv_direct_s24(const ConvDirectParams p) {
     // LDS: weights [Kd][DCO], zero past C_out, then (STAGE) the inputs of
     // this workgroup's images [imgs][Ci][H][W]
     extern __shared__ __align__(16) int32_t wsh[];
     int32_t(*ws)[DCO] = (int32_t(*)[DCO])wsh;
     const ConvGeom& g = p.g;
-    for (int i = threadIdx.x; i < p.Kd * DCO; i += RT) {
-        const int k = i / DCO, c = i % DCO;
-        ws[k][c] = c < p.Co ? p.w[(int64_t)c * p.Kd + k] : 0;
-    }
+    stage_weights<DCO>(ws, p.w, p.Co, p.Kd);
     const int hw = g.Ho * g.Wo;
     const int64_t groups = p.P / PXT;
     int64_t t;
@@ -209,8 +266,7 @@ __global__ __launch_bounds__(RT) void k_conv_direct_s24(const ConvDirectParams p
         const int img0 = (int)blockIdx.x * imgs, cnt = min(imgs, nimg - img0);
         const int chw = g.Ci * g.H * g.W;
         int32_t* xs = wsh + p.Kd * DCO;
-        const int32_t* src = p.x + (int64_t)img0 * chw;
-        for (int i = threadIdx.x; i < cnt * chw; i += RT) xs[i] = src[i];
+        copy_to_lds(xs, p.x + (int64_t)img0 * chw, cnt * chw);
         const int local = (int)threadIdx.x * PXT;             // pixel within the images
         live = local < cnt * hw;
         const int li = min(local, cnt * hw - PXT);
@@ -265,22 +321,45 @@ __global__ __launch_bounds__(RT) void k_conv_direct_s24(const ConvDirectParams p
                         xv[j][kw] = (kw < g.KW && rin && iw >= 0 && iw < g.W) ? xr[iw] : 0;
                     }
             }
+            if constexpr (S1P0 && KWT != DKW) {
+                // the whole kernel row's weights first (KWT x DCO / 4 reads
+                // in flight together), then its multiply-adds: one wait on
+                // LDS per row instead of one per tap
+                int32_t wr[KWT][DCO];
 #pragma unroll
-            for (int kw = 0; kw < KWT; ++kw) {
-                // DCO weights as 16-byte LDS reads (rows of DCO ints from a
-                // 16-byte aligned base)
-                const i4v* wk = (const i4v*)ws[k + (KWT == DKW ? min(kw, g.KW - 1) : kw)];
-                int32_t wv[DCO];
+                for (int kw = 0; kw < KWT; ++kw) {
+                    const i4v* wk = (const i4v*)ws[k + kw];
 #pragma unroll
-                for (int c4 = 0; c4 < DCO / 4; ++c4) {
-                    const i4v w4 = wk[c4];
+                    for (int c4 = 0; c4 < DCO / 4; ++c4) {
+                        const i4v w4 = wk[c4];
 #pragma unroll
-                    for (int e = 0; e < 4; ++e) wv[4 * c4 + e] = w4[e];
+                        for (int e = 0; e < 4; ++e) wr[kw][4 * c4 + e] = w4[e];
+                    }
                 }
 #pragma unroll
-                for (int j = 0; j < PXT; ++j)
+                for (int kw = 0; kw < KWT; ++kw)
 #pragma unroll
-                    for (int c = 0; c < DCO; ++c) acc[j][c] += (uint32_t)__mul24(xv[j][kw], wv[c]);
+                    for (int j = 0; j < PXT; ++j)
+#pragma unroll
+                        for (int c = 0; c < DCO; ++c) acc[j][c] += (uint32_t)__mul24(xv[j][kw], wr[kw][c]);
+            } else {
+#pragma unroll
+                for (int kw = 0; kw < KWT; ++kw) {
+                    // DCO weights as 16-byte LDS reads (rows of DCO ints from a
+                    // 16-byte aligned base)
+                    const i4v* wk = (const i4v*)ws[k + (KWT == DKW ? min(kw, g.KW - 1) : kw)];
+                    int32_t wv[DCO];
+#pragma unroll
+                    for (int c4 = 0; c4 < DCO / 4; ++c4) {
+                        const i4v w4 = wk[c4];
+#pragma unroll
+                        for (int e = 0; e < 4; ++e) wv[4 * c4 + e] = w4[e];
+                    }
+#pragma unroll
+                    for (int j = 0; j < PXT; ++j)
+#pragma unroll
+                        for (int c = 0; c < DCO; ++c) acc[j][c] += (uint32_t)__mul24(xv[j][kw], wv[c]);
+                }
             }
         }
     (void)t;
@@ -304,10 +383,7 @@ __global__ __launch_bounds__(RT) void k_conv_pool_s24(const ConvDirectParams p) 
     extern __shared__ __align__(16) int32_t wsh[];
     int32_t(*ws)[DCO] = (int32_t(*)[DCO])wsh;
     const ConvGeom& g = p.g;
-    for (int i = threadIdx.x; i < p.Kd * DCO; i += RT) {
-        const int k = i / DCO, c = i % DCO;
-        ws[k][c] = c < p.Co ? p.w[(int64_t)c * p.Kd + k] : 0;
-    }
+    stage_weights<DCO>(ws, p.w, p.Co, p.Kd);
     const int Wq = g.Wo / 2, hwq = (g.Ho / 2) * Wq;
     const int64_t pq = p.P / 4;   // pooled pixels
     // images [img0, img0 + cnt) of the batch; thread -> one pooled pixel
@@ -315,8 +391,7 @@ __global__ __launch_bounds__(RT) void k_conv_pool_s24(const ConvDirectParams p) 
     const int img0 = (int)blockIdx.x * imgs, cnt = min(imgs, nimg - img0);
     const int chw = g.Ci * g.H * g.W;
     int32_t* xs = wsh + p.Kd * DCO;
-    const int32_t* src = p.x + (int64_t)img0 * chw;
-    for (int i = threadIdx.x; i < cnt * chw; i += RT) xs[i] = src[i];
+    copy_to_lds(xs, p.x + (int64_t)img0 * chw, cnt * chw);
     const int local = (int)threadIdx.x;
     const bool live = local < cnt * hwq;
     const int li = min(local, cnt * hwq - 1);
@@ -366,21 +441,24 @@ __global__ __launch_bounds__(RT) void k_conv_pool_s24(const ConvDirectParams p) 
                         }
                 }
             }
+            // the kernel row's weights first, all reads in flight together
+            int32_t wr[KWT][DCO];
 #pragma unroll
             for (int kw = 0; kw < KWT; ++kw) {
                 const i4v* wk = (const i4v*)ws[k + (KWT == DKW ? min(kw, g.KW - 1) : kw)];
-                int32_t wv[DCO];
 #pragma unroll
                 for (int c4 = 0; c4 < (DCU + 3) / 4; ++c4) {
                     const i4v w4 = wk[c4];
 #pragma unroll
-                    for (int e = 0; e < 4; ++e) wv[4 * c4 + e] = w4[e];
+                    for (int e = 0; e < 4; ++e) wr[kw][4 * c4 + e] = w4[e];
                 }
+            }
+#pragma unroll
+            for (int kw = 0; kw < KWT; ++kw)
 #pragma unroll
                 for (int j = 0; j < 4; ++j)
 #pragma unroll
-                    for (int c = 0; c < DCU; ++c) acc[j][c] += (uint32_t)__mul24(xv[j][kw], wv[c]);
-            }
+                    for (int c = 0; c < DCU; ++c) acc[j][c] += (uint32_t)__mul24(xv[j][kw], wr[kw][c]);
         }
     if (live)
 #pragma unroll
