@@ -1088,16 +1088,17 @@ qx_status plan_lenet(Plan* pl, int64_t B) {
         pl->launches.push_back(r);
     };
     // conv 5x5 (smul24, few output channels: the direct kernel), ReLU and the
-    // 2x2 average pool into the workspace.  One launch when the pooled map
-    // (one thread per pooled pixel) still gives every SIMD four waves and an
-    // image fits the kernel's LDS; else the conv (four pixels per thread)
-    // and the pool as two launches.
+    // 2x2 average pool into the workspace: one launch (one thread per pooled
+    // pixel) when an image fits the kernel's LDS, else the conv and the pool
+    // as two launches.  The second conv at batch 4096 fused: 48.8 us against
+    // 49.6 + 11.5 (the grid is smaller, 1.6 waves per SIMD, but its busiest
+    // CUs carry the same work and the conv map never reaches HBM).
     auto conv_pool = [&](Target x, Bind w, uint64_t to, int64_t Ci, int32_t H, int64_t Co) {
         const int32_t Ho = H - 4;
         ConvDirectParams cd{};
         cd.P = B * Ho * Ho; cd.Co = (int32_t)Co; cd.Kd = (int32_t)(Ci * 25);
         cd.g = ConvGeom{(int32_t)Ci, H, H, 5, 5, 1, 0, Ho, Ho};
-        const bool fuse = B * (Ho / 2) * (Ho / 2) >= 4 * 1024 * 64 && conv_pool_images(cd) > 0;
+        const bool fuse = conv_pool_images(cd) > 0;
         cd.pool = fuse ? 1 : 0;
         const uint64_t y = fuse ? to : take(4 * (uint64_t)B * Co * Ho * Ho);
         LaunchRec r;

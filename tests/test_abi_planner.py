@@ -138,16 +138,14 @@ def test_conv_f32_i32_plans():
 
 def test_lenet_plan_chains_the_operators():
     p = qx.plan_lenet_i32(4096)
-    # conv1: one direct launch with ReLU and the 2x2 average fused (its
-    # 4096 x 14 x 14 pooled pixels give every SIMD four waves; only the pooled
-    # map reaches the workspace); conv2 (4096 x 5 x 5 pooled pixels) keeps
-    # conv and pool apart; then 3 FC GEMMs: the first through its limb
-    # encoder and the int8 contraction, the other two one skinny vector-ALU
-    # launch each; the first two store through their ReLU.  A small batch
-    # fuses none of these and runs every FC layer through the limb planes:
-    # 2 pools, 2 encoders or sums and 2 ReLU launches more.
-    assert p["kernels"] == 7, p
-    assert qx.plan_lenet_i32(7)["kernels"] == 12
+    # both convs: one direct launch each with ReLU and the 2x2 average fused
+    # (only the pooled maps reach the workspace); then 3 FC GEMMs: the first
+    # through its limb encoder and the int8 contraction, the other two one
+    # skinny vector-ALU launch each; the first two store through their ReLU.
+    # A small batch runs every FC layer through the limb planes and their
+    # sums, with the two ReLUs as launches of their own: 4 launches more.
+    assert p["kernels"] == 6, p
+    assert qx.plan_lenet_i32(7)["kernels"] == 10
     assert 4 * 4096 * (6 * 14 * 14 + 400) <= p["workspace_bytes"] < 4 * 4096 * 6 * 28 * 28
     assert qx.plan_lenet_i32(0)["kernels"] == 0
     with pytest.raises(qx.QxError):
