@@ -267,6 +267,23 @@ qx_status plan_int_gemm(const GemmSpec& s, Plan* pl, uint64_t* ws_used) {
         v.b_trans = 0; v.out_mode = s.out_mode; v.hw = s.hw;
         LaunchRec rec;
         const bool skinny = route == R_S24_VALU && skinny_s24(s);
+        // K slices when the 64x64 tiles give under four waves per SIMD
+        // (1024 workgroups) and K is long: the slices add into the output,
+        // cleared first, with wrapping int32 atomics (exact in any order).
+        // smul24 1024^3: 256 tiles, 4 slices of 256.
+        int32_t ksplit = 1;
+        if (!skinny) {
+            const int64_t tiles = ((s.M + 63) / 64) * ((s.N + 63) / 64) * s.batch;
+            const bool dense_out = s.out_mode == OUT_CONV ||
+                                   (s.ldc == s.N && (s.batch == 1 || s.sC == s.M * s.N));
+            if (dense_out && tiles > 0 && tiles < 1024 && s.K >= 256) {
+                const int64_t want = std::min<int64_t>({(1024 + tiles - 1) / tiles, s.K / 128, 8});
+                if (want > 1 && s.batch * want <= 65535) ksplit = (int32_t)want;
+            }
+        }
+        v.ksplit = ksplit;
+        info.k_splits = ksplit > 1 ? ksplit : 0;
+        if (ksplit > 1) add_fill_out(pl, s.M * s.N * s.batch);
         if (skinny) build_valu_skinny_s24(v, (int)s.batch, &rec);
         else build_valu_gemm(route == R_VALU_DOT2 ? VK_I16_DOT2 : VK_S24, v, (int)s.batch, &rec);
         rec.bind(offsetof(ValuGemmParams, A), s.a_bind);

@@ -37,7 +37,15 @@ __global__ __launch_bounds__(VT) void k_valu_gemm(const ValuGemmParams p) {
     const int tid = threadIdx.x;
     const int tx = tid % 16, ty = tid / 16;        // 16 x 16 threads, 4 x 4 outputs each
     const int m0 = blockIdx.y * VBM, n0 = blockIdx.x * VBN;
-    const int b = blockIdx.z;
+    // K slices (integer kinds): slice kz covers [kb, ke), whole 16-k steps
+    const int ks = (VK != VK_F32 && p.ksplit > 1) ? p.ksplit : 1;
+    const int b = (int)blockIdx.z / ks, kz = (int)blockIdx.z - b * ks;
+    int kb = 0, ke = p.K;
+    if (ks > 1) {
+        const int per = ((p.K + ks - 1) / ks + VBK - 1) / VBK * VBK;
+        kb = min(p.K, kz * per);
+        ke = min(p.K, kb + per);
+    }
     const In* A = (const In*)p.A + b * p.sA;
     const In* B = (const In*)p.B + b * p.sB;
 
@@ -47,13 +55,13 @@ __global__ __launch_bounds__(VT) void k_valu_gemm(const ValuGemmParams p) {
 #pragma unroll
         for (int j = 0; j < 4; ++j) acc[i][j] = (Acc)0;
 
-    for (int k0 = 0; k0 < p.K; k0 += VBK) {
+    for (int k0 = kb; k0 < ke; k0 += VBK) {
         // A tile: 64 rows x 16 k, 4 elements per thread.
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
             const int idx = tid + VT * e, r = idx / VBK, kk = idx % VBK;
             const int gm = m0 + r, gk = k0 + kk;
-            As[kk][r] = (gm < p.M && gk < p.K) ? A[(int64_t)gm * p.lda + gk] : (In)0;
+            As[kk][r] = (gm < p.M && gk < ke) ? A[(int64_t)gm * p.lda + gk] : (In)0;
         }
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
@@ -63,7 +71,7 @@ __global__ __launch_bounds__(VT) void k_valu_gemm(const ValuGemmParams p) {
             else { kk = idx / VBN; c = idx % VBN; }
             const int gk = k0 + kk, gn = n0 + c;
             In v = (In)0;
-            if (gk < p.K && gn < p.N)
+            if (gk < ke && gn < p.N)
                 v = p.b_trans ? B[(int64_t)gn * p.ldb + gk] : B[(int64_t)gk * p.ldb + gn];
             Bs[kk][c] = v;
         }
@@ -121,8 +129,13 @@ __global__ __launch_bounds__(VT) void k_valu_gemm(const ValuGemmParams p) {
                 const int img = gn / p.hw, pix = gn - img * p.hw;
                 off = ((int64_t)img * p.M + gm) * p.hw + pix;
             }
-            if (VK == VK_F32) ((float*)p.C + b * p.sC)[off] = (float)acc[i][j];
-            else ((int32_t*)p.C + b * p.sC)[off] = (int32_t)acc[i][j];
+            if constexpr (VK == VK_F32) {
+                ((float*)p.C + b * p.sC)[off] = (float)acc[i][j];
+            } else {
+                uint32_t* c = (uint32_t*)p.C + b * p.sC + off;
+                if (ks > 1) atomicAdd(c, (uint32_t)acc[i][j]);   // wrapping: exact in any order
+                else *c = (uint32_t)acc[i][j];
+            }
         }
 }
 
@@ -293,7 +306,8 @@ void build_valu_gemm(int32_t kind, const ValuGemmParams& p, int batch, LaunchRec
     case VK_I32: rec->fn = (const void*)k_valu_gemm<VK_I32>; rec->name = "valu_i32"; break;
     default: rec->fn = (const void*)k_valu_gemm<VK_F32>; rec->name = "valu_f32"; break;
     }
-    rec->grid = dim3((unsigned)((p.N + VBN - 1) / VBN), (unsigned)((p.M + VBM - 1) / VBM), (unsigned)batch);
+    const int ks = (kind != VK_F32 && p.ksplit > 1) ? p.ksplit : 1;
+    rec->grid = dim3((unsigned)((p.N + VBN - 1) / VBN), (unsigned)((p.M + VBM - 1) / VBM), (unsigned)(batch * ks));
     rec->block = dim3(VT, 1, 1);
     rec->set_params(p);
 }

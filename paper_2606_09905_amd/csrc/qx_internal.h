@@ -292,6 +292,8 @@ struct ValuGemmParams {
     int32_t out_mode;
     int32_t hw;
     int32_t relu;           // skinny smul24 kernel only: max(c, 0) on store
+    int32_t ksplit;         // k_valu_gemm, integer kinds: K slices on grid z (batch * ksplit),
+                            // added with wrapping atomics into C cleared beforehand; 0 or 1: none
 };
 
 // ---------------------------------------------------------------------------

@@ -45,6 +45,13 @@ def test_auto_routes_for_the_workloads():
     assert qx.plan_gemm_i32_s24(64, 64, 8448, 1)["route_name"] == "s24_i8limb"
     # the vector-ALU route asked for by name takes the skinny kernel too
     assert qx.plan_gemm_i32_s24(4096, 120, 400, 1, "s24_valu")["tile_n"] == 8
+    # its 64x64 tiles slice K when they give under 1024 workgroups: the
+    # output is cleared, then the slices add into it
+    p = qx.plan_gemm_i32_s24(1024, 1024, 1024, 1, "s24_valu")
+    assert p["k_splits"] == 4 and p["kernels"] == 2, p
+    assert qx.plan_gemm_i32_s24(512, 512, 512, 16, "s24_valu")["k_splits"] == 0
+    assert qx.plan_gemm_i16i32(256, 256, 256, 1, 0, 0, "valu_dot2")["k_splits"] == 2
+    assert qx.plan_gemm_i32_s24(0, 1024, 1024, 1, "s24_valu")["kernels"] == 0
     d = w["conv_8x64x56x56_128_3x3"].dims
     p = qx.plan_conv2d(d["N"], d["Ci"], d["H"], d["W"], d["Co"], d["KH"], d["KW"], 1, 1, 256, 256)
     # one launch writes the bordered NHWC fp16 image and the fp16 weights,
