@@ -55,13 +55,16 @@ __global__ __launch_bounds__(VT) void k_valu_gemm(const ValuGemmParams p) {
 #pragma unroll
         for (int j = 0; j < 4; ++j) acc[i][j] = (Acc)0;
 
-    for (int k0 = kb; k0 < ke; k0 += VBK) {
-        // A tile: 64 rows x 16 k, 4 elements per thread.
+    // A tile: 64 rows x 16 k, B tile 16 k x 64 columns, 4 elements of each
+    // per thread; the next step's elements are loaded into registers while
+    // the current step's multiply-adds run
+    In ra[4], rb[4];
+    auto load_step = [&](int k0) {
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
             const int idx = tid + VT * e, r = idx / VBK, kk = idx % VBK;
             const int gm = m0 + r, gk = k0 + kk;
-            As[kk][r] = (gm < p.M && gk < ke) ? A[(int64_t)gm * p.lda + gk] : (In)0;
+            ra[e] = (gm < p.M && gk < ke) ? A[(int64_t)gm * p.lda + gk] : (In)0;
         }
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
@@ -73,9 +76,20 @@ __global__ __launch_bounds__(VT) void k_valu_gemm(const ValuGemmParams p) {
             In v = (In)0;
             if (gk < ke && gn < p.N)
                 v = p.b_trans ? B[(int64_t)gn * p.ldb + gk] : B[(int64_t)gk * p.ldb + gn];
-            Bs[kk][c] = v;
+            rb[e] = v;
+        }
+    };
+    if (kb < ke) load_step(kb);
+    for (int k0 = kb; k0 < ke; k0 += VBK) {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            const int idx = tid + VT * e;
+            As[idx % VBK][idx / VBK] = ra[e];
+            if (p.b_trans) Bs[idx % VBK][idx / VBK] = rb[e];
+            else Bs[idx / VBN][idx % VBN] = rb[e];
         }
         __syncthreads();
+        if (k0 + VBK < ke) load_step(k0 + VBK);
         if (VK == VK_I16_DOT2) {
 #pragma unroll
             for (int kk = 0; kk < VBK; kk += 2) {
