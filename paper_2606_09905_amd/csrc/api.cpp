@@ -219,7 +219,8 @@ void add_fill_out(Plan* pl, int64_t n32);
 // workgroup) takes GEMMs of at most 128 columns with at least 1024 rows over
 // the batch, enough workgroups to occupy the chip, and K up to 4096.
 static bool skinny_s24(const GemmSpec& s) {
-    return s.s24 && s.N <= 128 && s.M * s.batch >= 1024 && s.K <= 4096;
+    // (its B row offsets are 32-bit: K x ldb words stay under 2 MiB)
+    return s.s24 && s.N <= 128 && s.ldb <= 128 && s.M * s.batch >= 1024 && s.K <= 4096;
 }
 
 // Appends the launches of one integer GEMM; ws_used is the workspace end.

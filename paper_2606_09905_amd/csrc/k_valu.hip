@@ -226,9 +226,10 @@ __global__ __launch_bounds__(VT) void k_valu_skinny_s24(const ValuGemmParams p) 
         __builtin_amdgcn_wave_barrier();
         __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
     };
-    // B rows are addressed by a 32-bit byte offset from B (K x ldb words
-    // of B, K <= 4096 and ldb <= 2^17: under 2^31 bytes), stepped by one row
-    // per load, which keeps the scalar address arithmetic to one add per row
+    // B rows are addressed by a 32-bit byte offset from B (the planner sends
+    // K <= 4096 rows of ldb = N <= 128 words: under 2 MiB), stepped by one
+    // row per load, which keeps the scalar address arithmetic to one add per
+    // row
     typedef const __attribute__((address_space(4))) char* cbptr;
     const cbptr Bb = (cbptr)B;
     const uint32_t row_bytes = 4u * (uint32_t)p.ldb;
