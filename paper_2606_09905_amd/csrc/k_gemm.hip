@@ -1200,8 +1200,11 @@ __global__ __launch_bounds__(64 * WAVES) void k_gemm_i8nt(const GemmParams p) {
                     v += ccol;
                     if (lead) v += cc * rs_l[lr] - kcc;
                 }
+                // non-temporal: the output is not re-read by this launch and
+                // kept out of L2 it does not evict other workgroups' operand
+                // tiles (16 x 512^3: 27.0 -> 24.8 us, INT32 conv 30.2 -> 28.6)
                 if (split) atomicAdd((uint32_t*)C + c_index(p, gm, gn), v);
-                else C[c_index(p, gm, gn)] = p.relu ? max((int32_t)v, 0) : (int32_t)v;
+                else __builtin_nontemporal_store(p.relu ? max((int32_t)v, 0) : (int32_t)v, &C[c_index(p, gm, gn)]);
             }
     }
 }
