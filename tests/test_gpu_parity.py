@@ -70,6 +70,7 @@ def _gpu():
 GEMM_SHAPES = [  # M, N, K, batch
     (1, 1, 1, 1), (3, 5, 7, 1), (15, 17, 16, 2), (33, 65, 127, 1), (128, 128, 64, 1),
     (129, 257, 200, 3), (256, 256, 256, 1), (200, 136, 64, 2), (64, 72, 520, 1),
+    (100, 200, 600, 3),   # vector-ALU routes: 4 K slices per batch (grid z = batch x slices)
 ]
 I16_ROUTES = [  # route, bound
     ("i8_direct", 127), ("f16_exact", 256), ("f16_exact", 1024), ("f16_exact", 2048),
