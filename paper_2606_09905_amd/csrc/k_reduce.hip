@@ -245,6 +245,9 @@ __device__ __forceinline__ void stage_weights(int32_t (*ws)[DCO], const int32_t*
 // and first copies their inputs into LDS with coalesced loads, so the
 // window reads (scattered across rows and cache lines) come from LDS;
 // otherwise the windows are read from global memory.
+// At most four waves per SIMD: the registers that frees hold a kernel row's
+// weights (KWT x DCO words) at once, so their LDS reads are in flight
+// together (the grids of these convolutions give a few waves per SIMD).
 template <int DCO, int KWT, int PXT, bool STAGE, bool S1P0>
 __global__ __launch_bounds__(RT) __attribute__((amdgpu_waves_per_eu(1, 4)))
 void k_conv_direct_s24(const ConvDirectParams p) {
