@@ -635,7 +635,8 @@ def test_conv_f32(case):
                                                      (7, 6, 14, 14, 16, 5, 5, 1, 0), (1, 16, 40, 40, 4, 3, 3, 1, 0),
                                                      (2, 3, 70, 70, 6, 5, 5, 2, 2), (2, 3, 12, 12, 8, 5, 5, 1, 0),
                                                      (3, 4, 9, 10, 5, 4, 4, 1, 0), (2, 2, 8, 14, 16, 2, 7, 1, 0),
-                                                     (1, 3, 50, 50, 6, 3, 3, 1, 0), (2, 2, 9, 9, 3, 3, 3, 1, 0)])
+                                                     (1, 3, 50, 50, 6, 3, 3, 1, 0), (2, 2, 9, 9, 3, 3, 3, 1, 0),
+                                                     (2, 3, 6, 6, 1100, 3, 3, 1, 1)])
 def test_conv_i32_smul24(route, case):
     # INT32 conv under the smul24 contract: full 32-bit words (bits 24..31
     # ignored), bit-exact mod 2^32 against the oracle.  On the vector-ALU
@@ -645,7 +646,9 @@ def test_conv_i32_smul24(route, case):
     # than a workgroup's threads cover (40x40, 50x50 and 70x70 inputs).
     # Stride 1 without padding takes unguarded window reads shared between
     # a thread's pixels: 4, 2 and 1 pixels per thread, kernel widths 3 and 5
-    # and the generic width path (1, 4, 7).
+    # and the generic width path (1, 4, 7).  1100 output channels over 72
+    # positions lower explicitly onto the skinny vector-ALU GEMM, whose
+    # stores scatter into NCHW.
     N, Ci, H, W, Co, KH, KW, s, p = case
     rng = np.random.default_rng(zlib.crc32(repr(("i32", route, case)).encode()))
     x = rng.integers(-(1 << 31), (1 << 31) - 1, (N, Ci, H, W), dtype=np.int32, endpoint=True)
